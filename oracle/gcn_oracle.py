@@ -1,0 +1,374 @@
+"""CPU fp64 oracle for the GCN training hot path.
+
+TEST INFRASTRUCTURE ONLY.  This module is the slow, plain reference that the
+HIP library is checked against.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import it; the product path never does.  It
+shares no code with the HIP path (no kernels, headers, helpers or constant
+tables) and imports nothing from the library package.
+
+What it computes follows the paper's statement of the problem
+(Section "Graph Convolutions", Eq. (1); Section "Background and Motivation",
+optimisation levels O0 and O2; Section "Reduced Precision Changes") together
+with the readings recorded in the design notes for everything the paper
+leaves open:
+
+* graph(): undirected graph G=(V,E) given as unordered vertex pairs; input
+  self-loops and repeated pairs are dropped, each edge is stored in both
+  directions and one self-loop per vertex is added (A + I).
+* norm_values(): A_hat = D^-1/2 (A + I) D^-1/2, D counting the self-loop
+  (the renormalised adjacency of Kipf & Welling, which the paper cites for
+  the normalised adjacency it feeds to every layer).
+* layer_fwd(): one layer of Eq. (1) read as A_hat (H W) + b, then ReLU and
+  inverted dropout on hidden layers, identity on the output layer.
+* softmax_ce(): masked mean softmax cross-entropy with a scaled gradient.
+* layer_bwd(): the exact gradients of layer_fwd.
+* adam_step() / LossScaler: fp32 master weights updated by Adam on unscaled
+  gradients, dynamic loss scaling that skips a step and halves the scale on
+  overflow and doubles it after a run of good steps (O1/O2 description).
+* philox4x64(): the counter-based generator (Salmon et al., SC'11) that
+  draws the dropout keep decisions.
+
+Every floating-point quantity is float64.  Parity status: every function
+here is pinned by the CPU tests (brute force, closed forms, invariants,
+finite differences, library special cases); none is "parity unpinned".
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "Graph", "graph", "norm_values", "dinv_f32", "dense_adj", "transpose_csr",
+    "spmm", "philox4x64", "dropout_keep", "layer_fwd", "softmax_ce",
+    "layer_bwd", "adam_step", "LossScaler", "AdamState",
+]
+
+
+# ---------------------------------------------------------------------------
+# Graph and normalised adjacency
+# ---------------------------------------------------------------------------
+
+class Graph:
+    """Canonical CSR of A + I: rows sorted, columns sorted and unique."""
+
+    def __init__(self, n, rowptr, colidx):
+        self.n = int(n)
+        self.rowptr = rowptr          # int64 [n+1]
+        self.colidx = colidx          # int32 [nnz]
+
+    @property
+    def nnz(self):
+        return int(self.rowptr[-1])
+
+    @property
+    def deg(self):
+        """Degree of A + I (the self-loop counts once)."""
+        return np.diff(self.rowptr).astype(np.int32)
+
+    def rows(self):
+        """Row index of every stored entry."""
+        return np.repeat(np.arange(self.n, dtype=np.int64), np.diff(self.rowptr))
+
+
+def graph(n, src, dst):
+    """Build the canonical CSR of A + I from an undirected edge list.
+
+    The paper's graphs are undirected with edges as unordered vertex pairs
+    (Section "Introduction", footnote on A); pairs are therefore taken as
+    sets {u, v}: a pair and its reverse are the same edge, repeats collapse,
+    and u == v pairs are dropped because the self-loop of every vertex is
+    added exactly once afterwards (the "+ I" of the renormalised adjacency).
+    Vertex ids outside [0, n) raise ValueError.
+    """
+    src = np.asarray(src, dtype=np.int64)
+    dst = np.asarray(dst, dtype=np.int64)
+    if src.shape != dst.shape:
+        raise ValueError("src and dst differ in length")
+    if src.size and (src.min() < 0 or dst.min() < 0 or src.max() >= n or dst.max() >= n):
+        raise ValueError("vertex id out of range")
+    keep = src != dst
+    lo = np.minimum(src[keep], dst[keep])
+    hi = np.maximum(src[keep], dst[keep])
+    pairs = np.unique(lo * n + hi)                      # each undirected edge once
+    u, v = pairs // n, pairs % n
+    loops = np.arange(n, dtype=np.int64)
+    rows = np.concatenate([u, v, loops])
+    cols = np.concatenate([v, u, loops])
+    order = np.lexsort((cols, rows))                    # by row, then column
+    rows, cols = rows[order], cols[order]
+    counts = np.bincount(rows, minlength=n)
+    rowptr = np.zeros(n + 1, np.int64)
+    np.cumsum(counts, out=rowptr[1:])
+    return Graph(n, rowptr, cols.astype(np.int32))
+
+
+def dinv_f32(g: Graph):
+    """D^-1/2 rounded once to float32 from the fp64 value 1/sqrt(deg)."""
+    return (1.0 / np.sqrt(g.deg.astype(np.float64))).astype(np.float32)
+
+
+def norm_values(g: Graph):
+    """Stored values of A_hat = D^-1/2 (A+I) D^-1/2 (fp64), one per CSR entry."""
+    d = 1.0 / np.sqrt(g.deg.astype(np.float64))
+    return d[g.rows()] * d[g.colidx.astype(np.int64)]
+
+
+def dense_adj(g: Graph, values=None):
+    """A_hat as a dense n x n fp64 array (the paper's own storage, Section
+    "Reduced Precision Changes": every tensor was cast to dense)."""
+    if values is None:
+        values = norm_values(g)
+    a = np.zeros((g.n, g.n), np.float64)
+    a[g.rows(), g.colidx.astype(np.int64)] = values
+    return a
+
+
+def transpose_csr(g: Graph, values):
+    """CSR of the transpose, built by swapping row and column of every entry.
+    Used by the backward pass so that it does not rely on A_hat being
+    symmetric."""
+    rows = g.rows()
+    cols = g.colidx.astype(np.int64)
+    order = np.lexsort((rows, cols))
+    t_rows, t_cols, t_vals = cols[order], rows[order], values[order]
+    counts = np.bincount(t_rows, minlength=g.n)
+    rowptr = np.zeros(g.n + 1, np.int64)
+    np.cumsum(counts, out=rowptr[1:])
+    return Graph(g.n, rowptr, t_cols.astype(np.int32)), t_vals
+
+
+def spmm(g: Graph, values, x):
+    """Y = A X for A in CSR (fp64): Y[i] = sum over stored (i, j) of a_ij X[j]."""
+    x = np.asarray(x, np.float64)
+    prod = values[:, None] * x[g.colidx.astype(np.int64)]
+    y = np.zeros((g.n, x.shape[1]), np.float64)
+    np.add.at(y, g.rows(), prod)
+    return y
+
+
+# ---------------------------------------------------------------------------
+# Counter-based RNG for dropout: Philox-4x64-10 (Salmon, Moraes, Dror, Shaw,
+# "Parallel random numbers: as easy as 1, 2, 3", SC'11)
+# ---------------------------------------------------------------------------
+
+_M64 = (1 << 64) - 1
+_PHILOX_M0 = 0xD2E7470EE14C6C93
+_PHILOX_M1 = 0xCA5A826395121157
+_PHILOX_W0 = 0x9E3779B97F4A7C15
+_PHILOX_W1 = 0xBB67AE8584CAA73B
+
+
+def _mulhilo64(a, b):
+    """Full 128-bit product of uint64 arrays a*b split into (hi, lo), via
+    32-bit halves (numpy has no 128-bit integers)."""
+    mask32 = np.uint64(0xFFFFFFFF)
+    s32 = np.uint64(32)
+    a = a.astype(np.uint64)
+    b = np.uint64(b) if np.isscalar(b) else b.astype(np.uint64)
+    a_lo, a_hi = a & mask32, a >> s32
+    b_lo, b_hi = b & mask32, b >> s32
+    ll = a_lo * b_lo
+    lh = a_lo * b_hi
+    hl = a_hi * b_lo
+    hh = a_hi * b_hi
+    mid = (ll >> s32) + (lh & mask32) + (hl & mask32)
+    lo = (ll & mask32) | ((mid & mask32) << s32)
+    hi = hh + (lh >> s32) + (hl >> s32) + (mid >> s32)
+    return hi, lo
+
+
+def philox4x64(ctr, key, rounds=10):
+    """Philox-4x64 with ``rounds`` rounds.  ctr: uint64 array [..., 4];
+    key: uint64 array [..., 2].  Returns uint64 [..., 4].
+
+    Each round multiplies words 0 and 2 by the two round multipliers, forms
+    the new state (hi(M1*x2) ^ x1 ^ k0, lo(M1*x2), hi(M0*x0) ^ x3 ^ k1,
+    lo(M0*x0)), and the key is bumped by the two Weyl constants between
+    rounds."""
+    with np.errstate(over="ignore"):
+        c = np.array(ctr, dtype=np.uint64, copy=True)
+        k = np.array(key, dtype=np.uint64, copy=True)
+        x0, x1, x2, x3 = c[..., 0], c[..., 1], c[..., 2], c[..., 3]
+        k0, k1 = k[..., 0], k[..., 1]
+        for r in range(rounds):
+            hi0, lo0 = _mulhilo64(x0, _PHILOX_M0)
+            hi1, lo1 = _mulhilo64(x2, _PHILOX_M1)
+            x0, x1, x2, x3 = hi1 ^ x1 ^ k0, lo1, hi0 ^ x3 ^ k1, lo0
+            if r + 1 < rounds:
+                k0 = k0 + np.uint64(_PHILOX_W0)
+                k1 = k1 + np.uint64(_PHILOX_W1)
+        return np.stack([x0, x1, x2, x3], axis=-1)
+
+
+def dropout_keep(seed, layer_id, epoch, n, f, p):
+    """Keep mask (bool n x f) of inverted dropout with drop probability p.
+
+    Element (i, j) has linear index e = i*f + j over the logical width f.
+    One Philox-4x64-10 block with key (seed, layer_id) and counter
+    (e // 8, epoch, 0, 0) yields 8 32-bit words (word 2t is the low half of
+    output t, word 2t+1 the high half); element e takes word e % 8 and is
+    kept iff word >= floor(p * 2^32)."""
+    blocks = np.arange((n * f + 7) // 8, dtype=np.uint64)
+    ctr = np.zeros((blocks.size, 4), np.uint64)
+    ctr[:, 0] = blocks
+    ctr[:, 1] = np.uint64(epoch)
+    key = np.zeros((blocks.size, 2), np.uint64)
+    key[:, 0] = np.uint64(seed & _M64)
+    key[:, 1] = np.uint64(layer_id)
+    out = philox4x64(ctr, key)                               # [blocks, 4]
+    words = np.empty((blocks.size, 8), np.uint64)
+    words[:, 0::2] = out & np.uint64(0xFFFFFFFF)
+    words[:, 1::2] = out >> np.uint64(32)
+    w = words.reshape(-1)[: n * f]
+    thr = np.uint64(int(np.floor(p * 4294967296.0)))
+    return (w >= thr).reshape(n, f)
+
+
+# ---------------------------------------------------------------------------
+# Layer forward / backward, loss
+# ---------------------------------------------------------------------------
+
+def layer_fwd(g: Graph, values, h, w, b, act="relu", p=0.0, training=True,
+              seed=0, layer_id=0, epoch=0, dense=None):
+    """One GCN layer, Eq. (1): S = H W, Z = A_hat S + b; hidden layers apply
+    ReLU then inverted dropout (kept entries scaled by 1/(1-p)), the output
+    layer returns Z unchanged.  ``dense`` (optional n x n fp64) replaces the
+    CSR product by the dense one.  Returns (S, Z, H_out), all fp64."""
+    h = np.asarray(h, np.float64)
+    w = np.asarray(w, np.float64)
+    s = h @ w
+    z = (dense @ s) if dense is not None else spmm(g, values, s)
+    if b is not None:
+        z = z + np.asarray(b, np.float64)[None, :]
+    if act == "relu":
+        out = np.maximum(z, 0.0)
+        if training and p > 0.0:
+            keep = dropout_keep(seed, layer_id, epoch, g.n, w.shape[1], p)
+            out = np.where(keep, out / (1.0 - p), 0.0)
+    elif act == "none":
+        out = z
+    else:
+        raise ValueError(act)
+    return s, z, out
+
+
+def softmax_ce(logits, labels, mask=None, loss_scale=1.0):
+    """Masked mean softmax cross-entropy.
+
+    loss = mean over masked rows i of (logsumexp(z_i) - z_i[y_i]);
+    dlogits = loss_scale * (softmax(z_i) - onehot(y_i)) / |mask| on masked
+    rows and 0 elsewhere; n_correct counts masked rows whose arg-max (lowest
+    index on ties) equals the label.  Returns (loss, dlogits, n_correct)."""
+    z = np.asarray(logits, np.float64)
+    n, c = z.shape
+    m = np.ones(n, bool) if mask is None else np.asarray(mask).astype(bool)
+    cnt = int(m.sum())
+    zmax = z.max(axis=1, keepdims=True)
+    ez = np.exp(z - zmax)
+    se = ez.sum(axis=1, keepdims=True)
+    lse = zmax[:, 0] + np.log(se[:, 0])
+    y = np.asarray(labels, np.int64)
+    per_row = lse - z[np.arange(n), y]
+    loss = per_row[m].sum() / cnt if cnt else 0.0
+    sm = ez / se
+    onehot = np.zeros_like(z)
+    onehot[np.arange(n), y] = 1.0
+    d = (sm - onehot) * (loss_scale / cnt if cnt else 0.0)
+    d[~m] = 0.0
+    n_correct = int((np.argmax(z, axis=1) == y)[m].sum())
+    return loss, d, n_correct
+
+
+def layer_bwd(g: Graph, values, h, w, dz, act_below="relu", p_below=0.0, dense=None,
+              need_dh=True):
+    """Gradients of layer_fwd given dZ (gradient w.r.t. Z = A_hat S + b).
+
+    G_S = A_hat^T dZ (explicit transpose, no symmetry assumed);
+    dW = H^T G_S; db = column sums of dZ; dH = G_S W^T; and, when H was
+    produced by ReLU + inverted dropout, dZ_below = dH * [H > 0] / (1 - p)
+    (the ReLU derivative at 0 is taken as 0).  Returns (G_S, dW, db,
+    dZ_below or None)."""
+    h = np.asarray(h, np.float64)
+    w = np.asarray(w, np.float64)
+    dz = np.asarray(dz, np.float64)
+    if dense is not None:
+        gs = dense.T @ dz
+    else:
+        gt, vt = transpose_csr(g, values)
+        gs = spmm(gt, vt, dz)
+    dw = h.T @ gs
+    db = dz.sum(axis=0)
+    dzb = None
+    if need_dh:
+        dh = gs @ w.T
+        if act_below == "relu":
+            dzb = np.where(h > 0.0, dh / (1.0 - p_below), 0.0)
+        elif act_below == "none":
+            dzb = dh
+        else:
+            raise ValueError(act_below)
+    return gs, dw, db, dzb
+
+
+# ---------------------------------------------------------------------------
+# Optimiser with fp32 master weights and dynamic loss scaling
+# ---------------------------------------------------------------------------
+
+class LossScaler:
+    """Dynamic loss scale state machine (O1/O2 "dynamic loss scaling"):
+    on overflow skip the update and multiply the scale by ``backoff``
+    (not below ``min_scale``) and reset the good-step counter; otherwise
+    count the good step and multiply the scale by ``growth`` (not above
+    ``max_scale``) after ``interval`` consecutive good steps."""
+
+    def __init__(self, scale=65536.0, backoff=0.5, growth=2.0, interval=2000,
+                 min_scale=1.0, max_scale=16777216.0):
+        self.scale = float(scale)
+        self.backoff, self.growth, self.interval = backoff, growth, interval
+        self.min_scale, self.max_scale = min_scale, max_scale
+        self.good = 0
+        self.skipped = 0
+
+    def update(self, overflow: bool) -> bool:
+        """Advance one step; returns True when the parameter update applies."""
+        if overflow:
+            self.scale = max(self.scale * self.backoff, self.min_scale)
+            self.good = 0
+            self.skipped += 1
+            return False
+        self.good += 1
+        if self.good == self.interval:
+            self.scale = min(self.scale * self.growth, self.max_scale)
+            self.good = 0
+        return True
+
+
+class AdamState:
+    def __init__(self, size):
+        self.m = np.zeros(size, np.float64)
+        self.v = np.zeros(size, np.float64)
+        self.t = 0
+
+
+def adam_step(master, grad_scaled, state: AdamState, scaler: LossScaler,
+              lr=0.01, beta1=0.9, beta2=0.999, eps=1e-8):
+    """One optimiser step on the fp32 master weights (as fp64 here).
+
+    overflow = any non-finite scaled gradient.  On overflow nothing but the
+    scaler changes.  Otherwise g = grad / scale and Adam (Kingma & Ba) with
+    bias correction: m = b1 m + (1-b1) g, v = b2 v + (1-b2) g^2,
+    theta -= lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps).
+    Returns (new master, applied)."""
+    grad_scaled = np.asarray(grad_scaled, np.float64)
+    overflow = not np.all(np.isfinite(grad_scaled))
+    scale = scaler.scale
+    applied = scaler.update(overflow)
+    if not applied:
+        return np.array(master, np.float64, copy=True), False
+    g = grad_scaled / scale
+    state.t += 1
+    state.m = beta1 * state.m + (1.0 - beta1) * g
+    state.v = beta2 * state.v + (1.0 - beta2) * g * g
+    mhat = state.m / (1.0 - beta1 ** state.t)
+    vhat = state.v / (1.0 - beta2 ** state.t)
+    new = np.asarray(master, np.float64) - lr * mhat / (np.sqrt(vhat) + eps)
+    return new, True

@@ -1,0 +1,417 @@
+"""Pins for the CPU oracle: each test checks it against something other than
+itself -- brute force, closed forms, invariants, finite differences or an
+independent library routine -- so that a dropped term, a wrong sign or
+index, or a transposed operand fails at least one of them."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+from hypothesis import given, settings, strategies as st
+
+from oracle import gcn_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- graph / CSR
+
+def brute_csr(n, src, dst):
+    """Set-based construction of the neighbour lists of A + I."""
+    nbrs = [set([i]) for i in range(n)]
+    for u, v in zip(src, dst):
+        if u != v:
+            nbrs[u].add(v)
+            nbrs[v].add(u)
+    rowptr = [0]
+    cols = []
+    for i in range(n):
+        cols.extend(sorted(nbrs[i]))
+        rowptr.append(len(cols))
+    return np.array(rowptr), np.array(cols)
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.integers(1, 12).flatmap(
+    lambda n: st.tuples(st.just(n), st.lists(st.tuples(st.integers(0, n - 1), st.integers(0, n - 1)), max_size=40))))
+def test_csr_matches_brute_force(case):
+    n, edges = case
+    src = [e[0] for e in edges]
+    dst = [e[1] for e in edges]
+    g = O.graph(n, np.array(src, np.int32), np.array(dst, np.int32))
+    rp, ci = brute_csr(n, src, dst)
+    assert np.array_equal(g.rowptr, rp)
+    assert np.array_equal(g.colidx, ci)
+    assert g.deg.sum() == g.nnz
+
+
+def test_csr_matches_scipy():
+    rng = np.random.default_rng(3)
+    n = 300
+    src = rng.integers(0, n, 2000)
+    dst = rng.integers(0, n, 2000)
+    g = O.graph(n, src, dst)
+    keep = src != dst
+    m = sp.coo_matrix((np.ones(keep.sum() * 2), (np.r_[src[keep], dst[keep]], np.r_[dst[keep], src[keep]])),
+                      shape=(n, n)).tocsr()
+    m.data[:] = 1.0
+    m = m + sp.identity(n, format="csr")
+    m.sum_duplicates()
+    m.sort_indices()
+    assert np.array_equal(g.rowptr, m.indptr)
+    assert np.array_equal(g.colidx, m.indices)
+    # sum of degrees = 2E + n
+    e_undirected = len({(min(a, b), max(a, b)) for a, b in zip(src, dst) if a != b})
+    assert g.nnz == 2 * e_undirected + n
+
+
+def test_out_of_range_rejected():
+    with pytest.raises(ValueError):
+        O.graph(4, np.array([0, 4]), np.array([1, 2]))
+    with pytest.raises(ValueError):
+        O.graph(4, np.array([-1]), np.array([1]))
+
+
+def test_empty_graph_is_identity():
+    g = O.graph(5, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    assert np.array_equal(O.dense_adj(g), np.eye(5))
+
+
+def _golden():
+    with open(os.path.join(GOLDEN, "closed_forms.json")) as f:
+        return json.load(f)
+
+
+def _dense_of(case):
+    e = np.array(case["edges"])
+    g = O.graph(case["n"], e[:, 0], e[:, 1])
+    return O.dense_adj(g)
+
+
+def test_closed_forms():
+    gold = _golden()
+    assert np.allclose(_dense_of(gold["K2"]), np.array(gold["K2"]["A_hat"]), rtol=0, atol=1e-15)
+    s6 = 1 / math.sqrt(6)
+    p3 = np.array([[0.5, s6, 0], [s6, 1 / 3, s6], [0, s6, 0.5]])
+    assert np.allclose(_dense_of(gold["P3"]), p3, rtol=0, atol=1e-15)
+    a = _dense_of(gold["star_K1_4"])
+    assert a[0, 0] == pytest.approx(1 / 5, abs=1e-15)
+    assert np.allclose(a[0, 1:], 1 / math.sqrt(10), atol=1e-15)
+    assert np.allclose(np.diag(a)[1:], 0.5, atol=1e-15)
+    assert np.allclose(a[1:, 1:] - np.diag(np.diag(a)[1:]), 0.0)
+    c5 = gold["C5"]
+    adj = np.eye(5)
+    for u, v in c5["edges"]:
+        adj[u, v] = adj[v, u] = 1
+    assert np.allclose(_dense_of(c5), adj / 3, atol=1e-15)
+    assert np.allclose(_dense_of(gold["K4"]), np.full((4, 4), 0.25), atol=1e-15)
+
+
+def test_invariants_random_graph():
+    rng = np.random.default_rng(7)
+    n = 120
+    src = rng.integers(0, n, 500)
+    dst = rng.integers(0, n, 500)
+    g = O.graph(n, src, dst)
+    a = O.dense_adj(g)
+    assert np.array_equal(a, a.T)                          # exact symmetry
+    d = np.sqrt(g.deg.astype(np.float64))
+    assert np.allclose(a @ d, d, rtol=1e-13)               # A_hat D^1/2 1 = D^1/2 1
+    ev = np.linalg.eigvalsh(a)
+    assert ev.max() == pytest.approx(1.0, abs=1e-12)
+    assert ev.min() > -1.0 - 1e-12
+
+
+def test_regular_graph_row_sums():
+    # 3-regular circulant on 20 vertices plus loops: each row sums to 1
+    n = 20
+    src = np.r_[np.arange(n), np.arange(n)]
+    dst = np.r_[(np.arange(n) + 1) % n, (np.arange(n) + 10) % n]
+    g = O.graph(n, src, dst)
+    assert np.all(g.deg == 4)
+    assert np.allclose(O.dense_adj(g).sum(axis=1), 1.0, atol=1e-15)
+
+
+def test_dinv_f32_is_rounded_fp64():
+    g = O.graph(6, np.array([0, 0, 0, 1]), np.array([1, 2, 3, 2]))
+    want = np.array([np.float32(1.0 / math.sqrt(float(d))) for d in g.deg], np.float32)
+    assert np.array_equal(O.dinv_f32(g), want)
+
+
+def test_transpose_matches_scipy():
+    rng = np.random.default_rng(11)
+    n = 50
+    g = O.graph(n, rng.integers(0, n, 150), rng.integers(0, n, 150))
+    vals = rng.standard_normal(g.nnz)                      # deliberately non-symmetric values
+    gt, vt = O.transpose_csr(g, vals)
+    m = sp.csr_matrix((vals, g.colidx, g.rowptr), shape=(n, n)).T.tocsr()
+    m.sort_indices()
+    assert np.array_equal(gt.rowptr, m.indptr)
+    assert np.array_equal(gt.colidx, m.indices)
+    assert np.allclose(vt, m.data, rtol=0, atol=0)
+
+
+def test_spmm_matches_scipy_and_dense():
+    rng = np.random.default_rng(5)
+    n = 80
+    g = O.graph(n, rng.integers(0, n, 300), rng.integers(0, n, 300))
+    vals = O.norm_values(g)
+    x = rng.standard_normal((n, 9))
+    y = O.spmm(g, vals, x)
+    ref = sp.csr_matrix((vals, g.colidx, g.rowptr), shape=(n, n)) @ x
+    assert np.allclose(y, ref, rtol=1e-13, atol=1e-13)
+    assert np.allclose(y, O.dense_adj(g) @ x, rtol=1e-13, atol=1e-13)
+
+
+# ---------------------------------------------------------------- dropout RNG
+
+def test_philox_matches_numpy():
+    # numpy's Philox is Philox-4x64-10; it increments the counter before
+    # producing a block, so block(c) == philox(c + 1).
+    for ctr, key in [([0, 0, 0, 0], [0, 0]), ([5, 7, 9, 11], [123, 456]),
+                     ([2**40 + 3, 2**33, 17, 2**62], [2**63 + 5, 2**61 + 9])]:
+        bg = np.random.Philox(counter=np.array(ctr, np.uint64), key=np.array(key, np.uint64))
+        ref = bg.random_raw(4)
+        c1 = np.array([ctr], np.uint64)
+        c1[0, 0] += np.uint64(1)
+        mine = O.philox4x64(c1, np.array([key], np.uint64))[0]
+        assert [int(x) for x in mine] == [int(x) for x in ref]
+
+
+def test_dropout_p0_keeps_all_and_fraction():
+    assert O.dropout_keep(1, 0, 0, 10, 7, 0.0).all()
+    keep = O.dropout_keep(123, 1, 3, 500, 40, 0.5)
+    n = keep.size
+    frac = keep.mean()
+    assert abs(frac - 0.5) < 5 * math.sqrt(0.25 / n)       # binomial 5-sigma
+    keep3 = O.dropout_keep(123, 1, 3, 500, 40, 0.3)
+    assert abs(keep3.mean() - 0.7) < 5 * math.sqrt(0.21 / n)
+    # different epoch / layer / seed give different masks
+    assert (keep != O.dropout_keep(123, 1, 4, 500, 40, 0.5)).mean() > 0.4
+    assert (keep != O.dropout_keep(123, 2, 3, 500, 40, 0.5)).mean() > 0.4
+    assert (keep != O.dropout_keep(124, 1, 3, 500, 40, 0.5)).mean() > 0.4
+
+
+def test_dropout_word_layout():
+    # element e uses word e % 8 of block e // 8: check one block by hand
+    seed, layer, epoch = 99, 2, 5
+    out = O.philox4x64(np.array([[3, epoch, 0, 0]], np.uint64), np.array([[seed, layer]], np.uint64))[0]
+    words = []
+    for x in out:
+        words += [int(x) & 0xFFFFFFFF, int(x) >> 32]
+    thr = int(math.floor(0.5 * 2**32))
+    keep = O.dropout_keep(seed, layer, epoch, 4, 8, 0.5)  # 32 elements, block 3 = row 3
+    assert [bool(w >= thr) for w in words] == keep[3].tolist()
+
+
+def test_dropout_scales_kept_by_two():
+    rng = np.random.default_rng(0)
+    n, f = 64, 16
+    g = O.graph(n, np.zeros(0, np.int32), np.zeros(0, np.int32))   # A_hat = I
+    h = rng.standard_normal((n, 8))
+    w = rng.standard_normal((8, f))
+    _, z, out = O.layer_fwd(g, O.norm_values(g), h, w, None, "relu", 0.5, True, 7, 1, 0)
+    keep = O.dropout_keep(7, 1, 0, n, f, 0.5)
+    assert np.array_equal(out[keep], 2.0 * np.maximum(z, 0)[keep])
+    assert np.all(out[~keep] == 0)
+
+
+# ---------------------------------------------------------------- layer math
+
+def _small_problem(seed=0, n=40, fin=6, fh=5, c=4, e=90):
+    rng = np.random.default_rng(seed)
+    g = O.graph(n, rng.integers(0, n, e), rng.integers(0, n, e))
+    vals = O.norm_values(g)
+    x = rng.standard_normal((n, fin))
+    w1 = rng.standard_normal((fin, fh)) * 0.5
+    b1 = rng.standard_normal(fh) * 0.1
+    w2 = rng.standard_normal((fh, c)) * 0.5
+    b2 = rng.standard_normal(c) * 0.1
+    y = rng.integers(0, c, n)
+    mask = rng.random(n) < 0.6
+    return rng, g, vals, x, w1, b1, w2, b2, y, mask
+
+
+def test_identity_graph_reduces_to_dense_layer():
+    rng = np.random.default_rng(2)
+    n = 30
+    g = O.graph(n, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    h = rng.standard_normal((n, 7))
+    w = rng.standard_normal((7, 3))
+    b = rng.standard_normal(3)
+    s, z, out = O.layer_fwd(g, O.norm_values(g), h, w, b, "relu", 0.0)
+    ref = np.einsum("ik,kj->ij", h, w) + b
+    assert np.allclose(z, ref, rtol=1e-14)
+    assert np.allclose(out, np.maximum(ref, 0))
+
+
+def test_featureless_input_gives_weights():
+    # X = I (the paper's default featureless input): S = W
+    rng = np.random.default_rng(4)
+    n = 12
+    g = O.graph(n, rng.integers(0, n, 20), rng.integers(0, n, 20))
+    w = rng.standard_normal((n, 5))
+    s, z, _ = O.layer_fwd(g, O.norm_values(g), np.eye(n), w, None, "none")
+    assert np.array_equal(s, w)
+    assert np.allclose(z, O.dense_adj(g) @ w, rtol=1e-13)
+
+
+def test_dense_and_csr_forward_agree():
+    _, g, vals, x, w1, b1, *_ = _small_problem(1)
+    a = O.dense_adj(g, vals)
+    for act in ("relu", "none"):
+        r1 = O.layer_fwd(g, vals, x, w1, b1, act, 0.5, True, 3, 0, 1)
+        r2 = O.layer_fwd(g, vals, x, w1, b1, act, 0.5, True, 3, 0, 1, dense=a)
+        for u, v in zip(r1, r2):
+            assert np.allclose(u, v, rtol=1e-13, atol=1e-13)
+
+
+def test_permutation_equivariance():
+    _, g, vals, x, w1, b1, *_ = _small_problem(3)
+    n = g.n
+    perm = np.random.default_rng(9).permutation(n)
+    inv = np.argsort(perm)
+    rows = g.rows()
+    # relabel vertex v -> inv[v]
+    src = inv[rows]
+    dst = inv[g.colidx]
+    gp = O.graph(n, src, dst)
+    _, z, _ = O.layer_fwd(g, vals, x, w1, b1, "none")
+    _, zp, _ = O.layer_fwd(gp, O.norm_values(gp), x[perm], w1, b1, "none")
+    assert np.allclose(zp, z[perm], rtol=1e-12, atol=1e-12)
+
+
+def test_adjoint_identity():
+    rng, g, vals, *_ = _small_problem(5)
+    vals = rng.standard_normal(g.nnz)                      # generic, non-symmetric A
+    x = rng.standard_normal((g.n, 3))
+    y = rng.standard_normal((g.n, 3))
+    gt, vt = O.transpose_csr(g, vals)
+    lhs = np.sum(O.spmm(g, vals, x) * y)
+    rhs = np.sum(x * O.spmm(gt, vt, y))
+    assert lhs == pytest.approx(rhs, rel=1e-12)
+
+
+def test_softmax_ce_closed_forms():
+    n, c = 10, 7
+    z = np.full((n, c), 0.3)
+    y = np.arange(n) % c
+    mask = np.zeros(n, bool)
+    mask[[1, 4, 6]] = True
+    loss, d, nc = O.softmax_ce(z, y, mask, loss_scale=8.0)
+    assert loss == pytest.approx(math.log(c), rel=1e-15)
+    want = np.zeros((n, c))
+    for i in np.flatnonzero(mask):
+        want[i] = 1.0 / c
+        want[i, y[i]] -= 1.0
+    assert np.allclose(d, want * 8.0 / 3, rtol=1e-14, atol=1e-16)
+    # uniform logits: arg-max ties resolve to class 0
+    assert nc == int(np.sum(y[mask] == 0))
+
+
+def _loss_of(params, g, vals, x, y, mask, p, seed):
+    w1, b1, w2, b2 = params
+    _, _, h1 = O.layer_fwd(g, vals, x, w1, b1, "relu", p, True, seed, 0, 0)
+    _, z2, _ = O.layer_fwd(g, vals, h1, w2, b2, "none")
+    return O.softmax_ce(z2, y, mask)[0]
+
+
+def test_two_layer_gradients_finite_difference():
+    _, g, vals, x, w1, b1, w2, b2, y, mask = _small_problem(6)
+    p, seed = 0.5, 77
+    params = [w1, b1, w2, b2]
+    s1, z1, h1 = O.layer_fwd(g, vals, x, w1, b1, "relu", p, True, seed, 0, 0)
+    _, z2, _ = O.layer_fwd(g, vals, h1, w2, b2, "none")
+    _, dz2, _ = O.softmax_ce(z2, y, mask)
+    _, dw2, db2, dz1 = O.layer_bwd(g, vals, h1, w2, dz2, "relu", p)
+    _, dw1, db1, _ = O.layer_bwd(g, vals, x, w1, dz1, "none", 0.0, need_dh=False)
+    assert np.min(np.abs(z1)) > 1e-4                       # away from ReLU kinks
+    grads = [dw1, db1, dw2, db2]
+    h = 1e-6
+    rng = np.random.default_rng(0)
+    for k, (par, gr) in enumerate(zip(params, grads)):
+        flat = par.reshape(-1)
+        for idx in rng.choice(flat.size, size=min(flat.size, 8), replace=False):
+            old = flat[idx]
+            flat[idx] = old + h
+            lp = _loss_of(params, g, vals, x, y, mask, p, seed)
+            flat[idx] = old - h
+            lm = _loss_of(params, g, vals, x, y, mask, p, seed)
+            flat[idx] = old
+            fd = (lp - lm) / (2 * h)
+            assert gr.reshape(-1)[idx] == pytest.approx(fd, rel=1e-5, abs=1e-9), (k, idx)
+
+
+def test_input_gradient_finite_difference():
+    # gradient w.r.t. the layer input H through a non-symmetric A
+    rng, g, vals, x, w1, b1, *_ = _small_problem(8)
+    vals = rng.uniform(0.1, 1.0, g.nnz)
+    r = rng.standard_normal((g.n, w1.shape[1]))
+
+    def f(xx):
+        return np.sum(O.layer_fwd(g, vals, xx, w1, b1, "none")[1] * r)
+
+    _, dw, db, dx = O.layer_bwd(g, vals, x, w1, r, "none", 0.0)
+    h = 1e-6
+    for i, j in [(0, 0), (5, 2), (17, 4), (33, 1)]:
+        xp = x.copy(); xp[i, j] += h
+        xm = x.copy(); xm[i, j] -= h
+        assert dx[i, j] == pytest.approx((f(xp) - f(xm)) / (2 * h), rel=1e-6, abs=1e-9)
+    assert np.allclose(db, r.sum(axis=0))
+
+
+def test_relu_dropout_mask_in_backward():
+    # dZ_below is zero exactly where H is zero and scaled by 1/(1-p) elsewhere
+    rng = np.random.default_rng(12)
+    n = 16
+    g = O.graph(n, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    h = np.maximum(rng.standard_normal((n, 4)), 0) * 2.0
+    w = rng.standard_normal((4, 3))
+    dz = rng.standard_normal((n, 3))
+    _, _, _, dzb = O.layer_bwd(g, O.norm_values(g), h, w, dz, "relu", 0.5)
+    dh = dz @ w.T
+    assert np.all(dzb[h == 0] == 0)
+    assert np.allclose(dzb[h > 0], 2.0 * dh[h > 0], rtol=1e-15)
+
+
+# ---------------------------------------------------------------- optimiser
+
+def test_adam_first_step_closed_form():
+    g = np.array([3.0, -0.5, 1e-3, -7.0])
+    st_ = O.AdamState(4)
+    sc = O.LossScaler(scale=1024.0)
+    w0 = np.array([1.0, 2.0, 3.0, 4.0])
+    w1, applied = O.adam_step(w0, g * 1024.0, st_, sc, lr=0.01)
+    assert applied
+    # m_hat = g, v_hat = g^2: every coordinate moves by lr * g / (|g| + eps)
+    assert np.allclose(w1, w0 - 0.01 * g / (np.abs(g) + 1e-8), rtol=1e-15)
+
+
+def test_adam_overflow_skips_and_backs_off():
+    st_ = O.AdamState(3)
+    sc = O.LossScaler(scale=2.0**16)
+    w0 = np.array([1.0, 2.0, 3.0])
+    w1, applied = O.adam_step(w0, np.array([1.0, np.inf, 0.0]), st_, sc)
+    assert not applied and np.array_equal(w1, w0)
+    assert sc.scale == 2.0**15 and st_.t == 0
+    w2, applied = O.adam_step(w0, np.array([np.nan, 0, 0]), st_, sc)
+    assert not applied and sc.scale == 2.0**14
+
+
+def test_loss_scaler_script():
+    sc = O.LossScaler(scale=4.0, interval=3, min_scale=1.0, max_scale=16.0)
+    seq = [False, False, False, True, True, True, False, False, False, False, False, False,
+           False, False, False, False, False, False]
+    states = []
+    for ov in seq:
+        sc.update(ov)
+        states.append((sc.scale, sc.good))
+    assert states[:3] == [(4.0, 1), (4.0, 2), (8.0, 0)]
+    assert states[3:6] == [(4.0, 0), (2.0, 0), (1.0, 0)]           # clamps at min
+    assert states[6:9] == [(1.0, 1), (1.0, 2), (2.0, 0)]
+    assert states[9:15] == [(2.0, 1), (2.0, 2), (4.0, 0), (4.0, 1), (4.0, 2), (8.0, 0)]
+    assert states[15:18] == [(8.0, 1), (8.0, 2), (16.0, 0)]
+    sc.update(False); sc.update(False); sc.update(False)
+    assert sc.scale == 16.0                                         # clamps at max
