@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Training throughput of the two-layer GCN on one MI355X.
+
+One step = one full training epoch of the workload (both layers forward,
+softmax cross-entropy, both layers backward, Adam with dynamic loss scaling),
+all through the libgcn C ABI, inputs resident in HBM before timing starts.
+
+Default workload: dense-adjacency 2-layer GCN on a 32-block stochastic block
+model (n = 16,384, p_in = 0.01, p_out = 0.0002, plus self-loops; A_hat dense
+fp16 n x n; features 16384 x 500 N(0,1); hidden 64; 32 classes = block id;
+Adam lr 0.01; loss scale starts at 2^16; 200 epochs).
+
+Prints one JSON line on stdout: epochs/s in 16-bit storage mode (value) and
+fp32 mode, the roofline of the dominant kernel (the A_hat aggregation),
+timed live with HIP events around its launches inside the timed region, and
+the CPU fp64 oracle timed on a bounded sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "GCN train epochs/s (fp16 vs fp32) + SpMM HBM GB/s and GEMM MFMA % of peak"
+HBM_PEAK_GBS = 8000.0
+PRECS = {"f32": 0, "f16": 1, "bf16": 2}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class EventTimer:
+    """Brackets library calls with HIP events on the current stream."""
+
+    def __init__(self):
+        import torch
+        self.torch = torch
+        self.pairs = []
+        self.enabled = False
+
+    def __call__(self):
+        timer = self
+
+        class _Ctx:
+            def __enter__(self_inner):
+                if timer.enabled:
+                    e = timer.torch.cuda.Event(enable_timing=True)
+                    e.record()
+                    self_inner.e = e
+                return self_inner
+
+            def __exit__(self_inner, *exc):
+                if timer.enabled:
+                    e2 = timer.torch.cuda.Event(enable_timing=True)
+                    e2.record()
+                    timer.pairs.append((self_inner.e, e2))
+                return False
+
+        return _Ctx()
+
+    def total_ms(self):
+        return sum(a.elapsed_time(b) for a, b in self.pairs)
+
+
+def agg_bytes(n, F, s):
+    """Algorithmic bytes of one dense aggregation Y = A_hat X: read A_hat
+    (s n^2), read X (s n F), write Y (s n F)."""
+    return s * n * n + 2 * s * n * F
+
+
+def run_gpu(wl, prec, steps, warmup, dense=True):
+    import torch
+    from paper_2010_12635_amd import gcn as G
+    from paper_2010_12635_amd.model import DeviceGraph, GCN2
+
+    spec = wl["spec"]
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    dg = DeviceGraph(wl["n"], wl["src"], wl["dst"], prec=prec, dense=dense,
+                     index=G.GCN_I64 if spec.index64 else G.GCN_I32)
+    scale0 = spec.loss_scale0 if prec != G.GCN_F32 else 1.0
+    m = GCN2(dg, wl["X"], wl["labels"], wl["mask"], wl["W1"], wl["W2"], wl["b1"], wl["b2"], prec=prec,
+             dropout=0.0 if spec.dropout is None else spec.dropout, seed=wl["dropout_seed"], loss_scale=scale0)
+    timer = EventTimer()
+    for ep in range(warmup):
+        m.step(ep, agg_timer=timer)
+    torch.cuda.synchronize()
+    timer.enabled = True
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    t_start.record()
+    for k in range(steps):
+        m.step(warmup + k, agg_timer=timer)
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = t_start.elapsed_time(t_end)
+    agg_ms = timer.total_ms()
+    loss = float(m.loss.item())
+    st = m.scaler_state()
+    peak = torch.cuda.max_memory_allocated() - base
+    res = dict(prec=prec, wall_s=wall, gpu_ms=gpu_ms, agg_ms=agg_ms, agg_launches=len(timer.pairs),
+               loss=loss, scaler=st, peak_bytes=int(peak), n=dg.n, nnz=dg.nnz,
+               f_h=m.f_h, C=m.C, f_in=m.f_in, n_correct=int(m.n_correct.item()), n_mask=m.n_mask)
+    del m, dg
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle, as it stands, on a bounded sample: full training epochs
+    (fp64) of the same workload until ``budget_s`` seconds have passed."""
+    import numpy as np
+    from oracle import gcn_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    spec = wl["spec"]
+    n = wl["n"]
+    g = O.graph(n, wl["src"], wl["dst"])
+    vals = O.norm_values(g)
+    dense = O.dense_adj(g, vals) if spec.dense_adj else None
+    x = wl["X"].astype(np.float16).astype(np.float64)
+    w1, w2 = wl["W1"].astype(np.float64), wl["W2"].astype(np.float64)
+    b1, b2 = wl["b1"].astype(np.float64), wl["b2"].astype(np.float64)
+    sizes = [w1.size, b1.size, w2.size, b2.size]
+    master = np.concatenate([w1.ravel(), b1, w2.ravel(), b2])
+    ad = O.AdamState(master.size)
+    sc = O.LossScaler(scale=1.0)
+    p = spec.dropout
+    epochs = 0
+    t0 = time.perf_counter()
+    while True:
+        o = np.cumsum([0] + sizes)
+        w1 = master[o[0]:o[1]].reshape(w1.shape); b1 = master[o[1]:o[2]]
+        w2 = master[o[2]:o[3]].reshape(w2.shape); b2 = master[o[3]:o[4]]
+        _, _, h1 = O.layer_fwd(g, vals, x, w1, b1, "relu", p, True, wl["dropout_seed"], 0, epochs, dense=dense)
+        _, z2, _ = O.layer_fwd(g, vals, h1, w2, b2, "none", dense=dense)
+        _, dz2, _ = O.softmax_ce(z2, wl["labels"], wl["mask"], 1.0)
+        _, dw2, db2, dz1 = O.layer_bwd(g, vals, h1, w2, dz2, "relu", p, dense=dense)
+        _, dw1, db1, _ = O.layer_bwd(g, vals, x, w1, dz1, "none", 0.0, dense=dense, need_dh=False)
+        master, _ = O.adam_step(master, np.concatenate([dw1.ravel(), db1, dw2.ravel(), db2]), ad, sc,
+                                lr=spec.lr)
+        epochs += 1
+        el = time.perf_counter() - t0
+        log(f"[bench] cpu oracle epoch {epochs} done, {el:.1f} s")
+        if el >= budget_s:
+            break
+    return dict(value=epochs / el, unit="epochs/s", cores=int(threads), kind="oracle",
+                sample=f"{epochs} full training epoch(s) (fwd+loss+bwd+Adam, fp64) of the same workload, "
+                       f"{el:.1f} s; host cores available: {len(os.sched_getaffinity(0))}")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="sbm16k_dense")
+    ap.add_argument("--prec", default="f16", choices=sorted(PRECS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-fp32", action="store_true", help="skip the fp32-mode run")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0 = skip)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build runs the GCN hot path on a single MI355X "
+              f"and has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    from paper_2010_12635_amd import gcn as G
+    from paper_2010_12635_amd import inputs as I
+    if not os.path.exists(G.LIB_PATH):
+        from paper_2010_12635_amd.build import build
+        build()
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    log(f"[bench] generating workload {args.workload} seed {args.seed}")
+    wl = I.workload(args.workload, args.seed)
+    spec = wl["spec"]
+    prec = PRECS[args.prec]
+    log(f"[bench] {args.prec} run: {args.warmup} warmup + {args.steps} timed epochs")
+    r = run_gpu(wl, prec, args.steps, args.warmup, dense=spec.dense_adj)
+    log(f"[bench] {args.prec}: {r['gpu_ms'] / args.steps:.3f} ms/epoch, loss {r['loss']:.4f}")
+    r32 = None
+    if not args.no_fp32 and prec != 0:
+        log("[bench] f32 run")
+        r32 = run_gpu(wl, 0, args.steps, args.warmup, dense=spec.dense_adj)
+        log(f"[bench] f32: {r32['gpu_ms'] / args.steps:.3f} ms/epoch, loss {r32['loss']:.4f}")
+
+    s = 4 if prec == 0 else 2
+    n = r["n"]
+    # forward aggregations per epoch: layer 1 (F = hidden), layer 2 (F = classes)
+    per_epoch_bytes = agg_bytes(n, r["f_h"], s) + agg_bytes(n, r["C"], s)
+    n_epochs_timed = r["agg_launches"] // 2
+    achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9
+    roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
+                    kernel="dense A_hat aggregation (MFMA GEMM, K split + fixed-order reduce)",
+                    launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
+                    algorithmic_bytes_per_launch_avg=int(per_epoch_bytes / 2))
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        log("[bench] cpu oracle baseline")
+        cpu = cpu_baseline(wl, args.cpu_seconds)
+
+    ms = r["gpu_ms"] / args.steps
+    out = {
+        "metric": METRIC,
+        "value": round(args.steps / (r["gpu_ms"] * 1e-3), 2),
+        "unit": "epochs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": args.prec,
+        "data": "synthetic",
+        "config": {
+            "workload": f"{spec.name}: 2-layer GCN, SBM n={n}, 32 blocks, p_in 0.01, p_out 0.0002, + self-loops; "
+                        f"dense {args.prec} A_hat; X {n}x{r['f_in']} N(0,1); hidden {r['f_h']}; {r['C']} classes "
+                        f"(block id); Adam lr {spec.lr}; loss scale 2^16" if spec.dense_adj else spec.name,
+            "n": n, "nnz": r["nnz"], "f_in": r["f_in"], "hidden": r["f_h"], "classes": r["C"],
+            "adjacency": "dense" if spec.dense_adj else "csr", "seed": args.seed,
+            "wall_s_timed": round(r["wall_s"], 4),
+        },
+        "fp32": None if r32 is None else {
+            "value": round(args.steps / (r32["gpu_ms"] * 1e-3), 2), "ms_per_step": round(r32["gpu_ms"] / args.steps, 4),
+            "peak_mem_bytes": r32["peak_bytes"], "final_loss": r32["loss"]},
+        "peak_mem_bytes": r["peak_bytes"],
+        "final_loss": r["loss"],
+        "train_acc": round(r["n_correct"] / max(1, r["n_mask"]), 4),
+        "loss_scale": r["scaler"],
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,281 @@
+/*
+ * gcn.h -- C ABI of libgcn: forward and backward of the graph convolutional
+ * layer on AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the layer of Kipf & Welling that the paper studies
+ * (Section "Graph Convolutions", Eq. (1)):
+ *
+ *     H' = sigma(A_hat (H W) + b),   A_hat = D^-1/2 (A + I) D^-1/2,
+ *
+ * for an undirected graph G = (V, E) whose edges are unordered vertex pairs
+ * (Section "Introduction", definition of A), with A: n x n, H: n x f_in,
+ * W: f_in x f_out (the shape list of Section "Graph Convolutions").  sigma is
+ * ReLU followed by inverted dropout on hidden layers and the identity on the
+ * output layer.  Storage precision follows the optimisation levels of Section
+ * "Background and Motivation": GCN_F32 is the all-fp32 level O0; GCN_F16 and
+ * GCN_BF16 are the O2 "almost fp16" level (16-bit weights and activations,
+ * fp32 master weights, fp32 optimiser, dynamic loss scaling).  Every product
+ * accumulates in fp32 in every mode.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.    Every array argument is device memory allocated and owned by the
+ *            caller (this library allocates nothing and keeps no global
+ *            state), except the documented host outputs (nnz_out, sizes).
+ *            Base pointers must be 16-byte aligned.
+ * Layout.    Row-major.  A matrix with logical width f has a leading
+ *            dimension ld >= f with ld % 8 == 0: the paper pads matrices to
+ *            multiples of 8 for 16-bit matrix units (Section "Reduced
+ *            Precision Changes"); here that rule is a layout rule and the
+ *            logical widths stay arbitrary.  Columns [f, ld) of an input are
+ *            ignored; columns [f, ld) of an output may be overwritten with 0.
+ * Streams.   `stream` is a hipStream_t (NULL = default stream).  All calls are
+ *            asynchronous on it, except gcn_normalize and gcn_schedule, which
+ *            synchronise it once to return sizes to the host.
+ * Errors.    Every call validates its arguments on the host before it
+ *            launches anything and returns a gcn_status; a call that returns
+ *            an argument error has had no effect.  GCN_ERR_DEVICE reports a
+ *            failed launch or runtime call.  Numeric overflow is not an
+ *            error: it sets *overflow (a device int32) to 1.
+ * Precision. `prec` (gcn_precision) is the storage type of H, W, S, H_out,
+ *            dZ, G_S and dZ_below.  Biases, gradients of W and b, dinv,
+ *            losses and optimiser state are fp32.
+ */
+#ifndef GCN_H
+#define GCN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GCN_ABI_VERSION 1
+
+typedef enum gcn_status {
+  GCN_OK = 0,
+  GCN_ERR_INVALID_ARG = 1,  /* NULL required pointer, bad enum, bad scalar   */
+  GCN_ERR_SHAPE = 2,        /* non-positive or inconsistent sizes            */
+  GCN_ERR_ALIGNMENT = 3,    /* ld % 8 != 0 or pointer not 16-byte aligned   */
+  GCN_ERR_UNSUPPORTED = 4,  /* valid but not implemented combination        */
+  GCN_ERR_CAPACITY = 5,     /* an output buffer is too small                 */
+  GCN_ERR_WORKSPACE = 6,    /* workspace missing or smaller than required   */
+  GCN_ERR_DEVICE = 7,       /* HIP runtime or launch failure                */
+  GCN_ERR_GRAPH = 8         /* edge list holds a vertex id outside [0, n)    */
+} gcn_status;
+
+typedef enum gcn_precision { GCN_F32 = 0, GCN_F16 = 1, GCN_BF16 = 2 } gcn_precision;
+typedef enum gcn_index { GCN_I32 = 0, GCN_I64 = 1 } gcn_index;       /* rowptr width */
+typedef enum gcn_adj_format { GCN_CSR = 0, GCN_DENSE = 1 } gcn_adj_format;
+typedef enum gcn_act { GCN_ACT_NONE = 0, GCN_ACT_RELU = 1 } gcn_act;
+
+/* Normalised adjacency A_hat (device arrays, caller-owned).
+ * CSR: rows sorted, columns sorted and unique within a row, A_hat symmetric
+ * (gcn_layer_bwd uses A_hat^T = A_hat).  values == NULL means
+ * A_hat_ij = dinv[i] * dinv[j] computed on the fly.
+ * DENSE: dense[i * ld_dense + j] = A_hat_ij in value_prec.
+ * The heavy-row schedule (filled by gcn_schedule) lets the CSR product split
+ * rows with more than heavy_threshold entries across workgroups; with
+ * n_heavy == 0 every row is processed whole. */
+typedef struct gcn_adj {
+  int64_t n;
+  int64_t nnz;
+  int32_t format;        /* gcn_adj_format */
+  int32_t index;         /* gcn_index of rowptr; colidx is always int32 */
+  int32_t value_prec;    /* gcn_precision of values / dense (== layer prec) */
+  int32_t reserved0;
+  const void* rowptr;    /* [n + 1] */
+  const int32_t* colidx; /* [nnz]   */
+  const void* values;    /* [nnz] or NULL */
+  const float* dinv;     /* [n]: deg^-1/2, deg counting the self-loop */
+  const void* dense;     /* [n x ld_dense] (GCN_DENSE) */
+  int64_t ld_dense;
+  int64_t heavy_threshold;        /* rows with more entries are "heavy"      */
+  int64_t chunk_nnz;              /* entries per chunk of a heavy row        */
+  int64_t n_heavy;                /* number of heavy rows                    */
+  int64_t n_chunks;               /* total chunks over all heavy rows        */
+  const int32_t* heavy_rows;      /* [n_heavy] ascending row ids             */
+  const int32_t* heavy_chunk_off; /* [n_heavy + 1] first chunk of each row   */
+  const int32_t* chunk_heavy;     /* [n_chunks] heavy-row slot of a chunk    */
+} gcn_adj;
+
+/* One layer: H (n x f_in, ld_in) -> H_out (n x f_out, ld_out); W is
+ * f_in x f_out with leading dimension ld_out; bias has f_out entries. */
+typedef struct gcn_layer {
+  int64_t f_in;
+  int64_t f_out;
+  int64_t ld_in;
+  int64_t ld_out;
+  int32_t act;           /* gcn_act applied after aggregation              */
+  float dropout_p;       /* in [0, 1); only with GCN_ACT_RELU and training  */
+  int32_t layer_id;      /* dropout stream id                               */
+  int32_t reserved0;
+} gcn_layer;
+
+/* Dynamic loss-scale state, device-resident (16 bytes). */
+typedef struct gcn_scaler {
+  float scale;           /* current loss scale S                            */
+  int32_t good_steps;    /* consecutive steps without overflow              */
+  int32_t step;          /* Adam step count t (applied steps only)          */
+  int32_t skipped;       /* total skipped steps                             */
+} gcn_scaler;
+
+typedef struct gcn_adam_config {
+  float lr, beta1, beta2, eps;
+  float backoff;         /* scale multiplier on overflow (0.5)              */
+  float growth;          /* scale multiplier after `interval` good steps (2)*/
+  int32_t interval;      /* good steps before growth (2000)                 */
+  float min_scale;       /* lower clamp of S (1)                            */
+  float max_scale;       /* upper clamp of S (2^24)                         */
+} gcn_adam_config;
+
+/* Human-readable name of a status code (static string). */
+const char* gcn_status_string(int32_t status);
+/* GCN_ABI_VERSION of the built library. */
+int32_t gcn_abi_version(void);
+
+/* ---------------------------------------------------------------------------
+ * gcn_normalize: build A_hat from an undirected edge list.
+ *
+ * Input: num_edges pairs (src[k], dst[k]) of vertex ids in [0, n).  A pair is
+ * an unordered edge {u, v} (Section "Introduction", definition of A):
+ * (u, v) and (v, u) are the same edge, repeats collapse, u == v pairs are
+ * dropped, and one self-loop per vertex is added (A + I).  Output is the
+ * canonical CSR (rows ascending, columns ascending and unique) with
+ * deg[i] = |N(i)| + 1, dinv[i] = float(1 / sqrt(double(deg[i]))),
+ * values[k] = dinv[row] * dinv[col] rounded to value_prec, and optionally
+ * the dense n x ld_dense matrix (all other entries zero).
+ *
+ * rowptr: [n + 1] of `index` width; colidx: [nnz_capacity] with
+ * nnz_capacity >= 2 * num_edges + n (always sufficient); deg (int32, may be
+ * NULL), dinv (required), values (may be NULL), dense (may be NULL).
+ * GCN_I32 requires 2 * num_edges + n < 2^31.  workspace: at least
+ * gcn_normalize_workspace_size() bytes.  *nnz_out (host) receives nnz.
+ * Synchronises `stream` once.  Returns GCN_ERR_GRAPH if a vertex id lies
+ * outside [0, n) (outputs are then undefined).  The result is bit-identical
+ * from run to run.
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_normalize_workspace_size(int64_t n, int64_t num_edges, size_t* bytes);
+gcn_status gcn_normalize(int64_t n, int64_t num_edges, const int32_t* src, const int32_t* dst,
+                         int32_t index, void* rowptr, int32_t* colidx, int64_t nnz_capacity,
+                         int32_t* deg, float* dinv, int32_t value_prec, void* values,
+                         void* dense, int64_t ld_dense, int64_t* nnz_out,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_schedule: fill the heavy-row fields of a CSR gcn_adj (n, nnz, index,
+ * rowptr must be set) so that rows with more than heavy_threshold entries
+ * are aggregated in chunks of chunk_nnz entries by separate workgroups and
+ * summed in a fixed order (run-to-run deterministic).  heavy_threshold <= 0
+ * and chunk_nnz <= 0 select the defaults (512 and 2048).  sched: device
+ * buffer of at least gcn_schedule_size() bytes that must outlive every use
+ * of *A.  Synchronises `stream` once.
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_schedule_size(int64_t n, int64_t nnz, int64_t heavy_threshold, int64_t chunk_nnz,
+                             size_t* bytes);
+gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz,
+                        void* sched, size_t sched_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_layer_fwd: one layer of Eq. (1), computed as A_hat (H W) + b.
+ *   S     = H W                               (n x f_out, ld_out, prec)
+ *   Z     = A_hat S + bias                    (bias fp32 [f_out], may be NULL)
+ *   H_out = dropout(ReLU(Z)) if act == RELU, else Z     (n x f_out, ld_out)
+ * Inverted dropout (training != 0, dropout_p > 0): element (i, j) with
+ * e = i * f_out + j is kept iff word (e % 8) of Philox-4x64-10 with key
+ * (seed, layer_id) and counter (e / 8, epoch, 0, 0) -- word 2t is the low
+ * and 2t + 1 the high half of output t -- is >= floor(p * 2^32); kept
+ * values are multiplied by 1 / (1 - p) in fp32.
+ * S is caller scratch that the backward pass does not need.  workspace: at
+ * least gcn_layer_workspace_size() bytes.  *overflow is set to 1 if any
+ * stored element of H_out is not finite.
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_layer_workspace_size(const gcn_adj* A, const gcn_layer* L, int32_t prec, size_t* bytes);
+gcn_status gcn_layer_fwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, int32_t training,
+                         const void* H, const void* W, const float* bias,
+                         uint64_t seed, uint64_t epoch, void* S, void* H_out,
+                         int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_transform and gcn_aggregate: the two halves of gcn_layer_fwd, for
+ * callers that schedule or time them separately (Eq. (1) read as
+ * A_hat (H W); the product is never re-associated).
+ *   gcn_transform:  S = H W     H: n x f_in (ld_in), W: f_in x f_out (ld_w),
+ *                               S: n x f_out (ld_s), all prec, fp32 accumulation.
+ *   gcn_aggregate:  Y = sigma(A_hat X + bias) with the epilogue of
+ *                   gcn_layer_fwd (act, dropout with key (seed, layer_id),
+ *                   counter (e / 8, epoch, 0, 0), e = i * F + j).
+ *                   X, Y: n x F (ldx, ldy), prec.
+ * Workspace sizes come from the matching *_workspace_size call.
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_transform_workspace_size(int64_t n, int64_t f_in, int64_t f_out, int32_t prec, size_t* bytes);
+gcn_status gcn_transform(int64_t n, int64_t f_in, int64_t f_out, int32_t prec, const void* H, int64_t ld_in,
+                         const void* W, int64_t ld_w, void* S, int64_t ld_s, int32_t* overflow,
+                         void* workspace, size_t workspace_bytes, void* stream);
+gcn_status gcn_aggregate_workspace_size(const gcn_adj* A, int64_t F, int32_t prec, size_t* bytes);
+gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* X, int64_t ldx,
+                         const float* bias, int32_t act, float dropout_p, int32_t training,
+                         uint64_t seed, int32_t layer_id, uint64_t epoch, void* Y, int64_t ldy,
+                         int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_layer_bwd: gradients of gcn_layer_fwd given dZ = dLoss/dZ (n x f_out,
+ * ld_out, prec, already multiplied by the loss scale):
+ *   G_S      = A_hat^T dZ = A_hat dZ           (GS: n x f_out, ld_out, prec)
+ *   dW       = H^T G_S                          (f_in x ld_out fp32; cols >= f_out set to 0)
+ *   dbias    = column sums of dZ                (ld_out fp32, may be NULL)
+ *   dZ_below = (G_S W^T) * [H > 0] / (1 - p_below)   if act_below == RELU
+ *            =  G_S W^T                               if act_below == NONE
+ *              (n x f_in, ld_in, prec; NULL skips it, e.g. for the first layer)
+ * The ReLU derivative at 0 is 0.  *overflow is set to 1 if any stored
+ * element of GS, dW, dbias or dZ_below is not finite.  dW and dbias are
+ * summed in a fixed order (run-to-run deterministic).
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec,
+                         const void* H, const void* W, const void* dZ,
+                         int32_t act_below, float p_below,
+                         float* dW, float* dbias, void* dZ_below, void* GS,
+                         int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_loss: masked mean softmax cross-entropy over logits (n x C, ld, prec)
+ * and labels (int32 in [0, C)); mask (uint8, NULL = every row) selects the
+ * n_mask training rows (n_mask = number of nonzero mask entries, > 0).
+ *   *loss        = mean over masked rows of logsumexp(z_i) - z_i[y_i]   (fp32, unscaled)
+ *   dlogits      = S * (softmax(z_i) - onehot(y_i)) / n_mask on masked rows, 0 elsewhere
+ *   *n_correct   = masked rows whose arg-max (lowest index on ties) is y_i (may be NULL)
+ * S is *loss_scale (device float; NULL means 1).  Class padding [C, ld) is
+ * excluded from the softmax.  The loss is reduced in a fixed order.
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_loss_workspace_size(int64_t n, int64_t C, size_t* bytes);
+gcn_status gcn_loss(int64_t n, int64_t C, int64_t ld, int32_t prec, const void* logits,
+                    const int32_t* labels, const uint8_t* mask, int64_t n_mask,
+                    const float* loss_scale, float* loss, void* dlogits, int32_t* n_correct,
+                    int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_optimizer_step: one step of Adam on fp32 master weights with dynamic
+ * loss scaling (Section "Background and Motivation", levels O1/O2), on
+ * `count` flat parameters.  grad holds loss-scaled gradients.
+ *   overflow = *overflow_flag != 0 or any grad element is not finite.
+ *   overflow: no parameter changes; S = max(S * backoff, min_scale);
+ *             good_steps = 0; skipped += 1.
+ *   else:     g = grad / S; step += 1; m = b1 m + (1 - b1) g;
+ *             v = b2 v + (1 - b2) g^2;
+ *             master -= lr * (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps);
+ *             working = master rounded to prec (may be NULL);
+ *             good_steps += 1; if good_steps == interval:
+ *             S = min(S * growth, max_scale), good_steps = 0.
+ * *overflow_flag is cleared to 0 for the next step.  state and
+ * overflow_flag are device memory; no host synchronisation happens.
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_optimizer_step(int64_t count, float* master, const float* grad, float* m, float* v,
+                              void* working, int32_t prec, const gcn_adam_config* cfg,
+                              gcn_scaler* state, int32_t* overflow_flag, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GCN_H */

@@ -1,0 +1,448 @@
+// C ABI of libgcn: argument validation on the host, then the kernel
+// sequence of each call on the caller's stream.  Nothing here allocates
+// device memory; scratch comes from the caller's workspace.
+#include <cmath>
+#include <cstdlib>
+
+#include "../../include/gcn.h"
+#include "internal.h"
+
+using namespace gcn;
+
+namespace {
+
+constexpr int64_t DEFAULT_HEAVY = 512;
+constexpr int64_t DEFAULT_CHUNK = 2048;
+
+bool valid_prec(int32_t p) { return p == GCN_F32 || p == GCN_F16 || p == GCN_BF16; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+size_t elem_bytes(int32_t prec) { return prec == GCN_F32 ? 4 : 2; }
+bool debug_sync() {
+  const char* e = std::getenv("GCN_DEBUG_SYNC");
+  return e && e[0] && e[0] != '0';
+}
+
+gcn_status finish(hipError_t e, hipStream_t s) {
+  if (e != hipSuccess) return GCN_ERR_DEVICE;
+  if (debug_sync()) {
+    if (hipStreamSynchronize(s) != hipSuccess) return GCN_ERR_DEVICE;
+    if (hipGetLastError() != hipSuccess) return GCN_ERR_DEVICE;
+  }
+  return GCN_OK;
+}
+
+#define GCN_HIP(x) do { hipError_t _e = (x); if (_e != hipSuccess) return finish(_e, s); } while (0)
+
+gcn_status check_layer(const gcn_layer* L) {
+  if (!L) return GCN_ERR_INVALID_ARG;
+  if (L->f_in <= 0 || L->f_out <= 0) return GCN_ERR_SHAPE;
+  if (L->ld_in < L->f_in || L->ld_out < L->f_out) return GCN_ERR_SHAPE;
+  if (L->ld_in % 8 || L->ld_out % 8) return GCN_ERR_ALIGNMENT;
+  if (L->act != GCN_ACT_NONE && L->act != GCN_ACT_RELU) return GCN_ERR_INVALID_ARG;
+  if (!(L->dropout_p >= 0.f && L->dropout_p < 1.f)) return GCN_ERR_INVALID_ARG;
+  return GCN_OK;
+}
+
+gcn_status check_adj(const gcn_adj* A, int32_t prec) {
+  if (!A) return GCN_ERR_INVALID_ARG;
+  if (A->n <= 0) return GCN_ERR_SHAPE;
+  if (A->format == GCN_DENSE) {
+    if (!A->dense) return GCN_ERR_INVALID_ARG;
+    if (A->value_prec != prec) return GCN_ERR_UNSUPPORTED;
+    if (A->ld_dense < A->n) return GCN_ERR_SHAPE;
+    if (A->ld_dense % 8 || !aligned16(A->dense)) return GCN_ERR_ALIGNMENT;
+    return GCN_OK;
+  }
+  if (A->format != GCN_CSR) return GCN_ERR_INVALID_ARG;
+  if (A->index != GCN_I32 && A->index != GCN_I64) return GCN_ERR_INVALID_ARG;
+  if (A->nnz < 0) return GCN_ERR_SHAPE;
+  if (!A->rowptr || (A->nnz > 0 && !A->colidx)) return GCN_ERR_INVALID_ARG;
+  if (A->values) {
+    if (A->value_prec != prec) return GCN_ERR_UNSUPPORTED;
+  } else if (!A->dinv) {
+    return GCN_ERR_INVALID_ARG;
+  }
+  if (A->n_heavy > 0) {
+    if (!A->heavy_rows || !A->heavy_chunk_off || !A->chunk_heavy) return GCN_ERR_INVALID_ARG;
+    if (A->chunk_nnz <= 0 || A->heavy_threshold <= 0 || A->n_chunks <= 0) return GCN_ERR_INVALID_ARG;
+  }
+  return GCN_OK;
+}
+
+CsrView view_of(const gcn_adj* A) {
+  CsrView v;
+  v.n = A->n; v.nnz = A->nnz; v.idx64 = A->index == GCN_I64;
+  v.rowptr = A->rowptr; v.colidx = A->colidx; v.values = A->values; v.dinv = A->dinv;
+  v.heavy_threshold = A->heavy_threshold; v.chunk_nnz = A->chunk_nnz;
+  v.n_heavy = A->n_heavy > 0 ? A->n_heavy : 0; v.n_chunks = A->n_chunks;
+  v.heavy_rows = A->heavy_rows; v.heavy_chunk_off = A->heavy_chunk_off; v.chunk_heavy = A->chunk_heavy;
+  return v;
+}
+
+// Partial-sum floats needed by each step of the layer (the workspace holds
+// one step's partials at a time).
+struct LayerPlan {
+  int s_split;       // S = H W
+  int agg_split;     // dense aggregation
+  int dw_split;      // dW = H^T G_S
+  int dh_split;      // dZ_below = G_S W^T
+  int64_t floats;
+};
+
+LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
+  LayerPlan p;
+  const int64_t n = A->n;
+  p.s_split = gemm_choose_splits(prec, n, L->f_out, L->f_in);
+  p.dh_split = gemm_choose_splits(prec, n, L->f_in, L->f_out);
+  p.dw_split = gemm_choose_splits(prec, L->f_in, L->f_out, n);
+  p.agg_split = A->format == GCN_DENSE ? gemm_choose_splits(prec, n, L->f_out, n) : 1;
+  int64_t f = 0;
+  auto upd = [&](int64_t x) { if (x > f) f = x; };
+  if (p.s_split > 1) upd(p.s_split * n * L->f_out);
+  if (p.dh_split > 1) upd(p.dh_split * n * L->f_in);
+  upd(p.dw_split * L->f_in * L->f_out);
+  if (A->format == GCN_DENSE) {
+    if (p.agg_split > 1) upd(p.agg_split * n * L->f_out);
+  } else {
+    upd(spmm_partials_floats(view_of(A), prec, L->f_out));
+  }
+  upd(colsum_partials_floats(n, L->ld_out));
+  p.floats = f;
+  return p;
+}
+
+size_t plan_bytes(const LayerPlan& p) { return (size_t)p.floats * sizeof(float) + 256; }
+
+Epilogue base_epi(void* out, int64_t ldo, int64_t rows, int64_t cols, int mode, int32_t* flag) {
+  Epilogue e{};
+  e.out = out; e.ldo = ldo; e.rows = rows; e.cols = cols; e.mode = mode; e.flag = flag;
+  e.keep_scale = 1.f;
+  return e;
+}
+
+hipError_t run_gemm(int32_t prec, bool akc, bool bkc, const void* A, int64_t lda, const void* B, int64_t ldb,
+                    int64_t M, int64_t N, int64_t K, int splits, bool force_partials, float* ws,
+                    const Epilogue& epi, hipStream_t s) {
+  GemmCall c;
+  c.prec = prec; c.a_kc = akc; c.b_kc = bkc; c.A = A; c.lda = lda; c.B = B; c.ldb = ldb;
+  c.M = M; c.N = N; c.K = K; c.splits = splits;
+  const bool use_partials = splits > 1 || force_partials;
+  c.partials = use_partials ? ws : nullptr;
+  c.epi = epi;
+  hipError_t e = gemm_launch(c, s);
+  if (e != hipSuccess || !use_partials) return e;
+  return reduce_partials(prec, ws, splits, M, N, epi, s);
+}
+
+hipError_t aggregate(const gcn_adj* A, int32_t prec, const void* X, int64_t ldx, int64_t F, int split,
+                     const Epilogue& epi, float* ws, hipStream_t s) {
+  if (A->format == GCN_DENSE)
+    return run_gemm(prec, true, false, A->dense, A->ld_dense, X, ldx, A->n, F, A->n, split, false, ws, epi, s);
+  return spmm_launch(view_of(A), prec, X, ldx, F, epi, ws, s);
+}
+
+size_t aggregate_bytes(const gcn_adj* A, int32_t prec, int64_t F) {
+  int64_t f = 0;
+  if (A->format == GCN_DENSE) {
+    const int sp = gemm_choose_splits(prec, A->n, F, A->n);
+    if (sp > 1) f = sp * A->n * F;
+  } else {
+    f = spmm_partials_floats(view_of(A), prec, F);
+  }
+  return (size_t)f * sizeof(float) + 256;
+}
+
+Epilogue agg_epi(void* Y, int64_t ldy, int64_t n, int64_t F, const float* bias, int32_t act, float p,
+                 int32_t training, uint64_t seed, int32_t layer_id, uint64_t epoch, int32_t* overflow) {
+  Epilogue ea = base_epi(Y, ldy, n, F, EPI_AGG, overflow);
+  ea.bias = bias;
+  ea.relu = act == GCN_ACT_RELU;
+  ea.dropout = ea.relu && training && p > 0.f;
+  if (ea.dropout) {
+    const double t = std::floor((double)p * 4294967296.0);
+    ea.thr = (uint32_t)(t > 4294967295.0 ? 4294967295.0 : t);
+    ea.keep_scale = 1.f / (1.f - p);
+  }
+  ea.seed = seed;
+  ea.layer = (uint64_t)(uint32_t)layer_id;
+  ea.epoch = epoch;
+  return ea;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gcn_status_string(int32_t status) {
+  switch (status) {
+    case GCN_OK: return "GCN_OK";
+    case GCN_ERR_INVALID_ARG: return "GCN_ERR_INVALID_ARG: missing pointer or invalid enum/scalar argument";
+    case GCN_ERR_SHAPE: return "GCN_ERR_SHAPE: non-positive or inconsistent sizes";
+    case GCN_ERR_ALIGNMENT: return "GCN_ERR_ALIGNMENT: leading dimension not a multiple of 8 or pointer not 16-byte aligned";
+    case GCN_ERR_UNSUPPORTED: return "GCN_ERR_UNSUPPORTED: combination not implemented";
+    case GCN_ERR_CAPACITY: return "GCN_ERR_CAPACITY: output buffer too small";
+    case GCN_ERR_WORKSPACE: return "GCN_ERR_WORKSPACE: workspace missing or too small";
+    case GCN_ERR_DEVICE: return "GCN_ERR_DEVICE: HIP runtime or kernel launch failure";
+    case GCN_ERR_GRAPH: return "GCN_ERR_GRAPH: vertex id outside [0, n)";
+  }
+  return "unknown gcn_status";
+}
+
+int32_t gcn_abi_version(void) { return GCN_ABI_VERSION; }
+
+gcn_status gcn_normalize_workspace_size(int64_t n, int64_t num_edges, size_t* bytes) {
+  if (!bytes) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || num_edges < 0) return GCN_ERR_SHAPE;
+  *bytes = normalize_workspace_bytes(n, num_edges);
+  return GCN_OK;
+}
+
+gcn_status gcn_normalize(int64_t n, int64_t num_edges, const int32_t* src, const int32_t* dst, int32_t index,
+                         void* rowptr, int32_t* colidx, int64_t nnz_capacity, int32_t* deg, float* dinv,
+                         int32_t value_prec, void* values, void* dense, int64_t ld_dense, int64_t* nnz_out,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n <= 0 || num_edges < 0) return GCN_ERR_SHAPE;
+  if (n > INT32_MAX) return GCN_ERR_UNSUPPORTED;
+  if (num_edges > 0 && (!src || !dst)) return GCN_ERR_INVALID_ARG;
+  if (!rowptr || !colidx || !dinv || !nnz_out) return GCN_ERR_INVALID_ARG;
+  if (index != GCN_I32 && index != GCN_I64) return GCN_ERR_INVALID_ARG;
+  if ((values || dense) && !valid_prec(value_prec)) return GCN_ERR_INVALID_ARG;
+  const int64_t max_nnz = 2 * num_edges + n;
+  if (nnz_capacity < max_nnz) return GCN_ERR_CAPACITY;
+  if (index == GCN_I32 && max_nnz >= INT32_MAX) return GCN_ERR_UNSUPPORTED;
+  if (dense) {
+    if (ld_dense < n) return GCN_ERR_SHAPE;
+    if (ld_dense % 8 || !aligned16(dense)) return GCN_ERR_ALIGNMENT;
+  }
+  if (!workspace || workspace_bytes < normalize_workspace_bytes(n, num_edges)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  int64_t nnz = 0;
+  int32_t bad = 0;
+  hipError_t e = normalize_run(n, num_edges, src, dst, index == GCN_I64, rowptr, colidx, deg, dinv, value_prec,
+                               values, dense, ld_dense, &nnz, &bad, workspace, workspace_bytes, s);
+  if (e != hipSuccess) return GCN_ERR_DEVICE;
+  if (bad) return GCN_ERR_GRAPH;
+  *nnz_out = nnz;
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_schedule_size(int64_t n, int64_t nnz, int64_t heavy_threshold, int64_t chunk_nnz, size_t* bytes) {
+  if (!bytes) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || nnz < 0) return GCN_ERR_SHAPE;
+  (void)heavy_threshold;
+  if (chunk_nnz <= 0) chunk_nnz = DEFAULT_CHUNK;
+  *bytes = schedule_bytes(n, nnz, chunk_nnz);
+  return GCN_OK;
+}
+
+gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, void* sched, size_t sched_bytes,
+                        void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!A || !sched) return GCN_ERR_INVALID_ARG;
+  if (A->format != GCN_CSR || !A->rowptr) return GCN_ERR_INVALID_ARG;
+  if (A->index != GCN_I32 && A->index != GCN_I64) return GCN_ERR_INVALID_ARG;
+  if (A->n <= 0 || A->nnz < 0) return GCN_ERR_SHAPE;
+  if (heavy_threshold <= 0) heavy_threshold = DEFAULT_HEAVY;
+  if (chunk_nnz <= 0) chunk_nnz = DEFAULT_CHUNK;
+  if (sched_bytes < schedule_bytes(A->n, A->nnz, chunk_nnz)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(sched)) return GCN_ERR_ALIGNMENT;
+  int32_t *hr = nullptr, *hco = nullptr, *ch = nullptr;
+  int64_t nh = 0, nc = 0;
+  hipError_t e = schedule_run(A->n, A->nnz, A->index == GCN_I64, A->rowptr, heavy_threshold, chunk_nnz, sched,
+                              sched_bytes, &hr, &hco, &ch, &nh, &nc, s);
+  if (e != hipSuccess) return GCN_ERR_DEVICE;
+  A->heavy_threshold = heavy_threshold;
+  A->chunk_nnz = chunk_nnz;
+  A->n_heavy = nh;
+  A->n_chunks = nc;
+  A->heavy_rows = hr;
+  A->heavy_chunk_off = hco;
+  A->chunk_heavy = ch;
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_layer_workspace_size(const gcn_adj* A, const gcn_layer* L, int32_t prec, size_t* bytes) {
+  if (!bytes || !valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  gcn_status st = check_adj(A, prec);
+  if (st != GCN_OK) return st;
+  st = check_layer(L);
+  if (st != GCN_OK) return st;
+  *bytes = plan_bytes(plan_layer(A, L, prec));
+  return GCN_OK;
+}
+
+gcn_status gcn_layer_fwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, int32_t training, const void* H,
+                         const void* W, const float* bias, uint64_t seed, uint64_t epoch, void* S, void* H_out,
+                         int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  gcn_status st = check_adj(A, prec);
+  if (st != GCN_OK) return st;
+  st = check_layer(L);
+  if (st != GCN_OK) return st;
+  if (!H || !W || !S || !H_out) return GCN_ERR_INVALID_ARG;
+  if (!aligned16(H) || !aligned16(W) || !aligned16(S) || !aligned16(H_out)) return GCN_ERR_ALIGNMENT;
+  const LayerPlan plan = plan_layer(A, L, prec);
+  if (!workspace || workspace_bytes < plan_bytes(plan)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  float* ws = static_cast<float*>(workspace);
+  const int64_t n = A->n;
+
+  Epilogue es = base_epi(S, L->ld_out, n, L->f_out, EPI_STORE, overflow);
+  GCN_HIP(run_gemm(prec, true, false, H, L->ld_in, W, L->ld_out, n, L->f_out, L->f_in, plan.s_split, false, ws, es, s));
+
+  Epilogue ea = agg_epi(H_out, L->ld_out, n, L->f_out, bias, L->act, L->dropout_p, training, seed, L->layer_id,
+                        epoch, overflow);
+  GCN_HIP(aggregate(A, prec, S, L->ld_out, L->f_out, plan.agg_split, ea, ws, s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_transform_workspace_size(int64_t n, int64_t f_in, int64_t f_out, int32_t prec, size_t* bytes) {
+  if (!bytes || !valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || f_in <= 0 || f_out <= 0) return GCN_ERR_SHAPE;
+  const int sp = gemm_choose_splits(prec, n, f_out, f_in);
+  *bytes = (size_t)(sp > 1 ? sp * n * f_out : 0) * sizeof(float) + 256;
+  return GCN_OK;
+}
+
+gcn_status gcn_transform(int64_t n, int64_t f_in, int64_t f_out, int32_t prec, const void* H, int64_t ld_in,
+                         const void* W, int64_t ld_w, void* S, int64_t ld_s, int32_t* overflow, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || f_in <= 0 || f_out <= 0 || ld_in < f_in || ld_w < f_out || ld_s < f_out) return GCN_ERR_SHAPE;
+  if (ld_in % 8 || ld_w % 8 || ld_s % 8) return GCN_ERR_ALIGNMENT;
+  if (!H || !W || !S) return GCN_ERR_INVALID_ARG;
+  if (!aligned16(H) || !aligned16(W) || !aligned16(S)) return GCN_ERR_ALIGNMENT;
+  const int sp = gemm_choose_splits(prec, n, f_out, f_in);
+  const size_t need = (size_t)(sp > 1 ? sp * n * f_out : 0) * sizeof(float) + 256;
+  if (sp > 1 && (!workspace || workspace_bytes < need)) return GCN_ERR_WORKSPACE;
+  if (workspace && !aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  Epilogue es = base_epi(S, ld_s, n, f_out, EPI_STORE, overflow);
+  GCN_HIP(run_gemm(prec, true, false, H, ld_in, W, ld_w, n, f_out, f_in, sp, false, static_cast<float*>(workspace),
+                   es, s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_aggregate_workspace_size(const gcn_adj* A, int64_t F, int32_t prec, size_t* bytes) {
+  if (!bytes || !valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  gcn_status st = check_adj(A, prec);
+  if (st != GCN_OK) return st;
+  if (F <= 0) return GCN_ERR_SHAPE;
+  *bytes = aggregate_bytes(A, prec, F);
+  return GCN_OK;
+}
+
+gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* X, int64_t ldx, const float* bias,
+                         int32_t act, float dropout_p, int32_t training, uint64_t seed, int32_t layer_id,
+                         uint64_t epoch, void* Y, int64_t ldy, int32_t* overflow, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  gcn_status st = check_adj(A, prec);
+  if (st != GCN_OK) return st;
+  if (F <= 0 || ldx < F || ldy < F) return GCN_ERR_SHAPE;
+  if (ldx % 8 || ldy % 8) return GCN_ERR_ALIGNMENT;
+  if (act != GCN_ACT_NONE && act != GCN_ACT_RELU) return GCN_ERR_INVALID_ARG;
+  if (!(dropout_p >= 0.f && dropout_p < 1.f)) return GCN_ERR_INVALID_ARG;
+  if (!X || !Y) return GCN_ERR_INVALID_ARG;
+  if (!aligned16(X) || !aligned16(Y)) return GCN_ERR_ALIGNMENT;
+  if (workspace_bytes < aggregate_bytes(A, prec, F) || (!workspace && aggregate_bytes(A, prec, F) > 256))
+    return GCN_ERR_WORKSPACE;
+  if (workspace && !aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  Epilogue ea = agg_epi(Y, ldy, A->n, F, bias, act, dropout_p, training, seed, layer_id, epoch, overflow);
+  const int split = A->format == GCN_DENSE ? gemm_choose_splits(prec, A->n, F, A->n) : 1;
+  GCN_HIP(aggregate(A, prec, X, ldx, F, split, ea, static_cast<float*>(workspace), s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
+                         const void* dZ, int32_t act_below, float p_below, float* dW, float* dbias, void* dZ_below,
+                         void* GS, int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  gcn_status st = check_adj(A, prec);
+  if (st != GCN_OK) return st;
+  st = check_layer(L);
+  if (st != GCN_OK) return st;
+  if (!H || !W || !dZ || !dW || !GS) return GCN_ERR_INVALID_ARG;
+  if (act_below != GCN_ACT_NONE && act_below != GCN_ACT_RELU) return GCN_ERR_INVALID_ARG;
+  if (!(p_below >= 0.f && p_below < 1.f)) return GCN_ERR_INVALID_ARG;
+  if (!aligned16(H) || !aligned16(W) || !aligned16(dZ) || !aligned16(dW) || !aligned16(GS) ||
+      (dZ_below && !aligned16(dZ_below)) || (dbias && !aligned16(dbias)))
+    return GCN_ERR_ALIGNMENT;
+  const LayerPlan plan = plan_layer(A, L, prec);
+  if (!workspace || workspace_bytes < plan_bytes(plan)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  float* ws = static_cast<float*>(workspace);
+  const int64_t n = A->n;
+
+  // G_S = A_hat^T dZ = A_hat dZ (A_hat symmetric)
+  Epilogue eg = base_epi(GS, L->ld_out, n, L->f_out, EPI_STORE, overflow);
+  GCN_HIP(aggregate(A, prec, dZ, L->ld_out, L->f_out, plan.agg_split, eg, ws, s));
+  // dbias = column sums of dZ
+  if (dbias) GCN_HIP(colsum(prec, dZ, n, L->f_out, L->ld_out, ws, dbias, L->ld_out, overflow, s));
+  // dW = H^T G_S (fp32, split over vertices, fixed-order reduction)
+  Epilogue ew = base_epi(dW, L->ld_out, L->f_in, L->f_out, EPI_F32, overflow);
+  GCN_HIP(run_gemm(prec, false, false, H, L->ld_in, GS, L->ld_out, L->f_in, L->f_out, n, plan.dw_split, true, ws,
+                   ew, s));
+  // dZ_below = (G_S W^T) * [H > 0] / (1 - p_below)
+  if (dZ_below) {
+    Epilogue ed = base_epi(dZ_below, L->ld_in, n, L->f_in, EPI_DMASK, overflow);
+    ed.relu = act_below == GCN_ACT_RELU;
+    ed.keep_scale = 1.f / (1.f - p_below);
+    ed.hmask = H;
+    ed.ldh = L->ld_in;
+    GCN_HIP(run_gemm(prec, true, true, GS, L->ld_out, W, L->ld_out, n, L->f_in, L->f_out, plan.dh_split, false, ws,
+                     ed, s));
+  }
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_loss_workspace_size(int64_t n, int64_t C, size_t* bytes) {
+  if (!bytes) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || C <= 0) return GCN_ERR_SHAPE;
+  *bytes = loss_workspace_bytes(n, C);
+  return GCN_OK;
+}
+
+gcn_status gcn_loss(int64_t n, int64_t C, int64_t ld, int32_t prec, const void* logits, const int32_t* labels,
+                    const uint8_t* mask, int64_t n_mask, const float* loss_scale, float* loss, void* dlogits,
+                    int32_t* n_correct, int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || C <= 0 || ld < C || n_mask <= 0 || n_mask > n) return GCN_ERR_SHAPE;
+  if (ld % 8) return GCN_ERR_ALIGNMENT;
+  if (C > 64 * (prec == GCN_F32 ? 4 : 8)) return GCN_ERR_UNSUPPORTED;
+  if (!logits || !labels || !loss || !dlogits) return GCN_ERR_INVALID_ARG;
+  if (!aligned16(logits) || !aligned16(dlogits)) return GCN_ERR_ALIGNMENT;
+  if (!workspace || workspace_bytes < loss_workspace_bytes(n, C)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  GCN_HIP(loss_launch(prec, n, C, ld, logits, labels, mask, n_mask, loss_scale, loss, dlogits, n_correct, overflow,
+                      workspace, s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_optimizer_step(int64_t count, float* master, const float* grad, float* m, float* v, void* working,
+                              int32_t prec, const gcn_adam_config* cfg, gcn_scaler* state, int32_t* overflow_flag,
+                              void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (count <= 0) return GCN_ERR_SHAPE;
+  if (!master || !grad || !m || !v || !cfg || !state || !overflow_flag) return GCN_ERR_INVALID_ARG;
+  if (working && !valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  if (!(cfg->lr > 0.f) || !(cfg->beta1 >= 0.f && cfg->beta1 < 1.f) || !(cfg->beta2 >= 0.f && cfg->beta2 < 1.f) ||
+      !(cfg->eps >= 0.f) || !(cfg->backoff > 0.f && cfg->backoff <= 1.f) || !(cfg->growth >= 1.f) ||
+      cfg->interval <= 0 || !(cfg->min_scale > 0.f) || !(cfg->max_scale >= cfg->min_scale))
+    return GCN_ERR_INVALID_ARG;
+  AdamHyper hp;
+  hp.lr = cfg->lr; hp.beta1 = cfg->beta1; hp.beta2 = cfg->beta2; hp.eps = cfg->eps;
+  hp.backoff = cfg->backoff; hp.growth = cfg->growth; hp.interval = cfg->interval;
+  hp.min_scale = cfg->min_scale; hp.max_scale = cfg->max_scale;
+  static_assert(sizeof(gcn_scaler) == sizeof(ScalerState), "scaler layout");
+  GCN_HIP(optimizer_launch(count, master, grad, m, v, working, prec, hp, reinterpret_cast<ScalerState*>(state),
+                           overflow_flag, s));
+  return finish(hipSuccess, s);
+}
+
+}  // extern "C"

@@ -1,0 +1,193 @@
+// Device-side helpers shared by the libgcn kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gcn {
+
+typedef _Float16 f16;
+typedef __bf16 bf16;
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte vector of storage elements: 8 x 16-bit or 4 x fp32.
+template <typename T> struct Vec;
+template <> struct Vec<float> { static constexpr int N = 4; typedef f32x4 type; };
+template <> struct Vec<f16>   { static constexpr int N = 8; typedef f16x8 type; };
+template <> struct Vec<bf16>  { static constexpr int N = 8; typedef bf16x8 type; };
+
+template <typename T> __device__ __forceinline__ float to_f32(T x) { return (float)x; }
+// Round-to-nearest-even conversions (v_cvt_f16_f32 / bf16 RNE), never the
+// round-toward-zero packed forms.
+template <typename T> __device__ __forceinline__ T from_f32(float x) { return (T)x; }
+
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+__device__ __forceinline__ void stg16(void* p, uint4 v) {
+  *reinterpret_cast<uint4*>(p) = v;
+}
+
+// Unpack a 16-byte vector of storage elements into fp32.
+template <typename T>
+__device__ __forceinline__ void unpack(uint4 raw, float* out) {
+  const T* e = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+  for (int i = 0; i < Vec<T>::N; ++i) out[i] = to_f32<T>(e[i]);
+}
+template <typename T>
+__device__ __forceinline__ uint4 pack(const float* in) {
+  uint4 raw;
+  T* e = reinterpret_cast<T*>(&raw);
+#pragma unroll
+  for (int i = 0; i < Vec<T>::N; ++i) e[i] = from_f32<T>(in[i]);
+  return raw;
+}
+
+__device__ __forceinline__ bool finite_f32(float x) {
+  return (__float_as_uint(x) & 0x7f800000u) != 0x7f800000u;
+}
+
+// ---------------------------------------------------------------------------
+// Philox-4x64-10 (Salmon, Moraes, Dror & Shaw, SC'11): ten rounds of two
+// 64x64->128-bit multiplies; the key is bumped by two Weyl constants between
+// rounds.
+// ---------------------------------------------------------------------------
+struct Philox8 { uint64_t w[4]; };
+
+__device__ __forceinline__ Philox8 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
+                                                  uint64_t k0, uint64_t k1) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+    uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+    uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+    k0 += W0; k1 += W1;
+  }
+  Philox8 o; o.w[0] = c0; o.w[1] = c1; o.w[2] = c2; o.w[3] = c3;
+  return o;
+}
+
+__device__ __forceinline__ uint32_t philox_word(const Philox8& o, uint32_t w) {
+  uint64_t x = o.w[w >> 1];
+  return (w & 1) ? (uint32_t)(x >> 32) : (uint32_t)x;
+}
+
+// ---------------------------------------------------------------------------
+// Output epilogue shared by the aggregation and GEMM kernels.
+// ---------------------------------------------------------------------------
+enum EpiMode : int {
+  EPI_STORE = 0,   // out = cvt(acc)
+  EPI_AGG = 1,     // out = cvt(dropout(act(acc + bias)))
+  EPI_DMASK = 2,   // out = cvt(acc * [H > 0] * keep_scale)  (or acc if !relu_below)
+  EPI_F32 = 3,     // out(fp32) = acc
+};
+
+struct Epilogue {
+  void* out;             // output base (T or fp32 for EPI_F32)
+  int64_t ldo;
+  int64_t rows, cols;    // logical output size
+  int mode;
+  // EPI_AGG
+  const float* bias;
+  int relu;
+  int dropout;           // training && p > 0
+  uint32_t thr;          // floor(p * 2^32)
+  float keep_scale;      // 1 / (1 - p)
+  uint64_t seed;
+  uint64_t layer;
+  uint64_t epoch;
+  // EPI_DMASK
+  const void* hmask;     // H (T), same shape as output
+  int64_t ldh;
+  // overflow flag (may be NULL)
+  int32_t* flag;
+};
+
+// Keep decision for element linear index e = row * cols + col.
+__device__ __forceinline__ bool dropout_keep(const Epilogue& ep, uint64_t e) {
+  Philox8 o = philox4x64_10(e >> 3, ep.epoch, 0, 0, ep.seed, ep.layer);
+  return philox_word(o, (uint32_t)(e & 7)) >= ep.thr;
+}
+
+__device__ __forceinline__ void raise_flag(int32_t* flag) {
+  if (flag) *reinterpret_cast<volatile int32_t*>(flag) = 1;
+}
+
+// Scalar epilogue for one element (row < rows, col < cols).
+template <typename T>
+__device__ __forceinline__ void epi_store1(const Epilogue& ep, int64_t row, int64_t col, float acc) {
+  if (ep.mode == EPI_F32) {
+    reinterpret_cast<float*>(ep.out)[row * ep.ldo + col] = acc;
+    if (!finite_f32(acc)) raise_flag(ep.flag);
+    return;
+  }
+  float z = acc;
+  if (ep.mode == EPI_AGG) {
+    if (ep.bias) z += ep.bias[col];
+    if (ep.relu) {
+      z = z > 0.f ? z : 0.f;
+      if (ep.dropout) z = dropout_keep(ep, (uint64_t)row * (uint64_t)ep.cols + (uint64_t)col) ? z * ep.keep_scale : 0.f;
+    }
+  } else if (ep.mode == EPI_DMASK) {
+    if (ep.relu) {
+      float h = to_f32<T>(reinterpret_cast<const T*>(ep.hmask)[row * ep.ldh + col]);
+      z = h > 0.f ? z * ep.keep_scale : 0.f;
+    }
+  }
+  T o = from_f32<T>(z);
+  reinterpret_cast<T*>(ep.out)[row * ep.ldo + col] = o;
+  if (!finite_f32(to_f32<T>(o))) raise_flag(ep.flag);
+}
+
+// Vector epilogue: Vec<T>::N consecutive columns starting at col0 (col0 is a
+// multiple of the vector width, col0 < cols).  Columns >= cols are written 0.
+template <typename T>
+__device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, int64_t col0, float* acc) {
+  constexpr int VE = Vec<T>::N;
+  const int64_t cols = ep.cols;
+  if (ep.mode == EPI_AGG) {
+    if (ep.bias) {
+#pragma unroll
+      for (int i = 0; i < VE; ++i)
+        if (col0 + i < cols) acc[i] += ep.bias[col0 + i];
+    }
+    if (ep.relu) {
+#pragma unroll
+      for (int i = 0; i < VE; ++i) acc[i] = acc[i] > 0.f ? acc[i] : 0.f;
+      if (ep.dropout) {
+        const uint64_t e0 = (uint64_t)row * (uint64_t)cols + (uint64_t)col0;
+        uint64_t blk = e0 >> 3;
+        Philox8 o = philox4x64_10(blk, ep.epoch, 0, 0, ep.seed, ep.layer);
+#pragma unroll
+        for (int i = 0; i < VE; ++i) {
+          uint64_t e = e0 + i;
+          if ((e >> 3) != blk) {
+            blk = e >> 3;
+            o = philox4x64_10(blk, ep.epoch, 0, 0, ep.seed, ep.layer);
+          }
+          acc[i] = philox_word(o, (uint32_t)(e & 7)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
+        }
+      }
+    }
+  }
+  bool bad = false;
+  uint4 raw;
+  T* e = reinterpret_cast<T*>(&raw);
+#pragma unroll
+  for (int i = 0; i < VE; ++i) {
+    float z = (col0 + i < cols) ? acc[i] : 0.f;
+    e[i] = from_f32<T>(z);
+    bad |= !finite_f32(to_f32<T>(e[i]));
+  }
+  stg16(reinterpret_cast<T*>(ep.out) + row * ep.ldo + col0, raw);
+  if (bad) raise_flag(ep.flag);
+}
+
+}  // namespace gcn

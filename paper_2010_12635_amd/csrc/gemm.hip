@@ -1,0 +1,352 @@
+// Dense contractions of the GCN layer on gfx950 matrix cores:
+//   S = H W, dH = G_S W^T (epilogue: ReLU / dropout derivative), dW = H^T G_S
+//   (split over the vertex dimension), and the dense-A_hat aggregation.
+//
+// One templated kernel covers every operand orientation.  Tiles of A and B
+// are staged through LDS in "k-contiguous" form (each row of the LDS tile
+// holds consecutive k of one output row / column), so that every MFMA
+// operand fragment is one 16-byte LDS read:
+//   16-bit storage: v_mfma_f32_16x16x32_{f16,bf16}, 8 k per lane;
+//   fp32 storage:   four v_mfma_f32_16x16x4_f32, 4 k per lane.
+// Within an MFMA, lane l supplies row (l % 16) of A and column (l % 16) of
+// B; which k a lane group supplies only has to agree between A and B, so
+// the fp32 path assigns k = 4 * (l / 16) + step to keep 16-byte reads.
+// Operands stored with k as the slow axis (H^T, G_S in dW; W in S = H W)
+// are transposed while being written to LDS.
+#include "internal.h"
+
+#include <algorithm>
+
+namespace gcn {
+
+namespace {
+
+template <typename T> struct Mfma;
+
+template <> struct Mfma<f16> {
+  static __device__ __forceinline__ f32x4 run(uint4 a, uint4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<bf16> {
+  static __device__ __forceinline__ f32x4 run(uint4 a, uint4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<float> {
+  static __device__ __forceinline__ f32x4 run(uint4 a, uint4 b, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    return c;
+  }
+};
+
+template <typename T> constexpr int k_tile() { return 8 * Vec<T>::N; }   // 64 (16-bit) / 32 (fp32)
+
+struct GemmParams {
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  int64_t M, N, K;
+  int64_t k_per_split;
+  int splits;
+  float* partials;
+  Epilogue epi;
+};
+
+// Loads a (R x BK) operand tile (R = output rows or columns) from global
+// memory into registers, then writes it k-contiguous into LDS.
+//   KC:  element (r, k) at base[r * ld + k]
+//   !KC: element (r, k) at base[k * ld + r]
+// Elements outside [0, Rtot) x [k0, kend) are zero.  16-byte loads stay in
+// bounds because ld >= round_up(width, 8) and ld % 8 == 0.
+template <typename T, bool KC, int R, int BK>
+struct TileLoader {
+  static constexpr int VE = Vec<T>::N;
+  static constexpr int LDK = BK + VE;
+  static constexpr int NVEC = R * BK / VE;
+  static constexpr int PER = (NVEC + 255) / 256;
+  uint4 reg[PER];
+
+  __device__ __forceinline__ void load(const T* __restrict__ base, int64_t ld, int64_t r0, int64_t Rtot,
+                                       int64_t k0, int64_t kend, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int v = tid + i * 256;
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (v < NVEC) {
+        if (KC) {
+          const int r = v / (BK / VE), kv = v % (BK / VE);
+          const int64_t gr = r0 + r, gk = k0 + (int64_t)kv * VE;
+          if (gr < Rtot && gk < kend) {
+            x = ldg16(base + gr * ld + gk);
+            if (gk + VE > kend) {
+              T* e = reinterpret_cast<T*>(&x);
+#pragma unroll
+              for (int j = 0; j < VE; ++j)
+                if (gk + j >= kend) e[j] = T(0);
+            }
+          }
+        } else {
+          const int k = v / (R / VE), rv = v % (R / VE);
+          const int64_t gk = k0 + k, gr = r0 + (int64_t)rv * VE;
+          if (gk < kend && gr < Rtot) {
+            x = ldg16(base + gk * ld + gr);
+            if (gr + VE > Rtot) {
+              T* e = reinterpret_cast<T*>(&x);
+#pragma unroll
+              for (int j = 0; j < VE; ++j)
+                if (gr + j >= Rtot) e[j] = T(0);
+            }
+          }
+        }
+      }
+      reg[i] = x;
+    }
+  }
+
+  __device__ __forceinline__ void store(T* __restrict__ s, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int v = tid + i * 256;
+      if (v < NVEC) {
+        if (KC) {
+          const int r = v / (BK / VE), kv = v % (BK / VE);
+          *reinterpret_cast<uint4*>(s + r * LDK + kv * VE) = reg[i];
+        } else {
+          const int k = v / (R / VE), rv = v % (R / VE);
+          const T* e = reinterpret_cast<const T*>(&reg[i]);
+#pragma unroll
+          for (int j = 0; j < VE; ++j) s[(rv * VE + j) * LDK + k] = e[j];
+        }
+      }
+    }
+  }
+};
+
+template <typename T, bool AKC, bool BKC, int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
+  constexpr int VE = Vec<T>::N;
+  constexpr int BK = k_tile<T>();
+  constexpr int LDK = BK + VE;
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 16, TN = WTN / 16;
+  static_assert(WM * WN == 4, "four waves per workgroup");
+  static_assert(TM >= 1 && TN >= 1, "wave tile at least 16 x 16");
+
+  __shared__ __align__(16) T sA[2][BM * LDK];
+  __shared__ __align__(16) T sB[2][BN * LDK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int64_t m0 = (int64_t)blockIdx.x * BM, n0 = (int64_t)blockIdx.y * BN;
+  const int64_t kb = (int64_t)blockIdx.z * p.k_per_split;
+  const int64_t ke = min(p.K, kb + p.k_per_split);
+  const T* __restrict__ A = reinterpret_cast<const T*>(p.A);
+  const T* __restrict__ B = reinterpret_cast<const T*>(p.B);
+
+  f32x4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  TileLoader<T, AKC, BM, BK> la;
+  TileLoader<T, BKC, BN, BK> lb;
+  const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+  if (nk > 0) {
+    la.load(A, p.lda, m0, p.M, kb, ke, tid);
+    lb.load(B, p.ldb, n0, p.N, kb, ke, tid);
+  }
+  for (int64_t t = 0; t < nk; ++t) {
+    const int st = (int)(t & 1);
+    la.store(sA[st], tid);
+    lb.store(sB[st], tid);
+    __syncthreads();
+    if (t + 1 < nk) {
+      const int64_t k0 = kb + (t + 1) * BK;
+      la.load(A, p.lda, m0, p.M, k0, ke, tid);
+      lb.load(B, p.ldb, n0, p.N, k0, ke, tid);
+    }
+    const T* a_s = sA[st] + (wm * WTM + (lane & 15)) * LDK + (lane >> 4) * VE;
+    const T* b_s = sB[st] + (wn * WTN + (lane & 15)) * LDK + (lane >> 4) * VE;
+#pragma unroll
+    for (int ks = 0; ks < BK / (4 * VE); ++ks) {
+      uint4 af[TM], bf[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const uint4*>(a_s + i * 16 * LDK + ks * 4 * VE);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bf[j] = *reinterpret_cast<const uint4*>(b_s + j * 16 * LDK + ks * 4 * VE);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::run(af[i], bf[j], acc[i][j]);
+    }
+  }
+
+  // Accumulator layout of a 16 x 16 MFMA tile: lane l holds rows
+  // 4 * (l / 16) + v, v = 0..3, of column l % 16.
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t row = m0 + wm * WTM + i * 16 + (lane >> 4) * 4 + v;
+        const int64_t col = n0 + wn * WTN + j * 16 + (lane & 15);
+        if (row < p.M && col < p.N) {
+          if (p.partials)
+            p.partials[((int64_t)blockIdx.z * p.M + row) * p.N + col] = acc[i][j][v];
+          else
+            epi_store1<T>(p.epi, row, col, acc[i][j][v]);
+        }
+      }
+}
+
+template <typename T, bool AKC, bool BKC>
+hipError_t launch_layout(const GemmParams& p, hipStream_t s) {
+  const dim3 block(256);
+  const int64_t BM = 128;
+  if (p.N <= 16) {
+    dim3 grid((unsigned)((p.M + BM - 1) / BM), (unsigned)((p.N + 15) / 16), (unsigned)p.splits);
+    hipLaunchKernelGGL((gemm_kernel<T, AKC, BKC, 128, 16, 4, 1>), grid, block, 0, s, p);
+  } else if (p.N <= 32) {
+    dim3 grid((unsigned)((p.M + BM - 1) / BM), (unsigned)((p.N + 31) / 32), (unsigned)p.splits);
+    hipLaunchKernelGGL((gemm_kernel<T, AKC, BKC, 128, 32, 4, 1>), grid, block, 0, s, p);
+  } else if (p.N <= 64) {
+    dim3 grid((unsigned)((p.M + BM - 1) / BM), (unsigned)((p.N + 63) / 64), (unsigned)p.splits);
+    hipLaunchKernelGGL((gemm_kernel<T, AKC, BKC, 128, 64, 4, 1>), grid, block, 0, s, p);
+  } else {
+    dim3 grid((unsigned)((p.M + BM - 1) / BM), (unsigned)((p.N + 127) / 128), (unsigned)p.splits);
+    hipLaunchKernelGGL((gemm_kernel<T, AKC, BKC, 128, 128, 2, 2>), grid, block, 0, s, p);
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_typed(const GemmCall& c, const GemmParams& p, hipStream_t s) {
+  if (c.a_kc && !c.b_kc) return launch_layout<T, true, false>(p, s);
+  if (c.a_kc && c.b_kc) return launch_layout<T, true, true>(p, s);
+  if (!c.a_kc && !c.b_kc) return launch_layout<T, false, false>(p, s);
+  return hipErrorInvalidValue;
+}
+
+// ------------------------------------------------------------ reductions ----
+
+template <typename T>
+__global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __restrict__ part, int splits,
+                                                              int64_t M, int64_t N, int64_t width, Epilogue ep) {
+  const int64_t total = M * width;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = idx / width, c = idx % width;
+    if (c >= N) {   // EPI_F32 padding columns
+      reinterpret_cast<float*>(ep.out)[r * ep.ldo + c] = 0.f;
+      continue;
+    }
+    float a = 0.f;
+    const float* q = part + r * N + c;
+    for (int sidx = 0; sidx < splits; ++sidx) a += q[(int64_t)sidx * M * N];
+    epi_store1<T>(ep, r, c, a);
+  }
+}
+
+// Column sums over a block of rows; threads of one column group walk rows in
+// a fixed order, then the row groups are combined in a fixed order.
+constexpr int64_t COLSUM_ROWS = 2048;
+
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ X, int64_t rows, int64_t cols,
+                                                             int64_t ld, int64_t ldp, float* __restrict__ part) {
+  __shared__ float red[256];
+  const int64_t c = (int64_t)blockIdx.y * 64 + (threadIdx.x & 63);
+  const int rg = threadIdx.x >> 6;   // 4 row groups
+  const int64_t r0 = (int64_t)blockIdx.x * COLSUM_ROWS;
+  const int64_t r1 = min(rows, r0 + COLSUM_ROWS);
+  float a = 0.f;
+  if (c < cols)
+    for (int64_t r = r0 + rg; r < r1; r += 4) a += to_f32<T>(X[r * ld + c]);
+  red[threadIdx.x] = a;
+  __syncthreads();
+  if (rg == 0 && c < ldp) {
+    float s = red[threadIdx.x] + red[threadIdx.x + 64];
+    s += red[threadIdx.x + 128];
+    s += red[threadIdx.x + 192];
+    part[(int64_t)blockIdx.x * ldp + c] = c < cols ? s : 0.f;
+  }
+}
+
+}  // namespace
+
+int gemm_choose_splits(int prec, int64_t M, int64_t N, int64_t K) {
+  const int64_t BK = prec == 0 ? 32 : 64;
+  const int64_t BN = N <= 16 ? 16 : N <= 32 ? 32 : N <= 64 ? 64 : 128;
+  const int64_t tiles = ((M + 127) / 128) * ((N + BN - 1) / BN);
+  const int64_t ktiles = (K + BK - 1) / BK;
+  const int64_t target = 512;
+  if (tiles >= target / 2 || ktiles < 8) return 1;
+  int64_t splits = (target + tiles - 1) / tiles;
+  splits = std::min(splits, ktiles / 4);
+  return (int)std::max<int64_t>(splits, 1);
+}
+
+hipError_t gemm_launch(const GemmCall& c, hipStream_t s) {
+  GemmParams p;
+  p.A = c.A; p.lda = c.lda; p.B = c.B; p.ldb = c.ldb;
+  p.M = c.M; p.N = c.N; p.K = c.K;
+  p.splits = c.splits < 1 ? 1 : c.splits;
+  p.partials = c.partials;
+  p.epi = c.epi;
+  const int64_t BK = c.prec == 0 ? 32 : 64;
+  const int64_t ktiles = (c.K + BK - 1) / BK;
+  p.k_per_split = ((ktiles + p.splits - 1) / p.splits) * BK;
+  if (p.k_per_split <= 0) p.k_per_split = BK;
+  switch (c.prec) {
+    case 0: return launch_typed<float>(c, p, s);
+    case 1: return launch_typed<f16>(c, p, s);
+    case 2: return launch_typed<bf16>(c, p, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t M, int64_t N,
+                           const Epilogue& epi, hipStream_t s) {
+  const int64_t width = epi.mode == EPI_F32 ? epi.ldo : N;
+  const int64_t total = M * width;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  if (blocks <= 0) return hipSuccess;
+  switch (prec) {
+    case 0: hipLaunchKernelGGL(reduce_partials_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, s, partials, splits, M, N, width, epi); break;
+    case 1: hipLaunchKernelGGL(reduce_partials_kernel<f16>, dim3((unsigned)blocks), dim3(256), 0, s, partials, splits, M, N, width, epi); break;
+    case 2: hipLaunchKernelGGL(reduce_partials_kernel<bf16>, dim3((unsigned)blocks), dim3(256), 0, s, partials, splits, M, N, width, epi); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+int64_t colsum_partials_floats(int64_t rows, int64_t ld) {
+  return ((rows + COLSUM_ROWS - 1) / COLSUM_ROWS) * ld;
+}
+
+hipError_t colsum(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld,
+                  float* partials, float* out, int64_t ldo, int32_t* flag, hipStream_t s) {
+  const int64_t nb = (rows + COLSUM_ROWS - 1) / COLSUM_ROWS;
+  dim3 grid((unsigned)nb, (unsigned)((ldo + 63) / 64));
+  switch (prec) {
+    case 0: hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, rows, cols, ld, ldo, partials); break;
+    case 1: hipLaunchKernelGGL(colsum_partial_kernel<f16>, grid, dim3(256), 0, s, (const f16*)X, rows, cols, ld, ldo, partials); break;
+    case 2: hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, rows, cols, ld, ldo, partials); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // out[c] = sum over blocks b of partials[b][c] (fixed order), 1 x ldo
+  Epilogue ep{};
+  ep.out = out; ep.ldo = ldo; ep.rows = 1; ep.cols = ldo; ep.mode = EPI_F32; ep.flag = flag;
+  return reduce_partials(prec, partials, (int)nb, 1, ldo, ep, s);
+}
+
+}  // namespace gcn

@@ -1,0 +1,96 @@
+// Host-side launch functions of the libgcn kernels (internal; not exported).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace gcn {
+
+// ----------------------------------------------------------------- GEMM ----
+// C[M x N] = sum_k A(m, k) * B(k, n) with fp32 accumulation on MFMA.
+// A(m, k) = a_kc ? A[m * lda + k] : A[k * lda + m]
+// B(k, n) = b_kc ? B[n * ldb + k] : B[k * ldb + n]
+// With splits > 1 the K range is cut into `splits` pieces (multiples of the
+// K tile) whose fp32 partial sums go to `partials` [splits][M][N]; the
+// caller then runs reduce_partials.  With splits == 1 the epilogue is
+// applied directly.
+struct GemmCall {
+  int prec;              // gcn_precision
+  bool a_kc, b_kc;
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  int64_t M, N, K;
+  int splits;
+  float* partials;
+  Epilogue epi;
+};
+// Number of K splits the GEMM would use for these sizes (1 = none).
+int gemm_choose_splits(int prec, int64_t M, int64_t N, int64_t K);
+hipError_t gemm_launch(const GemmCall& c, hipStream_t s);
+
+// out = epilogue(sum over s < splits of partials[s][r][c]) for r < M, c < N;
+// for EPI_F32 columns [N, ldo) are written 0.
+hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t M, int64_t N,
+                           const Epilogue& epi, hipStream_t s);
+
+// Column sums of X (rows x cols, ld) in fixed order -> out (fp32 [ldo],
+// zero beyond cols).  partials needs colsum_partials_floats() floats.
+int64_t colsum_partials_floats(int64_t rows, int64_t ld);
+hipError_t colsum(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld,
+                  float* partials, float* out, int64_t ldo, int32_t* flag, hipStream_t s);
+
+// ----------------------------------------------------------------- SpMM ----
+struct CsrView {
+  int64_t n, nnz;
+  bool idx64;
+  const void* rowptr;
+  const int32_t* colidx;
+  const void* values;    // storage type == prec, or NULL (dinv product)
+  const float* dinv;
+  int64_t heavy_threshold, chunk_nnz, n_heavy, n_chunks;
+  const int32_t* heavy_rows;
+  const int32_t* heavy_chunk_off;
+  const int32_t* chunk_heavy;
+};
+// Y = A_hat X (+ epilogue) for X: n x F (ld), Y described by epi.
+int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F);
+hipError_t spmm_launch(const CsrView& A, int prec, const void* X, int64_t ldx, int64_t F,
+                       const Epilogue& epi, float* partials, hipStream_t s);
+
+// ------------------------------------------------------------ normalize ----
+size_t normalize_workspace_bytes(int64_t n, int64_t num_edges);
+hipError_t normalize_run(int64_t n, int64_t num_edges, const int32_t* src, const int32_t* dst,
+                         bool idx64, void* rowptr, int32_t* colidx, int32_t* deg, float* dinv,
+                         int value_prec, void* values, void* dense, int64_t ld_dense,
+                         int64_t* nnz_out, int32_t* bad_ids, void* ws, size_t ws_bytes,
+                         hipStream_t s);
+size_t schedule_bytes(int64_t n, int64_t nnz, int64_t chunk_nnz);
+hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr,
+                        int64_t threshold, int64_t chunk_nnz, void* sched, size_t sched_bytes,
+                        int32_t** heavy_rows, int32_t** heavy_chunk_off, int32_t** chunk_heavy,
+                        int64_t* n_heavy, int64_t* n_chunks, hipStream_t s);
+
+// ----------------------------------------------------------------- loss ----
+size_t loss_workspace_bytes(int64_t n, int64_t C);
+hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* logits,
+                       const int32_t* labels, const uint8_t* mask, int64_t n_mask,
+                       const float* loss_scale, float* loss, void* dlogits, int32_t* n_correct,
+                       int32_t* flag, void* ws, hipStream_t s);
+
+// ------------------------------------------------------------ optimiser ----
+struct AdamHyper {
+  float lr, beta1, beta2, eps, backoff, growth, min_scale, max_scale;
+  int32_t interval;
+};
+struct ScalerState { float scale; int32_t good_steps; int32_t step; int32_t skipped; };
+hipError_t optimizer_launch(int64_t count, float* master, const float* grad, float* m, float* v,
+                            void* working, int prec, const AdamHyper& hp, ScalerState* state,
+                            int32_t* flag, hipStream_t s);
+
+// --------------------------------------------------------------- helpers ----
+hipError_t fill_zero(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace gcn

@@ -1,0 +1,479 @@
+// A_hat = D^-1/2 (A + I) D^-1/2 from an undirected edge list, as canonical
+// CSR (rows ascending, columns ascending and unique), plus the heavy-row
+// schedule used by the sparse aggregation.
+//
+// Steps (all integer work is order-independent, so the CSR is bit-identical
+// from run to run even though the scatter uses atomics):
+//   count    per-row counts of both directions of every u != v pair
+//   scan     segment offsets (count + 1 slot for the self-loop)
+//   scatter  neighbour ids into per-row segments (+ the self-loop)
+//   sort     each segment: wave bitonic (<= 64), LDS bitonic (<= 4096),
+//            global-memory bitonic (larger hubs)
+//   unique   per-row count of distinct neighbours -> degree
+//   scan     row pointers; compact; dinv = fp32(1 / sqrt(fp64(deg)))
+//   values   dinv[row] * dinv[col] in the value precision; optional dense
+#include "internal.h"
+
+#include <vector>
+
+namespace gcn {
+
+namespace {
+
+constexpr int SCAN_BLOCK = 1024;   // elements per scan block (256 threads x 4)
+constexpr int64_t SORT_LDS_MAX = 4096;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int64_t scan_scratch_elems(int64_t count) {
+  int64_t total = 0;
+  while (count > SCAN_BLOCK) {
+    count = (count + SCAN_BLOCK - 1) / SCAN_BLOCK;
+    total += count;
+  }
+  return total + 1;
+}
+
+// ------------------------------------------------------------------ scan ----
+__global__ __launch_bounds__(256) void scan_block_kernel(int64_t* __restrict__ data, int64_t count,
+                                                         int64_t* __restrict__ block_sums) {
+  __shared__ int64_t s[256];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_BLOCK + threadIdx.x * 4;
+  int64_t v[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = base + i < count ? data[base + i] : 0;
+  const int64_t tsum = v[0] + v[1] + v[2] + v[3];
+  s[threadIdx.x] = tsum;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int64_t add = threadIdx.x >= off ? s[threadIdx.x - off] : 0;
+    __syncthreads();
+    s[threadIdx.x] += add;
+    __syncthreads();
+  }
+  int64_t run = s[threadIdx.x] - tsum;   // exclusive prefix of this thread
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (base + i < count) data[base + i] = run;
+    run += v[i];
+  }
+  if (threadIdx.x == 255 && block_sums) block_sums[blockIdx.x] = s[255];
+}
+
+__global__ __launch_bounds__(256) void scan_add_kernel(int64_t* __restrict__ data, int64_t count,
+                                                       const int64_t* __restrict__ block_off) {
+  const int64_t base = (int64_t)blockIdx.x * SCAN_BLOCK + threadIdx.x * 4;
+  const int64_t add = block_off[blockIdx.x];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (base + i < count) data[base + i] += add;
+}
+
+// In-place exclusive scan of data[0..count); scratch holds scan_scratch_elems(count).
+hipError_t scan_exclusive(int64_t* data, int64_t count, int64_t* scratch, hipStream_t s) {
+  const int64_t nb = (count + SCAN_BLOCK - 1) / SCAN_BLOCK;
+  hipLaunchKernelGGL(scan_block_kernel, dim3((unsigned)nb), dim3(256), 0, s, data, count, nb > 1 ? scratch : nullptr);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || nb <= 1) return e;
+  e = scan_exclusive(scratch, nb, scratch + nb, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(scan_add_kernel, dim3((unsigned)nb), dim3(256), 0, s, data, count, scratch);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- helpers ----
+__global__ void fill_zero_kernel(uint32_t* p, int64_t words) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+unsigned grid_for(int64_t items, int per_block = 256, int64_t cap = 65536) {
+  int64_t g = (items + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return (unsigned)g;
+}
+
+// ---------------------------------------------------------------- kernels ----
+__global__ void count_kernel(int64_t n, int64_t E, const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                             int32_t* __restrict__ cnt, int32_t* __restrict__ bad) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < E; k += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t u = src[k], v = dst[k];
+    if (u < 0 || v < 0 || u >= n || v >= n) { *reinterpret_cast<volatile int32_t*>(bad) = 1; continue; }
+    if (u == v) continue;
+    atomicAdd(&cnt[u], 1);
+    atomicAdd(&cnt[v], 1);
+  }
+}
+
+// seg[r] = cnt[r] + 1 (self-loop slot), seg[n] = 0
+__global__ void seglen_kernel(int64_t n, const int32_t* __restrict__ cnt, int64_t* __restrict__ seg) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r <= n; r += (int64_t)gridDim.x * blockDim.x)
+    seg[r] = r < n ? (int64_t)cnt[r] + 1 : 0;
+}
+
+// out[r] = in[r], out[n] = 0
+__global__ void widen_kernel(int64_t n, const int32_t* __restrict__ in, int64_t* __restrict__ out) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r <= n; r += (int64_t)gridDim.x * blockDim.x)
+    out[r] = r < n ? (int64_t)in[r] : 0;
+}
+
+__global__ void scatter_kernel(int64_t n, int64_t E, const int32_t* __restrict__ src, const int32_t* __restrict__ dst,
+                               const int64_t* __restrict__ off, int32_t* __restrict__ cur, int32_t* __restrict__ tmp) {
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < E; k += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t u = src[k], v = dst[k];
+    if (u < 0 || v < 0 || u >= n || v >= n || u == v) continue;
+    const int32_t pu = atomicAdd(&cur[u], 1);
+    tmp[off[u] + pu] = v;
+    const int32_t pv = atomicAdd(&cur[v], 1);
+    tmp[off[v] + pv] = u;
+  }
+}
+
+__global__ void selfloop_kernel(int64_t n, const int64_t* __restrict__ off, const int32_t* __restrict__ cnt,
+                                int32_t* __restrict__ tmp) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x)
+    tmp[off[r] + cnt[r]] = (int32_t)r;
+}
+
+// Segments of at most 64 entries: one wave, register bitonic sort.
+__global__ __launch_bounds__(256) void sort_small_kernel(int64_t n, const int64_t* __restrict__ off,
+                                                         int32_t* __restrict__ tmp, int32_t* __restrict__ ucnt) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= n) return;
+  const int64_t b = off[r], len = off[r + 1] - b;
+  if (len > 64) return;
+  int x = lane < len ? tmp[b + lane] : INT32_MAX;
+  for (int k = 2; k <= 64; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const int y = __shfl_xor(x, j);
+      const bool asc = (lane & k) == 0;
+      const bool lower = (lane & j) == 0;
+      x = (lower == asc) ? min(x, y) : max(x, y);
+    }
+  }
+  const int prev = __shfl(x, lane == 0 ? 0 : lane - 1);
+  const bool flag = lane < len && (lane == 0 || x != prev);
+  const uint64_t bal = __ballot(flag);
+  if (lane < len) tmp[b + lane] = x;
+  if (lane == 0) ucnt[r] = __popcll(bal);
+}
+
+__device__ int block_sum_int(int v, int* red) {
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (threadIdx.x < s) red[threadIdx.x] += red[threadIdx.x + s];
+    __syncthreads();
+  }
+  const int out = red[0];
+  __syncthreads();
+  return out;
+}
+
+// Segments of 65..4096 entries: one workgroup, bitonic sort in LDS.
+__global__ __launch_bounds__(256) void sort_medium_kernel(int64_t n, const int64_t* __restrict__ off,
+                                                          int32_t* __restrict__ tmp, int32_t* __restrict__ ucnt) {
+  __shared__ int s[SORT_LDS_MAX];
+  __shared__ int red[256];
+  for (int64_t r = blockIdx.x; r < n; r += gridDim.x) {
+    const int64_t b = off[r], len = off[r + 1] - b;
+    if (len <= 64 || len > SORT_LDS_MAX) continue;
+    int P = 128;
+    while (P < len) P <<= 1;
+    for (int i = threadIdx.x; i < P; i += 256) s[i] = i < len ? tmp[b + i] : INT32_MAX;
+    __syncthreads();
+    for (int k = 2; k <= P; k <<= 1) {
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        for (int i = threadIdx.x; i < P; i += 256) {
+          const int ixj = i ^ j;
+          if (ixj > i) {
+            const int a = s[i], c = s[ixj];
+            const bool asc = (i & k) == 0;
+            if ((a > c) == asc) { s[i] = c; s[ixj] = a; }
+          }
+        }
+        __syncthreads();
+      }
+    }
+    int cntu = 0;
+    for (int i = threadIdx.x; i < len; i += 256) {
+      tmp[b + i] = s[i];
+      cntu += (i == 0 || s[i] != s[i - 1]) ? 1 : 0;
+    }
+    const int tot = block_sum_int(cntu, red);
+    if (threadIdx.x == 0) ucnt[r] = tot;
+    __syncthreads();
+  }
+}
+
+// Segments above 4096 entries: one workgroup, bitonic network in global
+// memory in its "always ascending" form (the first step of each merge
+// compares i with its mirror in the block), so positions >= len act as +inf
+// and are never touched.
+__global__ __launch_bounds__(256) void sort_large_kernel(int64_t n, const int64_t* __restrict__ off,
+                                                         int32_t* __restrict__ tmp, int32_t* __restrict__ ucnt) {
+  __shared__ int red[256];
+  for (int64_t r = blockIdx.x; r < n; r += gridDim.x) {
+    const int64_t b = off[r], len = off[r + 1] - b;
+    if (len <= SORT_LDS_MAX) continue;
+    int32_t* a = tmp + b;
+    int64_t P = 1;
+    while (P < len) P <<= 1;
+    for (int64_t k = 2; k <= P; k <<= 1) {
+      // mirror step
+      for (int64_t t = threadIdx.x; t < P / 2; t += 256) {
+        const int64_t blk = t / (k / 2), w = t % (k / 2);
+        const int64_t i = blk * k + w, p = blk * k + (k - 1 - w);
+        if (p < len) {
+          const int32_t x = a[i], y = a[p];
+          if (x > y) { a[i] = y; a[p] = x; }
+        }
+      }
+      __syncthreads();
+      for (int64_t j = k / 4; j > 0; j >>= 1) {
+        for (int64_t t = threadIdx.x; t < P / 2; t += 256) {
+          const int64_t blk = t / j, w = t % j;
+          const int64_t i = blk * 2 * j + w, p = i + j;
+          if (p < len) {
+            const int32_t x = a[i], y = a[p];
+            if (x > y) { a[i] = y; a[p] = x; }
+          }
+        }
+        __syncthreads();
+      }
+    }
+    int cntu = 0;
+    for (int64_t i = threadIdx.x; i < len; i += 256) cntu += (i == 0 || a[i] != a[i - 1]) ? 1 : 0;
+    const int tot = block_sum_int(cntu, red);
+    if (threadIdx.x == 0) ucnt[r] = tot;
+    __syncthreads();
+  }
+}
+
+// Compact sorted segments to unique columns; write rowptr, deg, dinv.
+template <typename IdxT>
+__global__ __launch_bounds__(256) void compact_kernel(int64_t n, const int64_t* __restrict__ off,
+                                                      const int32_t* __restrict__ tmp, const int64_t* __restrict__ rp64,
+                                                      const int32_t* __restrict__ ucnt, IdxT* __restrict__ rowptr,
+                                                      int32_t* __restrict__ colidx, int32_t* __restrict__ deg,
+                                                      float* __restrict__ dinv) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r > n) return;
+  if (r == n) {
+    if (lane == 0) rowptr[n] = (IdxT)rp64[n];
+    return;
+  }
+  const int64_t b = off[r], len = off[r + 1] - b;
+  const int64_t o = rp64[r];
+  int64_t run = 0;
+  for (int64_t base = 0; base < len; base += 64) {
+    const int64_t i = base + lane;
+    const int x = i < len ? tmp[b + i] : 0;
+    const bool flag = i < len && (i == 0 || x != tmp[b + i - 1]);
+    const uint64_t bal = __ballot(flag);
+    const int pre = __popcll(bal & __lanemask_lt());
+    if (flag) colidx[o + run + pre] = x;
+    run += __popcll(bal);
+  }
+  if (lane == 0) {
+    rowptr[r] = (IdxT)o;
+    const int32_t d = ucnt[r];
+    if (deg) deg[r] = d;
+    dinv[r] = (float)(1.0 / sqrt((double)d));
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void values_kernel(int64_t n, const int64_t* __restrict__ rp64,
+                                                     const int32_t* __restrict__ colidx, const float* __restrict__ dinv,
+                                                     T* __restrict__ values, T* __restrict__ dense, int64_t ld_dense) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= n) return;
+  const float dr = dinv[r];
+  for (int64_t k = rp64[r] + lane; k < rp64[r + 1]; k += 64) {
+    const int32_t c = colidx[k];
+    const T v = from_f32<T>(dr * dinv[c]);
+    if (values) values[k] = v;
+    if (dense) dense[r * ld_dense + c] = v;
+  }
+}
+
+// ---------------------------------------------------------------- schedule ----
+template <typename IdxT>
+__global__ void heavy_flag_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr, int64_t chunk,
+                                  int64_t* __restrict__ flag, int64_t* __restrict__ nch) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r <= n; r += (int64_t)gridDim.x * blockDim.x) {
+    if (r == n) { flag[n] = 0; nch[n] = 0; continue; }
+    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
+    const bool h = d > thr;
+    flag[r] = h ? 1 : 0;
+    nch[r] = h ? (d + chunk - 1) / chunk : 0;
+  }
+}
+
+template <typename IdxT>
+__global__ void heavy_fill_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
+                                  const int64_t* __restrict__ hidx, const int64_t* __restrict__ choff,
+                                  int32_t* __restrict__ heavy_rows, int32_t* __restrict__ heavy_chunk_off,
+                                  int32_t* __restrict__ chunk_heavy) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r <= n; r += (int64_t)gridDim.x * blockDim.x) {
+    if (r == n) { heavy_chunk_off[hidx[n]] = (int32_t)choff[n]; continue; }
+    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
+    if (d <= thr) continue;
+    const int64_t h = hidx[r];
+    heavy_rows[h] = (int32_t)r;
+    heavy_chunk_off[h] = (int32_t)choff[r];
+    for (int64_t c = choff[r]; c < choff[r + 1]; ++c) chunk_heavy[c] = (int32_t)h;
+  }
+}
+
+}  // namespace
+
+hipError_t fill_zero(void* p, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  // callers pass 4-byte multiples
+  const int64_t words = (int64_t)(bytes / 4);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(words, 256, 16384)), dim3(256), 0, s, (uint32_t*)p, words);
+  return hipGetLastError();
+}
+
+size_t normalize_workspace_bytes(int64_t n, int64_t E) {
+  size_t b = 0;
+  b += align256(sizeof(int32_t) * n);                         // cnt / ucnt
+  b += align256(sizeof(int32_t) * n);                         // cur
+  b += align256(sizeof(int64_t) * (n + 1));                   // off
+  b += align256(sizeof(int64_t) * (n + 1));                   // rp64
+  b += align256(sizeof(int32_t) * (2 * E + n));               // tmp
+  b += align256(sizeof(int64_t) * scan_scratch_elems(n + 1)); // scan scratch
+  b += align256(sizeof(int64_t) * 4);                         // misc
+  return b;
+}
+
+hipError_t normalize_run(int64_t n, int64_t E, const int32_t* src, const int32_t* dst, bool idx64,
+                         void* rowptr, int32_t* colidx, int32_t* deg, float* dinv, int value_prec,
+                         void* values, void* dense, int64_t ld_dense, int64_t* nnz_out, int32_t* bad_ids,
+                         void* ws, size_t ws_bytes, hipStream_t s) {
+  char* w = static_cast<char*>(ws);
+  auto take = [&](size_t bytes) { char* p = w; w += align256(bytes); return p; };
+  int32_t* cnt = (int32_t*)take(sizeof(int32_t) * n);
+  int32_t* cur = (int32_t*)take(sizeof(int32_t) * n);
+  int64_t* off = (int64_t*)take(sizeof(int64_t) * (n + 1));
+  int64_t* rp64 = (int64_t*)take(sizeof(int64_t) * (n + 1));
+  int32_t* tmp = (int32_t*)take(sizeof(int32_t) * (2 * E + n));
+  int64_t* scr = (int64_t*)take(sizeof(int64_t) * scan_scratch_elems(n + 1));
+  int64_t* misc = (int64_t*)take(sizeof(int64_t) * 4);
+  if ((size_t)(w - static_cast<char*>(ws)) > ws_bytes) return hipErrorInvalidValue;
+
+  hipError_t e;
+#define GCN_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
+  GCN_TRY(fill_zero(cnt, sizeof(int32_t) * n, s));
+  GCN_TRY(fill_zero(cur, sizeof(int32_t) * n, s));
+  GCN_TRY(fill_zero(misc, sizeof(int64_t) * 4, s));
+  int32_t* bad = reinterpret_cast<int32_t*>(misc + 1);
+  if (E > 0) {
+    hipLaunchKernelGGL(count_kernel, dim3(grid_for(E)), dim3(256), 0, s, n, E, src, dst, cnt, bad);
+    GCN_TRY(hipGetLastError());
+  }
+  hipLaunchKernelGGL(seglen_kernel, dim3(grid_for(n + 1)), dim3(256), 0, s, n, cnt, off);
+  GCN_TRY(hipGetLastError());
+  GCN_TRY(scan_exclusive(off, n + 1, scr, s));
+  if (E > 0) {
+    hipLaunchKernelGGL(scatter_kernel, dim3(grid_for(E)), dim3(256), 0, s, n, E, src, dst, off, cur, tmp);
+    GCN_TRY(hipGetLastError());
+  }
+  hipLaunchKernelGGL(selfloop_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, off, cnt, tmp);
+  GCN_TRY(hipGetLastError());
+  int32_t* ucnt = cnt;   // counts are no longer needed after the self-loop slots are placed
+  hipLaunchKernelGGL(sort_small_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, n, off, tmp, ucnt);
+  GCN_TRY(hipGetLastError());
+  hipLaunchKernelGGL(sort_medium_kernel, dim3(grid_for(n, 1, 4096)), dim3(256), 0, s, n, off, tmp, ucnt);
+  GCN_TRY(hipGetLastError());
+  hipLaunchKernelGGL(sort_large_kernel, dim3(grid_for(n, 1, 1024)), dim3(256), 0, s, n, off, tmp, ucnt);
+  GCN_TRY(hipGetLastError());
+  hipLaunchKernelGGL(widen_kernel, dim3(grid_for(n + 1)), dim3(256), 0, s, n, ucnt, rp64);
+  GCN_TRY(hipGetLastError());
+  GCN_TRY(scan_exclusive(rp64, n + 1, scr, s));
+  if (idx64)
+    hipLaunchKernelGGL(compact_kernel<int64_t>, dim3((unsigned)((n + 1 + 3) / 4)), dim3(256), 0, s, n, off, tmp, rp64,
+                       ucnt, (int64_t*)rowptr, colidx, deg, dinv);
+  else
+    hipLaunchKernelGGL(compact_kernel<int32_t>, dim3((unsigned)((n + 1 + 3) / 4)), dim3(256), 0, s, n, off, tmp, rp64,
+                       ucnt, (int32_t*)rowptr, colidx, deg, dinv);
+  GCN_TRY(hipGetLastError());
+  if (dense) GCN_TRY(fill_zero(dense, (size_t)n * (size_t)ld_dense * (value_prec == 0 ? 4 : 2), s));
+  if (values || dense) {
+    const dim3 g((unsigned)((n + 3) / 4));
+    switch (value_prec) {
+      case 0: hipLaunchKernelGGL(values_kernel<float>, g, dim3(256), 0, s, n, rp64, colidx, dinv, (float*)values, (float*)dense, ld_dense); break;
+      case 1: hipLaunchKernelGGL(values_kernel<f16>, g, dim3(256), 0, s, n, rp64, colidx, dinv, (f16*)values, (f16*)dense, ld_dense); break;
+      case 2: hipLaunchKernelGGL(values_kernel<bf16>, g, dim3(256), 0, s, n, rp64, colidx, dinv, (bf16*)values, (bf16*)dense, ld_dense); break;
+      default: return hipErrorInvalidValue;
+    }
+    GCN_TRY(hipGetLastError());
+  }
+  // the one synchronisation: nnz and the bad-id flag back to the host
+  int64_t host[2] = {0, 0};
+  GCN_TRY(hipMemcpyAsync(&host[0], rp64 + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  int32_t hbad = 0;
+  GCN_TRY(hipMemcpyAsync(&hbad, bad, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  GCN_TRY(hipStreamSynchronize(s));
+  *nnz_out = host[0];
+  *bad_ids = hbad;
+#undef GCN_TRY
+  return hipSuccess;
+}
+
+size_t schedule_bytes(int64_t n, int64_t nnz, int64_t chunk_nnz) {
+  const int64_t max_chunks = nnz / chunk_nnz + n + 1;
+  size_t b = 0;
+  b += align256(sizeof(int32_t) * n);                          // heavy_rows
+  b += align256(sizeof(int32_t) * (n + 1));                    // heavy_chunk_off
+  b += align256(sizeof(int32_t) * max_chunks);                 // chunk_heavy
+  b += align256(sizeof(int64_t) * (n + 1));                    // flags -> heavy index
+  b += align256(sizeof(int64_t) * (n + 1));                    // chunks per row -> chunk offsets
+  b += align256(sizeof(int64_t) * scan_scratch_elems(n + 1));  // scan scratch
+  return b;
+}
+
+hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, int64_t thr, int64_t chunk,
+                        void* sched, size_t sched_bytes, int32_t** heavy_rows, int32_t** heavy_chunk_off,
+                        int32_t** chunk_heavy, int64_t* n_heavy, int64_t* n_chunks, hipStream_t s) {
+  char* w = static_cast<char*>(sched);
+  auto take = [&](size_t bytes) { char* p = w; w += align256(bytes); return p; };
+  const int64_t max_chunks = nnz / chunk + n + 1;
+  int32_t* hr = (int32_t*)take(sizeof(int32_t) * n);
+  int32_t* hco = (int32_t*)take(sizeof(int32_t) * (n + 1));
+  int32_t* ch = (int32_t*)take(sizeof(int32_t) * max_chunks);
+  int64_t* hidx = (int64_t*)take(sizeof(int64_t) * (n + 1));
+  int64_t* choff = (int64_t*)take(sizeof(int64_t) * (n + 1));
+  int64_t* scr = (int64_t*)take(sizeof(int64_t) * scan_scratch_elems(n + 1));
+  if ((size_t)(w - static_cast<char*>(sched)) > sched_bytes) return hipErrorInvalidValue;
+  hipError_t e;
+#define GCN_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
+  if (idx64)
+    hipLaunchKernelGGL(heavy_flag_kernel<int64_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, chunk, hidx, choff);
+  else
+    hipLaunchKernelGGL(heavy_flag_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, chunk, hidx, choff);
+  GCN_TRY(hipGetLastError());
+  GCN_TRY(scan_exclusive(hidx, n + 1, scr, s));
+  GCN_TRY(scan_exclusive(choff, n + 1, scr, s));
+  if (idx64)
+    hipLaunchKernelGGL(heavy_fill_kernel<int64_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, hidx, choff, hr, hco, ch);
+  else
+    hipLaunchKernelGGL(heavy_fill_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, hidx, choff, hr, hco, ch);
+  GCN_TRY(hipGetLastError());
+  int64_t host[2] = {0, 0};
+  GCN_TRY(hipMemcpyAsync(&host[0], hidx + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  GCN_TRY(hipMemcpyAsync(&host[1], choff + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  GCN_TRY(hipStreamSynchronize(s));
+#undef GCN_TRY
+  *heavy_rows = hr; *heavy_chunk_off = hco; *chunk_heavy = ch;
+  *n_heavy = host[0]; *n_chunks = host[1];
+  return hipSuccess;
+}
+
+}  // namespace gcn

@@ -1,0 +1,263 @@
+// Neighbourhood aggregation Y = A_hat X for A_hat in CSR (the sparse
+// product the paper could not run in half precision, Section "Reduced
+// Precision Changes"), with the layer epilogue fused into the store.
+//
+// Work mapping (wave64):
+//  * Light rows (<= heavy_threshold entries): a group of LPR lanes owns one
+//    row; lane li of the group owns the 16-byte column slice li of the
+//    feature row (8 x 16-bit or 4 x fp32), so one neighbour row of X is a
+//    single coalesced LPR * 16-byte read.  Neighbours are walked 4 at a
+//    time to keep several gathers in flight.  fp32 accumulation.
+//  * Heavy rows (power-law hubs): split into chunks of chunk_nnz entries;
+//    one workgroup per chunk reduces its entries across 256/LPR lane groups
+//    through LDS in a fixed order into an fp32 partial row; a fixup kernel
+//    sums the partials of each heavy row in chunk order and applies the
+//    epilogue.  No atomics: results are run-to-run identical.
+#include "internal.h"
+
+namespace gcn {
+
+namespace {
+
+template <typename IdxT>
+struct SpmmParams {
+  int64_t n;
+  const IdxT* rowptr;
+  const int32_t* colidx;
+  const void* values;
+  const float* dinv;
+  int64_t heavy_threshold;      // 0: no heavy split
+  const void* X;
+  int64_t ldx;
+  int64_t F;
+  Epilogue epi;
+};
+
+template <typename T, bool HAS_VAL>
+__device__ __forceinline__ float edge_value(const void* values, const float* dinv, float drow, int64_t e, int32_t c) {
+  if (HAS_VAL) return to_f32<T>(reinterpret_cast<const T*>(values)[e]);
+  return drow * dinv[c];
+}
+
+template <typename T>
+__device__ __forceinline__ void fma_vec(float* acc, float v, uint4 raw) {
+  float x[Vec<T>::N];
+  unpack<T>(raw, x);
+#pragma unroll
+  for (int i = 0; i < Vec<T>::N; ++i) acc[i] = fmaf(v, x[i], acc[i]);
+}
+
+template <typename T, typename IdxT, int LPR, bool HAS_VAL>
+__global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
+  constexpr int VE = Vec<T>::N;
+  constexpr int G = 64 / LPR;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane / LPR, li = lane % LPR;
+  const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * G + g;
+  const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
+  if (row >= p.n || col0 >= p.F) return;
+  const int64_t beg = (int64_t)p.rowptr[row], end = (int64_t)p.rowptr[row + 1];
+  if (p.heavy_threshold > 0 && end - beg > p.heavy_threshold) return;
+  const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
+  const float drow = HAS_VAL ? 0.f : p.dinv[row];
+  float acc[VE];
+#pragma unroll
+  for (int i = 0; i < VE; ++i) acc[i] = 0.f;
+  int64_t e = beg;
+  for (; e + 4 <= end; e += 4) {
+    const int32_t c0 = p.colidx[e], c1 = p.colidx[e + 1], c2 = p.colidx[e + 2], c3 = p.colidx[e + 3];
+    const uint4 x0 = ldg16(X + (int64_t)c0 * p.ldx);
+    const uint4 x1 = ldg16(X + (int64_t)c1 * p.ldx);
+    const uint4 x2 = ldg16(X + (int64_t)c2 * p.ldx);
+    const uint4 x3 = ldg16(X + (int64_t)c3 * p.ldx);
+    const float v0 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c0);
+    const float v1 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 1, c1);
+    const float v2 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 2, c2);
+    const float v3 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 3, c3);
+    fma_vec<T>(acc, v0, x0);
+    fma_vec<T>(acc, v1, x1);
+    fma_vec<T>(acc, v2, x2);
+    fma_vec<T>(acc, v3, x3);
+  }
+  for (; e < end; ++e) {
+    const int32_t c = p.colidx[e];
+    fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c), ldg16(X + (int64_t)c * p.ldx));
+  }
+  epi_store_vec<T>(p.epi, row, col0, acc);
+}
+
+template <typename IdxT>
+struct HeavyParams {
+  const IdxT* rowptr;
+  const int32_t* colidx;
+  const void* values;
+  const float* dinv;
+  const int32_t* heavy_rows;
+  const int32_t* heavy_chunk_off;
+  const int32_t* chunk_heavy;
+  int64_t chunk_nnz;
+  int64_t n_chunks;
+  const void* X;
+  int64_t ldx;
+  int64_t F;
+  int64_t ldp;                  // floats per partial row
+  float* partials;              // [n_chunks][ldp]
+  Epilogue epi;
+};
+
+// One workgroup per (chunk, column block).
+template <typename T, typename IdxT, int LPR, bool HAS_VAL>
+__global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT> p) {
+  constexpr int VE = Vec<T>::N;
+  constexpr int NG = 256 / LPR;
+  __shared__ float red[256 * VE];
+  const int64_t chunk = blockIdx.x;
+  const int g = threadIdx.x / LPR, li = threadIdx.x % LPR;
+  const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
+  const int32_t h = p.chunk_heavy[chunk];
+  const int64_t row = p.heavy_rows[h];
+  const int64_t rbeg = (int64_t)p.rowptr[row], rend = (int64_t)p.rowptr[row + 1];
+  const int64_t cbeg = rbeg + (chunk - p.heavy_chunk_off[h]) * p.chunk_nnz;
+  const int64_t cend = min(rend, cbeg + p.chunk_nnz);
+  float acc[VE];
+#pragma unroll
+  for (int i = 0; i < VE; ++i) acc[i] = 0.f;
+  if (col0 < p.F) {
+    const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
+    const float drow = HAS_VAL ? 0.f : p.dinv[row];
+    int64_t e = cbeg + g;
+    for (; e + 3 * NG < cend; e += 4 * NG) {
+      const int32_t c0 = p.colidx[e], c1 = p.colidx[e + NG], c2 = p.colidx[e + 2 * NG], c3 = p.colidx[e + 3 * NG];
+      const uint4 x0 = ldg16(X + (int64_t)c0 * p.ldx);
+      const uint4 x1 = ldg16(X + (int64_t)c1 * p.ldx);
+      const uint4 x2 = ldg16(X + (int64_t)c2 * p.ldx);
+      const uint4 x3 = ldg16(X + (int64_t)c3 * p.ldx);
+      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c0), x0);
+      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + NG, c1), x1);
+      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 2 * NG, c2), x2);
+      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 3 * NG, c3), x3);
+    }
+    for (; e < cend; e += NG) {
+      const int32_t c = p.colidx[e];
+      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c), ldg16(X + (int64_t)c * p.ldx));
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < VE; ++i) red[threadIdx.x * VE + i] = acc[i];
+  __syncthreads();
+  if (g == 0 && col0 < p.ldp) {
+    float s[VE];
+#pragma unroll
+    for (int i = 0; i < VE; ++i) s[i] = 0.f;
+    for (int gg = 0; gg < NG; ++gg)
+#pragma unroll
+      for (int i = 0; i < VE; ++i) s[i] += red[(gg * LPR + li) * VE + i];
+    float* out = p.partials + chunk * p.ldp + col0;
+#pragma unroll
+    for (int i = 0; i < VE; ++i)
+      if (col0 + i < p.ldp) out[i] = s[i];
+  }
+}
+
+// One thread per (heavy row, column): fixed-order sum of the chunk partials.
+template <typename T, typename IdxT>
+__global__ __launch_bounds__(256) void spmm_heavy_fixup_kernel(HeavyParams<IdxT> p) {
+  const int64_t h = blockIdx.x;
+  const int64_t col = (int64_t)blockIdx.y * 256 + threadIdx.x;
+  if (col >= p.F) return;
+  const int64_t row = p.heavy_rows[h];
+  const int64_t c0 = p.heavy_chunk_off[h], c1 = p.heavy_chunk_off[h + 1];
+  float a = 0.f;
+  for (int64_t c = c0; c < c1; ++c) a += p.partials[c * p.ldp + col];
+  epi_store1<T>(p.epi, row, col, a);
+}
+
+template <typename T, typename IdxT, int LPR, bool HAS_VAL>
+hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
+                      float* partials, hipStream_t s) {
+  constexpr int VE = Vec<T>::N;
+  constexpr int G = 64 / LPR;
+  const int64_t colblocks = (F + LPR * VE - 1) / (LPR * VE);
+  SpmmParams<IdxT> p;
+  p.n = A.n;
+  p.rowptr = reinterpret_cast<const IdxT*>(A.rowptr);
+  p.colidx = A.colidx;
+  p.values = A.values;
+  p.dinv = A.dinv;
+  p.heavy_threshold = A.n_heavy > 0 ? A.heavy_threshold : 0;
+  p.X = X; p.ldx = ldx; p.F = F; p.epi = epi;
+  const int64_t rows_per_block = 4 * G;
+  dim3 grid((unsigned)((A.n + rows_per_block - 1) / rows_per_block), (unsigned)colblocks);
+  hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), grid, dim3(256), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || A.n_heavy <= 0) return e;
+
+  HeavyParams<IdxT> hp;
+  hp.rowptr = p.rowptr; hp.colidx = A.colidx; hp.values = A.values; hp.dinv = A.dinv;
+  hp.heavy_rows = A.heavy_rows; hp.heavy_chunk_off = A.heavy_chunk_off; hp.chunk_heavy = A.chunk_heavy;
+  hp.chunk_nnz = A.chunk_nnz; hp.n_chunks = A.n_chunks;
+  hp.X = X; hp.ldx = ldx; hp.F = F;
+  hp.ldp = colblocks * LPR * VE;
+  hp.partials = partials; hp.epi = epi;
+  dim3 gridc((unsigned)A.n_chunks, (unsigned)colblocks);
+  hipLaunchKernelGGL((spmm_heavy_chunk_kernel<T, IdxT, LPR, HAS_VAL>), gridc, dim3(256), 0, s, hp);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 gridf((unsigned)A.n_heavy, (unsigned)((F + 255) / 256));
+  hipLaunchKernelGGL((spmm_heavy_fixup_kernel<T, IdxT>), gridf, dim3(256), 0, s, hp);
+  return hipGetLastError();
+}
+
+template <typename T, typename IdxT, bool HAS_VAL>
+hipError_t launch_lpr(const CsrView& A, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
+                      float* partials, hipStream_t s) {
+  constexpr int VE = Vec<T>::N;
+  const int64_t nvec = (F + VE - 1) / VE;
+  if (nvec <= 1) return launch_cfg<T, IdxT, 1, HAS_VAL>(A, X, ldx, F, epi, partials, s);
+  if (nvec <= 2) return launch_cfg<T, IdxT, 2, HAS_VAL>(A, X, ldx, F, epi, partials, s);
+  if (nvec <= 4) return launch_cfg<T, IdxT, 4, HAS_VAL>(A, X, ldx, F, epi, partials, s);
+  if (nvec <= 8) return launch_cfg<T, IdxT, 8, HAS_VAL>(A, X, ldx, F, epi, partials, s);
+  if (nvec <= 16) return launch_cfg<T, IdxT, 16, HAS_VAL>(A, X, ldx, F, epi, partials, s);
+  if (nvec <= 32) return launch_cfg<T, IdxT, 32, HAS_VAL>(A, X, ldx, F, epi, partials, s);
+  return launch_cfg<T, IdxT, 64, HAS_VAL>(A, X, ldx, F, epi, partials, s);
+}
+
+template <typename T>
+hipError_t launch_t(const CsrView& A, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
+                    float* partials, hipStream_t s) {
+  if (A.idx64)
+    return A.values ? launch_lpr<T, int64_t, true>(A, X, ldx, F, epi, partials, s)
+                    : launch_lpr<T, int64_t, false>(A, X, ldx, F, epi, partials, s);
+  return A.values ? launch_lpr<T, int32_t, true>(A, X, ldx, F, epi, partials, s)
+                  : launch_lpr<T, int32_t, false>(A, X, ldx, F, epi, partials, s);
+}
+
+int lpr_for(int prec, int64_t F) {
+  const int VE = prec == 0 ? 4 : 8;
+  const int64_t nvec = (F + VE - 1) / VE;
+  int l = 1;
+  while (l < nvec && l < 64) l <<= 1;
+  return l;
+}
+
+}  // namespace
+
+int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F) {
+  if (A.n_heavy <= 0) return 0;
+  const int VE = prec == 0 ? 4 : 8;
+  const int lpr = lpr_for(prec, F);
+  const int64_t colblocks = (F + (int64_t)lpr * VE - 1) / ((int64_t)lpr * VE);
+  return A.n_chunks * colblocks * lpr * VE;
+}
+
+hipError_t spmm_launch(const CsrView& A, int prec, const void* X, int64_t ldx, int64_t F,
+                       const Epilogue& epi, float* partials, hipStream_t s) {
+  switch (prec) {
+    case 0: return launch_t<float>(A, X, ldx, F, epi, partials, s);
+    case 1: return launch_t<f16>(A, X, ldx, F, epi, partials, s);
+    case 2: return launch_t<bf16>(A, X, ldx, F, epi, partials, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace gcn

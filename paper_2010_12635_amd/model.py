@@ -1,0 +1,226 @@
+"""Two-layer GCN training on the libgcn C ABI.
+
+This module only allocates device buffers (through torch) and sequences the
+library calls; every arithmetic step runs in the HIP kernels.  One training
+step is (Section "Graph Convolutions", Eq. (1), two stacked layers; O2 mixed
+precision of Section "Background and Motivation"):
+
+    H1 = dropout(ReLU(A_hat (X W1) + b1))        gcn_layer_fwd, layer 0
+    Z2 = A_hat (H1 W2) + b2                       gcn_layer_fwd, layer 1
+    loss, dZ2 = softmax-CE(Z2) * S                gcn_loss (S = loss scale)
+    dW2, db2, dZ1 = backward of layer 1           gcn_layer_bwd
+    dW1, db1      = backward of layer 0           gcn_layer_bwd
+    Adam on fp32 masters + dynamic loss scale     gcn_optimizer_step
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import gcn as G
+
+
+def round8(x: int) -> int:
+    return (x + 7) // 8 * 8
+
+
+class DeviceGraph:
+    """A_hat on the device, built by gcn_normalize (+ gcn_schedule for CSR)."""
+
+    def __init__(self, n, src, dst, prec=G.GCN_F16, index=G.GCN_I32, dense=False, values=True,
+                 schedule=True, device="cuda", heavy_threshold=0, chunk_nnz=0, stream=None):
+        self.n = int(n)
+        self.prec = prec
+        dev = torch.device(device)
+        src_t = torch.as_tensor(np.ascontiguousarray(src, dtype=np.int32)).to(dev)
+        dst_t = torch.as_tensor(np.ascontiguousarray(dst, dtype=np.int32)).to(dev)
+        ne = src_t.numel()
+        cap = 2 * ne + self.n
+        itype = torch.int64 if index == G.GCN_I64 else torch.int32
+        self.rowptr = torch.empty(self.n + 1, dtype=itype, device=dev)
+        self.colidx = torch.empty(cap, dtype=torch.int32, device=dev)
+        self.deg = torch.empty(self.n, dtype=torch.int32, device=dev)
+        self.dinv = torch.empty(self.n, dtype=torch.float32, device=dev)
+        vdt = G.torch_dtype(prec)
+        self.values = torch.empty(cap, dtype=vdt, device=dev) if (values and not dense) else None
+        self.ld_dense = round8(self.n) if dense else 0
+        self.dense = torch.empty((self.n, self.ld_dense), dtype=vdt, device=dev) if dense else None
+        ws = torch.empty(G.gcn_normalize_workspace_size(self.n, ne), dtype=torch.uint8, device=dev)
+        self.nnz = G.gcn_normalize(self.n, src_t if ne else None, dst_t if ne else None, index, self.rowptr,
+                                   self.colidx, self.deg, self.dinv, prec, self.values, self.dense,
+                                   self.ld_dense, ws, stream)
+        del ws, src_t, dst_t
+        self.adj = G.GcnAdj()
+        a = self.adj
+        a.n = self.n
+        a.nnz = self.nnz
+        a.format = G.GCN_DENSE if dense else G.GCN_CSR
+        a.index = index
+        a.value_prec = prec
+        a.rowptr = self.rowptr.data_ptr()
+        a.colidx = self.colidx.data_ptr()
+        a.values = self.values.data_ptr() if self.values is not None else None
+        a.dinv = self.dinv.data_ptr()
+        a.dense = self.dense.data_ptr() if dense else None
+        a.ld_dense = self.ld_dense
+        self.sched = None
+        if schedule and not dense:
+            nbytes = G.gcn_schedule_size(self.n, self.nnz, heavy_threshold, chunk_nnz)
+            self.sched = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+            G.gcn_schedule(a, self.sched, heavy_threshold, chunk_nnz, stream)
+
+    def csr_host(self):
+        rp = self.rowptr.cpu().numpy().astype(np.int64)
+        return rp, self.colidx[: self.nnz].cpu().numpy()
+
+
+@dataclass
+class AdamConfig:
+    lr: float = 0.01
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    backoff: float = 0.5
+    growth: float = 2.0
+    interval: int = 2000
+    min_scale: float = 1.0
+    max_scale: float = 16777216.0
+
+    def c(self):
+        return G.GcnAdamConfig(self.lr, self.beta1, self.beta2, self.eps, self.backoff, self.growth,
+                               self.interval, self.min_scale, self.max_scale)
+
+
+class GCN2:
+    """Two-layer GCN for vertex classification with device-resident state."""
+
+    def __init__(self, graph: DeviceGraph, X, labels, mask, W1, W2, b1=None, b2=None, prec=G.GCN_F16,
+                 dropout=0.5, seed=0, loss_scale=65536.0, adam: AdamConfig | None = None, device="cuda"):
+        dev = torch.device(device)
+        self.g = graph
+        self.prec = prec
+        self.dt = G.torch_dtype(prec)
+        n = graph.n
+        self.n = n
+        self.f_in, self.f_h = W1.shape
+        self.C = W2.shape[1]
+        assert W2.shape[0] == self.f_h
+        self.ld_x, self.ld_h, self.ld_c = round8(self.f_in), round8(self.f_h), round8(self.C)
+        self.p = float(dropout)
+        self.seed = int(seed)
+        self.adam = adam or AdamConfig()
+        # inputs (padding columns zero)
+        self.X = torch.zeros((n, self.ld_x), dtype=self.dt, device=dev)
+        self.X[:, : self.f_in] = torch.as_tensor(np.asarray(X, np.float32)).to(dev).to(self.dt)
+        self.labels = torch.as_tensor(np.asarray(labels, np.int32)).to(dev)
+        mask = np.asarray(mask, np.uint8)
+        self.mask = torch.as_tensor(mask).to(dev)
+        self.n_mask = int(mask.sum())
+        # flat parameters: [W1 (f_in x ld_h), b1 (ld_h), W2 (f_h x ld_c), b2 (ld_c)]
+        sizes = [self.f_in * self.ld_h, self.ld_h, self.f_h * self.ld_c, self.ld_c]
+        offs = np.cumsum([0] + sizes)
+        self.P = int(offs[-1])
+        self.offs = offs
+        master = np.zeros(self.P, np.float32)
+        w1 = np.zeros((self.f_in, self.ld_h), np.float32)
+        w1[:, : self.f_h] = W1
+        w2 = np.zeros((self.f_h, self.ld_c), np.float32)
+        w2[:, : self.C] = W2
+        master[offs[0]:offs[1]] = w1.ravel()
+        if b1 is not None:
+            master[offs[1]:offs[1] + self.f_h] = b1
+        master[offs[2]:offs[3]] = w2.ravel()
+        if b2 is not None:
+            master[offs[3]:offs[3] + self.C] = b2
+        self.master = torch.as_tensor(master).to(dev)
+        self.working = self.master.to(self.dt)
+        self.grad = torch.zeros(self.P, dtype=torch.float32, device=dev)
+        self.m = torch.zeros(self.P, dtype=torch.float32, device=dev)
+        self.v = torch.zeros(self.P, dtype=torch.float32, device=dev)
+        self.scaler = torch.zeros(4, dtype=torch.int32, device=dev)   # gcn_scaler (16 bytes)
+        self.scaler.view(torch.float32)[0] = loss_scale if prec != G.GCN_F32 else 1.0
+        self.overflow = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
+        self.n_correct = torch.zeros(1, dtype=torch.int32, device=dev)
+        # activations
+        self.H1 = torch.empty((n, self.ld_h), dtype=self.dt, device=dev)
+        self.SG1 = torch.empty((n, self.ld_h), dtype=self.dt, device=dev)   # S1, later G_S1
+        self.dZ1 = torch.empty((n, self.ld_h), dtype=self.dt, device=dev)
+        self.Z2 = torch.empty((n, self.ld_c), dtype=self.dt, device=dev)
+        self.SG2 = torch.empty((n, self.ld_c), dtype=self.dt, device=dev)   # S2, later G_S2
+        self.dZ2 = torch.empty((n, self.ld_c), dtype=self.dt, device=dev)
+        # layers
+        self.L1 = G.GcnLayer(self.f_in, self.f_h, self.ld_x, self.ld_h, G.GCN_ACT_RELU, self.p, 0, 0)
+        self.L2 = G.GcnLayer(self.f_h, self.C, self.ld_h, self.ld_c, G.GCN_ACT_NONE, 0.0, 1, 0)
+        ws = max(G.gcn_layer_workspace_size(graph.adj, self.L1, prec),
+                 G.gcn_layer_workspace_size(graph.adj, self.L2, prec),
+                 G.gcn_loss_workspace_size(n, self.C),
+                 G.gcn_transform_workspace_size(n, self.f_in, self.f_h, prec),
+                 G.gcn_transform_workspace_size(n, self.f_h, self.C, prec),
+                 G.gcn_aggregate_workspace_size(graph.adj, self.f_h, prec),
+                 G.gcn_aggregate_workspace_size(graph.adj, self.C, prec))
+        self.ws = torch.empty(ws // 4 + 64, dtype=torch.float32, device=dev)
+        self.adam_c = self.adam.c()
+
+    # parameter views
+    def _view(self, buf, k, shape):
+        return buf[self.offs[k]:self.offs[k + 1]].view(*shape)
+
+    def W1w(self): return self._view(self.working, 0, (self.f_in, self.ld_h))
+    def W2w(self): return self._view(self.working, 2, (self.f_h, self.ld_c))
+    def b1m(self): return self._view(self.master, 1, (self.ld_h,))
+    def b2m(self): return self._view(self.master, 3, (self.ld_c,))
+    def dW1(self): return self._view(self.grad, 0, (self.f_in, self.ld_h))
+    def db1(self): return self._view(self.grad, 1, (self.ld_h,))
+    def dW2(self): return self._view(self.grad, 2, (self.f_h, self.ld_c))
+    def db2(self): return self._view(self.grad, 3, (self.ld_c,))
+
+    def scale_ptr(self):
+        return self.scaler.data_ptr()   # first field of gcn_scaler is the float scale
+
+    def forward(self, epoch: int, training: bool = True, stream=None, agg_timer=None):
+        """Both layers.  With ``agg_timer`` (a callable returning a context
+        manager), each layer runs as gcn_transform + gcn_aggregate and the
+        aggregation call is bracketed by the timer; the arithmetic is the
+        same as gcn_layer_fwd."""
+        a = self.g.adj
+        if agg_timer is None:
+            G.gcn_layer_fwd(a, self.L1, self.prec, training, self.X, self.W1w(), self.b1m(), self.seed, epoch,
+                            self.SG1, self.H1, self.overflow, self.ws, stream)
+            G.gcn_layer_fwd(a, self.L2, self.prec, training, self.H1, self.W2w(), self.b2m(), self.seed, epoch,
+                            self.SG2, self.Z2, self.overflow, self.ws, stream)
+            return
+        for L, H, W, b, S, out in ((self.L1, self.X, self.W1w(), self.b1m(), self.SG1, self.H1),
+                                   (self.L2, self.H1, self.W2w(), self.b2m(), self.SG2, self.Z2)):
+            G.gcn_transform(self.n, L.f_in, L.f_out, self.prec, H, L.ld_in, W, L.ld_out, S, L.ld_out,
+                            self.overflow, self.ws, stream)
+            with agg_timer():
+                G.gcn_aggregate(a, L.f_out, self.prec, S, L.ld_out, b, L.act, L.dropout_p, training, self.seed,
+                                L.layer_id, epoch, out, L.ld_out, self.overflow, self.ws, stream)
+
+    def loss_and_backward(self, stream=None):
+        a = self.g.adj
+        G.gcn_loss(self.n, self.C, self.ld_c, self.prec, self.Z2, self.labels, self.mask, self.n_mask,
+                   self.scale_ptr(), self.loss, self.dZ2, self.n_correct, self.overflow, self.ws, stream)
+        G.gcn_layer_bwd(a, self.L2, self.prec, self.H1, self.W2w(), self.dZ2, G.GCN_ACT_RELU, self.p,
+                        self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream)
+        G.gcn_layer_bwd(a, self.L1, self.prec, self.X, self.W1w(), self.dZ1, G.GCN_ACT_NONE, 0.0,
+                        self.dW1(), self.db1(), None, self.SG1, self.overflow, self.ws, stream)
+
+    def optimizer_step(self, stream=None):
+        G.gcn_optimizer_step(self.P, self.master, self.grad, self.m, self.v, self.working, self.prec,
+                             self.adam_c, self.scaler, self.overflow, stream)
+
+    def step(self, epoch: int, stream=None, agg_timer=None):
+        """One full training step; asynchronous (no host synchronisation)."""
+        self.forward(epoch, True, stream, agg_timer)
+        self.loss_and_backward(stream)
+        self.optimizer_step(stream)
+
+    def scaler_state(self):
+        s = self.scaler.cpu()
+        return dict(scale=float(s.view(torch.float32)[0]), good_steps=int(s[1]), step=int(s[2]),
+                    skipped=int(s[3]))

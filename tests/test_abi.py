@@ -1,0 +1,131 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+that include/gcn.h declares, and rejects bad arguments before launching
+anything (these calls never reach the GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch  # noqa: F401  (loads the HIP runtime libgcn links against)
+
+from paper_2010_12635_amd import gcn as G
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gcn.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(G.LIB_PATH), reason="libgcn.so not built")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\**(gcn_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_and_binding_agree():
+    assert header_functions() == sorted(G.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(G.LIB_PATH)
+    for name in header_functions():
+        assert hasattr(lib, name), name
+
+
+def test_abi_version_and_status_strings():
+    assert G.gcn_abi_version() == 1
+    assert G.gcn_status_string(0) == "GCN_OK"
+    for s in range(1, 9):
+        assert G.gcn_status_string(s).startswith("GCN_ERR_")
+    assert "unknown" in G.gcn_status_string(99)
+
+
+def test_struct_sizes_match_header_layout():
+    assert ctypes.sizeof(G.GcnAdj) == 8 * 2 + 4 * 4 + 8 * 5 + 8 * 5 + 8 * 3
+    assert ctypes.sizeof(G.GcnLayer) == 8 * 4 + 4 * 4
+    assert ctypes.sizeof(G.GcnScaler) == 16
+    assert ctypes.sizeof(G.GcnAdamConfig) == 36
+
+
+def test_workspace_queries():
+    assert G.gcn_normalize_workspace_size(1000, 5000) > 4 * (2 * 5000 + 1000)
+    assert G.gcn_loss_workspace_size(1000, 7) > 0
+    assert G.gcn_schedule_size(1000, 9000) > 0
+    with pytest.raises(G.GcnError):
+        G.gcn_normalize_workspace_size(0, 10)
+    with pytest.raises(G.GcnError):
+        G.gcn_loss_workspace_size(10, 0)
+
+
+def _adj(n=100, fmt=G.GCN_CSR):
+    a = G.GcnAdj()
+    a.n = n
+    a.nnz = 300
+    a.format = fmt
+    a.index = G.GCN_I32
+    a.value_prec = G.GCN_F16
+    a.rowptr = 0x1000
+    a.colidx = 0x2000
+    a.values = 0x3000
+    a.dinv = 0x4000
+    return a
+
+
+def _call_fwd(adj, layer, prec=G.GCN_F16, H=0x10000, ws_bytes=1 << 20):
+    lib = G.lib()
+    return lib.gcn_layer_fwd(ctypes.byref(adj), ctypes.byref(layer), prec, 1, H, 0x20000, None, 0, 0,
+                             0x30000, 0x40000, None, 0x50000, ws_bytes, None)
+
+
+def test_layer_fwd_validation_codes():
+    L = G.GcnLayer(16, 8, 16, 8, G.GCN_ACT_RELU, 0.5, 0, 0)
+    assert _call_fwd(_adj(), L, prec=7) == 1                              # bad precision
+    assert _call_fwd(_adj(), G.GcnLayer(10, 8, 12, 8, 1, 0.5, 0, 0)) == 3   # ld % 8
+    assert _call_fwd(_adj(), G.GcnLayer(16, 8, 8, 8, 1, 0.5, 0, 0)) == 2    # ld < f
+    assert _call_fwd(_adj(), G.GcnLayer(0, 8, 8, 8, 1, 0.5, 0, 0)) == 2     # f = 0
+    assert _call_fwd(_adj(), G.GcnLayer(16, 8, 16, 8, 1, 1.0, 0, 0)) == 1   # p = 1
+    assert _call_fwd(_adj(), G.GcnLayer(16, 8, 16, 8, 5, 0.5, 0, 0)) == 1   # bad act
+    assert _call_fwd(_adj(), L, H=0x10004) == 3                            # misaligned
+    assert _call_fwd(_adj(), L, ws_bytes=0) == 6                           # workspace
+    a = _adj(); a.value_prec = G.GCN_F32
+    assert _call_fwd(a, L) == 4                                            # value precision
+    a = _adj(); a.values = None; a.dinv = None
+    assert _call_fwd(a, L) == 1                                            # no values, no dinv
+    a = _adj(fmt=G.GCN_DENSE)
+    assert _call_fwd(a, L) == 1                                            # dense pointer missing
+    a.dense = 0x8000; a.ld_dense = 100
+    assert _call_fwd(a, L) == 3                                            # ld_dense % 8
+    a = _adj(n=0)
+    assert _call_fwd(a, L) == 2
+
+
+def test_normalize_validation_codes():
+    lib = G.lib()
+    nnz = ctypes.c_int64(0)
+    f = lib.gcn_normalize
+    # capacity below 2E + n
+    assert f(10, 5, 0x1000, 0x2000, 0, 0x3000, 0x4000, 19, None, 0x5000, 1, None, None, 0,
+             ctypes.byref(nnz), 0x6000, 1 << 20, None) == 5
+    # missing dinv
+    assert f(10, 5, 0x1000, 0x2000, 0, 0x3000, 0x4000, 20, None, None, 1, None, None, 0,
+             ctypes.byref(nnz), 0x6000, 1 << 20, None) == 1
+    # workspace too small
+    assert f(10, 5, 0x1000, 0x2000, 0, 0x3000, 0x4000, 20, None, 0x5000, 1, None, None, 0,
+             ctypes.byref(nnz), 0x6000, 16, None) == 6
+    # dense with ld not a multiple of 8
+    assert f(10, 5, 0x1000, 0x2000, 0, 0x3000, 0x4000, 20, None, 0x5000, 1, None, 0x7000, 12,
+             ctypes.byref(nnz), 0x6000, 1 << 20, None) == 3
+
+
+def test_loss_and_optimizer_validation_codes():
+    lib = G.lib()
+    assert lib.gcn_loss(10, 7, 7, 1, 0x1000, 0x2000, None, 5, None, 0x3000, 0x4000, None, None,
+                        0x5000, 1 << 20, None) == 3                          # ld % 8
+    assert lib.gcn_loss(10, 7, 8, 1, 0x1000, 0x2000, None, 0, None, 0x3000, 0x4000, None, None,
+                        0x5000, 1 << 20, None) == 2                          # empty mask
+    cfg = G.GcnAdamConfig(0.01, 0.9, 0.999, 1e-8, 0.5, 2.0, 2000, 1.0, 2.0**24)
+    assert lib.gcn_optimizer_step(0, 0x1000, 0x2000, 0x3000, 0x4000, None, 1, ctypes.byref(cfg),
+                                  0x5000, 0x6000, None) == 2
+    bad = G.GcnAdamConfig(0.01, 1.0, 0.999, 1e-8, 0.5, 2.0, 2000, 1.0, 2.0**24)
+    assert lib.gcn_optimizer_step(10, 0x1000, 0x2000, 0x3000, 0x4000, None, 1, ctypes.byref(bad),
+                                  0x5000, 0x6000, None) == 1

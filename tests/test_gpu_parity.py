@@ -1,0 +1,361 @@
+"""GPU parity: every libgcn call against the CPU fp64 oracle on the same
+seeded inputs.  Integer outputs are compared bit-exactly; floating-point
+outputs to the tolerances in tests/parity.py (fp32: 1e-5 normwise; fp16:
+2e-2 per element with the tensor RMS as floor; bf16: 1e-1 provisional)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import gcn_oracle as O
+from paper_2010_12635_amd import gcn as G
+from paper_2010_12635_amd import inputs as I
+from paper_2010_12635_amd.model import DeviceGraph, GCN2, round8
+from tests.parity import assert_close, hub_graph, tol_for
+
+pytestmark = pytest.mark.gpu
+
+PRECS = [G.GCN_F32, G.GCN_F16, G.GCN_BF16]
+PNAME = {0: "f32", 1: "f16", 2: "bf16"}
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def to_dev(a, prec, ld=None):
+    a = np.asarray(a, np.float32)
+    n, f = a.shape
+    ld = ld or round8(f)
+    t = torch.zeros((n, ld), dtype=G.torch_dtype(prec), device=dev())
+    t[:, :f] = torch.as_tensor(a).to(dev()).to(G.torch_dtype(prec))
+    return t
+
+
+def host(t, f=None):
+    x = t.float().cpu().numpy().astype(np.float64)
+    return x if f is None else x[:, :f]
+
+
+def rounded(a, prec):
+    """The values the device actually holds for a host array in `prec`."""
+    return torch.as_tensor(np.asarray(a, np.float32)).to(G.torch_dtype(prec)).float().numpy().astype(np.float64)
+
+
+# ------------------------------------------------------------- normalize ----
+
+@pytest.mark.parametrize("index", [G.GCN_I32, G.GCN_I64])
+def test_normalize_bit_exact(index):
+    n = 6000
+    # one hub above the LDS sort limit (4096), medium hubs, many small rows
+    src, dst = hub_graph(n, 20000, [(7, 5000), (100, 700), (200, 90), (300, 64)], seed=1)
+    g = O.graph(n, src, dst)
+    dg = DeviceGraph(n, src, dst, prec=G.GCN_F32, index=index, schedule=False)
+    rp, ci = dg.csr_host()
+    assert dg.nnz == g.nnz
+    assert np.array_equal(rp, g.rowptr)
+    assert np.array_equal(ci, g.colidx)
+    assert np.array_equal(dg.deg.cpu().numpy(), g.deg)
+    assert np.array_equal(dg.dinv.cpu().numpy(), O.dinv_f32(g))
+    vals = dg.values[: dg.nnz].cpu().numpy().astype(np.float64)
+    assert np.max(np.abs(vals - O.norm_values(g)) / O.norm_values(g)) < 3e-7
+    # run-to-run identical
+    dg2 = DeviceGraph(n, src, dst, prec=G.GCN_F32, index=index, schedule=False)
+    assert np.array_equal(dg2.csr_host()[1], ci)
+
+
+@pytest.mark.parametrize("prec", [G.GCN_F16, G.GCN_F32])
+def test_normalize_dense(prec):
+    n = 700
+    src, dst = hub_graph(n, 3000, [(3, 300)], seed=2)
+    g = O.graph(n, src, dst)
+    dg = DeviceGraph(n, src, dst, prec=prec, dense=True)
+    want = O.dense_adj(g)
+    got = dg.dense[:, :n].float().cpu().numpy().astype(np.float64)
+    assert np.array_equal(got != 0, want != 0)
+    assert_close(got, want, prec, "dense A_hat")
+
+
+def test_normalize_empty_and_bad_ids():
+    dg = DeviceGraph(37, np.zeros(0, np.int32), np.zeros(0, np.int32), prec=G.GCN_F32)
+    rp, ci = dg.csr_host()
+    assert np.array_equal(rp, np.arange(38)) and np.array_equal(ci, np.arange(37))
+    assert np.all(dg.dinv.cpu().numpy() == 1.0)
+    with pytest.raises(G.GcnError) as e:
+        DeviceGraph(10, np.array([0, 3], np.int32), np.array([1, 10], np.int32))
+    assert e.value.status == 8
+
+
+def test_schedule_lists_heavy_rows():
+    n = 3000
+    src, dst = hub_graph(n, 9000, [(5, 400), (17, 120), (2999, 1000)], seed=3)
+    g = O.graph(n, src, dst)
+    dg = DeviceGraph(n, src, dst, prec=G.GCN_F16, heavy_threshold=32, chunk_nnz=64)
+    a = dg.adj
+    heavy = np.flatnonzero(g.deg > 32)
+    assert a.n_heavy == heavy.size
+    hr = torch.empty(0)  # noqa: F841
+    # read the schedule arrays back through their device addresses
+    base = dg.sched
+    off = lambda p: (p - base.data_ptr())
+    rows = base[off(a.heavy_rows): off(a.heavy_rows) + 4 * a.n_heavy].view(torch.int32).cpu().numpy()
+    assert np.array_equal(rows, heavy)
+    cho = base[off(a.heavy_chunk_off): off(a.heavy_chunk_off) + 4 * (a.n_heavy + 1)].view(torch.int32).cpu().numpy()
+    want = np.concatenate([[0], np.cumsum((g.deg[heavy] + 63) // 64)])
+    assert np.array_equal(cho, want)
+    assert a.n_chunks == want[-1]
+
+
+# ------------------------------------------------------------ layer fwd ----
+
+def _layer_case(n, f_in, f_out, seed, hubs=True):
+    rng = np.random.default_rng(seed)
+    src, dst = hub_graph(n, 4 * n, [(1, 600), (2, 150)] if hubs else [], seed)
+    g = O.graph(n, src, dst)
+    h = rng.standard_normal((n, f_in)).astype(np.float32)
+    w = (rng.standard_normal((f_in, f_out)) / np.sqrt(f_in)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(f_out)).astype(np.float32)
+    return g, src, dst, h, w, b
+
+
+FWD_CASES = [
+    # (n, f_in, f_out, act, p, dense)
+    (3000, 500, 64, G.GCN_ACT_RELU, 0.5, False),
+    (3000, 128, 7, G.GCN_ACT_NONE, 0.0, False),
+    (2100, 40, 130, G.GCN_ACT_RELU, 0.3, False),
+    (1500, 500, 64, G.GCN_ACT_RELU, 0.5, True),
+    (1500, 64, 32, G.GCN_ACT_NONE, 0.0, True),
+]
+
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_act{c[3]}_p{c[4]}_{'dense' if c[5] else 'csr'}")
+def test_layer_fwd(prec, case):
+    n, f_in, f_out, act, p, dense = case
+    g, src, dst, h, w, b = _layer_case(n, f_in, f_out, seed=n + f_in)
+    dg = DeviceGraph(n, src, dst, prec=prec, dense=dense, heavy_threshold=48, chunk_nnz=96)
+    L = G.GcnLayer(f_in, f_out, round8(f_in), round8(f_out), act, p, 3, 0)
+    H, W = to_dev(h, prec), to_dev(w, prec, round8(f_out))
+    bias = torch.as_tensor(b).to(dev())
+    S = torch.empty((n, round8(f_out)), dtype=G.torch_dtype(prec), device=dev())
+    Hout = torch.empty_like(S)
+    ov = torch.zeros(1, dtype=torch.int32, device=dev())
+    ws = torch.empty(G.gcn_layer_workspace_size(dg.adj, L, prec), dtype=torch.uint8, device=dev())
+    seed, epoch = 1234567, 5
+    G.gcn_layer_fwd(dg.adj, L, prec, True, H, W, bias, seed, epoch, S, Hout, ov, ws)
+    torch.cuda.synchronize()
+    hr, wr = rounded(h, prec), rounded(w, prec)
+    vals = O.norm_values(g)
+    s_o, z_o, out_o = O.layer_fwd(g, vals, hr, wr, b, "relu" if act else "none", p, True, seed, 3, epoch,
+                                  dense=O.dense_adj(g, vals) if dense else None)
+    assert_close(host(S, f_out), s_o, prec, "S = H W")
+    assert_close(host(Hout, f_out), out_o, prec, "H_out")
+    assert int(ov.item()) == 0
+    if p > 0:   # dropout decisions are bit-identical: zero pattern of kept positives matches
+        keep = O.dropout_keep(seed, 3, epoch, n, f_out, p)
+        got = host(Hout, f_out)
+        # positions whose sign no rounding of the device path can flip
+        pos = z_o > (1e-3 if prec == 0 else 10 * tol_for(prec) * np.sqrt(np.mean(z_o * z_o)))
+        assert np.array_equal(got[pos] != 0, keep[pos])
+
+
+# ------------------------------------------------------------ layer bwd ----
+
+BWD_CASES = [
+    (3000, 500, 64, G.GCN_ACT_NONE, 0.0, False),
+    (3000, 64, 7, G.GCN_ACT_RELU, 0.5, False),
+    (2100, 130, 40, G.GCN_ACT_RELU, 0.3, False),
+    (1500, 64, 32, G.GCN_ACT_RELU, 0.5, True),
+]
+
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("case", BWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_below{c[3]}_p{c[4]}_{'dense' if c[5] else 'csr'}")
+def test_layer_bwd(prec, case):
+    n, f_in, f_out, act_below, p, dense = case
+    g, src, dst, h, w, _ = _layer_case(n, f_in, f_out, seed=7 * n + f_out)
+    rng = np.random.default_rng(n)
+    if act_below == G.GCN_ACT_RELU:   # H as produced by ReLU + dropout: exact zeros
+        h = np.where(rng.random(h.shape) < 0.5, 0.0, np.abs(h) * 2).astype(np.float32)
+    dz = (rng.standard_normal((n, f_out)) * 8.0).astype(np.float32)
+    dg = DeviceGraph(n, src, dst, prec=prec, dense=dense, heavy_threshold=48, chunk_nnz=96)
+    L = G.GcnLayer(f_in, f_out, round8(f_in), round8(f_out), G.GCN_ACT_NONE, 0.0, 0, 0)
+    H, W, dZ = to_dev(h, prec), to_dev(w, prec, round8(f_out)), to_dev(dz, prec)
+    dW = torch.full((f_in, round8(f_out)), 7.0, dtype=torch.float32, device=dev())
+    db = torch.full((round8(f_out),), 7.0, dtype=torch.float32, device=dev())
+    dZb = torch.empty((n, round8(f_in)), dtype=G.torch_dtype(prec), device=dev())
+    GS = torch.empty((n, round8(f_out)), dtype=G.torch_dtype(prec), device=dev())
+    ov = torch.zeros(1, dtype=torch.int32, device=dev())
+    ws = torch.empty(G.gcn_layer_workspace_size(dg.adj, L, prec), dtype=torch.uint8, device=dev())
+    G.gcn_layer_bwd(dg.adj, L, prec, H, W, dZ, act_below, p, dW, db, dZb, GS, ov, ws)
+    torch.cuda.synchronize()
+    hr, wr, dzr = rounded(h, prec), rounded(w, prec), rounded(dz, prec)
+    vals = O.norm_values(g)
+    gs_o, dw_o, db_o, dzb_o = O.layer_bwd(g, vals, hr, wr, dzr, "relu" if act_below else "none", p,
+                                          dense=O.dense_adj(g, vals) if dense else None)
+    assert_close(host(GS, f_out), gs_o, prec, "G_S")
+    assert_close(dW.cpu().numpy()[:, :f_out], dw_o, prec, "dW")
+    assert np.all(dW.cpu().numpy()[:, f_out:] == 0)
+    assert_close(db.cpu().numpy()[:f_out], db_o, prec, "db")
+    assert np.all(db.cpu().numpy()[f_out:] == 0)
+    assert_close(host(dZb, f_in), dzb_o, prec, "dZ_below")
+    assert int(ov.item()) == 0
+
+
+def test_bwd_power_of_two_scale_invariance():
+    """fp32: scaling dZ by 2^k scales G_S, dW, db, dZ_below by exactly 2^k."""
+    prec = G.GCN_F32
+    n, f_in, f_out = 1200, 40, 24
+    g, src, dst, h, w, _ = _layer_case(n, f_in, f_out, seed=99)
+    dz = np.random.default_rng(3).standard_normal((n, f_out)).astype(np.float32)
+    dg = DeviceGraph(n, src, dst, prec=prec, heavy_threshold=48, chunk_nnz=96)
+    L = G.GcnLayer(f_in, f_out, round8(f_in), round8(f_out), G.GCN_ACT_NONE, 0.0, 0, 0)
+    ws = torch.empty(G.gcn_layer_workspace_size(dg.adj, L, prec), dtype=torch.uint8, device=dev())
+    outs = []
+    for k in (0, 12):
+        dZ = to_dev(dz * (2.0 ** k), prec)
+        dW = torch.empty((f_in, round8(f_out)), dtype=torch.float32, device=dev())
+        db = torch.empty((round8(f_out),), dtype=torch.float32, device=dev())
+        dZb = torch.empty((n, round8(f_in)), dtype=torch.float32, device=dev())
+        GS = torch.empty((n, round8(f_out)), dtype=torch.float32, device=dev())
+        G.gcn_layer_bwd(dg.adj, L, prec, to_dev(h, prec), to_dev(w, prec, round8(f_out)), dZ, G.GCN_ACT_RELU,
+                        0.5, dW, db, dZb, GS, None, ws)
+        outs.append([t.cpu() for t in (GS, dW, db, dZb)])
+    for a, b in zip(*outs):
+        assert torch.equal(a * 4096.0, b)
+
+
+# ----------------------------------------------------------------- loss ----
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("C", [7, 40, 64])
+def test_loss(prec, C):
+    n = 5000
+    rng = np.random.default_rng(C)
+    z = (rng.standard_normal((n, C)) * 3).astype(np.float32)
+    y = rng.integers(0, C, n).astype(np.int32)
+    mask = (rng.random(n) < 0.3).astype(np.uint8)
+    ld = round8(C)
+    Z = to_dev(z, prec)
+    dZ = torch.empty_like(Z)
+    scale = torch.tensor([1024.0], device=dev())
+    loss = torch.zeros(1, device=dev())
+    nc = torch.zeros(1, dtype=torch.int32, device=dev())
+    ws = torch.empty(G.gcn_loss_workspace_size(n, C), dtype=torch.uint8, device=dev())
+    G.gcn_loss(n, C, ld, prec, Z, torch.as_tensor(y).to(dev()), torch.as_tensor(mask).to(dev()), int(mask.sum()),
+               scale, loss, dZ, nc, None, ws)
+    torch.cuda.synchronize()
+    zr = rounded(z, prec)
+    l_o, d_o, nc_o = O.softmax_ce(zr, y, mask, 1024.0)
+    assert abs(loss.item() - l_o) <= (1e-5 if prec == 0 else 1e-4) * max(1.0, abs(l_o))
+    assert_close(host(dZ, C), d_o, prec, "dlogits")
+    assert np.all(host(dZ)[:, C:] == 0)
+    assert nc.item() == nc_o
+
+
+# ------------------------------------------------------------ optimiser ----
+
+def test_optimizer_matches_oracle_and_skips_on_overflow():
+    P = 5000
+    rng = np.random.default_rng(0)
+    w0 = rng.standard_normal(P).astype(np.float32)
+    g0 = (rng.standard_normal(P) * 65536).astype(np.float32)
+    master = torch.as_tensor(w0).to(dev())
+    grad = torch.as_tensor(g0).to(dev())
+    m = torch.zeros(P, device=dev())
+    v = torch.zeros(P, device=dev())
+    working = torch.empty(P, dtype=torch.float16, device=dev())
+    state = torch.zeros(4, dtype=torch.int32, device=dev())
+    state.view(torch.float32)[0] = 65536.0
+    ov = torch.zeros(1, dtype=torch.int32, device=dev())
+    cfg = G.GcnAdamConfig(0.01, 0.9, 0.999, 1e-8, 0.5, 2.0, 3, 1.0, 2.0**24)
+    sc = O.LossScaler(65536.0, 0.5, 2.0, 3, 1.0, 2.0**24)
+    ad = O.AdamState(P)
+    w_o = w0.astype(np.float64)
+    for step in range(4):
+        gs = g0 * (1 + step)
+        grad.copy_(torch.as_tensor(gs))
+        G.gcn_optimizer_step(P, master, grad, m, v, working, G.GCN_F16, cfg, state, ov)
+        w_o, applied = O.adam_step(w_o, gs.astype(np.float64), ad, sc, lr=0.01)
+        torch.cuda.synchronize()
+        assert_close(master.cpu().numpy(), w_o, 0, f"master step {step}")
+        assert np.array_equal(working.cpu().numpy(), master.cpu().numpy().astype(np.float16))
+        st = state.cpu()
+        assert float(st.view(torch.float32)[0]) == sc.scale and int(st[1]) == sc.good
+    # overflow: weights bit-unchanged, scale halved, flag cleared
+    before = master.clone()
+    bad = g0.copy()
+    bad[17] = np.inf
+    grad.copy_(torch.as_tensor(bad))
+    G.gcn_optimizer_step(P, master, grad, m, v, working, G.GCN_F16, cfg, state, ov)
+    sc.update(True)
+    torch.cuda.synchronize()
+    assert torch.equal(master, before)
+    st = state.cpu()
+    assert float(st.view(torch.float32)[0]) == sc.scale and int(st[3]) == 1 and ov.item() == 0
+    # overflow flagged by an earlier kernel
+    ov.fill_(1)
+    grad.copy_(torch.as_tensor(g0))
+    G.gcn_optimizer_step(P, master, grad, m, v, working, G.GCN_F16, cfg, state, ov)
+    torch.cuda.synchronize()
+    assert torch.equal(master, before) and int(state.cpu()[3]) == 2
+
+
+# ------------------------------------------------------- full training step ----
+
+def _oracle_step(g, x, y, mask, w1, b1, w2, b2, p, seed, epoch, scale):
+    vals = O.norm_values(g)
+    _, _, h1 = O.layer_fwd(g, vals, x, w1, b1, "relu", p, True, seed, 0, epoch)
+    _, z2, _ = O.layer_fwd(g, vals, h1, w2, b2, "none", 0.0, True, seed, 1, epoch)
+    loss, dz2, nc = O.softmax_ce(z2, y, mask, scale)
+    _, dw2, db2, dz1 = O.layer_bwd(g, vals, h1, w2, dz2, "relu", p)
+    _, dw1, db1, _ = O.layer_bwd(g, vals, x, w1, dz1, "none", 0.0, need_dh=False)
+    return loss, nc, dw1, db1, dw2, db2, h1, z2
+
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+def test_full_step_er2k(prec):
+    """One forward + loss + backward step of the tiny 2-layer workload
+    (ER n=2048, 512 -> 16 -> 7, 140-vertex train mask, dropout 0.5)."""
+    wl = I.workload("er2k", 0)
+    n = wl["n"]
+    g = O.graph(n, wl["src"], wl["dst"])
+    dg = DeviceGraph(n, wl["src"], wl["dst"], prec=prec)
+    scale = 65536.0 if prec else 1.0
+    m = GCN2(dg, wl["X"], wl["labels"], wl["mask"], wl["W1"], wl["W2"], prec=prec, dropout=0.5,
+             seed=wl["dropout_seed"], loss_scale=scale)
+    m.forward(epoch=0)
+    m.loss_and_backward()
+    torch.cuda.synchronize()
+    x, w1, w2 = rounded(wl["X"], prec), rounded(wl["W1"], prec), rounded(wl["W2"], prec)
+    loss, nc, dw1, db1, dw2, db2, h1, z2 = _oracle_step(g, x, wl["labels"], wl["mask"], w1, wl["b1"], w2,
+                                                        wl["b2"], 0.5, wl["dropout_seed"], 0, scale)
+    assert abs(m.loss.item() - loss) <= (1e-5 if prec == 0 else 2e-3) * abs(loss)
+    assert_close(host(m.H1, 16), h1, prec, "H1")
+    assert_close(host(m.Z2, 7), z2, prec, "Z2")
+    # gradients through a chain of 16-bit roundings: compared per element in
+    # fp32 mode, normwise (same bound) in 16-bit modes (see design notes)
+    grads = [(m.dW1().cpu().numpy()[:, :16], dw1, "dW1"), (m.db1().cpu().numpy()[:16], db1, "db1"),
+             (m.dW2().cpu().numpy()[:, :7], dw2, "dW2"), (m.db2().cpu().numpy()[:7], db2, "db2")]
+    for got, want, name in grads:
+        if prec == 0:
+            assert_close(got, want, 0, name)
+        else:
+            err = np.max(np.abs(got - want)) / np.max(np.abs(want))
+            assert err <= (2e-2 if prec == 1 else 1e-1), f"{name}: normwise {err}"
+    assert m.overflow.item() == 0
+
+
+def test_full_step_deterministic():
+    wl = I.workload("er2k", 1)
+    n = wl["n"]
+    res = []
+    for _ in range(2):
+        dg = DeviceGraph(n, wl["src"], wl["dst"], prec=G.GCN_F16, heavy_threshold=16, chunk_nnz=16)
+        m = GCN2(dg, wl["X"], wl["labels"], wl["mask"], wl["W1"], wl["W2"], prec=G.GCN_F16,
+                 seed=wl["dropout_seed"])
+        for ep in range(3):
+            m.step(ep)
+        torch.cuda.synchronize()
+        res.append((m.master.cpu(), m.H1.cpu(), m.loss.cpu()))
+    for a, b in zip(*res):
+        assert torch.equal(a, b)
