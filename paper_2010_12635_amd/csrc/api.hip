@@ -95,14 +95,14 @@ LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
   p.s_split = gemm_choose_splits(prec, n, L->f_out, L->f_in);
   p.dh_split = gemm_choose_splits(prec, n, L->f_in, L->f_out);
   p.dw_split = gemm_choose_splits(prec, L->f_in, L->f_out, n);
-  p.agg_split = A->format == GCN_DENSE ? gemm_choose_splits(prec, n, L->f_out, n) : 1;
+  p.agg_split = 1;
   int64_t f = 0;
   auto upd = [&](int64_t x) { if (x > f) f = x; };
   if (p.s_split > 1) upd(p.s_split * n * L->f_out);
   if (p.dh_split > 1) upd(p.dh_split * n * L->f_in);
   upd(p.dw_split * L->f_in * L->f_out);
   if (A->format == GCN_DENSE) {
-    if (p.agg_split > 1) upd(p.agg_split * n * L->f_out);
+    upd((int64_t)(dense_agg_workspace_bytes(prec, n, L->f_out) / sizeof(float)) + 1);
   } else {
     upd(spmm_partials_floats(view_of(A), prec, L->f_out));
   }
@@ -136,16 +136,15 @@ hipError_t run_gemm(int32_t prec, bool akc, bool bkc, const void* A, int64_t lda
 
 hipError_t aggregate(const gcn_adj* A, int32_t prec, const void* X, int64_t ldx, int64_t F, int split,
                      const Epilogue& epi, float* ws, hipStream_t s) {
-  if (A->format == GCN_DENSE)
-    return run_gemm(prec, true, false, A->dense, A->ld_dense, X, ldx, A->n, F, A->n, split, false, ws, epi, s);
+  (void)split;
+  if (A->format == GCN_DENSE) return dense_agg_launch(prec, A->dense, A->ld_dense, A->n, X, ldx, F, epi, ws, s);
   return spmm_launch(view_of(A), prec, X, ldx, F, epi, ws, s);
 }
 
 size_t aggregate_bytes(const gcn_adj* A, int32_t prec, int64_t F) {
   int64_t f = 0;
   if (A->format == GCN_DENSE) {
-    const int sp = gemm_choose_splits(prec, A->n, F, A->n);
-    if (sp > 1) f = sp * A->n * F;
+    f = (int64_t)(dense_agg_workspace_bytes(prec, A->n, F) / sizeof(float)) + 1;
   } else {
     f = spmm_partials_floats(view_of(A), prec, F);
   }
@@ -352,8 +351,7 @@ gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* 
     return GCN_ERR_WORKSPACE;
   if (workspace && !aligned16(workspace)) return GCN_ERR_ALIGNMENT;
   Epilogue ea = agg_epi(Y, ldy, A->n, F, bias, act, dropout_p, training, seed, layer_id, epoch, overflow);
-  const int split = A->format == GCN_DENSE ? gemm_choose_splits(prec, A->n, F, A->n) : 1;
-  GCN_HIP(aggregate(A, prec, X, ldx, F, split, ea, static_cast<float*>(workspace), s));
+  GCN_HIP(aggregate(A, prec, X, ldx, F, 1, ea, static_cast<float*>(workspace), s));
   return finish(hipSuccess, s);
 }
 

@@ -74,8 +74,11 @@ __device__ __forceinline__ Philox8 philox4x64_10(uint64_t c0, uint64_t c1, uint6
   return o;
 }
 
+// Word w (0..7) of a Philox block: low half of output w/2 for even w, high
+// half for odd w.  Selected without indexing so the block stays in registers.
 __device__ __forceinline__ uint32_t philox_word(const Philox8& o, uint32_t w) {
-  uint64_t x = o.w[w >> 1];
+  const uint32_t h = w >> 1;
+  const uint64_t x = h == 0 ? o.w[0] : h == 1 ? o.w[1] : h == 2 ? o.w[2] : o.w[3];
   return (w & 1) ? (uint32_t)(x >> 32) : (uint32_t)x;
 }
 

@@ -236,39 +236,55 @@ hipError_t launch_typed(const GemmCall& c, const GemmParams& p, hipStream_t s) {
 
 // ------------------------------------------------------------ reductions ----
 
+// 64 output elements per workgroup; 4 lane groups each sum every 4th split
+// (in split order), then the 4 group sums are added in group order.
 template <typename T>
 __global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __restrict__ part, int splits,
                                                               int64_t M, int64_t N, int64_t width, Epilogue ep) {
+  __shared__ float red[4][64];
   const int64_t total = M * width;
-  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t r = idx / width, c = idx % width;
-    if (c >= N) {   // EPI_F32 padding columns
-      reinterpret_cast<float*>(ep.out)[r * ep.ldo + c] = 0.f;
-      continue;
-    }
-    float a = 0.f;
+  const int64_t idx = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
+  const int g = threadIdx.x >> 6;
+  const int64_t r = idx / width, c = idx % width;
+  const bool live = idx < total && c < N;
+  float a = 0.f;
+  if (live) {
     const float* q = part + r * N + c;
-    for (int sidx = 0; sidx < splits; ++sidx) a += q[(int64_t)sidx * M * N];
-    epi_store1<T>(ep, r, c, a);
+    const int64_t stride = M * N;
+#pragma unroll 8
+    for (int sidx = g; sidx < splits; sidx += 4) a += q[(int64_t)sidx * stride];
   }
+  red[g][threadIdx.x & 63] = a;
+  __syncthreads();
+  if (g != 0 || idx >= total) return;
+  if (c >= N) {   // EPI_F32 padding columns
+    reinterpret_cast<float*>(ep.out)[r * ep.ldo + c] = 0.f;
+    return;
+  }
+  const int t = threadIdx.x & 63;
+  float sum = red[0][t] + red[1][t];
+  sum += red[2][t];
+  sum += red[3][t];
+  epi_store1<T>(ep, r, c, sum);
 }
 
-// Column sums over a block of rows; threads of one column group walk rows in
-// a fixed order, then the row groups are combined in a fixed order.
-constexpr int64_t COLSUM_ROWS = 2048;
-
+// Column sums: a workgroup sums `rows_per_block` consecutive rows, 4 row
+// groups x 64 columns, each walking its rows in order; the row groups are
+// then added in group order.
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ X, int64_t rows, int64_t cols,
-                                                             int64_t ld, int64_t ldp, float* __restrict__ part) {
+                                                             int64_t ld, int64_t ldp, int64_t rows_per_block,
+                                                             float* __restrict__ part) {
   __shared__ float red[256];
   const int64_t c = (int64_t)blockIdx.y * 64 + (threadIdx.x & 63);
-  const int rg = threadIdx.x >> 6;   // 4 row groups
-  const int64_t r0 = (int64_t)blockIdx.x * COLSUM_ROWS;
-  const int64_t r1 = min(rows, r0 + COLSUM_ROWS);
+  const int rg = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+  const int64_t r1 = min(rows, r0 + rows_per_block);
   float a = 0.f;
-  if (c < cols)
+  if (c < cols) {
+#pragma unroll 8
     for (int64_t r = r0 + rg; r < r1; r += 4) a += to_f32<T>(X[r * ld + c]);
+  }
   red[threadIdx.x] = a;
   __syncthreads();
   if (rg == 0 && c < ldp) {
@@ -277,6 +293,11 @@ __global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict
     s += red[threadIdx.x + 192];
     part[(int64_t)blockIdx.x * ldp + c] = c < cols ? s : 0.f;
   }
+}
+
+int64_t colsum_rows_per_block(int64_t rows) {
+  int64_t r = (rows + 2047) / 2048;
+  return r < 64 ? 64 : r;
 }
 
 }  // namespace
@@ -316,7 +337,7 @@ hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t 
                            const Epilogue& epi, hipStream_t s) {
   const int64_t width = epi.mode == EPI_F32 ? epi.ldo : N;
   const int64_t total = M * width;
-  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  const int64_t blocks = (total + 63) / 64;
   if (blocks <= 0) return hipSuccess;
   switch (prec) {
     case 0: hipLaunchKernelGGL(reduce_partials_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, s, partials, splits, M, N, width, epi); break;
@@ -328,17 +349,19 @@ hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t 
 }
 
 int64_t colsum_partials_floats(int64_t rows, int64_t ld) {
-  return ((rows + COLSUM_ROWS - 1) / COLSUM_ROWS) * ld;
+  const int64_t rpb = colsum_rows_per_block(rows);
+  return ((rows + rpb - 1) / rpb) * ld;
 }
 
 hipError_t colsum(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld,
                   float* partials, float* out, int64_t ldo, int32_t* flag, hipStream_t s) {
-  const int64_t nb = (rows + COLSUM_ROWS - 1) / COLSUM_ROWS;
+  const int64_t rpb = colsum_rows_per_block(rows);
+  const int64_t nb = (rows + rpb - 1) / rpb;
   dim3 grid((unsigned)nb, (unsigned)((ldo + 63) / 64));
   switch (prec) {
-    case 0: hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, rows, cols, ld, ldo, partials); break;
-    case 1: hipLaunchKernelGGL(colsum_partial_kernel<f16>, grid, dim3(256), 0, s, (const f16*)X, rows, cols, ld, ldo, partials); break;
-    case 2: hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, rows, cols, ld, ldo, partials); break;
+    case 0: hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, rows, cols, ld, ldo, rpb, partials); break;
+    case 1: hipLaunchKernelGGL(colsum_partial_kernel<f16>, grid, dim3(256), 0, s, (const f16*)X, rows, cols, ld, ldo, rpb, partials); break;
+    case 2: hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, rows, cols, ld, ldo, rpb, partials); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();

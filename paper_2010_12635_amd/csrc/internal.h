@@ -60,6 +60,13 @@ int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F);
 hipError_t spmm_launch(const CsrView& A, int prec, const void* X, int64_t ldx, int64_t F,
                        const Epilogue& epi, float* partials, hipStream_t s);
 
+// ------------------------------------------------ dense-A_hat aggregation ----
+// Y = epilogue(A_hat X) for dense A_hat (n x lda); ws holds the padded
+// transpose of X (dense_agg_workspace_bytes).
+size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F);
+hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, int64_t n, const void* X, int64_t ldx, int64_t F,
+                            const Epilogue& epi, void* ws, hipStream_t s);
+
 // ------------------------------------------------------------ normalize ----
 size_t normalize_workspace_bytes(int64_t n, int64_t num_edges);
 hipError_t normalize_run(int64_t n, int64_t num_edges, const int32_t* src, const int32_t* dst,

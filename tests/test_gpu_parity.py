@@ -124,6 +124,8 @@ FWD_CASES = [
     (2100, 40, 130, G.GCN_ACT_RELU, 0.3, False),
     (1500, 500, 64, G.GCN_ACT_RELU, 0.5, True),
     (1500, 64, 32, G.GCN_ACT_NONE, 0.0, True),
+    (1003, 40, 7, G.GCN_ACT_NONE, 0.0, True),
+    (777, 16, 130, G.GCN_ACT_RELU, 0.5, True),
 ]
 
 
@@ -165,6 +167,7 @@ BWD_CASES = [
     (3000, 64, 7, G.GCN_ACT_RELU, 0.5, False),
     (2100, 130, 40, G.GCN_ACT_RELU, 0.3, False),
     (1500, 64, 32, G.GCN_ACT_RELU, 0.5, True),
+    (1003, 130, 7, G.GCN_ACT_RELU, 0.5, True),
 ]
 
 
