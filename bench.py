@@ -210,7 +210,7 @@ def main():
     achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
-                    kernel="dense A_hat aggregation (MFMA GEMM, K split + fixed-order reduce)",
+                    kernel="dense A_hat aggregation: transpose of X + dense_agg_kernel (A_hat in tiled MFMA operand order, 8-wave k split)",
                     launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
                     algorithmic_bytes_per_launch_avg=int(per_epoch_bytes / 2))
 

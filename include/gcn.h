@@ -67,7 +67,7 @@ typedef enum gcn_status {
 
 typedef enum gcn_precision { GCN_F32 = 0, GCN_F16 = 1, GCN_BF16 = 2 } gcn_precision;
 typedef enum gcn_index { GCN_I32 = 0, GCN_I64 = 1 } gcn_index;       /* rowptr width */
-typedef enum gcn_adj_format { GCN_CSR = 0, GCN_DENSE = 1 } gcn_adj_format;
+typedef enum gcn_adj_format { GCN_CSR = 0, GCN_DENSE = 1, GCN_DENSE_TILED = 2 } gcn_adj_format;
 typedef enum gcn_act { GCN_ACT_NONE = 0, GCN_ACT_RELU = 1 } gcn_act;
 
 /* Normalised adjacency A_hat (device arrays, caller-owned).
@@ -75,6 +75,8 @@ typedef enum gcn_act { GCN_ACT_NONE = 0, GCN_ACT_RELU = 1 } gcn_act;
  * (gcn_layer_bwd uses A_hat^T = A_hat).  values == NULL means
  * A_hat_ij = dinv[i] * dinv[j] computed on the fly.
  * DENSE: dense[i * ld_dense + j] = A_hat_ij in value_prec.
+ * DENSE_TILED: the dense matrix stored in matrix-core operand order (see
+ * gcn_densify); ld_dense is ignored.
  * The heavy-row schedule (filled by gcn_schedule) lets the CSR product split
  * rows with more than heavy_threshold entries across workgroups; with
  * n_heavy == 0 every row is processed whole. */
@@ -162,6 +164,26 @@ gcn_status gcn_normalize(int64_t n, int64_t num_edges, const int32_t* src, const
                          int32_t* deg, float* dinv, int32_t value_prec, void* values,
                          void* dense, int64_t ld_dense, int64_t* nnz_out,
                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_densify: write the dense form of a CSR A_hat (values, or dinv[i] *
+ * dinv[j] when values is NULL, rounded to value_prec) into `dense`, every
+ * other entry zero.
+ *   format GCN_DENSE:       dense[i * ld_dense + j], ld_dense >= n, % 8 == 0.
+ *   format GCN_DENSE_TILED: rows are grouped in blocks of 64, columns in
+ *     chunks of KC = 32 (16-bit) or 16 (fp32) elements; with VE = KC / 4,
+ *     element (i, j) lives at
+ *       (((i / 64) * NC + j / KC) * 4 + (i % 64) / 16) * 16 * KC
+ *       + ((j % KC) / VE * 16 + i % 16) * VE + j % VE,
+ *     NC = ceil(n / KC): each 16-row x KC-column piece is one contiguous
+ *     1 KiB block in the lane order of a 16x16 MFMA operand, and the 64 rows
+ *     of a block are contiguous along k.  Size: gcn_dense_tiled_elems().
+ *     This is the layout the dense aggregation streams at full bandwidth.
+ * Asynchronous on `stream`.
+ * ------------------------------------------------------------------------- */
+gcn_status gcn_dense_tiled_elems(int64_t n, int32_t prec, int64_t* elems);
+gcn_status gcn_densify(const gcn_adj* A, int32_t format, int32_t value_prec, void* dense, int64_t ld_dense,
+                       void* stream);
 
 /* ---------------------------------------------------------------------------
  * gcn_schedule: fill the heavy-row fields of a CSR gcn_adj (n, nnz, index,

@@ -46,11 +46,13 @@ gcn_status check_layer(const gcn_layer* L) {
 gcn_status check_adj(const gcn_adj* A, int32_t prec) {
   if (!A) return GCN_ERR_INVALID_ARG;
   if (A->n <= 0) return GCN_ERR_SHAPE;
-  if (A->format == GCN_DENSE) {
+  if (A->format == GCN_DENSE || A->format == GCN_DENSE_TILED) {
     if (!A->dense) return GCN_ERR_INVALID_ARG;
     if (A->value_prec != prec) return GCN_ERR_UNSUPPORTED;
+    if (!aligned16(A->dense)) return GCN_ERR_ALIGNMENT;
+    if (A->format == GCN_DENSE_TILED) return GCN_OK;
     if (A->ld_dense < A->n) return GCN_ERR_SHAPE;
-    if (A->ld_dense % 8 || !aligned16(A->dense)) return GCN_ERR_ALIGNMENT;
+    if (A->ld_dense % 8) return GCN_ERR_ALIGNMENT;
     return GCN_OK;
   }
   if (A->format != GCN_CSR) return GCN_ERR_INVALID_ARG;
@@ -101,7 +103,7 @@ LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
   if (p.s_split > 1) upd(p.s_split * n * L->f_out);
   if (p.dh_split > 1) upd(p.dh_split * n * L->f_in);
   upd(p.dw_split * L->f_in * L->f_out);
-  if (A->format == GCN_DENSE) {
+  if (A->format != GCN_CSR) {
     upd((int64_t)(dense_agg_workspace_bytes(prec, n, L->f_out) / sizeof(float)) + 1);
   } else {
     upd(spmm_partials_floats(view_of(A), prec, L->f_out));
@@ -137,13 +139,14 @@ hipError_t run_gemm(int32_t prec, bool akc, bool bkc, const void* A, int64_t lda
 hipError_t aggregate(const gcn_adj* A, int32_t prec, const void* X, int64_t ldx, int64_t F, int split,
                      const Epilogue& epi, float* ws, hipStream_t s) {
   (void)split;
-  if (A->format == GCN_DENSE) return dense_agg_launch(prec, A->dense, A->ld_dense, A->n, X, ldx, F, epi, ws, s);
+  if (A->format != GCN_CSR)
+    return dense_agg_launch(prec, A->dense, A->ld_dense, A->format == GCN_DENSE_TILED, A->n, X, ldx, F, epi, ws, s);
   return spmm_launch(view_of(A), prec, X, ldx, F, epi, ws, s);
 }
 
 size_t aggregate_bytes(const gcn_adj* A, int32_t prec, int64_t F) {
   int64_t f = 0;
-  if (A->format == GCN_DENSE) {
+  if (A->format != GCN_CSR) {
     f = (int64_t)(dense_agg_workspace_bytes(prec, A->n, F) / sizeof(float)) + 1;
   } else {
     f = spmm_partials_floats(view_of(A), prec, F);
@@ -223,6 +226,29 @@ gcn_status gcn_normalize(int64_t n, int64_t num_edges, const int32_t* src, const
   if (e != hipSuccess) return GCN_ERR_DEVICE;
   if (bad) return GCN_ERR_GRAPH;
   *nnz_out = nnz;
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_dense_tiled_elems(int64_t n, int32_t prec, int64_t* elems) {
+  if (!elems || !valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  if (n <= 0) return GCN_ERR_SHAPE;
+  *elems = dense_tiled_elems(prec, n);
+  return GCN_OK;
+}
+
+gcn_status gcn_densify(const gcn_adj* A, int32_t format, int32_t value_prec, void* dense, int64_t ld_dense,
+                       void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!A || !dense || !valid_prec(value_prec)) return GCN_ERR_INVALID_ARG;
+  if (A->format != GCN_CSR || (format != GCN_DENSE && format != GCN_DENSE_TILED)) return GCN_ERR_INVALID_ARG;
+  gcn_status st = check_adj(A, value_prec);
+  if (st != GCN_OK) return st;
+  if (!aligned16(dense)) return GCN_ERR_ALIGNMENT;
+  if (format == GCN_DENSE) {
+    if (ld_dense < A->n) return GCN_ERR_SHAPE;
+    if (ld_dense % 8) return GCN_ERR_ALIGNMENT;
+  }
+  GCN_HIP(densify_launch(view_of(A), value_prec, format == GCN_DENSE_TILED, dense, ld_dense, s));
   return finish(hipSuccess, s);
 }
 

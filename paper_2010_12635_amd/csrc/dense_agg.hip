@@ -4,18 +4,21 @@
 // product is bound by streaming A_hat from HBM (s * n^2 bytes against
 // 2 * n^2 * F flops), so the kernel is built around that stream:
 //
-//  * X is first transposed into Xt (Fp x ldt, Fp = F rounded up to 16,
-//    zero-padded), so that both MFMA operands are k-contiguous and every
-//    operand fragment is one 16-byte global load: A_hat rows come straight
-//    from HBM into registers, Xt (a few MB) is served from L2.
-//  * A workgroup owns 64 rows and all (up to 64) columns; its 8 waves split
-//    the k range in 8 contiguous parts, each keeping its partial 64 x Fp
-//    tile in MFMA accumulators, with a 3-deep register ring of loads in
-//    flight.  No global partial sums, one launch.
+//  * Operand order.  MFMA 16x16 operands take, in lane l, 16 bytes of row
+//    l % 16 at k-group l / 16.  In the tiled layout every 16-row x KC-column
+//    piece (KC = 4 x 16 bytes of k) is one contiguous 1 KiB block in exactly
+//    that lane order, and the four 16-row pieces of a 64-row block follow
+//    each other, so each operand load is one contiguous 1 KiB and a wave's
+//    k range is one contiguous stream (row-major rows give 16 short runs per
+//    load, which measured far below the stream rate on MI355X).
+//    X is transposed into the same tiled layout (Xt) before the product.
+//  * A workgroup owns 64 rows and a 64-column block; its 8 waves split the
+//    k range in 8 contiguous parts, each keeping its partial 64 x 64 tile in
+//    MFMA accumulators, with a 3-deep register ring of loads in flight.
 //  * The 8 partial tiles are summed through LDS in a fixed order (wave w
 //    adds wave w + 4, then the four sums are added in wave order), then the
 //    fused epilogue (bias, ReLU, dropout, cast, overflow flag) stores
-//    16-byte vectors row by row.
+//    16-byte vectors row by row.  No global partial sums, one launch.
 #include "internal.h"
 
 namespace gcn {
@@ -26,21 +29,43 @@ constexpr int DA_BM = 64;     // rows per workgroup
 constexpr int DA_BN = 64;     // columns per workgroup (column block of Xt)
 constexpr int DA_WAVES = 8;   // waves per workgroup, one k range each
 
-// Xt[f][k] = X[k][f] for f < F, k < n; zero for F <= f < Fp or n <= k < ldt.
+// Tiled offset (elements) of entry (i, j) of an R x K matrix in operand
+// order: 64-row blocks, KC-column chunks, 16-row pieces of 1 KiB.
 template <typename T>
-__global__ __launch_bounds__(256) void transpose_pad_kernel(const T* __restrict__ X, int64_t ldx, int64_t n, int64_t F,
-                                                            T* __restrict__ Xt, int64_t ldt, int64_t Fp) {
-  __shared__ T tile[64][65];
+__host__ __device__ __forceinline__ int64_t tiled_off(int64_t i, int64_t j, int64_t nc) {
+  constexpr int VE = Vec<T>::N, KC = 4 * VE;
+  return (((i / 64) * nc + j / KC) * 4 + (i % 64) / 16) * (16 * KC) + ((j % KC) / VE * 16 + i % 16) * VE + j % VE;
+}
+template <typename T> constexpr int tile_kc() { return 4 * Vec<T>::N; }
+
+// Xt = tiled(X^T): X is n x F (ldx); Xt has ceil(F / 64) * 64 rows and
+// nc * KC columns; entries outside F x n are zero.  One workgroup converts a
+// 64 (features) x 64 (vertices) tile through LDS; its output is contiguous.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_tiled_kernel(const T* __restrict__ X, int64_t ldx, int64_t n, int64_t F,
+                                                              T* __restrict__ Xt, int64_t nc) {
+  constexpr int VE = Vec<T>::N, KC = 4 * VE;
+  __shared__ T tile[64][65];                    // [k - k0][f - f0]
   const int64_t k0 = (int64_t)blockIdx.x * 64, f0 = (int64_t)blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;   // 64 x 4
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int r = ty; r < 64; r += 4) {
     const int64_t k = k0 + r, f = f0 + tx;
     tile[r][tx] = (k < n && f < F) ? X[k * ldx + f] : T(0);
   }
   __syncthreads();
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t f = f0 + r, k = k0 + tx;
-    if (f < Fp && k < ldt) Xt[f * ldt + k] = tile[tx][r];
+  // the 64 x 64 tile covers chunks k0/KC .. k0/KC + 64/KC - 1 of row block
+  // f0/64: a contiguous run of (64 / KC) * 4 * 16 * KC elements
+  constexpr int TILE_ELEMS = 64 * 64;
+  const int64_t base = tiled_off<T>(f0, k0, nc);
+  for (int o = threadIdx.x; o < TILE_ELEMS; o += 256) {
+    const int cl = o / (4 * 16 * KC);             // chunk within the tile
+    const int rem = o % (4 * 16 * KC);
+    const int tn = rem / (16 * KC);
+    const int q = rem % (16 * KC);
+    const int g = q / (16 * VE), cc = (q / VE) % 16, e = q % VE;
+    const int64_t c = k0 / KC + cl;
+    if (c >= nc) continue;
+    Xt[base + o] = tile[cl * KC + g * VE + e][tn * 16 + cc];
   }
 }
 
@@ -80,34 +105,46 @@ struct Frag {
   uint4 b[TN];
 };
 
-template <typename T, int TN>
+// In chunk c lane group g (= lane / 16) holds k = c * KC + g * VE + [0, VE)
+// of A_hat and of Xt alike, so the MFMA sums over exactly the same k.
+template <typename T, int TN, bool TILED>
 __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
   constexpr int VE = Vec<T>::N;
   constexpr int KC = 4 * VE;                 // k per chunk: 32 (16-bit) / 16 (fp32)
+  constexpr int PIECE = 16 * KC;             // elements of one 16-row piece (1 KiB)
   constexpr int LDR = DA_BN + 4;             // LDS row stride (floats)
   __shared__ float red[4][DA_BM * LDR];
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t m0 = (int64_t)blockIdx.x * DA_BM;
   const int64_t c0 = (int64_t)blockIdx.y * DA_BN;
+  const int64_t nc = (p.n + KC - 1) / KC;
   const T* __restrict__ A = reinterpret_cast<const T*>(p.A);
   const T* __restrict__ Xt = reinterpret_cast<const T*>(p.Xt);
 
-  // rows beyond n read row n-1 (their results are never stored)
-  const T* arow[4];
+  // Operand base pointers; fragment (chunk c, tile t) is at base + c * step + t * tstep.
+  const T* abase[4];
+  int64_t astep;
+  if (TILED) {
+    const T* blk = A + (int64_t)blockIdx.x * nc * 4 * PIECE + lane * VE;
 #pragma unroll
-  for (int tm = 0; tm < 4; ++tm) {
-    int64_t r = m0 + tm * 16 + (lane & 15);
-    if (r >= p.n) r = p.n - 1;
-    arow[tm] = A + r * p.lda + (lane >> 4) * VE;
+    for (int tm = 0; tm < 4; ++tm) abase[tm] = blk + tm * PIECE;
+    astep = 4 * PIECE;
+  } else {
+    // rows beyond n read row n-1 (their results are never stored)
+#pragma unroll
+    for (int tm = 0; tm < 4; ++tm) {
+      int64_t r = m0 + tm * 16 + (lane & 15);
+      if (r >= p.n) r = p.n - 1;
+      abase[tm] = A + r * p.lda + (lane >> 4) * VE;
+    }
+    astep = KC;
   }
-  const T* brow[TN];
-#pragma unroll
-  for (int tn = 0; tn < TN; ++tn) brow[tn] = Xt + (c0 + tn * 16 + (lane & 15)) * p.ldt + (lane >> 4) * VE;
+  const T* bbase = Xt + (int64_t)blockIdx.y * nc * 4 * PIECE + lane * VE;
 
-  const int64_t chunks = (p.n + KC - 1) / KC;
-  const int64_t cb = chunks * wave / DA_WAVES, ce = chunks * (wave + 1) / DA_WAVES;
-  const int64_t full_end = min(ce, p.n / KC);   // chunks entirely below n
+  const int64_t cb = nc * wave / DA_WAVES, ce = nc * (wave + 1) / DA_WAVES;
+  const int64_t full_end = TILED ? ce : min(ce, p.n / KC);   // chunks needing no mask
 
   f32x4 acc[4][TN];
 #pragma unroll
@@ -116,11 +153,10 @@ __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto load = [&](Frag<TN>& f, int64_t c) {
-    const int64_t k = c * KC;
 #pragma unroll
-    for (int tm = 0; tm < 4; ++tm) f.a[tm] = ldg16(arow[tm] + k);
+    for (int tm = 0; tm < 4; ++tm) f.a[tm] = ldg16(abase[tm] + c * astep);
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) f.b[tn] = ldg16(brow[tn] + k);
+    for (int tn = 0; tn < TN; ++tn) f.b[tn] = ldg16(bbase + c * 4 * PIECE + tn * PIECE);
   };
   auto compute = [&](const Frag<TN>& f) {
 #pragma unroll
@@ -128,19 +164,22 @@ __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = DaMfma<T>::run(f.a[tm], f.b[tn], acc[tm][tn]);
   };
+  // keep the scheduler from moving MFMAs ahead of the loads issued before them
+#define DA_FENCE() __builtin_amdgcn_sched_barrier(0)
 
-  // full chunks: 4-deep ring of fragments (3 loads in flight while computing)
+  // full chunks: 4-deep ring of fragments (3 chunks in flight while computing)
   Frag<TN> f0, f1, f2, f3;
   int64_t c = cb;
   if (c + 3 <= full_end) {
     load(f0, c);
     load(f1, c + 1);
     load(f2, c + 2);
+    DA_FENCE();
     for (; c + 7 <= full_end; c += 4) {
-      load(f3, c + 3); compute(f0);
-      load(f0, c + 4); compute(f1);
-      load(f1, c + 5); compute(f2);
-      load(f2, c + 6); compute(f3);
+      load(f3, c + 3); DA_FENCE(); compute(f0); DA_FENCE();
+      load(f0, c + 4); DA_FENCE(); compute(f1); DA_FENCE();
+      load(f1, c + 5); DA_FENCE(); compute(f2); DA_FENCE();
+      load(f2, c + 6); DA_FENCE(); compute(f3); DA_FENCE();
     }
     // drain: f0, f1, f2 hold chunks c, c+1, c+2
     compute(f0);
@@ -152,17 +191,17 @@ __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
     load(f0, c);
     compute(f0);
   }
-  // the chunk that straddles n (only in the last wave's range): mask k >= n
-  if (c < ce) {
-    const int64_t k = c * KC;
-    const int64_t kl = k + (lane >> 4) * VE;   // first k of this lane's vector
+#undef DA_FENCE
+  // row-major A_hat only: the chunk that straddles n (last wave): mask k >= n
+  if (!TILED && c < ce) {
+    const int64_t kl = c * KC + (lane >> 4) * VE;   // first k of this lane's vector
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) f0.b[tn] = ldg16(brow[tn] + k);   // Xt is zero-padded to ldt
+    for (int tn = 0; tn < TN; ++tn) f0.b[tn] = ldg16(bbase + c * 4 * PIECE + tn * PIECE);   // Xt is zero-padded
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm) {
-      // a vector starting below n ends inside the row (lda >= n rounded up to 8);
-      // one starting at or beyond n is not loaded at all
-      f0.a[tm] = kl < p.n ? ldg16(arow[tm] + k) : make_uint4(0, 0, 0, 0);
+      // a vector starting below n ends inside the row (lda >= n rounded up
+      // to 8); one starting at or beyond n is not loaded at all
+      f0.a[tm] = kl < p.n ? ldg16(abase[tm] + c * astep) : make_uint4(0, 0, 0, 0);
       T* e = reinterpret_cast<T*>(&f0.a[tm]);
 #pragma unroll
       for (int j = 0; j < VE; ++j)
@@ -224,26 +263,76 @@ __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
   }
 }
 
+int64_t xt_elems(int prec, int64_t n, int64_t F) {
+  const int64_t kc = prec == 0 ? 16 : 32;
+  const int64_t nc = (n + kc - 1) / kc;
+  return ((F + 63) / 64) * 64 * nc * kc;
+}
+
 template <typename T>
-hipError_t launch_t(const void* A, int64_t lda, int64_t n, const void* X, int64_t ldx, int64_t F,
+hipError_t launch_t(const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx, int64_t F,
                     const Epilogue& epi, void* ws, hipStream_t s) {
-  const int64_t Fp = F <= DA_BN ? (F + 15) / 16 * 16 : (F + DA_BN - 1) / DA_BN * DA_BN;
-  const int64_t ldt = (n + 63) / 64 * 64;
+  constexpr int KC = tile_kc<T>();
+  const int64_t nc = (n + KC - 1) / KC;
+  const int64_t fblocks = (F + 63) / 64;
   T* Xt = reinterpret_cast<T*>(ws);
-  dim3 tg((unsigned)(ldt / 64), (unsigned)((Fp + 63) / 64));
-  hipLaunchKernelGGL(transpose_pad_kernel<T>, tg, dim3(256), 0, s, reinterpret_cast<const T*>(X), ldx, n, F, Xt,
-                     ldt, Fp);
+  dim3 tg((unsigned)((n + 63) / 64), (unsigned)fblocks);
+  hipLaunchKernelGGL(transpose_tiled_kernel<T>, tg, dim3(256), 0, s, reinterpret_cast<const T*>(X), ldx, n, F, Xt, nc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   DaParams p;
-  p.A = A; p.lda = lda; p.Xt = Xt; p.ldt = ldt; p.n = n; p.F = F; p.epi = epi;
-  dim3 grid((unsigned)((n + DA_BM - 1) / DA_BM), (unsigned)((Fp + DA_BN - 1) / DA_BN));
-  const int tn = Fp >= 64 ? 4 : (int)(Fp / 16);
+  p.A = A; p.lda = lda; p.Xt = Xt; p.ldt = 0; p.n = n; p.F = F; p.epi = epi;
+  dim3 grid((unsigned)((n + DA_BM - 1) / DA_BM), (unsigned)fblocks);
+  const int tn = F > 48 ? 4 : (int)((F + 15) / 16);
+  const dim3 blk(64 * DA_WAVES);
+#define DA_LAUNCH(TN_)                                                                          \
+  if (tiled) hipLaunchKernelGGL((dense_agg_kernel<T, TN_, true>), grid, blk, 0, s, p);          \
+  else hipLaunchKernelGGL((dense_agg_kernel<T, TN_, false>), grid, blk, 0, s, p);
   switch (tn) {
-    case 1: hipLaunchKernelGGL((dense_agg_kernel<T, 1>), grid, dim3(64 * DA_WAVES), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((dense_agg_kernel<T, 2>), grid, dim3(64 * DA_WAVES), 0, s, p); break;
-    case 3: hipLaunchKernelGGL((dense_agg_kernel<T, 3>), grid, dim3(64 * DA_WAVES), 0, s, p); break;
-    default: hipLaunchKernelGGL((dense_agg_kernel<T, 4>), grid, dim3(64 * DA_WAVES), 0, s, p); break;
+    case 1: DA_LAUNCH(1) break;
+    case 2: DA_LAUNCH(2) break;
+    case 3: DA_LAUNCH(3) break;
+    default: DA_LAUNCH(4) break;
+  }
+#undef DA_LAUNCH
+  return hipGetLastError();
+}
+
+// Dense form of a CSR A_hat: one wave per row scatters its entries.
+template <typename T, typename IdxT, bool TILED>
+__global__ __launch_bounds__(256) void densify_kernel(int64_t n, const IdxT* __restrict__ rowptr,
+                                                      const int32_t* __restrict__ colidx, const T* __restrict__ values,
+                                                      const float* __restrict__ dinv, T* __restrict__ dense,
+                                                      int64_t ld, int64_t nc) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= n) return;
+  const float dr = values ? 0.f : dinv[r];
+  for (int64_t k = (int64_t)rowptr[r] + lane; k < (int64_t)rowptr[r + 1]; k += 64) {
+    const int32_t c = colidx[k];
+    const T v = values ? values[k] : from_f32<T>(dr * dinv[c]);
+    dense[TILED ? tiled_off<T>(r, c, nc) : r * ld + c] = v;
+  }
+}
+
+template <typename T>
+hipError_t densify_t(const CsrView& A, bool tiled, void* dense, int64_t ld, hipStream_t s) {
+  constexpr int KC = tile_kc<T>();
+  const int64_t nc = (A.n + KC - 1) / KC;
+  const size_t bytes = tiled ? (size_t)((A.n + 63) / 64) * 64 * nc * KC * sizeof(T) : (size_t)A.n * ld * sizeof(T);
+  hipError_t e = fill_zero(dense, bytes, s);
+  if (e != hipSuccess) return e;
+  const dim3 g((unsigned)((A.n + 3) / 4));
+  const T* vals = reinterpret_cast<const T*>(A.values);
+  T* d = reinterpret_cast<T*>(dense);
+  if (A.idx64) {
+    const int64_t* rp = reinterpret_cast<const int64_t*>(A.rowptr);
+    if (tiled) hipLaunchKernelGGL((densify_kernel<T, int64_t, true>), g, dim3(256), 0, s, A.n, rp, A.colidx, vals, A.dinv, d, ld, nc);
+    else hipLaunchKernelGGL((densify_kernel<T, int64_t, false>), g, dim3(256), 0, s, A.n, rp, A.colidx, vals, A.dinv, d, ld, nc);
+  } else {
+    const int32_t* rp = reinterpret_cast<const int32_t*>(A.rowptr);
+    if (tiled) hipLaunchKernelGGL((densify_kernel<T, int32_t, true>), g, dim3(256), 0, s, A.n, rp, A.colidx, vals, A.dinv, d, ld, nc);
+    else hipLaunchKernelGGL((densify_kernel<T, int32_t, false>), g, dim3(256), 0, s, A.n, rp, A.colidx, vals, A.dinv, d, ld, nc);
   }
   return hipGetLastError();
 }
@@ -251,17 +340,29 @@ hipError_t launch_t(const void* A, int64_t lda, int64_t n, const void* X, int64_
 }  // namespace
 
 size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F) {
-  const int64_t Fp = F <= DA_BN ? (F + 15) / 16 * 16 : (F + DA_BN - 1) / DA_BN * DA_BN;
-  const int64_t ldt = (n + 63) / 64 * 64;
-  return (size_t)Fp * (size_t)ldt * (prec == 0 ? 4 : 2);
+  return (size_t)xt_elems(prec, n, F) * (prec == 0 ? 4 : 2);
 }
 
-hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, int64_t n, const void* X, int64_t ldx, int64_t F,
-                            const Epilogue& epi, void* ws, hipStream_t s) {
+int64_t dense_tiled_elems(int prec, int64_t n) {
+  const int64_t kc = prec == 0 ? 16 : 32;
+  return ((n + 63) / 64) * 64 * ((n + kc - 1) / kc) * kc;
+}
+
+hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx,
+                            int64_t F, const Epilogue& epi, void* ws, hipStream_t s) {
   switch (prec) {
-    case 0: return launch_t<float>(A, lda, n, X, ldx, F, epi, ws, s);
-    case 1: return launch_t<f16>(A, lda, n, X, ldx, F, epi, ws, s);
-    case 2: return launch_t<bf16>(A, lda, n, X, ldx, F, epi, ws, s);
+    case 0: return launch_t<float>(A, lda, tiled, n, X, ldx, F, epi, ws, s);
+    case 1: return launch_t<f16>(A, lda, tiled, n, X, ldx, F, epi, ws, s);
+    case 2: return launch_t<bf16>(A, lda, tiled, n, X, ldx, F, epi, ws, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t densify_launch(const CsrView& A, int prec, bool tiled, void* dense, int64_t ld, hipStream_t s) {
+  switch (prec) {
+    case 0: return densify_t<float>(A, tiled, dense, ld, s);
+    case 1: return densify_t<f16>(A, tiled, dense, ld, s);
+    case 2: return densify_t<bf16>(A, tiled, dense, ld, s);
   }
   return hipErrorInvalidValue;
 }

@@ -64,8 +64,12 @@ hipError_t spmm_launch(const CsrView& A, int prec, const void* X, int64_t ldx, i
 // Y = epilogue(A_hat X) for dense A_hat (n x lda); ws holds the padded
 // transpose of X (dense_agg_workspace_bytes).
 size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F);
-hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, int64_t n, const void* X, int64_t ldx, int64_t F,
-                            const Epilogue& epi, void* ws, hipStream_t s);
+hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx,
+                            int64_t F, const Epilogue& epi, void* ws, hipStream_t s);
+// Elements of the tiled dense A_hat (rows padded to 64, columns to the chunk).
+int64_t dense_tiled_elems(int prec, int64_t n);
+// Dense A_hat from CSR: row-major (ld) or tiled operand order.
+hipError_t densify_launch(const CsrView& A, int prec, bool tiled, void* dense, int64_t ld, hipStream_t s);
 
 // ------------------------------------------------------------ normalize ----
 size_t normalize_workspace_bytes(int64_t n, int64_t num_edges);

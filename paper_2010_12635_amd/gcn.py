@@ -15,7 +15,7 @@ import torch
 
 __all__ = [
     "GCN_F32", "GCN_F16", "GCN_BF16", "GCN_I32", "GCN_I64", "GCN_CSR", "GCN_DENSE",
-    "GCN_ACT_NONE", "GCN_ACT_RELU", "GcnError", "GcnAdj", "GcnLayer", "GcnScaler",
+    "GCN_ACT_NONE", "GCN_ACT_RELU", "GCN_DENSE_TILED", "gcn_dense_tiled_elems", "gcn_densify", "GcnError", "GcnAdj", "GcnLayer", "GcnScaler",
     "GcnAdamConfig", "lib", "LIB_PATH", "EXPORTED", "torch_dtype",
     "gcn_status_string", "gcn_abi_version", "gcn_normalize_workspace_size", "gcn_normalize",
     "gcn_schedule_size", "gcn_schedule", "gcn_layer_workspace_size", "gcn_layer_fwd",
@@ -25,7 +25,7 @@ __all__ = [
 
 GCN_F32, GCN_F16, GCN_BF16 = 0, 1, 2
 GCN_I32, GCN_I64 = 0, 1
-GCN_CSR, GCN_DENSE = 0, 1
+GCN_CSR, GCN_DENSE, GCN_DENSE_TILED = 0, 1, 2
 GCN_ACT_NONE, GCN_ACT_RELU = 0, 1
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgcn.so")
@@ -36,6 +36,7 @@ EXPORTED = (
     "gcn_schedule_size", "gcn_schedule", "gcn_layer_workspace_size", "gcn_layer_fwd",
     "gcn_layer_bwd", "gcn_loss_workspace_size", "gcn_loss", "gcn_optimizer_step",
     "gcn_transform_workspace_size", "gcn_transform", "gcn_aggregate_workspace_size", "gcn_aggregate",
+    "gcn_dense_tiled_elems", "gcn_densify",
 )
 
 _DTYPES = {GCN_F32: torch.float32, GCN_F16: torch.float16, GCN_BF16: torch.bfloat16}
@@ -121,6 +122,8 @@ def lib():
         "gcn_transform_workspace_size": (I32, [I64, I64, I64, I32, PSZ]),
         "gcn_transform": (I32, [I64, I64, I64, I32, P, I64, P, I64, P, I64, P, P, SZ, P]),
         "gcn_aggregate_workspace_size": (I32, [PADJ, I64, I32, PSZ]),
+        "gcn_dense_tiled_elems": (I32, [I64, I32, PI64]),
+        "gcn_densify": (I32, [PADJ, I32, I32, P, I64, P]),
         "gcn_aggregate": (I32, [PADJ, I64, I32, P, I64, P, I32, ctypes.c_float, I32, ctypes.c_uint64, I32,
                                 ctypes.c_uint64, P, I64, P, P, SZ, P]),
     }
@@ -262,3 +265,14 @@ def gcn_aggregate(adj, F, prec, X, ldx, bias, act, dropout_p, training, seed, la
                              _ptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),
                              _stream(stream))
     _check(st, "gcn_aggregate")
+
+
+def gcn_dense_tiled_elems(n, prec) -> int:
+    e = ctypes.c_int64(0)
+    _check(lib().gcn_dense_tiled_elems(n, prec, ctypes.byref(e)), "gcn_dense_tiled_elems")
+    return e.value
+
+
+def gcn_densify(adj, fmt, value_prec, dense, ld_dense, stream=None):
+    _check(lib().gcn_densify(ctypes.byref(adj), fmt, value_prec, _ptr(dense), ld_dense, _stream(stream)),
+           "gcn_densify")

@@ -31,7 +31,9 @@ class DeviceGraph:
     """A_hat on the device, built by gcn_normalize (+ gcn_schedule for CSR)."""
 
     def __init__(self, n, src, dst, prec=G.GCN_F16, index=G.GCN_I32, dense=False, values=True,
-                 schedule=True, device="cuda", heavy_threshold=0, chunk_nnz=0, stream=None):
+                 schedule=True, device="cuda", heavy_threshold=0, chunk_nnz=0, stream=None, tiled=None):
+        """dense=True stores A_hat densely: in the tiled operand order by
+        default (tiled=None or True), row-major when tiled=False."""
         self.n = int(n)
         self.prec = prec
         dev = torch.device(device)
@@ -45,27 +47,37 @@ class DeviceGraph:
         self.deg = torch.empty(self.n, dtype=torch.int32, device=dev)
         self.dinv = torch.empty(self.n, dtype=torch.float32, device=dev)
         vdt = G.torch_dtype(prec)
+        self.tiled = bool(dense) and (tiled is None or tiled)
         self.values = torch.empty(cap, dtype=vdt, device=dev) if (values and not dense) else None
-        self.ld_dense = round8(self.n) if dense else 0
-        self.dense = torch.empty((self.n, self.ld_dense), dtype=vdt, device=dev) if dense else None
+        self.ld_dense = round8(self.n) if (dense and not self.tiled) else 0
+        if not dense:
+            self.dense = None
+        elif self.tiled:
+            self.dense = torch.empty(G.gcn_dense_tiled_elems(self.n, prec), dtype=vdt, device=dev)
+        else:
+            self.dense = torch.empty((self.n, self.ld_dense), dtype=vdt, device=dev)
         ws = torch.empty(G.gcn_normalize_workspace_size(self.n, ne), dtype=torch.uint8, device=dev)
         self.nnz = G.gcn_normalize(self.n, src_t if ne else None, dst_t if ne else None, index, self.rowptr,
-                                   self.colidx, self.deg, self.dinv, prec, self.values, self.dense,
-                                   self.ld_dense, ws, stream)
+                                   self.colidx, self.deg, self.dinv, prec, self.values,
+                                   None if self.tiled else self.dense, self.ld_dense, ws, stream)
         del ws, src_t, dst_t
         self.adj = G.GcnAdj()
         a = self.adj
         a.n = self.n
         a.nnz = self.nnz
-        a.format = G.GCN_DENSE if dense else G.GCN_CSR
+        a.format = G.GCN_CSR
         a.index = index
         a.value_prec = prec
         a.rowptr = self.rowptr.data_ptr()
         a.colidx = self.colidx.data_ptr()
         a.values = self.values.data_ptr() if self.values is not None else None
         a.dinv = self.dinv.data_ptr()
-        a.dense = self.dense.data_ptr() if dense else None
-        a.ld_dense = self.ld_dense
+        if self.tiled:   # the CSR (values from dinv) is the source of the tiled copy
+            G.gcn_densify(a, G.GCN_DENSE_TILED, prec, self.dense, 0, stream)
+        if dense:
+            a.format = G.GCN_DENSE_TILED if self.tiled else G.GCN_DENSE
+            a.dense = self.dense.data_ptr()
+            a.ld_dense = self.ld_dense
         self.sched = None
         if schedule and not dense:
             nbytes = G.gcn_schedule_size(self.n, self.nnz, heavy_threshold, chunk_nnz)

@@ -63,14 +63,33 @@ def test_normalize_bit_exact(index):
     assert np.array_equal(dg2.csr_host()[1], ci)
 
 
-@pytest.mark.parametrize("prec", [G.GCN_F16, G.GCN_F32])
-def test_normalize_dense(prec):
+def untile(flat, n, prec):
+    """Row-major n x n from the tiled operand layout documented in gcn.h."""
+    kc = 16 if prec == G.GCN_F32 else 32
+    ve = kc // 4
+    nc = (n + kc - 1) // kc
+    i = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    off = (((i // 64) * nc + j // kc) * 4 + (i % 64) // 16) * (16 * kc) + ((j % kc) // ve * 16 + i % 16) * ve + j % ve
+    assert flat.size == ((n + 63) // 64) * 64 * nc * kc
+    return flat[off]
+
+
+@pytest.mark.parametrize("prec", [G.GCN_F16, G.GCN_F32, G.GCN_BF16], ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("tiled", [False, True], ids=["rowmajor", "tiled"])
+def test_normalize_dense(prec, tiled):
     n = 700
     src, dst = hub_graph(n, 3000, [(3, 300)], seed=2)
     g = O.graph(n, src, dst)
-    dg = DeviceGraph(n, src, dst, prec=prec, dense=True)
+    dg = DeviceGraph(n, src, dst, prec=prec, dense=True, tiled=tiled)
     want = O.dense_adj(g)
-    got = dg.dense[:, :n].float().cpu().numpy().astype(np.float64)
+    if tiled:
+        flat = dg.dense.float().cpu().numpy().astype(np.float64)
+        got = untile(flat, n, prec)
+        # padding entries (outside n x n) are zero
+        assert np.count_nonzero(flat) == np.count_nonzero(got)
+    else:
+        got = dg.dense[:, :n].float().cpu().numpy().astype(np.float64)
     assert np.array_equal(got != 0, want != 0)
     assert_close(got, want, prec, "dense A_hat")
 
@@ -118,23 +137,32 @@ def _layer_case(n, f_in, f_out, seed, hubs=True):
 
 
 FWD_CASES = [
-    # (n, f_in, f_out, act, p, dense)
-    (3000, 500, 64, G.GCN_ACT_RELU, 0.5, False),
-    (3000, 128, 7, G.GCN_ACT_NONE, 0.0, False),
-    (2100, 40, 130, G.GCN_ACT_RELU, 0.3, False),
-    (1500, 500, 64, G.GCN_ACT_RELU, 0.5, True),
-    (1500, 64, 32, G.GCN_ACT_NONE, 0.0, True),
-    (1003, 40, 7, G.GCN_ACT_NONE, 0.0, True),
-    (777, 16, 130, G.GCN_ACT_RELU, 0.5, True),
+    # (n, f_in, f_out, act, p, adjacency storage)
+    (3000, 500, 64, G.GCN_ACT_RELU, 0.5, "csr"),
+    (3000, 128, 7, G.GCN_ACT_NONE, 0.0, "csr"),
+    (2100, 40, 130, G.GCN_ACT_RELU, 0.3, "csr"),
+    (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "tiled"),
+    (1500, 64, 32, G.GCN_ACT_NONE, 0.0, "tiled"),
+    (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "tiled"),
+    (777, 16, 130, G.GCN_ACT_RELU, 0.5, "tiled"),
+    (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "dense"),
+    (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "dense"),
+    (777, 16, 130, G.GCN_ACT_RELU, 0.5, "dense"),
 ]
 
 
+def _graph_for(n, src, dst, prec, storage):
+    return DeviceGraph(n, src, dst, prec=prec, dense=storage != "csr", tiled=storage == "tiled",
+                       heavy_threshold=48, chunk_nnz=96)
+
+
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
-@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_act{c[3]}_p{c[4]}_{'dense' if c[5] else 'csr'}")
+@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_act{c[3]}_p{c[4]}_{c[5]}")
 def test_layer_fwd(prec, case):
-    n, f_in, f_out, act, p, dense = case
+    n, f_in, f_out, act, p, storage = case
+    dense = storage != "csr"
     g, src, dst, h, w, b = _layer_case(n, f_in, f_out, seed=n + f_in)
-    dg = DeviceGraph(n, src, dst, prec=prec, dense=dense, heavy_threshold=48, chunk_nnz=96)
+    dg = _graph_for(n, src, dst, prec, storage)
     L = G.GcnLayer(f_in, f_out, round8(f_in), round8(f_out), act, p, 3, 0)
     H, W = to_dev(h, prec), to_dev(w, prec, round8(f_out))
     bias = torch.as_tensor(b).to(dev())
@@ -163,24 +191,26 @@ def test_layer_fwd(prec, case):
 # ------------------------------------------------------------ layer bwd ----
 
 BWD_CASES = [
-    (3000, 500, 64, G.GCN_ACT_NONE, 0.0, False),
-    (3000, 64, 7, G.GCN_ACT_RELU, 0.5, False),
-    (2100, 130, 40, G.GCN_ACT_RELU, 0.3, False),
-    (1500, 64, 32, G.GCN_ACT_RELU, 0.5, True),
-    (1003, 130, 7, G.GCN_ACT_RELU, 0.5, True),
+    (3000, 500, 64, G.GCN_ACT_NONE, 0.0, "csr"),
+    (3000, 64, 7, G.GCN_ACT_RELU, 0.5, "csr"),
+    (2100, 130, 40, G.GCN_ACT_RELU, 0.3, "csr"),
+    (1500, 64, 32, G.GCN_ACT_RELU, 0.5, "tiled"),
+    (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "tiled"),
+    (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "dense"),
 ]
 
 
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
-@pytest.mark.parametrize("case", BWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_below{c[3]}_p{c[4]}_{'dense' if c[5] else 'csr'}")
+@pytest.mark.parametrize("case", BWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_below{c[3]}_p{c[4]}_{c[5]}")
 def test_layer_bwd(prec, case):
-    n, f_in, f_out, act_below, p, dense = case
+    n, f_in, f_out, act_below, p, storage = case
+    dense = storage != "csr"
     g, src, dst, h, w, _ = _layer_case(n, f_in, f_out, seed=7 * n + f_out)
     rng = np.random.default_rng(n)
     if act_below == G.GCN_ACT_RELU:   # H as produced by ReLU + dropout: exact zeros
         h = np.where(rng.random(h.shape) < 0.5, 0.0, np.abs(h) * 2).astype(np.float32)
     dz = (rng.standard_normal((n, f_out)) * 8.0).astype(np.float32)
-    dg = DeviceGraph(n, src, dst, prec=prec, dense=dense, heavy_threshold=48, chunk_nnz=96)
+    dg = _graph_for(n, src, dst, prec, storage)
     L = G.GcnLayer(f_in, f_out, round8(f_in), round8(f_out), G.GCN_ACT_NONE, 0.0, 0, 0)
     H, W, dZ = to_dev(h, prec), to_dev(w, prec, round8(f_out)), to_dev(dz, prec)
     dW = torch.full((f_in, round8(f_out)), 7.0, dtype=torch.float32, device=dev())
