@@ -75,6 +75,12 @@ def agg_bytes(n, F, s):
     return s * n * n + 2 * s * n * F
 
 
+def spmm_bytes(n, nnz, F, s, s_p):
+    """Algorithmic bytes of one CSR aggregation: row pointers, column
+    indices (4 B) and values (s) once, X once (s n F), Y once (s n F)."""
+    return (n + 1) * s_p + nnz * (4 + s) + 2 * s * n * F
+
+
 def run_gpu(wl, prec, steps, warmup, dense=True):
     import torch
     from paper_2010_12635_amd import gcn as G
@@ -164,6 +170,19 @@ def cpu_baseline(wl, budget_s):
                        f"{el:.1f} s; host cores available: {len(os.sched_getaffinity(0))}")
 
 
+def describe(spec, n, r, prec_name):
+    if spec.dense_adj:
+        return (f"{spec.name}: 2-layer GCN, SBM n={n}, 32 blocks, p_in 0.01, p_out 0.0002, + self-loops; "
+                f"dense {prec_name} A_hat; X {n}x{r['f_in']} N(0,1); hidden {r['f_h']}; {r['C']} classes "
+                f"(block id); Adam lr {spec.lr}; loss scale 2^16")
+    graph = {"ba": f"Barabasi-Albert n={n}, m={spec.graph_args[1]}",
+             "rmat": f"R-MAT scale {spec.graph_args[0]}, edge factor {spec.graph_args[1]}, (0.57, 0.19, 0.19, 0.05)",
+             "er": f"Erdos-Renyi n={n}"}.get(spec.graph, spec.graph)
+    return (f"{spec.name}: 2-layer GCN, {graph}, + self-loops, CSR {prec_name} values (nnz {r['nnz']}); "
+            f"X {n}x{r['f_in']} N(0,1); hidden {r['f_h']}; {r['C']} classes; dropout {spec.dropout}; "
+            f"Adam lr {spec.lr}; loss scale 2^16")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -205,12 +224,18 @@ def main():
     s = 4 if prec == 0 else 2
     n = r["n"]
     # forward aggregations per epoch: layer 1 (F = hidden), layer 2 (F = classes)
-    per_epoch_bytes = agg_bytes(n, r["f_h"], s) + agg_bytes(n, r["C"], s)
+    if spec.dense_adj:
+        per_epoch_bytes = agg_bytes(n, r["f_h"], s) + agg_bytes(n, r["C"], s)
+        kname = ("dense A_hat aggregation: transpose_tiled_kernel + dense_agg_kernel "
+                 "(A_hat in tiled MFMA operand order, 8-wave k split)")
+    else:
+        s_p = 8 if spec.index64 else 4
+        per_epoch_bytes = spmm_bytes(n, r["nnz"], r["f_h"], s, s_p) + spmm_bytes(n, r["nnz"], r["C"], s, s_p)
+        kname = "CSR aggregation: spmm_rows_kernel + heavy-row chunk/fixup kernels"
     n_epochs_timed = r["agg_launches"] // 2
     achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
-                    kernel="dense A_hat aggregation: transpose of X + dense_agg_kernel (A_hat in tiled MFMA operand order, 8-wave k split)",
+                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None, kernel=kname,
                     launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
                     algorithmic_bytes_per_launch_avg=int(per_epoch_bytes / 2))
 
@@ -234,9 +259,7 @@ def main():
         "dtype": args.prec,
         "data": "synthetic",
         "config": {
-            "workload": f"{spec.name}: 2-layer GCN, SBM n={n}, 32 blocks, p_in 0.01, p_out 0.0002, + self-loops; "
-                        f"dense {args.prec} A_hat; X {n}x{r['f_in']} N(0,1); hidden {r['f_h']}; {r['C']} classes "
-                        f"(block id); Adam lr {spec.lr}; loss scale 2^16" if spec.dense_adj else spec.name,
+            "workload": describe(spec, n, r, args.prec),
             "n": n, "nnz": r["nnz"], "f_in": r["f_in"], "hidden": r["f_h"], "classes": r["C"],
             "adjacency": "dense" if spec.dense_adj else "csr", "seed": args.seed,
             "wall_s_timed": round(r["wall_s"], 4),

@@ -39,6 +39,7 @@ import numpy as np
 __all__ = [
     "Graph", "graph", "norm_values", "dinv_f32", "dense_adj", "transpose_csr",
     "spmm", "philox4x64", "dropout_keep", "layer_fwd", "softmax_ce",
+    "graph_degrees", "graph_rows", "dropout_keep_rows", "norm_adj_matvec",
     "layer_bwd", "adam_step", "LossScaler", "AdamState",
 ]
 
@@ -99,6 +100,53 @@ def graph(n, src, dst):
     rowptr = np.zeros(n + 1, np.int64)
     np.cumsum(counts, out=rowptr[1:])
     return Graph(n, rowptr, cols.astype(np.int32))
+
+
+def _undirected_pairs(n, src, dst):
+    """Distinct unordered pairs {u, v}, u != v, as sorted int64 keys u*n+v (u<v)."""
+    src = np.asarray(src, dtype=np.int64)
+    dst = np.asarray(dst, dtype=np.int64)
+    if src.size and (src.min() < 0 or dst.min() < 0 or src.max() >= n or dst.max() >= n):
+        raise ValueError("vertex id out of range")
+    keep = src != dst
+    return np.unique(np.minimum(src[keep], dst[keep]) * n + np.maximum(src[keep], dst[keep]))
+
+
+def graph_degrees(n, src, dst):
+    """Degrees of A + I (as in graph()) without building the CSR: each
+    distinct unordered pair adds one to both endpoints, plus one self-loop."""
+    pairs = _undirected_pairs(n, src, dst)
+    deg = np.bincount(pairs // n, minlength=n) + np.bincount(pairs % n, minlength=n) + 1
+    return deg.astype(np.int32)
+
+
+def graph_rows(n, src, dst, rows):
+    """Sorted neighbour lists (self-loop included) of the selected rows of
+    A + I, as in graph(); for checks of sampled rows of large graphs."""
+    pairs = _undirected_pairs(n, src, dst)
+    u, v = pairs // n, pairs % n
+    out = {}
+    for r in rows:
+        nb = np.concatenate([v[u == r], u[v == r], [r]])
+        out[int(r)] = np.sort(nb)
+    return out
+
+
+def norm_adj_matvec(n, src, dst, y):
+    """A_hat y (fp64) for a vector or n x k block y, straight from the
+    distinct unordered pairs: (A_hat y)_i = d_i^-1/2 (d_i^-1/2 y_i +
+    sum over pairs {i, j} of d_j^-1/2 y_j)."""
+    pairs = _undirected_pairs(n, src, dst)
+    u, v = pairs // n, pairs % n
+    deg = np.bincount(u, minlength=n) + np.bincount(v, minlength=n) + 1
+    d = 1.0 / np.sqrt(deg.astype(np.float64))
+    y = np.asarray(y, np.float64)
+    yy = y.reshape(n, -1)
+    acc = d[:, None] * yy
+    for c in range(yy.shape[1]):
+        acc[:, c] += np.bincount(u, weights=d[v] * yy[v, c], minlength=n)
+        acc[:, c] += np.bincount(v, weights=d[u] * yy[u, c], minlength=n)
+    return (d[:, None] * acc).reshape(y.shape)
 
 
 def dinv_f32(g: Graph):
@@ -221,6 +269,26 @@ def dropout_keep(seed, layer_id, epoch, n, f, p):
     w = words.reshape(-1)[: n * f]
     thr = np.uint64(int(np.floor(p * 4294967296.0)))
     return (w >= thr).reshape(n, f)
+
+
+def dropout_keep_rows(seed, layer_id, epoch, rows, f, p):
+    """dropout_keep() restricted to the given rows (same element indexing
+    e = i*f + j over the logical width f)."""
+    rows = np.asarray(rows, np.int64)
+    e = (rows[:, None] * f + np.arange(f, dtype=np.int64)[None, :]).astype(np.uint64)
+    blocks = e >> np.uint64(3)
+    ctr = np.zeros(blocks.shape + (4,), np.uint64)
+    ctr[..., 0] = blocks
+    ctr[..., 1] = np.uint64(epoch)
+    key = np.zeros(blocks.shape + (2,), np.uint64)
+    key[..., 0] = np.uint64(seed & _M64)
+    key[..., 1] = np.uint64(layer_id)
+    out = philox4x64(ctr, key)
+    w = (e & np.uint64(7)).astype(np.int64)
+    word64 = np.take_along_axis(out, (w // 2)[..., None], axis=-1)[..., 0]
+    word = np.where(w % 2 == 0, word64 & np.uint64(0xFFFFFFFF), word64 >> np.uint64(32))
+    thr = np.uint64(int(np.floor(p * 4294967296.0)))
+    return word >= thr
 
 
 # ---------------------------------------------------------------------------

@@ -415,3 +415,34 @@ def test_loss_scaler_script():
     assert states[15:18] == [(8.0, 1), (8.0, 2), (16.0, 0)]
     sc.update(False); sc.update(False); sc.update(False)
     assert sc.scale == 16.0                                         # clamps at max
+
+
+def test_sampled_graph_helpers_match_full_graph():
+    rng = np.random.default_rng(21)
+    n = 400
+    src = rng.integers(0, n, 3000)
+    dst = rng.integers(0, n, 3000)
+    g = O.graph(n, src, dst)
+    assert np.array_equal(O.graph_degrees(n, src, dst), g.deg)
+    rows = [0, 5, 17, 399]
+    nb = O.graph_rows(n, src, dst, rows)
+    for r in rows:
+        assert np.array_equal(nb[r], g.colidx[g.rowptr[r]:g.rowptr[r + 1]])
+
+
+def test_dropout_keep_rows_matches_full_mask():
+    full = O.dropout_keep(77, 3, 9, 50, 13, 0.4)
+    rows = [0, 7, 49, 23]
+    assert np.array_equal(O.dropout_keep_rows(77, 3, 9, rows, 13, 0.4), full[rows])
+
+
+def test_norm_adj_matvec_matches_csr_product():
+    rng = np.random.default_rng(22)
+    n = 300
+    src = rng.integers(0, n, 2000)
+    dst = rng.integers(0, n, 2000)
+    g = O.graph(n, src, dst)
+    y = rng.standard_normal((n, 3))
+    want = O.spmm(g, O.norm_values(g), y)
+    assert np.allclose(O.norm_adj_matvec(n, src, dst, y), want, rtol=1e-13, atol=1e-13)
+    assert np.allclose(O.norm_adj_matvec(n, src, dst, y[:, 0]), want[:, 0], rtol=1e-13, atol=1e-13)
