@@ -79,7 +79,10 @@ typedef enum gcn_act { GCN_ACT_NONE = 0, GCN_ACT_RELU = 1 } gcn_act;
  * gcn_densify); ld_dense is ignored.
  * The heavy-row schedule (filled by gcn_schedule) lets the CSR product split
  * rows with more than heavy_threshold entries across workgroups; with
- * n_heavy == 0 every row is processed whole. */
+ * n_heavy == 0 every row is processed whole.  gcn_schedule also lists the
+ * other ("light") rows in order of decreasing degree (row_perm), so that the
+ * rows a wavefront processes together have similar lengths; with
+ * row_perm == NULL rows are processed in index order. */
 typedef struct gcn_adj {
   int64_t n;
   int64_t nnz;
@@ -100,6 +103,8 @@ typedef struct gcn_adj {
   const int32_t* heavy_rows;      /* [n_heavy] ascending row ids             */
   const int32_t* heavy_chunk_off; /* [n_heavy + 1] first chunk of each row   */
   const int32_t* chunk_heavy;     /* [n_chunks] heavy-row slot of a chunk    */
+  int64_t n_light;                /* rows listed in row_perm                 */
+  const int32_t* row_perm;        /* [n_light] light rows, degree descending */
 } gcn_adj;
 
 /* One layer: H (n x f_in, ld_in) -> H_out (n x f_out, ld_out); W is

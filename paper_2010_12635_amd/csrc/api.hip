@@ -68,6 +68,7 @@ gcn_status check_adj(const gcn_adj* A, int32_t prec) {
     if (!A->heavy_rows || !A->heavy_chunk_off || !A->chunk_heavy) return GCN_ERR_INVALID_ARG;
     if (A->chunk_nnz <= 0 || A->heavy_threshold <= 0 || A->n_chunks <= 0) return GCN_ERR_INVALID_ARG;
   }
+  if (A->row_perm && (A->n_light < 0 || A->n_light > A->n)) return GCN_ERR_SHAPE;
   return GCN_OK;
 }
 
@@ -78,6 +79,8 @@ CsrView view_of(const gcn_adj* A) {
   v.heavy_threshold = A->heavy_threshold; v.chunk_nnz = A->chunk_nnz;
   v.n_heavy = A->n_heavy > 0 ? A->n_heavy : 0; v.n_chunks = A->n_chunks;
   v.heavy_rows = A->heavy_rows; v.heavy_chunk_off = A->heavy_chunk_off; v.chunk_heavy = A->chunk_heavy;
+  v.n_light = A->row_perm ? A->n_light : 0;
+  v.row_perm = A->row_perm;
   return v;
 }
 
@@ -96,7 +99,7 @@ LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
   const int64_t n = A->n;
   p.s_split = gemm_choose_splits(prec, n, L->f_out, L->f_in);
   p.dh_split = gemm_choose_splits(prec, n, L->f_in, L->f_out);
-  p.dw_split = gemm_choose_splits(prec, L->f_in, L->f_out, n);
+  p.dw_split = wgrad_splits(prec, n, L->f_in, L->f_out);
   p.agg_split = 1;
   int64_t f = 0;
   auto upd = [&](int64_t x) { if (x > f) f = x; };
@@ -134,6 +137,16 @@ hipError_t run_gemm(int32_t prec, bool akc, bool bkc, const void* A, int64_t lda
   hipError_t e = gemm_launch(c, s);
   if (e != hipSuccess || !use_partials) return e;
   return reduce_partials(prec, ws, splits, M, N, epi, s);
+}
+
+// Row-streaming product C = A B for the n-row operands of the layer
+// (S = H W, dZ_below = G_S W^T); the generic tiled GEMM covers the rest.
+bool use_tsgemm(int32_t prec, int64_t M, int64_t K) { return M >= 1024 && tsgemm_supported(prec, K); }
+
+hipError_t row_product(int32_t prec, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_kc, int64_t M,
+                       int64_t N, int64_t K, int splits, float* ws, const Epilogue& epi, hipStream_t s) {
+  if (use_tsgemm(prec, M, K)) return tsgemm_launch(prec, A, lda, B, ldb, b_kc, M, N, K, epi, s);
+  return run_gemm(prec, true, b_kc, A, lda, B, ldb, M, N, K, splits, false, ws, epi, s);
 }
 
 hipError_t aggregate(const gcn_adj* A, int32_t prec, const void* X, int64_t ldx, int64_t F, int split,
@@ -255,9 +268,9 @@ gcn_status gcn_densify(const gcn_adj* A, int32_t format, int32_t value_prec, voi
 gcn_status gcn_schedule_size(int64_t n, int64_t nnz, int64_t heavy_threshold, int64_t chunk_nnz, size_t* bytes) {
   if (!bytes) return GCN_ERR_INVALID_ARG;
   if (n <= 0 || nnz < 0) return GCN_ERR_SHAPE;
-  (void)heavy_threshold;
+  if (heavy_threshold <= 0) heavy_threshold = DEFAULT_HEAVY;
   if (chunk_nnz <= 0) chunk_nnz = DEFAULT_CHUNK;
-  *bytes = schedule_bytes(n, nnz, chunk_nnz);
+  *bytes = schedule_bytes(n, nnz, heavy_threshold, chunk_nnz);
   return GCN_OK;
 }
 
@@ -270,12 +283,12 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, 
   if (A->n <= 0 || A->nnz < 0) return GCN_ERR_SHAPE;
   if (heavy_threshold <= 0) heavy_threshold = DEFAULT_HEAVY;
   if (chunk_nnz <= 0) chunk_nnz = DEFAULT_CHUNK;
-  if (sched_bytes < schedule_bytes(A->n, A->nnz, chunk_nnz)) return GCN_ERR_WORKSPACE;
+  if (sched_bytes < schedule_bytes(A->n, A->nnz, heavy_threshold, chunk_nnz)) return GCN_ERR_WORKSPACE;
   if (!aligned16(sched)) return GCN_ERR_ALIGNMENT;
-  int32_t *hr = nullptr, *hco = nullptr, *ch = nullptr;
-  int64_t nh = 0, nc = 0;
+  int32_t *hr = nullptr, *hco = nullptr, *ch = nullptr, *perm = nullptr;
+  int64_t nh = 0, nc = 0, nl = 0;
   hipError_t e = schedule_run(A->n, A->nnz, A->index == GCN_I64, A->rowptr, heavy_threshold, chunk_nnz, sched,
-                              sched_bytes, &hr, &hco, &ch, &nh, &nc, s);
+                              sched_bytes, &hr, &hco, &ch, &perm, &nh, &nc, &nl, s);
   if (e != hipSuccess) return GCN_ERR_DEVICE;
   A->heavy_threshold = heavy_threshold;
   A->chunk_nnz = chunk_nnz;
@@ -284,6 +297,8 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, 
   A->heavy_rows = hr;
   A->heavy_chunk_off = hco;
   A->chunk_heavy = ch;
+  A->row_perm = perm;
+  A->n_light = nl;
   return finish(hipSuccess, s);
 }
 
@@ -315,7 +330,7 @@ gcn_status gcn_layer_fwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, int
   const int64_t n = A->n;
 
   Epilogue es = base_epi(S, L->ld_out, n, L->f_out, EPI_STORE, overflow);
-  GCN_HIP(run_gemm(prec, true, false, H, L->ld_in, W, L->ld_out, n, L->f_out, L->f_in, plan.s_split, false, ws, es, s));
+  GCN_HIP(row_product(prec, H, L->ld_in, W, L->ld_out, false, n, L->f_out, L->f_in, plan.s_split, ws, es, s));
 
   Epilogue ea = agg_epi(H_out, L->ld_out, n, L->f_out, bias, L->act, L->dropout_p, training, seed, L->layer_id,
                         epoch, overflow);
@@ -345,8 +360,7 @@ gcn_status gcn_transform(int64_t n, int64_t f_in, int64_t f_out, int32_t prec, c
   if (sp > 1 && (!workspace || workspace_bytes < need)) return GCN_ERR_WORKSPACE;
   if (workspace && !aligned16(workspace)) return GCN_ERR_ALIGNMENT;
   Epilogue es = base_epi(S, ld_s, n, f_out, EPI_STORE, overflow);
-  GCN_HIP(run_gemm(prec, true, false, H, ld_in, W, ld_w, n, f_out, f_in, sp, false, static_cast<float*>(workspace),
-                   es, s));
+  GCN_HIP(row_product(prec, H, ld_in, W, ld_w, false, n, f_out, f_in, sp, static_cast<float*>(workspace), es, s));
   return finish(hipSuccess, s);
 }
 
@@ -409,8 +423,8 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
   if (dbias) GCN_HIP(colsum(prec, dZ, n, L->f_out, L->ld_out, ws, dbias, L->ld_out, overflow, s));
   // dW = H^T G_S (fp32, split over vertices, fixed-order reduction)
   Epilogue ew = base_epi(dW, L->ld_out, L->f_in, L->f_out, EPI_F32, overflow);
-  GCN_HIP(run_gemm(prec, false, false, H, L->ld_in, GS, L->ld_out, L->f_in, L->f_out, n, plan.dw_split, true, ws,
-                   ew, s));
+  GCN_HIP(wgrad_launch(prec, H, L->ld_in, GS, L->ld_out, n, L->f_in, L->f_out, plan.dw_split, ws, s));
+  GCN_HIP(reduce_partials(prec, ws, plan.dw_split, L->f_in, L->f_out, ew, s));
   // dZ_below = (G_S W^T) * [H > 0] / (1 - p_below)
   if (dZ_below) {
     Epilogue ed = base_epi(dZ_below, L->ld_in, n, L->f_in, EPI_DMASK, overflow);
@@ -418,8 +432,7 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
     ed.keep_scale = 1.f / (1.f - p_below);
     ed.hmask = H;
     ed.ldh = L->ld_in;
-    GCN_HIP(run_gemm(prec, true, true, GS, L->ld_out, W, L->ld_out, n, L->f_in, L->f_out, plan.dh_split, false, ws,
-                     ed, s));
+    GCN_HIP(row_product(prec, GS, L->ld_out, W, L->ld_out, true, n, L->f_in, L->f_out, plan.dh_split, ws, ed, s));
   }
   return finish(hipSuccess, s);
 }

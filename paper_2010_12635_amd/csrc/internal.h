@@ -54,11 +54,27 @@ struct CsrView {
   const int32_t* heavy_rows;
   const int32_t* heavy_chunk_off;
   const int32_t* chunk_heavy;
+  int64_t n_light;
+  const int32_t* row_perm;   // light rows, degree descending (NULL: index order)
 };
 // Y = A_hat X (+ epilogue) for X: n x F (ld), Y described by epi.
 int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F);
 hipError_t spmm_launch(const CsrView& A, int prec, const void* X, int64_t ldx, int64_t F,
                        const Epilogue& epi, float* partials, hipStream_t s);
+
+// ------------------------------------------------- tall-skinny products ----
+// C (M x N) = A (M x K, row-major, lda) . B, B(k, n) = b_kc ? B[n * ldb + k]
+// : B[k * ldb + n]; epilogue EPI_STORE or EPI_DMASK (16-byte row stores).
+bool tsgemm_supported(int prec, int64_t K);
+hipError_t tsgemm_launch(int prec, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_kc, int64_t M,
+                         int64_t N, int64_t K, const Epilogue& epi, hipStream_t s);
+
+// ----------------------------------------------------- weight gradient ----
+// partials[s][m][n] = sum over the s-th vertex span of H[k][m] * G[k][n];
+// reduce_partials then adds the spans in order.
+int wgrad_splits(int prec, int64_t n, int64_t M, int64_t N);
+hipError_t wgrad_launch(int prec, const void* H, int64_t ldh, const void* G, int64_t ldg, int64_t n, int64_t M,
+                        int64_t N, int splits, float* partials, hipStream_t s);
 
 // ------------------------------------------------ dense-A_hat aggregation ----
 // Y = epilogue(A_hat X) for dense A_hat (n x lda); ws holds the padded
@@ -78,11 +94,12 @@ hipError_t normalize_run(int64_t n, int64_t num_edges, const int32_t* src, const
                          int value_prec, void* values, void* dense, int64_t ld_dense,
                          int64_t* nnz_out, int32_t* bad_ids, void* ws, size_t ws_bytes,
                          hipStream_t s);
-size_t schedule_bytes(int64_t n, int64_t nnz, int64_t chunk_nnz);
+size_t schedule_bytes(int64_t n, int64_t nnz, int64_t threshold, int64_t chunk_nnz);
 hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr,
                         int64_t threshold, int64_t chunk_nnz, void* sched, size_t sched_bytes,
                         int32_t** heavy_rows, int32_t** heavy_chunk_off, int32_t** chunk_heavy,
-                        int64_t* n_heavy, int64_t* n_chunks, hipStream_t s);
+                        int32_t** row_perm, int64_t* n_heavy, int64_t* n_chunks, int64_t* n_light,
+                        hipStream_t s);
 
 // ----------------------------------------------------------------- loss ----
 size_t loss_workspace_bytes(int64_t n, int64_t C);

@@ -331,6 +331,27 @@ __global__ void heavy_fill_kernel(int64_t n, const IdxT* __restrict__ rowptr, in
   }
 }
 
+// Histogram of light rows over buckets thr - deg (deg <= thr).
+template <typename IdxT>
+__global__ void light_hist_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr, int32_t* __restrict__ hist) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
+    if (d <= thr) atomicAdd(&hist[thr - d], 1);
+  }
+}
+
+template <typename IdxT>
+__global__ void light_scatter_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
+                                     const int64_t* __restrict__ boff, int32_t* __restrict__ cur,
+                                     int32_t* __restrict__ perm) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
+    if (d > thr) continue;
+    const int64_t b = thr - d;
+    perm[boff[b] + atomicAdd(&cur[b], 1)] = (int32_t)r;
+  }
+}
+
 }  // namespace
 
 hipError_t fill_zero(void* p, size_t bytes, hipStream_t s) {
@@ -427,30 +448,41 @@ hipError_t normalize_run(int64_t n, int64_t E, const int32_t* src, const int32_t
   return hipSuccess;
 }
 
-size_t schedule_bytes(int64_t n, int64_t nnz, int64_t chunk_nnz) {
+size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
   const int64_t max_chunks = nnz / chunk_nnz + n + 1;
+  const int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
   size_t b = 0;
-  b += align256(sizeof(int32_t) * n);                          // heavy_rows
-  b += align256(sizeof(int32_t) * (n + 1));                    // heavy_chunk_off
-  b += align256(sizeof(int32_t) * max_chunks);                 // chunk_heavy
-  b += align256(sizeof(int64_t) * (n + 1));                    // flags -> heavy index
-  b += align256(sizeof(int64_t) * (n + 1));                    // chunks per row -> chunk offsets
-  b += align256(sizeof(int64_t) * scan_scratch_elems(n + 1));  // scan scratch
+  b += align256(sizeof(int32_t) * n);                           // heavy_rows
+  b += align256(sizeof(int32_t) * (n + 1));                     // heavy_chunk_off
+  b += align256(sizeof(int32_t) * max_chunks);                  // chunk_heavy
+  b += align256(sizeof(int32_t) * n);                           // row_perm
+  b += align256(sizeof(int64_t) * (n + 1));                     // flags -> heavy index
+  b += align256(sizeof(int64_t) * (n + 1));                     // chunks per row -> chunk offsets
+  b += align256(sizeof(int32_t) * (thr + 1));                   // degree histogram
+  b += align256(sizeof(int32_t) * (thr + 1));                   // bucket cursors
+  b += align256(sizeof(int64_t) * (thr + 2));                   // bucket offsets
+  b += align256(sizeof(int64_t) * scan_scratch_elems(scan_n));  // scan scratch
   return b;
 }
 
 hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, int64_t thr, int64_t chunk,
                         void* sched, size_t sched_bytes, int32_t** heavy_rows, int32_t** heavy_chunk_off,
-                        int32_t** chunk_heavy, int64_t* n_heavy, int64_t* n_chunks, hipStream_t s) {
+                        int32_t** chunk_heavy, int32_t** row_perm, int64_t* n_heavy, int64_t* n_chunks,
+                        int64_t* n_light, hipStream_t s) {
   char* w = static_cast<char*>(sched);
   auto take = [&](size_t bytes) { char* p = w; w += align256(bytes); return p; };
   const int64_t max_chunks = nnz / chunk + n + 1;
+  const int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
   int32_t* hr = (int32_t*)take(sizeof(int32_t) * n);
   int32_t* hco = (int32_t*)take(sizeof(int32_t) * (n + 1));
   int32_t* ch = (int32_t*)take(sizeof(int32_t) * max_chunks);
+  int32_t* perm = (int32_t*)take(sizeof(int32_t) * n);
   int64_t* hidx = (int64_t*)take(sizeof(int64_t) * (n + 1));
   int64_t* choff = (int64_t*)take(sizeof(int64_t) * (n + 1));
-  int64_t* scr = (int64_t*)take(sizeof(int64_t) * scan_scratch_elems(n + 1));
+  int32_t* hist = (int32_t*)take(sizeof(int32_t) * (thr + 1));
+  int32_t* cur = (int32_t*)take(sizeof(int32_t) * (thr + 1));
+  int64_t* boff = (int64_t*)take(sizeof(int64_t) * (thr + 2));
+  int64_t* scr = (int64_t*)take(sizeof(int64_t) * scan_scratch_elems(scan_n));
   if ((size_t)(w - static_cast<char*>(sched)) > sched_bytes) return hipErrorInvalidValue;
   hipError_t e;
 #define GCN_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
@@ -466,13 +498,30 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   else
     hipLaunchKernelGGL(heavy_fill_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, hidx, choff, hr, hco, ch);
   GCN_TRY(hipGetLastError());
-  int64_t host[2] = {0, 0};
+  // light rows by decreasing degree: counting sort on bucket thr - deg
+  GCN_TRY(fill_zero(hist, sizeof(int32_t) * (thr + 1), s));
+  GCN_TRY(fill_zero(cur, sizeof(int32_t) * (thr + 1), s));
+  if (idx64)
+    hipLaunchKernelGGL(light_hist_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, hist);
+  else
+    hipLaunchKernelGGL(light_hist_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, hist);
+  GCN_TRY(hipGetLastError());
+  hipLaunchKernelGGL(widen_kernel, dim3(grid_for(thr + 2)), dim3(256), 0, s, thr + 1, hist, boff);
+  GCN_TRY(hipGetLastError());
+  GCN_TRY(scan_exclusive(boff, thr + 2, scr, s));
+  if (idx64)
+    hipLaunchKernelGGL(light_scatter_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, boff, cur, perm);
+  else
+    hipLaunchKernelGGL(light_scatter_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, boff, cur, perm);
+  GCN_TRY(hipGetLastError());
+  int64_t host[3] = {0, 0, 0};
   GCN_TRY(hipMemcpyAsync(&host[0], hidx + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipMemcpyAsync(&host[1], choff + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  GCN_TRY(hipMemcpyAsync(&host[2], boff + thr + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipStreamSynchronize(s));
 #undef GCN_TRY
-  *heavy_rows = hr; *heavy_chunk_off = hco; *chunk_heavy = ch;
-  *n_heavy = host[0]; *n_chunks = host[1];
+  *heavy_rows = hr; *heavy_chunk_off = hco; *chunk_heavy = ch; *row_perm = perm;
+  *n_heavy = host[0]; *n_chunks = host[1]; *n_light = host[2];
   return hipSuccess;
 }
 

@@ -6,8 +6,10 @@
 //  * Light rows (<= heavy_threshold entries): a group of LPR lanes owns one
 //    row; lane li of the group owns the 16-byte column slice li of the
 //    feature row (8 x 16-bit or 4 x fp32), so one neighbour row of X is a
-//    single coalesced LPR * 16-byte read.  Neighbours are walked 4 at a
-//    time to keep several gathers in flight.  fp32 accumulation.
+//    single coalesced LPR * 16-byte read.  Neighbours are walked 8 at a
+//    time to keep several gathers in flight.  Rows are taken in the order of
+//    the schedule's permutation (decreasing degree), so the groups of a
+//    wave walk rows of similar length.  fp32 accumulation.
 //  * Heavy rows (power-law hubs): split into chunks of chunk_nnz entries;
 //    one workgroup per chunk reduces its entries across 256/LPR lane groups
 //    through LDS in a fixed order into an fp32 partial row; a fixup kernel
@@ -22,6 +24,8 @@ namespace {
 template <typename IdxT>
 struct SpmmParams {
   int64_t n;
+  int64_t n_rows;               // rows to process: n_light with a permutation, else n
+  const int32_t* row_perm;      // may be NULL
   const IdxT* rowptr;
   const int32_t* colidx;
   const void* values;
@@ -47,42 +51,46 @@ __device__ __forceinline__ void fma_vec(float* acc, float v, uint4 raw) {
   for (int i = 0; i < Vec<T>::N; ++i) acc[i] = fmaf(v, x[i], acc[i]);
 }
 
+template <typename T, bool HAS_VAL, int U>
+__device__ __forceinline__ void gather_block(float* acc, const T* __restrict__ X, int64_t ldx, const int32_t* __restrict__ colidx,
+                                             const void* values, const float* dinv, float drow, int64_t e, int64_t stride) {
+  int32_t c[U];
+  uint4 x[U];
+  float v[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) c[u] = colidx[e + u * stride];
+#pragma unroll
+  for (int u = 0; u < U; ++u) x[u] = ldg16(X + (int64_t)c[u] * ldx);
+#pragma unroll
+  for (int u = 0; u < U; ++u) v[u] = edge_value<T, HAS_VAL>(values, dinv, drow, e + u * stride, c[u]);
+#pragma unroll
+  for (int u = 0; u < U; ++u) fma_vec<T>(acc, v[u], x[u]);
+}
+
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane / LPR, li = lane % LPR;
-  const int64_t row = ((int64_t)blockIdx.x * 4 + wave) * G + g;
+  const int64_t slot = ((int64_t)blockIdx.x * 4 + wave) * G + g;
   const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
-  if (row >= p.n || col0 >= p.F) return;
+  if (slot >= p.n_rows || col0 >= p.F) return;
+  const int64_t row = p.row_perm ? (int64_t)p.row_perm[slot] : slot;
   const int64_t beg = (int64_t)p.rowptr[row], end = (int64_t)p.rowptr[row + 1];
-  if (p.heavy_threshold > 0 && end - beg > p.heavy_threshold) return;
+  if (!p.row_perm && p.heavy_threshold > 0 && end - beg > p.heavy_threshold) return;
   const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
   const float drow = HAS_VAL ? 0.f : p.dinv[row];
   float acc[VE];
 #pragma unroll
   for (int i = 0; i < VE; ++i) acc[i] = 0.f;
   int64_t e = beg;
-  for (; e + 4 <= end; e += 4) {
-    const int32_t c0 = p.colidx[e], c1 = p.colidx[e + 1], c2 = p.colidx[e + 2], c3 = p.colidx[e + 3];
-    const uint4 x0 = ldg16(X + (int64_t)c0 * p.ldx);
-    const uint4 x1 = ldg16(X + (int64_t)c1 * p.ldx);
-    const uint4 x2 = ldg16(X + (int64_t)c2 * p.ldx);
-    const uint4 x3 = ldg16(X + (int64_t)c3 * p.ldx);
-    const float v0 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c0);
-    const float v1 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 1, c1);
-    const float v2 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 2, c2);
-    const float v3 = edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 3, c3);
-    fma_vec<T>(acc, v0, x0);
-    fma_vec<T>(acc, v1, x1);
-    fma_vec<T>(acc, v2, x2);
-    fma_vec<T>(acc, v3, x3);
+  for (; e + 8 <= end; e += 8) gather_block<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
+  if (e + 4 <= end) {
+    gather_block<T, HAS_VAL, 4>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
+    e += 4;
   }
-  for (; e < end; ++e) {
-    const int32_t c = p.colidx[e];
-    fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c), ldg16(X + (int64_t)c * p.ldx));
-  }
+  for (; e < end; ++e) gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
   epi_store_vec<T>(p.epi, row, col0, acc);
 }
 
@@ -110,7 +118,7 @@ template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 __global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT> p) {
   constexpr int VE = Vec<T>::N;
   constexpr int NG = 256 / LPR;
-  __shared__ float red[256 * VE];
+  __shared__ float red[4 * LPR * VE];
   const int64_t chunk = blockIdx.x;
   const int g = threadIdx.x / LPR, li = threadIdx.x % LPR;
   const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
@@ -126,32 +134,31 @@ __global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT>
     const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
     const float drow = HAS_VAL ? 0.f : p.dinv[row];
     int64_t e = cbeg + g;
-    for (; e + 3 * NG < cend; e += 4 * NG) {
-      const int32_t c0 = p.colidx[e], c1 = p.colidx[e + NG], c2 = p.colidx[e + 2 * NG], c3 = p.colidx[e + 3 * NG];
-      const uint4 x0 = ldg16(X + (int64_t)c0 * p.ldx);
-      const uint4 x1 = ldg16(X + (int64_t)c1 * p.ldx);
-      const uint4 x2 = ldg16(X + (int64_t)c2 * p.ldx);
-      const uint4 x3 = ldg16(X + (int64_t)c3 * p.ldx);
-      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c0), x0);
-      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + NG, c1), x1);
-      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 2 * NG, c2), x2);
-      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e + 3 * NG, c3), x3);
-    }
-    for (; e < cend; e += NG) {
-      const int32_t c = p.colidx[e];
-      fma_vec<T>(acc, edge_value<T, HAS_VAL>(p.values, p.dinv, drow, e, c), ldg16(X + (int64_t)c * p.ldx));
-    }
+    for (; e + 7 * NG < cend; e += 8 * NG)
+      gather_block<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, NG);
+    for (; e < cend; e += NG)
+      gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, NG);
   }
+  // reduce over the lane groups of a wave (xor butterfly over the group
+  // bits of the lane id), then over the 4 waves through LDS in wave order
 #pragma unroll
-  for (int i = 0; i < VE; ++i) red[threadIdx.x * VE + i] = acc[i];
+  for (int o = 32; o >= LPR; o >>= 1)
+#pragma unroll
+    for (int i = 0; i < VE; ++i) acc[i] += __shfl_xor(acc[i], o);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane < LPR) {
+#pragma unroll
+    for (int i = 0; i < VE; ++i) red[(wave * LPR + lane) * VE + i] = acc[i];
+  }
   __syncthreads();
-  if (g == 0 && col0 < p.ldp) {
+  if (threadIdx.x < LPR && col0 < p.ldp) {
     float s[VE];
 #pragma unroll
-    for (int i = 0; i < VE; ++i) s[i] = 0.f;
-    for (int gg = 0; gg < NG; ++gg)
-#pragma unroll
-      for (int i = 0; i < VE; ++i) s[i] += red[(gg * LPR + li) * VE + i];
+    for (int i = 0; i < VE; ++i) {
+      s[i] = red[(0 * LPR + li) * VE + i] + red[(1 * LPR + li) * VE + i];
+      s[i] += red[(2 * LPR + li) * VE + i];
+      s[i] += red[(3 * LPR + li) * VE + i];
+    }
     float* out = p.partials + chunk * p.ldp + col0;
 #pragma unroll
     for (int i = 0; i < VE; ++i)
@@ -180,6 +187,8 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   const int64_t colblocks = (F + LPR * VE - 1) / (LPR * VE);
   SpmmParams<IdxT> p;
   p.n = A.n;
+  p.row_perm = A.row_perm;
+  p.n_rows = A.row_perm ? A.n_light : A.n;
   p.rowptr = reinterpret_cast<const IdxT*>(A.rowptr);
   p.colidx = A.colidx;
   p.values = A.values;
@@ -187,9 +196,12 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   p.heavy_threshold = A.n_heavy > 0 ? A.heavy_threshold : 0;
   p.X = X; p.ldx = ldx; p.F = F; p.epi = epi;
   const int64_t rows_per_block = 4 * G;
-  dim3 grid((unsigned)((A.n + rows_per_block - 1) / rows_per_block), (unsigned)colblocks);
-  hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), grid, dim3(256), 0, s, p);
-  hipError_t e = hipGetLastError();
+  hipError_t e = hipSuccess;
+  if (p.n_rows > 0) {
+    dim3 grid((unsigned)((p.n_rows + rows_per_block - 1) / rows_per_block), (unsigned)colblocks);
+    hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), grid, dim3(256), 0, s, p);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess || A.n_heavy <= 0) return e;
 
   HeavyParams<IdxT> hp;

@@ -1,0 +1,292 @@
+// Tall-skinny products of the layer, C (n x N) = A (n x K) . B (K x N) with
+// n large and K, N <= a few hundred:
+//   S = H W                        (B(k, n) = W[k][n])
+//   dZ_below = (G_S W^T) * mask    (B(k, n) = W[n][k])
+// Both are bound by streaming A and C through HBM (arithmetic intensity
+// <= 64 flop/byte in 16-bit storage), so the kernel is organised around the
+// stream:
+//  * a workgroup stages its block of B (up to 128 columns x K, k-contiguous,
+//    zero-padded to the MFMA k chunk) in LDS once;
+//  * each of its 4 waves owns TM x 16 consecutive rows of A and reads their
+//    MFMA operand fragments straight from global memory (rows are adjacent,
+//    so a wave's loads stay inside one compact region), with a 3-deep
+//    register ring of chunks in flight; B fragments come from LDS;
+//  * the output of each 16-row tile is staged through a per-wave LDS buffer
+//    and written as 16-byte row-contiguous vectors after the epilogue
+//    (plain store, or the ReLU/dropout derivative read from H).
+#include "internal.h"
+
+#include <algorithm>
+
+namespace gcn {
+
+namespace {
+
+template <typename T> struct TsMfma;
+template <> struct TsMfma<f16> {
+  static __device__ __forceinline__ f32x4 run(uint4 a, uint4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct TsMfma<bf16> {
+  static __device__ __forceinline__ f32x4 run(uint4 a, uint4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+};
+template <> struct TsMfma<float> {
+  static __device__ __forceinline__ f32x4 run(uint4 a, uint4 b, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    return c;
+  }
+};
+
+constexpr int TS_LDS_B_BYTES = 80 * 1024;   // cap of the B block in LDS
+
+struct TsParams {
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  int64_t M, N, K;
+  int64_t kpad;            // K rounded up to the k chunk
+  int nblk;                // columns per workgroup (multiple of 16)
+  Epilogue epi;
+};
+
+// Dynamic LDS: B block [nblk][kpad + VE] (T), then 4 per-wave staging
+// buffers [16][nblk + 4] (fp32).
+template <typename T, bool BKC, int TM, int TNW>
+__global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
+  constexpr int VE = Vec<T>::N;
+  constexpr int KC = 4 * VE;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nblk = p.nblk;
+  const int64_t ldsb = p.kpad + VE;                 // LDS row stride of B (elements)
+  T* sB = reinterpret_cast<T*>(smem);
+  float* sC = reinterpret_cast<float*>(smem + ((size_t)nblk * ldsb * sizeof(T) + 15) / 16 * 16);
+  const int ldc = nblk + 4;
+  float* myC = sC + wave * 16 * ldc;
+  const int64_t n0 = (int64_t)blockIdx.y * nblk;
+  const T* __restrict__ Bg = reinterpret_cast<const T*>(p.B);
+
+  // ---- B block -> LDS, k-contiguous: sB[c][k] = B(k, n0 + c), zero outside
+  if (BKC) {   // B(k, n) = Bg[n * ldb + k]: copy 16-byte vectors
+    const int vpr = (int)(p.kpad / VE);
+    for (int v = threadIdx.x; v < nblk * vpr; v += 256) {
+      const int c = v / vpr, kv = v % vpr;
+      const int64_t n = n0 + c, k = (int64_t)kv * VE;
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (n < p.N && k < p.K) {
+        x = ldg16(Bg + n * p.ldb + k);
+        T* e = reinterpret_cast<T*>(&x);
+#pragma unroll
+        for (int j = 0; j < VE; ++j)
+          if (k + j >= p.K) e[j] = T(0);
+      }
+      *reinterpret_cast<uint4*>(sB + c * ldsb + k) = x;
+    }
+  } else {     // B(k, n) = Bg[k * ldb + n]: 16-byte loads along n, transposed into LDS
+    const int vpk = nblk / VE;                       // vectors per k row of the block
+    for (int64_t idx = threadIdx.x; idx < (int64_t)vpk * p.kpad; idx += 256) {
+      const int64_t k = idx / vpk;
+      const int cv = (int)(idx % vpk);
+      const int64_t n = n0 + (int64_t)cv * VE;
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (k < p.K && n < p.N) {
+        x = ldg16(Bg + k * p.ldb + n);               // n + VE <= round_up(N, 8) <= ldb
+        T* e = reinterpret_cast<T*>(&x);
+#pragma unroll
+        for (int j = 0; j < VE; ++j)
+          if (n + j >= p.N) e[j] = T(0);
+      }
+      const T* e = reinterpret_cast<const T*>(&x);
+#pragma unroll
+      for (int j = 0; j < VE; ++j) sB[(cv * VE + j) * ldsb + k] = e[j];
+    }
+  }
+  __syncthreads();
+
+  // ---- stream row tiles of A (4 waves x TM x 16 rows per tile), B stays in LDS
+  const int64_t tile_rows = 4 * TM * 16;
+  const int64_t ntiles = (p.M + tile_rows - 1) / tile_rows;
+  const T* __restrict__ Ag = reinterpret_cast<const T*>(p.A);
+  const T* bfrag = sB + (lane & 15) * ldsb + (lane >> 4) * VE;
+  const int64_t nch = p.kpad / KC;
+  const int64_t full = p.K / KC;                    // chunks with no k >= K
+  const int tnw = min(TNW, nblk / 16);              // live column tiles of this block
+  constexpr int OV = Vec<T>::N;
+  const int vpr = nblk / OV;
+
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t r0 = tile * tile_rows + (int64_t)wave * (TM * 16);
+    const T* arow[TM];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      int64_t r = r0 + tm * 16 + (lane & 15);
+      if (r >= p.M) r = p.M - 1;                     // clamped rows are never stored
+      arow[tm] = Ag + r * p.lda + (lane >> 4) * VE;
+    }
+    f32x4 acc[TM][TNW];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto loadA = [&](uint4* a, int64_t c) {
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) a[tm] = ldg16(arow[tm] + c * KC);
+    };
+    auto compute = [&](const uint4* a, int64_t c) {
+#pragma unroll
+      for (int tn = 0; tn < TNW; ++tn) {
+        if (tn < tnw) {
+          const uint4 b = *reinterpret_cast<const uint4*>(bfrag + tn * 16 * ldsb + c * KC);
+#pragma unroll
+          for (int tm = 0; tm < TM; ++tm) acc[tm][tn] = TsMfma<T>::run(a[tm], b, acc[tm][tn]);
+        }
+      }
+    };
+#define TS_FENCE() __builtin_amdgcn_sched_barrier(0)
+    uint4 a0[TM], a1[TM], a2[TM], a3[TM];
+    int64_t c = 0;
+    if (full >= 3) {
+      loadA(a0, 0); loadA(a1, 1); loadA(a2, 2);
+      TS_FENCE();
+      for (; c + 7 <= full; c += 4) {
+        loadA(a3, c + 3); TS_FENCE(); compute(a0, c); TS_FENCE();
+        loadA(a0, c + 4); TS_FENCE(); compute(a1, c + 1); TS_FENCE();
+        loadA(a1, c + 5); TS_FENCE(); compute(a2, c + 2); TS_FENCE();
+        loadA(a2, c + 6); TS_FENCE(); compute(a3, c + 3); TS_FENCE();
+      }
+      compute(a0, c); compute(a1, c + 1); compute(a2, c + 2);
+      c += 3;
+    }
+    for (; c < full; ++c) { loadA(a0, c); compute(a0, c); }
+#undef TS_FENCE
+    if (c < nch) {   // the chunk that straddles K: mask k >= K (B rows there are zero too)
+      const int64_t kl = c * KC + (lane >> 4) * VE;
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        // a vector starting below K ends inside the row (lda >= K rounded up to 8)
+        a0[tm] = kl < p.K ? ldg16(arow[tm] + c * KC) : make_uint4(0, 0, 0, 0);
+        T* e = reinterpret_cast<T*>(&a0[tm]);
+#pragma unroll
+        for (int j = 0; j < VE; ++j)
+          if (kl + j >= p.K) e[j] = T(0);
+      }
+      compute(a0, c);
+    }
+
+    // ---- epilogue: per 16-row tile, MFMA layout -> LDS -> row vectors
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+#pragma unroll
+      for (int tn = 0; tn < TNW; ++tn)
+        if (tn < tnw) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) myC[((lane >> 4) * 4 + v) * ldc + tn * 16 + (lane & 15)] = acc[tm][tn][v];
+        }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      for (int idx = lane; idx < 16 * vpr; idx += 64) {
+        const int rr = idx / vpr, cv = idx % vpr;
+        const int64_t row = r0 + tm * 16 + rr, col = n0 + cv * OV;
+        if (row >= p.M || col >= p.N) continue;
+        float v[OV];
+#pragma unroll
+        for (int j = 0; j < OV; ++j) v[j] = myC[rr * ldc + cv * OV + j];
+        if (p.epi.mode == EPI_DMASK && p.epi.relu) {
+          float h[OV];
+          unpack<T>(ldg16(reinterpret_cast<const T*>(p.epi.hmask) + row * p.epi.ldh + col), h);
+#pragma unroll
+          for (int j = 0; j < OV; ++j) v[j] = h[j] > 0.f ? v[j] * p.epi.keep_scale : 0.f;
+        }
+        Epilogue plain = p.epi;
+        plain.mode = EPI_STORE;
+        epi_store_vec<T>(plain, row, col, v);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+  }
+}
+
+template <typename T>
+int ts_nblk(int64_t N, int64_t kpad) {
+  int64_t nb = std::min<int64_t>(128, (N + 15) / 16 * 16);
+  const int64_t cap = (TS_LDS_B_BYTES / ((kpad + Vec<T>::N) * (int64_t)sizeof(T))) / 16 * 16;
+  nb = std::min<int64_t>(nb, std::max<int64_t>(cap, 16));
+  return (int)nb;
+}
+
+template <typename T, bool BKC, int TM>
+hipError_t launch_tm(const TsParams& p, hipStream_t s) {
+  const int tnw = p.nblk / 16;
+  const size_t lds = ((size_t)p.nblk * (p.kpad + Vec<T>::N) * sizeof(T) + 15) / 16 * 16 +
+                     (size_t)4 * 16 * (p.nblk + 4) * sizeof(float);
+  // persistent workgroups: enough to fill every CU twice, each looping over row tiles
+  const int64_t nb = (p.N + p.nblk - 1) / p.nblk;
+  const int64_t ntiles = (p.M + 64 * TM - 1) / (64 * TM);
+  const int64_t per_col = std::max<int64_t>(1, 512 / nb);
+  dim3 grid((unsigned)std::min<int64_t>(ntiles, per_col), (unsigned)nb);
+#define TS_L(TNW_)                                                                                          \
+  do {                                                                                                      \
+    if (lds > 65536) {                                                                                      \
+      hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&tsgemm_kernel<T, BKC, TM, TNW_>),  \
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);           \
+      if (ea != hipSuccess) return ea;                                                                      \
+    }                                                                                                       \
+    hipLaunchKernelGGL((tsgemm_kernel<T, BKC, TM, TNW_>), grid, dim3(256), lds, s, p);                     \
+  } while (0)
+  if (tnw <= 1) TS_L(1);
+  else if (tnw <= 2) TS_L(2);
+  else if (tnw <= 4) TS_L(4);
+  else TS_L(8);
+#undef TS_L
+  return hipGetLastError();
+}
+
+template <typename T, bool BKC>
+hipError_t launch_b(TsParams p, hipStream_t s) {
+  constexpr int KC = 4 * Vec<T>::N;
+  p.kpad = (p.K + KC - 1) / KC * KC;
+  p.nblk = ts_nblk<T>(p.N, p.kpad);
+  // rows per wave: 64 when there are enough rows to fill the GPU twice, else fewer
+  const int64_t tiles64 = (p.M + 255) / 256 * ((p.N + p.nblk - 1) / p.nblk);
+  if (tiles64 >= 512) return launch_tm<T, BKC, 4>(p, s);
+  if (tiles64 >= 256) return launch_tm<T, BKC, 2>(p, s);
+  return launch_tm<T, BKC, 1>(p, s);
+}
+
+template <typename T>
+hipError_t launch_t(const TsParams& p, bool bkc, hipStream_t s) {
+  return bkc ? launch_b<T, true>(p, s) : launch_b<T, false>(p, s);
+}
+
+}  // namespace
+
+bool tsgemm_supported(int prec, int64_t K) {
+  const int64_t kc = prec == 0 ? 16 : 32;
+  const int64_t kpad = (K + kc - 1) / kc * kc;
+  const int64_t s = prec == 0 ? 4 : 2;
+  return (kpad + 16 / s) * s * 16 <= TS_LDS_B_BYTES;   // at least one 16-column block fits
+}
+
+hipError_t tsgemm_launch(int prec, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_kc, int64_t M,
+                         int64_t N, int64_t K, const Epilogue& epi, hipStream_t s) {
+  TsParams p;
+  p.A = A; p.lda = lda; p.B = B; p.ldb = ldb; p.M = M; p.N = N; p.K = K; p.kpad = 0; p.nblk = 0; p.epi = epi;
+  switch (prec) {
+    case 0: return launch_t<float>(p, b_kc, s);
+    case 1: return launch_t<f16>(p, b_kc, s);
+    case 2: return launch_t<bf16>(p, b_kc, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace gcn

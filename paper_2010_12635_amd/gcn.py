@@ -62,7 +62,7 @@ class GcnAdj(ctypes.Structure):
         ("heavy_threshold", ctypes.c_int64), ("chunk_nnz", ctypes.c_int64),
         ("n_heavy", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
         ("heavy_rows", ctypes.c_void_p), ("heavy_chunk_off", ctypes.c_void_p),
-        ("chunk_heavy", ctypes.c_void_p),
+        ("chunk_heavy", ctypes.c_void_p), ("n_light", ctypes.c_int64), ("row_perm", ctypes.c_void_p),
     ]
 
 

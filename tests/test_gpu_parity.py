@@ -122,6 +122,12 @@ def test_schedule_lists_heavy_rows():
     want = np.concatenate([[0], np.cumsum((g.deg[heavy] + 63) // 64)])
     assert np.array_equal(cho, want)
     assert a.n_chunks == want[-1]
+    # light rows: every row with deg <= threshold exactly once, degree non-increasing
+    perm = base[off(a.row_perm): off(a.row_perm) + 4 * a.n_light].view(torch.int32).cpu().numpy()
+    light = np.flatnonzero(g.deg <= 32)
+    assert a.n_light == light.size
+    assert np.array_equal(np.sort(perm), light)
+    assert np.all(np.diff(g.deg[perm]) <= 0)
 
 
 # ------------------------------------------------------------ layer fwd ----
