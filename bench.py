@@ -170,6 +170,105 @@ def cpu_baseline(wl, budget_s):
                        f"{el:.1f} s; host cores available: {len(os.sched_getaffinity(0))}")
 
 
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "dense_agg_sbm16k_traffic.md")
+def kernel_hash(*files):
+    import hashlib
+    h = hashlib.sha256()
+    for f in files + ("common.h",):
+        with open(os.path.join(ROOT, "paper_2010_12635_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(key, *sources):
+    """A traffic figure from the committed counter summary, or None if the
+    kernel's sources changed since the counters were taken."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+        block = text.split("```json", 1)[1].split("```", 1)[0]
+        d = json.loads(block)
+    except (OSError, IndexError, ValueError):
+        return None
+    if d.get(key + "_source_hash") != kernel_hash(*sources):
+        return None
+    return d.get(key)
+
+
+def summarize_counters(fetch_dir, write_dir, out_path, command):
+    """Per-kernel FETCH_SIZE / WRITE_SIZE averages (KiB per dispatch in the
+    rocprofv3 CSV), scaled by what the same counters read for the plain
+    device copy of known size run by --copy-calibration."""
+    import csv
+    from collections import defaultdict
+
+    def read(d):
+        rows = list(csv.DictReader(open(os.path.join(d, "run_counter_collection.csv"))))
+        per = defaultdict(list)
+        for r in rows:
+            per[r["Kernel_Name"]].append(float(r["Counter_Value"]) * 1024.0)
+        return rows, per
+
+    frows, fetch = read(fetch_dir)
+    wrows, write = read(write_dir)
+    # calibration: the three largest __amd_rocclr_copyBuffer dispatches at the start are 256 MiB copies
+    calib_bytes = 256 << 20
+    cf = [float(r["Counter_Value"]) * 1024.0 for r in frows if "copyBuffer" in r["Kernel_Name"]][:3]
+    cw = [float(r["Counter_Value"]) * 1024.0 for r in wrows if "copyBuffer" in r["Kernel_Name"]][:3]
+    f_scale = calib_bytes / (sum(cf) / len(cf))
+    w_scale = calib_bytes / (sum(cw) / len(cw))
+
+    def avg(d, k):
+        v = d.get(k, [])
+        return sum(v) / len(v) if v else 0.0
+
+    kernels = sorted(fetch, key=lambda k: -sum(fetch[k]))
+    rows_out = []
+    for k in kernels[:16]:
+        rows_out.append((k, len(fetch[k]), avg(fetch, k) * f_scale, avg(write, k) * w_scale))
+    agg = [r for r in rows_out if "dense_agg_kernel" in r[0] and ("DF16" in r[0] or "half" in r[0])]
+    per_launch = sum(r[2] + r[3] for r in agg) / max(1, len(agg))
+    spmm = [r for r in rows_out if "spmm_" in r[0] and "DF16" in r[0]]
+    summary = {
+        "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+        "dense_agg_f16": int(per_launch),
+        "dense_agg_f16_source_hash": kernel_hash("dense_agg.hip"),
+        # light + heavy kernels of one F=hidden and one F=classes aggregation, halved: bytes per launch
+        "spmm_f16": int(sum(r[2] + r[3] for r in spmm) / 2),
+        "spmm_f16_source_hash": kernel_hash("spmm.hip"),
+    }
+    lines = ["# HBM traffic counters: dense aggregation (SBM n=16384) and CSR aggregation (R-MAT scale 21), fp16", "",
+             "Commands (from the repository root, on one MI355X; one counter per run):", "", "```", command, "```", "",
+             f"Scaling: a plain 256 MiB device copy (`--copy-calibration 256`, `__amd_rocclr_copyBuffer`) reads "
+             f"{sum(cf) / len(cf) / 2**20:.1f} MiB of FETCH_SIZE and {sum(cw) / len(cw) / 2**20:.1f} MiB of WRITE_SIZE, "
+             f"so fetch is scaled by {f_scale:.3f} and write by {w_scale:.3f}. These counters count L2 misses "
+             f"(requests to the fabric, which the 256 MB Infinity Cache may serve), labelled HBM traffic here.", "",
+             "| kernel | dispatches | fetch MB/dispatch (scaled) | write MB/dispatch (scaled) |", "|---|---:|---:|---:|"]
+    for k, c, fb, wb in rows_out:
+        name = k if len(k) < 100 else k[:100] + "..."
+        lines.append(f"| `{name}` | {c} | {fb / 1e6:.1f} | {wb / 1e6:.1f} |")
+    lines += ["", "Machine-readable summary read by bench.py (bytes per launch; a figure is reported only while",
+              "the hash of its kernel's sources matches):", "", "```json", json.dumps(summary, indent=1), "```", ""]
+    with open(out_path, "w") as fh:
+        fh.write("\n".join(lines))
+    return summary
+
+
+def summarize_stats(stats_dir, out_path, command, title):
+    """Kernel time table from a rocprofv3 --stats run (run_kernel_stats.csv)."""
+    import csv
+    rows = list(csv.DictReader(open(os.path.join(stats_dir, "run_kernel_stats.csv"))))
+    lines = [f"# {title}", "", "Command (from the repository root, on one MI355X):", "", "```", command, "```", "",
+             "Source: `run_kernel_stats.csv` of that command; times in microseconds.", "",
+             "| kernel | calls | avg us | min us | max us | total % |", "|---|---:|---:|---:|---:|---:|"]
+    for r in rows[:30]:
+        name = r["Name"].replace("gcn::(anonymous namespace)::", "")
+        name = name if len(name) < 110 else name[:110] + "..."
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} "
+                     f"| {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    with open(out_path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
 def describe(spec, n, r, prec_name):
     if spec.dense_adj:
         return (f"{spec.name}: 2-layer GCN, SBM n={n}, 32 blocks, p_in 0.01, p_out 0.0002, + self-loops; "
@@ -193,7 +292,32 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-fp32", action="store_true", help="skip the fp32-mode run")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0 = skip)")
+    ap.add_argument("--spmm-workload", default="rmat21",
+                    help="CSR workload whose aggregation bandwidth is reported as 'spmm' ('none' = skip)")
+    ap.add_argument("--spmm-steps", type=int, default=10)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="before the runs, copy a MIB-MiB device buffer 3 times (reference kernel for "
+                         "hardware traffic counters)")
+    ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_DIR", "OUT_MD", "TITLE"),
+                    help="write a kernel time table from a rocprofv3 --stats folder and exit")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the traffic summary from two rocprofv3 --pmc output folders and exit")
     args = ap.parse_args()
+
+    if args.summarize_stats:
+        d, out, title = args.summarize_stats
+        cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_default -o run -- "
+               "python3 bench.py --steps 50 --cpu-seconds 0")
+        summarize_stats(d, out, cmd, title)
+        return
+
+    if args.summarize_counters:
+        cmd = ("rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py "
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --copy-calibration 256\n"
+               "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py "
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --copy-calibration 256")
+        print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, cmd)))
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build runs the GCN hot path on a single MI355X "
@@ -208,6 +332,15 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
+    if args.copy_calibration > 0:
+        nbytes = args.copy_calibration << 20
+        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy calibration: 3 x {args.copy_calibration} MiB device-to-device")
+        del src, dst
     log(f"[bench] generating workload {args.workload} seed {args.seed}")
     wl = I.workload(args.workload, args.seed)
     spec = wl["spec"]
@@ -234,10 +367,34 @@ def main():
         kname = "CSR aggregation: spmm_rows_kernel + heavy-row chunk/fixup kernels"
     n_epochs_timed = r["agg_launches"] // 2
     achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9
+    traffic = None
+    if prec != 0:
+        traffic = load_traffic("dense_agg_f16", "dense_agg.hip") if spec.dense_adj else load_traffic("spmm_f16", "spmm.hip")
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None, kernel=kname,
+                    frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kname,
                     launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
                     algorithmic_bytes_per_launch_avg=int(per_epoch_bytes / 2))
+
+    spmm = None
+    if args.spmm_workload != "none" and args.spmm_steps > 0:
+        log(f"[bench] spmm workload {args.spmm_workload}: generating")
+        wl2 = I.workload(args.spmm_workload, args.seed)
+        spec2 = wl2["spec"]
+        r2 = run_gpu(wl2, prec, args.spmm_steps, 1, dense=spec2.dense_adj)
+        s_p = 8 if spec2.index64 else 4
+        b2 = spmm_bytes(r2["n"], r2["nnz"], r2["f_h"], s, s_p) + spmm_bytes(r2["n"], r2["nnz"], r2["C"], s, s_p)
+        ach2 = b2 * (r2["agg_launches"] // 2) / (r2["agg_ms"] * 1e-3) / 1e9
+        spmm = dict(workload=describe(spec2, r2["n"], r2, args.prec), epochs_per_s=round(args.spmm_steps / (r2["gpu_ms"] * 1e-3), 2),
+                    ms_per_step=round(r2["gpu_ms"] / args.spmm_steps, 3), bound="hbm", achieved=round(ach2, 1),
+                    peak=HBM_PEAK_GBS, unit="GB/s", frac=round(ach2 / HBM_PEAK_GBS, 4),
+                    kernel="CSR aggregation: spmm_rows_kernel + heavy-row chunk/fixup kernels",
+                    launches=r2["agg_launches"], avg_launch_us=round(r2["agg_ms"] * 1e3 / r2["agg_launches"], 2),
+                    algorithmic_bytes_per_launch_avg=int(b2 / 2),
+                    gather_bytes_per_launch_avg=int(r2["nnz"] * (r2["f_h"] + r2["C"]) * s / 2),
+                    traffic=load_traffic("spmm_f16", "spmm.hip") if prec != 0 and args.spmm_workload == "rmat21" else None,
+                    peak_mem_bytes=r2["peak_bytes"])
+        log(f"[bench] spmm: {spmm['ms_per_step']} ms/epoch, {spmm['achieved']} GB/s algorithmic")
+        del wl2
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -272,6 +429,7 @@ def main():
         "train_acc": round(r["n_correct"] / max(1, r["n_mask"]), 4),
         "loss_scale": r["scaler"],
         "roofline": roofline,
+        "spmm": spmm,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
