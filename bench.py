@@ -43,7 +43,17 @@ class EventTimer:
         import torch
         self.torch = torch
         self.pairs = []
+        self.pool = []
         self.enabled = False
+
+    def reserve(self, brackets):
+        """Create the events of ``brackets`` brackets up front, so that the
+        timed loop only records them."""
+        self.pool = [self.torch.cuda.Event(enable_timing=True) for _ in range(2 * brackets)]
+        self.pool.reverse()
+
+    def _event(self):
+        return self.pool.pop() if self.pool else self.torch.cuda.Event(enable_timing=True)
 
     def __call__(self):
         timer = self
@@ -51,14 +61,14 @@ class EventTimer:
         class _Ctx:
             def __enter__(self_inner):
                 if timer.enabled:
-                    e = timer.torch.cuda.Event(enable_timing=True)
+                    e = timer._event()
                     e.record()
                     self_inner.e = e
                 return self_inner
 
             def __exit__(self_inner, *exc):
                 if timer.enabled:
-                    e2 = timer.torch.cuda.Event(enable_timing=True)
+                    e2 = timer._event()
                     e2.record()
                     timer.pairs.append((self_inner.e, e2))
                 return False
@@ -99,6 +109,11 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     timer = EventTimer()
     for ep in range(warmup):
         m.step(ep, agg_timer=timer)
+    # the aggregation calls of every `every`-th timed step are bracketed by
+    # events (each event record costs the stream a few microseconds, so
+    # bracketing every step would slow the throughput being measured)
+    every = max(1, steps // 25)
+    timer.reserve(2 * (steps // every + 1))
     torch.cuda.synchronize()
     timer.enabled = True
     t_start = torch.cuda.Event(enable_timing=True)
@@ -106,8 +121,9 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     t0 = time.perf_counter()
     t_start.record()
     for k in range(steps):
-        m.step(warmup + k, agg_timer=timer)
+        m.step(warmup + k, agg_timer=timer if k % every == 0 else None)
     t_end.record()
+    host_submit = time.perf_counter() - t0      # host time to enqueue the timed steps
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = t_start.elapsed_time(t_end)
@@ -115,7 +131,7 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     loss = float(m.loss.item())
     st = m.scaler_state()
     peak = torch.cuda.max_memory_allocated() - base
-    res = dict(prec=prec, wall_s=wall, gpu_ms=gpu_ms, agg_ms=agg_ms, agg_launches=len(timer.pairs),
+    res = dict(prec=prec, wall_s=wall, gpu_ms=gpu_ms, host_submit_s=host_submit, agg_ms=agg_ms, agg_launches=len(timer.pairs),
                loss=loss, scaler=st, peak_bytes=int(peak), n=dg.n, nnz=dg.nnz,
                f_h=m.f_h, C=m.C, f_in=m.f_in, n_correct=int(m.n_correct.item()), n_mask=m.n_mask)
     del m, dg
@@ -231,7 +247,7 @@ def summarize_counters(fetch_dir, write_dir, out_path, command):
     summary = {
         "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
         "dense_agg_f16": int(per_launch),
-        "dense_agg_f16_source_hash": kernel_hash("dense_agg.hip"),
+        "dense_agg_f16_source_hash": kernel_hash("dense_agg.hip", "xpose.h"),
         # light + heavy kernels of one F=hidden and one F=classes aggregation, halved: bytes per launch
         "spmm_f16": int(sum(r[2] + r[3] for r in spmm) / 2),
         "spmm_f16_source_hash": kernel_hash("spmm.hip"),
@@ -369,7 +385,7 @@ def main():
     achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9
     traffic = None
     if prec != 0:
-        traffic = load_traffic("dense_agg_f16", "dense_agg.hip") if spec.dense_adj else load_traffic("spmm_f16", "spmm.hip")
+        traffic = load_traffic("dense_agg_f16", "dense_agg.hip", "xpose.h") if spec.dense_adj else load_traffic("spmm_f16", "spmm.hip")
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kname,
                     launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
@@ -420,6 +436,7 @@ def main():
             "n": n, "nnz": r["nnz"], "f_in": r["f_in"], "hidden": r["f_h"], "classes": r["C"],
             "adjacency": "dense" if spec.dense_adj else "csr", "seed": args.seed,
             "wall_s_timed": round(r["wall_s"], 4),
+            "host_submit_ms_per_step": round(r["host_submit_s"] * 1e3 / args.steps, 4),
         },
         "fp32": None if r32 is None else {
             "value": round(args.steps / (r32["gpu_ms"] * 1e-3), 2), "ms_per_step": round(r32["gpu_ms"] / args.steps, 4),

@@ -84,14 +84,16 @@ CsrView view_of(const gcn_adj* A) {
   return v;
 }
 
-// Partial-sum floats needed by each step of the layer (the workspace holds
-// one step's partials at a time).
+// Workspace of a layer call: the column-sum partials of dZ (kept from the
+// aggregation step to the final reduction) at the front, then the scratch
+// of one step at a time.
 struct LayerPlan {
   int s_split;       // S = H W
   int agg_split;     // dense aggregation
   int dw_split;      // dW = H^T G_S
   int dh_split;      // dZ_below = G_S W^T
-  int64_t floats;
+  int64_t cs_floats; // column-sum partial region (multiple of 64 floats)
+  int64_t floats;    // total
 };
 
 LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
@@ -106,13 +108,16 @@ LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
   if (p.s_split > 1) upd(p.s_split * n * L->f_out);
   if (p.dh_split > 1) upd(p.dh_split * n * L->f_in);
   upd(p.dw_split * L->f_in * L->f_out);
+  int64_t cs = 0;
   if (A->format != GCN_CSR) {
     upd((int64_t)(dense_agg_workspace_bytes(prec, n, L->f_out) / sizeof(float)) + 1);
+    cs = dense_agg_colsum_rows(prec, n) * L->f_out;
   } else {
     upd(spmm_partials_floats(view_of(A), prec, L->f_out));
+    cs = colsum_partials_floats(n, L->ld_out);
   }
-  upd(colsum_partials_floats(n, L->ld_out));
-  p.floats = f;
+  p.cs_floats = (cs + 63) / 64 * 64;
+  p.floats = p.cs_floats + f;
   return p;
 }
 
@@ -149,11 +154,13 @@ hipError_t row_product(int32_t prec, const void* A, int64_t lda, const void* B, 
   return run_gemm(prec, true, b_kc, A, lda, B, ldb, M, N, K, splits, false, ws, epi, s);
 }
 
-hipError_t aggregate(const gcn_adj* A, int32_t prec, const void* X, int64_t ldx, int64_t F, int split,
-                     const Epilogue& epi, float* ws, hipStream_t s) {
-  (void)split;
+// Y = epilogue(A_hat X).  For dense A_hat, colsum (may be NULL) receives the
+// column-sum partials of X computed during its transposition.
+hipError_t aggregate(const gcn_adj* A, int32_t prec, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
+                     float* ws, float* colsum, hipStream_t s) {
   if (A->format != GCN_CSR)
-    return dense_agg_launch(prec, A->dense, A->ld_dense, A->format == GCN_DENSE_TILED, A->n, X, ldx, F, epi, ws, s);
+    return dense_agg_launch(prec, A->dense, A->ld_dense, A->format == GCN_DENSE_TILED, A->n, X, ldx, F, epi, ws,
+                            colsum, s);
   return spmm_launch(view_of(A), prec, X, ldx, F, epi, ws, s);
 }
 
@@ -334,7 +341,7 @@ gcn_status gcn_layer_fwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, int
 
   Epilogue ea = agg_epi(H_out, L->ld_out, n, L->f_out, bias, L->act, L->dropout_p, training, seed, L->layer_id,
                         epoch, overflow);
-  GCN_HIP(aggregate(A, prec, S, L->ld_out, L->f_out, plan.agg_split, ea, ws, s));
+  GCN_HIP(aggregate(A, prec, S, L->ld_out, L->f_out, ea, ws, nullptr, s));
   return finish(hipSuccess, s);
 }
 
@@ -391,7 +398,7 @@ gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* 
     return GCN_ERR_WORKSPACE;
   if (workspace && !aligned16(workspace)) return GCN_ERR_ALIGNMENT;
   Epilogue ea = agg_epi(Y, ldy, A->n, F, bias, act, dropout_p, training, seed, layer_id, epoch, overflow);
-  GCN_HIP(aggregate(A, prec, X, ldx, F, 1, ea, static_cast<float*>(workspace), s));
+  GCN_HIP(aggregate(A, prec, X, ldx, F, ea, static_cast<float*>(workspace), nullptr, s));
   return finish(hipSuccess, s);
 }
 
@@ -413,18 +420,33 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
   const LayerPlan plan = plan_layer(A, L, prec);
   if (!workspace || workspace_bytes < plan_bytes(plan)) return GCN_ERR_WORKSPACE;
   if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
-  float* ws = static_cast<float*>(workspace);
+  float* cs = static_cast<float*>(workspace);     // column-sum partials of dZ
+  float* ws = cs + plan.cs_floats;                 // per-step scratch
   const int64_t n = A->n;
+  const bool dense = A->format != GCN_CSR;
 
-  // G_S = A_hat^T dZ = A_hat dZ (A_hat symmetric)
+  // G_S = A_hat^T dZ = A_hat dZ (A_hat symmetric); for dense A_hat the
+  // transposition of dZ also yields the column-sum partials for dbias
   Epilogue eg = base_epi(GS, L->ld_out, n, L->f_out, EPI_STORE, overflow);
-  GCN_HIP(aggregate(A, prec, dZ, L->ld_out, L->f_out, plan.agg_split, eg, ws, s));
-  // dbias = column sums of dZ
-  if (dbias) GCN_HIP(colsum(prec, dZ, n, L->f_out, L->ld_out, ws, dbias, L->ld_out, overflow, s));
-  // dW = H^T G_S (fp32, split over vertices, fixed-order reduction)
+  GCN_HIP(aggregate(A, prec, dZ, L->ld_out, L->f_out, eg, ws, dbias && dense ? cs : nullptr, s));
+  RedJob jb{};
+  if (dbias) {
+    Epilogue eb = base_epi(dbias, L->ld_out, 1, L->f_out, EPI_F32, overflow);
+    if (dense) {
+      jb = make_job(cs, (int)dense_agg_colsum_rows(prec, n), 1, L->f_out, eb);
+    } else {
+      int nb = 0;
+      GCN_HIP(colsum_partial_launch(prec, dZ, n, L->f_out, L->ld_out, cs, L->ld_out, &nb, s));
+      eb.cols = L->ld_out;
+      jb = make_job(cs, nb, 1, L->ld_out, eb);
+    }
+  }
+  // dW = H^T G_S (fp32, split over vertices), then one launch reduces the dW
+  // spans and the dbias partials, each in a fixed order
   Epilogue ew = base_epi(dW, L->ld_out, L->f_in, L->f_out, EPI_F32, overflow);
   GCN_HIP(wgrad_launch(prec, H, L->ld_in, GS, L->ld_out, n, L->f_in, L->f_out, plan.dw_split, ws, s));
-  GCN_HIP(reduce_partials(prec, ws, plan.dw_split, L->f_in, L->f_out, ew, s));
+  const RedJob jw = make_job(ws, plan.dw_split, L->f_in, L->f_out, ew);
+  GCN_HIP(reduce_partials2(prec, jw, dbias ? &jb : nullptr, s));
   // dZ_below = (G_S W^T) * [H > 0] / (1 - p_below)
   if (dZ_below) {
     Epilogue ed = base_epi(dZ_below, L->ld_in, n, L->f_in, EPI_DMASK, overflow);

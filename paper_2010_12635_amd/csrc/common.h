@@ -157,9 +157,13 @@ __device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, i
   const int64_t cols = ep.cols;
   if (ep.mode == EPI_AGG) {
     if (ep.bias) {
+      // all VE loads in flight at once (an index past cols re-reads col0)
+      float bv[VE];
+#pragma unroll
+      for (int i = 0; i < VE; ++i) bv[i] = ep.bias[col0 + i < cols ? col0 + i : col0];
 #pragma unroll
       for (int i = 0; i < VE; ++i)
-        if (col0 + i < cols) acc[i] += ep.bias[col0 + i];
+        if (col0 + i < cols) acc[i] += bv[i];
     }
     if (ep.relu) {
 #pragma unroll

@@ -20,6 +20,7 @@
 //    fused epilogue (bias, ReLU, dropout, cast, overflow flag) stores
 //    16-byte vectors row by row.  No global partial sums, one launch.
 #include "internal.h"
+#include "xpose.h"
 
 namespace gcn {
 
@@ -38,34 +39,78 @@ __host__ __device__ __forceinline__ int64_t tiled_off(int64_t i, int64_t j, int6
 }
 template <typename T> constexpr int tile_kc() { return 4 * Vec<T>::N; }
 
-// Xt = tiled(X^T): X is n x F (ldx); Xt has ceil(F / 64) * 64 rows and
-// nc * KC columns; entries outside F x n are zero.  One workgroup converts a
-// 64 (features) x 64 (vertices) tile through LDS; its output is contiguous.
+// Xt = tiled(X^T): X is n x F (ldx); Xt has Fp = ceil(F / 64) * 64 rows
+// and kpad = nc * KC columns; entries outside F x n are zero.  Each thread
+// turns one VE x VE block (VE vertices x VE features) around in registers:
+// VE 16-byte row loads, a register transpose, VE 16-byte stores, each of
+// VE consecutive vertices of one feature, i.e. one contiguous piece of the
+// tiled layout.  A wave covers 64 features x XB_K vertices, a workgroup four
+// waves along the vertices.  With colsum != NULL the kernel also sums each
+// feature over the workgroup's vertices (fixed order: block rows, a xor
+// butterfly over the wave's vertex blocks, then the four waves in order)
+// and writes row blockIdx.x of colsum ([gridDim.x][F] floats).
+template <typename T>
+struct XpGeom {
+  static constexpr int VE = Vec<T>::N;
+  static constexpr int FB = 64 / VE;          // feature blocks per wave
+  static constexpr int KB = 64 / FB;          // vertex blocks per wave
+  static constexpr int WAVE_K = KB * VE;      // vertices per wave
+  static constexpr int WG_K = 4 * WAVE_K;     // vertices per workgroup
+};
+
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_tiled_kernel(const T* __restrict__ X, int64_t ldx, int64_t n, int64_t F,
-                                                              T* __restrict__ Xt, int64_t nc) {
-  constexpr int VE = Vec<T>::N, KC = 4 * VE;
-  __shared__ T tile[64][65];                    // [k - k0][f - f0]
-  const int64_t k0 = (int64_t)blockIdx.x * 64, f0 = (int64_t)blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t k = k0 + r, f = f0 + tx;
-    tile[r][tx] = (k < n && f < F) ? X[k * ldx + f] : T(0);
+                                                              T* __restrict__ Xt, int64_t nc, float* __restrict__ colsum) {
+  using G = XpGeom<T>;
+  constexpr int VE = G::VE, KC = 4 * VE;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fb = lane % G::FB, kb = lane / G::FB;
+  const int64_t f0 = (int64_t)blockIdx.y * 64 + fb * VE;
+  const int64_t k0 = (int64_t)blockIdx.x * G::WG_K + wave * G::WAVE_K + kb * VE;
+  const int64_t kpad = nc * KC;
+  // all VE loads go out before any is used: rows >= n and feature blocks
+  // >= F read row 0 / column 0 (in bounds) and are zeroed afterwards
+  const int64_t nf = F - f0;
+  const int vc = nf <= 0 ? 0 : nf >= VE ? VE : (int)nf;
+  const T* colp = X + (vc > 0 ? f0 : 0);         // f0 + VE <= round_up(F, 8) <= ldx
+  uint4 in[VE];
+#pragma unroll
+  for (int i = 0; i < VE; ++i) in[i] = ldg16(colp + (k0 + i < n ? k0 + i : 0) * ldx);
+#pragma unroll
+  for (int i = 0; i < VE; ++i) in[i] = keep_first<T>(in[i], k0 + i < n ? vc : 0);
+  uint4 out[VE];
+  transpose_block(in, out, T());
+  if (k0 < kpad) {
+#pragma unroll
+    for (int j = 0; j < VE; ++j) stg16(Xt + tiled_off<T>(f0 + j, k0, nc), out[j]);
+  }
+  if (!colsum) return;
+  __shared__ float red[4][64];
+  float cs[VE];
+#pragma unroll
+  for (int j = 0; j < VE; ++j) {
+    float v[VE];
+    unpack<T>(out[j], v);
+    float a = v[0];
+#pragma unroll
+    for (int i = 1; i < VE; ++i) a += v[i];
+    cs[j] = a;
+  }
+#pragma unroll
+  for (int off = G::FB; off < 64; off <<= 1)
+#pragma unroll
+    for (int j = 0; j < VE; ++j) cs[j] += __shfl_xor(cs[j], off);
+  if (kb == 0) {
+#pragma unroll
+    for (int j = 0; j < VE; ++j) red[wave][fb * VE + j] = cs[j];
   }
   __syncthreads();
-  // the 64 x 64 tile covers chunks k0/KC .. k0/KC + 64/KC - 1 of row block
-  // f0/64: a contiguous run of (64 / KC) * 4 * 16 * KC elements
-  constexpr int TILE_ELEMS = 64 * 64;
-  const int64_t base = tiled_off<T>(f0, k0, nc);
-  for (int o = threadIdx.x; o < TILE_ELEMS; o += 256) {
-    const int cl = o / (4 * 16 * KC);             // chunk within the tile
-    const int rem = o % (4 * 16 * KC);
-    const int tn = rem / (16 * KC);
-    const int q = rem % (16 * KC);
-    const int g = q / (16 * VE), cc = (q / VE) % 16, e = q % VE;
-    const int64_t c = k0 / KC + cl;
-    if (c >= nc) continue;
-    Xt[base + o] = tile[cl * KC + g * VE + e][tn * 16 + cc];
+  if (threadIdx.x < 64) {
+    const int64_t f = (int64_t)blockIdx.y * 64 + threadIdx.x;
+    float a = red[0][threadIdx.x] + red[1][threadIdx.x];
+    a += red[2][threadIdx.x];
+    a += red[3][threadIdx.x];
+    if (f < F) colsum[(int64_t)blockIdx.x * F + f] = a;
   }
 }
 
@@ -271,13 +316,14 @@ int64_t xt_elems(int prec, int64_t n, int64_t F) {
 
 template <typename T>
 hipError_t launch_t(const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx, int64_t F,
-                    const Epilogue& epi, void* ws, hipStream_t s) {
+                    const Epilogue& epi, void* ws, float* colsum, hipStream_t s) {
   constexpr int KC = tile_kc<T>();
   const int64_t nc = (n + KC - 1) / KC;
   const int64_t fblocks = (F + 63) / 64;
   T* Xt = reinterpret_cast<T*>(ws);
-  dim3 tg((unsigned)((n + 63) / 64), (unsigned)fblocks);
-  hipLaunchKernelGGL(transpose_tiled_kernel<T>, tg, dim3(256), 0, s, reinterpret_cast<const T*>(X), ldx, n, F, Xt, nc);
+  dim3 tg((unsigned)((nc * KC + XpGeom<T>::WG_K - 1) / XpGeom<T>::WG_K), (unsigned)fblocks);
+  hipLaunchKernelGGL(transpose_tiled_kernel<T>, tg, dim3(256), 0, s, reinterpret_cast<const T*>(X), ldx, n, F, Xt, nc,
+                     colsum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   DaParams p;
@@ -349,13 +395,19 @@ int64_t dense_tiled_elems(int prec, int64_t n) {
 }
 
 hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx,
-                            int64_t F, const Epilogue& epi, void* ws, hipStream_t s) {
+                            int64_t F, const Epilogue& epi, void* ws, float* colsum, hipStream_t s) {
   switch (prec) {
-    case 0: return launch_t<float>(A, lda, tiled, n, X, ldx, F, epi, ws, s);
-    case 1: return launch_t<f16>(A, lda, tiled, n, X, ldx, F, epi, ws, s);
-    case 2: return launch_t<bf16>(A, lda, tiled, n, X, ldx, F, epi, ws, s);
+    case 0: return launch_t<float>(A, lda, tiled, n, X, ldx, F, epi, ws, colsum, s);
+    case 1: return launch_t<f16>(A, lda, tiled, n, X, ldx, F, epi, ws, colsum, s);
+    case 2: return launch_t<bf16>(A, lda, tiled, n, X, ldx, F, epi, ws, colsum, s);
   }
   return hipErrorInvalidValue;
+}
+
+int64_t dense_agg_colsum_rows(int prec, int64_t n) {
+  const int64_t kc = prec == 0 ? 16 : 32;
+  const int64_t wg_k = prec == 0 ? XpGeom<float>::WG_K : XpGeom<f16>::WG_K;
+  return ((n + kc - 1) / kc * kc + wg_k - 1) / wg_k;
 }
 
 hipError_t densify_launch(const CsrView& A, int prec, bool tiled, void* dense, int64_t ld, hipStream_t s) {

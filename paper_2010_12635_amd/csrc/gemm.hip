@@ -238,34 +238,43 @@ hipError_t launch_typed(const GemmCall& c, const GemmParams& p, hipStream_t s) {
 
 // 64 output elements per workgroup; 4 lane groups each sum every 4th split
 // (in split order), then the 4 group sums are added in group order.
+// One reduction: 64 outputs per workgroup, 4 groups of splits each walking
+// its splits in order, then the 4 group sums added in group order.
 template <typename T>
-__global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __restrict__ part, int splits,
-                                                              int64_t M, int64_t N, int64_t width, Epilogue ep) {
+__device__ __forceinline__ void reduce_body(const RedJob& j, int64_t blk) {
   __shared__ float red[4][64];
-  const int64_t total = M * width;
-  const int64_t idx = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
+  const int64_t total = j.M * j.width;
+  const int64_t idx = blk * 64 + (threadIdx.x & 63);
   const int g = threadIdx.x >> 6;
-  const int64_t r = idx / width, c = idx % width;
-  const bool live = idx < total && c < N;
+  const int64_t r = idx / j.width, c = idx % j.width;
+  const bool live = idx < total && c < j.N;
   float a = 0.f;
   if (live) {
-    const float* q = part + r * N + c;
-    const int64_t stride = M * N;
+    const float* q = j.part + r * j.N + c;
+    const int64_t stride = j.M * j.N;
 #pragma unroll 8
-    for (int sidx = g; sidx < splits; sidx += 4) a += q[(int64_t)sidx * stride];
+    for (int sidx = g; sidx < j.splits; sidx += 4) a += q[(int64_t)sidx * stride];
   }
   red[g][threadIdx.x & 63] = a;
   __syncthreads();
   if (g != 0 || idx >= total) return;
-  if (c >= N) {   // EPI_F32 padding columns
-    reinterpret_cast<float*>(ep.out)[r * ep.ldo + c] = 0.f;
+  if (c >= j.N) {   // EPI_F32 padding columns
+    reinterpret_cast<float*>(j.ep.out)[r * j.ep.ldo + c] = 0.f;
     return;
   }
   const int t = threadIdx.x & 63;
   float sum = red[0][t] + red[1][t];
   sum += red[2][t];
   sum += red[3][t];
-  epi_store1<T>(ep, r, c, sum);
+  epi_store1<T>(j.ep, r, c, sum);
+}
+
+// Up to two independent reductions in one launch: blocks [0, j0.blocks)
+// take j0, the rest j1.
+template <typename T>
+__global__ __launch_bounds__(256) void reduce_partials_kernel(RedJob j0, RedJob j1) {
+  if ((int64_t)blockIdx.x < j0.blocks) reduce_body<T>(j0, blockIdx.x);
+  else reduce_body<T>(j1, (int64_t)blockIdx.x - j0.blocks);
 }
 
 // Column sums: a workgroup sums `rows_per_block` consecutive rows, 4 row
@@ -333,19 +342,31 @@ hipError_t gemm_launch(const GemmCall& c, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t M, int64_t N,
-                           const Epilogue& epi, hipStream_t s) {
-  const int64_t width = epi.mode == EPI_F32 ? epi.ldo : N;
-  const int64_t total = M * width;
-  const int64_t blocks = (total + 63) / 64;
+RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const Epilogue& epi) {
+  RedJob j;
+  j.part = partials; j.splits = splits; j.M = M; j.N = N; j.ep = epi;
+  j.width = epi.mode == EPI_F32 ? epi.ldo : N;
+  j.blocks = (M * j.width + 63) / 64;
+  return j;
+}
+
+hipError_t reduce_partials2(int prec, const RedJob& a, const RedJob* b, hipStream_t s) {
+  RedJob j1 = b ? *b : a;
+  if (!b) j1.blocks = 0;
+  const int64_t blocks = a.blocks + j1.blocks;
   if (blocks <= 0) return hipSuccess;
   switch (prec) {
-    case 0: hipLaunchKernelGGL(reduce_partials_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, s, partials, splits, M, N, width, epi); break;
-    case 1: hipLaunchKernelGGL(reduce_partials_kernel<f16>, dim3((unsigned)blocks), dim3(256), 0, s, partials, splits, M, N, width, epi); break;
-    case 2: hipLaunchKernelGGL(reduce_partials_kernel<bf16>, dim3((unsigned)blocks), dim3(256), 0, s, partials, splits, M, N, width, epi); break;
+    case 0: hipLaunchKernelGGL(reduce_partials_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, s, a, j1); break;
+    case 1: hipLaunchKernelGGL(reduce_partials_kernel<f16>, dim3((unsigned)blocks), dim3(256), 0, s, a, j1); break;
+    case 2: hipLaunchKernelGGL(reduce_partials_kernel<bf16>, dim3((unsigned)blocks), dim3(256), 0, s, a, j1); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t M, int64_t N,
+                           const Epilogue& epi, hipStream_t s) {
+  return reduce_partials2(prec, make_job(partials, splits, M, N, epi), nullptr, s);
 }
 
 int64_t colsum_partials_floats(int64_t rows, int64_t ld) {
@@ -353,23 +374,19 @@ int64_t colsum_partials_floats(int64_t rows, int64_t ld) {
   return ((rows + rpb - 1) / rpb) * ld;
 }
 
-hipError_t colsum(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld,
-                  float* partials, float* out, int64_t ldo, int32_t* flag, hipStream_t s) {
+hipError_t colsum_partial_launch(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld, float* partials,
+                                 int64_t ldp, int* splits, hipStream_t s) {
   const int64_t rpb = colsum_rows_per_block(rows);
   const int64_t nb = (rows + rpb - 1) / rpb;
-  dim3 grid((unsigned)nb, (unsigned)((ldo + 63) / 64));
+  dim3 grid((unsigned)nb, (unsigned)((ldp + 63) / 64));
   switch (prec) {
-    case 0: hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, rows, cols, ld, ldo, rpb, partials); break;
-    case 1: hipLaunchKernelGGL(colsum_partial_kernel<f16>, grid, dim3(256), 0, s, (const f16*)X, rows, cols, ld, ldo, rpb, partials); break;
-    case 2: hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, rows, cols, ld, ldo, rpb, partials); break;
+    case 0: hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, rows, cols, ld, ldp, rpb, partials); break;
+    case 1: hipLaunchKernelGGL(colsum_partial_kernel<f16>, grid, dim3(256), 0, s, (const f16*)X, rows, cols, ld, ldp, rpb, partials); break;
+    case 2: hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, rows, cols, ld, ldp, rpb, partials); break;
     default: return hipErrorInvalidValue;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // out[c] = sum over blocks b of partials[b][c] (fixed order), 1 x ldo
-  Epilogue ep{};
-  ep.out = out; ep.ldo = ldo; ep.rows = 1; ep.cols = ldo; ep.mode = EPI_F32; ep.flag = flag;
-  return reduce_partials(prec, partials, (int)nb, 1, ldo, ep, s);
+  *splits = (int)nb;
+  return hipGetLastError();
 }
 
 }  // namespace gcn

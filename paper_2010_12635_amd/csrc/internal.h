@@ -31,16 +31,27 @@ struct GemmCall {
 int gemm_choose_splits(int prec, int64_t M, int64_t N, int64_t K);
 hipError_t gemm_launch(const GemmCall& c, hipStream_t s);
 
-// out = epilogue(sum over s < splits of partials[s][r][c]) for r < M, c < N;
-// for EPI_F32 columns [N, ldo) are written 0.
+// out = epilogue(sum over s < splits of partials[s][r][c]) for r < M, c < N,
+// splits added in order; for EPI_F32 columns [N, ldo) are written 0.
+struct RedJob {
+  const float* part;
+  int splits;
+  int64_t M, N, width, blocks;
+  Epilogue ep;
+};
+RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const Epilogue& epi);
+// One launch for job a and, if b != NULL, job b.
+hipError_t reduce_partials2(int prec, const RedJob& a, const RedJob* b, hipStream_t s);
 hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t M, int64_t N,
                            const Epilogue& epi, hipStream_t s);
 
-// Column sums of X (rows x cols, ld) in fixed order -> out (fp32 [ldo],
-// zero beyond cols).  partials needs colsum_partials_floats() floats.
+// Column-sum partials of X (rows x cols, ld): partials[b][c] for c < ldp
+// (zero for c >= cols), *splits = number of row blocks b; reduce with
+// make_job(partials, *splits, 1, ldp, epi).  partials needs
+// colsum_partials_floats() floats.
 int64_t colsum_partials_floats(int64_t rows, int64_t ld);
-hipError_t colsum(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld,
-                  float* partials, float* out, int64_t ldo, int32_t* flag, hipStream_t s);
+hipError_t colsum_partial_launch(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld, float* partials,
+                                 int64_t ldp, int* splits, hipStream_t s);
 
 // ----------------------------------------------------------------- SpMM ----
 struct CsrView {
@@ -78,10 +89,13 @@ hipError_t wgrad_launch(int prec, const void* H, int64_t ldh, const void* G, int
 
 // ------------------------------------------------ dense-A_hat aggregation ----
 // Y = epilogue(A_hat X) for dense A_hat (n x lda); ws holds the padded
-// transpose of X (dense_agg_workspace_bytes).
+// transpose of X (dense_agg_workspace_bytes).  With colsum != NULL the
+// transposition also writes column-sum partials of X, [rows][F] floats with
+// rows = dense_agg_colsum_rows(); reduce with make_job(colsum, rows, 1, F, ..).
 size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F);
+int64_t dense_agg_colsum_rows(int prec, int64_t n);
 hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx,
-                            int64_t F, const Epilogue& epi, void* ws, hipStream_t s);
+                            int64_t F, const Epilogue& epi, void* ws, float* colsum, hipStream_t s);
 // Elements of the tiled dense A_hat (rows padded to 64, columns to the chunk).
 int64_t dense_tiled_elems(int prec, int64_t n);
 // Dense A_hat from CSR: row-major (ld) or tiled operand order.

@@ -15,6 +15,7 @@
 //    and written as 16-byte row-contiguous vectors after the epilogue
 //    (plain store, or the ReLU/dropout derivative read from H).
 #include "internal.h"
+#include "xpose.h"
 
 #include <algorithm>
 
@@ -72,39 +73,51 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
   const int64_t n0 = (int64_t)blockIdx.y * nblk;
   const T* __restrict__ Bg = reinterpret_cast<const T*>(p.B);
 
-  // ---- B block -> LDS, k-contiguous: sB[c][k] = B(k, n0 + c), zero outside
+  // ---- B block -> LDS, k-contiguous: sB[c][k] = B(k, n0 + c), zero outside.
+  // Every load of a batch is issued (at an in-bounds address) before any is
+  // used; out-of-range elements are zeroed afterwards with dword masks.
   if (BKC) {   // B(k, n) = Bg[n * ldb + k]: copy 16-byte vectors
+    constexpr int TS_STAGE = 8;
     const int vpr = (int)(p.kpad / VE);
-    for (int v = threadIdx.x; v < nblk * vpr; v += 256) {
-      const int c = v / vpr, kv = v % vpr;
-      const int64_t n = n0 + c, k = (int64_t)kv * VE;
-      uint4 x = make_uint4(0, 0, 0, 0);
-      if (n < p.N && k < p.K) {
-        x = ldg16(Bg + n * p.ldb + k);
-        T* e = reinterpret_cast<T*>(&x);
+    const int total = nblk * vpr;
+    for (int base = 0; base < total; base += 256 * TS_STAGE) {
+      uint4 x[TS_STAGE];
 #pragma unroll
-        for (int j = 0; j < VE; ++j)
-          if (k + j >= p.K) e[j] = T(0);
+      for (int u = 0; u < TS_STAGE; ++u) {
+        const int v = base + u * 256 + (int)threadIdx.x;
+        const int64_t n = n0 + v / vpr, k = (int64_t)(v % vpr) * VE;
+        const bool ok = v < total && n < p.N && k < p.K;
+        x[u] = ldg16(Bg + (ok ? n * p.ldb + k : 0));
       }
-      *reinterpret_cast<uint4*>(sB + c * ldsb + k) = x;
+#pragma unroll
+      for (int u = 0; u < TS_STAGE; ++u) {
+        const int v = base + u * 256 + (int)threadIdx.x;
+        if (v >= total) break;
+        const int c = v / vpr;
+        const int64_t n = n0 + c, k = (int64_t)(v % vpr) * VE;
+        const int64_t nk = p.K - k;
+        const int vk = (n >= p.N || nk <= 0) ? 0 : nk >= VE ? VE : (int)nk;
+        *reinterpret_cast<uint4*>(sB + c * ldsb + k) = keep_first<T>(x[u], vk);
+      }
     }
-  } else {     // B(k, n) = Bg[k * ldb + n]: 16-byte loads along n, transposed into LDS
-    const int vpk = nblk / VE;                       // vectors per k row of the block
-    for (int64_t idx = threadIdx.x; idx < (int64_t)vpk * p.kpad; idx += 256) {
-      const int64_t k = idx / vpk;
-      const int cv = (int)(idx % vpk);
-      const int64_t n = n0 + (int64_t)cv * VE;
-      uint4 x = make_uint4(0, 0, 0, 0);
-      if (k < p.K && n < p.N) {
-        x = ldg16(Bg + k * p.ldb + n);               // n + VE <= round_up(N, 8) <= ldb
-        T* e = reinterpret_cast<T*>(&x);
+  } else {     // B(k, n) = Bg[k * ldb + n]: VE x VE blocks (VE k rows x VE columns) turned around in registers
+    const int cpb = nblk / VE;                        // column blocks
+    const int kpb = (int)(p.kpad / VE);               // k blocks
+    const int total = cpb * kpb;
+    for (int blk = threadIdx.x; blk < total; blk += 256) {
+      const int kb = blk % kpb, cb = blk / kpb;       // consecutive threads: consecutive k blocks (LDS banks)
+      const int64_t k0 = (int64_t)kb * VE, n = n0 + (int64_t)cb * VE;
+      const int64_t nn = p.N - n;
+      const int vc = nn <= 0 ? 0 : nn >= VE ? VE : (int)nn;
+      const T* colp = Bg + (vc > 0 ? n : 0);         // n + VE <= round_up(N, 8) <= ldb
+      uint4 in[VE], out[VE];
 #pragma unroll
-        for (int j = 0; j < VE; ++j)
-          if (n + j >= p.N) e[j] = T(0);
-      }
-      const T* e = reinterpret_cast<const T*>(&x);
+      for (int i = 0; i < VE; ++i) in[i] = ldg16(colp + (k0 + i < p.K ? k0 + i : 0) * p.ldb);
 #pragma unroll
-      for (int j = 0; j < VE; ++j) sB[(cv * VE + j) * ldsb + k] = e[j];
+      for (int i = 0; i < VE; ++i) in[i] = keep_first<T>(in[i], k0 + i < p.K ? vc : 0);
+      transpose_block(in, out, T());
+#pragma unroll
+      for (int j = 0; j < VE; ++j) *reinterpret_cast<uint4*>(sB + (cb * VE + j) * ldsb + k0) = out[j];
     }
   }
   __syncthreads();

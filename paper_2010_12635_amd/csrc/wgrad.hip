@@ -11,6 +11,7 @@
 //    columns into a double-buffered LDS tile, from which MFMA fragments are
 //    16-byte reads.
 #include "internal.h"
+#include "xpose.h"
 
 #include <algorithm>
 
@@ -49,32 +50,6 @@ struct WgParams {
   float* partials;                        // [splits][M][N]
 };
 
-// Transpose of a VE x VE block held as VE 16-byte rows (row i = k, element
-// j = column) into VE 16-byte columns (column j, element i = k).
-__device__ __forceinline__ void transpose_block(const uint4* in, uint4* out, f16) {
-  // 8 x 8 halves: output dword e of column c packs rows 2e and 2e+1
-#pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    uint32_t d[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t lo = (&in[2 * e].x)[c >> 1], hi = (&in[2 * e + 1].x)[c >> 1];
-      // v_perm_b32: bytes {hi, lo} selected; low half for even c, high half for odd c
-      d[e] = (c & 1) ? __builtin_amdgcn_perm(hi, lo, 0x07060302u) : __builtin_amdgcn_perm(hi, lo, 0x05040100u);
-    }
-    out[c] = make_uint4(d[0], d[1], d[2], d[3]);
-  }
-}
-__device__ __forceinline__ void transpose_block(const uint4* in, uint4* out, bf16) {
-  transpose_block(in, out, f16());
-}
-__device__ __forceinline__ void transpose_block(const uint4* in, uint4* out, float) {
-  out[0] = make_uint4(in[0].x, in[1].x, in[2].x, in[3].x);
-  out[1] = make_uint4(in[0].y, in[1].y, in[2].y, in[3].y);
-  out[2] = make_uint4(in[0].z, in[1].z, in[2].z, in[3].z);
-  out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
-}
-
 // One k tile of H and G_S (KT vertices x 128 columns each) cut into VE x VE
 // blocks; thread t holds block(s) of VE rows x 16 bytes in registers.
 //   16-bit: 8 x 16 blocks per operand, threads 0..127 take H, 128..255 G_S.
@@ -86,41 +61,64 @@ struct Tile {
   static constexpr int CB = WG_B / VE;             // column blocks per operand
   static constexpr int NBLK = VE == 8 ? 1 : 2;     // blocks per thread
   uint4 r[NBLK][VE];
+  int vrows[NBLK];                                 // rows of the block inside the span
+  int vcols[NBLK];                                 // columns of the block inside the operand
 
+  // Issue the block's VE row loads without waiting for any of them: rows
+  // beyond the span and blocks beyond the operand read row kfirst / column 0
+  // instead (always in bounds) and are zeroed in store(), so the loads are
+  // unconditional and stay in flight while the previous tile is multiplied.
   __device__ __forceinline__ void load_block(int b, const T* __restrict__ base, int64_t ld, int64_t c0, int64_t cols,
-                                             int64_t k0, int64_t kend, int blk) {
+                                             int64_t k0, int64_t kend, int64_t kfirst, int blk) {
     const int rb = blk / CB, cb = blk % CB;
     const int64_t gc = c0 + (int64_t)cb * VE;
+    const int64_t r0 = k0 + rb * VE;
+    const int64_t nr = kend - r0, ncol = cols - gc;
+    vrows[b] = nr <= 0 ? 0 : nr >= VE ? VE : (int)nr;
+    vcols[b] = ncol <= 0 ? 0 : ncol >= VE ? VE : (int)ncol;
+    const T* colp = base + (gc < cols ? gc : 0);   // gc + VE <= round_up(cols, 8) <= ld
 #pragma unroll
     for (int i = 0; i < VE; ++i) {
-      const int64_t gk = k0 + rb * VE + i;
-      uint4 x = make_uint4(0, 0, 0, 0);
-      if (gk < kend && gc < cols) {
-        x = ldg16(base + gk * ld + gc);             // gc + VE <= round_up(cols, 8) <= ld
-        if (gc + VE > cols) {
-          T* e = reinterpret_cast<T*>(&x);
-#pragma unroll
-          for (int j = 0; j < VE; ++j)
-            if (gc + j >= cols) e[j] = T(0);
-        }
-      }
-      r[b][i] = x;
+      const int64_t gk = r0 + i < kend ? r0 + i : kfirst;
+      r[b][i] = ldg16(colp + gk * ld);
     }
   }
   __device__ __forceinline__ void load(const WgParams& p, const T* H, const T* G, int64_t m0, int64_t n0,
-                                       int64_t k0, int64_t kend, int tid) {
+                                       int64_t k0, int64_t kend, int64_t kfirst, int tid) {
     if (VE == 8) {
-      if (tid < 128) load_block(0, H, p.ldh, m0, p.M, k0, kend, tid);
-      else load_block(0, G, p.ldg, n0, p.N, k0, kend, tid - 128);
+      if (tid < 128) load_block(0, H, p.ldh, m0, p.M, k0, kend, kfirst, tid);
+      else load_block(0, G, p.ldg, n0, p.N, k0, kend, kfirst, tid - 128);
     } else {
-      load_block(0, H, p.ldh, m0, p.M, k0, kend, tid);
-      load_block(NBLK - 1, G, p.ldg, n0, p.N, k0, kend, tid);
+      load_block(0, H, p.ldh, m0, p.M, k0, kend, kfirst, tid);
+      load_block(NBLK - 1, G, p.ldg, n0, p.N, k0, kend, kfirst, tid);
+    }
+  }
+  // Zero the rows and columns outside the operand (first use of the data),
+  // with whole-dword masks so the data is never split into 16-bit pieces.
+  __device__ __forceinline__ void mask(int b) {
+    const int vc = vcols[b];
+    uint32_t m[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (VE == 8)
+        m[w] = (2 * w < vc ? 0x0000ffffu : 0u) | (2 * w + 1 < vc ? 0xffff0000u : 0u);
+      else
+        m[w] = w < vc ? 0xffffffffu : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < VE; ++i) {
+      const uint32_t rm = i < vrows[b] ? 0xffffffffu : 0u;
+      r[b][i].x &= m[0] & rm;
+      r[b][i].y &= m[1] & rm;
+      r[b][i].z &= m[2] & rm;
+      r[b][i].w &= m[3] & rm;
     }
   }
   // LDS tiles [column][KT + VE], k-contiguous: one 16-byte store per column
-  __device__ __forceinline__ void store(T* __restrict__ sA, T* __restrict__ sB, int tid) const {
+  __device__ __forceinline__ void store(T* __restrict__ sA, T* __restrict__ sB, int tid) {
 #pragma unroll
     for (int b = 0; b < NBLK; ++b) {
+      mask(b);
       const bool isB = VE == 8 ? tid >= 128 : b == 1;
       const int blk = VE == 8 ? (tid & 127) : tid;
       const int rb = blk / CB, cb = blk % CB;
@@ -159,7 +157,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgParams p) {
 
   const int64_t nt = ke > kb ? (ke - kb + KT - 1) / KT : 0;
   Tile<T> t0, t1;
-  auto load = [&](Tile<T>& x, int64_t t) { x.load(p, Hg, Gg, m0, n0, kb + t * KT, ke, tid); };
+  auto load = [&](Tile<T>& x, int64_t t) { x.load(p, Hg, Gg, m0, n0, kb + t * KT, ke, kb, tid); };
   auto compute = [&](int st) {
     const T* as = sA[st] + (wm * 64 + (lane & 15)) * LDK + (lane >> 4) * VE;
     const T* bs = sB[st] + (wn * 64 + (lane & 15)) * LDK + (lane >> 4) * VE;

@@ -203,6 +203,7 @@ BWD_CASES = [
     (1500, 64, 32, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "dense"),
+    (777, 40, 130, G.GCN_ACT_RELU, 0.5, "tiled"),   # three 64-feature groups, ragged tail
 ]
 
 
@@ -293,8 +294,9 @@ def test_loss(prec, C):
 
 # ------------------------------------------------------------ optimiser ----
 
-def test_optimizer_matches_oracle_and_skips_on_overflow():
-    P = 5000
+# a few workgroups and a grid of several hundred: same state sequence
+@pytest.mark.parametrize("P", [5000, 70001])
+def test_optimizer_matches_oracle_and_skips_on_overflow(P):
     rng = np.random.default_rng(0)
     w0 = rng.standard_normal(P).astype(np.float32)
     g0 = (rng.standard_normal(P) * 65536).astype(np.float32)
@@ -323,7 +325,7 @@ def test_optimizer_matches_oracle_and_skips_on_overflow():
     # overflow: weights bit-unchanged, scale halved, flag cleared
     before = master.clone()
     bad = g0.copy()
-    bad[17] = np.inf
+    bad[P - 1] = np.inf
     grad.copy_(torch.as_tensor(bad))
     G.gcn_optimizer_step(P, master, grad, m, v, working, G.GCN_F16, cfg, state, ov)
     sc.update(True)
