@@ -50,6 +50,9 @@ class EventTimer:
         """Create the events of ``brackets`` brackets up front, so that the
         timed loop only records them."""
         self.pool = [self.torch.cuda.Event(enable_timing=True) for _ in range(2 * brackets)]
+        for e in self.pool:      # torch creates the HIP event at its first record
+            e.record()
+        self.torch.cuda.synchronize()
         self.pool.reverse()
 
     def _event(self):
@@ -113,7 +116,7 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     # events (each event record costs the stream a few microseconds, so
     # bracketing every step would slow the throughput being measured)
     every = max(1, steps // 25)
-    timer.reserve(2 * (steps // every + 1))
+    timer.reserve(2 * (steps // every + 1))        # two aggregation brackets per sampled step
     torch.cuda.synchronize()
     timer.enabled = True
     t_start = torch.cuda.Event(enable_timing=True)

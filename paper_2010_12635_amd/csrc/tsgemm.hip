@@ -57,7 +57,9 @@ struct TsParams {
 
 // Dynamic LDS: B block [nblk][kpad + VE] (T), then 4 per-wave staging
 // buffers [16][nblk + 4] (fp32).
-template <typename T, bool BKC, int TM, int TNW>
+// DM: epilogue multiplies by the ReLU/dropout derivative read from H
+// (EPI_DMASK with relu); otherwise a plain store.
+template <typename T, bool BKC, bool DM, int TM, int TNW>
 __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
   constexpr int VE = Vec<T>::N;
   constexpr int KC = 4 * VE;
@@ -162,36 +164,87 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
         }
       }
     };
+    // The ReLU/dropout derivative of the epilogue reads H: for 16-bit types
+    // the wave's H vectors are requested together with its A fragments, so
+    // the tile costs one memory latency.
+    constexpr bool dmask = DM;
+    constexpr bool HPRE = DM && sizeof(T) == 2;          // H prefetched into registers
+    constexpr int EIT = HPRE ? 4 : 1;                    // vectors per lane per 16 rows (nblk <= 128)
+    uint4 hv[TM][EIT];
+    auto prefetch_h = [&]() {
+      if constexpr (HPRE) {
+        const T* hm = reinterpret_cast<const T*>(p.epi.hmask);
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int it = 0; it < EIT; ++it) {
+            const int idx = lane + 64 * it;
+            const int rr = idx / vpr, cv = idx % vpr;
+            const int64_t row = r0 + tm * 16 + rr, col = n0 + cv * OV;
+            const bool ok = idx < 16 * vpr && row < p.M && col < p.N;
+            hv[tm][it] = ldg16(hm + (ok ? row * p.epi.ldh + col : 0));
+          }
+      }
+    };
 #define TS_FENCE() __builtin_amdgcn_sched_barrier(0)
     uint4 a0[TM], a1[TM], a2[TM], a3[TM];
-    int64_t c = 0;
-    if (full >= 3) {
-      loadA(a0, 0); loadA(a1, 1); loadA(a2, 2);
+    if (nch <= 4) {
+      // The whole K range fits the four fragment sets: every load of the
+      // tile is issued before the first is used (one memory latency per
+      // tile).  Vectors at or past K read the row start and are zeroed.
+      const int64_t kl0 = (lane >> 4) * VE;
+      auto loadw = [&](uint4* a, int64_t c) {
+        const int64_t off = c * KC + kl0 < p.K ? c * KC : -kl0;
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) a[tm] = ldg16(arow[tm] + off);
+      };
+      auto maskw = [&](uint4* a, int64_t c) {
+        const int64_t nk = p.K - (c * KC + kl0);
+        const int vk = nk <= 0 ? 0 : nk >= VE ? VE : (int)nk;
+        if (vk < VE) {
+#pragma unroll
+          for (int tm = 0; tm < TM; ++tm) a[tm] = keep_first<T>(a[tm], vk);
+        }
+      };
+      loadw(a0, 0);
+      if (nch > 1) loadw(a1, 1);
+      if (nch > 2) loadw(a2, 2);
+      if (nch > 3) loadw(a3, 3);
+      prefetch_h();   // after the A loads: waiting for A does not wait for H
       TS_FENCE();
-      for (; c + 7 <= full; c += 4) {
-        loadA(a3, c + 3); TS_FENCE(); compute(a0, c); TS_FENCE();
-        loadA(a0, c + 4); TS_FENCE(); compute(a1, c + 1); TS_FENCE();
-        loadA(a1, c + 5); TS_FENCE(); compute(a2, c + 2); TS_FENCE();
-        loadA(a2, c + 6); TS_FENCE(); compute(a3, c + 3); TS_FENCE();
+      maskw(a0, 0); compute(a0, 0);
+      if (nch > 1) { maskw(a1, 1); compute(a1, 1); }
+      if (nch > 2) { maskw(a2, 2); compute(a2, 2); }
+      if (nch > 3) { maskw(a3, 3); compute(a3, 3); }
+    } else {
+      prefetch_h();
+      int64_t c = 0;
+      if (full >= 3) {
+        loadA(a0, 0); loadA(a1, 1); loadA(a2, 2);
+        TS_FENCE();
+        for (; c + 7 <= full; c += 4) {
+          loadA(a3, c + 3); TS_FENCE(); compute(a0, c); TS_FENCE();
+          loadA(a0, c + 4); TS_FENCE(); compute(a1, c + 1); TS_FENCE();
+          loadA(a1, c + 5); TS_FENCE(); compute(a2, c + 2); TS_FENCE();
+          loadA(a2, c + 6); TS_FENCE(); compute(a3, c + 3); TS_FENCE();
+        }
+        compute(a0, c); compute(a1, c + 1); compute(a2, c + 2);
+        c += 3;
       }
-      compute(a0, c); compute(a1, c + 1); compute(a2, c + 2);
-      c += 3;
-    }
-    for (; c < full; ++c) { loadA(a0, c); compute(a0, c); }
-#undef TS_FENCE
-    if (c < nch) {   // the chunk that straddles K: mask k >= K (B rows there are zero too)
-      const int64_t kl = c * KC + (lane >> 4) * VE;
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
+      for (; c < full; ++c) { loadA(a0, c); compute(a0, c); }
+      if (c < nch) {   // the chunk that straddles K: mask k >= K (B rows there are zero too)
+        const int64_t kl = c * KC + (lane >> 4) * VE;
         // a vector starting below K ends inside the row (lda >= K rounded up to 8)
-        a0[tm] = kl < p.K ? ldg16(arow[tm] + c * KC) : make_uint4(0, 0, 0, 0);
-        T* e = reinterpret_cast<T*>(&a0[tm]);
+        const int64_t nk = p.K - kl;
+        const int vk = nk <= 0 ? 0 : nk >= VE ? VE : (int)nk;
 #pragma unroll
-        for (int j = 0; j < VE; ++j)
-          if (kl + j >= p.K) e[j] = T(0);
+        for (int tm = 0; tm < TM; ++tm) a0[tm] = ldg16(arow[tm] + (vk > 0 ? c * KC : -(lane >> 4) * VE));
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) a0[tm] = keep_first<T>(a0[tm], vk);
+        compute(a0, c);
       }
-      compute(a0, c);
     }
+#undef TS_FENCE
 
     // ---- epilogue: per 16-row tile, MFMA layout -> LDS -> row vectors
 #pragma unroll
@@ -205,16 +258,21 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      for (int idx = lane; idx < 16 * vpr; idx += 64) {
+      constexpr int NIT = 16 * 128 / Vec<T>::N / 64;   // iterations covering nblk <= 128
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        const int idx = lane + 64 * it;
+        if (idx >= 16 * vpr) break;
         const int rr = idx / vpr, cv = idx % vpr;
         const int64_t row = r0 + tm * 16 + rr, col = n0 + cv * OV;
         if (row >= p.M || col >= p.N) continue;
         float v[OV];
 #pragma unroll
         for (int j = 0; j < OV; ++j) v[j] = myC[rr * ldc + cv * OV + j];
-        if (p.epi.mode == EPI_DMASK && p.epi.relu) {
+        if constexpr (dmask) {
           float h[OV];
-          unpack<T>(ldg16(reinterpret_cast<const T*>(p.epi.hmask) + row * p.epi.ldh + col), h);
+          if constexpr (HPRE) unpack<T>(hv[tm][it], h);
+          else unpack<T>(ldg16(reinterpret_cast<const T*>(p.epi.hmask) + row * p.epi.ldh + col), h);
 #pragma unroll
           for (int j = 0; j < OV; ++j) v[j] = h[j] > 0.f ? v[j] * p.epi.keep_scale : 0.f;
         }
@@ -237,7 +295,7 @@ int ts_nblk(int64_t N, int64_t kpad) {
   return (int)nb;
 }
 
-template <typename T, bool BKC, int TM>
+template <typename T, bool BKC, bool DM, int TM>
 hipError_t launch_tm(const TsParams& p, hipStream_t s) {
   const int tnw = p.nblk / 16;
   const size_t lds = ((size_t)p.nblk * (p.kpad + Vec<T>::N) * sizeof(T) + 15) / 16 * 16 +
@@ -250,11 +308,11 @@ hipError_t launch_tm(const TsParams& p, hipStream_t s) {
 #define TS_L(TNW_)                                                                                          \
   do {                                                                                                      \
     if (lds > 65536) {                                                                                      \
-      hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&tsgemm_kernel<T, BKC, TM, TNW_>),  \
+      hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&tsgemm_kernel<T, BKC, DM, TM, TNW_>),  \
                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);           \
       if (ea != hipSuccess) return ea;                                                                      \
     }                                                                                                       \
-    hipLaunchKernelGGL((tsgemm_kernel<T, BKC, TM, TNW_>), grid, dim3(256), lds, s, p);                     \
+    hipLaunchKernelGGL((tsgemm_kernel<T, BKC, DM, TM, TNW_>), grid, dim3(256), lds, s, p);                     \
   } while (0)
   if (tnw <= 1) TS_L(1);
   else if (tnw <= 2) TS_L(2);
@@ -264,21 +322,27 @@ hipError_t launch_tm(const TsParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <typename T, bool BKC>
+template <typename T, bool BKC, bool DM>
 hipError_t launch_b(TsParams p, hipStream_t s) {
   constexpr int KC = 4 * Vec<T>::N;
   p.kpad = (p.K + KC - 1) / KC * KC;
   p.nblk = ts_nblk<T>(p.N, p.kpad);
-  // rows per wave: 64 when there are enough rows to fill the GPU twice, else fewer
+  // rows per wave: 32 when there are enough rows to fill the GPU, else 16
   const int64_t tiles64 = (p.M + 255) / 256 * ((p.N + p.nblk - 1) / p.nblk);
-  if (tiles64 >= 512) return launch_tm<T, BKC, 4>(p, s);
-  if (tiles64 >= 256) return launch_tm<T, BKC, 2>(p, s);
-  return launch_tm<T, BKC, 1>(p, s);
+  // (TM = 4 would need more than 256 registers per lane with the whole-K
+  // fragment sets, i.e. one wave per SIMD; TM = 2 keeps two)
+  // (the H-mask epilogue with 128-column blocks holds another 32 registers:
+  // one row tile per wave keeps two waves per SIMD there)
+  if (tiles64 >= 256 && !(DM && p.nblk > 64)) return launch_tm<T, BKC, DM, 2>(p, s);
+  return launch_tm<T, BKC, DM, 1>(p, s);
 }
 
 template <typename T>
 hipError_t launch_t(const TsParams& p, bool bkc, hipStream_t s) {
-  return bkc ? launch_b<T, true>(p, s) : launch_b<T, false>(p, s);
+  const bool dm = p.epi.mode == EPI_DMASK && p.epi.relu;
+  if (!bkc && !dm) return launch_b<T, false, false>(p, s);
+  if (!dm) return launch_b<T, true, false>(p, s);
+  return bkc ? launch_b<T, true, true>(p, s) : launch_b<T, false, true>(p, s);
 }
 
 }  // namespace
