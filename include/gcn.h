@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 1
+#define GCN_ABI_VERSION 2
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -105,6 +105,8 @@ typedef struct gcn_adj {
   const int32_t* chunk_heavy;     /* [n_chunks] heavy-row slot of a chunk    */
   int64_t n_light;                /* rows listed in row_perm                 */
   const int32_t* row_perm;        /* [n_light] light rows, degree descending */
+  const int32_t* chunk_order;     /* [n_chunks] launch order of the chunks by
+                                     their first column, or NULL            */
 } gcn_adj;
 
 /* One layer: H (n x f_in, ld_in) -> H_out (n x f_out, ld_out); W is
@@ -192,12 +194,17 @@ gcn_status gcn_densify(const gcn_adj* A, int32_t format, int32_t value_prec, voi
 
 /* ---------------------------------------------------------------------------
  * gcn_schedule: fill the heavy-row fields of a CSR gcn_adj (n, nnz, index,
- * rowptr must be set) so that rows with more than heavy_threshold entries
- * are aggregated in chunks of chunk_nnz entries by separate workgroups and
- * summed in a fixed order (run-to-run deterministic).  heavy_threshold <= 0
- * and chunk_nnz <= 0 select the defaults (512 and 2048).  sched: device
- * buffer of at least gcn_schedule_size() bytes that must outlive every use
- * of *A.  Synchronises `stream` once.
+ * rowptr, colidx must be set) so that rows with more than heavy_threshold
+ * entries are aggregated in chunks of chunk_nnz entries by separate
+ * workgroups and summed in a fixed order (run-to-run deterministic), the
+ * remaining rows listed by decreasing length (row_perm), and the chunks
+ * launched in order of their first column (chunk_order; chunks of
+ * different hubs that cover the same column range then run together and
+ * share the cached rows of X).  The launch orders are permutations whose
+ * ties may come out in any order; results do not depend on them.
+ * heavy_threshold <= 0 and chunk_nnz <= 0 select the defaults (512 and
+ * 2048).  sched: device buffer of at least gcn_schedule_size() bytes that
+ * must outlive every use of *A.  Synchronises `stream` once.
  * ------------------------------------------------------------------------- */
 gcn_status gcn_schedule_size(int64_t n, int64_t nnz, int64_t heavy_threshold, int64_t chunk_nnz,
                              size_t* bytes);

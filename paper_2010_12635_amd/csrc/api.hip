@@ -81,6 +81,7 @@ CsrView view_of(const gcn_adj* A) {
   v.heavy_rows = A->heavy_rows; v.heavy_chunk_off = A->heavy_chunk_off; v.chunk_heavy = A->chunk_heavy;
   v.n_light = A->row_perm ? A->n_light : 0;
   v.row_perm = A->row_perm;
+  v.chunk_order = A->n_heavy > 0 ? A->chunk_order : nullptr;
   return v;
 }
 
@@ -285,17 +286,17 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, 
                         void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (!A || !sched) return GCN_ERR_INVALID_ARG;
-  if (A->format != GCN_CSR || !A->rowptr) return GCN_ERR_INVALID_ARG;
+  if (A->format != GCN_CSR || !A->rowptr || (A->nnz > 0 && !A->colidx)) return GCN_ERR_INVALID_ARG;
   if (A->index != GCN_I32 && A->index != GCN_I64) return GCN_ERR_INVALID_ARG;
   if (A->n <= 0 || A->nnz < 0) return GCN_ERR_SHAPE;
   if (heavy_threshold <= 0) heavy_threshold = DEFAULT_HEAVY;
   if (chunk_nnz <= 0) chunk_nnz = DEFAULT_CHUNK;
   if (sched_bytes < schedule_bytes(A->n, A->nnz, heavy_threshold, chunk_nnz)) return GCN_ERR_WORKSPACE;
   if (!aligned16(sched)) return GCN_ERR_ALIGNMENT;
-  int32_t *hr = nullptr, *hco = nullptr, *ch = nullptr, *perm = nullptr;
+  int32_t *hr = nullptr, *hco = nullptr, *ch = nullptr, *perm = nullptr, *corder = nullptr;
   int64_t nh = 0, nc = 0, nl = 0;
-  hipError_t e = schedule_run(A->n, A->nnz, A->index == GCN_I64, A->rowptr, heavy_threshold, chunk_nnz, sched,
-                              sched_bytes, &hr, &hco, &ch, &perm, &nh, &nc, &nl, s);
+  hipError_t e = schedule_run(A->n, A->nnz, A->index == GCN_I64, A->rowptr, A->colidx, heavy_threshold, chunk_nnz,
+                              sched, sched_bytes, &hr, &hco, &ch, &perm, &corder, &nh, &nc, &nl, s);
   if (e != hipSuccess) return GCN_ERR_DEVICE;
   A->heavy_threshold = heavy_threshold;
   A->chunk_nnz = chunk_nnz;
@@ -306,6 +307,7 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, 
   A->chunk_heavy = ch;
   A->row_perm = perm;
   A->n_light = nl;
+  A->chunk_order = corder;
   return finish(hipSuccess, s);
 }
 

@@ -67,6 +67,7 @@ struct CsrView {
   const int32_t* chunk_heavy;
   int64_t n_light;
   const int32_t* row_perm;   // light rows, degree descending (NULL: index order)
+  const int32_t* chunk_order;  // launch order of the heavy chunks (NULL: chunk order)
 };
 // Y = A_hat X (+ epilogue) for X: n x F (ld), Y described by epi.
 int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F);
@@ -109,11 +110,11 @@ hipError_t normalize_run(int64_t n, int64_t num_edges, const int32_t* src, const
                          int64_t* nnz_out, int32_t* bad_ids, void* ws, size_t ws_bytes,
                          hipStream_t s);
 size_t schedule_bytes(int64_t n, int64_t nnz, int64_t threshold, int64_t chunk_nnz);
-hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr,
+hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, const int32_t* colidx,
                         int64_t threshold, int64_t chunk_nnz, void* sched, size_t sched_bytes,
                         int32_t** heavy_rows, int32_t** heavy_chunk_off, int32_t** chunk_heavy,
-                        int32_t** row_perm, int64_t* n_heavy, int64_t* n_chunks, int64_t* n_light,
-                        hipStream_t s);
+                        int32_t** row_perm, int32_t** chunk_order, int64_t* n_heavy, int64_t* n_chunks,
+                        int64_t* n_light, hipStream_t s);
 
 // ----------------------------------------------------------------- loss ----
 size_t loss_workspace_bytes(int64_t n, int64_t C);

@@ -352,6 +352,32 @@ __global__ void light_scatter_kernel(int64_t n, const IdxT* __restrict__ rowptr,
   }
 }
 
+// Chunk launch order: counting sort of the chunks by the column bucket of
+// their first entry (CHUNK_BUCKETS buckets over [0, n)).
+constexpr int64_t CHUNK_BUCKETS = 4096;
+
+template <typename IdxT>
+__global__ void chunk_key_kernel(int64_t n, int64_t n_chunks, const IdxT* __restrict__ rowptr,
+                                 const int32_t* __restrict__ colidx, const int32_t* __restrict__ heavy_rows,
+                                 const int32_t* __restrict__ heavy_chunk_off, const int32_t* __restrict__ chunk_heavy,
+                                 int64_t chunk, int32_t* __restrict__ key, int32_t* __restrict__ hist) {
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t h = chunk_heavy[c];
+    const int64_t start = (int64_t)rowptr[heavy_rows[h]] + (c - heavy_chunk_off[h]) * chunk;
+    const int32_t b = (int32_t)((int64_t)colidx[start] * CHUNK_BUCKETS / n);
+    key[c] = b;
+    atomicAdd(&hist[b], 1);
+  }
+}
+
+__global__ void chunk_scatter_kernel(int64_t n_chunks, const int32_t* __restrict__ key, const int64_t* __restrict__ boff,
+                                     int32_t* __restrict__ cur, int32_t* __restrict__ order) {
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t b = key[c];
+    order[boff[b] + atomicAdd(&cur[b], 1)] = (int32_t)c;
+  }
+}
+
 }  // namespace
 
 hipError_t fill_zero(void* p, size_t bytes, hipStream_t s) {
@@ -450,8 +476,14 @@ hipError_t normalize_run(int64_t n, int64_t E, const int32_t* src, const int32_t
 
 size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
   const int64_t max_chunks = nnz / chunk_nnz + n + 1;
-  const int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
+  int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
+  if (scan_n < CHUNK_BUCKETS + 1) scan_n = CHUNK_BUCKETS + 1;
   size_t b = 0;
+  b += align256(sizeof(int32_t) * max_chunks);                  // chunk_order
+  b += align256(sizeof(int32_t) * max_chunks);                  // chunk keys
+  b += align256(sizeof(int32_t) * CHUNK_BUCKETS);               // chunk bucket histogram
+  b += align256(sizeof(int32_t) * CHUNK_BUCKETS);               // chunk bucket cursors
+  b += align256(sizeof(int64_t) * (CHUNK_BUCKETS + 1));         // chunk bucket offsets
   b += align256(sizeof(int32_t) * n);                           // heavy_rows
   b += align256(sizeof(int32_t) * (n + 1));                     // heavy_chunk_off
   b += align256(sizeof(int32_t) * max_chunks);                  // chunk_heavy
@@ -465,14 +497,20 @@ size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
   return b;
 }
 
-hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, int64_t thr, int64_t chunk,
-                        void* sched, size_t sched_bytes, int32_t** heavy_rows, int32_t** heavy_chunk_off,
-                        int32_t** chunk_heavy, int32_t** row_perm, int64_t* n_heavy, int64_t* n_chunks,
-                        int64_t* n_light, hipStream_t s) {
+hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, const int32_t* colidx, int64_t thr,
+                        int64_t chunk, void* sched, size_t sched_bytes, int32_t** heavy_rows,
+                        int32_t** heavy_chunk_off, int32_t** chunk_heavy, int32_t** row_perm, int32_t** chunk_order,
+                        int64_t* n_heavy, int64_t* n_chunks, int64_t* n_light, hipStream_t s) {
   char* w = static_cast<char*>(sched);
   auto take = [&](size_t bytes) { char* p = w; w += align256(bytes); return p; };
   const int64_t max_chunks = nnz / chunk + n + 1;
-  const int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
+  int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
+  if (scan_n < CHUNK_BUCKETS + 1) scan_n = CHUNK_BUCKETS + 1;
+  int32_t* corder = (int32_t*)take(sizeof(int32_t) * max_chunks);
+  int32_t* ckey = (int32_t*)take(sizeof(int32_t) * max_chunks);
+  int32_t* chist = (int32_t*)take(sizeof(int32_t) * CHUNK_BUCKETS);
+  int32_t* ccur = (int32_t*)take(sizeof(int32_t) * CHUNK_BUCKETS);
+  int64_t* cboff = (int64_t*)take(sizeof(int64_t) * (CHUNK_BUCKETS + 1));
   int32_t* hr = (int32_t*)take(sizeof(int32_t) * n);
   int32_t* hco = (int32_t*)take(sizeof(int32_t) * (n + 1));
   int32_t* ch = (int32_t*)take(sizeof(int32_t) * max_chunks);
@@ -519,6 +557,24 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   GCN_TRY(hipMemcpyAsync(&host[1], choff + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipMemcpyAsync(&host[2], boff + thr + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipStreamSynchronize(s));
+  // chunks in order of the column bucket of their first entry
+  const int64_t nch = host[1];
+  *chunk_order = nullptr;
+  if (nch > 0 && colidx) {
+    GCN_TRY(fill_zero(chist, sizeof(int32_t) * CHUNK_BUCKETS, s));
+    GCN_TRY(fill_zero(ccur, sizeof(int32_t) * CHUNK_BUCKETS, s));
+    if (idx64)
+      hipLaunchKernelGGL(chunk_key_kernel<int64_t>, dim3(grid_for(nch)), dim3(256), 0, s, n, nch, (const int64_t*)rowptr, colidx, hr, hco, ch, chunk, ckey, chist);
+    else
+      hipLaunchKernelGGL(chunk_key_kernel<int32_t>, dim3(grid_for(nch)), dim3(256), 0, s, n, nch, (const int32_t*)rowptr, colidx, hr, hco, ch, chunk, ckey, chist);
+    GCN_TRY(hipGetLastError());
+    hipLaunchKernelGGL(widen_kernel, dim3(grid_for(CHUNK_BUCKETS + 1)), dim3(256), 0, s, CHUNK_BUCKETS, chist, cboff);
+    GCN_TRY(hipGetLastError());
+    GCN_TRY(scan_exclusive(cboff, CHUNK_BUCKETS + 1, scr, s));
+    hipLaunchKernelGGL(chunk_scatter_kernel, dim3(grid_for(nch)), dim3(256), 0, s, nch, ckey, cboff, ccur, corder);
+    GCN_TRY(hipGetLastError());
+    *chunk_order = corder;
+  }
 #undef GCN_TRY
   *heavy_rows = hr; *heavy_chunk_off = hco; *chunk_heavy = ch; *row_perm = perm;
   *n_heavy = host[0]; *n_chunks = host[1]; *n_light = host[2];

@@ -12,7 +12,10 @@
 //    wave walk rows of similar length.  fp32 accumulation.
 //  * Heavy rows (power-law hubs): split into chunks of chunk_nnz entries;
 //    one workgroup per chunk reduces its entries across 256/LPR lane groups
-//    through LDS in a fixed order into an fp32 partial row; a fixup kernel
+//    through LDS in a fixed order into an fp32 partial row.  Chunks are
+//    launched in the schedule's order of their first column, so chunks of
+//    different hubs that cover the same columns run at the same time and
+//    find those rows of X in cache.  A fixup kernel
 //    sums the partials of each heavy row in chunk order and applies the
 //    epilogue.  No atomics: results are run-to-run identical.
 #include "internal.h"
@@ -103,6 +106,7 @@ struct HeavyParams {
   const int32_t* heavy_rows;
   const int32_t* heavy_chunk_off;
   const int32_t* chunk_heavy;
+  const int32_t* chunk_order;   // launch order (may be NULL)
   int64_t chunk_nnz;
   int64_t n_chunks;
   const void* X;
@@ -119,7 +123,7 @@ __global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT>
   constexpr int VE = Vec<T>::N;
   constexpr int NG = 256 / LPR;
   __shared__ float red[4 * LPR * VE];
-  const int64_t chunk = blockIdx.x;
+  const int64_t chunk = p.chunk_order ? (int64_t)p.chunk_order[blockIdx.x] : (int64_t)blockIdx.x;
   const int g = threadIdx.x / LPR, li = threadIdx.x % LPR;
   const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
   const int32_t h = p.chunk_heavy[chunk];
@@ -207,6 +211,7 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   HeavyParams<IdxT> hp;
   hp.rowptr = p.rowptr; hp.colidx = A.colidx; hp.values = A.values; hp.dinv = A.dinv;
   hp.heavy_rows = A.heavy_rows; hp.heavy_chunk_off = A.heavy_chunk_off; hp.chunk_heavy = A.chunk_heavy;
+  hp.chunk_order = A.chunk_order;
   hp.chunk_nnz = A.chunk_nnz; hp.n_chunks = A.n_chunks;
   hp.X = X; hp.ldx = ldx; hp.F = F;
   hp.ldp = colblocks * LPR * VE;

@@ -63,6 +63,7 @@ class GcnAdj(ctypes.Structure):
         ("n_heavy", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
         ("heavy_rows", ctypes.c_void_p), ("heavy_chunk_off", ctypes.c_void_p),
         ("chunk_heavy", ctypes.c_void_p), ("n_light", ctypes.c_int64), ("row_perm", ctypes.c_void_p),
+        ("chunk_order", ctypes.c_void_p),
     ]
 
 

@@ -128,6 +128,13 @@ def test_schedule_lists_heavy_rows():
     assert a.n_light == light.size
     assert np.array_equal(np.sort(perm), light)
     assert np.all(np.diff(g.deg[perm]) <= 0)
+    # chunk launch order: every chunk once, first columns in non-decreasing buckets
+    order = base[off(a.chunk_order): off(a.chunk_order) + 4 * a.n_chunks].view(torch.int32).cpu().numpy()
+    assert np.array_equal(np.sort(order), np.arange(a.n_chunks))
+    owner = np.repeat(np.arange(heavy.size), np.diff(want))
+    first = np.array([g.rowptr[heavy[owner[c]]] + (c - want[owner[c]]) * 64 for c in range(a.n_chunks)])
+    bucket = g.colidx[first].astype(np.int64) * 4096 // n
+    assert np.all(np.diff(bucket[order]) >= 0)
 
 
 # ------------------------------------------------------------ layer fwd ----
