@@ -242,18 +242,20 @@ def summarize_counters(fetch_dir, write_dir, out_path, command):
 
     kernels = sorted(fetch, key=lambda k: -sum(fetch[k]))
     rows_out = []
-    for k in kernels[:16]:
+    for k in kernels[:24]:
         rows_out.append((k, len(fetch[k]), avg(fetch, k) * f_scale, avg(write, k) * w_scale))
-    agg = [r for r in rows_out if "dense_agg_kernel" in r[0] and ("DF16" in r[0] or "half" in r[0])]
-    per_launch = sum(r[2] + r[3] for r in agg) / max(1, len(agg))
+    # one dense aggregation = one transposition of X + one dense_agg_kernel
+    agg = [r for r in rows_out if "dense_agg_kernel" in r[0] and "DF16" in r[0]]
+    xp = [r for r in rows_out if "transpose_tiled_kernel" in r[0] and "DF16" in r[0]]
+    per_launch = sum(r[2] + r[3] for r in agg) / max(1, len(agg)) + sum(r[2] + r[3] for r in xp) / max(1, len(xp))
     spmm = [r for r in rows_out if "spmm_" in r[0] and "DF16" in r[0]]
     summary = {
         "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
         "dense_agg_f16": int(per_launch),
         "dense_agg_f16_source_hash": kernel_hash("dense_agg.hip", "xpose.h"),
-        # light + heavy kernels of one F=hidden and one F=classes aggregation, halved: bytes per launch
+        # light, heavy and fixup kernels of one F=hidden and one F=classes aggregation, halved: bytes per launch
         "spmm_f16": int(sum(r[2] + r[3] for r in spmm) / 2),
-        "spmm_f16_source_hash": kernel_hash("spmm.hip"),
+        "spmm_f16_source_hash": kernel_hash("spmm.hip", "normalize.hip"),
     }
     lines = ["# HBM traffic counters: dense aggregation (SBM n=16384) and CSR aggregation (R-MAT scale 21), fp16", "",
              "Commands (from the repository root, on one MI355X; one counter per run):", "", "```", command, "```", "",
@@ -388,7 +390,7 @@ def main():
     achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9
     traffic = None
     if prec != 0:
-        traffic = load_traffic("dense_agg_f16", "dense_agg.hip", "xpose.h") if spec.dense_adj else load_traffic("spmm_f16", "spmm.hip")
+        traffic = load_traffic("dense_agg_f16", "dense_agg.hip", "xpose.h") if spec.dense_adj else load_traffic("spmm_f16", "spmm.hip", "normalize.hip")
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kname,
                     launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
@@ -410,7 +412,7 @@ def main():
                     launches=r2["agg_launches"], avg_launch_us=round(r2["agg_ms"] * 1e3 / r2["agg_launches"], 2),
                     algorithmic_bytes_per_launch_avg=int(b2 / 2),
                     gather_bytes_per_launch_avg=int(r2["nnz"] * (r2["f_h"] + r2["C"]) * s / 2),
-                    traffic=load_traffic("spmm_f16", "spmm.hip") if prec != 0 and args.spmm_workload == "rmat21" else None,
+                    traffic=load_traffic("spmm_f16", "spmm.hip", "normalize.hip") if prec != 0 and args.spmm_workload == "rmat21" else None,
                     peak_mem_bytes=r2["peak_bytes"])
         log(f"[bench] spmm: {spmm['ms_per_step']} ms/epoch, {spmm['achieved']} GB/s algorithmic")
         del wl2
