@@ -143,6 +143,74 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     return res
 
 
+def _scale_run(scale, pname, epochs, seed):
+    """One scale-test point; every device buffer it allocates is local, so
+    it is freed when the call returns (or its exception is handled)."""
+    import torch
+    from paper_2010_12635_amd import gcn as G
+    from paper_2010_12635_amd import inputs as I
+    from paper_2010_12635_amd.model import DeviceGraph, GCN2
+
+    prec = PRECS[pname]
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    t0 = time.perf_counter()
+    log(f"[scale] {pname} scale {scale}: drawing the graph on the device")
+    wl = I.scale_workload_device(scale, seed, dtype=G.torch_dtype(prec))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"[scale] {pname} scale {scale}: normalize + schedule ({wl['src'].numel()} samples)")
+    dg = DeviceGraph(wl["n"], wl["src"], wl["dst"], prec=prec, index=G.GCN_I64)
+    del wl["src"], wl["dst"]
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    log(f"[scale] {pname} scale {scale}: nnz {dg.nnz}; building the model")
+    m = GCN2(dg, wl["X"], wl["labels"], wl["mask"], wl["W1"], wl["W2"], wl["b1"], wl["b2"], prec=prec,
+             dropout=0.5, seed=wl["dropout_seed"], loss_scale=65536.0)
+    del wl
+    m.step(0)
+    torch.cuda.synchronize()
+    log(f"[scale] {pname} scale {scale}: first epoch done; timing {epochs}")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for k in range(epochs):
+        m.step(1 + k)
+    e1.record()
+    torch.cuda.synchronize()
+    return dict(ok=True, nnz=int(dg.nnz), ms_per_epoch=round(e0.elapsed_time(e1) / epochs, 2),
+                peak_mem_bytes=int(torch.cuda.max_memory_allocated() - base), loss=float(m.loss.item()),
+                draw_s=round(t1 - t0, 2), normalize_s=round(t2 - t1, 2))
+
+
+def scale_test(start, stop, precs, epochs, seed):
+    """Largest graph trained within the device memory: R-MAT graphs of
+    growing scale (edge factor 16, features 128, hidden 128, 64 classes,
+    int64 row pointers), drawn on the device, each trained for 1 + `epochs`
+    epochs per precision until torch cannot allocate the next one."""
+    import gc
+    import torch
+
+    results, largest = [], {}
+    for pname in precs:
+        for scale in range(start, stop + 1):
+            rec = dict(prec=pname, scale=scale, n=1 << scale)
+            try:
+                rec.update(_scale_run(scale, pname, epochs, seed))
+                largest[pname] = dict(scale=scale, n=rec["n"], nnz=rec["nnz"], peak_mem_bytes=rec["peak_mem_bytes"],
+                                      ms_per_epoch=rec["ms_per_epoch"])
+            except torch.cuda.OutOfMemoryError as e:
+                rec.update(ok=False, error="torch out of memory: " + str(e).split("\n")[0][:160])
+            gc.collect()
+            torch.cuda.empty_cache()
+            log(f"[scale] {json.dumps(rec)} (allocated after cleanup: {torch.cuda.memory_allocated()})")
+            results.append(rec)
+            if not rec["ok"]:
+                break
+    total = torch.cuda.get_device_properties(0).total_memory
+    return dict(scale_test=results, largest=largest, device_memory_bytes=int(total))
+
+
 def cpu_baseline(wl, budget_s):
     """The oracle, as it stands, on a bounded sample: full training epochs
     (fp64) of the same workload until ``budget_s`` seconds have passed."""
@@ -312,10 +380,16 @@ def main():
     ap.add_argument("--prec", default="f16", choices=sorted(PRECS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-fp32", action="store_true", help="skip the fp32-mode run")
+    ap.add_argument("--no-largest", dest="largest", action="store_false",
+                    help="skip the largest-graph runs (R-MAT scale 27 fp16, 26 and 27 fp32)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0 = skip)")
     ap.add_argument("--spmm-workload", default="rmat21",
                     help="CSR workload whose aggregation bandwidth is reported as 'spmm' ('none' = skip)")
     ap.add_argument("--spmm-steps", type=int, default=10)
+    ap.add_argument("--scale-test", nargs=2, type=int, metavar=("FIRST", "LAST"),
+                    help="train R-MAT graphs of scale FIRST..LAST (fp16, then fp32) until device memory runs out; "
+                         "prints one JSON line and exits")
+    ap.add_argument("--scale-epochs", type=int, default=2)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before the runs, copy a MIB-MiB device buffer 3 times (reference kernel for "
                          "hardware traffic counters)")
@@ -328,15 +402,15 @@ def main():
     if args.summarize_stats:
         d, out, title = args.summarize_stats
         cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_default -o run -- "
-               "python3 bench.py --steps 50 --cpu-seconds 0")
+               "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest")
         summarize_stats(d, out, cmd, title)
         return
 
     if args.summarize_counters:
         cmd = ("rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --copy-calibration 256\n"
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --copy-calibration 256\n"
                "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --copy-calibration 256")
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --copy-calibration 256")
         print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, cmd)))
         return
 
@@ -352,6 +426,11 @@ def main():
         build()
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    if args.scale_test:
+        print(json.dumps(scale_test(args.scale_test[0], args.scale_test[1], ["f16", "f32"], args.scale_epochs,
+                                    args.seed)), flush=True)
+        return
 
     if args.copy_calibration > 0:
         nbytes = args.copy_calibration << 20
@@ -417,6 +496,28 @@ def main():
         log(f"[bench] spmm: {spmm['ms_per_step']} ms/epoch, {spmm['achieved']} GB/s algorithmic")
         del wl2
 
+    largest = None
+    if args.largest:
+        # the largest R-MAT graphs that train within the device memory (found
+        # by --scale-test): scale 27 in fp16, scale 26 in fp32; the fp32 run at
+        # scale 27 shows the bound (fp16 at scale 28 needs ~380 GB of
+        # activations alone)
+        import gc
+        largest = dict(workload="R-MAT edge factor 16 (0.57, 0.19, 0.19, 0.05) + self-loops, int64 row pointers, "
+                                "2-layer GCN 128 -> 128 -> 64, dropout 0.5, all vertices labelled; drawn on the device",
+                       device_memory_bytes=int(torch.cuda.get_device_properties(0).total_memory))
+        for pname, scale in (("f16", 27), ("f32", 26), ("f32", 27)):
+            key = f"{pname}_scale{scale}"
+            try:
+                rec = _scale_run(scale, pname, 2, args.seed)
+                largest[key] = dict(n=1 << scale, nnz=rec["nnz"], peak_mem_bytes=rec["peak_mem_bytes"],
+                                    ms_per_epoch=rec["ms_per_epoch"], epochs_per_s=round(1e3 / rec["ms_per_epoch"], 3))
+            except torch.cuda.OutOfMemoryError as e:
+                largest[key] = "does not fit: " + str(e).split("\n")[0][:120]
+            gc.collect()
+            torch.cuda.empty_cache()
+            log(f"[bench] largest graph {key}: {largest[key]}")
+
     cpu = None
     if args.cpu_seconds > 0:
         log("[bench] cpu oracle baseline")
@@ -452,6 +553,7 @@ def main():
         "loss_scale": r["scaler"],
         "roofline": roofline,
         "spmm": spmm,
+        "largest_graph": largest,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -351,13 +351,13 @@ __global__ __launch_bounds__(256) void densify_kernel(int64_t n, const IdxT* __r
                                                       const float* __restrict__ dinv, T* __restrict__ dense,
                                                       int64_t ld, int64_t nc) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= n) return;
-  const float dr = values ? 0.f : dinv[r];
-  for (int64_t k = (int64_t)rowptr[r] + lane; k < (int64_t)rowptr[r + 1]; k += 64) {
-    const int32_t c = colidx[k];
-    const T v = values ? values[k] : from_f32<T>(dr * dinv[c]);
-    dense[TILED ? tiled_off<T>(r, c, nc) : r * ld + c] = v;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < n; r += (int64_t)gridDim.x * 4) {
+    const float dr = values ? 0.f : dinv[r];
+    for (int64_t k = (int64_t)rowptr[r] + lane; k < (int64_t)rowptr[r + 1]; k += 64) {
+      const int32_t c = colidx[k];
+      const T v = values ? values[k] : from_f32<T>(dr * dinv[c]);
+      dense[TILED ? tiled_off<T>(r, c, nc) : r * ld + c] = v;
+    }
   }
 }
 
@@ -368,7 +368,7 @@ hipError_t densify_t(const CsrView& A, bool tiled, void* dense, int64_t ld, hipS
   const size_t bytes = tiled ? (size_t)((A.n + 63) / 64) * 64 * nc * KC * sizeof(T) : (size_t)A.n * ld * sizeof(T);
   hipError_t e = fill_zero(dense, bytes, s);
   if (e != hipSuccess) return e;
-  const dim3 g((unsigned)((A.n + 3) / 4));
+  const dim3 g((unsigned)std::min<int64_t>((A.n + 3) / 4, 1 << 20));   // the kernel loops over rows
   const T* vals = reinterpret_cast<const T*>(A.values);
   T* d = reinterpret_cast<T*>(dense);
   if (A.idx64) {

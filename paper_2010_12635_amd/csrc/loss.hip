@@ -45,8 +45,13 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane / LPR, li = lane % LPR;
   const int slot = wave * G + g;
-  const int64_t row = (int64_t)blockIdx.x * (4 * G) + slot;
   const int64_t col0 = (int64_t)li * VE;
+  // the workgroup walks row groups blockIdx.x, blockIdx.x + gridDim.x, ...
+  // (in that order for the per-slot sums)
+  float acc_loss = 0.f;
+  int32_t acc_corr = 0;
+  for (int64_t base = (int64_t)blockIdx.x * (4 * G); base < p.n; base += (int64_t)gridDim.x * (4 * G)) {
+  const int64_t row = base + slot;
   const bool row_ok = row < p.n;
   float z[VE];
 #pragma unroll
@@ -101,9 +106,12 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
     for (int i = 0; i < VE; ++i) bad |= !finite_f32(to_f32<T>(e[i]));
     if (bad) raise_flag(p.flag);
   }
+  acc_loss += in_mask ? (lse - zy) : 0.f;
+  acc_corr += (in_mask && am == y) ? 1 : 0;
+  }
   if (li == 0) {
-    s_loss[slot] = in_mask ? (lse - zy) : 0.f;
-    s_corr[slot] = (in_mask && am == y) ? 1 : 0;
+    s_loss[slot] = acc_loss;
+    s_corr[slot] = acc_corr;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -138,11 +146,16 @@ __global__ __launch_bounds__(256) void loss_final_kernel(const float* __restrict
   }
 }
 
+// Workgroups of the loss kernel: one per row group up to 65536 (each then
+// walks several groups).
+int64_t loss_blocks(int64_t n, int64_t rows_per_group) {
+  const int64_t nb = (n + rows_per_group - 1) / rows_per_group;
+  return nb < 65536 ? nb : 65536;
+}
+
 template <typename T, int LPR>
 hipError_t launch_cfg(const LossParams& p, hipStream_t s) {
-  constexpr int G = 64 / LPR;
-  const int64_t nb = (p.n + 4 * G - 1) / (4 * G);
-  hipLaunchKernelGGL((softmax_ce_kernel<T, LPR>), dim3((unsigned)nb), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((softmax_ce_kernel<T, LPR>), dim3((unsigned)loss_blocks(p.n, 4 * (64 / LPR))), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
@@ -179,8 +192,7 @@ size_t loss_workspace_bytes(int64_t n, int64_t C) {
 hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* logits, const int32_t* labels,
                        const uint8_t* mask, int64_t n_mask, const float* loss_scale, float* loss, void* dlogits,
                        int32_t* n_correct, int32_t* flag, void* ws, hipStream_t s) {
-  const int64_t rpb = rows_per_block(prec, C);
-  const int64_t nb = (n + rpb - 1) / rpb;
+  const int64_t nb = loss_blocks(n, rows_per_block(prec, C));
   LossParams p;
   p.n = n; p.C = C; p.ld = ld; p.logits = logits; p.labels = labels; p.mask = mask;
   p.inv_count = 1.f / (float)n_mask;

@@ -87,6 +87,16 @@ __global__ void fill_zero_kernel(uint32_t* p, int64_t words) {
     p[i] = 0u;
 }
 
+// Workgroups for one wave per row, 4 rows per workgroup of 256 threads; the
+// kernels loop over rows, so the grid is capped (a dispatch may not exceed
+// 2^32 work-items per dimension).
+unsigned wave_rows_grid(int64_t rows) {
+  int64_t g = (rows + 3) / 4;
+  if (g < 1) g = 1;
+  if (g > (1 << 20)) g = 1 << 20;
+  return (unsigned)g;
+}
+
 unsigned grid_for(int64_t items, int per_block = 256, int64_t cap = 65536) {
   int64_t g = (items + per_block - 1) / per_block;
   if (g < 1) g = 1;
@@ -140,24 +150,24 @@ __global__ void selfloop_kernel(int64_t n, const int64_t* __restrict__ off, cons
 __global__ __launch_bounds__(256) void sort_small_kernel(int64_t n, const int64_t* __restrict__ off,
                                                          int32_t* __restrict__ tmp, int32_t* __restrict__ ucnt) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= n) return;
-  const int64_t b = off[r], len = off[r + 1] - b;
-  if (len > 64) return;
-  int x = lane < len ? tmp[b + lane] : INT32_MAX;
-  for (int k = 2; k <= 64; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const int y = __shfl_xor(x, j);
-      const bool asc = (lane & k) == 0;
-      const bool lower = (lane & j) == 0;
-      x = (lower == asc) ? min(x, y) : max(x, y);
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < n; r += (int64_t)gridDim.x * 4) {
+    const int64_t b = off[r], len = off[r + 1] - b;
+    if (len > 64) continue;
+    int x = lane < len ? tmp[b + lane] : INT32_MAX;
+    for (int k = 2; k <= 64; k <<= 1) {
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        const int y = __shfl_xor(x, j);
+        const bool asc = (lane & k) == 0;
+        const bool lower = (lane & j) == 0;
+        x = (lower == asc) ? min(x, y) : max(x, y);
+      }
     }
+    const int prev = __shfl(x, lane == 0 ? 0 : lane - 1);
+    const bool flag = lane < len && (lane == 0 || x != prev);
+    const uint64_t bal = __ballot(flag);
+    if (lane < len) tmp[b + lane] = x;
+    if (lane == 0) ucnt[r] = __popcll(bal);
   }
-  const int prev = __shfl(x, lane == 0 ? 0 : lane - 1);
-  const bool flag = lane < len && (lane == 0 || x != prev);
-  const uint64_t bal = __ballot(flag);
-  if (lane < len) tmp[b + lane] = x;
-  if (lane == 0) ucnt[r] = __popcll(bal);
 }
 
 __device__ int block_sum_int(int v, int* red) {
@@ -260,29 +270,29 @@ __global__ __launch_bounds__(256) void compact_kernel(int64_t n, const int64_t* 
                                                       int32_t* __restrict__ colidx, int32_t* __restrict__ deg,
                                                       float* __restrict__ dinv) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r > n) return;
-  if (r == n) {
-    if (lane == 0) rowptr[n] = (IdxT)rp64[n];
-    return;
-  }
-  const int64_t b = off[r], len = off[r + 1] - b;
-  const int64_t o = rp64[r];
-  int64_t run = 0;
-  for (int64_t base = 0; base < len; base += 64) {
-    const int64_t i = base + lane;
-    const int x = i < len ? tmp[b + i] : 0;
-    const bool flag = i < len && (i == 0 || x != tmp[b + i - 1]);
-    const uint64_t bal = __ballot(flag);
-    const int pre = __popcll(bal & __lanemask_lt());
-    if (flag) colidx[o + run + pre] = x;
-    run += __popcll(bal);
-  }
-  if (lane == 0) {
-    rowptr[r] = (IdxT)o;
-    const int32_t d = ucnt[r];
-    if (deg) deg[r] = d;
-    dinv[r] = (float)(1.0 / sqrt((double)d));
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r <= n; r += (int64_t)gridDim.x * 4) {
+    if (r == n) {
+      if (lane == 0) rowptr[n] = (IdxT)rp64[n];
+      continue;
+    }
+    const int64_t b = off[r], len = off[r + 1] - b;
+    const int64_t o = rp64[r];
+    int64_t run = 0;
+    for (int64_t base = 0; base < len; base += 64) {
+      const int64_t i = base + lane;
+      const int x = i < len ? tmp[b + i] : 0;
+      const bool flag = i < len && (i == 0 || x != tmp[b + i - 1]);
+      const uint64_t bal = __ballot(flag);
+      const int pre = __popcll(bal & __lanemask_lt());
+      if (flag) colidx[o + run + pre] = x;
+      run += __popcll(bal);
+    }
+    if (lane == 0) {
+      rowptr[r] = (IdxT)o;
+      const int32_t d = ucnt[r];
+      if (deg) deg[r] = d;
+      dinv[r] = (float)(1.0 / sqrt((double)d));
+    }
   }
 }
 
@@ -291,14 +301,14 @@ __global__ __launch_bounds__(256) void values_kernel(int64_t n, const int64_t* _
                                                      const int32_t* __restrict__ colidx, const float* __restrict__ dinv,
                                                      T* __restrict__ values, T* __restrict__ dense, int64_t ld_dense) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= n) return;
-  const float dr = dinv[r];
-  for (int64_t k = rp64[r] + lane; k < rp64[r + 1]; k += 64) {
-    const int32_t c = colidx[k];
-    const T v = from_f32<T>(dr * dinv[c]);
-    if (values) values[k] = v;
-    if (dense) dense[r * ld_dense + c] = v;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < n; r += (int64_t)gridDim.x * 4) {
+    const float dr = dinv[r];
+    for (int64_t k = rp64[r] + lane; k < rp64[r + 1]; k += 64) {
+      const int32_t c = colidx[k];
+      const T v = from_f32<T>(dr * dinv[c]);
+      if (values) values[k] = v;
+      if (dense) dense[r * ld_dense + c] = v;
+    }
   }
 }
 
@@ -331,24 +341,64 @@ __global__ void heavy_fill_kernel(int64_t n, const IdxT* __restrict__ rowptr, in
   }
 }
 
-// Histogram of light rows over buckets thr - deg (deg <= thr).
-template <typename IdxT>
-__global__ void light_hist_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr, int32_t* __restrict__ hist) {
-  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
-    if (d <= thr) atomicAdd(&hist[thr - d], 1);
-  }
+// Light rows by decreasing degree: counting sort over buckets thr - deg
+// (deg <= thr).  A workgroup owns a contiguous range of rows and first
+// counts them per bucket in LDS, so the global atomics are one per bucket
+// and workgroup instead of one per row (most rows of a power-law graph fall
+// into a handful of buckets).  Buckets beyond LIGHT_LDS_BINS use global
+// atomics directly.
+constexpr int LIGHT_LDS_BINS = 1024;
+
+__device__ __forceinline__ void row_range(int64_t n, int64_t* r0, int64_t* r1) {
+  const int64_t per = (n + gridDim.x - 1) / gridDim.x;
+  *r0 = (int64_t)blockIdx.x * per;
+  *r1 = *r0 + per < n ? *r0 + per : n;
 }
 
 template <typename IdxT>
-__global__ void light_scatter_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
-                                     const int64_t* __restrict__ boff, int32_t* __restrict__ cur,
-                                     int32_t* __restrict__ perm) {
-  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n; r += (int64_t)gridDim.x * blockDim.x) {
+__global__ __launch_bounds__(256) void light_hist_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
+                                                         int32_t* __restrict__ hist) {
+  __shared__ int32_t lh[LIGHT_LDS_BINS];
+  for (int b = threadIdx.x; b < LIGHT_LDS_BINS; b += 256) lh[b] = 0;
+  __syncthreads();
+  int64_t r0, r1;
+  row_range(n, &r0, &r1);
+  for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
     const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
     if (d > thr) continue;
     const int64_t b = thr - d;
-    perm[boff[b] + atomicAdd(&cur[b], 1)] = (int32_t)r;
+    if (b < LIGHT_LDS_BINS) atomicAdd(&lh[b], 1);
+    else atomicAdd(&hist[b], 1);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < LIGHT_LDS_BINS && b <= thr; b += 256)
+    if (lh[b]) atomicAdd(&hist[b], lh[b]);
+}
+
+template <typename IdxT>
+__global__ __launch_bounds__(256) void light_scatter_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
+                                                            const int64_t* __restrict__ boff, int32_t* __restrict__ cur,
+                                                            int32_t* __restrict__ perm) {
+  __shared__ int32_t lh[LIGHT_LDS_BINS];     // count, then this workgroup's base within the bucket
+  __shared__ int32_t lc[LIGHT_LDS_BINS];     // local cursor
+  for (int b = threadIdx.x; b < LIGHT_LDS_BINS; b += 256) { lh[b] = 0; lc[b] = 0; }
+  __syncthreads();
+  int64_t r0, r1;
+  row_range(n, &r0, &r1);
+  for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
+    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
+    if (d <= thr && thr - d < LIGHT_LDS_BINS) atomicAdd(&lh[thr - d], 1);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < LIGHT_LDS_BINS && b <= thr; b += 256)
+    if (lh[b]) lh[b] = atomicAdd(&cur[b], lh[b]);
+  __syncthreads();
+  for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
+    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
+    if (d > thr) continue;
+    const int64_t b = thr - d;
+    const int64_t pos = b < LIGHT_LDS_BINS ? (int64_t)lh[b] + atomicAdd(&lc[b], 1) : (int64_t)atomicAdd(&cur[b], 1);
+    perm[boff[b] + pos] = (int32_t)r;
   }
 }
 
@@ -435,7 +485,7 @@ hipError_t normalize_run(int64_t n, int64_t E, const int32_t* src, const int32_t
   hipLaunchKernelGGL(selfloop_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, off, cnt, tmp);
   GCN_TRY(hipGetLastError());
   int32_t* ucnt = cnt;   // counts are no longer needed after the self-loop slots are placed
-  hipLaunchKernelGGL(sort_small_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, n, off, tmp, ucnt);
+  hipLaunchKernelGGL(sort_small_kernel, dim3(wave_rows_grid(n)), dim3(256), 0, s, n, off, tmp, ucnt);
   GCN_TRY(hipGetLastError());
   hipLaunchKernelGGL(sort_medium_kernel, dim3(grid_for(n, 1, 4096)), dim3(256), 0, s, n, off, tmp, ucnt);
   GCN_TRY(hipGetLastError());
@@ -445,15 +495,15 @@ hipError_t normalize_run(int64_t n, int64_t E, const int32_t* src, const int32_t
   GCN_TRY(hipGetLastError());
   GCN_TRY(scan_exclusive(rp64, n + 1, scr, s));
   if (idx64)
-    hipLaunchKernelGGL(compact_kernel<int64_t>, dim3((unsigned)((n + 1 + 3) / 4)), dim3(256), 0, s, n, off, tmp, rp64,
+    hipLaunchKernelGGL(compact_kernel<int64_t>, dim3(wave_rows_grid(n + 1)), dim3(256), 0, s, n, off, tmp, rp64,
                        ucnt, (int64_t*)rowptr, colidx, deg, dinv);
   else
-    hipLaunchKernelGGL(compact_kernel<int32_t>, dim3((unsigned)((n + 1 + 3) / 4)), dim3(256), 0, s, n, off, tmp, rp64,
+    hipLaunchKernelGGL(compact_kernel<int32_t>, dim3(wave_rows_grid(n + 1)), dim3(256), 0, s, n, off, tmp, rp64,
                        ucnt, (int32_t*)rowptr, colidx, deg, dinv);
   GCN_TRY(hipGetLastError());
   if (dense) GCN_TRY(fill_zero(dense, (size_t)n * (size_t)ld_dense * (value_prec == 0 ? 4 : 2), s));
   if (values || dense) {
-    const dim3 g((unsigned)((n + 3) / 4));
+    const dim3 g(wave_rows_grid(n));
     switch (value_prec) {
       case 0: hipLaunchKernelGGL(values_kernel<float>, g, dim3(256), 0, s, n, rp64, colidx, dinv, (float*)values, (float*)dense, ld_dense); break;
       case 1: hipLaunchKernelGGL(values_kernel<f16>, g, dim3(256), 0, s, n, rp64, colidx, dinv, (f16*)values, (f16*)dense, ld_dense); break;

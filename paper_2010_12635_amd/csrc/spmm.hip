@@ -76,25 +76,28 @@ __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
   constexpr int G = 64 / LPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane / LPR, li = lane % LPR;
-  const int64_t slot = ((int64_t)blockIdx.x * 4 + wave) * G + g;
   const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
-  if (slot >= p.n_rows || col0 >= p.F) return;
-  const int64_t row = p.row_perm ? (int64_t)p.row_perm[slot] : slot;
-  const int64_t beg = (int64_t)p.rowptr[row], end = (int64_t)p.rowptr[row + 1];
-  if (!p.row_perm && p.heavy_threshold > 0 && end - beg > p.heavy_threshold) return;
+  if (col0 >= p.F) return;
   const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
-  const float drow = HAS_VAL ? 0.f : p.dinv[row];
-  float acc[VE];
+  // the grid is capped (at most 2^32 work-items per dispatch dimension):
+  // a workgroup takes row slots blockIdx.x, blockIdx.x + gridDim.x, ...
+  for (int64_t slot = ((int64_t)blockIdx.x * 4 + wave) * G + g; slot < p.n_rows; slot += (int64_t)gridDim.x * 4 * G) {
+    const int64_t row = p.row_perm ? (int64_t)p.row_perm[slot] : slot;
+    const int64_t beg = (int64_t)p.rowptr[row], end = (int64_t)p.rowptr[row + 1];
+    if (!p.row_perm && p.heavy_threshold > 0 && end - beg > p.heavy_threshold) continue;
+    const float drow = HAS_VAL ? 0.f : p.dinv[row];
+    float acc[VE];
 #pragma unroll
-  for (int i = 0; i < VE; ++i) acc[i] = 0.f;
-  int64_t e = beg;
-  for (; e + 8 <= end; e += 8) gather_block<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-  if (e + 4 <= end) {
-    gather_block<T, HAS_VAL, 4>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-    e += 4;
+    for (int i = 0; i < VE; ++i) acc[i] = 0.f;
+    int64_t e = beg;
+    for (; e + 8 <= end; e += 8) gather_block<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
+    if (e + 4 <= end) {
+      gather_block<T, HAS_VAL, 4>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
+      e += 4;
+    }
+    for (; e < end; ++e) gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
+    epi_store_vec<T>(p.epi, row, col0, acc);
   }
-  for (; e < end; ++e) gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-  epi_store_vec<T>(p.epi, row, col0, acc);
 }
 
 template <typename IdxT>
@@ -202,7 +205,8 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   const int64_t rows_per_block = 4 * G;
   hipError_t e = hipSuccess;
   if (p.n_rows > 0) {
-    dim3 grid((unsigned)((p.n_rows + rows_per_block - 1) / rows_per_block), (unsigned)colblocks);
+    const int64_t blocks = (p.n_rows + rows_per_block - 1) / rows_per_block;
+    dim3 grid((unsigned)(blocks < (1 << 20) ? blocks : (1 << 20)), (unsigned)colblocks);
     hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), grid, dim3(256), 0, s, p);
     e = hipGetLastError();
   }

@@ -31,7 +31,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 __all__ = [
-    "er_graph", "sbm_graph", "ba_graph", "rmat_graph",
+    "er_graph", "sbm_graph", "ba_graph", "rmat_graph", "rmat_graph_device", "scale_workload_device",
     "features", "uniform_labels", "train_mask", "glorot_uniform",
     "WorkloadSpec", "SPECS", "workload",
 ]
@@ -164,6 +164,71 @@ def rmat_graph(scale: int, edge_factor: int, a: float, b: float, c: float,
         dst[lo:hi] = d
     perm = rng.permutation(n)
     return perm[src].astype(np.int32), perm[dst].astype(np.int32)
+
+
+def rmat_graph_device(scale: int, edge_factor: int, a: float, b: float, c: float, seed: int,
+                      device="cuda", chunk: int = 1 << 27):
+    """The R-MAT recipe of rmat_graph drawn on the device with torch's
+    generator (seeded by ``seed``), for graphs too large to draw on the host:
+    per sample and bit level one uniform draw picks the quadrant, then a
+    uniform random relabelling.  Returns int32 device tensors (raw samples,
+    repeats and self-loops included).  Not the same stream as rmat_graph."""
+    import torch
+    n = 1 << scale
+    n_samples = edge_factor * n
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    src = torch.empty(n_samples, dtype=torch.int32, device=device)
+    dst = torch.empty(n_samples, dtype=torch.int32, device=device)
+    ab, abc = a + b, a + b + c
+    for lo in range(0, n_samples, chunk):
+        hi = min(lo + chunk, n_samples)
+        s = torch.zeros(hi - lo, dtype=torch.int32, device=device)
+        d = torch.zeros(hi - lo, dtype=torch.int32, device=device)
+        for bit in range(scale):
+            r = torch.rand(hi - lo, generator=gen, device=device)
+            s |= (r >= ab).to(torch.int32) << bit
+            d |= (((r >= a) & (r < ab)) | (r >= abc)).to(torch.int32) << bit
+            del r
+        src[lo:hi] = s
+        dst[lo:hi] = d
+        del s, d
+    perm = torch.randperm(n, generator=gen, device=device, dtype=torch.int32)
+    for lo in range(0, n_samples, chunk):
+        hi = min(lo + chunk, n_samples)
+        src[lo:hi] = perm[src[lo:hi].long()]
+        dst[lo:hi] = perm[dst[lo:hi].long()]
+    del perm
+    return src, dst
+
+
+def scale_workload_device(scale: int, seed: int, f_in: int = 128, hidden: int = 128, classes: int = 64,
+                          dtype=None, device="cuda"):
+    """The scale-test workload (R-MAT scale ``scale``, edge factor 16,
+    (0.57, 0.19, 0.19, 0.05); features N(0,1); uniform labels over
+    ``classes``; every vertex in the training mask; Glorot-uniform weights)
+    with the graph, features and labels drawn on the device.  X is returned
+    as n x round8(f_in) in ``dtype`` with zero padding columns."""
+    import torch
+    dtype = dtype or torch.float16
+    src, dst = rmat_graph_device(scale, 16, 0.57, 0.19, 0.19, seed, device)
+    n = 1 << scale
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed) + 1)
+    ld = (f_in + 7) // 8 * 8
+    X = torch.zeros((n, ld), dtype=dtype, device=device)
+    step = 1 << 22
+    for lo in range(0, n, step):
+        hi = min(lo + step, n)
+        X[lo:hi, :f_in] = torch.randn((hi - lo, f_in), generator=gen, device=device).to(dtype)
+    labels = torch.randint(0, classes, (n,), generator=gen, device=device, dtype=torch.int32)
+    mask = torch.ones(n, dtype=torch.uint8, device=device)
+    w_rng = np.random.default_rng(seed)
+    W1 = glorot_uniform(f_in, hidden, w_rng)
+    W2 = glorot_uniform(hidden, classes, w_rng)
+    return dict(n=n, src=src, dst=dst, X=X, labels=labels, mask=mask, W1=W1, W2=W2,
+                b1=np.zeros(hidden, np.float32), b2=np.zeros(classes, np.float32),
+                dropout_seed=int(seed) * 7919 + 1)
 
 
 def features(n: int, f: int, kind: str, rng: np.random.Generator, density: float = 1.0):

@@ -37,8 +37,11 @@ class DeviceGraph:
         self.n = int(n)
         self.prec = prec
         dev = torch.device(device)
-        src_t = torch.as_tensor(np.ascontiguousarray(src, dtype=np.int32)).to(dev)
-        dst_t = torch.as_tensor(np.ascontiguousarray(dst, dtype=np.int32)).to(dev)
+        if isinstance(src, torch.Tensor):   # device-drawn edges (large graphs)
+            src_t, dst_t = src.to(dev, torch.int32), dst.to(dev, torch.int32)
+        else:
+            src_t = torch.as_tensor(np.ascontiguousarray(src, dtype=np.int32)).to(dev)
+            dst_t = torch.as_tensor(np.ascontiguousarray(dst, dtype=np.int32)).to(dev)
         ne = src_t.numel()
         cap = 2 * ne + self.n
         itype = torch.int64 if index == G.GCN_I64 else torch.int32
@@ -124,13 +127,22 @@ class GCN2:
         self.p = float(dropout)
         self.seed = int(seed)
         self.adam = adam or AdamConfig()
-        # inputs (padding columns zero)
-        self.X = torch.zeros((n, self.ld_x), dtype=self.dt, device=dev)
-        self.X[:, : self.f_in] = torch.as_tensor(np.asarray(X, np.float32)).to(dev).to(self.dt)
-        self.labels = torch.as_tensor(np.asarray(labels, np.int32)).to(dev)
-        mask = np.asarray(mask, np.uint8)
-        self.mask = torch.as_tensor(mask).to(dev)
-        self.n_mask = int(mask.sum())
+        # inputs (padding columns zero); a device tensor already in the
+        # storage layout (n x round8(f_in), storage dtype) is used in place
+        if isinstance(X, torch.Tensor) and X.is_cuda and X.dtype == self.dt and tuple(X.shape) == (n, self.ld_x):
+            self.X = X
+        else:
+            self.X = torch.zeros((n, self.ld_x), dtype=self.dt, device=dev)
+            self.X[:, : self.f_in] = torch.as_tensor(np.asarray(X, np.float32)).to(dev).to(self.dt)
+        if isinstance(labels, torch.Tensor):
+            self.labels = labels.to(dev, torch.int32)
+            self.mask = mask.to(dev, torch.uint8)
+            self.n_mask = int(self.mask.sum().item())
+        else:
+            self.labels = torch.as_tensor(np.asarray(labels, np.int32)).to(dev)
+            mask = np.asarray(mask, np.uint8)
+            self.mask = torch.as_tensor(mask).to(dev)
+            self.n_mask = int(mask.sum())
         # flat parameters: [W1 (f_in x ld_h), b1 (ld_h), W2 (f_h x ld_c), b2 (ld_c)]
         sizes = [self.f_in * self.ld_h, self.ld_h, self.f_h * self.ld_c, self.ld_c]
         offs = np.cumsum([0] + sizes)
