@@ -385,7 +385,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0 = skip)")
     ap.add_argument("--spmm-workload", default="rmat21",
                     help="CSR workload whose aggregation bandwidth is reported as 'spmm' ('none' = skip)")
-    ap.add_argument("--spmm-steps", type=int, default=10)
+    ap.add_argument("--spmm-steps", type=int, default=30)
     ap.add_argument("--scale-test", nargs=2, type=int, metavar=("FIRST", "LAST"),
                     help="train R-MAT graphs of scale FIRST..LAST (fp16, then fp32) until device memory runs out; "
                          "prints one JSON line and exits")
@@ -480,7 +480,7 @@ def main():
         log(f"[bench] spmm workload {args.spmm_workload}: generating")
         wl2 = I.workload(args.spmm_workload, args.seed)
         spec2 = wl2["spec"]
-        r2 = run_gpu(wl2, prec, args.spmm_steps, 1, dense=spec2.dense_adj)
+        r2 = run_gpu(wl2, prec, args.spmm_steps, 3, dense=spec2.dense_adj)
         s_p = 8 if spec2.index64 else 4
         b2 = spmm_bytes(r2["n"], r2["nnz"], r2["f_h"], s, s_p) + spmm_bytes(r2["n"], r2["nnz"], r2["C"], s, s_p)
         ach2 = b2 * (r2["agg_launches"] // 2) / (r2["agg_ms"] * 1e-3) / 1e9
