@@ -26,7 +26,14 @@ leaves open:
   gradients, dynamic loss scaling that skips a step and halves the scale on
   overflow and doubles it after a run of good steps (O1/O2 description).
 * philox4x64(): the counter-based generator (Salmon et al., SC'11) that
-  draws the dropout keep decisions.
+  draws the dropout keep decisions and the decoder's pairs.
+* Link prediction (Section "Graph Auto-Encoders", Eq. (2): the decoder
+  sigma(Z Z^T) read on sampled vertex pairs): sample_pairs() draws an
+  epoch's positive and negative pairs, pair_loss() scores them by inner
+  products and takes the mean logistic (binary cross-entropy) loss and its
+  gradient per pair, pair_backward() scatters that gradient into dZ, and
+  auc_ap() gives the area under the ROC curve and the average precision
+  of held-out pairs (the paper's link-prediction metrics).
 
 Every floating-point quantity is float64.  Parity status: every function
 here is pinned by the CPU tests (brute force, closed forms, invariants,
@@ -41,6 +48,7 @@ __all__ = [
     "spmm", "philox4x64", "dropout_keep", "layer_fwd", "softmax_ce",
     "graph_degrees", "graph_rows", "dropout_keep_rows", "norm_adj_matvec",
     "layer_bwd", "adam_step", "LossScaler", "AdamState",
+    "PAIR_STREAM", "sample_pairs", "pair_loss", "pair_backward", "auc_ap",
 ]
 
 
@@ -440,3 +448,98 @@ def adam_step(master, grad_scaled, state: AdamState, scaler: LossScaler,
     vhat = state.v / (1.0 - beta2 ** state.t)
     new = np.asarray(master, np.float64) - lr * mhat / (np.sqrt(vhat) + eps)
     return new, True
+
+
+# ---------------------------------------------------------------------------
+# Link prediction: Eq. (2) on sampled pairs
+# ---------------------------------------------------------------------------
+
+PAIR_STREAM = 0x50414952   # second key word of the pair sampler's Philox stream
+
+
+def sample_pairs(seed, epoch, n, edge_u, edge_v, n_pos, n_neg):
+    """Pairs of one training epoch of the decoder.  Pair k (0 <= k <
+    n_pos + n_neg) takes the Philox-4x64-10 block with key (seed,
+    PAIR_STREAM) and counter (k, epoch, 0, 0), outputs w0, w1:
+      k <  n_pos: the training edge e = w0 mod n_edges, (u, v) = (edge_u[e], edge_v[e]);
+      k >= n_pos: u = w0 mod n, v = (u + 1 + (w1 mod (n - 1))) mod n, so v != u.
+    Returns int32 arrays u, v; pairs k < n_pos are positives (label 1)."""
+    total = n_pos + n_neg
+    ctr = np.zeros((total, 4), np.uint64)
+    ctr[:, 0] = np.arange(total, dtype=np.uint64)
+    ctr[:, 1] = np.uint64(epoch)
+    key = np.zeros((total, 2), np.uint64)
+    key[:, 0] = np.uint64(seed & _M64)
+    key[:, 1] = np.uint64(PAIR_STREAM)
+    out = philox4x64(ctr, key)
+    w0, w1 = out[:, 0], out[:, 1]
+    edge_u = np.asarray(edge_u, np.int64)
+    edge_v = np.asarray(edge_v, np.int64)
+    u = np.empty(total, np.int64)
+    v = np.empty(total, np.int64)
+    e = (w0[:n_pos] % np.uint64(edge_u.size)).astype(np.int64)
+    u[:n_pos], v[:n_pos] = edge_u[e], edge_v[e]
+    un = w0[n_pos:] % np.uint64(n)
+    u[n_pos:] = un.astype(np.int64)
+    v[n_pos:] = ((un + np.uint64(1) + w1[n_pos:] % np.uint64(n - 1)) % np.uint64(n)).astype(np.int64)
+    return u.astype(np.int32), v.astype(np.int32)
+
+
+def _softplus(x):
+    return np.maximum(x, 0.0) + np.log1p(np.exp(-np.abs(x)))
+
+
+def _sigmoid(x):
+    out = np.empty_like(x)
+    pos = x >= 0
+    out[pos] = 1.0 / (1.0 + np.exp(-x[pos]))
+    ex = np.exp(x[~pos])
+    out[~pos] = ex / (1.0 + ex)
+    return out
+
+
+def pair_loss(Z, u, v, n_pos, loss_scale=1.0):
+    """Decoder of Eq. (2) on pairs: score s_k = <Z[u_k], Z[v_k]>, label
+    y_k = 1 for k < n_pos else 0, loss = mean_k BCE(sigmoid(s_k), y_k)
+    = mean_k softplus(s_k) - y_k s_k, gradient per pair
+    g_k = loss_scale * (sigmoid(s_k) - y_k) / K (K = number of pairs).
+    Returns (loss, scores, g)."""
+    z = np.asarray(Z, np.float64)
+    u = np.asarray(u, np.int64)
+    v = np.asarray(v, np.int64)
+    s = np.einsum("kf,kf->k", z[u], z[v])
+    y = (np.arange(u.size) < n_pos).astype(np.float64)
+    loss = float(np.mean(_softplus(s) - y * s))
+    g = loss_scale * (_sigmoid(s) - y) / u.size
+    return loss, s, g
+
+
+def pair_backward(n, Z, u, v, g):
+    """dZ of sum_k g_k s_k with s_k = <Z[u_k], Z[v_k]>: row r collects
+    g_k Z[v_k] for every pair with u_k = r and g_k Z[u_k] for every pair
+    with v_k = r.  Rows in no pair are 0."""
+    z = np.asarray(Z, np.float64)
+    u = np.asarray(u, np.int64)
+    v = np.asarray(v, np.int64)
+    g = np.asarray(g, np.float64)
+    dz = np.zeros((n, z.shape[1]))
+    np.add.at(dz, u, g[:, None] * z[v])
+    np.add.at(dz, v, g[:, None] * z[u])
+    return dz
+
+
+def auc_ap(scores_pos, scores_neg):
+    """Link-prediction metrics from the scores of positive and negative
+    pairs, by their definitions (brute force over all pairs of scores):
+    AUC = P(score of a random positive > score of a random negative), ties
+    counting 1/2; AP = mean over positives i of the precision among all
+    pairs scoring >= s_i."""
+    sp = np.asarray(scores_pos, np.float64)
+    sn = np.asarray(scores_neg, np.float64)
+    gt = (sp[:, None] > sn[None, :]).sum()
+    eq = (sp[:, None] == sn[None, :]).sum()
+    auc = (gt + 0.5 * eq) / (sp.size * sn.size)
+    pos_ge = (sp[None, :] >= sp[:, None]).sum(axis=1)
+    all_ge = pos_ge + (sn[None, :] >= sp[:, None]).sum(axis=1)
+    ap = float(np.mean(pos_ge / all_ge))
+    return float(auc), ap

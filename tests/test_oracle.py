@@ -446,3 +446,103 @@ def test_norm_adj_matvec_matches_csr_product():
     want = O.spmm(g, O.norm_values(g), y)
     assert np.allclose(O.norm_adj_matvec(n, src, dst, y), want, rtol=1e-13, atol=1e-13)
     assert np.allclose(O.norm_adj_matvec(n, src, dst, y[:, 0]), want[:, 0], rtol=1e-13, atol=1e-13)
+
+
+# ------------------------------------------------------ link prediction (Eq. 2)
+
+def _numpy_philox_block(ctr, key):
+    """One Philox-4x64-10 block from numpy's generator (an implementation
+    independent of the oracle's): numpy increments the counter before it
+    produces a block (ctr[0] >= 1 here, so no carry)."""
+    c = np.array(ctr, np.uint64)
+    assert c[0] >= 1
+    c[0] -= np.uint64(1)
+    return np.random.Philox(counter=c, key=np.array(key, np.uint64)).random_raw(4)
+
+
+def test_sample_pairs_draws_and_layout():
+    rng = np.random.default_rng(31)
+    n = 1000
+    eu = rng.integers(0, n, 300).astype(np.int32)
+    ev = (eu + 1 + rng.integers(0, n - 1, 300)).astype(np.int32) % n
+    seed, epoch, n_pos, n_neg = 2**40 + 7, 3, 500, 700
+    u, v = O.sample_pairs(seed, epoch, n, eu, ev, n_pos, n_neg)
+    # pairs by hand from numpy's Philox: positives 1 and n_pos - 1, negatives n_pos and last
+    for k in (1, n_pos - 1, n_pos, n_pos + n_neg - 1):
+        w = _numpy_philox_block([k, epoch, 0, 0], [seed, O.PAIR_STREAM])
+        if k < n_pos:
+            e = int(w[0]) % eu.size
+            assert (u[k], v[k]) == (eu[e], ev[e])
+        else:
+            uu = int(w[0]) % n
+            assert (u[k], v[k]) == (uu, (uu + 1 + int(w[1]) % (n - 1)) % n)
+    # positives are training edges; negatives are distinct vertices in range
+    edges = set(zip(eu.tolist(), ev.tolist()))
+    assert all((a, b) in edges for a, b in zip(u[:n_pos].tolist(), v[:n_pos].tolist()))
+    assert np.all(u[n_pos:] != v[n_pos:]) and u.min() >= 0 and v.max() < n
+    # roughly uniform negatives (mean of a uniform id over [0, n) within 5 sigma)
+    sd = math.sqrt((n * n - 1) / 12 / n_neg)
+    assert abs(u[n_pos:].mean() - (n - 1) / 2) < 5 * sd
+    # another epoch gives other pairs
+    u2, _ = O.sample_pairs(seed, epoch + 1, n, eu, ev, n_pos, n_neg)
+    assert (u2 != u).mean() > 0.9
+
+
+def test_pair_loss_closed_forms():
+    rng = np.random.default_rng(32)
+    n, f, n_pos, n_neg = 50, 6, 30, 40
+    u = rng.integers(0, n, n_pos + n_neg)
+    v = (u + 1 + rng.integers(0, n - 1, n_pos + n_neg)) % n
+    # Z = 0: every score 0, loss = log 2, g = S (1/2 - y) / K
+    loss, s, g = O.pair_loss(np.zeros((n, f)), u, v, n_pos, loss_scale=8.0)
+    assert s.tolist() == [0.0] * u.size
+    assert abs(loss - math.log(2.0)) < 1e-15
+    y = (np.arange(u.size) < n_pos)
+    assert np.allclose(g, 8.0 * (0.5 - y) / u.size, rtol=0, atol=1e-17)
+    # textbook binary cross-entropy -[y log p + (1 - y) log (1 - p)], p = sigmoid(s)
+    z = 0.4 * rng.standard_normal((n, f))
+    loss, s, g = O.pair_loss(z, u, v, n_pos)
+    p = 1.0 / (1.0 + np.exp(-s))
+    want = -np.mean(np.where(y, np.log(p), np.log(1.0 - p)))
+    assert abs(loss - want) < 1e-12
+    assert np.allclose(s, [z[a] @ z[b] for a, b in zip(u, v)], rtol=1e-13, atol=1e-13)
+    # large scores stay finite (stable softplus / sigmoid)
+    zz = np.zeros((n, f)); zz[:, 0] = 40.0
+    loss, s, g = O.pair_loss(zz, u, v, n_pos)
+    assert np.isfinite(loss) and np.all(np.isfinite(g))
+    assert abs(loss - n_neg * 1600.0 / u.size) < 1e-9    # negatives pay ~s, positives ~0
+
+
+def test_pair_gradient_finite_differences():
+    rng = np.random.default_rng(33)
+    n, f, n_pos, n_neg = 20, 5, 25, 25
+    u = rng.integers(0, n, n_pos + n_neg)
+    v = (u + 1 + rng.integers(0, n - 1, n_pos + n_neg)) % n
+    z = 0.5 * rng.standard_normal((n, f))
+    _, _, g = O.pair_loss(z, u, v, n_pos)
+    dz = O.pair_backward(n, z, u, v, g)
+    h = 1e-6
+    for r, c in [(0, 0), (3, 2), (int(u[0]), 4), (int(v[7]), 1), (19, 3)]:
+        zp, zm = z.copy(), z.copy()
+        zp[r, c] += h
+        zm[r, c] -= h
+        fd = (O.pair_loss(zp, u, v, n_pos)[0] - O.pair_loss(zm, u, v, n_pos)[0]) / (2 * h)
+        assert abs(dz[r, c] - fd) < 1e-8, (r, c, dz[r, c], fd)
+    # rows that appear in no pair get zero
+    unused = np.setdiff1d(np.arange(n), np.concatenate([u, v]))
+    assert np.all(dz[unused] == 0)
+
+
+def test_auc_ap_match_sklearn():
+    from sklearn.metrics import average_precision_score, roc_auc_score
+    rng = np.random.default_rng(34)
+    for p, q in [(50, 70), (200, 200), (7, 3)]:
+        sp = np.round(rng.standard_normal(p) + 0.7, 1)     # rounded: many ties
+        sn = np.round(rng.standard_normal(q), 1)
+        auc, ap = O.auc_ap(sp, sn)
+        y = np.r_[np.ones(p), np.zeros(q)]
+        sc = np.r_[sp, sn]
+        assert abs(auc - roc_auc_score(y, sc)) < 1e-12
+        assert abs(ap - average_precision_score(y, sc)) < 1e-12
+    assert O.auc_ap([2.0, 3.0], [0.0, 1.0]) == (1.0, 1.0)
+    assert O.auc_ap([0.0], [1.0])[0] == 0.0
