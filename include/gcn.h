@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 2
+#define GCN_ABI_VERSION 3
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -307,6 +307,63 @@ gcn_status gcn_loss(int64_t n, int64_t C, int64_t ld, int32_t prec, const void* 
 gcn_status gcn_optimizer_step(int64_t count, float* master, const float* grad, float* m, float* v,
                               void* working, int32_t prec, const gcn_adam_config* cfg,
                               gcn_scaler* state, int32_t* overflow_flag, void* stream);
+
+/* ===========================================================================
+ * Link prediction: the graph auto-encoder of Section "Graph Auto-Encoders",
+ * Eq. (2), A' = sigmoid(Z Z^T) with Z = GCN(A_hat, X), evaluated on sampled
+ * vertex pairs (k = 0 .. K-1, K = n_pos + n_neg; pairs k < n_pos are
+ * positives with label 1, the others negatives with label 0).  Vertex ids
+ * are int32 in [0, n); Z is n x F (ld, prec).
+ * ======================================================================== */
+
+/* gcn_sample_pairs: the pairs of one training epoch.  Pair k takes the
+ * Philox-4x64-10 block with key (seed, 0x50414952) and counter
+ * (k, epoch, 0, 0), outputs w0, w1:
+ *   k <  n_pos: e = w0 mod n_edges, pair = (edge_u[e], edge_v[e]);
+ *   k >= n_pos: u = w0 mod n, v = (u + 1 + (w1 mod (n - 1))) mod n (v != u).
+ * pair_u, pair_v: [n_pos + n_neg] int32 device outputs.  Requires n >= 2 and,
+ * with n_pos > 0, n_edges >= 1.  Asynchronous. */
+gcn_status gcn_sample_pairs(int64_t n, const int32_t* edge_u, const int32_t* edge_v, int64_t n_edges,
+                            int64_t n_pos, int64_t n_neg, uint64_t seed, uint64_t epoch,
+                            int32_t* pair_u, int32_t* pair_v, void* stream);
+
+/* gcn_pair_loss: decoder scores and the logistic loss on pairs.
+ *   s_k    = <Z[u_k], Z[v_k]>                       (fp32 accumulation)
+ *   *loss  = mean_k softplus(s_k) - y_k s_k          (binary cross-entropy of sigmoid(s_k))
+ *   g[k]   = S (sigmoid(s_k) - y_k) / K              (fp32; S = *loss_scale, NULL means 1)
+ *   scores[k] = s_k (fp32, may be NULL)
+ * The loss is summed in a fixed order.  A pair with an id outside [0, n) is
+ * skipped (g = 0, score NaN) and sets *overflow, as does a non-finite score,
+ * g or loss.  F <= 64 * (16 / element size).  workspace: at least
+ * gcn_pair_loss_workspace_size() bytes. */
+gcn_status gcn_pair_loss_workspace_size(int64_t n_pairs, size_t* bytes);
+gcn_status gcn_pair_loss(int64_t n, int64_t F, int64_t ld, int32_t prec, const void* Z,
+                         const int32_t* pair_u, const int32_t* pair_v, int64_t n_pos, int64_t n_neg,
+                         const float* loss_scale, float* loss, float* scores, float* g,
+                         int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
+
+/* gcn_pair_backward: dZ = d(sum_k g_k s_k)/dZ: row r sums g_k Z[v_k] over
+ * the pairs with u_k = r and g_k Z[u_k] over the pairs with v_k = r, in
+ * increasing k (run-to-run deterministic); rows in no pair are 0.
+ * dZ: n x F (ldz, prec; padding columns may be overwritten with 0).  Pairs with an id
+ * outside [0, n) are skipped.  *overflow is set if a stored element is not
+ * finite.  workspace: gcn_pair_backward_workspace_size() bytes. */
+gcn_status gcn_pair_backward_workspace_size(int64_t n, int64_t n_pairs, size_t* bytes);
+gcn_status gcn_pair_backward(int64_t n, int64_t F, int64_t ld, int32_t prec, const void* Z,
+                             const int32_t* pair_u, const int32_t* pair_v, int64_t n_pairs,
+                             const float* g, void* dZ, int64_t ldz, int32_t* overflow,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* gcn_pair_metrics: the paper's link-prediction metrics (Section
+ * "Experimental Setup": AUC and AP) of held-out pairs from their fp32
+ * scores (scores[0 .. n_pos) positives, then n_neg negatives; all finite):
+ *   auc_ap[0] = AUC = #{(i, j): s_i > s_j} + #{s_i == s_j} / 2, over P x N, divided by P N;
+ *   auc_ap[1] = AP  = mean over positives i of #{pos with s >= s_i} / #{all with s >= s_i}.
+ * Exact counts (O(P (P + N)) comparisons), fixed-order sums; auc_ap is a
+ * device array of 2 doubles.  workspace: gcn_pair_metrics_workspace_size(). */
+gcn_status gcn_pair_metrics_workspace_size(int64_t n_pos, size_t* bytes);
+gcn_status gcn_pair_metrics(const float* scores, int64_t n_pos, int64_t n_neg, double* auc_ap,
+                            void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -506,4 +506,84 @@ gcn_status gcn_optimizer_step(int64_t count, float* master, const float* grad, f
   return finish(hipSuccess, s);
 }
 
+gcn_status gcn_sample_pairs(int64_t n, const int32_t* edge_u, const int32_t* edge_v, int64_t n_edges, int64_t n_pos,
+                            int64_t n_neg, uint64_t seed, uint64_t epoch, int32_t* pair_u, int32_t* pair_v,
+                            void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n < 2 || n > INT32_MAX || n_pos < 0 || n_neg < 0 || n_pos + n_neg <= 0) return GCN_ERR_SHAPE;
+  if (n_pos + n_neg > INT32_MAX) return GCN_ERR_UNSUPPORTED;
+  if (n_pos > 0 && (n_edges < 1 || !edge_u || !edge_v)) return GCN_ERR_INVALID_ARG;
+  if (!pair_u || !pair_v) return GCN_ERR_INVALID_ARG;
+  GCN_HIP(sample_pairs_launch(n, edge_u, edge_v, n_edges, n_pos, n_neg, seed, epoch, pair_u, pair_v, s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_pair_loss_workspace_size(int64_t n_pairs, size_t* bytes) {
+  if (!bytes) return GCN_ERR_INVALID_ARG;
+  if (n_pairs <= 0) return GCN_ERR_SHAPE;
+  *bytes = pair_loss_workspace_bytes(n_pairs);
+  return GCN_OK;
+}
+
+gcn_status gcn_pair_loss(int64_t n, int64_t F, int64_t ld, int32_t prec, const void* Z, const int32_t* pair_u,
+                         const int32_t* pair_v, int64_t n_pos, int64_t n_neg, const float* loss_scale, float* loss,
+                         float* scores, float* g, int32_t* overflow, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || F <= 0 || ld < F || n_pos < 0 || n_neg < 0 || n_pos + n_neg <= 0) return GCN_ERR_SHAPE;
+  if (n_pos + n_neg > INT32_MAX) return GCN_ERR_UNSUPPORTED;
+  if (ld % 8) return GCN_ERR_ALIGNMENT;
+  if (F > 64 * (prec == GCN_F32 ? 4 : 8)) return GCN_ERR_UNSUPPORTED;
+  if (!Z || !pair_u || !pair_v || !loss || !g) return GCN_ERR_INVALID_ARG;
+  if (!aligned16(Z)) return GCN_ERR_ALIGNMENT;
+  if (!workspace || workspace_bytes < pair_loss_workspace_bytes(n_pos + n_neg)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  GCN_HIP(pair_loss_launch(prec, n, F, ld, Z, pair_u, pair_v, n_pos, n_neg, loss_scale, loss, scores, g, overflow,
+                           workspace, s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_pair_backward_workspace_size(int64_t n, int64_t n_pairs, size_t* bytes) {
+  if (!bytes) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || n_pairs < 0) return GCN_ERR_SHAPE;
+  *bytes = pair_backward_workspace_bytes(n, n_pairs);
+  return GCN_OK;
+}
+
+gcn_status gcn_pair_backward(int64_t n, int64_t F, int64_t ld, int32_t prec, const void* Z, const int32_t* pair_u,
+                             const int32_t* pair_v, int64_t n_pairs, const float* g, void* dZ, int64_t ldz,
+                             int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
+  if (n <= 0 || n > INT32_MAX || F <= 0 || ld < F || ldz < F || n_pairs < 0) return GCN_ERR_SHAPE;
+  if (n_pairs > INT32_MAX) return GCN_ERR_UNSUPPORTED;
+  if (ld % 8 || ldz % 8) return GCN_ERR_ALIGNMENT;
+  if (F > 64 * (prec == GCN_F32 ? 4 : 8)) return GCN_ERR_UNSUPPORTED;
+  if (!Z || !dZ || (n_pairs > 0 && (!pair_u || !pair_v || !g))) return GCN_ERR_INVALID_ARG;
+  if (!aligned16(Z) || !aligned16(dZ)) return GCN_ERR_ALIGNMENT;
+  if (!workspace || workspace_bytes < pair_backward_workspace_bytes(n, n_pairs)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  GCN_HIP(pair_backward_launch(prec, n, F, ld, Z, pair_u, pair_v, n_pairs, g, dZ, ldz, overflow, workspace, s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_pair_metrics_workspace_size(int64_t n_pos, size_t* bytes) {
+  if (!bytes) return GCN_ERR_INVALID_ARG;
+  if (n_pos <= 0) return GCN_ERR_SHAPE;
+  *bytes = pair_metrics_workspace_bytes(n_pos);
+  return GCN_OK;
+}
+
+gcn_status gcn_pair_metrics(const float* scores, int64_t n_pos, int64_t n_neg, double* auc_ap, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n_pos <= 0 || n_neg <= 0) return GCN_ERR_SHAPE;
+  if (!scores || !auc_ap) return GCN_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < pair_metrics_workspace_bytes(n_pos)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  GCN_HIP(pair_metrics_launch(scores, n_pos, n_neg, auc_ap, workspace, s));
+  return finish(hipSuccess, s);
+}
+
 }  // extern "C"

@@ -135,5 +135,29 @@ hipError_t optimizer_launch(int64_t count, float* master, const float* grad, flo
 
 // --------------------------------------------------------------- helpers ----
 hipError_t fill_zero(void* p, size_t bytes, hipStream_t s);
+// In-place exclusive scan of int64 data[0..count); scratch holds
+// segment_scan_scratch_elems(count) int64.
+int64_t segment_scan_scratch_elems(int64_t count);
+hipError_t segment_scan_exclusive(int64_t* data, int64_t count, int64_t* scratch, hipStream_t s);
+// Sort every segment [off[r], off[r+1]) of keys ascending (r < n); ucnt[r]
+// receives the number of distinct keys of the segment.
+hipError_t sort_segments(int64_t n, const int64_t* off, int32_t* keys, int32_t* ucnt, hipStream_t s);
+
+// ------------------------------------------------------ link prediction ----
+// Pair decoder of Eq. (2) on sampled pairs (see gcn.h for the definitions).
+hipError_t sample_pairs_launch(int64_t n, const int32_t* edge_u, const int32_t* edge_v, int64_t n_edges, int64_t n_pos,
+                               int64_t n_neg, uint64_t seed, uint64_t epoch, int32_t* pair_u, int32_t* pair_v,
+                               hipStream_t s);
+size_t pair_loss_workspace_bytes(int64_t n_pairs);
+hipError_t pair_loss_launch(int prec, int64_t n, int64_t F, int64_t ld, const void* Z, const int32_t* pair_u,
+                            const int32_t* pair_v, int64_t n_pos, int64_t n_neg, const float* loss_scale, float* loss,
+                            float* scores, float* g, int32_t* flag, void* ws, hipStream_t s);
+size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs);
+hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, const void* Z, const int32_t* pair_u,
+                                const int32_t* pair_v, int64_t n_pairs, const float* g, void* dZ, int64_t ldz,
+                                int32_t* flag, void* ws, hipStream_t s);
+size_t pair_metrics_workspace_bytes(int64_t n_pos);
+hipError_t pair_metrics_launch(const float* scores, int64_t n_pos, int64_t n_neg, double* auc_ap, void* ws,
+                               hipStream_t s);
 
 }  // namespace gcn

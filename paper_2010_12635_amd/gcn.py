@@ -21,6 +21,8 @@ __all__ = [
     "gcn_schedule_size", "gcn_schedule", "gcn_layer_workspace_size", "gcn_layer_fwd",
     "gcn_layer_bwd", "gcn_loss_workspace_size", "gcn_loss", "gcn_optimizer_step",
     "gcn_transform_workspace_size", "gcn_transform", "gcn_aggregate_workspace_size", "gcn_aggregate",
+    "gcn_sample_pairs", "gcn_pair_loss_workspace_size", "gcn_pair_loss", "gcn_pair_backward_workspace_size",
+    "gcn_pair_backward", "gcn_pair_metrics_workspace_size", "gcn_pair_metrics",
 ]
 
 GCN_F32, GCN_F16, GCN_BF16 = 0, 1, 2
@@ -37,6 +39,8 @@ EXPORTED = (
     "gcn_layer_bwd", "gcn_loss_workspace_size", "gcn_loss", "gcn_optimizer_step",
     "gcn_transform_workspace_size", "gcn_transform", "gcn_aggregate_workspace_size", "gcn_aggregate",
     "gcn_dense_tiled_elems", "gcn_densify",
+    "gcn_sample_pairs", "gcn_pair_loss_workspace_size", "gcn_pair_loss", "gcn_pair_backward_workspace_size",
+    "gcn_pair_backward", "gcn_pair_metrics_workspace_size", "gcn_pair_metrics",
 )
 
 _DTYPES = {GCN_F32: torch.float32, GCN_F16: torch.float16, GCN_BF16: torch.bfloat16}
@@ -127,6 +131,13 @@ def lib():
         "gcn_densify": (I32, [PADJ, I32, I32, P, I64, P]),
         "gcn_aggregate": (I32, [PADJ, I64, I32, P, I64, P, I32, ctypes.c_float, I32, ctypes.c_uint64, I32,
                                 ctypes.c_uint64, P, I64, P, P, SZ, P]),
+        "gcn_sample_pairs": (I32, [I64, P, P, I64, I64, I64, ctypes.c_uint64, ctypes.c_uint64, P, P, P]),
+        "gcn_pair_loss_workspace_size": (I32, [I64, PSZ]),
+        "gcn_pair_loss": (I32, [I64, I64, I64, I32, P, P, P, I64, I64, P, P, P, P, P, P, SZ, P]),
+        "gcn_pair_backward_workspace_size": (I32, [I64, I64, PSZ]),
+        "gcn_pair_backward": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, I64, P, P, SZ, P]),
+        "gcn_pair_metrics_workspace_size": (I32, [I64, PSZ]),
+        "gcn_pair_metrics": (I32, [P, I64, I64, P, P, SZ, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -277,3 +288,51 @@ def gcn_dense_tiled_elems(n, prec) -> int:
 def gcn_densify(adj, fmt, value_prec, dense, ld_dense, stream=None):
     _check(lib().gcn_densify(ctypes.byref(adj), fmt, value_prec, _ptr(dense), ld_dense, _stream(stream)),
            "gcn_densify")
+
+
+# ------------------------------------------------------- link prediction ----
+
+def gcn_sample_pairs(n, edge_u, edge_v, n_pos, n_neg, seed, epoch, pair_u, pair_v, stream=None):
+    n_edges = 0 if edge_u is None else edge_u.numel()
+    _check(lib().gcn_sample_pairs(n, _ptr(edge_u), _ptr(edge_v), n_edges, n_pos, n_neg,
+                                  seed & 0xFFFFFFFFFFFFFFFF, epoch, _ptr(pair_u), _ptr(pair_v), _stream(stream)),
+           "gcn_sample_pairs")
+
+
+def gcn_pair_loss_workspace_size(n_pairs) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().gcn_pair_loss_workspace_size(n_pairs, ctypes.byref(b)), "gcn_pair_loss_workspace_size")
+    return b.value
+
+
+def gcn_pair_loss(n, F, ld, prec, Z, pair_u, pair_v, n_pos, n_neg, loss_scale, loss, scores, g, overflow,
+                  workspace, stream=None):
+    st = lib().gcn_pair_loss(n, F, ld, prec, _ptr(Z), _ptr(pair_u), _ptr(pair_v), n_pos, n_neg, _ptr(loss_scale),
+                             _ptr(loss), _ptr(scores), _ptr(g), _ptr(overflow), _ptr(workspace),
+                             workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "gcn_pair_loss")
+
+
+def gcn_pair_backward_workspace_size(n, n_pairs) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().gcn_pair_backward_workspace_size(n, n_pairs, ctypes.byref(b)), "gcn_pair_backward_workspace_size")
+    return b.value
+
+
+def gcn_pair_backward(n, F, ld, prec, Z, pair_u, pair_v, n_pairs, g, dZ, ldz, overflow, workspace, stream=None):
+    st = lib().gcn_pair_backward(n, F, ld, prec, _ptr(Z), _ptr(pair_u), _ptr(pair_v), n_pairs, _ptr(g), _ptr(dZ),
+                                 ldz, _ptr(overflow), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 _stream(stream))
+    _check(st, "gcn_pair_backward")
+
+
+def gcn_pair_metrics_workspace_size(n_pos) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().gcn_pair_metrics_workspace_size(n_pos, ctypes.byref(b)), "gcn_pair_metrics_workspace_size")
+    return b.value
+
+
+def gcn_pair_metrics(scores, n_pos, n_neg, auc_ap, workspace, stream=None):
+    st = lib().gcn_pair_metrics(_ptr(scores), n_pos, n_neg, _ptr(auc_ap), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "gcn_pair_metrics")

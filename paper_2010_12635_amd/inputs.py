@@ -32,6 +32,7 @@ import numpy as np
 
 __all__ = [
     "er_graph", "sbm_graph", "ba_graph", "rmat_graph", "rmat_graph_device", "scale_workload_device",
+    "link_split", "gae_workload",
     "features", "uniform_labels", "train_mask", "glorot_uniform",
     "WorkloadSpec", "SPECS", "workload",
 ]
@@ -371,3 +372,50 @@ def _shrunk(spec: WorkloadSpec, n: int) -> WorkloadSpec:
         scale = max(1, int(np.log2(n)))
         return replace(spec, graph_args=(scale,) + tuple(spec.graph_args[1:]))
     raise ValueError(spec.graph)
+
+
+def link_split(n: int, src, dst, test_frac: float, rng: np.random.Generator):
+    """Held-out split for link prediction: the distinct undirected edges
+    (self-loops and repeats of the raw samples dropped) are shuffled, a
+    ``test_frac`` share becomes the test positives and the rest the training
+    edges; as many test negatives are drawn uniformly among vertex pairs
+    that are not edges (distinct, u < v).  Returns (train_u, train_v,
+    test_u, test_v, n_test_pos) with the test positives first."""
+    src = np.asarray(src, np.int64)
+    dst = np.asarray(dst, np.int64)
+    keep = src != dst
+    a, b = np.minimum(src[keep], dst[keep]), np.maximum(src[keep], dst[keep])
+    key = np.unique(a * n + b)
+    key = key[rng.permutation(key.size)]
+    n_test = int(round(test_frac * key.size))
+    test_pos, train = key[:n_test], key[n_test:]
+    edges = np.sort(key)
+    neg = np.empty(0, np.int64)
+    while neg.size < n_test:
+        m = 2 * (n_test - neg.size) + 16
+        u = rng.integers(0, n, m)
+        v = rng.integers(0, n, m)
+        ok = u != v
+        k = np.minimum(u, v)[ok] * n + np.maximum(u, v)[ok]
+        pos = np.searchsorted(edges, k)
+        is_edge = (pos < edges.size) & (edges[np.minimum(pos, edges.size - 1)] == k)
+        k = k[~is_edge]
+        neg = np.unique(np.concatenate([neg, k]))
+    neg = neg[rng.permutation(neg.size)][:n_test]
+    test = np.concatenate([test_pos, neg])
+    return ((train // n).astype(np.int32), (train % n).astype(np.int32),
+            (test // n).astype(np.int32), (test % n).astype(np.int32), n_test)
+
+
+def gae_workload(seed: int = 0, *, n_override: int | None = None, test_frac: float = 0.1):
+    """The link-prediction workload (graph auto-encoder): the R-MAT scale-17
+    graph of SPECS["rmat17"] (edge factor 16), features 256 N(0,1), encoder
+    256 -> 256 -> 64; 10 % of the distinct edges held out as test positives
+    with as many non-edges as test negatives.  Adds train_u/train_v (the
+    encoder's graph and the pool of training positives), test_u/test_v and
+    n_test_pos to the workload dict."""
+    wl = workload("rmat17", seed, n_override=n_override)
+    rng = np.random.default_rng(np.random.SeedSequence(seed).spawn(7)[6])
+    tu, tv, eu, ev, nt = link_split(wl["n"], wl["src"], wl["dst"], test_frac, rng)
+    wl.update(train_u=tu, train_v=tv, test_u=eu, test_v=ev, n_test_pos=nt)
+    return wl

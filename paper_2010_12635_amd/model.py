@@ -248,3 +248,146 @@ class GCN2:
         s = self.scaler.cpu()
         return dict(scale=float(s.view(torch.float32)[0]), good_steps=int(s[1]), step=int(s[2]),
                     skipped=int(s[3]))
+
+
+class GAE2:
+    """Graph auto-encoder for link prediction (Section "Graph Auto-Encoders",
+    Eq. (2)): Z = GCN(A_hat, X) with two layers (ReLU on the hidden layer, no
+    dropout, linear embedding layer), A' = sigmoid(Z Z^T) evaluated on the
+    pairs of each epoch: n_pos training edges and n_neg uniform pairs drawn
+    by gcn_sample_pairs, logistic loss by gcn_pair_loss, its gradient into Z
+    by gcn_pair_backward, then the encoder's backward pass and Adam with
+    dynamic loss scaling as in GCN2."""
+
+    def __init__(self, graph: DeviceGraph, X, W1, W2, train_u, train_v, b1=None, b2=None, prec=G.GCN_F16,
+                 n_pos=1 << 20, n_neg=1 << 20, seed=0, loss_scale=65536.0, adam: AdamConfig | None = None,
+                 device="cuda"):
+        dev = torch.device(device)
+        self.g = graph
+        self.prec = prec
+        self.dt = G.torch_dtype(prec)
+        n = graph.n
+        self.n = n
+        self.f_in, self.f_h = W1.shape
+        self.f_e = W2.shape[1]
+        self.ld_x, self.ld_h, self.ld_e = round8(self.f_in), round8(self.f_h), round8(self.f_e)
+        self.n_pos, self.n_neg = int(n_pos), int(n_neg)
+        self.K = self.n_pos + self.n_neg
+        self.seed = int(seed)
+        self.adam = adam or AdamConfig()
+        if isinstance(X, torch.Tensor) and X.is_cuda and X.dtype == self.dt and tuple(X.shape) == (n, self.ld_x):
+            self.X = X
+        else:
+            self.X = torch.zeros((n, self.ld_x), dtype=self.dt, device=dev)
+            self.X[:, : self.f_in] = torch.as_tensor(np.asarray(X, np.float32)).to(dev).to(self.dt)
+        self.train_u = torch.as_tensor(np.asarray(train_u, np.int32)).to(dev)
+        self.train_v = torch.as_tensor(np.asarray(train_v, np.int32)).to(dev)
+        sizes = [self.f_in * self.ld_h, self.ld_h, self.f_h * self.ld_e, self.ld_e]
+        offs = np.cumsum([0] + sizes)
+        self.P = int(offs[-1])
+        self.offs = offs
+        master = np.zeros(self.P, np.float32)
+        w1 = np.zeros((self.f_in, self.ld_h), np.float32)
+        w1[:, : self.f_h] = W1
+        w2 = np.zeros((self.f_h, self.ld_e), np.float32)
+        w2[:, : self.f_e] = W2
+        master[offs[0]:offs[1]] = w1.ravel()
+        if b1 is not None:
+            master[offs[1]:offs[1] + self.f_h] = b1
+        master[offs[2]:offs[3]] = w2.ravel()
+        if b2 is not None:
+            master[offs[3]:offs[3] + self.f_e] = b2
+        self.master = torch.as_tensor(master).to(dev)
+        self.working = self.master.to(self.dt)
+        self.grad = torch.zeros(self.P, dtype=torch.float32, device=dev)
+        self.m = torch.zeros(self.P, dtype=torch.float32, device=dev)
+        self.v = torch.zeros(self.P, dtype=torch.float32, device=dev)
+        self.scaler = torch.zeros(4, dtype=torch.int32, device=dev)
+        self.scaler.view(torch.float32)[0] = loss_scale if prec != G.GCN_F32 else 1.0
+        self.overflow = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
+        self.H1 = torch.empty((n, self.ld_h), dtype=self.dt, device=dev)
+        self.SG1 = torch.empty((n, self.ld_h), dtype=self.dt, device=dev)
+        self.dZ1 = torch.empty((n, self.ld_h), dtype=self.dt, device=dev)
+        self.Z = torch.empty((n, self.ld_e), dtype=self.dt, device=dev)
+        self.SG2 = torch.empty((n, self.ld_e), dtype=self.dt, device=dev)
+        self.dZ = torch.empty((n, self.ld_e), dtype=self.dt, device=dev)
+        self.pair_u = torch.empty(self.K, dtype=torch.int32, device=dev)
+        self.pair_v = torch.empty(self.K, dtype=torch.int32, device=dev)
+        self.pair_g = torch.empty(self.K, dtype=torch.float32, device=dev)
+        self.L1 = G.GcnLayer(self.f_in, self.f_h, self.ld_x, self.ld_h, G.GCN_ACT_RELU, 0.0, 0, 0)
+        self.L2 = G.GcnLayer(self.f_h, self.f_e, self.ld_h, self.ld_e, G.GCN_ACT_NONE, 0.0, 1, 0)
+        ws = max(G.gcn_layer_workspace_size(graph.adj, self.L1, prec),
+                 G.gcn_layer_workspace_size(graph.adj, self.L2, prec),
+                 G.gcn_pair_loss_workspace_size(self.K),
+                 G.gcn_pair_backward_workspace_size(n, self.K))
+        self.ws = torch.empty(ws // 4 + 64, dtype=torch.float32, device=dev)
+        self.adam_c = self.adam.c()
+
+    def _view(self, buf, k, shape):
+        return buf[self.offs[k]:self.offs[k + 1]].view(*shape)
+
+    def W1w(self): return self._view(self.working, 0, (self.f_in, self.ld_h))
+    def W2w(self): return self._view(self.working, 2, (self.f_h, self.ld_e))
+    def b1m(self): return self._view(self.master, 1, (self.ld_h,))
+    def b2m(self): return self._view(self.master, 3, (self.ld_e,))
+    def dW1(self): return self._view(self.grad, 0, (self.f_in, self.ld_h))
+    def db1(self): return self._view(self.grad, 1, (self.ld_h,))
+    def dW2(self): return self._view(self.grad, 2, (self.f_h, self.ld_e))
+    def db2(self): return self._view(self.grad, 3, (self.ld_e,))
+
+    def encode(self, stream=None):
+        a = self.g.adj
+        G.gcn_layer_fwd(a, self.L1, self.prec, True, self.X, self.W1w(), self.b1m(), 0, 0, self.SG1, self.H1,
+                        self.overflow, self.ws, stream)
+        G.gcn_layer_fwd(a, self.L2, self.prec, True, self.H1, self.W2w(), self.b2m(), 0, 0, self.SG2, self.Z,
+                        self.overflow, self.ws, stream)
+
+    def loss_and_backward(self, epoch: int, stream=None):
+        a = self.g.adj
+        G.gcn_sample_pairs(self.n, self.train_u, self.train_v, self.n_pos, self.n_neg, self.seed, epoch,
+                           self.pair_u, self.pair_v, stream)
+        G.gcn_pair_loss(self.n, self.f_e, self.ld_e, self.prec, self.Z, self.pair_u, self.pair_v, self.n_pos,
+                        self.n_neg, self.scaler, self.loss, None, self.pair_g, self.overflow, self.ws, stream)
+        G.gcn_pair_backward(self.n, self.f_e, self.ld_e, self.prec, self.Z, self.pair_u, self.pair_v, self.K,
+                            self.pair_g, self.dZ, self.ld_e, self.overflow, self.ws, stream)
+        G.gcn_layer_bwd(a, self.L2, self.prec, self.H1, self.W2w(), self.dZ, G.GCN_ACT_RELU, 0.0,
+                        self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream)
+        G.gcn_layer_bwd(a, self.L1, self.prec, self.X, self.W1w(), self.dZ1, G.GCN_ACT_NONE, 0.0,
+                        self.dW1(), self.db1(), None, self.SG1, self.overflow, self.ws, stream)
+
+    def optimizer_step(self, stream=None):
+        G.gcn_optimizer_step(self.P, self.master, self.grad, self.m, self.v, self.working, self.prec,
+                             self.adam_c, self.scaler, self.overflow, stream)
+
+    def step(self, epoch: int, stream=None):
+        """One training epoch; asynchronous."""
+        self.encode(stream)
+        self.loss_and_backward(epoch, stream)
+        self.optimizer_step(stream)
+
+    def evaluate(self, test_u, test_v, n_test_pos, stream=None):
+        """AUC and AP of held-out pairs (positives first) on the current
+        embeddings; one host synchronisation."""
+        dev = self.Z.device
+        tu = torch.as_tensor(np.asarray(test_u, np.int32)).to(dev)
+        tv = torch.as_tensor(np.asarray(test_v, np.int32)).to(dev)
+        k = tu.numel()
+        self.encode(stream)
+        scores = torch.empty(k, dtype=torch.float32, device=dev)
+        g = torch.empty(k, dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        flag = torch.zeros(1, dtype=torch.int32, device=dev)
+        ws = torch.empty(G.gcn_pair_loss_workspace_size(k) // 4 + 64, dtype=torch.float32, device=dev)
+        G.gcn_pair_loss(self.n, self.f_e, self.ld_e, self.prec, self.Z, tu, tv, n_test_pos, k - n_test_pos, None,
+                        loss, scores, g, flag, ws, stream)
+        out = torch.empty(2, dtype=torch.float64, device=dev)
+        mws = torch.empty(G.gcn_pair_metrics_workspace_size(n_test_pos), dtype=torch.uint8, device=dev)
+        G.gcn_pair_metrics(scores, n_test_pos, k - n_test_pos, out, mws, stream)
+        auc, ap = out.cpu().tolist()
+        return auc, ap, float(loss.item())
+
+    def scaler_state(self):
+        s = self.scaler.cpu()
+        return dict(scale=float(s.view(torch.float32)[0]), good_steps=int(s[1]), step=int(s[2]),
+                    skipped=int(s[3]))
