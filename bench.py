@@ -110,21 +110,24 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     m = GCN2(dg, wl["X"], wl["labels"], wl["mask"], wl["W1"], wl["W2"], wl["b1"], wl["b2"], prec=prec,
              dropout=0.0 if spec.dropout is None else spec.dropout, seed=wl["dropout_seed"], loss_scale=scale0)
     timer = EventTimer()
+    gtimer = EventTimer()
     for ep in range(warmup):
-        m.step(ep, agg_timer=timer)
+        m.step(ep, agg_timer=timer, gemm_timer=gtimer)
     # the aggregation calls of every `every`-th timed step are bracketed by
     # events (each event record costs the stream a few microseconds, so
     # bracketing every step would slow the throughput being measured)
     every = max(1, steps // 25)
     timer.reserve(2 * (steps // every + 1))        # two aggregation brackets per sampled step
+    gtimer.reserve(2 * (steps // every + 1))       # and two transform brackets
     torch.cuda.synchronize()
     timer.enabled = True
+    gtimer.enabled = True
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     t_start.record()
     for k in range(steps):
-        m.step(warmup + k, agg_timer=timer if k % every == 0 else None)
+        m.step(warmup + k, agg_timer=timer if k % every == 0 else None, gemm_timer=gtimer if k % every == 0 else None)
     t_end.record()
     host_submit = time.perf_counter() - t0      # host time to enqueue the timed steps
     torch.cuda.synchronize()
@@ -135,8 +138,67 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     st = m.scaler_state()
     peak = torch.cuda.max_memory_allocated() - base
     res = dict(prec=prec, wall_s=wall, gpu_ms=gpu_ms, host_submit_s=host_submit, agg_ms=agg_ms, agg_launches=len(timer.pairs),
+               gemm_ms=gtimer.total_ms(), gemm_launches=len(gtimer.pairs),
                loss=loss, scaler=st, peak_bytes=int(peak), n=dg.n, nnz=dg.nnz,
                f_h=m.f_h, C=m.C, f_in=m.f_in, n_correct=int(m.n_correct.item()), n_mask=m.n_mask)
+    del m, dg
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+MFMA_PEAK_TFLOPS = {0: 157.3, 1: 2500.0, 2: 2500.0}   # dense MFMA: fp32, f16, bf16
+
+
+def gemm_object(r, prec, f_in, f_h, C):
+    """The feature transforms S = H W of both layers (one tsgemm launch
+    each), timed with HIP events in the sampled steps: achieved TFLOP/s
+    against the MFMA peak of the storage type, and the ceiling that HBM
+    bandwidth sets at this arithmetic intensity."""
+    n, s = r["n"], (4 if prec == 0 else 2)
+    flops = 2 * n * (f_in * f_h + f_h * C)
+    byts = s * (n * f_in + n * f_h + f_in * f_h) + s * (n * f_h + n * C + f_h * C)
+    calls = r["gemm_launches"] // 2
+    sec = r["gemm_ms"] * 1e-3
+    tf = flops * calls / sec / 1e12
+    peak = MFMA_PEAK_TFLOPS[prec]
+    ceiling = min(1.0, flops / byts * HBM_PEAK_GBS * 1e9 / 1e12 / peak)
+    return dict(kernel="tsgemm_kernel: S = H W of both layers (row-streaming MFMA)", bound="hbm" if ceiling < 1 else "mfma",
+                achieved_tflops=round(tf, 2), peak_tflops=peak, mfma_frac=round(tf / peak, 4),
+                hbm_gbs=round(byts * calls / sec / 1e9, 1), ceiling_frac_at_hbm_peak=round(ceiling, 4),
+                launches=r["gemm_launches"], avg_launch_us=round(r["gemm_ms"] * 1e3 / max(1, r["gemm_launches"]), 2))
+
+
+def run_gae(wl, prec, epochs, warmup, n_pairs=1 << 20):
+    """The link-prediction workload: GAE2 on the training edges, n_pairs
+    positive and n_pairs negative pairs per epoch; epochs timed with HIP
+    events; AUC / AP of the held-out pairs after training (outside the
+    timed region)."""
+    import torch
+    from paper_2010_12635_amd import gcn as G
+    from paper_2010_12635_amd.model import DeviceGraph, GAE2
+
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    dg = DeviceGraph(wl["n"], wl["train_u"], wl["train_v"], prec=prec)
+    m = GAE2(dg, wl["X"], wl["W1"], wl["W2"], wl["train_u"], wl["train_v"], prec=prec, n_pos=n_pairs,
+             n_neg=n_pairs, seed=wl["dropout_seed"], loss_scale=65536.0 if prec != G.GCN_F32 else 1.0)
+    for ep in range(warmup):
+        m.step(ep)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for k in range(epochs):
+        m.step(warmup + k)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    auc, ap, test_loss = m.evaluate(wl["test_u"], wl["test_v"], wl["n_test_pos"])
+    res = dict(ms=ms, auc=auc, ap=ap, test_loss=test_loss, train_loss=float(m.loss.item()),
+               peak_bytes=int(torch.cuda.max_memory_allocated() - base), nnz=dg.nnz, scaler=m.scaler_state())
     del m, dg
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -380,6 +442,8 @@ def main():
     ap.add_argument("--prec", default="f16", choices=sorted(PRECS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-fp32", action="store_true", help="skip the fp32-mode run")
+    ap.add_argument("--gae-epochs", type=int, default=100,
+                    help="epochs of the link-prediction workload (0 skips it)")
     ap.add_argument("--no-largest", dest="largest", action="store_false",
                     help="skip the largest-graph runs (R-MAT scale 27 fp16, 26 and 27 fp32)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0 = skip)")
@@ -408,9 +472,9 @@ def main():
 
     if args.summarize_counters:
         cmd = ("rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --copy-calibration 256\n"
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --gae-epochs 0 --copy-calibration 256\n"
                "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --copy-calibration 256")
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --gae-epochs 0 --copy-calibration 256")
         print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, cmd)))
         return
 
@@ -475,6 +539,8 @@ def main():
                     launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
                     algorithmic_bytes_per_launch_avg=int(per_epoch_bytes / 2))
 
+    gemm = gemm_object(r, prec, r["f_in"], r["f_h"], r["C"])
+
     spmm = None
     if args.spmm_workload != "none" and args.spmm_steps > 0:
         log(f"[bench] spmm workload {args.spmm_workload}: generating")
@@ -492,9 +558,29 @@ def main():
                     algorithmic_bytes_per_launch_avg=int(b2 / 2),
                     gather_bytes_per_launch_avg=int(r2["nnz"] * (r2["f_h"] + r2["C"]) * s / 2),
                     traffic=load_traffic("spmm_f16", "spmm.hip", "normalize.hip") if prec != 0 and args.spmm_workload == "rmat21" else None,
-                    peak_mem_bytes=r2["peak_bytes"])
+                    peak_mem_bytes=r2["peak_bytes"], gemm=gemm_object(r2, prec, r2["f_in"], r2["f_h"], r2["C"]))
         log(f"[bench] spmm: {spmm['ms_per_step']} ms/epoch, {spmm['achieved']} GB/s algorithmic")
         del wl2
+
+    gae = None
+    if args.gae_epochs > 0:
+        log("[bench] link-prediction workload (graph auto-encoder, R-MAT scale 17): generating")
+        wl3 = I.gae_workload(args.seed)
+        rg = run_gae(wl3, prec, args.gae_epochs, 3)
+        rg32 = None if args.no_fp32 else run_gae(wl3, 0, args.gae_epochs, 3)
+        gae = dict(workload=(f"R-MAT scale 17 (edge factor 16, 0.57/0.19/0.19/0.05), {wl3['train_u'].size} training edges, "
+                             f"{wl3['n_test_pos']} held-out positives + as many non-edges; X 131072x256 N(0,1); "
+                             f"encoder 256 -> 256 -> 64 (ReLU, no dropout); decoder sigmoid(<z_u, z_v>) on 2^20 "
+                             f"positive + 2^20 negative pairs per epoch; Adam lr 0.01; loss scale 2^16"),
+                   epochs=args.gae_epochs, epochs_per_s=round(args.gae_epochs / (rg["ms"] * 1e-3), 2),
+                   ms_per_step=round(rg["ms"] / args.gae_epochs, 3), auc=round(rg["auc"], 4), ap=round(rg["ap"], 4),
+                   train_loss=round(rg["train_loss"], 4), held_out_loss=round(rg["test_loss"], 4),
+                   peak_mem_bytes=rg["peak_bytes"], loss_scale=rg["scaler"],
+                   fp32=None if rg32 is None else dict(epochs_per_s=round(args.gae_epochs / (rg32["ms"] * 1e-3), 2),
+                                                       auc=round(rg32["auc"], 4), ap=round(rg32["ap"], 4),
+                                                       peak_mem_bytes=rg32["peak_bytes"]))
+        log(f"[bench] gae: {gae['epochs_per_s']} epochs/s, AUC {gae['auc']}, AP {gae['ap']}")
+        del wl3
 
     largest = None
     if args.largest:
@@ -552,7 +638,9 @@ def main():
         "train_acc": round(r["n_correct"] / max(1, r["n_mask"]), 4),
         "loss_scale": r["scaler"],
         "roofline": roofline,
+        "gemm": gemm,
         "spmm": spmm,
+        "gae": gae,
         "largest_graph": largest,
         "cpu_baseline": cpu,
     }

@@ -27,6 +27,11 @@ def round8(x: int) -> int:
     return (x + 7) // 8 * 8
 
 
+def _nullctx():
+    import contextlib
+    return contextlib.nullcontext()
+
+
 class DeviceGraph:
     """A_hat on the device, built by gcn_normalize (+ gcn_schedule for CSR)."""
 
@@ -205,11 +210,12 @@ class GCN2:
     def scale_ptr(self):
         return self.scaler.data_ptr()   # first field of gcn_scaler is the float scale
 
-    def forward(self, epoch: int, training: bool = True, stream=None, agg_timer=None):
+    def forward(self, epoch: int, training: bool = True, stream=None, agg_timer=None, gemm_timer=None):
         """Both layers.  With ``agg_timer`` (a callable returning a context
         manager), each layer runs as gcn_transform + gcn_aggregate and the
-        aggregation call is bracketed by the timer; the arithmetic is the
-        same as gcn_layer_fwd."""
+        aggregation call is bracketed by the timer (the transform by
+        ``gemm_timer`` if given); the arithmetic is the same as
+        gcn_layer_fwd."""
         a = self.g.adj
         if agg_timer is None:
             G.gcn_layer_fwd(a, self.L1, self.prec, training, self.X, self.W1w(), self.b1m(), self.seed, epoch,
@@ -219,8 +225,9 @@ class GCN2:
             return
         for L, H, W, b, S, out in ((self.L1, self.X, self.W1w(), self.b1m(), self.SG1, self.H1),
                                    (self.L2, self.H1, self.W2w(), self.b2m(), self.SG2, self.Z2)):
-            G.gcn_transform(self.n, L.f_in, L.f_out, self.prec, H, L.ld_in, W, L.ld_out, S, L.ld_out,
-                            self.overflow, self.ws, stream)
+            with (gemm_timer() if gemm_timer is not None else _nullctx()):
+                G.gcn_transform(self.n, L.f_in, L.f_out, self.prec, H, L.ld_in, W, L.ld_out, S, L.ld_out,
+                                self.overflow, self.ws, stream)
             with agg_timer():
                 G.gcn_aggregate(a, L.f_out, self.prec, S, L.ld_out, b, L.act, L.dropout_p, training, self.seed,
                                 L.layer_id, epoch, out, L.ld_out, self.overflow, self.ws, stream)
@@ -238,9 +245,9 @@ class GCN2:
         G.gcn_optimizer_step(self.P, self.master, self.grad, self.m, self.v, self.working, self.prec,
                              self.adam_c, self.scaler, self.overflow, stream)
 
-    def step(self, epoch: int, stream=None, agg_timer=None):
+    def step(self, epoch: int, stream=None, agg_timer=None, gemm_timer=None):
         """One full training step; asynchronous (no host synchronisation)."""
-        self.forward(epoch, True, stream, agg_timer)
+        self.forward(epoch, True, stream, agg_timer, gemm_timer)
         self.loss_and_backward(stream)
         self.optimizer_step(stream)
 
