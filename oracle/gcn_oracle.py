@@ -25,6 +25,10 @@ leaves open:
 * adam_step() / LossScaler: fp32 master weights updated by Adam on unscaled
   gradients, dynamic loss scaling that skips a step and halves the scale on
   overflow and doubles it after a run of good steps (O1/O2 description).
+* round_to() / round_storage(): rounding to the 16-bit storage types
+  (the casts of the O1 cast policy and of every 16-bit tensor).
+* adam_step_half(): the O3 level, Adam with parameters and moments held in
+  16 bits and no loss scale, each elementwise operation rounded.
 * philox4x64(): the counter-based generator (Salmon et al., SC'11) that
   draws the dropout keep decisions and the decoder's pairs.
 * Link prediction (Section "Graph Auto-Encoders", Eq. (2): the decoder
@@ -49,6 +53,7 @@ __all__ = [
     "graph_degrees", "graph_rows", "dropout_keep_rows", "norm_adj_matvec",
     "layer_bwd", "adam_step", "LossScaler", "AdamState",
     "PAIR_STREAM", "sample_pairs", "pair_loss", "pair_backward", "auc_ap",
+    "round_to", "round_storage", "adam_step_half",
 ]
 
 
@@ -448,6 +453,100 @@ def adam_step(master, grad_scaled, state: AdamState, scaler: LossScaler,
     vhat = state.v / (1.0 - beta2 ** state.t)
     new = np.asarray(master, np.float64) - lr * mhat / (np.sqrt(vhat) + eps)
     return new, True
+
+
+# ---------------------------------------------------------------------------
+# Storage rounding and the pure 16-bit optimiser (optimisation level O3)
+# ---------------------------------------------------------------------------
+
+_FORMATS = {            # fraction bits, smallest normal exponent, largest finite value
+    "f16": (10, -14, 65504.0),
+    "bf16": (7, -126, 255.0 * 2.0 ** 120),
+}
+
+
+def round_to(z, prec):
+    """float64 values ``z`` rounded to the 16-bit format ``prec`` ("f16":
+    IEEE 754 binary16; "bf16": 8 exponent bits, 7 fraction bits) with
+    round-to-nearest, ties to even, straight from the exact value.
+
+    Written out from the formats' definition: around |z| the representable
+    values are spaced 2^(e - p) apart, with p the fraction bits and
+    e = max(floor(log2 |z|), e_min) (the subnormal range shares the
+    spacing of the smallest binade); z / spacing is rounded to the nearest
+    integer, ties to the even one; a result beyond the largest finite value
+    becomes infinity.  NaN, infinities and signed zeros pass through."""
+    if prec == "f32":
+        return np.asarray(z, np.float32).astype(np.float64)
+    p, emin, vmax = _FORMATS[prec]
+    z = np.asarray(z, np.float64)
+    out = z.copy()
+    fin = np.isfinite(z) & (z != 0.0)
+    if np.any(fin):
+        a = np.abs(z[fin])
+        e = np.floor(np.log2(a))
+        # floor(log2) of a float64 can be off by one next to powers of two
+        e = np.where(np.exp2(e) > a, e - 1.0, e)
+        e = np.where(np.exp2(e + 1.0) <= a, e + 1.0, e)
+        e = np.maximum(e, float(emin))
+        spacing = np.exp2(e - p)
+        q = a / spacing                  # exact: division by a power of two
+        lo = np.floor(q)
+        frac = q - lo
+        up = (frac > 0.5) | ((frac == 0.5) & (np.mod(lo, 2.0) == 1.0))
+        mag = (lo + up) * spacing
+        out[fin] = np.copysign(np.where(mag > vmax, np.inf, mag), z[fin])
+    return out
+
+
+def round_storage(x, prec):
+    """Values of float32 array ``x`` stored in a 16-bit type (the cast of
+    the O1 cast lists and of every 16-bit tensor), as float64.
+    "f16": round_to(x, "f16").  "bf16": the upper half of the binary32
+    encoding after rounding its lower 16 bits to nearest, ties to even
+    (NaN stays NaN) -- the encoding-level statement of the same rounding.
+    "f32": x itself."""
+    x32 = np.asarray(x, np.float32)
+    if prec == "bf16":
+        b = x32.view(np.uint32).astype(np.uint64)
+        r = ((b + np.uint64(0x7FFF) + ((b >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)) << np.uint64(16)
+        out = r.astype(np.uint32).view(np.float32).astype(np.float64)
+        out[np.isnan(x32)] = np.nan
+        return out
+    return round_to(x32.astype(np.float64), prec)
+
+
+def adam_step_half(w, grad, m, v, t, prec="f16", lr=0.01, beta1=0.9, beta2=0.999, eps=1e-8):
+    """One Adam step of optimisation level O3 (Section "Background and
+    Motivation": every operation in 16 bits): parameters and both moments
+    are held in the storage type ``prec``, there is no master copy and no
+    loss scale, and a non-finite value is applied like any other.  Each
+    line below is one elementwise operation whose exact result, computed
+    from the already rounded operands, is rounded to ``prec`` (round_to):
+        g  = r(grad)
+        m' = r(b1 m + (1 - b1) g)
+        v' = r(b2 v + (1 - b2) g g)
+        mh = r(m' / (1 - b1^t))
+        vh = r(v' / (1 - b2^t))
+        d  = r(r(sqrt(vh)) + eps)
+        w' = r(w - r(lr mh / d))
+    t >= 1 is the step number of this update.  The hyper-parameters are
+    taken at float32 precision, as the device receives them.
+    Returns (w', m', v') as float64 arrays of representable values."""
+    r = lambda z: round_to(z, prec)
+    lr, b1, b2, eps = (float(np.float32(z)) for z in (lr, beta1, beta2, eps))
+    w = np.asarray(w, np.float64)
+    m = np.asarray(m, np.float64)
+    v = np.asarray(v, np.float64)
+    with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
+        g = round_storage(grad, prec)
+        m2 = r(b1 * m + (1.0 - b1) * g)
+        v2 = r(b2 * v + (1.0 - b2) * g * g)
+        mh = r(m2 / (1.0 - b1 ** t))
+        vh = r(v2 / (1.0 - b2 ** t))
+        d = r(r(np.sqrt(vh)) + eps)
+        w2 = r(w - r(lr * mh / d))
+    return w2, m2, v2
 
 
 # ---------------------------------------------------------------------------

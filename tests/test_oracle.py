@@ -417,6 +417,119 @@ def test_loss_scaler_script():
     assert sc.scale == 16.0                                         # clamps at max
 
 
+# ------------------------------------------- storage rounding, O3 optimiser
+
+def _binary16_values():
+    """Every finite non-negative binary16 value from the format's fields:
+    (-1)^s 2^(E - 15) (1 + f / 1024) for E in 1..30, 2^-14 (f / 1024) for E = 0."""
+    E = np.arange(32)[:, None]
+    f = np.arange(1024)[None, :]
+    normal = np.exp2(E - 15.0) * (1.0 + f / 1024.0)
+    sub = np.exp2(-14.0) * (f / 1024.0)
+    vals = np.where(E == 0, sub, normal)[:31].ravel()
+    return np.sort(vals)
+
+
+def test_round_to_binary16_fixed_points_and_midpoints():
+    v = _binary16_values()
+    assert v[-1] == 65504.0 and v[1] == 2.0**-24
+    assert np.array_equal(O.round_to(v, "f16"), v)
+    assert np.array_equal(O.round_to(-v, "f16"), -v)
+    # the midpoint of two neighbours rounds to the one with an even fraction
+    # field (the even multiple of the local spacing); just off the midpoint,
+    # to the nearer one
+    lo, hi = v[:-1], v[1:]
+    mid = (lo + hi) / 2.0
+    spacing = hi - lo
+    even_lo = np.mod(np.round(lo / spacing), 2.0) == 0.0
+    assert np.array_equal(O.round_to(mid, "f16"), np.where(even_lo, lo, hi))
+    assert np.array_equal(O.round_to(mid - spacing / 8, "f16"), lo)
+    assert np.array_equal(O.round_to(mid + spacing / 8, "f16"), hi)
+
+
+def test_round_to_binary16_hand_values():
+    cases = [(65504.0, 65504.0), (65519.99, 65504.0), (65520.0, np.inf),      # tie above the max: to even (overflow)
+             (1e6, np.inf), (2.0**-24, 2.0**-24), (2.0**-25, 0.0),           # tie at the bottom: to even (zero)
+             (3 * 2.0**-26, 2.0**-24), (1 + 2.0**-11, 1.0), (1 + 3 * 2.0**-11, 1 + 2.0**-9),
+             (1e-8, 0.0), (0.1, 0.0999755859375), (-0.1, -0.0999755859375)]
+    x = np.array([c[0] for c in cases])
+    want = np.array([c[1] for c in cases])
+    assert np.array_equal(O.round_to(x, "f16"), want)
+    z = O.round_to(np.array([-0.0, np.inf, -np.inf, np.nan]), "f16")
+    assert np.signbit(z[0]) and z[1] == np.inf and z[2] == -np.inf and np.isnan(z[3])
+
+
+def test_round_storage_f16_matches_numpy_conversion():
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal(200_000) * np.exp2(rng.uniform(-30, 18, 200_000))).astype(np.float32)
+    with np.errstate(over="ignore"):
+        want = x.astype(np.float16).astype(np.float64)
+    assert np.array_equal(O.round_storage(x, "f16"), want)
+
+
+def test_round_storage_bf16_two_formulations_agree():
+    rng = np.random.default_rng(4)
+    with np.errstate(over="ignore"):
+        x = (rng.standard_normal(200_000) * np.exp2(rng.uniform(-140, 127, 200_000))).astype(np.float32)
+    x = np.concatenate([x, np.float32([3.4028235e38, -3.4028235e38, 1e-45, 0.0, -0.0, np.inf])])
+    a = O.round_storage(x, "bf16")          # encoding-level rounding
+    b = O.round_to(x.astype(np.float64), "bf16")   # spacing-level rounding
+    assert np.array_equal(a, b)
+    hand = O.round_storage(np.float32([1 + 2.0**-8, 1 + 3 * 2.0**-8, 0.1, 3.4028235e38]), "bf16")
+    assert np.array_equal(hand, [1.0, 1.015625, 0.10009765625, np.inf])
+    assert np.isnan(O.round_storage(np.float32([np.nan]), "bf16")[0])
+
+
+def test_adam_half_first_step_large_gradient_matches_adam():
+    # |g| well inside binary16's range: the O3 step lands within rounding of
+    # the exact first Adam step, w - lr g / (|g| + eps)
+    g = np.array([0.5, -0.75, 0.25, 1.0])
+    w0 = O.round_to(np.array([1.0, -2.0, 0.3, 0.05]), "f16")
+    z = np.zeros(4)
+    w1, m1, v1 = O.adam_step_half(w0, g.astype(np.float32), z, z, 1, "f16", lr=0.01)
+    exact = w0 - 0.01 * g / (np.abs(g) + 1e-8)
+    ulp = np.exp2(np.floor(np.log2(np.abs(exact))) - 10)
+    assert np.all(np.abs(w1 - exact) <= 2 * ulp)
+    assert np.array_equal(O.round_to(w1, "f16"), w1)
+
+
+def test_adam_half_small_gradient_underflows_to_infinity():
+    # (1 - b2) g^2 = 1e-3 * (1e-3)^2 = 1e-9 lies below half of binary16's
+    # smallest subnormal 2^-24 (about 6e-8), so v rounds to 0; eps = 1e-8
+    # rounds to 0 too, and the update m_hat / 0 is infinite
+    w0 = np.array([1.0, 1.0])
+    g = np.float32([1e-3, -1e-3])
+    w1, m1, v1 = O.adam_step_half(w0, g, np.zeros(2), np.zeros(2), 1, "f16")
+    assert np.array_equal(v1, [0.0, 0.0])
+    assert w1[0] == -np.inf and w1[1] == np.inf
+    # with zero gradient and zero moments the update is 0 / 0
+    w2, _, _ = O.adam_step_half(w0, np.float32([0.0, 0.0]), np.zeros(2), np.zeros(2), 1, "f16")
+    assert np.all(np.isnan(w2))
+    # bf16 has binary32's exponent range: the same step stays finite and
+    # within rounding of the exact step
+    w3, _, v3 = O.adam_step_half(w0, g, np.zeros(2), np.zeros(2), 1, "bf16")
+    assert np.all(v3 > 0)
+    assert np.all(np.abs(w3 - (1.0 - 0.01 * np.sign(g))) <= 2 * 2.0**-8)
+
+
+def test_adam_half_tracks_fp64_adam_for_large_gradients():
+    rng = np.random.default_rng(5)
+    n = 64
+    w = O.round_to(rng.uniform(-1, 1, n), "f16")
+    m = np.zeros(n)
+    v = np.zeros(n)
+    ref = w.copy()
+    st_ = O.AdamState(n)
+    sc = O.LossScaler(scale=1.0)
+    for t in range(1, 4):
+        g = (rng.choice([-1, 1], n) * rng.uniform(0.1, 1.0, n)).astype(np.float32)
+        w, m, v = O.adam_step_half(w, g, m, v, t, "f16", lr=0.001)
+        ref, _ = O.adam_step(ref, g.astype(np.float64), st_, sc, lr=0.001)
+    # three updates of about lr each: binary16 rounding of w (spacing
+    # <= 2^-11 on [-1, 1]) bounds the difference
+    assert np.max(np.abs(w - ref)) <= 4 * 2.0**-11
+
+
 def test_sampled_graph_helpers_match_full_graph():
     rng = np.random.default_rng(21)
     n = 400
