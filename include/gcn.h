@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 3
+#define GCN_ABI_VERSION 4
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -307,6 +307,51 @@ gcn_status gcn_loss(int64_t n, int64_t C, int64_t ld, int32_t prec, const void* 
 gcn_status gcn_optimizer_step(int64_t count, float* master, const float* grad, float* m, float* v,
                               void* working, int32_t prec, const gcn_adam_config* cfg,
                               gcn_scaler* state, int32_t* overflow_flag, void* stream);
+
+/* ===========================================================================
+ * Other optimisation levels (Section "Background and Motivation"): O0 is the
+ * fp32 path (prec = GCN_F32 everywhere), O2 the path above.  The two calls
+ * below supply what O1 and O3 need beyond it.
+ * ======================================================================== */
+
+/* gcn_cast: dst = src converted to dst_prec, for a rows x cols block
+ * (row-major, leading dimensions ld_src / ld_dst in elements; with rows == 1
+ * the leading dimensions are ignored and cols may be any length, e.g. a
+ * whole flat buffer).  16-bit results are rounded to nearest, ties to even;
+ * widening is exact; src_prec == dst_prec copies.  This is the cast of the
+ * O1 cast lists: GEMM-class operations run on 16-bit copies of fp32
+ * operands, the loss on an fp32 copy of 16-bit logits.
+ * *overflow is set to 1 when an output element is not finite (NULL ok).
+ * Columns [cols, ld_dst) of dst are not written.
+ * Errors: GCN_ERR_SHAPE (rows, cols <= 0, or rows > 1 with ld < cols),
+ * GCN_ERR_ALIGNMENT (src/dst not 16-byte aligned, or rows > 1 with
+ * ld_src or ld_dst not a multiple of 8), GCN_ERR_INVALID_ARG (NULL, or a
+ * bad precision).  Asynchronous on `stream`. */
+gcn_status gcn_cast(int64_t rows, int64_t cols, int32_t src_prec, const void* src, int64_t ld_src,
+                    int32_t dst_prec, void* dst, int64_t ld_dst, int32_t* overflow, void* stream);
+
+/* gcn_optimizer_step_half: one Adam step of level O3 ("full 16-bit"):
+ * parameters w and moments m, v are `count` elements of prec (GCN_F16 or
+ * GCN_BF16), with no fp32 master copy and no loss scale.  Each line is one
+ * elementwise operation, evaluated in fp32 (one rounding per arithmetic
+ * operation, no fused multiply-add) and rounded to prec by r(), with
+ * t = state->step + 1 and c1 = 1 - b1^t, c2 = 1 - b2^t computed in double
+ * and rounded to fp32:
+ *   g = r(grad);  m = r(b1 * m + (1 - b1) * g);  v = r(b2 * v + ((1 - b2) * g) * g);
+ *   mh = r(m / c1);  vh = r(v / c2);
+ *   d = r(r(sqrt(vh)) + eps);  w = r(w - r((lr * mh) / d)).
+ * Non-finite values are applied like any other (in binary16, eps = 1e-8
+ * and small second moments round to 0, and the update becomes infinite:
+ * the instability of level O3).  widened (NULL ok) receives w as fp32
+ * (e.g. the bias operand of the layer epilogue).  state->step += 1 always;
+ * state->skipped counts steps whose grad or *overflow_flag was non-finite;
+ * state->scale is left as it is (the loss kernel should read 1).  Only
+ * cfg's lr, beta1, beta2 and eps are used.  *overflow_flag is cleared.
+ * Errors: GCN_ERR_SHAPE (count <= 0), GCN_ERR_INVALID_ARG (NULL required
+ * pointer, prec not 16-bit, bad hyper-parameters).  Asynchronous. */
+gcn_status gcn_optimizer_step_half(int64_t count, void* w, const float* grad, void* m, void* v,
+                                   float* widened, int32_t prec, const gcn_adam_config* cfg,
+                                   gcn_scaler* state, int32_t* overflow_flag, void* stream);
 
 /* ===========================================================================
  * Link prediction: the graph auto-encoder of Section "Graph Auto-Encoders",

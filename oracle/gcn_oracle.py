@@ -520,33 +520,44 @@ def adam_step_half(w, grad, m, v, t, prec="f16", lr=0.01, beta1=0.9, beta2=0.999
     """One Adam step of optimisation level O3 (Section "Background and
     Motivation": every operation in 16 bits): parameters and both moments
     are held in the storage type ``prec``, there is no master copy and no
-    loss scale, and a non-finite value is applied like any other.  Each
-    line below is one elementwise operation whose exact result, computed
-    from the already rounded operands, is rounded to ``prec`` (round_to):
+    loss scale, and a non-finite value is applied like any other.
+
+    Reading: an elementwise operation on 16-bit tensors is evaluated in
+    single precision (IEEE binary32, one rounding per arithmetic operation,
+    no fused multiply-add) and its result rounded to the storage type.
+    Each line is one such operation, r() the rounding to ``prec``:
         g  = r(grad)
-        m' = r(b1 m + (1 - b1) g)
-        v' = r(b2 v + (1 - b2) g g)
-        mh = r(m' / (1 - b1^t))
-        vh = r(v' / (1 - b2^t))
+        m' = r(b1 * m + (1 - b1) * g)
+        v' = r(b2 * v + ((1 - b2) * g) * g)
+        mh = r(m' / c1),  c1 = 1 - b1^t
+        vh = r(v' / c2),  c2 = 1 - b2^t
         d  = r(r(sqrt(vh)) + eps)
-        w' = r(w - r(lr mh / d))
-    t >= 1 is the step number of this update.  The hyper-parameters are
-    taken at float32 precision, as the device receives them.
+        w' = r(w - r((lr * mh) / d))
+    The hyper-parameters are binary32 values; the bias corrections c1, c2
+    are 1 - b^t evaluated exactly (here in float64) and rounded to binary32.
+    t >= 1 is the step number of this update.
     Returns (w', m', v') as float64 arrays of representable values."""
-    r = lambda z: round_to(z, prec)
-    lr, b1, b2, eps = (float(np.float32(z)) for z in (lr, beta1, beta2, eps))
-    w = np.asarray(w, np.float64)
-    m = np.asarray(m, np.float64)
-    v = np.asarray(v, np.float64)
+    f32 = np.float32
+
+    def r(z):     # binary32 result -> storage type
+        return f32(round_to(np.asarray(z, f32).astype(np.float64), prec)) if np.ndim(z) == 0 else \
+            round_to(np.asarray(z, f32).astype(np.float64), prec).astype(f32)
+
+    lr, b1, b2, eps = (f32(z) for z in (lr, beta1, beta2, eps))
+    c1 = f32(1.0 - float(b1) ** t)
+    c2 = f32(1.0 - float(b2) ** t)
+    w = np.asarray(w, np.float64).astype(f32)
+    m = np.asarray(m, np.float64).astype(f32)
+    v = np.asarray(v, np.float64).astype(f32)
     with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
-        g = round_storage(grad, prec)
-        m2 = r(b1 * m + (1.0 - b1) * g)
-        v2 = r(b2 * v + (1.0 - b2) * g * g)
-        mh = r(m2 / (1.0 - b1 ** t))
-        vh = r(v2 / (1.0 - b2 ** t))
+        g = r(np.asarray(grad, f32))
+        m2 = r(b1 * m + (f32(1) - b1) * g)
+        v2 = r(b2 * v + ((f32(1) - b2) * g) * g)
+        mh = r(m2 / c1)
+        vh = r(v2 / c2)
         d = r(r(np.sqrt(vh)) + eps)
-        w2 = r(w - r(lr * mh / d))
-    return w2, m2, v2
+        w2 = r(w - r((lr * mh) / d))
+    return w2.astype(np.float64), m2.astype(np.float64), v2.astype(np.float64)
 
 
 # ---------------------------------------------------------------------------

@@ -506,6 +506,36 @@ gcn_status gcn_optimizer_step(int64_t count, float* master, const float* grad, f
   return finish(hipSuccess, s);
 }
 
+gcn_status gcn_cast(int64_t rows, int64_t cols, int32_t src_prec, const void* src, int64_t ld_src, int32_t dst_prec,
+                    void* dst, int64_t ld_dst, int32_t* overflow, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!valid_prec(src_prec) || !valid_prec(dst_prec) || !src || !dst) return GCN_ERR_INVALID_ARG;
+  if (rows <= 0 || cols <= 0) return GCN_ERR_SHAPE;
+  if (rows > 1 && (ld_src < cols || ld_dst < cols)) return GCN_ERR_SHAPE;
+  if (!aligned16(src) || !aligned16(dst)) return GCN_ERR_ALIGNMENT;
+  if (rows > 1 && (ld_src % 8 || ld_dst % 8)) return GCN_ERR_ALIGNMENT;
+  GCN_HIP(cast_launch(src_prec, dst_prec, rows, cols, src, rows > 1 ? ld_src : 0, dst, rows > 1 ? ld_dst : 0,
+                      overflow, s));
+  return finish(hipSuccess, s);
+}
+
+gcn_status gcn_optimizer_step_half(int64_t count, void* w, const float* grad, void* m, void* v, float* widened,
+                                   int32_t prec, const gcn_adam_config* cfg, gcn_scaler* state,
+                                   int32_t* overflow_flag, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (count <= 0) return GCN_ERR_SHAPE;
+  if (!w || !grad || !m || !v || !cfg || !state || !overflow_flag) return GCN_ERR_INVALID_ARG;
+  if (prec != GCN_F16 && prec != GCN_BF16) return GCN_ERR_INVALID_ARG;
+  if (!(cfg->lr > 0.f) || !(cfg->beta1 >= 0.f && cfg->beta1 < 1.f) || !(cfg->beta2 >= 0.f && cfg->beta2 < 1.f) ||
+      !(cfg->eps >= 0.f))
+    return GCN_ERR_INVALID_ARG;
+  AdamHyper hp{};
+  hp.lr = cfg->lr; hp.beta1 = cfg->beta1; hp.beta2 = cfg->beta2; hp.eps = cfg->eps;
+  GCN_HIP(adam_half_launch(count, w, grad, m, v, widened, prec, hp, reinterpret_cast<ScalerState*>(state),
+                           overflow_flag, s));
+  return finish(hipSuccess, s);
+}
+
 gcn_status gcn_sample_pairs(int64_t n, const int32_t* edge_u, const int32_t* edge_v, int64_t n_edges, int64_t n_pos,
                             int64_t n_neg, uint64_t seed, uint64_t epoch, int32_t* pair_u, int32_t* pair_v,
                             void* stream) {

@@ -41,6 +41,7 @@ EXPORTED = (
     "gcn_dense_tiled_elems", "gcn_densify",
     "gcn_sample_pairs", "gcn_pair_loss_workspace_size", "gcn_pair_loss", "gcn_pair_backward_workspace_size",
     "gcn_pair_backward", "gcn_pair_metrics_workspace_size", "gcn_pair_metrics",
+    "gcn_cast", "gcn_optimizer_step_half",
 )
 
 _DTYPES = {GCN_F32: torch.float32, GCN_F16: torch.float16, GCN_BF16: torch.bfloat16}
@@ -138,6 +139,8 @@ def lib():
         "gcn_pair_backward": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, I64, P, P, SZ, P]),
         "gcn_pair_metrics_workspace_size": (I32, [I64, PSZ]),
         "gcn_pair_metrics": (I32, [P, I64, I64, P, P, SZ, P]),
+        "gcn_cast": (I32, [I64, I64, I32, P, I64, I32, P, I64, P, P]),
+        "gcn_optimizer_step_half": (I32, [I64, P, P, P, P, P, I32, ctypes.POINTER(GcnAdamConfig), P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -248,6 +251,19 @@ def gcn_optimizer_step(count, master, grad, m, v, working, prec, cfg: GcnAdamCon
     st = lib().gcn_optimizer_step(count, _ptr(master), _ptr(grad), _ptr(m), _ptr(v), _ptr(working), prec,
                                   ctypes.byref(cfg), _ptr(state), _ptr(overflow), _stream(stream))
     _check(st, "gcn_optimizer_step")
+
+
+def gcn_optimizer_step_half(count, w, grad, m, v, widened, prec, cfg: GcnAdamConfig, state, overflow,
+                            stream=None):
+    st = lib().gcn_optimizer_step_half(count, _ptr(w), _ptr(grad), _ptr(m), _ptr(v), _ptr(widened), prec,
+                                       ctypes.byref(cfg), _ptr(state), _ptr(overflow), _stream(stream))
+    _check(st, "gcn_optimizer_step_half")
+
+
+def gcn_cast(rows, cols, src_prec, src, ld_src, dst_prec, dst, ld_dst, overflow=None, stream=None):
+    st = lib().gcn_cast(rows, cols, src_prec, _ptr(src), ld_src, dst_prec, _ptr(dst), ld_dst, _ptr(overflow),
+                        _stream(stream))
+    _check(st, "gcn_cast")
 
 
 def gcn_transform_workspace_size(n, f_in, f_out, prec) -> int:

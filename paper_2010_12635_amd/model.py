@@ -114,17 +114,61 @@ class AdamConfig:
                                self.interval, self.min_scale, self.max_scale)
 
 
+LEVELS = ("O0", "O1", "O2", "O3")
+
+
 class GCN2:
-    """Two-layer GCN for vertex classification with device-resident state."""
+    """Two-layer GCN for vertex classification with device-resident state.
+
+    ``level`` selects the optimisation level of Section "Background and
+    Motivation" (default: O0 for prec = GCN_F32, else O2):
+
+    * O0: everything in fp32.
+    * O2: 16-bit weights, activations and gradients; fp32 master weights
+      and Adam moments; dynamic loss scaling.
+    * O1: the cast-list policy.  The model's inputs (X and A_hat) and its
+      parameters stay fp32; the GEMM-class operations (the transform, the
+      aggregation and their backward products) run on 16-bit copies made by
+      gcn_cast at every forward pass (the weights' copy is cached per step:
+      it is the optimiser's working copy), and the loss runs in fp32 on an
+      fp32 copy of the logits; dynamic loss scaling.  ``graph`` must then
+      hold A_hat in fp32, CSR or row-major dense.
+    * O3: every tensor in 16 bits, the weights and the Adam moments
+      included (gcn_optimizer_step_half); no master copy and no loss scale.
+    """
 
     def __init__(self, graph: DeviceGraph, X, labels, mask, W1, W2, b1=None, b2=None, prec=G.GCN_F16,
-                 dropout=0.5, seed=0, loss_scale=65536.0, adam: AdamConfig | None = None, device="cuda"):
+                 dropout=0.5, seed=0, loss_scale=65536.0, adam: AdamConfig | None = None, device="cuda",
+                 level: str | None = None):
         dev = torch.device(device)
+        if level is None:
+            level = "O0" if prec == G.GCN_F32 else "O2"
+        if level not in LEVELS:
+            raise ValueError(f"level must be one of {LEVELS}")
+        if (level == "O0") != (prec == G.GCN_F32):
+            raise ValueError("O0 computes in fp32 (prec = GCN_F32); O1-O3 need a 16-bit prec")
+        self.level = level
         self.g = graph
         self.prec = prec
         self.dt = G.torch_dtype(prec)
         n = graph.n
         self.n = n
+        # the adjacency the layers read: for O1 a 16-bit copy of the fp32
+        # input, refreshed by every forward pass
+        self.adj = graph.adj
+        self.A16 = None
+        if level == "O1":
+            a = graph.adj
+            if a.value_prec != G.GCN_F32 or a.format == G.GCN_DENSE_TILED:
+                raise ValueError("O1 casts an fp32 A_hat: build the graph with prec=GCN_F32 and tiled=False")
+            self.adj = G.GcnAdj.from_buffer_copy(a)
+            self.adj.value_prec = prec
+            if a.format == G.GCN_DENSE:
+                self.A16 = torch.empty(graph.dense.shape, dtype=self.dt, device=dev)
+                self.adj.dense = self.A16.data_ptr()
+            elif graph.values is not None:
+                self.A16 = torch.empty(graph.nnz, dtype=self.dt, device=dev)
+                self.adj.values = self.A16.data_ptr()
         self.f_in, self.f_h = W1.shape
         self.C = W2.shape[1]
         assert W2.shape[0] == self.f_h
@@ -134,7 +178,12 @@ class GCN2:
         self.adam = adam or AdamConfig()
         # inputs (padding columns zero); a device tensor already in the
         # storage layout (n x round8(f_in), storage dtype) is used in place
-        if isinstance(X, torch.Tensor) and X.is_cuda and X.dtype == self.dt and tuple(X.shape) == (n, self.ld_x):
+        self.X32 = None
+        if level == "O1":     # fp32 input plus the 16-bit copy its GEMM reads
+            self.X32 = torch.zeros((n, self.ld_x), dtype=torch.float32, device=dev)
+            self.X32[:, : self.f_in] = torch.as_tensor(np.asarray(X, np.float32)).to(dev)
+            self.X = torch.zeros((n, self.ld_x), dtype=self.dt, device=dev)
+        elif isinstance(X, torch.Tensor) and X.is_cuda and X.dtype == self.dt and tuple(X.shape) == (n, self.ld_x):
             self.X = X
         else:
             self.X = torch.zeros((n, self.ld_x), dtype=self.dt, device=dev)
@@ -167,10 +216,16 @@ class GCN2:
         self.master = torch.as_tensor(master).to(dev)
         self.working = self.master.to(self.dt)
         self.grad = torch.zeros(self.P, dtype=torch.float32, device=dev)
-        self.m = torch.zeros(self.P, dtype=torch.float32, device=dev)
-        self.v = torch.zeros(self.P, dtype=torch.float32, device=dev)
+        # Adam moments: fp32 next to the masters, 16-bit in O3 (where
+        # `master` only holds the fp32 widening of the 16-bit parameters that
+        # the bias epilogue reads)
+        mdt = self.dt if level == "O3" else torch.float32
+        if level == "O3":
+            self.master = self.working.float()
+        self.m = torch.zeros(self.P, dtype=mdt, device=dev)
+        self.v = torch.zeros(self.P, dtype=mdt, device=dev)
         self.scaler = torch.zeros(4, dtype=torch.int32, device=dev)   # gcn_scaler (16 bytes)
-        self.scaler.view(torch.float32)[0] = loss_scale if prec != G.GCN_F32 else 1.0
+        self.scaler.view(torch.float32)[0] = loss_scale if level in ("O1", "O2") else 1.0
         self.overflow = torch.zeros(1, dtype=torch.int32, device=dev)
         self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
         self.n_correct = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -181,16 +236,19 @@ class GCN2:
         self.Z2 = torch.empty((n, self.ld_c), dtype=self.dt, device=dev)
         self.SG2 = torch.empty((n, self.ld_c), dtype=self.dt, device=dev)   # S2, later G_S2
         self.dZ2 = torch.empty((n, self.ld_c), dtype=self.dt, device=dev)
+        if level == "O1":     # the loss's fp32 copies of the logits and of their gradient
+            self.Z2f = torch.empty((n, self.ld_c), dtype=torch.float32, device=dev)
+            self.dZ2f = torch.empty((n, self.ld_c), dtype=torch.float32, device=dev)
         # layers
         self.L1 = G.GcnLayer(self.f_in, self.f_h, self.ld_x, self.ld_h, G.GCN_ACT_RELU, self.p, 0, 0)
         self.L2 = G.GcnLayer(self.f_h, self.C, self.ld_h, self.ld_c, G.GCN_ACT_NONE, 0.0, 1, 0)
-        ws = max(G.gcn_layer_workspace_size(graph.adj, self.L1, prec),
-                 G.gcn_layer_workspace_size(graph.adj, self.L2, prec),
+        ws = max(G.gcn_layer_workspace_size(self.adj, self.L1, prec),
+                 G.gcn_layer_workspace_size(self.adj, self.L2, prec),
                  G.gcn_loss_workspace_size(n, self.C),
                  G.gcn_transform_workspace_size(n, self.f_in, self.f_h, prec),
                  G.gcn_transform_workspace_size(n, self.f_h, self.C, prec),
-                 G.gcn_aggregate_workspace_size(graph.adj, self.f_h, prec),
-                 G.gcn_aggregate_workspace_size(graph.adj, self.C, prec))
+                 G.gcn_aggregate_workspace_size(self.adj, self.f_h, prec),
+                 G.gcn_aggregate_workspace_size(self.adj, self.C, prec))
         self.ws = torch.empty(ws // 4 + 64, dtype=torch.float32, device=dev)
         self.adam_c = self.adam.c()
 
@@ -216,7 +274,9 @@ class GCN2:
         aggregation call is bracketed by the timer (the transform by
         ``gemm_timer`` if given); the arithmetic is the same as
         gcn_layer_fwd."""
-        a = self.g.adj
+        a = self.adj
+        if self.level == "O1":
+            self.cast_inputs(stream)
         if agg_timer is None:
             G.gcn_layer_fwd(a, self.L1, self.prec, training, self.X, self.W1w(), self.b1m(), self.seed, epoch,
                             self.SG1, self.H1, self.overflow, self.ws, stream)
@@ -232,16 +292,39 @@ class GCN2:
                 G.gcn_aggregate(a, L.f_out, self.prec, S, L.ld_out, b, L.act, L.dropout_p, training, self.seed,
                                 L.layer_id, epoch, out, L.ld_out, self.overflow, self.ws, stream)
 
+    def cast_inputs(self, stream=None):
+        """O1: the 16-bit copies of X and A_hat that this forward pass's
+        GEMM-class operations read."""
+        G.gcn_cast(self.n, self.f_in, G.GCN_F32, self.X32, self.ld_x, self.prec, self.X, self.ld_x,
+                   self.overflow, stream)
+        g = self.g
+        if g.adj.format == G.GCN_DENSE:
+            G.gcn_cast(self.n, self.n, G.GCN_F32, g.dense, g.ld_dense, self.prec, self.A16, g.ld_dense,
+                       self.overflow, stream)
+        elif self.A16 is not None:
+            G.gcn_cast(1, g.nnz, G.GCN_F32, g.values, 0, self.prec, self.A16, 0, self.overflow, stream)
+
     def loss_and_backward(self, stream=None):
-        a = self.g.adj
-        G.gcn_loss(self.n, self.C, self.ld_c, self.prec, self.Z2, self.labels, self.mask, self.n_mask,
-                   self.scale_ptr(), self.loss, self.dZ2, self.n_correct, self.overflow, self.ws, stream)
+        a = self.adj
+        if self.level == "O1":     # the loss is on the fp32 list
+            G.gcn_cast(self.n, self.C, self.prec, self.Z2, self.ld_c, G.GCN_F32, self.Z2f, self.ld_c, None, stream)
+            G.gcn_loss(self.n, self.C, self.ld_c, G.GCN_F32, self.Z2f, self.labels, self.mask, self.n_mask,
+                       self.scale_ptr(), self.loss, self.dZ2f, self.n_correct, self.overflow, self.ws, stream)
+            G.gcn_cast(self.n, self.C, G.GCN_F32, self.dZ2f, self.ld_c, self.prec, self.dZ2, self.ld_c,
+                       self.overflow, stream)
+        else:
+            G.gcn_loss(self.n, self.C, self.ld_c, self.prec, self.Z2, self.labels, self.mask, self.n_mask,
+                       self.scale_ptr(), self.loss, self.dZ2, self.n_correct, self.overflow, self.ws, stream)
         G.gcn_layer_bwd(a, self.L2, self.prec, self.H1, self.W2w(), self.dZ2, G.GCN_ACT_RELU, self.p,
                         self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream)
         G.gcn_layer_bwd(a, self.L1, self.prec, self.X, self.W1w(), self.dZ1, G.GCN_ACT_NONE, 0.0,
                         self.dW1(), self.db1(), None, self.SG1, self.overflow, self.ws, stream)
 
     def optimizer_step(self, stream=None):
+        if self.level == "O3":
+            G.gcn_optimizer_step_half(self.P, self.working, self.grad, self.m, self.v, self.master, self.prec,
+                                      self.adam_c, self.scaler, self.overflow, stream)
+            return
         G.gcn_optimizer_step(self.P, self.master, self.grad, self.m, self.v, self.working, self.prec,
                              self.adam_c, self.scaler, self.overflow, stream)
 

@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert G.gcn_abi_version() == 3
+    assert G.gcn_abi_version() == 4
     assert G.gcn_status_string(0) == "GCN_OK"
     for s in range(1, 9):
         assert G.gcn_status_string(s).startswith("GCN_ERR_")
@@ -129,3 +129,21 @@ def test_loss_and_optimizer_validation_codes():
     bad = G.GcnAdamConfig(0.01, 1.0, 0.999, 1e-8, 0.5, 2.0, 2000, 1.0, 2.0**24)
     assert lib.gcn_optimizer_step(10, 0x1000, 0x2000, 0x3000, 0x4000, None, 1, ctypes.byref(bad),
                                   0x5000, 0x6000, None) == 1
+
+
+def test_cast_and_half_optimizer_validation_codes():
+    lib = G.lib()
+    f = lib.gcn_cast
+    assert f(0, 8, 0, 0x1000, 8, 1, 0x2000, 8, None, None) == 2              # rows <= 0
+    assert f(2, 9, 0, 0x1000, 8, 1, 0x2000, 16, None, None) == 2             # ld_src < cols
+    assert f(2, 8, 0, 0x1000, 12, 1, 0x2000, 16, None, None) == 3            # ld % 8 with rows > 1
+    assert f(1, 8, 0, 0x1008, 0, 1, 0x2000, 0, None, None) == 3              # misaligned
+    assert f(1, 8, 3, 0x1000, 0, 1, 0x2000, 0, None, None) == 1              # bad precision
+    assert f(1, 8, 0, None, 0, 1, 0x2000, 0, None, None) == 1                # NULL
+    cfg = G.GcnAdamConfig(0.01, 0.9, 0.999, 1e-8, 0.5, 2.0, 2000, 1.0, 2.0**24)
+    h = lib.gcn_optimizer_step_half
+    assert h(0, 0x1000, 0x2000, 0x3000, 0x4000, None, 1, ctypes.byref(cfg), 0x5000, 0x6000, None) == 2
+    assert h(10, 0x1000, 0x2000, 0x3000, 0x4000, None, 0, ctypes.byref(cfg), 0x5000, 0x6000, None) == 1   # fp32
+    assert h(10, 0x1000, 0x2000, 0x3000, None, None, 1, ctypes.byref(cfg), 0x5000, 0x6000, None) == 1
+    bad = G.GcnAdamConfig(0.0, 0.9, 0.999, 1e-8, 0.5, 2.0, 2000, 1.0, 2.0**24)
+    assert h(10, 0x1000, 0x2000, 0x3000, 0x4000, None, 1, ctypes.byref(bad), 0x5000, 0x6000, None) == 1
