@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -94,7 +95,7 @@ def spmm_bytes(n, nnz, F, s, s_p):
     return (n + 1) * s_p + nnz * (4 + s) + 2 * s * n * F
 
 
-def run_gpu(wl, prec, steps, warmup, dense=True):
+def run_gpu(wl, prec, steps, warmup, dense=True, level=None):
     import torch
     from paper_2010_12635_amd import gcn as G
     from paper_2010_12635_amd.model import DeviceGraph, GCN2
@@ -104,11 +105,15 @@ def run_gpu(wl, prec, steps, warmup, dense=True):
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_allocated()
-    dg = DeviceGraph(wl["n"], wl["src"], wl["dst"], prec=prec, dense=dense,
-                     index=G.GCN_I64 if spec.index64 else G.GCN_I32)
+    # O1 keeps A_hat as an fp32 input (row-major when dense) and casts it
+    # for every forward pass
+    gprec = G.GCN_F32 if level == "O1" else prec
+    dg = DeviceGraph(wl["n"], wl["src"], wl["dst"], prec=gprec, dense=dense,
+                     index=G.GCN_I64 if spec.index64 else G.GCN_I32, tiled=False if level == "O1" else None)
     scale0 = spec.loss_scale0 if prec != G.GCN_F32 else 1.0
     m = GCN2(dg, wl["X"], wl["labels"], wl["mask"], wl["W1"], wl["W2"], wl["b1"], wl["b2"], prec=prec,
-             dropout=0.0 if spec.dropout is None else spec.dropout, seed=wl["dropout_seed"], loss_scale=scale0)
+             dropout=0.0 if spec.dropout is None else spec.dropout, seed=wl["dropout_seed"], loss_scale=scale0,
+             level=level)
     timer = EventTimer()
     gtimer = EventTimer()
     for ep in range(warmup):
@@ -442,6 +447,8 @@ def main():
     ap.add_argument("--prec", default="f16", choices=sorted(PRECS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-fp32", action="store_true", help="skip the fp32-mode run")
+    ap.add_argument("--no-levels", dest="levels", action="store_false",
+                    help="skip the O0-O3 comparison on the main workload")
     ap.add_argument("--gae-epochs", type=int, default=100,
                     help="epochs of the link-prediction workload (0 skips it)")
     ap.add_argument("--no-largest", dest="largest", action="store_false",
@@ -466,15 +473,15 @@ def main():
     if args.summarize_stats:
         d, out, title = args.summarize_stats
         cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_default -o run -- "
-               "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest")
+               "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest --no-levels --gae-epochs 0")
         summarize_stats(d, out, cmd, title)
         return
 
     if args.summarize_counters:
         cmd = ("rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --gae-epochs 0 --copy-calibration 256\n"
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --copy-calibration 256\n"
                "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --gae-epochs 0 --copy-calibration 256")
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --copy-calibration 256")
         print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, cmd)))
         return
 
@@ -540,6 +547,26 @@ def main():
                     algorithmic_bytes_per_launch_avg=int(per_epoch_bytes / 2))
 
     gemm = gemm_object(r, prec, r["f_in"], r["f_h"], r["C"])
+
+    levels = None
+    if args.levels and prec != 0:
+        # the optimisation levels of the paper on the same workload and epochs:
+        # throughput, peak device memory and where training ends up
+        levels = {}
+        for lv in ("O0", "O1", "O2", "O3"):
+            if lv == "O2":
+                rr = r
+            elif lv == "O0" and r32 is not None:
+                rr = r32
+            else:
+                log(f"[bench] level {lv}")
+                rr = run_gpu(wl, 0 if lv == "O0" else prec, args.steps, args.warmup, dense=spec.dense_adj, level=lv)
+            levels[lv] = dict(epochs_per_s=round(args.steps / (rr["gpu_ms"] * 1e-3), 2),
+                              peak_mem_bytes=rr["peak_bytes"],
+                              final_loss=rr["loss"] if math.isfinite(rr["loss"]) else str(rr["loss"]),
+                              train_acc=round(rr["n_correct"] / max(1, rr["n_mask"]), 4),
+                              loss_scale=rr["scaler"]["scale"], nonfinite_steps=rr["scaler"]["skipped"])
+        log(f"[bench] levels: {levels}")
 
     spmm = None
     if args.spmm_workload != "none" and args.spmm_steps > 0:
@@ -639,6 +666,7 @@ def main():
         "loss_scale": r["scaler"],
         "roofline": roofline,
         "gemm": gemm,
+        "levels": levels,
         "spmm": spmm,
         "gae": gae,
         "largest_graph": largest,
