@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 4
+#define GCN_ABI_VERSION 5
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -110,7 +110,11 @@ typedef struct gcn_adj {
 } gcn_adj;
 
 /* One layer: H (n x f_in, ld_in) -> H_out (n x f_out, ld_out); W is
- * f_in x f_out with leading dimension ld_out; bias has f_out entries. */
+ * f_in x f_out with leading dimension ld_out; bias has f_out entries.
+ * identity_input != 0 declares H = I (the featureless input of the paper's
+ * run-time experiments, Section "Run-Time and Memory Usage Analysis"):
+ * f_in must equal n, H is not read (may be NULL), H W = W exactly, and the
+ * calls below skip the products with I. */
 typedef struct gcn_layer {
   int64_t f_in;
   int64_t f_out;
@@ -119,7 +123,7 @@ typedef struct gcn_layer {
   int32_t act;           /* gcn_act applied after aggregation              */
   float dropout_p;       /* in [0, 1); only with GCN_ACT_RELU and training  */
   int32_t layer_id;      /* dropout stream id                               */
-  int32_t reserved0;
+  int32_t identity_input;/* 1: H is the n x n identity (f_in == n)         */
 } gcn_layer;
 
 /* Dynamic loss-scale state, device-resident (16 bytes). */
@@ -224,6 +228,8 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz,
  * S is caller scratch that the backward pass does not need.  workspace: at
  * least gcn_layer_workspace_size() bytes.  *overflow is set to 1 if any
  * stored element of H_out is not finite.
+ * With L->identity_input, S = W and the aggregation reads W in place (S is
+ * not written and may be NULL); GCN_ERR_SHAPE unless f_in == n.
  * ------------------------------------------------------------------------- */
 gcn_status gcn_layer_workspace_size(const gcn_adj* A, const gcn_layer* L, int32_t prec, size_t* bytes);
 gcn_status gcn_layer_fwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, int32_t training,
@@ -265,6 +271,9 @@ gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* 
  * The ReLU derivative at 0 is 0.  *overflow is set to 1 if any stored
  * element of GS, dW, dbias or dZ_below is not finite.  dW and dbias are
  * summed in a fixed order (run-to-run deterministic).
+ * With L->identity_input, dW = I^T G_S = G_S widened to fp32 (exactly what
+ * the product with I gives); dZ_below must be NULL (GCN_ERR_INVALID_ARG
+ * otherwise: there is nothing below an input layer).
  * ------------------------------------------------------------------------- */
 gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec,
                          const void* H, const void* W, const void* dZ,

@@ -100,15 +100,16 @@ struct LayerPlan {
 LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
   LayerPlan p;
   const int64_t n = A->n;
-  p.s_split = gemm_choose_splits(prec, n, L->f_out, L->f_in);
-  p.dh_split = gemm_choose_splits(prec, n, L->f_in, L->f_out);
-  p.dw_split = wgrad_splits(prec, n, L->f_in, L->f_out);
+  const bool ident = L->identity_input != 0;    // no product with H = I
+  p.s_split = ident ? 1 : gemm_choose_splits(prec, n, L->f_out, L->f_in);
+  p.dh_split = ident ? 1 : gemm_choose_splits(prec, n, L->f_in, L->f_out);
+  p.dw_split = ident ? 0 : wgrad_splits(prec, n, L->f_in, L->f_out);
   p.agg_split = 1;
   int64_t f = 0;
   auto upd = [&](int64_t x) { if (x > f) f = x; };
   if (p.s_split > 1) upd(p.s_split * n * L->f_out);
   if (p.dh_split > 1) upd(p.dh_split * n * L->f_in);
-  upd(p.dw_split * L->f_in * L->f_out);
+  upd((int64_t)p.dw_split * L->f_in * L->f_out);
   int64_t cs = 0;
   if (A->format != GCN_CSR) {
     upd((int64_t)(dense_agg_workspace_bytes(prec, n, L->f_out) / sizeof(float)) + 1);
@@ -330,20 +331,27 @@ gcn_status gcn_layer_fwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, int
   if (st != GCN_OK) return st;
   st = check_layer(L);
   if (st != GCN_OK) return st;
-  if (!H || !W || !S || !H_out) return GCN_ERR_INVALID_ARG;
-  if (!aligned16(H) || !aligned16(W) || !aligned16(S) || !aligned16(H_out)) return GCN_ERR_ALIGNMENT;
+  const bool ident = L->identity_input != 0;
+  if (ident && L->f_in != A->n) return GCN_ERR_SHAPE;
+  if ((!ident && (!H || !S)) || !W || !H_out) return GCN_ERR_INVALID_ARG;
+  if ((H && !aligned16(H)) || !aligned16(W) || (S && !aligned16(S)) || !aligned16(H_out)) return GCN_ERR_ALIGNMENT;
   const LayerPlan plan = plan_layer(A, L, prec);
   if (!workspace || workspace_bytes < plan_bytes(plan)) return GCN_ERR_WORKSPACE;
   if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
   float* ws = static_cast<float*>(workspace);
   const int64_t n = A->n;
 
-  Epilogue es = base_epi(S, L->ld_out, n, L->f_out, EPI_STORE, overflow);
-  GCN_HIP(row_product(prec, H, L->ld_in, W, L->ld_out, false, n, L->f_out, L->f_in, plan.s_split, ws, es, s));
+  // S = H W; with H = I, S is W itself (n x f_out, ld_out)
+  const void* Sx = W;
+  if (!ident) {
+    Epilogue es = base_epi(S, L->ld_out, n, L->f_out, EPI_STORE, overflow);
+    GCN_HIP(row_product(prec, H, L->ld_in, W, L->ld_out, false, n, L->f_out, L->f_in, plan.s_split, ws, es, s));
+    Sx = S;
+  }
 
   Epilogue ea = agg_epi(H_out, L->ld_out, n, L->f_out, bias, L->act, L->dropout_p, training, seed, L->layer_id,
                         epoch, overflow);
-  GCN_HIP(aggregate(A, prec, S, L->ld_out, L->f_out, ea, ws, nullptr, s));
+  GCN_HIP(aggregate(A, prec, Sx, L->ld_out, L->f_out, ea, ws, nullptr, s));
   return finish(hipSuccess, s);
 }
 
@@ -413,10 +421,13 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
   if (st != GCN_OK) return st;
   st = check_layer(L);
   if (st != GCN_OK) return st;
-  if (!H || !W || !dZ || !dW || !GS) return GCN_ERR_INVALID_ARG;
+  const bool ident = L->identity_input != 0;
+  if (ident && L->f_in != A->n) return GCN_ERR_SHAPE;
+  if (ident && dZ_below) return GCN_ERR_INVALID_ARG;
+  if ((!ident && !H) || !W || !dZ || !dW || !GS) return GCN_ERR_INVALID_ARG;
   if (act_below != GCN_ACT_NONE && act_below != GCN_ACT_RELU) return GCN_ERR_INVALID_ARG;
   if (!(p_below >= 0.f && p_below < 1.f)) return GCN_ERR_INVALID_ARG;
-  if (!aligned16(H) || !aligned16(W) || !aligned16(dZ) || !aligned16(dW) || !aligned16(GS) ||
+  if ((H && !aligned16(H)) || !aligned16(W) || !aligned16(dZ) || !aligned16(dW) || !aligned16(GS) ||
       (dZ_below && !aligned16(dZ_below)) || (dbias && !aligned16(dbias)))
     return GCN_ERR_ALIGNMENT;
   const LayerPlan plan = plan_layer(A, L, prec);
@@ -442,6 +453,12 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
       eb.cols = L->ld_out;
       jb = make_job(cs, nb, 1, L->ld_out, eb);
     }
+  }
+  if (ident) {
+    // dW = I^T G_S = G_S: widened to fp32, padding columns zeroed
+    GCN_HIP(cast_launch(prec, 0, n, L->f_out, GS, L->ld_out, dW, L->ld_out, overflow, s, L->ld_out));
+    if (dbias) GCN_HIP(reduce_partials2(prec, jb, nullptr, s));
+    return finish(hipSuccess, s);
   }
   // dW = H^T G_S (fp32, split over vertices), then one launch reduces the dW
   // spans and the dbias partials, each in a fixed order

@@ -308,11 +308,162 @@ __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wide features (F >= 128, the large model sizes of the paper's Table 1):
+// 2 n^2 F flops against s n^2 bytes of A_hat put the product far above the
+// ridge point, so this kernel is built around the matrix cores.
+//  * A workgroup of 4 waves owns a 256 x 256 output tile, each wave a
+//    128 x 128 quarter (8 x 8 MFMA 16x16 tiles, 256 fp32 accumulators per
+//    lane, one wave per SIMD).
+//  * Both operands come straight from global memory in MFMA operand order
+//    (tiled A_hat, tiled X^T): a fragment is one contiguous 1 KiB, 16 per
+//    k chunk per wave, with MM_DEPTH - 1 chunks in flight.  The two waves
+//    that share the rows (or the columns) of the tile read the same lines.
+//  * Tiles are dealt out XCD by XCD: workgroup b runs on XCD b % 8, and each
+//    XCD takes a contiguous range of tiles in row-major order, so the column
+//    tiles of a row block run together and share A_hat in that XCD's L2.
+//  * The epilogue stages each 16-row strip of the wave's quarter through
+//    LDS and stores rows as 16-byte vectors through the fused epilogue.
+// ---------------------------------------------------------------------------
+constexpr int MM_LDR = 128 + 4;   // LDS stride (floats) of a staged strip
+
+struct MmParams {
+  const void* A;      // tiled A_hat
+  const void* Xt;     // tiled X^T
+  int64_t n, F, nc;   // vertices, features, k chunks
+  int64_t rblocks;    // 64-row blocks of A_hat
+  int64_t fblocks;    // 64-row blocks of X^T
+  int64_t tiles, cb, per_xcd;
+  Epilogue epi;
+};
+
+// Rows row0 .. row0 + 15, columns col0 .. col0 + W - 1 of the output from a
+// staged strip (16 x W fp32, stride MM_LDR), through the fused epilogue.
+template <typename T, int W>
+__device__ __forceinline__ void mm_store_strip(const MmParams& p, const float* st, int lane, int64_t row0, int64_t col0) {
+  constexpr int OV = Vec<T>::N;
+  constexpr int VPR = W / OV;                      // vectors per strip row
+  for (int k = 0; k < 16 * VPR / 64; ++k) {
+    const int idx = k * 64 + lane;
+    const int r = idx / VPR, cv = idx % VPR;
+    const int64_t row = row0 + r, col = col0 + cv * OV;
+    if (row >= p.n || col >= p.F) continue;
+    float v[OV];
+#pragma unroll
+    for (int e = 0; e < OV; ++e) v[e] = st[r * MM_LDR + cv * OV + e];
+    epi_store_vec<T>(p.epi, row, col, v);
+  }
+}
+
+// A wave owns WR x WC 64 x 64 blocks of the output (WR, WC in {1, 2}); the
+// workgroup's 2 x 2 waves own (128 WR) x (128 WC).
+template <typename T, int WR, int WC, int DEPTH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void dense_mm_kernel(MmParams p) {
+  constexpr int VE = Vec<T>::N, KC = 4 * VE, PIECE = 16 * KC;
+  constexpr int TM = 4 * WR, TN = 4 * WC;          // 16 x 16 MFMA tiles per wave
+  __shared__ float stage[4][16 * MM_LDR];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t b = blockIdx.x;
+  const int64_t t = (b & 7) * p.per_xcd + (b >> 3);
+  if (t >= p.tiles) return;
+  const int64_t tr = t / p.cb, tc = t - (t / p.cb) * p.cb;
+  const int64_t rb0 = (tr * 2 + (wave >> 1)) * WR;   // this wave's first 64-row block
+  const int64_t fb0 = (tc * 2 + (wave & 1)) * WC;    // and first 64-column block
+  const int64_t nc = p.nc;
+  const int64_t blk = nc * 4 * PIECE;                 // elements of one 64-row block
+  const T* __restrict__ A = reinterpret_cast<const T*>(p.A);
+  const T* __restrict__ Xt = reinterpret_cast<const T*>(p.Xt);
+  // blocks past the padded extent read the last one (never stored)
+  const T* abase[WR];
+  const T* bbase[WC];
+#pragma unroll
+  for (int i = 0; i < WR; ++i) abase[i] = A + min(rb0 + i, p.rblocks - 1) * blk + lane * VE;
+#pragma unroll
+  for (int i = 0; i < WC; ++i) bbase[i] = Xt + min(fb0 + i, p.fblocks - 1) * blk + lane * VE;
+
+  f32x4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  struct Fr { uint4 a[TM]; uint4 b[TN]; };
+  auto load = [&](Fr& f, int64_t c) {
+    c = c < nc ? c : nc - 1;                      // past the end: in bounds, unused
+    const int64_t off = c * 4 * PIECE;
+#pragma unroll
+    for (int i = 0; i < WR; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) f.a[i * 4 + q] = ldg16(abase[i] + off + q * PIECE);
+#pragma unroll
+    for (int i = 0; i < WC; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) f.b[i * 4 + q] = ldg16(bbase[i] + off + q * PIECE);
+  };
+  auto compute = [&](const Fr& f) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = DaMfma<T>::run(f.a[i], f.b[j], acc[i][j]);
+  };
+#define MM_FENCE() __builtin_amdgcn_sched_barrier(0)
+  // The chunks that do not fill a whole trip of the unrolled loop are done
+  // first, so that nothing follows the loop: with a compute after it the
+  // register allocator rotates the accumulators on every trip.
+  if (DEPTH == 2) {
+    Fr f0, f1;
+    int64_t c = 0;
+    if (nc & 1) { load(f0, 0); compute(f0); c = 1; }
+    load(f0, c);
+    for (; c + 2 <= nc; c += 2) {
+      load(f1, c + 1); MM_FENCE(); compute(f0); MM_FENCE();
+      load(f0, c + 2); MM_FENCE(); compute(f1); MM_FENCE();
+    }
+  } else {
+    Fr f0, f1, f2;
+    int64_t c = 0;
+    for (; c < nc % 3; ++c) { load(f0, c); compute(f0); }
+    load(f0, c);
+    load(f1, c + 1);
+    for (; c + 3 <= nc; c += 3) {
+      load(f2, c + 2); MM_FENCE(); compute(f0); MM_FENCE();
+      load(f0, c + 3); MM_FENCE(); compute(f1); MM_FENCE();
+      load(f1, c + 4); MM_FENCE(); compute(f2); MM_FENCE();
+    }
+  }
+#undef MM_FENCE
+
+  // epilogue: one 16-row strip of the wave's block at a time (the strip
+  // index is spelled out so that every accumulator index is static)
+  float* st = stage[wave];
+#define MM_STRIP(S)                                                                             \
+  if ((S) < TM) {                                                                               \
+    __syncthreads();                                                                            \
+    _Pragma("unroll") for (int j = 0; j < TN; ++j)                                              \
+      _Pragma("unroll") for (int v = 0; v < 4; ++v)                                             \
+        st[((lane >> 4) * 4 + v) * MM_LDR + j * 16 + (lane & 15)] = acc[(S) < TM ? (S) : 0][j][v]; \
+    __syncthreads();                                                                            \
+    mm_store_strip<T, 16 * TN>(p, st, lane, (rb0 + (S) / 4) * 64 + ((S) % 4) * 16, fb0 * 64);   \
+  }
+  MM_STRIP(0) MM_STRIP(1) MM_STRIP(2) MM_STRIP(3) MM_STRIP(4) MM_STRIP(5) MM_STRIP(6) MM_STRIP(7)
+#undef MM_STRIP
+}
+
 int64_t xt_elems(int prec, int64_t n, int64_t F) {
   const int64_t kc = prec == 0 ? 16 : 32;
   const int64_t nc = (n + kc - 1) / kc;
   return ((F + 63) / 64) * 64 * nc * kc;
 }
+
+#ifndef MM_MIN_F
+#define MM_MIN_F 192
+#endif
+// The wide-feature kernel takes over from F >= MM_MIN_F (tiled A_hat):
+// 128 x 64 per wave up to F = 384, 128 x 128 above (measured on MI355X at
+// n = 32768: F = 256 0.72 ms against 0.92 ms, F = 2048 3.3 ms against
+// 4.8 ms; the streaming kernel takes 0.77 ms at F = 128, 1.5 ms at 256).
+bool use_dense_mm(int64_t n, int64_t F) { return F >= MM_MIN_F && n >= 256; }
 
 template <typename T>
 hipError_t launch_t(const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx, int64_t F,
@@ -326,6 +477,22 @@ hipError_t launch_t(const void* A, int64_t lda, bool tiled, int64_t n, const voi
                      colsum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (tiled && use_dense_mm(n, F)) {
+    MmParams q;
+    q.A = A; q.Xt = Xt; q.n = n; q.F = F; q.nc = nc;
+    q.rblocks = (n + 63) / 64;
+    q.fblocks = fblocks;
+    const int WC = F > 384 ? 2 : 1;
+    const int64_t rt = (n + 255) / 256;
+    q.cb = (F + 128 * WC - 1) / (128 * WC);
+    q.tiles = rt * q.cb;
+    q.per_xcd = (q.tiles + 7) / 8;
+    q.epi = epi;
+    const dim3 g((unsigned)(8 * q.per_xcd));
+    if (WC == 2) hipLaunchKernelGGL((dense_mm_kernel<T, 2, 2, 2>), g, dim3(256), 0, s, q);
+    else hipLaunchKernelGGL((dense_mm_kernel<T, 2, 1, 2>), g, dim3(256), 0, s, q);
+    return hipGetLastError();
+  }
   DaParams p;
   p.A = A; p.lda = lda; p.Xt = Xt; p.ldt = 0; p.n = n; p.F = F; p.epi = epi;
   dim3 grid((unsigned)((n + DA_BM - 1) / DA_BM), (unsigned)fblocks);

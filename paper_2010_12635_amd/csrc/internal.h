@@ -134,8 +134,9 @@ hipError_t optimizer_launch(int64_t count, float* master, const float* grad, flo
                             int32_t* flag, hipStream_t s);
 hipError_t adam_half_launch(int64_t count, void* w, const float* grad, void* m, void* v, float* widened, int prec,
                             const AdamHyper& hp, ScalerState* state, int32_t* flag, hipStream_t s);
+// dst[:, :cols] = src converted; with zcols > cols, dst[:, cols:zcols] = 0.
 hipError_t cast_launch(int src_prec, int dst_prec, int64_t rows, int64_t cols, const void* src, int64_t lds,
-                       void* dst, int64_t ldd, int32_t* flag, hipStream_t s);
+                       void* dst, int64_t ldd, int32_t* flag, hipStream_t s, int64_t zcols = 0);
 
 // --------------------------------------------------------------- helpers ----
 hipError_t fill_zero(void* p, size_t bytes, hipStream_t s);

@@ -21,8 +21,8 @@ namespace {
 template <typename S, typename D>
 __global__ __launch_bounds__(256) void cast_kernel(int64_t rows, int64_t cols, const S* __restrict__ src,
                                                    int64_t lds, D* __restrict__ dst, int64_t ldd,
-                                                   int32_t* flag) {
-  const int64_t cpr = (cols + 7) >> 3;   // 8-element chunks per row
+                                                   int32_t* flag, int64_t zcols) {
+  const int64_t cpr = (zcols + 7) >> 3;  // 8-element chunks per row
   const int64_t total = rows * cpr;
   bool bad = false;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
@@ -31,7 +31,10 @@ __global__ __launch_bounds__(256) void cast_kernel(int64_t rows, int64_t cols, c
     const S* sp = src + r * lds + c0;
     D* dp = dst + r * ldd + c0;
     float x[8];
-    if (c0 + 8 <= cols) {
+    if (c0 >= cols) {                    // zero padding [cols, zcols)
+      const int m = (int)min<int64_t>(8, zcols - c0);
+      for (int k = 0; k < m; ++k) dp[k] = from_f32<D>(0.f);
+    } else if (c0 + 8 <= cols) {
       if constexpr (sizeof(S) == 4) {
         unpack<float>(ldg16(sp), x);
         unpack<float>(ldg16(sp + 4), x + 4);
@@ -57,6 +60,8 @@ __global__ __launch_bounds__(256) void cast_kernel(int64_t rows, int64_t cols, c
         dp[k] = y;
         bad |= !finite_f32(to_f32<D>(y));
       }
+      const int mz = (int)min<int64_t>(8, zcols - c0);
+      for (int k = m; k < mz; ++k) dp[k] = from_f32<D>(0.f);
     }
   }
   if (bad) raise_flag(flag);
@@ -64,23 +69,23 @@ __global__ __launch_bounds__(256) void cast_kernel(int64_t rows, int64_t cols, c
 
 template <typename S, typename D>
 hipError_t cast_t(int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst, int64_t ldd, int32_t* flag,
-                  hipStream_t s) {
-  const int64_t chunks = rows * ((cols + 7) >> 3);
+                  hipStream_t s, int64_t zcols) {
+  const int64_t chunks = rows * ((zcols + 7) >> 3);
   int64_t blocks = (chunks + 255) / 256;
   if (blocks > (int64_t)1 << 16) blocks = (int64_t)1 << 16;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL((cast_kernel<S, D>), dim3((unsigned)blocks), dim3(256), 0, s, rows, cols,
-                     reinterpret_cast<const S*>(src), lds, reinterpret_cast<D*>(dst), ldd, flag);
+                     reinterpret_cast<const S*>(src), lds, reinterpret_cast<D*>(dst), ldd, flag, zcols);
   return hipGetLastError();
 }
 
 template <typename S>
 hipError_t cast_from(int dst_prec, int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst, int64_t ldd,
-                     int32_t* flag, hipStream_t s) {
+                     int32_t* flag, hipStream_t s, int64_t zcols) {
   switch (dst_prec) {
-    case 0: return cast_t<S, float>(rows, cols, src, lds, dst, ldd, flag, s);
-    case 1: return cast_t<S, f16>(rows, cols, src, lds, dst, ldd, flag, s);
-    case 2: return cast_t<S, bf16>(rows, cols, src, lds, dst, ldd, flag, s);
+    case 0: return cast_t<S, float>(rows, cols, src, lds, dst, ldd, flag, s, zcols);
+    case 1: return cast_t<S, f16>(rows, cols, src, lds, dst, ldd, flag, s, zcols);
+    case 2: return cast_t<S, bf16>(rows, cols, src, lds, dst, ldd, flag, s, zcols);
   }
   return hipErrorInvalidValue;
 }
@@ -136,11 +141,12 @@ __global__ __launch_bounds__(256) void nonfinite_kernel(int64_t count, const flo
 }  // namespace
 
 hipError_t cast_launch(int src_prec, int dst_prec, int64_t rows, int64_t cols, const void* src, int64_t lds,
-                       void* dst, int64_t ldd, int32_t* flag, hipStream_t s) {
+                       void* dst, int64_t ldd, int32_t* flag, hipStream_t s, int64_t zcols) {
+  if (zcols < cols) zcols = cols;
   switch (src_prec) {
-    case 0: return cast_from<float>(dst_prec, rows, cols, src, lds, dst, ldd, flag, s);
-    case 1: return cast_from<f16>(dst_prec, rows, cols, src, lds, dst, ldd, flag, s);
-    case 2: return cast_from<bf16>(dst_prec, rows, cols, src, lds, dst, ldd, flag, s);
+    case 0: return cast_from<float>(dst_prec, rows, cols, src, lds, dst, ldd, flag, s, zcols);
+    case 1: return cast_from<f16>(dst_prec, rows, cols, src, lds, dst, ldd, flag, s, zcols);
+    case 2: return cast_from<bf16>(dst_prec, rows, cols, src, lds, dst, ldd, flag, s, zcols);
   }
   return hipErrorInvalidValue;
 }

@@ -77,7 +77,7 @@ class GcnLayer(ctypes.Structure):
         ("f_in", ctypes.c_int64), ("f_out", ctypes.c_int64),
         ("ld_in", ctypes.c_int64), ("ld_out", ctypes.c_int64),
         ("act", ctypes.c_int32), ("dropout_p", ctypes.c_float),
-        ("layer_id", ctypes.c_int32), ("reserved0", ctypes.c_int32),
+        ("layer_id", ctypes.c_int32), ("identity_input", ctypes.c_int32),
     ]
 
 

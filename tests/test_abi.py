@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert G.gcn_abi_version() == 4
+    assert G.gcn_abi_version() == 5
     assert G.gcn_status_string(0) == "GCN_OK"
     for s in range(1, 9):
         assert G.gcn_status_string(s).startswith("GCN_ERR_")

@@ -158,6 +158,10 @@ FWD_CASES = [
     (1500, 64, 32, G.GCN_ACT_NONE, 0.0, "tiled"),
     (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "tiled"),
     (777, 16, 130, G.GCN_ACT_RELU, 0.5, "tiled"),
+    # wide features: the MFMA-bound dense kernel (128 x 64 and 128 x 128 per wave)
+    (1300, 40, 200, G.GCN_ACT_RELU, 0.5, "tiled"),
+    (777, 24, 520, G.GCN_ACT_RELU, 0.3, "tiled"),
+    (2048, 16, 256, G.GCN_ACT_NONE, 0.0, "tiled"),
     (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "dense"),
     (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "dense"),
     (777, 16, 130, G.GCN_ACT_RELU, 0.5, "dense"),
@@ -211,6 +215,8 @@ BWD_CASES = [
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "dense"),
     (777, 40, 130, G.GCN_ACT_RELU, 0.5, "tiled"),   # three 64-feature groups, ragged tail
+    (1300, 200, 300, G.GCN_ACT_RELU, 0.5, "tiled"),  # wide G_S = A_hat dZ
+    (600, 64, 448, G.GCN_ACT_NONE, 0.0, "tiled"),
 ]
 
 
