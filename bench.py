@@ -142,7 +142,9 @@ def run_gpu(wl, prec, steps, warmup, dense=True, level=None):
     loss = float(m.loss.item())
     st = m.scaler_state()
     peak = torch.cuda.max_memory_allocated() - base
+    l1 = timer.pairs[0::2]     # brackets alternate: layer 1, layer 2 aggregation
     res = dict(prec=prec, wall_s=wall, gpu_ms=gpu_ms, host_submit_s=host_submit, agg_ms=agg_ms, agg_launches=len(timer.pairs),
+               agg_l1_ms=sum(a.elapsed_time(b) for a, b in l1), agg_l1_launches=len(l1),
                gemm_ms=gtimer.total_ms(), gemm_launches=len(gtimer.pairs),
                loss=loss, scaler=st, peak_bytes=int(peak), n=dg.n, nnz=dg.nnz,
                f_h=m.f_h, C=m.C, f_in=m.f_in, n_correct=int(m.n_correct.item()), n_mask=m.n_mask)
@@ -172,6 +174,49 @@ def gemm_object(r, prec, f_in, f_h, C):
                 achieved_tflops=round(tf, 2), peak_tflops=peak, mfma_frac=round(tf / peak, 4),
                 hbm_gbs=round(byts * calls / sec / 1e9, 1), ceiling_frac_at_hbm_peak=round(ceiling, 4),
                 launches=r["gemm_launches"], avg_launch_us=round(r["gemm_ms"] * 1e3 / max(1, r["gemm_launches"]), 2))
+
+
+TABLE1_SWEEPS = {
+    # (vertex counts, model sizes, levels): the paper's Table 1 ranges are
+    # n in {2048, 3072, ..., 32768}, model size 16 .. 2048, O0-O3
+    "default": ([4096, 16384, 32768], [16, 128, 512, 2048], ["O0", "O2"]),
+    "full": (list(range(2048, 32768 + 1, 1024)), [16, 32, 64, 128, 256, 512, 1024, 2048], ["O0", "O1", "O2", "O3"]),
+}
+
+
+def run_table1(which, epochs=5, warmup=2):
+    """The paper's run-time sweep (Table 1): featureless 2-layer GCN on a
+    Barabasi-Albert graph with dense A_hat, per (n, model size, level):
+    epochs/s, peak device memory and the layer-1 aggregation rate (the
+    2 n^2 d-flop product that dominates at large model sizes)."""
+    import gc
+    import torch
+    from paper_2010_12635_amd import inputs as I
+    ns, ds, levels = TABLE1_SWEEPS[which]
+    points = []
+    for n in ns:
+        for d in ds:
+            wl = I.table1_workload(n, d)
+            for lv in levels:
+                prec = 0 if lv == "O0" else PRECS["f16"]
+                try:
+                    r = run_gpu(wl, prec, epochs, warmup, dense=True, level=lv)
+                except torch.cuda.OutOfMemoryError:
+                    points.append(dict(n=n, model_size=d, level=lv, result="out of memory"))
+                    continue
+                calls = max(1, r["agg_l1_launches"])
+                agg_ms = r["agg_l1_ms"] / calls
+                tf = 2.0 * n * n * d / (agg_ms * 1e-3) / 1e12
+                peak = MFMA_PEAK_TFLOPS[prec]
+                points.append(dict(n=n, model_size=d, level=lv, epochs_per_s=round(epochs / (r["gpu_ms"] * 1e-3), 2),
+                                   peak_mem_bytes=r["peak_bytes"],
+                                   final_loss=r["loss"] if math.isfinite(r["loss"]) else str(r["loss"]),
+                                   agg_l1_ms=round(agg_ms, 4), agg_l1_tflops=round(tf, 1),
+                                   agg_l1_mfma_frac=round(tf / peak, 4)))
+                log(f"[bench] table1 n={n} d={d} {lv}: {points[-1]}")
+            del wl
+            gc.collect()
+    return points
 
 
 def run_gae(wl, prec, epochs, warmup, n_pairs=1 << 20):
@@ -447,6 +492,8 @@ def main():
     ap.add_argument("--prec", default="f16", choices=sorted(PRECS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-fp32", action="store_true", help="skip the fp32-mode run")
+    ap.add_argument("--table1", default="default", choices=sorted(TABLE1_SWEEPS) + ["none"],
+                    help="the model-size sweep of the paper's Table 1 (featureless input, dense A_hat)")
     ap.add_argument("--no-levels", dest="levels", action="store_false",
                     help="skip the O0-O3 comparison on the main workload")
     ap.add_argument("--gae-epochs", type=int, default=100,
@@ -473,15 +520,15 @@ def main():
     if args.summarize_stats:
         d, out, title = args.summarize_stats
         cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_default -o run -- "
-               "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest --no-levels --gae-epochs 0")
+               "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest --no-levels --gae-epochs 0 --table1 none")
         summarize_stats(d, out, cmd, title)
         return
 
     if args.summarize_counters:
         cmd = ("rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --copy-calibration 256\n"
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --table1 none --copy-calibration 256\n"
                "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --copy-calibration 256")
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --table1 none --copy-calibration 256")
         print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, cmd)))
         return
 
@@ -631,6 +678,25 @@ def main():
             torch.cuda.empty_cache()
             log(f"[bench] largest graph {key}: {largest[key]}")
 
+    table1 = None
+    if args.table1 != "none":
+        log(f"[bench] model-size sweep ({args.table1})")
+        pts = run_table1(args.table1)
+        big = [p for p in pts if "agg_l1_tflops" in p and p["level"] == "O2"]
+        top = max(big, key=lambda p: (p["n"], p["model_size"])) if big else None
+        top32 = next((p for p in pts if "agg_l1_tflops" in p and p["level"] == "O0" and top is not None
+                      and p["n"] == top["n"] and p["model_size"] == top["model_size"]), None)
+        table1 = dict(
+            workload="Barabasi-Albert (m = 8), featureless X = I, dense A_hat, 2-layer GCN n -> d -> 16, "
+                     "dropout 0.5, Adam lr 0.01; 2 warm-up + 5 timed epochs per point",
+            mfma=None if top is None else dict(
+                kernel="dense_mm_kernel: Z1 = A_hat W1 (layer-1 aggregation, 128 x 128 accumulator tile per wave)",
+                bound="mfma", n=top["n"], model_size=top["model_size"], achieved=top["agg_l1_tflops"],
+                peak=MFMA_PEAK_TFLOPS[1], unit="TFLOP/s", frac=top["agg_l1_mfma_frac"],
+                fp32=None if top32 is None else dict(achieved=top32["agg_l1_tflops"], peak=MFMA_PEAK_TFLOPS[0],
+                                                     frac=top32["agg_l1_mfma_frac"])),
+            points=pts)
+
     cpu = None
     if args.cpu_seconds > 0:
         log("[bench] cpu oracle baseline")
@@ -669,6 +735,7 @@ def main():
         "levels": levels,
         "spmm": spmm,
         "gae": gae,
+        "table1": table1,
         "largest_graph": largest,
         "cpu_baseline": cpu,
     }

@@ -355,6 +355,23 @@ def workload(spec: WorkloadSpec | str, seed: int = 0, *, n_override: int | None 
                 b2=np.zeros(spec.classes, np.float32), dropout_seed=dseed)
 
 
+def table1_workload(n: int, model_size: int, seed: int = 0, classes: int = 16, m: int = 8):
+    """One point of the paper's run-time sweep (Table 1): a Barabasi-Albert
+    graph of n vertices (m edges per new vertex), featureless input X = I
+    (returned as X = None), a 2-layer GCN n -> model_size -> classes,
+    uniform labels on every vertex, Glorot-uniform weights."""
+    ss = np.random.SeedSequence([seed, n, model_size])
+    g_rng, y_rng, w_rng, d_rng = [np.random.default_rng(s) for s in ss.spawn(4)]
+    src, dst = ba_graph(n, m, g_rng)
+    labels = uniform_labels(n, classes, y_rng)
+    spec = WorkloadSpec(f"table1_n{n}_d{model_size}", "ba", (n, m), n, model_size, classes, feat_kind="identity",
+                        epochs=5, dense_adj=True)
+    return dict(spec=spec, n=n, src=src, dst=dst, X=None, labels=labels, mask=np.ones(n, np.uint8),
+                W1=glorot_uniform(n, model_size, w_rng), W2=glorot_uniform(model_size, classes, w_rng),
+                b1=np.zeros(model_size, np.float32), b2=np.zeros(classes, np.float32),
+                dropout_seed=int(d_rng.integers(0, 2**63 - 1, dtype=np.int64)))
+
+
 def _shrunk(spec: WorkloadSpec, n: int) -> WorkloadSpec:
     from dataclasses import replace
     if spec.graph == "er":

@@ -179,7 +179,12 @@ class GCN2:
         # inputs (padding columns zero); a device tensor already in the
         # storage layout (n x round8(f_in), storage dtype) is used in place
         self.X32 = None
-        if level == "O1":     # fp32 input plus the 16-bit copy its GEMM reads
+        # X = None: the featureless input X = I (f_in = n, W1 is n x f_h)
+        self.featureless = X is None
+        if self.featureless:
+            assert self.f_in == n, "featureless input: W1 must have n rows"
+            self.X = None
+        elif level == "O1":     # fp32 input plus the 16-bit copy its GEMM reads
             self.X32 = torch.zeros((n, self.ld_x), dtype=torch.float32, device=dev)
             self.X32[:, : self.f_in] = torch.as_tensor(np.asarray(X, np.float32)).to(dev)
             self.X = torch.zeros((n, self.ld_x), dtype=self.dt, device=dev)
@@ -240,12 +245,13 @@ class GCN2:
             self.Z2f = torch.empty((n, self.ld_c), dtype=torch.float32, device=dev)
             self.dZ2f = torch.empty((n, self.ld_c), dtype=torch.float32, device=dev)
         # layers
-        self.L1 = G.GcnLayer(self.f_in, self.f_h, self.ld_x, self.ld_h, G.GCN_ACT_RELU, self.p, 0, 0)
+        self.L1 = G.GcnLayer(self.f_in, self.f_h, self.ld_x, self.ld_h, G.GCN_ACT_RELU, self.p, 0,
+                             1 if self.featureless else 0)
         self.L2 = G.GcnLayer(self.f_h, self.C, self.ld_h, self.ld_c, G.GCN_ACT_NONE, 0.0, 1, 0)
         ws = max(G.gcn_layer_workspace_size(self.adj, self.L1, prec),
                  G.gcn_layer_workspace_size(self.adj, self.L2, prec),
                  G.gcn_loss_workspace_size(n, self.C),
-                 G.gcn_transform_workspace_size(n, self.f_in, self.f_h, prec),
+                 0 if self.featureless else G.gcn_transform_workspace_size(n, self.f_in, self.f_h, prec),
                  G.gcn_transform_workspace_size(n, self.f_h, self.C, prec),
                  G.gcn_aggregate_workspace_size(self.adj, self.f_h, prec),
                  G.gcn_aggregate_workspace_size(self.adj, self.C, prec))
@@ -285,9 +291,12 @@ class GCN2:
             return
         for L, H, W, b, S, out in ((self.L1, self.X, self.W1w(), self.b1m(), self.SG1, self.H1),
                                    (self.L2, self.H1, self.W2w(), self.b2m(), self.SG2, self.Z2)):
-            with (gemm_timer() if gemm_timer is not None else _nullctx()):
-                G.gcn_transform(self.n, L.f_in, L.f_out, self.prec, H, L.ld_in, W, L.ld_out, S, L.ld_out,
-                                self.overflow, self.ws, stream)
+            if L.identity_input:      # S = I W = W
+                S = W
+            else:
+                with (gemm_timer() if gemm_timer is not None else _nullctx()):
+                    G.gcn_transform(self.n, L.f_in, L.f_out, self.prec, H, L.ld_in, W, L.ld_out, S, L.ld_out,
+                                    self.overflow, self.ws, stream)
             with agg_timer():
                 G.gcn_aggregate(a, L.f_out, self.prec, S, L.ld_out, b, L.act, L.dropout_p, training, self.seed,
                                 L.layer_id, epoch, out, L.ld_out, self.overflow, self.ws, stream)
@@ -295,8 +304,9 @@ class GCN2:
     def cast_inputs(self, stream=None):
         """O1: the 16-bit copies of X and A_hat that this forward pass's
         GEMM-class operations read."""
-        G.gcn_cast(self.n, self.f_in, G.GCN_F32, self.X32, self.ld_x, self.prec, self.X, self.ld_x,
-                   self.overflow, stream)
+        if self.X32 is not None:
+            G.gcn_cast(self.n, self.f_in, G.GCN_F32, self.X32, self.ld_x, self.prec, self.X, self.ld_x,
+                       self.overflow, stream)
         g = self.g
         if g.adj.format == G.GCN_DENSE:
             G.gcn_cast(self.n, self.n, G.GCN_F32, g.dense, g.ld_dense, self.prec, self.A16, g.ld_dense,
