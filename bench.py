@@ -181,6 +181,7 @@ TABLE1_SWEEPS = {
     # n in {2048, 3072, ..., 32768}, model size 16 .. 2048, O0-O3
     "default": ([4096, 16384, 32768], [16, 128, 512, 2048], ["O0", "O2"]),
     "full": (list(range(2048, 32768 + 1, 1024)), [16, 32, 64, 128, 256, 512, 1024, 2048], ["O0", "O1", "O2", "O3"]),
+    "top": ([32768], [2048], ["O2"]),
 }
 
 
