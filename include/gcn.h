@@ -398,11 +398,13 @@ gcn_status gcn_pair_loss(int64_t n, int64_t F, int64_t ld, int32_t prec, const v
 
 /* gcn_pair_backward: dZ = d(sum_k g_k s_k)/dZ: row r sums g_k Z[v_k] over
  * the pairs with u_k = r and g_k Z[u_k] over the pairs with v_k = r, in
- * increasing k (run-to-run deterministic); rows in no pair are 0.
- * dZ: n x F (ldz, prec; padding columns may be overwritten with 0).  Pairs with an id
- * outside [0, n) are skipped.  *overflow is set if a stored element is not
- * finite.  workspace: gcn_pair_backward_workspace_size() bytes. */
-gcn_status gcn_pair_backward_workspace_size(int64_t n, int64_t n_pairs, size_t* bytes);
+ * increasing k, rows that span several blocks of 256 pair endpoints being
+ * summed block by block in order (run-to-run deterministic); rows in no
+ * pair are 0.  dZ: n x F (ldz, prec; padding columns may be overwritten
+ * with 0).  Pairs with an id outside [0, n) are skipped.  n_pairs <= 2^30.
+ * *overflow is set if a stored element is not finite.  workspace:
+ * gcn_pair_backward_workspace_size(n, n_pairs, F) bytes. */
+gcn_status gcn_pair_backward_workspace_size(int64_t n, int64_t n_pairs, int64_t F, size_t* bytes);
 gcn_status gcn_pair_backward(int64_t n, int64_t F, int64_t ld, int32_t prec, const void* Z,
                              const int32_t* pair_u, const int32_t* pair_v, int64_t n_pairs,
                              const float* g, void* dZ, int64_t ldz, int32_t* overflow,

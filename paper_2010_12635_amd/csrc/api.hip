@@ -591,10 +591,10 @@ gcn_status gcn_pair_loss(int64_t n, int64_t F, int64_t ld, int32_t prec, const v
   return finish(hipSuccess, s);
 }
 
-gcn_status gcn_pair_backward_workspace_size(int64_t n, int64_t n_pairs, size_t* bytes) {
+gcn_status gcn_pair_backward_workspace_size(int64_t n, int64_t n_pairs, int64_t F, size_t* bytes) {
   if (!bytes) return GCN_ERR_INVALID_ARG;
-  if (n <= 0 || n_pairs < 0) return GCN_ERR_SHAPE;
-  *bytes = pair_backward_workspace_bytes(n, n_pairs);
+  if (n <= 0 || n_pairs < 0 || F <= 0) return GCN_ERR_SHAPE;
+  *bytes = pair_backward_workspace_bytes(n, n_pairs, F);
   return GCN_OK;
 }
 
@@ -604,12 +604,12 @@ gcn_status gcn_pair_backward(int64_t n, int64_t F, int64_t ld, int32_t prec, con
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
   if (n <= 0 || n > INT32_MAX || F <= 0 || ld < F || ldz < F || n_pairs < 0) return GCN_ERR_SHAPE;
-  if (n_pairs > INT32_MAX) return GCN_ERR_UNSUPPORTED;
+  if (n_pairs > INT32_MAX / 2) return GCN_ERR_UNSUPPORTED;
   if (ld % 8 || ldz % 8) return GCN_ERR_ALIGNMENT;
   if (F > 64 * (prec == GCN_F32 ? 4 : 8)) return GCN_ERR_UNSUPPORTED;
   if (!Z || !dZ || (n_pairs > 0 && (!pair_u || !pair_v || !g))) return GCN_ERR_INVALID_ARG;
   if (!aligned16(Z) || !aligned16(dZ)) return GCN_ERR_ALIGNMENT;
-  if (!workspace || workspace_bytes < pair_backward_workspace_bytes(n, n_pairs)) return GCN_ERR_WORKSPACE;
+  if (!workspace || workspace_bytes < pair_backward_workspace_bytes(n, n_pairs, F)) return GCN_ERR_WORKSPACE;
   if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
   GCN_HIP(pair_backward_launch(prec, n, F, ld, Z, pair_u, pair_v, n_pairs, g, dZ, ldz, overflow, workspace, s));
   return finish(hipSuccess, s);

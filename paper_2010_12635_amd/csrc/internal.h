@@ -157,7 +157,7 @@ size_t pair_loss_workspace_bytes(int64_t n_pairs);
 hipError_t pair_loss_launch(int prec, int64_t n, int64_t F, int64_t ld, const void* Z, const int32_t* pair_u,
                             const int32_t* pair_v, int64_t n_pos, int64_t n_neg, const float* loss_scale, float* loss,
                             float* scores, float* g, int32_t* flag, void* ws, hipStream_t s);
-size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs);
+size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs, int64_t F);
 hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, const void* Z, const int32_t* pair_u,
                                 const int32_t* pair_v, int64_t n_pairs, const float* g, void* dZ, int64_t ldz,
                                 int32_t* flag, void* ws, hipStream_t s);

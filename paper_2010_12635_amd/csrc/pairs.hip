@@ -9,10 +9,12 @@
 //    Z as 16-byte slices, reduces their inner product with shuffles, and
 //    takes the logistic loss and its gradient g_k in fp32.  Per-pair losses
 //    are summed per workgroup in a fixed order, then across workgroups.
-//  * pair backward: the pairs are bucketed by endpoint (count, scan,
-//    scatter, per-row sort by pair index), then a lane group per row sums
-//    g_k Z[other endpoint] in increasing k: dZ is run-to-run identical
-//    without floating-point atomics.
+//  * pair backward: the pair endpoints are sorted by vertex with a stable
+//    radix sort (so each row's entries stay in increasing k), then cut into
+//    equal segments of entries; a lane group per segment sums the rows
+//    inside it and a fix-up pass adds the partial sums of rows that cross
+//    segment ends, in segment order: dZ is run-to-run identical without
+//    floating-point atomics, and hub rows no longer serialise on one group.
 //  * pair_metrics_kernel: exact AUC and AP of held-out pairs by counting,
 //    for every positive, the scores below / equal / above it (O(P (P + N))
 //    comparisons through LDS tiles), then fixed-order sums.
@@ -167,90 +169,266 @@ hipError_t pair_loss_t(PairLossParams p, int lpr, hipStream_t s, int64_t* nb_out
   return hipGetLastError();
 }
 
-// ---- backward: pairs bucketed by endpoint
-__global__ void pair_count_kernel(int64_t n, int64_t total, const int32_t* __restrict__ pu, const int32_t* __restrict__ pv,
-                                  int32_t* __restrict__ cnt) {
-  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < total; k += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t u = pu[k], v = pv[k];
-    if (u < 0 || v < 0 || u >= n || v >= n) continue;
-    atomicAdd(&cnt[u], 1);
-    atomicAdd(&cnt[v], 1);
+// ---- backward: pair entries sorted by endpoint, then a balanced gather
+//
+// Entry i of the 2K entries is endpoint (i even ? u : v) of pair k = i / 2;
+// its key is that endpoint (n for a pair with an id outside [0, n)).  A
+// stable LSD radix sort by key (8-bit digits: per-tile digit histograms,
+// one exclusive scan, a stable scatter that ranks equal digits by ballots)
+// puts each row's entries together in increasing k without atomics.  The
+// sorted entries are cut into segments of SEG entries; a lane group per
+// segment sums the rows that lie inside it and leaves partial sums for the
+// rows that cross its ends, which a fix-up pass adds in segment order.
+constexpr int RS_BITS = 8, RS_DIGITS = 1 << RS_BITS;
+constexpr int RS_IPT = 8;                           // items per thread per tile
+constexpr int RS_TILE = 256 * RS_IPT;
+constexpr int SEG = 256;                            // sorted entries per gather segment
+
+__device__ __forceinline__ int32_t entry_key(int64_t n, const int32_t* __restrict__ pu, const int32_t* __restrict__ pv,
+                                             int64_t i) {
+  const int32_t u = pu[i >> 1], v = pv[i >> 1];
+  const bool ok = u >= 0 && v >= 0 && u < n && v < n;
+  return ok ? ((i & 1) ? v : u) : (int32_t)n;
+}
+
+// Digit histogram of one tile: hist[d * nblk + blockIdx.x] (digit-major).
+__global__ __launch_bounds__(256) void rs_hist_kernel(int64_t n, const int32_t* __restrict__ pu,
+                                                      const int32_t* __restrict__ pv, const int32_t* __restrict__ keys,
+                                                      int64_t total, int shift, int64_t nblk,
+                                                      int64_t* __restrict__ hist) {
+  __shared__ int cnt[RS_DIGITS];
+  cnt[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * RS_TILE;
+  for (int r = 0; r < RS_IPT; ++r) {
+    const int64_t i = base + r * 256 + threadIdx.x;
+    if (i < total) {
+      const int32_t k = keys ? keys[i] : entry_key(n, pu, pv, i);
+      atomicAdd(&cnt[(k >> shift) & (RS_DIGITS - 1)], 1);
+    }
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// Stable scatter of one tile: items are ranked round by round (256
+// consecutive items per round, thread order = item order); inside a wave
+// the lanes with the same digit are found with 8 ballots, across the four
+// waves through per-wave counts in LDS stamped with the round.
+__global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_t* __restrict__ pu,
+                                                         const int32_t* __restrict__ pv,
+                                                         const int32_t* __restrict__ kin, const int32_t* __restrict__ vin,
+                                                         int64_t total, int shift, int64_t nblk,
+                                                         const int64_t* __restrict__ off, int32_t* __restrict__ kout,
+                                                         int32_t* __restrict__ vout) {
+  __shared__ int cnt[4][RS_DIGITS];                 // (round << 16) | count
+  __shared__ int run[RS_DIGITS];
+  __shared__ int64_t dbase[RS_DIGITS];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  run[threadIdx.x] = 0;
+  dbase[threadIdx.x] = off[(int64_t)threadIdx.x * nblk + blockIdx.x];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) cnt[w][threadIdx.x] = -1;   // stamp -1: no round yet
+  __syncthreads();
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int64_t base = (int64_t)blockIdx.x * RS_TILE;
+  for (int r = 0; r < RS_IPT; ++r) {
+    const int64_t i = base + r * 256 + threadIdx.x;
+    const bool valid = i < total;
+    int32_t k = 0, val = 0;
+    if (valid) {
+      k = kin ? kin[i] : entry_key(n, pu, pv, i);
+      val = vin ? vin[i] : (int32_t)i;
+    }
+    const int d = (k >> shift) & (RS_DIGITS - 1);
+    uint64_t m = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < RS_BITS; ++bit) {
+      const uint64_t bb = __ballot((d >> bit) & 1);
+      m &= ((d >> bit) & 1) ? bb : ~bb;
+    }
+    const int rank = __popcll(m & lt);
+    if (valid && rank == 0) cnt[wave][d] = (r << 16) | __popcll(m);
+    __syncthreads();
+    if (valid) {
+      int before = 0;
+      for (int w = 0; w < wave; ++w) {
+        const int c = cnt[w][d];
+        if ((c >> 16) == r) before += c & 0xFFFF;
+      }
+      const int64_t pos = dbase[d] + run[d] + before + rank;
+      kout[pos] = k;
+      vout[pos] = val;
+    }
+    __syncthreads();
+    int add = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int c = cnt[w][threadIdx.x];
+      if ((c >> 16) == r) add += c & 0xFFFF;
+    }
+    run[threadIdx.x] += add;
+    __syncthreads();
   }
 }
 
-__global__ void pair_widen_kernel(int64_t n, const int32_t* __restrict__ in, int64_t* __restrict__ out) {
-  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r <= n; r += (int64_t)gridDim.x * blockDim.x)
-    out[r] = r < n ? (int64_t)in[r] : 0;
-}
-
-__global__ void pair_scatter_kernel(int64_t n, int64_t total, const int32_t* __restrict__ pu,
-                                    const int32_t* __restrict__ pv, const int64_t* __restrict__ off,
-                                    int32_t* __restrict__ cur, int32_t* __restrict__ entries) {
-  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < total; k += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t u = pu[k], v = pv[k];
-    if (u < 0 || v < 0 || u >= n || v >= n) continue;
-    entries[off[u] + atomicAdd(&cur[u], 1)] = (int32_t)k;
-    entries[off[v] + atomicAdd(&cur[v], 1)] = (int32_t)k;
+// Row offsets from sorted keys: off[r] = first position with key >= r,
+// r = 0 .. n (keys equal to n, the skipped pairs, lie past off[n]).
+__global__ void rs_bounds_kernel(int64_t n, const int32_t* __restrict__ keys, int64_t total,
+                                 int64_t* __restrict__ off) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j <= total; j += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t lo = j == 0 ? -1 : keys[j - 1];
+    const int64_t hi = j == total ? n : min<int64_t>(keys[j], n);
+    for (int64_t r = lo + 1; r <= hi; ++r) off[r] = j;
   }
 }
 
-// dZ[r] = sum over the (sorted) entries k of row r of g_k Z[other endpoint].
+__device__ __forceinline__ int64_t lower_row(const int64_t* __restrict__ off, int64_t n, int64_t x) {
+  int64_t lo = 0, hi = n;                           // first r in [0, n] with off[r] >= x
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (off[mid] < x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+struct SegParams {
+  int64_t n, F, ld;
+  const void* Z;
+  const int32_t* pu;
+  const int32_t* pv;
+  const float* g;
+  const int64_t* off;                               // [n + 1]
+  const int32_t* vals;                              // sorted entry ids
+  int64_t nseg;
+  float* head;                                      // [nseg][ldp]
+  float* tail;                                      // [nseg][ldp]
+  int32_t* tail_row;                                // [nseg]
+  int64_t ldp;
+  Epilogue ep;
+};
+
+// Sum of g_k Z[other endpoint] over sorted entries [e0, e1) into acc.
+template <typename T>
+__device__ __forceinline__ void seg_sum(const SegParams& p, int64_t e0, int64_t e1, int64_t col0, float* acc) {
+  constexpr int VE = Vec<T>::N, U = 4;
+  const T* __restrict__ Z = reinterpret_cast<const T*>(p.Z);
+  for (int64_t e = e0; e < e1; e += U) {
+    int32_t it[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) it[u] = p.vals[e + u < e1 ? e + u : e1 - 1];
+    int32_t other[U];
+    float w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t k = it[u] >> 1;
+      other[u] = (it[u] & 1) ? p.pu[k] : p.pv[k];
+      w[u] = e + u < e1 ? p.g[k] : 0.f;
+    }
+    uint4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = ldg16(Z + (int64_t)other[u] * p.ld + col0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float xv[VE];
+      unpack<T>(x[u], xv);
+#pragma unroll
+      for (int q = 0; q < VE; ++q) acc[q] = fmaf(w[u], xv[q], acc[q]);
+    }
+  }
+}
+
 template <typename T, int LPR>
-__global__ __launch_bounds__(256) void pair_gather_kernel(int64_t n, int64_t F, int64_t ld, const T* __restrict__ Z,
-                                                          const int32_t* __restrict__ pu, const int32_t* __restrict__ pv,
-                                                          const float* __restrict__ g, const int64_t* __restrict__ off,
-                                                          const int32_t* __restrict__ entries, Epilogue ep) {
+__global__ __launch_bounds__(256) void pair_segment_kernel(SegParams p) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int gi = lane / LPR, li = lane % LPR;
   const int64_t col0 = (int64_t)li * VE;
-  if (col0 >= ep.ldo) return;
-  const bool zero_slice = col0 >= F;   // padding columns [F, ldz): written 0
-  constexpr int U = 4;
-  for (int64_t r = ((int64_t)blockIdx.x * 4 + wave) * G + gi; r < n; r += (int64_t)gridDim.x * 4 * G) {
+  if (col0 >= p.ep.ldo) return;
+  const bool live = col0 < p.F;                     // padding slices only write zeros
+  const int64_t total = p.off[p.n];                 // entries of valid pairs
+  const int64_t nuse = total > 0 ? (total + SEG - 1) / SEG : 1;
+  for (int64_t sgi = ((int64_t)blockIdx.x * 4 + wave) * G + gi; sgi < p.nseg; sgi += (int64_t)gridDim.x * 4 * G) {
+    if (sgi >= nuse) {                              // past the valid entries
+      if (li == 0) p.tail_row[sgi] = -1;
+      continue;
+    }
+    // rows starting in [a, b) belong to this segment; the last one also
+    // takes the empty rows that start at the end
+    const int64_t a = sgi * SEG, b = min(a + SEG, total);
+    const int64_t r0 = lower_row(p.off, p.n, a);
+    const int64_t r1 = sgi == nuse - 1 ? p.n : lower_row(p.off, p.n, b);
     float acc[VE];
+    // head: the row that started before this segment
+    if (r0 > 0 && p.off[r0] > a && a < b) {
 #pragma unroll
-    for (int i = 0; i < VE; ++i) acc[i] = 0.f;
-    const int64_t beg = off[r], end = zero_slice ? off[r] : off[r + 1];
-    for (int64_t e = beg; e < end; e += U) {
-      int32_t k[U];
+      for (int q = 0; q < VE; ++q) acc[q] = 0.f;
+      if (live) seg_sum<T>(p, a, min(p.off[r0], b), col0, acc);
+      if (col0 < p.ldp) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) k[u] = entries[e + u < end ? e + u : end - 1];
-      int32_t other[U];
-      float w[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int32_t a = pu[k[u]], b = pv[k[u]];
-        other[u] = a == (int32_t)r ? b : a;
-        w[u] = e + u < end ? g[k[u]] : 0.f;
-      }
-      uint4 x[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) x[u] = ldg16(Z + (int64_t)other[u] * ld + col0);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (e + u >= end) break;
-        float xv[VE];
-        unpack<T>(x[u], xv);
-#pragma unroll
-        for (int i = 0; i < VE; ++i) acc[i] = fmaf(w[u], xv[i], acc[i]);
+        for (int q = 0; q < VE; ++q) p.head[sgi * p.ldp + col0 + q] = acc[q];
       }
     }
-    epi_store_vec<T>(ep, r, col0, acc);
+    int32_t trow = -1;
+    for (int64_t r = r0; r < r1; ++r) {
+      const int64_t rs = p.off[r], re = p.off[r + 1];
+#pragma unroll
+      for (int q = 0; q < VE; ++q) acc[q] = 0.f;
+      if (re <= b) {
+        if (live) seg_sum<T>(p, rs, re, col0, acc);
+        epi_store_vec<T>(p.ep, r, col0, acc);
+      } else {                                      // crosses the end: partial, fixed up later
+        if (live) seg_sum<T>(p, rs, b, col0, acc);
+        if (col0 < p.ldp) {
+#pragma unroll
+          for (int q = 0; q < VE; ++q) p.tail[sgi * p.ldp + col0 + q] = acc[q];
+        }
+        trow = (int32_t)r;
+      }
+    }
+    if (li == 0) p.tail_row[sgi] = trow;
+  }
+}
+
+// Rows that cross segment ends: the tail partial of the segment where the
+// row starts plus the head partials of the following segments, in order.
+template <typename T, int LPR>
+__global__ __launch_bounds__(256) void pair_fixup_kernel(SegParams p) {
+  constexpr int VE = Vec<T>::N;
+  constexpr int G = 64 / LPR;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int gi = lane / LPR, li = lane % LPR;
+  const int64_t col0 = (int64_t)li * VE;
+  if (col0 >= p.ep.ldo) return;
+  for (int64_t sgi = ((int64_t)blockIdx.x * 4 + wave) * G + gi; sgi < p.nseg; sgi += (int64_t)gridDim.x * 4 * G) {
+    const int32_t r = p.tail_row[sgi];
+    if (r < 0) continue;
+    float acc[VE];
+#pragma unroll
+    for (int q = 0; q < VE; ++q) acc[q] = 0.f;
+    if (col0 < p.F) {
+      const int64_t last = (p.off[r + 1] - 1) / SEG;
+#pragma unroll
+      for (int q = 0; q < VE; ++q) acc[q] = p.tail[sgi * p.ldp + col0 + q];
+      for (int64_t t = sgi + 1; t <= last; ++t) {
+#pragma unroll
+        for (int q = 0; q < VE; ++q) acc[q] += p.head[t * p.ldp + col0 + q];
+      }
+    }
+    epi_store_vec<T>(p.ep, r, col0, acc);
   }
 }
 
 template <typename T>
-hipError_t pair_gather_t(int64_t n, int64_t F, int64_t ld, const void* Z, const int32_t* pu, const int32_t* pv,
-                         const float* g, const int64_t* off, const int32_t* entries, const Epilogue& ep, int lpr,
-                         hipStream_t s) {
-  const T* z = reinterpret_cast<const T*>(Z);
-  const int64_t rows_per_block = 4 * (64 / lpr);
-  const unsigned blocks = (unsigned)capped_blocks(n, rows_per_block);
-  const int64_t colblocks = (F + (int64_t)lpr * Vec<T>::N - 1) / ((int64_t)lpr * Vec<T>::N);
-  (void)colblocks;   // lpr covers F (lpr * VE >= F for F <= 64 * VE)
-#define PG(L) hipLaunchKernelGGL((pair_gather_kernel<T, L>), dim3(blocks), dim3(256), 0, s, n, F, ld, z, pu, pv, g, off, entries, ep); break;
+hipError_t pair_segments_t(SegParams p, int lpr, hipStream_t s) {
+  const int64_t per_block = 4 * (64 / lpr);
+  const unsigned blocks = (unsigned)capped_blocks(p.nseg, per_block);
+#define PG(L)                                                                                   \
+  hipLaunchKernelGGL((pair_segment_kernel<T, L>), dim3(blocks), dim3(256), 0, s, p);            \
+  if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;                            \
+  hipLaunchKernelGGL((pair_fixup_kernel<T, L>), dim3(blocks), dim3(256), 0, s, p);              \
+  break;
   switch (lpr) {
     case 1: PG(1)
     case 2: PG(2)
@@ -375,50 +553,99 @@ hipError_t pair_loss_launch(int prec, int64_t n, int64_t F, int64_t ld, const vo
   return hipGetLastError();
 }
 
-size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs) {
+int rs_passes(int64_t n) {
+  int bits = 1;
+  while (((int64_t)1 << bits) <= n) ++bits;         // keys lie in [0, n]
+  return (bits + RS_BITS - 1) / RS_BITS;
+}
+
+int64_t pair_seg_count(int64_t n_pairs) {
+  const int64_t t = (2 * n_pairs + SEG - 1) / SEG;
+  return t < 1 ? 1 : t;
+}
+
+int64_t pair_partial_ld(int prec, int64_t F) {
+  const int64_t ve = prec == 0 ? 4 : 8;
+  return (F + ve - 1) / ve * ve;
+}
+
+size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs, int64_t F) {
+  const int64_t total = 2 * n_pairs;
+  const int64_t nblk = (total + RS_TILE - 1) / RS_TILE;
+  const int64_t nh = RS_DIGITS * (nblk < 1 ? 1 : nblk);
+  const int64_t nseg = pair_seg_count(n_pairs);
+  const int64_t ldp = pair_partial_ld(1, F) > pair_partial_ld(0, F) ? pair_partial_ld(1, F) : pair_partial_ld(0, F);
   size_t b = 0;
-  b += align256(sizeof(int32_t) * n);                                     // counts, then distinct counts
-  b += align256(sizeof(int32_t) * n);                                     // cursors
+  b += 4 * align256(sizeof(int32_t) * (total > 0 ? total : 1));          // keys and ids, two buffers each
+  b += align256(sizeof(int64_t) * nh);                                    // digit histograms / offsets
+  b += align256(sizeof(int64_t) * segment_scan_scratch_elems(nh));        // scan scratch
   b += align256(sizeof(int64_t) * (n + 1));                               // row offsets
-  b += align256(sizeof(int32_t) * 2 * n_pairs);                           // entries (pair ids)
-  b += align256(sizeof(int64_t) * segment_scan_scratch_elems(n + 1));     // scan scratch
+  b += 2 * align256(sizeof(float) * nseg * ldp);                          // head and tail partials
+  b += align256(sizeof(int32_t) * nseg);                                  // tail rows
   return b;
 }
 
 hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, const void* Z, const int32_t* pair_u,
                                 const int32_t* pair_v, int64_t n_pairs, const float* g, void* dZ, int64_t ldz,
                                 int32_t* flag, void* ws, hipStream_t s) {
+  const int64_t total = 2 * n_pairs;
+  const int64_t nblk = (total + RS_TILE - 1) / RS_TILE;
+  const int64_t nh = RS_DIGITS * (nblk < 1 ? 1 : nblk);
+  const int64_t nseg = pair_seg_count(n_pairs);
+  const int64_t ldp = pair_partial_ld(prec, F);
   char* w = static_cast<char*>(ws);
   auto take = [&](size_t bytes) { char* q = w; w += align256(bytes); return q; };
-  int32_t* cnt = (int32_t*)take(sizeof(int32_t) * n);
-  int32_t* cur = (int32_t*)take(sizeof(int32_t) * n);
+  const size_t tb = sizeof(int32_t) * (total > 0 ? total : 1);
+  int32_t* kA = (int32_t*)take(tb);
+  int32_t* vA = (int32_t*)take(tb);
+  int32_t* kB = (int32_t*)take(tb);
+  int32_t* vB = (int32_t*)take(tb);
+  int64_t* hist = (int64_t*)take(sizeof(int64_t) * nh);
+  int64_t* scr = (int64_t*)take(sizeof(int64_t) * segment_scan_scratch_elems(nh));
   int64_t* off = (int64_t*)take(sizeof(int64_t) * (n + 1));
-  int32_t* entries = (int32_t*)take(sizeof(int32_t) * 2 * n_pairs);
-  int64_t* scr = (int64_t*)take(sizeof(int64_t) * segment_scan_scratch_elems(n + 1));
+  const size_t pbytes = sizeof(float) * nseg * (pair_partial_ld(1, F) > pair_partial_ld(0, F) ? pair_partial_ld(1, F)
+                                                                                               : pair_partial_ld(0, F));
+  float* head = (float*)take(pbytes);
+  float* tail = (float*)take(pbytes);
+  int32_t* trow = (int32_t*)take(sizeof(int32_t) * nseg);
   hipError_t e;
 #define GCN_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
-  GCN_TRY(fill_zero(cnt, sizeof(int32_t) * n, s));
-  GCN_TRY(fill_zero(cur, sizeof(int32_t) * n, s));
-  const unsigned gp = (unsigned)capped_blocks(n_pairs, 256);
-  if (n_pairs > 0) {
-    hipLaunchKernelGGL(pair_count_kernel, dim3(gp), dim3(256), 0, s, n, n_pairs, pair_u, pair_v, cnt);
-    GCN_TRY(hipGetLastError());
+  const int32_t* kin = nullptr;
+  const int32_t* vin = nullptr;
+  int32_t* kout = kA;
+  int32_t* vout = vA;
+  if (total > 0) {
+    const int passes = rs_passes(n);
+    for (int ps = 0; ps < passes; ++ps) {
+      const int shift = ps * RS_BITS;
+      hipLaunchKernelGGL(rs_hist_kernel, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, total, shift,
+                         nblk, hist);
+      GCN_TRY(hipGetLastError());
+      GCN_TRY(segment_scan_exclusive(hist, nh, scr, s));
+      hipLaunchKernelGGL(rs_scatter_kernel, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, vin, total,
+                         shift, nblk, hist, kout, vout);
+      GCN_TRY(hipGetLastError());
+      kin = kout;
+      vin = vout;
+      kout = kout == kA ? kB : kA;
+      vout = vout == vA ? vB : vA;
+    }
   }
-  hipLaunchKernelGGL(pair_widen_kernel, dim3((unsigned)capped_blocks(n + 1, 256)), dim3(256), 0, s, n, cnt, off);
+  const unsigned bb = (unsigned)capped_blocks(total + 1, 256);
+  hipLaunchKernelGGL(rs_bounds_kernel, dim3(bb), dim3(256), 0, s, n, kin ? kin : kA, total, off);
   GCN_TRY(hipGetLastError());
-  GCN_TRY(segment_scan_exclusive(off, n + 1, scr, s));
-  if (n_pairs > 0) {
-    hipLaunchKernelGGL(pair_scatter_kernel, dim3(gp), dim3(256), 0, s, n, n_pairs, pair_u, pair_v, off, cur, entries);
-    GCN_TRY(hipGetLastError());
-  }
-  GCN_TRY(sort_segments(n, off, entries, cnt, s));
+  SegParams p;
+  p.n = n; p.F = F; p.ld = ld; p.Z = Z; p.pu = pair_u; p.pv = pair_v; p.g = g; p.off = off;
+  p.vals = vin ? vin : vA;
+  p.nseg = nseg; p.head = head; p.tail = tail; p.tail_row = trow; p.ldp = ldp;
   Epilogue ep{};
   ep.out = dZ; ep.ldo = ldz; ep.rows = n; ep.cols = F; ep.mode = EPI_STORE; ep.flag = flag; ep.keep_scale = 1.f;
+  p.ep = ep;
   const int lpr = lpr_for(prec, F);
   switch (prec) {
-    case 0: GCN_TRY(pair_gather_t<float>(n, F, ld, Z, pair_u, pair_v, g, off, entries, ep, lpr, s)); break;
-    case 1: GCN_TRY(pair_gather_t<f16>(n, F, ld, Z, pair_u, pair_v, g, off, entries, ep, lpr, s)); break;
-    case 2: GCN_TRY(pair_gather_t<bf16>(n, F, ld, Z, pair_u, pair_v, g, off, entries, ep, lpr, s)); break;
+    case 0: GCN_TRY(pair_segments_t<float>(p, lpr, s)); break;
+    case 1: GCN_TRY(pair_segments_t<f16>(p, lpr, s)); break;
+    case 2: GCN_TRY(pair_segments_t<bf16>(p, lpr, s)); break;
     default: return hipErrorInvalidValue;
   }
 #undef GCN_TRY

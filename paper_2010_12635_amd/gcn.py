@@ -135,7 +135,7 @@ def lib():
         "gcn_sample_pairs": (I32, [I64, P, P, I64, I64, I64, ctypes.c_uint64, ctypes.c_uint64, P, P, P]),
         "gcn_pair_loss_workspace_size": (I32, [I64, PSZ]),
         "gcn_pair_loss": (I32, [I64, I64, I64, I32, P, P, P, I64, I64, P, P, P, P, P, P, SZ, P]),
-        "gcn_pair_backward_workspace_size": (I32, [I64, I64, PSZ]),
+        "gcn_pair_backward_workspace_size": (I32, [I64, I64, I64, PSZ]),
         "gcn_pair_backward": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, I64, P, P, SZ, P]),
         "gcn_pair_metrics_workspace_size": (I32, [I64, PSZ]),
         "gcn_pair_metrics": (I32, [P, I64, I64, P, P, SZ, P]),
@@ -329,9 +329,9 @@ def gcn_pair_loss(n, F, ld, prec, Z, pair_u, pair_v, n_pos, n_neg, loss_scale, l
     _check(st, "gcn_pair_loss")
 
 
-def gcn_pair_backward_workspace_size(n, n_pairs) -> int:
+def gcn_pair_backward_workspace_size(n, n_pairs, F) -> int:
     b = ctypes.c_size_t(0)
-    _check(lib().gcn_pair_backward_workspace_size(n, n_pairs, ctypes.byref(b)), "gcn_pair_backward_workspace_size")
+    _check(lib().gcn_pair_backward_workspace_size(n, n_pairs, F, ctypes.byref(b)), "gcn_pair_backward_workspace_size")
     return b.value
 
 

@@ -420,7 +420,7 @@ class GAE2:
         ws = max(G.gcn_layer_workspace_size(graph.adj, self.L1, prec),
                  G.gcn_layer_workspace_size(graph.adj, self.L2, prec),
                  G.gcn_pair_loss_workspace_size(self.K),
-                 G.gcn_pair_backward_workspace_size(n, self.K))
+                 G.gcn_pair_backward_workspace_size(n, self.K, self.f_e))
         self.ws = torch.empty(ws // 4 + 64, dtype=torch.float32, device=dev)
         self.adam_c = self.adam.c()
 

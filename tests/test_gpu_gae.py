@@ -99,7 +99,7 @@ def test_pair_backward_matches_oracle(prec, F):
     Z = z_dev(z, prec, ld)
     dZ = torch.full((n, ld), 7.0, dtype=G.torch_dtype(prec), device="cuda")
     ov = torch.zeros(1, dtype=torch.int32, device="cuda")
-    ws = torch.empty(G.gcn_pair_backward_workspace_size(n, K), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(G.gcn_pair_backward_workspace_size(n, K, F), dtype=torch.uint8, device="cuda")
     G.gcn_pair_backward(n, F, ld, prec, Z, dev(u), dev(v), K, dev(gk), dZ, ld, ov, ws)
     torch.cuda.synchronize()
     want = O.pair_backward(n, host(Z, F), u, v, gk.astype(np.float64))
@@ -109,6 +109,41 @@ def test_pair_backward_matches_oracle(prec, F):
     # run-to-run identical (fixed summation order per row)
     first = dZ.clone()
     G.gcn_pair_backward(n, F, ld, prec, Z, dev(u), dev(v), K, dev(gk), dZ, ld, ov, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(first, dZ)
+
+
+@pytest.mark.parametrize("prec", [G.GCN_F32, G.GCN_F16])
+@pytest.mark.parametrize("n,hub_pairs,K", [(100_003, 5000, 9000), (300, 0, 0), (5000, 700, 700), (70_000, 3, 257)])
+def test_pair_backward_hub_rows_and_edges(prec, n, hub_pairs, K):
+    """Rows whose entries span many 256-entry blocks (a hub in thousands of
+    pairs), rows in no pair, no pairs at all, three radix passes (n > 2^16)
+    and entry counts just past a block boundary."""
+    F = 64
+    print(f"[pair-bwd] prec={prec} n={n} hub={hub_pairs} K={K}", flush=True)
+    rng = np.random.default_rng(n + K)
+    z = (0.5 * rng.standard_normal((n, F))).astype(np.float32)
+    u = rng.integers(0, n, K).astype(np.int32)
+    v = rng.integers(0, n, K).astype(np.int32)
+    if hub_pairs:
+        u[:hub_pairs] = 7
+        v[hub_pairs // 2: hub_pairs] = n - 1
+    gk = (rng.standard_normal(K) * 1e-2).astype(np.float32)
+    ld = F
+    Z = z_dev(z, prec, ld)
+    dZ = torch.full((n, ld), 7.0, dtype=G.torch_dtype(prec), device="cuda")
+    ov = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(G.gcn_pair_backward_workspace_size(n, K, F), dtype=torch.uint8, device="cuda")
+    du = dev(u) if K else None
+    dv = dev(v) if K else None
+    dg = dev(gk) if K else None
+    G.gcn_pair_backward(n, F, ld, prec, Z, du, dv, K, dg, dZ, ld, ov, ws)
+    torch.cuda.synchronize()
+    want = O.pair_backward(n, host(Z, F), u, v, gk.astype(np.float64))
+    assert_close(host(dZ, F), want, prec, "dZ")
+    assert ov.item() == 0
+    first = dZ.clone()
+    G.gcn_pair_backward(n, F, ld, prec, Z, du, dv, K, dg, dZ, ld, ov, ws)
     torch.cuda.synchronize()
     assert torch.equal(first, dZ)
 
@@ -135,7 +170,7 @@ def test_pair_invalid_ids_are_skipped():
     # the backward pass ignores them as well
     dZ = torch.empty((n, ld), device="cuda")
     ov.zero_()
-    bws = torch.empty(G.gcn_pair_backward_workspace_size(n, 5), dtype=torch.uint8, device="cuda")
+    bws = torch.empty(G.gcn_pair_backward_workspace_size(n, 5, F), dtype=torch.uint8, device="cuda")
     gk = np.array([0.5, 1.0, 1.0, -0.25, 1.0], np.float32)
     G.gcn_pair_backward(n, F, ld, G.GCN_F32, Z, dev(u), dev(v), 5, dev(gk), dZ, ld, ov, bws)
     torch.cuda.synchronize()
