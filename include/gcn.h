@@ -398,7 +398,7 @@ gcn_status gcn_pair_loss(int64_t n, int64_t F, int64_t ld, int32_t prec, const v
 
 /* gcn_pair_backward: dZ = d(sum_k g_k s_k)/dZ: row r sums g_k Z[v_k] over
  * the pairs with u_k = r and g_k Z[u_k] over the pairs with v_k = r, in
- * increasing k, rows that span several blocks of 256 pair endpoints being
+ * increasing k, rows that span several blocks of 64 pair endpoints being
  * summed block by block in order (run-to-run deterministic); rows in no
  * pair are 0.  dZ: n x F (ldz, prec; padding columns may be overwritten
  * with 0).  Pairs with an id outside [0, n) are skipped.  n_pairs <= 2^30.

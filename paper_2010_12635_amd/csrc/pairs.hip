@@ -153,7 +153,10 @@ int64_t capped_blocks(int64_t items, int64_t per_block) {
 
 template <typename T>
 hipError_t pair_loss_t(PairLossParams p, int lpr, hipStream_t s, int64_t* nb_out) {
-  const int64_t nb = capped_blocks(p.total, 4 * (64 / lpr));
+  // at most 4096 workgroups (each loops over pairs), so that the final
+  // fixed-order sum over their partials is short
+  int64_t nb = capped_blocks(p.total, 4 * (64 / lpr));
+  if (nb > 4096) nb = 4096;
   *nb_out = nb;
 #define PL(L) hipLaunchKernelGGL((pair_loss_kernel<T, L>), dim3((unsigned)nb), dim3(256), 0, s, p); break;
   switch (lpr) {
@@ -182,7 +185,7 @@ hipError_t pair_loss_t(PairLossParams p, int lpr, hipStream_t s, int64_t* nb_out
 constexpr int RS_BITS = 8, RS_DIGITS = 1 << RS_BITS;
 constexpr int RS_IPT = 8;                           // items per thread per tile
 constexpr int RS_TILE = 256 * RS_IPT;
-constexpr int SEG = 256;                            // sorted entries per gather segment
+constexpr int SEG = 64;                             // sorted entries per gather segment
 
 __device__ __forceinline__ int32_t entry_key(int64_t n, const int32_t* __restrict__ pu, const int32_t* __restrict__ pv,
                                              int64_t i) {
@@ -215,12 +218,14 @@ __global__ __launch_bounds__(256) void rs_hist_kernel(int64_t n, const int32_t* 
 // consecutive items per round, thread order = item order); inside a wave
 // the lanes with the same digit are found with 8 ballots, across the four
 // waves through per-wave counts in LDS stamped with the round.
+// Each item carries its pair index k and the other endpoint of the pair.
 __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_t* __restrict__ pu,
                                                          const int32_t* __restrict__ pv,
                                                          const int32_t* __restrict__ kin, const int32_t* __restrict__ vin,
+                                                         const int32_t* __restrict__ oin,
                                                          int64_t total, int shift, int64_t nblk,
                                                          const int64_t* __restrict__ off, int32_t* __restrict__ kout,
-                                                         int32_t* __restrict__ vout) {
+                                                         int32_t* __restrict__ vout, int32_t* __restrict__ oout) {
   __shared__ int cnt[4][RS_DIGITS];                 // (round << 16) | count
   __shared__ int run[RS_DIGITS];
   __shared__ int64_t dbase[RS_DIGITS];
@@ -235,10 +240,17 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
   for (int r = 0; r < RS_IPT; ++r) {
     const int64_t i = base + r * 256 + threadIdx.x;
     const bool valid = i < total;
-    int32_t k = 0, val = 0;
+    int32_t k = 0, val = 0, oth = 0;
     if (valid) {
-      k = kin ? kin[i] : entry_key(n, pu, pv, i);
-      val = vin ? vin[i] : (int32_t)i;
+      if (kin) {
+        k = kin[i];
+        val = vin[i];
+        oth = oin[i];
+      } else {                                      // first pass: items in pair order
+        k = entry_key(n, pu, pv, i);
+        val = (int32_t)(i >> 1);
+        oth = (i & 1) ? pu[i >> 1] : pv[i >> 1];
+      }
     }
     const int d = (k >> shift) & (RS_DIGITS - 1);
     uint64_t m = __ballot(valid);
@@ -259,6 +271,7 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
       const int64_t pos = dbase[d] + run[d] + before + rank;
       kout[pos] = k;
       vout[pos] = val;
+      oout[pos] = oth;
     }
     __syncthreads();
     int add = 0;
@@ -299,7 +312,8 @@ struct SegParams {
   const int32_t* pv;
   const float* g;
   const int64_t* off;                               // [n + 1]
-  const int32_t* vals;                              // sorted entry ids
+  const int32_t* pk;                                // sorted entries: pair index
+  const int32_t* po;                                // sorted entries: other endpoint
   int64_t nseg;
   float* head;                                      // [nseg][ldp]
   float* tail;                                      // [nseg][ldp]
@@ -314,17 +328,18 @@ __device__ __forceinline__ void seg_sum(const SegParams& p, int64_t e0, int64_t 
   constexpr int VE = Vec<T>::N, U = 4;
   const T* __restrict__ Z = reinterpret_cast<const T*>(p.Z);
   for (int64_t e = e0; e < e1; e += U) {
-    int32_t it[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) it[u] = p.vals[e + u < e1 ? e + u : e1 - 1];
-    int32_t other[U];
-    float w[U];
+    int32_t kk[U], other[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t k = it[u] >> 1;
-      other[u] = (it[u] & 1) ? p.pu[k] : p.pv[k];
-      w[u] = e + u < e1 ? p.g[k] : 0.f;
+      const int64_t ee = e + u < e1 ? e + u : e1 - 1;
+      kk[u] = p.pk[ee];
+      other[u] = p.po[ee];
     }
+    float w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = p.g[kk[u]];
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = e + u < e1 ? w[u] : 0.f;
     uint4 x[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) x[u] = ldg16(Z + (int64_t)other[u] * p.ld + col0);
@@ -576,7 +591,7 @@ size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs, int64_t F) {
   const int64_t nseg = pair_seg_count(n_pairs);
   const int64_t ldp = pair_partial_ld(1, F) > pair_partial_ld(0, F) ? pair_partial_ld(1, F) : pair_partial_ld(0, F);
   size_t b = 0;
-  b += 4 * align256(sizeof(int32_t) * (total > 0 ? total : 1));          // keys and ids, two buffers each
+  b += 6 * align256(sizeof(int32_t) * (total > 0 ? total : 1));          // key, pair, other: two buffers each
   b += align256(sizeof(int64_t) * nh);                                    // digit histograms / offsets
   b += align256(sizeof(int64_t) * segment_scan_scratch_elems(nh));        // scan scratch
   b += align256(sizeof(int64_t) * (n + 1));                               // row offsets
@@ -598,8 +613,10 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
   const size_t tb = sizeof(int32_t) * (total > 0 ? total : 1);
   int32_t* kA = (int32_t*)take(tb);
   int32_t* vA = (int32_t*)take(tb);
+  int32_t* oA = (int32_t*)take(tb);
   int32_t* kB = (int32_t*)take(tb);
   int32_t* vB = (int32_t*)take(tb);
+  int32_t* oB = (int32_t*)take(tb);
   int64_t* hist = (int64_t*)take(sizeof(int64_t) * nh);
   int64_t* scr = (int64_t*)take(sizeof(int64_t) * segment_scan_scratch_elems(nh));
   int64_t* off = (int64_t*)take(sizeof(int64_t) * (n + 1));
@@ -612,8 +629,10 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
 #define GCN_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
   const int32_t* kin = nullptr;
   const int32_t* vin = nullptr;
+  const int32_t* oin = nullptr;
   int32_t* kout = kA;
   int32_t* vout = vA;
+  int32_t* oout = oA;
   if (total > 0) {
     const int passes = rs_passes(n);
     for (int ps = 0; ps < passes; ++ps) {
@@ -622,13 +641,15 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
                          nblk, hist);
       GCN_TRY(hipGetLastError());
       GCN_TRY(segment_scan_exclusive(hist, nh, scr, s));
-      hipLaunchKernelGGL(rs_scatter_kernel, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, vin, total,
-                         shift, nblk, hist, kout, vout);
+      hipLaunchKernelGGL(rs_scatter_kernel, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, vin, oin,
+                         total, shift, nblk, hist, kout, vout, oout);
       GCN_TRY(hipGetLastError());
       kin = kout;
       vin = vout;
+      oin = oout;
       kout = kout == kA ? kB : kA;
       vout = vout == vA ? vB : vA;
+      oout = oout == oA ? oB : oA;
     }
   }
   const unsigned bb = (unsigned)capped_blocks(total + 1, 256);
@@ -636,7 +657,8 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
   GCN_TRY(hipGetLastError());
   SegParams p;
   p.n = n; p.F = F; p.ld = ld; p.Z = Z; p.pu = pair_u; p.pv = pair_v; p.g = g; p.off = off;
-  p.vals = vin ? vin : vA;
+  p.pk = vin ? vin : vA;
+  p.po = oin ? oin : oA;
   p.nseg = nseg; p.head = head; p.tail = tail; p.tail_row = trow; p.ldp = ldp;
   Epilogue ep{};
   ep.out = dZ; ep.ldo = ldz; ep.rows = n; ep.cols = F; ep.mode = EPI_STORE; ep.flag = flag; ep.keep_scale = 1.f;

@@ -116,7 +116,7 @@ def test_pair_backward_matches_oracle(prec, F):
 @pytest.mark.parametrize("prec", [G.GCN_F32, G.GCN_F16])
 @pytest.mark.parametrize("n,hub_pairs,K", [(100_003, 5000, 9000), (300, 0, 0), (5000, 700, 700), (70_000, 3, 257)])
 def test_pair_backward_hub_rows_and_edges(prec, n, hub_pairs, K):
-    """Rows whose entries span many 256-entry blocks (a hub in thousands of
+    """Rows whose entries span many 64-entry blocks (a hub in thousands of
     pairs), rows in no pair, no pairs at all, three radix passes (n > 2^16)
     and entry counts just past a block boundary."""
     F = 64
