@@ -512,6 +512,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before the runs, copy a MIB-MiB device buffer 3 times (reference kernel for "
                          "hardware traffic counters)")
+    ap.add_argument("--stats-command", default=None,
+                    help="with --summarize-stats: the command that produced the statistics")
     ap.add_argument("--summarize-stats", nargs=3, metavar=("STATS_DIR", "OUT_MD", "TITLE"),
                     help="write a kernel time table from a rocprofv3 --stats folder and exit")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -520,6 +522,9 @@ def main():
 
     if args.summarize_stats:
         d, out, title = args.summarize_stats
+        if args.stats_command:
+            summarize_stats(d, out, args.stats_command, title)
+            return
         cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_default -o run -- "
                "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest --no-levels --gae-epochs 0 --table1 none")
         summarize_stats(d, out, cmd, title)
