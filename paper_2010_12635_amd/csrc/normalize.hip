@@ -341,13 +341,19 @@ __global__ void heavy_fill_kernel(int64_t n, const IdxT* __restrict__ rowptr, in
   }
 }
 
-// Light rows by decreasing degree: counting sort over buckets thr - deg
-// (deg <= thr).  A workgroup owns a contiguous range of rows and first
-// counts them per bucket in LDS, so the global atomics are one per bucket
-// and workgroup instead of one per row (most rows of a power-law graph fall
-// into a handful of buckets).  Buckets beyond LIGHT_LDS_BINS use global
-// atomics directly.
+// Light rows, block by block of LIGHT_BLOCK consecutive row ids, by
+// decreasing degree inside a block: a counting sort over the buckets
+// (r / LIGHT_BLOCK) (thr + 1) + thr - deg (deg <= thr).  Rows of similar
+// length share a wave, and rows whose ids are close -- whose neighbours
+// overlap more in an R-MAT graph -- run together (measured on R-MAT scale
+// 21: 5 % faster than one global degree order).  A workgroup owns a
+// contiguous range of rows and first counts them per bucket in LDS, so the
+// global atomics are one per bucket and workgroup; buckets beyond
+// LIGHT_LDS_BINS of the workgroup's first bucket use global atomics.
 constexpr int LIGHT_LDS_BINS = 1024;
+constexpr int64_t LIGHT_BLOCK = 4096;
+
+int64_t light_buckets(int64_t n, int64_t thr) { return (n + LIGHT_BLOCK - 1) / LIGHT_BLOCK * (thr + 1); }
 
 __device__ __forceinline__ void row_range(int64_t n, int64_t* r0, int64_t* r1) {
   const int64_t per = (n + gridDim.x - 1) / gridDim.x;
@@ -357,47 +363,52 @@ __device__ __forceinline__ void row_range(int64_t n, int64_t* r0, int64_t* r1) {
 
 template <typename IdxT>
 __global__ __launch_bounds__(256) void light_hist_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
-                                                         int32_t* __restrict__ hist) {
+                                                         int64_t nb, int32_t* __restrict__ hist) {
   __shared__ int32_t lh[LIGHT_LDS_BINS];
   for (int b = threadIdx.x; b < LIGHT_LDS_BINS; b += 256) lh[b] = 0;
   __syncthreads();
   int64_t r0, r1;
   row_range(n, &r0, &r1);
+  const int64_t base = (r0 / LIGHT_BLOCK) * (thr + 1);
   for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
     const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
     if (d > thr) continue;
-    const int64_t b = thr - d;
-    if (b < LIGHT_LDS_BINS) atomicAdd(&lh[b], 1);
+    const int64_t b = (r / LIGHT_BLOCK) * (thr + 1) + thr - d;
+    if (b - base < LIGHT_LDS_BINS) atomicAdd(&lh[b - base], 1);
     else atomicAdd(&hist[b], 1);
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < LIGHT_LDS_BINS && b <= thr; b += 256)
-    if (lh[b]) atomicAdd(&hist[b], lh[b]);
+  for (int b = threadIdx.x; b < LIGHT_LDS_BINS && base + b < nb; b += 256)
+    if (lh[b]) atomicAdd(&hist[base + b], lh[b]);
 }
 
 template <typename IdxT>
 __global__ __launch_bounds__(256) void light_scatter_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
-                                                            const int64_t* __restrict__ boff, int32_t* __restrict__ cur,
-                                                            int32_t* __restrict__ perm) {
+                                                            int64_t nb, const int64_t* __restrict__ boff,
+                                                            int32_t* __restrict__ cur, int32_t* __restrict__ perm) {
   __shared__ int32_t lh[LIGHT_LDS_BINS];     // count, then this workgroup's base within the bucket
   __shared__ int32_t lc[LIGHT_LDS_BINS];     // local cursor
   for (int b = threadIdx.x; b < LIGHT_LDS_BINS; b += 256) { lh[b] = 0; lc[b] = 0; }
   __syncthreads();
   int64_t r0, r1;
   row_range(n, &r0, &r1);
+  const int64_t base = (r0 / LIGHT_BLOCK) * (thr + 1);
   for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
     const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
-    if (d <= thr && thr - d < LIGHT_LDS_BINS) atomicAdd(&lh[thr - d], 1);
+    if (d > thr) continue;
+    const int64_t b = (r / LIGHT_BLOCK) * (thr + 1) + thr - d;
+    if (b - base < LIGHT_LDS_BINS) atomicAdd(&lh[b - base], 1);
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < LIGHT_LDS_BINS && b <= thr; b += 256)
-    if (lh[b]) lh[b] = atomicAdd(&cur[b], lh[b]);
+  for (int b = threadIdx.x; b < LIGHT_LDS_BINS && base + b < nb; b += 256)
+    if (lh[b]) lh[b] = atomicAdd(&cur[base + b], lh[b]);
   __syncthreads();
   for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
     const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
     if (d > thr) continue;
-    const int64_t b = thr - d;
-    const int64_t pos = b < LIGHT_LDS_BINS ? (int64_t)lh[b] + atomicAdd(&lc[b], 1) : (int64_t)atomicAdd(&cur[b], 1);
+    const int64_t b = (r / LIGHT_BLOCK) * (thr + 1) + thr - d;
+    const int64_t pos = b - base < LIGHT_LDS_BINS ? (int64_t)lh[b - base] + atomicAdd(&lc[b - base], 1)
+                                                  : (int64_t)atomicAdd(&cur[b], 1);
     perm[boff[b] + pos] = (int32_t)r;
   }
 }
@@ -543,7 +554,8 @@ hipError_t normalize_run(int64_t n, int64_t E, const int32_t* src, const int32_t
 
 size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
   const int64_t max_chunks = nnz / chunk_nnz + n + 1;
-  int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
+  const int64_t nb = light_buckets(n, thr);
+  int64_t scan_n = (n + 1 > nb + 1) ? n + 1 : nb + 1;
   if (scan_n < CHUNK_BUCKETS + 1) scan_n = CHUNK_BUCKETS + 1;
   size_t b = 0;
   b += align256(sizeof(int32_t) * max_chunks);                  // chunk_order
@@ -557,9 +569,9 @@ size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
   b += align256(sizeof(int32_t) * n);                           // row_perm
   b += align256(sizeof(int64_t) * (n + 1));                     // flags -> heavy index
   b += align256(sizeof(int64_t) * (n + 1));                     // chunks per row -> chunk offsets
-  b += align256(sizeof(int32_t) * (thr + 1));                   // degree histogram
-  b += align256(sizeof(int32_t) * (thr + 1));                   // bucket cursors
-  b += align256(sizeof(int64_t) * (thr + 2));                   // bucket offsets
+  b += align256(sizeof(int32_t) * nb);                          // (block, degree) histogram
+  b += align256(sizeof(int32_t) * nb);                          // bucket cursors
+  b += align256(sizeof(int64_t) * (nb + 1));                    // bucket offsets
   b += align256(sizeof(int64_t) * scan_scratch_elems(scan_n));  // scan scratch
   return b;
 }
@@ -571,7 +583,8 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   char* w = static_cast<char*>(sched);
   auto take = [&](size_t bytes) { char* p = w; w += align256(bytes); return p; };
   const int64_t max_chunks = nnz / chunk + n + 1;
-  int64_t scan_n = (n + 1 > thr + 2) ? n + 1 : thr + 2;
+  const int64_t nb = light_buckets(n, thr);
+  int64_t scan_n = (n + 1 > nb + 1) ? n + 1 : nb + 1;
   if (scan_n < CHUNK_BUCKETS + 1) scan_n = CHUNK_BUCKETS + 1;
   int32_t* corder = (int32_t*)take(sizeof(int32_t) * max_chunks);
   int32_t* ckey = (int32_t*)take(sizeof(int32_t) * max_chunks);
@@ -584,9 +597,9 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   int32_t* perm = (int32_t*)take(sizeof(int32_t) * n);
   int64_t* hidx = (int64_t*)take(sizeof(int64_t) * (n + 1));
   int64_t* choff = (int64_t*)take(sizeof(int64_t) * (n + 1));
-  int32_t* hist = (int32_t*)take(sizeof(int32_t) * (thr + 1));
-  int32_t* cur = (int32_t*)take(sizeof(int32_t) * (thr + 1));
-  int64_t* boff = (int64_t*)take(sizeof(int64_t) * (thr + 2));
+  int32_t* hist = (int32_t*)take(sizeof(int32_t) * nb);
+  int32_t* cur = (int32_t*)take(sizeof(int32_t) * nb);
+  int64_t* boff = (int64_t*)take(sizeof(int64_t) * (nb + 1));
   int64_t* scr = (int64_t*)take(sizeof(int64_t) * scan_scratch_elems(scan_n));
   if ((size_t)(w - static_cast<char*>(sched)) > sched_bytes) return hipErrorInvalidValue;
   hipError_t e;
@@ -603,26 +616,26 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   else
     hipLaunchKernelGGL(heavy_fill_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, hidx, choff, hr, hco, ch);
   GCN_TRY(hipGetLastError());
-  // light rows by decreasing degree: counting sort on bucket thr - deg
-  GCN_TRY(fill_zero(hist, sizeof(int32_t) * (thr + 1), s));
-  GCN_TRY(fill_zero(cur, sizeof(int32_t) * (thr + 1), s));
+  // light rows, block by block, by decreasing degree inside a block
+  GCN_TRY(fill_zero(hist, sizeof(int32_t) * nb, s));
+  GCN_TRY(fill_zero(cur, sizeof(int32_t) * nb, s));
   if (idx64)
-    hipLaunchKernelGGL(light_hist_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, hist);
+    hipLaunchKernelGGL(light_hist_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, nb, hist);
   else
-    hipLaunchKernelGGL(light_hist_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, hist);
+    hipLaunchKernelGGL(light_hist_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, nb, hist);
   GCN_TRY(hipGetLastError());
-  hipLaunchKernelGGL(widen_kernel, dim3(grid_for(thr + 2)), dim3(256), 0, s, thr + 1, hist, boff);
+  hipLaunchKernelGGL(widen_kernel, dim3(grid_for(nb + 1)), dim3(256), 0, s, nb, hist, boff);
   GCN_TRY(hipGetLastError());
-  GCN_TRY(scan_exclusive(boff, thr + 2, scr, s));
+  GCN_TRY(scan_exclusive(boff, nb + 1, scr, s));
   if (idx64)
-    hipLaunchKernelGGL(light_scatter_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, boff, cur, perm);
+    hipLaunchKernelGGL(light_scatter_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, nb, boff, cur, perm);
   else
-    hipLaunchKernelGGL(light_scatter_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, boff, cur, perm);
+    hipLaunchKernelGGL(light_scatter_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, nb, boff, cur, perm);
   GCN_TRY(hipGetLastError());
   int64_t host[3] = {0, 0, 0};
   GCN_TRY(hipMemcpyAsync(&host[0], hidx + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipMemcpyAsync(&host[1], choff + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-  GCN_TRY(hipMemcpyAsync(&host[2], boff + thr + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  GCN_TRY(hipMemcpyAsync(&host[2], boff + nb, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipStreamSynchronize(s));
   // chunks in order of the column bucket of their first entry
   const int64_t nch = host[1];
