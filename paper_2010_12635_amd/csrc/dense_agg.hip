@@ -323,7 +323,8 @@ __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
 //    workgroup, measured slower: 41 % against 54 % of the MFMA peak.)
 //  * Tiles are dealt out XCD by XCD: workgroup b runs on XCD b % 8, and each
 //    XCD takes a contiguous range of tiles in row-major order, so the column
-//    tiles of a row block run together and share A_hat in that XCD's L2.
+//    tiles of a row block run together and share A_hat in that XCD's L2
+//    (measured at n = 32768: 1-2 % over plain order, 4 % over column-major).
 //  * The epilogue stages each 16-row strip of the wave's quarter through
 //    LDS and stores rows as 16-byte vectors through the fused epilogue.
 // ---------------------------------------------------------------------------
