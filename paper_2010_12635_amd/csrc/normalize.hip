@@ -341,19 +341,25 @@ __global__ void heavy_fill_kernel(int64_t n, const IdxT* __restrict__ rowptr, in
   }
 }
 
-// Light rows, block by block of LIGHT_BLOCK consecutive row ids, by
-// decreasing degree inside a block: a counting sort over the buckets
-// (r / LIGHT_BLOCK) (thr + 1) + thr - deg (deg <= thr).  Rows of similar
-// length share a wave, and rows whose ids are close -- whose neighbours
-// overlap more in an R-MAT graph -- run together (measured on R-MAT scale
-// 21: 5 % faster than one global degree order).  A workgroup owns a
-// contiguous range of rows and first counts them per bucket in LDS, so the
-// global atomics are one per bucket and workgroup; buckets beyond
-// LIGHT_LDS_BINS of the workgroup's first bucket use global atomics.
+// Light rows, block by block of `blk` consecutive row ids, by decreasing
+// degree inside a block: a counting sort over the buckets
+// (r / blk) (thr + 1) + thr - deg (deg <= thr).  Rows of similar length
+// share a wave, and on large graphs rows whose ids are close -- whose
+// neighbours overlap more in an R-MAT graph -- run together (R-MAT scale 21:
+// 5 % faster than one global degree order).  Below 2^20 rows one block (a
+// global decreasing-degree order) is kept: there the longest rows must
+// start first or they form the tail (R-MAT scale 17, F = 256: 23 % slower
+// with blocks of 4096).  A workgroup owns a contiguous range of rows and
+// first counts them per bucket in LDS, so the global atomics are one per
+// bucket and workgroup; buckets beyond LIGHT_LDS_BINS of the workgroup's
+// first bucket use global atomics.
 constexpr int LIGHT_LDS_BINS = 1024;
-constexpr int64_t LIGHT_BLOCK = 4096;
 
-int64_t light_buckets(int64_t n, int64_t thr) { return (n + LIGHT_BLOCK - 1) / LIGHT_BLOCK * (thr + 1); }
+int64_t light_block(int64_t n) { return n >= ((int64_t)1 << 20) ? 4096 : (n > 0 ? n : 1); }
+int64_t light_buckets(int64_t n, int64_t thr) {
+  const int64_t blk = light_block(n);
+  return (n + blk - 1) / blk * (thr + 1);
+}
 
 __device__ __forceinline__ void row_range(int64_t n, int64_t* r0, int64_t* r1) {
   const int64_t per = (n + gridDim.x - 1) / gridDim.x;
@@ -363,17 +369,17 @@ __device__ __forceinline__ void row_range(int64_t n, int64_t* r0, int64_t* r1) {
 
 template <typename IdxT>
 __global__ __launch_bounds__(256) void light_hist_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
-                                                         int64_t nb, int32_t* __restrict__ hist) {
+                                                         int64_t blk, int64_t nb, int32_t* __restrict__ hist) {
   __shared__ int32_t lh[LIGHT_LDS_BINS];
   for (int b = threadIdx.x; b < LIGHT_LDS_BINS; b += 256) lh[b] = 0;
   __syncthreads();
   int64_t r0, r1;
   row_range(n, &r0, &r1);
-  const int64_t base = (r0 / LIGHT_BLOCK) * (thr + 1);
+  const int64_t base = (r0 / blk) * (thr + 1);
   for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
     const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
     if (d > thr) continue;
-    const int64_t b = (r / LIGHT_BLOCK) * (thr + 1) + thr - d;
+    const int64_t b = (r / blk) * (thr + 1) + thr - d;
     if (b - base < LIGHT_LDS_BINS) atomicAdd(&lh[b - base], 1);
     else atomicAdd(&hist[b], 1);
   }
@@ -384,7 +390,7 @@ __global__ __launch_bounds__(256) void light_hist_kernel(int64_t n, const IdxT* 
 
 template <typename IdxT>
 __global__ __launch_bounds__(256) void light_scatter_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
-                                                            int64_t nb, const int64_t* __restrict__ boff,
+                                                            int64_t blk, int64_t nb, const int64_t* __restrict__ boff,
                                                             int32_t* __restrict__ cur, int32_t* __restrict__ perm) {
   __shared__ int32_t lh[LIGHT_LDS_BINS];     // count, then this workgroup's base within the bucket
   __shared__ int32_t lc[LIGHT_LDS_BINS];     // local cursor
@@ -392,11 +398,11 @@ __global__ __launch_bounds__(256) void light_scatter_kernel(int64_t n, const Idx
   __syncthreads();
   int64_t r0, r1;
   row_range(n, &r0, &r1);
-  const int64_t base = (r0 / LIGHT_BLOCK) * (thr + 1);
+  const int64_t base = (r0 / blk) * (thr + 1);
   for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
     const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
     if (d > thr) continue;
-    const int64_t b = (r / LIGHT_BLOCK) * (thr + 1) + thr - d;
+    const int64_t b = (r / blk) * (thr + 1) + thr - d;
     if (b - base < LIGHT_LDS_BINS) atomicAdd(&lh[b - base], 1);
   }
   __syncthreads();
@@ -406,7 +412,7 @@ __global__ __launch_bounds__(256) void light_scatter_kernel(int64_t n, const Idx
   for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) {
     const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
     if (d > thr) continue;
-    const int64_t b = (r / LIGHT_BLOCK) * (thr + 1) + thr - d;
+    const int64_t b = (r / blk) * (thr + 1) + thr - d;
     const int64_t pos = b - base < LIGHT_LDS_BINS ? (int64_t)lh[b - base] + atomicAdd(&lc[b - base], 1)
                                                   : (int64_t)atomicAdd(&cur[b], 1);
     perm[boff[b] + pos] = (int32_t)r;
@@ -620,17 +626,17 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   GCN_TRY(fill_zero(hist, sizeof(int32_t) * nb, s));
   GCN_TRY(fill_zero(cur, sizeof(int32_t) * nb, s));
   if (idx64)
-    hipLaunchKernelGGL(light_hist_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, nb, hist);
+    hipLaunchKernelGGL(light_hist_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, light_block(n), nb, hist);
   else
-    hipLaunchKernelGGL(light_hist_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, nb, hist);
+    hipLaunchKernelGGL(light_hist_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, light_block(n), nb, hist);
   GCN_TRY(hipGetLastError());
   hipLaunchKernelGGL(widen_kernel, dim3(grid_for(nb + 1)), dim3(256), 0, s, nb, hist, boff);
   GCN_TRY(hipGetLastError());
   GCN_TRY(scan_exclusive(boff, nb + 1, scr, s));
   if (idx64)
-    hipLaunchKernelGGL(light_scatter_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, nb, boff, cur, perm);
+    hipLaunchKernelGGL(light_scatter_kernel<int64_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, light_block(n), nb, boff, cur, perm);
   else
-    hipLaunchKernelGGL(light_scatter_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, nb, boff, cur, perm);
+    hipLaunchKernelGGL(light_scatter_kernel<int32_t>, dim3(grid_for(n)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, light_block(n), nb, boff, cur, perm);
   GCN_TRY(hipGetLastError());
   int64_t host[3] = {0, 0, 0};
   GCN_TRY(hipMemcpyAsync(&host[0], hidx + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));

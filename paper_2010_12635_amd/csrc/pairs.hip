@@ -182,7 +182,7 @@ hipError_t pair_loss_t(PairLossParams p, int lpr, hipStream_t s, int64_t* nb_out
 // sorted entries are cut into segments of SEG entries; a lane group per
 // segment sums the rows that lie inside it and leaves partial sums for the
 // rows that cross its ends, which a fix-up pass adds in segment order.
-constexpr int RS_BITS = 8, RS_DIGITS = 1 << RS_BITS;
+constexpr int RS_MAX_BITS = 8;                      // digit width
 constexpr int RS_IPT = 8;                           // items per thread per tile
 constexpr int RS_TILE = 256 * RS_IPT;
 constexpr int SEG = 64;                             // sorted entries per gather segment
@@ -195,23 +195,25 @@ __device__ __forceinline__ int32_t entry_key(int64_t n, const int32_t* __restric
 }
 
 // Digit histogram of one tile: hist[d * nblk + blockIdx.x] (digit-major).
+template <int BITS>
 __global__ __launch_bounds__(256) void rs_hist_kernel(int64_t n, const int32_t* __restrict__ pu,
                                                       const int32_t* __restrict__ pv, const int32_t* __restrict__ keys,
                                                       int64_t total, int shift, int64_t nblk,
                                                       int64_t* __restrict__ hist) {
-  __shared__ int cnt[RS_DIGITS];
-  cnt[threadIdx.x] = 0;
+  constexpr int DIGITS = 1 << BITS;
+  __shared__ int cnt[DIGITS];
+  for (int d = threadIdx.x; d < DIGITS; d += 256) cnt[d] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * RS_TILE;
   for (int r = 0; r < RS_IPT; ++r) {
     const int64_t i = base + r * 256 + threadIdx.x;
     if (i < total) {
       const int32_t k = keys ? keys[i] : entry_key(n, pu, pv, i);
-      atomicAdd(&cnt[(k >> shift) & (RS_DIGITS - 1)], 1);
+      atomicAdd(&cnt[(k >> shift) & (DIGITS - 1)], 1);
     }
   }
   __syncthreads();
-  hist[(int64_t)threadIdx.x * nblk + blockIdx.x] = cnt[threadIdx.x];
+  for (int d = threadIdx.x; d < DIGITS; d += 256) hist[(int64_t)d * nblk + blockIdx.x] = cnt[d];
 }
 
 // Stable scatter of one tile: items are ranked round by round (256
@@ -219,6 +221,7 @@ __global__ __launch_bounds__(256) void rs_hist_kernel(int64_t n, const int32_t* 
 // the lanes with the same digit are found with 8 ballots, across the four
 // waves through per-wave counts in LDS stamped with the round.
 // Each item carries its pair index k and the other endpoint of the pair.
+template <int BITS>
 __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_t* __restrict__ pu,
                                                          const int32_t* __restrict__ pv,
                                                          const int32_t* __restrict__ kin, const int32_t* __restrict__ vin,
@@ -226,14 +229,17 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
                                                          int64_t total, int shift, int64_t nblk,
                                                          const int64_t* __restrict__ off, int32_t* __restrict__ kout,
                                                          int32_t* __restrict__ vout, int32_t* __restrict__ oout) {
-  __shared__ int cnt[4][RS_DIGITS];                 // (round << 16) | count
-  __shared__ int run[RS_DIGITS];
-  __shared__ int64_t dbase[RS_DIGITS];
+  constexpr int DIGITS = 1 << BITS;
+  __shared__ int cnt[4][DIGITS];                    // (round << 16) | count
+  __shared__ int run[DIGITS];
+  __shared__ int64_t dbase[DIGITS];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  run[threadIdx.x] = 0;
-  dbase[threadIdx.x] = off[(int64_t)threadIdx.x * nblk + blockIdx.x];
+  for (int d = threadIdx.x; d < DIGITS; d += 256) {
+    run[d] = 0;
+    dbase[d] = off[(int64_t)d * nblk + blockIdx.x];
 #pragma unroll
-  for (int w = 0; w < 4; ++w) cnt[w][threadIdx.x] = -1;   // stamp -1: no round yet
+    for (int w = 0; w < 4; ++w) cnt[w][d] = -1;     // stamp -1: no round yet
+  }
   __syncthreads();
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t base = (int64_t)blockIdx.x * RS_TILE;
@@ -252,10 +258,10 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
         oth = (i & 1) ? pu[i >> 1] : pv[i >> 1];
       }
     }
-    const int d = (k >> shift) & (RS_DIGITS - 1);
+    const int d = (k >> shift) & (DIGITS - 1);
     uint64_t m = __ballot(valid);
 #pragma unroll
-    for (int bit = 0; bit < RS_BITS; ++bit) {
+    for (int bit = 0; bit < BITS; ++bit) {
       const uint64_t bb = __ballot((d >> bit) & 1);
       m &= ((d >> bit) & 1) ? bb : ~bb;
     }
@@ -274,13 +280,15 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
       oout[pos] = oth;
     }
     __syncthreads();
-    int add = 0;
+    for (int dd = threadIdx.x; dd < DIGITS; dd += 256) {
+      int add = 0;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const int c = cnt[w][threadIdx.x];
-      if ((c >> 16) == r) add += c & 0xFFFF;
+      for (int w = 0; w < 4; ++w) {
+        const int c = cnt[w][dd];
+        if ((c >> 16) == r) add += c & 0xFFFF;
+      }
+      run[dd] += add;
     }
-    run[threadIdx.x] += add;
     __syncthreads();
   }
 }
@@ -568,10 +576,13 @@ hipError_t pair_loss_launch(int prec, int64_t n, int64_t F, int64_t ld, const vo
   return hipGetLastError();
 }
 
-int rs_passes(int64_t n) {
+// Passes for keys in [0, n] with 8-bit digits (wider digits measured no
+// faster: the 9-bit scatter took as long as the pass it saved).
+void rs_plan(int64_t n, int* passes, int* width) {
   int bits = 1;
-  while (((int64_t)1 << bits) <= n) ++bits;         // keys lie in [0, n]
-  return (bits + RS_BITS - 1) / RS_BITS;
+  while (((int64_t)1 << bits) <= n) ++bits;
+  *width = 8;
+  *passes = (bits + 7) / 8;
 }
 
 int64_t pair_seg_count(int64_t n_pairs) {
@@ -587,7 +598,7 @@ int64_t pair_partial_ld(int prec, int64_t F) {
 size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs, int64_t F) {
   const int64_t total = 2 * n_pairs;
   const int64_t nblk = (total + RS_TILE - 1) / RS_TILE;
-  const int64_t nh = RS_DIGITS * (nblk < 1 ? 1 : nblk);
+  const int64_t nh = ((int64_t)1 << RS_MAX_BITS) * (nblk < 1 ? 1 : nblk);
   const int64_t nseg = pair_seg_count(n_pairs);
   const int64_t ldp = pair_partial_ld(1, F) > pair_partial_ld(0, F) ? pair_partial_ld(1, F) : pair_partial_ld(0, F);
   size_t b = 0;
@@ -605,7 +616,7 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
                                 int32_t* flag, void* ws, hipStream_t s) {
   const int64_t total = 2 * n_pairs;
   const int64_t nblk = (total + RS_TILE - 1) / RS_TILE;
-  const int64_t nh = RS_DIGITS * (nblk < 1 ? 1 : nblk);
+  const int64_t nh = ((int64_t)1 << RS_MAX_BITS) * (nblk < 1 ? 1 : nblk);
   const int64_t nseg = pair_seg_count(n_pairs);
   const int64_t ldp = pair_partial_ld(prec, F);
   char* w = static_cast<char*>(ws);
@@ -634,16 +645,21 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
   int32_t* vout = vA;
   int32_t* oout = oA;
   if (total > 0) {
-    const int passes = rs_passes(n);
+    int passes = 0, width = 8;
+    rs_plan(n, &passes, &width);
+    const int64_t nhw = ((int64_t)1 << width) * nblk;
     for (int ps = 0; ps < passes; ++ps) {
-      const int shift = ps * RS_BITS;
-      hipLaunchKernelGGL(rs_hist_kernel, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, total, shift,
-                         nblk, hist);
-      GCN_TRY(hipGetLastError());
-      GCN_TRY(segment_scan_exclusive(hist, nh, scr, s));
-      hipLaunchKernelGGL(rs_scatter_kernel, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, vin, oin,
-                         total, shift, nblk, hist, kout, vout, oout);
-      GCN_TRY(hipGetLastError());
+      const int shift = ps * width;
+#define RS_PASS(B)                                                                                          \
+  hipLaunchKernelGGL(rs_hist_kernel<B>, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, total, \
+                     shift, nblk, hist);                                                                    \
+  GCN_TRY(hipGetLastError());                                                                               \
+  GCN_TRY(segment_scan_exclusive(hist, nhw, scr, s));                                                       \
+  hipLaunchKernelGGL(rs_scatter_kernel<B>, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, vin, \
+                     oin, total, shift, nblk, hist, kout, vout, oout);                                      \
+  GCN_TRY(hipGetLastError());
+      RS_PASS(8)
+#undef RS_PASS
       kin = kout;
       vin = vout;
       oin = oout;

@@ -57,6 +57,19 @@ def test_csr_at_2pow26(big):
         assert np.array_equal(got, big["nbrs"][int(r)]), r
         assert dinv[r] == np.float32(1.0 / np.sqrt(np.float64(deg[r])))
     assert dg.adj.n_heavy == int((deg > 512).sum()) >= 1
+    # light-row schedule: every light row once, in blocks of 4096 consecutive
+    # ids, decreasing degree inside a block
+    a = dg.adj
+    base = dg.sched
+    o = a.row_perm - base.data_ptr()
+    perm = base[o: o + 4 * a.n_light].view(torch.int32).cpu().numpy()
+    light = deg <= 512
+    assert a.n_light == int(light.sum())
+    blk = perm.astype(np.int64) // 4096
+    assert np.all(np.diff(blk) >= 0)
+    same = np.diff(blk) == 0
+    assert np.all(np.diff(deg[perm].astype(np.int64))[same] <= 0)
+    assert np.all(light[perm]) and np.unique(perm).size == perm.size
 
 
 def test_layer_fwd_at_2pow26(big):

@@ -105,8 +105,8 @@ def test_normalize_empty_and_bad_ids():
 
 
 def test_schedule_lists_heavy_rows():
-    n = 9000                                      # three blocks of light rows
-    src, dst = hub_graph(n, 27000, [(5, 400), (17, 120), (8999, 1000)], seed=3)
+    n = 3000
+    src, dst = hub_graph(n, 9000, [(5, 400), (17, 120), (2999, 1000)], seed=3)
     g = O.graph(n, src, dst)
     dg = DeviceGraph(n, src, dst, prec=G.GCN_F16, heavy_threshold=32, chunk_nnz=64)
     a = dg.adj
@@ -122,16 +122,13 @@ def test_schedule_lists_heavy_rows():
     want = np.concatenate([[0], np.cumsum((g.deg[heavy] + 63) // 64)])
     assert np.array_equal(cho, want)
     assert a.n_chunks == want[-1]
-    # light rows: every row with deg <= threshold exactly once, in blocks of
-    # 4096 consecutive ids (ascending), degree non-increasing inside a block
+    # light rows: every row with deg <= threshold exactly once, degree
+    # non-increasing (below 2^20 rows the order is one global degree order)
     perm = base[off(a.row_perm): off(a.row_perm) + 4 * a.n_light].view(torch.int32).cpu().numpy()
     light = np.flatnonzero(g.deg <= 32)
     assert a.n_light == light.size
     assert np.array_equal(np.sort(perm), light)
-    blk = perm // 4096
-    assert np.all(np.diff(blk) >= 0)
-    same = np.diff(blk) == 0
-    assert np.all(np.diff(g.deg[perm])[same] <= 0)
+    assert np.all(np.diff(g.deg[perm]) <= 0)
     # chunk launch order: every chunk once, first columns in non-decreasing buckets
     order = base[off(a.chunk_order): off(a.chunk_order) + 4 * a.n_chunks].view(torch.int32).cpu().numpy()
     assert np.array_equal(np.sort(order), np.arange(a.n_chunks))
