@@ -144,9 +144,6 @@ hipError_t fill_zero(void* p, size_t bytes, hipStream_t s);
 // segment_scan_scratch_elems(count) int64.
 int64_t segment_scan_scratch_elems(int64_t count);
 hipError_t segment_scan_exclusive(int64_t* data, int64_t count, int64_t* scratch, hipStream_t s);
-// Sort every segment [off[r], off[r+1]) of keys ascending (r < n); ucnt[r]
-// receives the number of distinct keys of the segment.
-hipError_t sort_segments(int64_t n, const int64_t* off, int32_t* keys, int32_t* ucnt, hipStream_t s);
 
 // ------------------------------------------------------ link prediction ----
 // Pair decoder of Eq. (2) on sampled pairs (see gcn.h for the definitions).

@@ -453,17 +453,6 @@ hipError_t segment_scan_exclusive(int64_t* data, int64_t count, int64_t* scratch
   return scan_exclusive(data, count, scratch, s);
 }
 
-hipError_t sort_segments(int64_t n, const int64_t* off, int32_t* keys, int32_t* ucnt, hipStream_t s) {
-  hipLaunchKernelGGL(sort_small_kernel, dim3(wave_rows_grid(n)), dim3(256), 0, s, n, off, keys, ucnt);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sort_medium_kernel, dim3(grid_for(n, 1, 4096)), dim3(256), 0, s, n, off, keys, ucnt);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sort_large_kernel, dim3(grid_for(n, 1, 1024)), dim3(256), 0, s, n, off, keys, ucnt);
-  return hipGetLastError();
-}
-
 hipError_t fill_zero(void* p, size_t bytes, hipStream_t s) {
   if (bytes == 0) return hipSuccess;
   // callers pass 4-byte multiples
