@@ -247,3 +247,57 @@ def test_gae_trains_and_scores_held_out_pairs():
           f"held-out loss {loss0:.3f} -> {loss1:.3f}", flush=True)
     assert m.scaler_state()["skipped"] <= 2
     assert loss1 < loss0 and auc1 > 0.6 and ap1 > 0.6
+
+
+def test_pair_path_at_full_size():
+    """The link-prediction calls at the benchmark's size (R-MAT scale 17
+    training edges, 2^20 + 2^20 pairs, F = 64, fp16): the pairs bit-exact,
+    sampled scores and gradients against the oracle's per-pair formula, the
+    mean loss over all pairs, and sampled rows of dZ (the hubs among them)
+    against the oracle's per-row sum."""
+    wl = I.gae_workload(0)
+    n, F = wl["n"], 64
+    n_pos = n_neg = 1 << 20
+    K = n_pos + n_neg
+    print(f"[gae-full] n={n} K={K}", flush=True)
+    eu, ev = wl["train_u"], wl["train_v"]
+    pu = torch.empty(K, dtype=torch.int32, device="cuda")
+    pv = torch.empty_like(pu)
+    G.gcn_sample_pairs(n, dev(eu), dev(ev), n_pos, n_neg, 11, 4, pu, pv)
+    u, v = O.sample_pairs(11, 4, n, eu, ev, n_pos, n_neg)
+    assert np.array_equal(pu.cpu().numpy(), u) and np.array_equal(pv.cpu().numpy(), v)
+    rng = np.random.default_rng(12)
+    z = (0.3 * rng.standard_normal((n, F))).astype(np.float32)
+    Z = z_dev(z, G.GCN_F16, F)
+    zr = host(Z, F)
+    scale = torch.tensor([1024.0], device="cuda")
+    loss = torch.zeros(1, device="cuda")
+    scores = torch.empty(K, device="cuda")
+    g = torch.empty(K, device="cuda")
+    ov = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(G.gcn_pair_loss_workspace_size(K), dtype=torch.uint8, device="cuda")
+    G.gcn_pair_loss(n, F, F, G.GCN_F16, Z, pu, pv, n_pos, n_neg, scale, loss, scores, g, ov, ws)
+    torch.cuda.synchronize()
+    s_all = np.einsum("ij,ij->i", zr[u], zr[v])
+    y = (np.arange(K) < n_pos).astype(np.float64)
+    want_loss = np.mean(np.logaddexp(0.0, s_all) - y * s_all)
+    assert abs(loss.item() - want_loss) <= 1e-4 * abs(want_loss)
+    ks = np.unique(np.concatenate([[0, n_pos - 1, n_pos, K - 1], rng.choice(K, 500, replace=False)]))
+    sg, gg = scores.cpu().numpy()[ks], g.cpu().numpy()[ks]
+    assert np.allclose(sg, s_all[ks], rtol=1e-4, atol=1e-4)
+    want_g = (1.0 / (1.0 + np.exp(-s_all[ks])) - y[ks]) * 1024.0 / K
+    assert np.allclose(gg, want_g, rtol=1e-4, atol=1e-9)
+    # backward: sampled rows, hubs included
+    gk = g.cpu().numpy().astype(np.float64)
+    dZ = torch.empty((n, F), dtype=torch.float16, device="cuda")
+    bws = torch.empty(G.gcn_pair_backward_workspace_size(n, K, F), dtype=torch.uint8, device="cuda")
+    G.gcn_pair_backward(n, F, F, G.GCN_F16, Z, pu, pv, K, g, dZ, F, ov, bws)
+    torch.cuda.synchronize()
+    cnt = np.bincount(u, minlength=n) + np.bincount(v, minlength=n)
+    rows = np.unique(np.concatenate([np.argsort(cnt)[-5:], rng.choice(n, 40, replace=False),
+                                     np.flatnonzero(cnt == 0)[:3]]))
+    got = dZ[torch.as_tensor(rows).cuda()].float().cpu().numpy().astype(np.float64)
+    want = np.stack([(gk[u == r, None] * zr[v[u == r]]).sum(0) + (gk[v == r, None] * zr[u[v == r]]).sum(0)
+                     for r in rows])
+    assert_close(got, want, G.GCN_F16, "dZ sampled rows at full size")
+    assert ov.item() == 0
