@@ -371,6 +371,12 @@ def cpu_baseline(wl, budget_s):
 
 
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "dense_agg_sbm16k_traffic.md")
+# sources of the kernels whose counters are reported (with the shared
+# device helpers they include)
+DENSE_SOURCES = ("dense_agg.hip", "xpose.h", "common.h")
+SPMM_SOURCES = ("spmm.hip", "normalize.hip", "common.h")
+
+
 def kernel_hash(*files):
     import hashlib
     h = hashlib.sha256()
@@ -433,10 +439,10 @@ def summarize_counters(fetch_dir, write_dir, out_path, command):
     summary = {
         "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
         "dense_agg_f16": int(per_launch),
-        "dense_agg_f16_source_hash": kernel_hash("dense_agg.hip", "xpose.h"),
+        "dense_agg_f16_source_hash": kernel_hash(*DENSE_SOURCES),
         # light, heavy and fixup kernels of one F=hidden and one F=classes aggregation, halved: bytes per launch
         "spmm_f16": int(sum(r[2] + r[3] for r in spmm) / 2),
-        "spmm_f16_source_hash": kernel_hash("spmm.hip", "normalize.hip"),
+        "spmm_f16_source_hash": kernel_hash(*SPMM_SOURCES),
     }
     lines = ["# HBM traffic counters: dense aggregation (SBM n=16384) and CSR aggregation (R-MAT scale 21), fp16", "",
              "Commands (from the repository root, on one MI355X; one counter per run):", "", "```", command, "```", "",
@@ -593,7 +599,7 @@ def main():
     achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9
     traffic = None
     if prec != 0:
-        traffic = load_traffic("dense_agg_f16", "dense_agg.hip", "xpose.h") if spec.dense_adj else load_traffic("spmm_f16", "spmm.hip", "normalize.hip")
+        traffic = load_traffic("dense_agg_f16", *DENSE_SOURCES) if spec.dense_adj else load_traffic("spmm_f16", *SPMM_SOURCES)
     roofline = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(achieved / HBM_PEAK_GBS, 4), traffic=traffic, kernel=kname,
                     launches=r["agg_launches"], avg_launch_us=round(r["agg_ms"] * 1e3 / r["agg_launches"], 2),
@@ -637,7 +643,7 @@ def main():
                     launches=r2["agg_launches"], avg_launch_us=round(r2["agg_ms"] * 1e3 / r2["agg_launches"], 2),
                     algorithmic_bytes_per_launch_avg=int(b2 / 2),
                     gather_bytes_per_launch_avg=int(r2["nnz"] * (r2["f_h"] + r2["C"]) * s / 2),
-                    traffic=load_traffic("spmm_f16", "spmm.hip", "normalize.hip") if prec != 0 and args.spmm_workload == "rmat21" else None,
+                    traffic=load_traffic("spmm_f16", *SPMM_SOURCES) if prec != 0 and args.spmm_workload == "rmat21" else None,
                     peak_mem_bytes=r2["peak_bytes"], gemm=gemm_object(r2, prec, r2["f_in"], r2["f_h"], r2["C"]))
         log(f"[bench] spmm: {spmm['ms_per_step']} ms/epoch, {spmm['achieved']} GB/s algorithmic")
         del wl2

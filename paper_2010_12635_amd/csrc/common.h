@@ -119,8 +119,16 @@ __device__ __forceinline__ bool dropout_keep(const Epilogue& ep, uint64_t e) {
   return philox_word(o, (uint32_t)(e & 7)) >= ep.thr;
 }
 
+// Called by the lanes that saw a non-finite value: the lowest of them
+// reports for its wave, and only if the flag is not set yet, so that a
+// tensor full of NaN or infinity costs one store per wave at most.
 __device__ __forceinline__ void raise_flag(int32_t* flag) {
-  if (flag) *reinterpret_cast<volatile int32_t*>(flag) = 1;
+  if (!flag) return;
+  const uint64_t active = __ballot(1);
+  if ((threadIdx.x & 63) == (unsigned)(__ffsll((unsigned long long)active) - 1)) {
+    volatile int32_t* f = flag;
+    if (*f == 0) *f = 1;
+  }
 }
 
 // Scalar epilogue for one element (row < rows, col < cols).
