@@ -499,6 +499,7 @@ def main():
     ap.add_argument("--prec", default="f16", choices=sorted(PRECS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-fp32", action="store_true", help="skip the fp32-mode run")
+    ap.add_argument("--ba-epochs", type=int, default=100, help="epochs of the Barabasi-Albert workload (0 = skip)")
     ap.add_argument("--seeds", type=int, default=5, help="seeds of the main workload for mean and std (1 = seed 0 only)")
     ap.add_argument("--table1", default="default", choices=sorted(TABLE1_SWEEPS) + ["none"],
                     help="the model-size sweep of the paper's Table 1 (featureless input, dense A_hat)")
@@ -533,15 +534,15 @@ def main():
             summarize_stats(d, out, args.stats_command, title)
             return
         cmd = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_default -o run -- "
-               "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest --no-levels --gae-epochs 0 --table1 none --seeds 1")
+               "python3 bench.py --steps 50 --cpu-seconds 0 --no-largest --no-levels --gae-epochs 0 --table1 none --seeds 1 --ba-epochs 0")
         summarize_stats(d, out, cmd, title)
         return
 
     if args.summarize_counters:
         cmd = ("rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --table1 none --seeds 1 --copy-calibration 256\n"
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --table1 none --seeds 1 --ba-epochs 0 --copy-calibration 256\n"
                "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py "
-               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --table1 none --seeds 1 --copy-calibration 256")
+               "--steps 5 --warmup 1 --no-fp32 --cpu-seconds 0 --spmm-steps 3 --no-largest --no-levels --gae-epochs 0 --table1 none --seeds 1 --ba-epochs 0 --copy-calibration 256")
         print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, cmd)))
         return
 
@@ -623,6 +624,8 @@ def main():
     torch.cuda.synchronize()
     copy_gbs = 5 * 2 * src_t.numel() * 2 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del src_t, dst_t
+    if roofline["traffic"]:
+        roofline["counter_gbs"] = round(roofline["traffic"] / (roofline["avg_launch_us"] * 1e-6) / 1e9, 1)
     roofline["achievable_copy_gbs"] = round(copy_gbs, 1)
     roofline["frac_of_achievable"] = round(roofline["achieved"] / copy_gbs, 4)
 
@@ -684,8 +687,29 @@ def main():
                     gather_bytes_per_launch_avg=int(r2["nnz"] * (r2["f_h"] + r2["C"]) * s / 2),
                     traffic=load_traffic("spmm_f16", *SPMM_SOURCES) if prec != 0 and args.spmm_workload == "rmat21" else None,
                     peak_mem_bytes=r2["peak_bytes"], gemm=gemm_object(r2, prec, r2["f_in"], r2["f_h"], r2["C"]))
+        if spmm["traffic"]:
+            spmm["counter_gbs"] = round(spmm["traffic"] / (spmm["avg_launch_us"] * 1e-6) / 1e9, 1)
+            spmm["counter_frac"] = round(spmm["counter_gbs"] / HBM_PEAK_GBS, 4)
         log(f"[bench] spmm: {spmm['ms_per_step']} ms/epoch, {spmm['achieved']} GB/s algorithmic")
         del wl2
+
+    ba = None
+    if args.ba_epochs > 0:
+        # the sparse Barabasi-Albert workload (n = 200000, m = 8, 128 -> 128 -> 40)
+        log("[bench] ba200k workload: generating")
+        wl4 = I.workload("ba200k", args.seed)
+        rb = run_gpu(wl4, prec, args.ba_epochs, 3, dense=False)
+        rb32 = None if args.no_fp32 else run_gpu(wl4, 0, args.ba_epochs, 3, dense=False)
+        ba = dict(workload=describe(wl4["spec"], rb["n"], rb, args.prec), epochs=args.ba_epochs,
+                  epochs_per_s=round(args.ba_epochs / (rb["gpu_ms"] * 1e-3), 2),
+                  ms_per_step=round(rb["gpu_ms"] / args.ba_epochs, 4), peak_mem_bytes=rb["peak_bytes"],
+                  final_loss=rb["loss"],
+                  fp32=None if rb32 is None else dict(
+                      epochs_per_s=round(args.ba_epochs / (rb32["gpu_ms"] * 1e-3), 2),
+                      ms_per_step=round(rb32["gpu_ms"] / args.ba_epochs, 4), peak_mem_bytes=rb32["peak_bytes"],
+                      final_loss=rb32["loss"]))
+        log(f"[bench] ba200k: {ba['epochs_per_s']} epochs/s (fp32 {ba['fp32'] and ba['fp32']['epochs_per_s']})")
+        del wl4
 
     gae = None
     if args.gae_epochs > 0:
@@ -786,6 +810,7 @@ def main():
         "seeds": seeds,
         "levels": levels,
         "spmm": spmm,
+        "ba200k": ba,
         "gae": gae,
         "table1": table1,
         "largest_graph": largest,
