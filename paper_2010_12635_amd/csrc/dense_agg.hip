@@ -469,6 +469,9 @@ int64_t xt_elems(int prec, int64_t n, int64_t F) {
 #ifndef MM_DEPTH
 #define MM_DEPTH 3
 #endif
+#ifndef MM_SMALL_TILES
+#define MM_SMALL_TILES 256
+#endif
 // The wide-feature kernel takes over from F >= MM_MIN_F (tiled A_hat):
 // 128 x 64 per wave up to F = 384, 128 x 128 above (measured on MI355X at
 // n = 32768: F = 256 0.72 ms against 0.92 ms, F = 2048 3.3 ms against
@@ -492,14 +495,24 @@ hipError_t launch_t(const void* A, int64_t lda, bool tiled, int64_t n, const voi
     q.A = A; q.Xt = Xt; q.n = n; q.F = F; q.nc = nc;
     q.rblocks = (n + 63) / 64;
     q.fblocks = fblocks;
-    const int WC = F > 384 ? 2 : 1;
-    const int64_t rt = (n + 255) / 256;
+    int WR = 2, WC = F > 384 ? 2 : 1;
+#ifndef MM_NO_SMALL
+    // fewer tiles than compute units: step down to 256 x 128, then to
+    // 128 x 128 workgroup tiles, so that more of the chip is busy
+    auto tiles_of = [&](int wr, int wc) { return (n + 128 * wr - 1) / (128 * wr) * ((F + 128 * wc - 1) / (128 * wc)); };
+    if (tiles_of(WR, WC) < MM_SMALL_TILES) {
+      if (WC == 2 && tiles_of(2, 1) >= MM_SMALL_TILES) WC = 1;
+      else WR = WC = 1;
+    }
+#endif
+    const int64_t rt = (n + 128 * WR - 1) / (128 * WR);
     q.cb = (F + 128 * WC - 1) / (128 * WC);
     q.tiles = rt * q.cb;
     q.per_xcd = (q.tiles + 7) / 8;
     q.epi = epi;
     const dim3 g((unsigned)(8 * q.per_xcd));
-    if (WC == 2) hipLaunchKernelGGL((dense_mm_kernel<T, 2, 2, MM_DEPTH>), g, dim3(256), 0, s, q);
+    if (WR == 1) hipLaunchKernelGGL((dense_mm_kernel<T, 1, 1, MM_DEPTH>), g, dim3(256), 0, s, q);
+    else if (WC == 2) hipLaunchKernelGGL((dense_mm_kernel<T, 2, 2, MM_DEPTH>), g, dim3(256), 0, s, q);
     else hipLaunchKernelGGL((dense_mm_kernel<T, 2, 1, 2>), g, dim3(256), 0, s, q);
     return hipGetLastError();
   }

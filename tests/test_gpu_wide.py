@@ -6,9 +6,12 @@ MFMA-bound dense aggregation it leads to.
   with h = I (a dense identity), CSR and tiled dense A_hat, 16-bit and fp32;
   dW = G_S widened, padding zero; the argument checks (f_in != n,
   dZ_below given).
-* The dense aggregation at the benchmark's widest shape (n = 32768,
-  F = 2048, the launch the model-size sweep times): sampled output rows
-  against the oracle's per-row formula."""
+* The dense aggregation at full size, one shape per workgroup tile of the
+  MFMA kernel: the benchmark's widest (n = 32768, F = 2048, the launch the
+  model-size sweep times, 256 x 256 tiles), shapes whose tile count falls
+  below the compute-unit count (256 x 128 and 128 x 128 tiles, ragged n and
+  F), and an fp32 shape: sampled output rows against the oracle's per-row
+  formula."""
 import numpy as np
 import pytest
 import torch
@@ -91,30 +94,36 @@ def test_identity_input_layer(prec, storage, f_out):
         G.gcn_layer_fwd(dg.adj, L_bad, prec, True, None, W, bias, seed, epoch, None, Hout, ov, ws)
 
 
-def test_wide_dense_aggregation_at_full_size():
-    n, F = 32768, 2048
-    print(f"[wide] n={n} F={F} tiled f16", flush=True)
+@pytest.mark.parametrize("n,F,prec", [
+    (32768, 2048, G.GCN_F16),   # 256 x 256 workgroup tiles
+    (16384, 520, G.GCN_BF16),   # 256 x 128: 192 tiles of 256 x 256 would not fill the chip
+    (32768, 256, G.GCN_F32),    # 256 x 128, fp32 MFMA
+    (6000, 1000, G.GCN_F16),    # 128 x 128, ragged rows and columns
+], ids=["n32768_F2048_f16", "n16384_F520_bf16", "n32768_F256_f32", "n6000_F1000_f16"])
+def test_wide_dense_aggregation_at_full_size(n, F, prec):
+    print(f"[wide] n={n} F={F} tiled {PNAME[prec]}", flush=True)
     rng = np.random.default_rng(21)
     src = rng.integers(0, n, 8 * n).astype(np.int32)
     dst = rng.integers(0, n, 8 * n).astype(np.int32)
-    dg = DeviceGraph(n, src, dst, prec=G.GCN_F16, dense=True)
+    dg = DeviceGraph(n, src, dst, prec=prec, dense=True)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(3)
-    X = torch.randn((n, F), generator=gen, device="cuda").half()
+    ld = round8(F)
+    X = torch.randn((n, ld), generator=gen, device="cuda").to(G.torch_dtype(prec))
     Y = torch.empty_like(X)
     bias = torch.as_tensor((0.1 * rng.standard_normal(F)).astype(np.float32)).to(dev())
     ov = torch.zeros(1, dtype=torch.int32, device=dev())
-    ws = torch.empty(G.gcn_aggregate_workspace_size(dg.adj, F, G.GCN_F16), dtype=torch.uint8, device=dev())
-    G.gcn_aggregate(dg.adj, F, G.GCN_F16, X, F, bias, G.GCN_ACT_RELU, 0.0, 0, 0, 0, 0, Y, F, ov, ws)
+    ws = torch.empty(G.gcn_aggregate_workspace_size(dg.adj, F, prec), dtype=torch.uint8, device=dev())
+    G.gcn_aggregate(dg.adj, F, prec, X, ld, bias, G.GCN_ACT_RELU, 0.0, 0, 0, 0, 0, Y, ld, ov, ws)
     torch.cuda.synchronize()
     deg = O.graph_degrees(n, src, dst)
     rows = np.unique(np.concatenate([[0, 255, 256, n - 1], rng.choice(n, 60, replace=False)]))
     nbrs = O.graph_rows(n, src, dst, rows)
     d = 1.0 / np.sqrt(deg.astype(np.float64))
     need = np.unique(np.concatenate([nbrs[int(r)] for r in rows]))
-    xs = dict(zip(need.tolist(), X[torch.as_tensor(need).cuda()].float().cpu().numpy().astype(np.float64)))
+    xs = dict(zip(need.tolist(), X[torch.as_tensor(need).cuda(), :F].float().cpu().numpy().astype(np.float64)))
     bh = bias.cpu().numpy().astype(np.float64)
     want = np.stack([np.maximum(sum(d[r] * d[c] * xs[int(c)] for c in nbrs[int(r)]) + bh, 0.0) for r in rows])
-    got = Y[torch.as_tensor(rows).cuda()].float().cpu().numpy().astype(np.float64)
-    assert_close(got, want, G.GCN_F16, "Y sampled rows at n = 32768, F = 2048")
+    got = Y[torch.as_tensor(rows).cuda(), :F].float().cpu().numpy().astype(np.float64)
+    assert_close(got, want, prec, f"Y sampled rows at n = {n}, F = {F}")
     assert int(ov.item()) == 0
