@@ -70,6 +70,33 @@ __device__ __forceinline__ void gather_block(float* acc, const T* __restrict__ X
   for (int u = 0; u < U; ++u) fma_vec<T>(acc, v[u], x[u]);
 }
 
+// Entries e .. end - 1 (fewer than U) of a row in one round: every load is
+// issued at an in-bounds index (past the end: the row's last entry again)
+// and only the terms of real entries are added, in entry order, so the sum
+// is the one that U single steps give.  The add is selected rather than
+// scaled by zero, which a non-finite neighbour row would turn into NaN.
+template <typename T, bool HAS_VAL, int U>
+__device__ __forceinline__ void gather_tail(float* acc, const T* __restrict__ X, int64_t ldx, const int32_t* __restrict__ colidx,
+                                            const void* values, const float* dinv, float drow, int64_t e, int64_t end) {
+  int32_t c[U];
+  uint4 x[U];
+  float v[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) c[u] = colidx[e + u < end ? e + u : end - 1];
+#pragma unroll
+  for (int u = 0; u < U; ++u) x[u] = ldg16(X + (int64_t)c[u] * ldx);
+#pragma unroll
+  for (int u = 0; u < U; ++u) v[u] = edge_value<T, HAS_VAL>(values, dinv, drow, e + u < end ? e + u : end - 1, c[u]);
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    float xs[Vec<T>::N];
+    unpack<T>(x[u], xs);
+    const bool live = e + u < end;
+#pragma unroll
+    for (int i = 0; i < Vec<T>::N; ++i) acc[i] = live ? fmaf(v[u], xs[i], acc[i]) : acc[i];
+  }
+}
+
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
   constexpr int VE = Vec<T>::N;
@@ -91,11 +118,20 @@ __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
     for (int i = 0; i < VE; ++i) acc[i] = 0.f;
     int64_t e = beg;
     for (; e + 8 <= end; e += 8) gather_block<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-    if (e + 4 <= end) {
-      gather_block<T, HAS_VAL, 4>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-      e += 4;
+    if constexpr (LPR * Vec<T>::N * (int)sizeof(T) <= 256) {
+      // neighbour rows of at most 256 bytes: the walk is bound by dependent
+      // load latency, so the last 1 .. 7 entries go in one round rather than
+      // a round of 4 and single steps (up to 5 dependent rounds)
+      if (e < end) gather_tail<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, end);
+    } else {
+      // wider rows are bound by the gathered bytes, which the in-bounds
+      // repeats of a one-round tail would add to
+      if (e + 4 <= end) {
+        gather_block<T, HAS_VAL, 4>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
+        e += 4;
+      }
+      for (; e < end; ++e) gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
     }
-    for (; e < end; ++e) gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
     epi_store_vec<T>(p.epi, row, col0, acc);
   }
 }
