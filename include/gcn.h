@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 5
+#define GCN_ABI_VERSION 6
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -415,9 +415,13 @@ gcn_status gcn_pair_backward(int64_t n, int64_t F, int64_t ld, int32_t prec, con
  * scores (scores[0 .. n_pos) positives, then n_neg negatives; all finite):
  *   auc_ap[0] = AUC = #{(i, j): s_i > s_j} + #{s_i == s_j} / 2, over P x N, divided by P N;
  *   auc_ap[1] = AP  = mean over positives i of #{pos with s >= s_i} / #{all with s >= s_i}.
- * Exact counts (O(P (P + N)) comparisons), fixed-order sums; auc_ap is a
- * device array of 2 doubles.  workspace: gcn_pair_metrics_workspace_size(). */
-gcn_status gcn_pair_metrics_workspace_size(int64_t n_pos, size_t* bytes);
+ * Exact counts from one sort of the P + N scores (-0 and +0 are equal), a
+ * count of the negatives before every sorted position and two binary
+ * searches per positive: O((P + N) log(P + N)); fixed-order sums.  auc_ap is
+ * a device array of 2 doubles.  n_pos + n_neg <= 2^31 - 1, else
+ * GCN_ERR_SHAPE.  workspace: gcn_pair_metrics_workspace_size(), about
+ * 32 (P + N) bytes. */
+gcn_status gcn_pair_metrics_workspace_size(int64_t n_pos, int64_t n_neg, size_t* bytes);
 gcn_status gcn_pair_metrics(const float* scores, int64_t n_pos, int64_t n_neg, double* auc_ap,
                             void* workspace, size_t workspace_bytes, void* stream);
 

@@ -615,19 +615,19 @@ gcn_status gcn_pair_backward(int64_t n, int64_t F, int64_t ld, int32_t prec, con
   return finish(hipSuccess, s);
 }
 
-gcn_status gcn_pair_metrics_workspace_size(int64_t n_pos, size_t* bytes) {
+gcn_status gcn_pair_metrics_workspace_size(int64_t n_pos, int64_t n_neg, size_t* bytes) {
   if (!bytes) return GCN_ERR_INVALID_ARG;
-  if (n_pos <= 0) return GCN_ERR_SHAPE;
-  *bytes = pair_metrics_workspace_bytes(n_pos);
+  if (n_pos <= 0 || n_neg <= 0 || n_pos + n_neg > INT32_MAX) return GCN_ERR_SHAPE;
+  *bytes = pair_metrics_workspace_bytes(n_pos, n_neg);
   return GCN_OK;
 }
 
 gcn_status gcn_pair_metrics(const float* scores, int64_t n_pos, int64_t n_neg, double* auc_ap, void* workspace,
                             size_t workspace_bytes, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (n_pos <= 0 || n_neg <= 0) return GCN_ERR_SHAPE;
+  if (n_pos <= 0 || n_neg <= 0 || n_pos + n_neg > INT32_MAX) return GCN_ERR_SHAPE;
   if (!scores || !auc_ap) return GCN_ERR_INVALID_ARG;
-  if (!workspace || workspace_bytes < pair_metrics_workspace_bytes(n_pos)) return GCN_ERR_WORKSPACE;
+  if (!workspace || workspace_bytes < pair_metrics_workspace_bytes(n_pos, n_neg)) return GCN_ERR_WORKSPACE;
   if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
   GCN_HIP(pair_metrics_launch(scores, n_pos, n_neg, auc_ap, workspace, s));
   return finish(hipSuccess, s);

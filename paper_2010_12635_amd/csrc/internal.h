@@ -158,7 +158,7 @@ size_t pair_backward_workspace_bytes(int64_t n, int64_t n_pairs, int64_t F);
 hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, const void* Z, const int32_t* pair_u,
                                 const int32_t* pair_v, int64_t n_pairs, const float* g, void* dZ, int64_t ldz,
                                 int32_t* flag, void* ws, hipStream_t s);
-size_t pair_metrics_workspace_bytes(int64_t n_pos);
+size_t pair_metrics_workspace_bytes(int64_t n_pos, int64_t n_neg);
 hipError_t pair_metrics_launch(const float* scores, int64_t n_pos, int64_t n_neg, double* auc_ap, void* ws,
                                hipStream_t s);
 

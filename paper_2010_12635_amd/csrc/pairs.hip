@@ -15,9 +15,12 @@
 //    inside it and a fix-up pass adds the partial sums of rows that cross
 //    segment ends, in segment order: dZ is run-to-run identical without
 //    floating-point atomics, and hub rows no longer serialise on one group.
-//  * pair_metrics_kernel: exact AUC and AP of held-out pairs by counting,
-//    for every positive, the scores below / equal / above it (O(P (P + N))
-//    comparisons through LDS tiles), then fixed-order sums.
+//  * pair metrics: exact AUC and AP of held-out pairs.  The scores are
+//    sorted once (the same stable radix sort, on order-preserving 32-bit
+//    keys), the negatives before every position are counted by a scan, and
+//    every positive finds the ends of its run of equal scores by binary
+//    search: negatives below / equal and all scores >= it follow from the
+//    counts at those ends, O((P + N) log(P + N)) in all.  Fixed-order sums.
 #include "internal.h"
 
 namespace gcn {
@@ -466,34 +469,66 @@ hipError_t pair_segments_t(SegParams p, int lpr, hipStream_t s) {
 }
 
 // ---- metrics
-constexpr int MT_TILE = 2048;
 
-__global__ __launch_bounds__(256) void pair_metrics_kernel(const float* __restrict__ scores, int64_t P, int64_t N,
-                                                           unsigned long long* __restrict__ auc_part,
-                                                           double* __restrict__ ap_part) {
-  __shared__ float tile[MT_TILE];
+// Order-preserving key of a finite score: unsigned comparison of the keys
+// agrees with < on the floats; -0 is taken as +0 (the two compare equal).
+__device__ __forceinline__ uint32_t score_key(float x) {
+  uint32_t b = __float_as_uint(x);
+  if (b == 0x80000000u) b = 0u;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Sort input: key, positive flag and index of each of the P + N scores.
+__global__ __launch_bounds__(256) void metrics_prep_kernel(const float* __restrict__ scores, int64_t P, int64_t total,
+                                                           int32_t* __restrict__ key, int32_t* __restrict__ pos,
+                                                           int32_t* __restrict__ idx) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    key[i] = (int32_t)score_key(scores[i]);
+    pos[i] = i < P ? 1 : 0;
+    idx[i] = (int32_t)i;
+  }
+}
+
+// cnt[j] = 1 for a negative at sorted position j, cnt[total] = 0; an
+// exclusive scan then gives the negatives before every position.
+__global__ __launch_bounds__(256) void metrics_negflag_kernel(const int32_t* __restrict__ pos, int64_t total,
+                                                              int64_t* __restrict__ cnt) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j <= total; j += (int64_t)gridDim.x * blockDim.x)
+    cnt[j] = j < total ? 1 - pos[j] : 0;
+}
+
+// For the positive at sorted position j with key k: lo = first position
+// with key k, hi = first position past them (binary searches).  Negatives
+// below: neg[lo]; equal: neg[hi] - neg[lo]; scores >= s: total - lo, of
+// which positives: P - (lo - neg[lo]).  Sums per workgroup in position order.
+__global__ __launch_bounds__(256) void metrics_count_kernel(const int32_t* __restrict__ key,
+                                                            const int32_t* __restrict__ pos,
+                                                            const int64_t* __restrict__ neg, int64_t P, int64_t total,
+                                                            unsigned long long* __restrict__ auc_part,
+                                                            double* __restrict__ ap_part) {
   __shared__ double sd[256];
   __shared__ unsigned long long su[256];
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const float si = i < P ? scores[i] : 0.f;
-  unsigned long long pos_ge = 0, neg_ge = 0, auc2 = 0;   // auc2 = 2 * #{neg < s_i} + #{neg == s_i}
-  const int64_t total = P + N;
-  for (int64_t t0 = 0; t0 < total; t0 += MT_TILE) {
-    const int64_t len = total - t0 < MT_TILE ? total - t0 : MT_TILE;
-    __syncthreads();
-    for (int j = threadIdx.x; j < len; j += 256) tile[j] = scores[t0 + j];
-    __syncthreads();
-    const int64_t npos = P - t0 <= 0 ? 0 : (P - t0 < len ? P - t0 : len);   // tile entries that are positives
-    for (int j = 0; j < npos; ++j) pos_ge += tile[j] >= si ? 1ull : 0ull;
-    for (int j = (int)npos; j < len; ++j) {
-      const float sj = tile[j];
-      neg_ge += sj >= si ? 1ull : 0ull;
-      auc2 += sj < si ? 2ull : (sj == si ? 1ull : 0ull);
-    }
-  }
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
   double ap = 0.0;
-  if (i < P) ap = (double)pos_ge / (double)(pos_ge + neg_ge);
-  else auc2 = 0;
+  unsigned long long auc2 = 0;
+  if (j < total && pos[j]) {
+    const uint32_t k = (uint32_t)key[j];
+    int64_t a = 0, b = j;                           // first position in [0, j] with key >= k
+    while (a < b) {
+      const int64_t m = a + (b - a) / 2;
+      if ((uint32_t)key[m] < k) a = m + 1; else b = m;
+    }
+    const int64_t lo = a;
+    a = j + 1; b = total;                           // first position in [j + 1, total) with key > k
+    while (a < b) {
+      const int64_t m = a + (b - a) / 2;
+      if ((uint32_t)key[m] <= k) a = m + 1; else b = m;
+    }
+    const int64_t hi = a;
+    const int64_t nlo = neg[lo], nhi = neg[hi];
+    auc2 = 2ull * (unsigned long long)nlo + (unsigned long long)(nhi - nlo);
+    ap = (double)(P - (lo - nlo)) / (double)(total - lo);
+  }
   sd[threadIdx.x] = ap;
   su[threadIdx.x] = auc2;
   __syncthreads();
@@ -690,21 +725,76 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
   return hipSuccess;
 }
 
-size_t pair_metrics_workspace_bytes(int64_t n_pos) {
-  const int64_t nb = (n_pos + 255) / 256;
-  return align256(sizeof(double) * nb) + align256(sizeof(unsigned long long) * nb);
+namespace {
+struct MetricsLayout {
+  int32_t *kA, *pA, *iA, *kB, *pB, *iB;
+  int64_t *hist, *scr, *neg;
+  double* ap_part;
+  unsigned long long* auc_part;
+  size_t bytes;
+};
+// Carves the workspace (ws may be NULL to size it).
+MetricsLayout metrics_layout(int64_t total, void* ws) {
+  const int64_t nblk = (total + RS_TILE - 1) / RS_TILE;
+  const int64_t nh = ((int64_t)1 << RS_MAX_BITS) * (nblk < 1 ? 1 : nblk);
+  const int64_t nb = (total + 255) / 256;
+  const int64_t scan_n = nh > total + 1 ? nh : total + 1;
+  MetricsLayout L;
+  char* base = static_cast<char*>(ws);
+  size_t o = 0;
+  auto take = [&](size_t bytes) { char* q = base ? base + o : nullptr; o += align256(bytes); return q; };
+  const size_t tb = sizeof(int32_t) * total;
+  L.kA = (int32_t*)take(tb); L.pA = (int32_t*)take(tb); L.iA = (int32_t*)take(tb);
+  L.kB = (int32_t*)take(tb); L.pB = (int32_t*)take(tb); L.iB = (int32_t*)take(tb);
+  L.hist = (int64_t*)take(sizeof(int64_t) * nh);
+  L.scr = (int64_t*)take(sizeof(int64_t) * segment_scan_scratch_elems(scan_n));
+  L.neg = (int64_t*)take(sizeof(int64_t) * (total + 1));
+  L.ap_part = (double*)take(sizeof(double) * nb);
+  L.auc_part = (unsigned long long*)take(sizeof(unsigned long long) * nb);
+  L.bytes = o;
+  return L;
+}
+}  // namespace
+
+size_t pair_metrics_workspace_bytes(int64_t n_pos, int64_t n_neg) {
+  return metrics_layout(n_pos + n_neg, nullptr).bytes;
 }
 
 hipError_t pair_metrics_launch(const float* scores, int64_t n_pos, int64_t n_neg, double* auc_ap, void* ws,
                                hipStream_t s) {
-  const int64_t nb = (n_pos + 255) / 256;
-  double* ap_part = reinterpret_cast<double*>(ws);
-  unsigned long long* auc_part =
-      reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) + align256(sizeof(double) * nb));
-  hipLaunchKernelGGL(pair_metrics_kernel, dim3((unsigned)nb), dim3(256), 0, s, scores, n_pos, n_neg, auc_part, ap_part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(pair_metrics_final_kernel, dim3(1), dim3(256), 0, s, auc_part, ap_part, nb, n_pos, n_neg, auc_ap);
+  const int64_t total = n_pos + n_neg;
+  const MetricsLayout L = metrics_layout(total, ws);
+  const int64_t nblk = (total + RS_TILE - 1) / RS_TILE;
+  const int64_t nb = (total + 255) / 256;
+  const unsigned gb = (unsigned)capped_blocks(total + 1, 256);
+  hipError_t e;
+#define GCN_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
+  hipLaunchKernelGGL(metrics_prep_kernel, dim3(gb), dim3(256), 0, s, scores, n_pos, total, L.kA, L.pA, L.iA);
+  GCN_TRY(hipGetLastError());
+  // four stable 8-bit passes over the 32-bit keys: A -> B -> A -> B -> A
+  int32_t *kin = L.kA, *pin = L.pA, *iin = L.iA, *kout = L.kB, *pout = L.pB, *iout = L.iB;
+  for (int shift = 0; shift < 32; shift += RS_MAX_BITS) {
+    hipLaunchKernelGGL(rs_hist_kernel<RS_MAX_BITS>, dim3((unsigned)nblk), dim3(256), 0, s, (int64_t)0, nullptr, nullptr,
+                       kin, total, shift, nblk, L.hist);
+    GCN_TRY(hipGetLastError());
+    GCN_TRY(segment_scan_exclusive(L.hist, ((int64_t)1 << RS_MAX_BITS) * nblk, L.scr, s));
+    hipLaunchKernelGGL(rs_scatter_kernel<RS_MAX_BITS>, dim3((unsigned)nblk), dim3(256), 0, s, (int64_t)0, nullptr,
+                       nullptr, kin, pin, iin, total, shift, nblk, L.hist, kout, pout, iout);
+    GCN_TRY(hipGetLastError());
+    int32_t* t;
+    t = kin; kin = kout; kout = t;
+    t = pin; pin = pout; pout = t;
+    t = iin; iin = iout; iout = t;
+  }
+  hipLaunchKernelGGL(metrics_negflag_kernel, dim3(gb), dim3(256), 0, s, pin, total, L.neg);
+  GCN_TRY(hipGetLastError());
+  GCN_TRY(segment_scan_exclusive(L.neg, total + 1, L.scr, s));
+  hipLaunchKernelGGL(metrics_count_kernel, dim3((unsigned)nb), dim3(256), 0, s, kin, pin, L.neg, n_pos, total,
+                     L.auc_part, L.ap_part);
+  GCN_TRY(hipGetLastError());
+  hipLaunchKernelGGL(pair_metrics_final_kernel, dim3(1), dim3(256), 0, s, L.auc_part, L.ap_part, nb, n_pos, n_neg,
+                     auc_ap);
+#undef GCN_TRY
   return hipGetLastError();
 }
 

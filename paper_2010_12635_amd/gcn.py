@@ -137,7 +137,7 @@ def lib():
         "gcn_pair_loss": (I32, [I64, I64, I64, I32, P, P, P, I64, I64, P, P, P, P, P, P, SZ, P]),
         "gcn_pair_backward_workspace_size": (I32, [I64, I64, I64, PSZ]),
         "gcn_pair_backward": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, I64, P, P, SZ, P]),
-        "gcn_pair_metrics_workspace_size": (I32, [I64, PSZ]),
+        "gcn_pair_metrics_workspace_size": (I32, [I64, I64, PSZ]),
         "gcn_pair_metrics": (I32, [P, I64, I64, P, P, SZ, P]),
         "gcn_cast": (I32, [I64, I64, I32, P, I64, I32, P, I64, P, P]),
         "gcn_optimizer_step_half": (I32, [I64, P, P, P, P, P, I32, ctypes.POINTER(GcnAdamConfig), P, P, P]),
@@ -342,9 +342,9 @@ def gcn_pair_backward(n, F, ld, prec, Z, pair_u, pair_v, n_pairs, g, dZ, ldz, ov
     _check(st, "gcn_pair_backward")
 
 
-def gcn_pair_metrics_workspace_size(n_pos) -> int:
+def gcn_pair_metrics_workspace_size(n_pos, n_neg) -> int:
     b = ctypes.c_size_t(0)
-    _check(lib().gcn_pair_metrics_workspace_size(n_pos, ctypes.byref(b)), "gcn_pair_metrics_workspace_size")
+    _check(lib().gcn_pair_metrics_workspace_size(n_pos, n_neg, ctypes.byref(b)), "gcn_pair_metrics_workspace_size")
     return b.value
 
 

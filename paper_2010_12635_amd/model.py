@@ -482,7 +482,7 @@ class GAE2:
         G.gcn_pair_loss(self.n, self.f_e, self.ld_e, self.prec, self.Z, tu, tv, n_test_pos, k - n_test_pos, None,
                         loss, scores, g, flag, ws, stream)
         out = torch.empty(2, dtype=torch.float64, device=dev)
-        mws = torch.empty(G.gcn_pair_metrics_workspace_size(n_test_pos), dtype=torch.uint8, device=dev)
+        mws = torch.empty(G.gcn_pair_metrics_workspace_size(n_test_pos, k - n_test_pos), dtype=torch.uint8, device=dev)
         G.gcn_pair_metrics(scores, n_test_pos, k - n_test_pos, out, mws, stream)
         auc, ap = out.cpu().tolist()
         return auc, ap, float(loss.item())

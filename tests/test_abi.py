@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert G.gcn_abi_version() == 5
+    assert G.gcn_abi_version() == 6
     assert G.gcn_status_string(0) == "GCN_OK"
     for s in range(1, 9):
         assert G.gcn_status_string(s).startswith("GCN_ERR_")
@@ -55,6 +55,13 @@ def test_workspace_queries():
         G.gcn_normalize_workspace_size(0, 10)
     with pytest.raises(G.GcnError):
         G.gcn_loss_workspace_size(10, 0)
+    # link-prediction metrics: one sort of all P + N scores (int32 positions)
+    small, big = G.gcn_pair_metrics_workspace_size(10, 20), G.gcn_pair_metrics_workspace_size(1000, 2000)
+    assert 0 < small < big and big >= 24 * 3000
+    for p, q in ((0, 5), (5, 0), (1 << 30, 1 << 30)):
+        with pytest.raises(G.GcnError) as e:
+            G.gcn_pair_metrics_workspace_size(p, q)
+        assert e.value.status == 2          # GCN_ERR_SHAPE
 
 
 def _adj(n=100, fmt=G.GCN_CSR):

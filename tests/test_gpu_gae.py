@@ -178,19 +178,45 @@ def test_pair_invalid_ids_are_skipped():
     assert_close(dZ.cpu().numpy().astype(np.float64), want, G.GCN_F32, "dZ with skipped pairs")
 
 
-@pytest.mark.parametrize("P,N", [(1000, 1500), (37, 5), (300, 300)])
+@pytest.mark.parametrize("P,N", [(1000, 1500), (37, 5), (300, 300), (4000, 6003), (1, 1)])
 def test_pair_metrics_match_oracle(P, N):
     rng = np.random.default_rng(46 + P)
     sp = np.round(rng.standard_normal(P) + 0.8, 1).astype(np.float32)   # rounded: ties
     sn = np.round(rng.standard_normal(N), 1).astype(np.float32)
     scores = dev(np.concatenate([sp, sn]))
     out = torch.empty(2, dtype=torch.float64, device="cuda")
-    ws = torch.empty(G.gcn_pair_metrics_workspace_size(P), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(G.gcn_pair_metrics_workspace_size(P, N), dtype=torch.uint8, device="cuda")
     G.gcn_pair_metrics(scores, P, N, out, ws)
     auc, ap = out.cpu().tolist()
     auc_o, ap_o = O.auc_ap(sp.astype(np.float64), sn.astype(np.float64))
     assert auc == auc_o                    # an exact count over P x N
     assert abs(ap - ap_o) <= 1e-12
+
+
+def _metrics(sp, sn):
+    P, N = sp.size, sn.size
+    scores = dev(np.concatenate([sp, sn]).astype(np.float32))
+    out = torch.empty(2, dtype=torch.float64, device="cuda")
+    ws = torch.empty(G.gcn_pair_metrics_workspace_size(P, N), dtype=torch.uint8, device="cuda")
+    G.gcn_pair_metrics(scores, P, N, out, ws)
+    return out.cpu().tolist()
+
+
+def test_pair_metrics_ties_signed_zero_and_extremes():
+    # every score equal: AUC 1/2, AP = P / (P + N)
+    auc, ap = _metrics(np.full(70, 0.25, np.float32), np.full(130, 0.25, np.float32))
+    assert auc == 0.5 and abs(ap - 70 / 200) <= 1e-15
+    # -0 and +0 are equal scores; negative, denormal and large magnitudes order as floats
+    sp = np.array([-0.0, 0.0, 1e-42, -1e-42, 3.0e38, -2.5, 7.0], np.float32)
+    sn = np.array([0.0, -0.0, -1e-42, 2e-42, -3.0e38, -2.5, 7.0, 6.999999], np.float32)
+    auc, ap = _metrics(sp, sn)
+    auc_o, ap_o = O.auc_ap(sp.astype(np.float64), sn.astype(np.float64))
+    assert auc == auc_o and abs(ap - ap_o) <= 1e-12
+    # perfect and reversed separation
+    assert _metrics(np.array([2.0, 3.0], np.float32), np.array([-1.0, 0.5, 1.0], np.float32)) == [1.0, 1.0]
+    auc, ap = _metrics(np.array([-2.0, -3.0], np.float32), np.array([-1.0, 0.5, 1.0], np.float32))
+    auc_o, ap_o = O.auc_ap(np.array([-2.0, -3.0]), np.array([-1.0, 0.5, 1.0]))
+    assert auc == 0.0 and abs(ap - ap_o) <= 1e-15
 
 
 @pytest.mark.parametrize("prec", [G.GCN_F32, G.GCN_F16], ids=lambda p: PNAME[p])
