@@ -208,13 +208,16 @@ __global__ __launch_bounds__(256) void rs_hist_kernel(int64_t n, const int32_t* 
   for (int d = threadIdx.x; d < DIGITS; d += 256) cnt[d] = 0;
   __syncthreads();
   const int64_t base = (int64_t)blockIdx.x * RS_TILE;
+  int32_t ks[RS_IPT];                               // all loads first (clamped indices)
+#pragma unroll
   for (int r = 0; r < RS_IPT; ++r) {
-    const int64_t i = base + r * 256 + threadIdx.x;
-    if (i < total) {
-      const int32_t k = keys ? keys[i] : entry_key(n, pu, pv, i);
-      atomicAdd(&cnt[(k >> shift) & (DIGITS - 1)], 1);
-    }
+    int64_t i = base + r * 256 + threadIdx.x;
+    i = i < total ? i : total - 1;
+    ks[r] = keys ? keys[i] : entry_key(n, pu, pv, i);
   }
+#pragma unroll
+  for (int r = 0; r < RS_IPT; ++r)
+    if (base + r * 256 + threadIdx.x < total) atomicAdd(&cnt[(ks[r] >> shift) & (DIGITS - 1)], 1);
   __syncthreads();
   for (int d = threadIdx.x; d < DIGITS; d += 256) hist[(int64_t)d * nblk + blockIdx.x] = cnt[d];
 }
@@ -222,7 +225,11 @@ __global__ __launch_bounds__(256) void rs_hist_kernel(int64_t n, const int32_t* 
 // Stable scatter of one tile: items are ranked round by round (256
 // consecutive items per round, thread order = item order); inside a wave
 // the lanes with the same digit are found with 8 ballots, across the four
-// waves through per-wave counts in LDS stamped with the round.
+// waves through per-wave counts in LDS stamped with the round.  The ranked
+// items are first placed in LDS in the tile's own digit order, then written
+// out digit run by digit run, so that neighbouring lanes store to
+// neighbouring addresses (placed straight at their global positions, every
+// lane of a store would hit another cache line).
 // Each item carries its pair index k and the other endpoint of the pair.
 template <int BITS>
 __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_t* __restrict__ pu,
@@ -233,34 +240,65 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
                                                          const int64_t* __restrict__ off, int32_t* __restrict__ kout,
                                                          int32_t* __restrict__ vout, int32_t* __restrict__ oout) {
   constexpr int DIGITS = 1 << BITS;
+  static_assert(DIGITS == 256, "one digit per thread");
   __shared__ int cnt[4][DIGITS];                    // (round << 16) | count
   __shared__ int run[DIGITS];
+  __shared__ int toff[DIGITS];                      // first slot of each digit in the tile
+  __shared__ int wsum[4];
   __shared__ int64_t dbase[DIGITS];
+  __shared__ int32_t lk[RS_TILE], lv[RS_TILE], lo[RS_TILE];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int d = threadIdx.x; d < DIGITS; d += 256) {
+  const int64_t base = (int64_t)blockIdx.x * RS_TILE;
+  // every item of the tile is requested before the first round: the rounds
+  // are separated by barriers, and loads issued round by round would cost a
+  // memory latency each (indices past the end read the last item, unused)
+  int32_t ks[RS_IPT], vs[RS_IPT], os[RS_IPT];
+#pragma unroll
+  for (int r = 0; r < RS_IPT; ++r) {
+    int64_t i = base + r * 256 + threadIdx.x;
+    i = i < total ? i : total - 1;
+    if (kin) {
+      ks[r] = kin[i];
+      vs[r] = vin[i];
+      os[r] = oin[i];
+    } else {                                        // first pass: items in pair order
+      ks[r] = entry_key(n, pu, pv, i);
+      vs[r] = (int32_t)(i >> 1);
+      os[r] = (i & 1) ? pu[i >> 1] : pv[i >> 1];
+    }
+  }
+  {
+    // thread d: the global start of digit d for this tile, and the tile's
+    // count of digit d (difference of consecutive entries of the scanned
+    // digit-major histogram); an exclusive scan of the counts gives toff
+    const int d = threadIdx.x;
+    const int64_t L = (int64_t)d * nblk + blockIdx.x;
+    const int64_t b0 = off[L];
+    const int64_t b1 = L + 1 < (int64_t)DIGITS * nblk ? off[L + 1] : total;
+    const int c = (int)(b1 - b0);
     run[d] = 0;
-    dbase[d] = off[(int64_t)d * nblk + blockIdx.x];
+    dbase[d] = b0;
 #pragma unroll
     for (int w = 0; w < 4; ++w) cnt[w][d] = -1;     // stamp -1: no round yet
+    int x = c;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    toff[d] = before + x - c;
   }
   __syncthreads();
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  const int64_t base = (int64_t)blockIdx.x * RS_TILE;
+#pragma unroll
   for (int r = 0; r < RS_IPT; ++r) {
     const int64_t i = base + r * 256 + threadIdx.x;
     const bool valid = i < total;
-    int32_t k = 0, val = 0, oth = 0;
-    if (valid) {
-      if (kin) {
-        k = kin[i];
-        val = vin[i];
-        oth = oin[i];
-      } else {                                      // first pass: items in pair order
-        k = entry_key(n, pu, pv, i);
-        val = (int32_t)(i >> 1);
-        oth = (i & 1) ? pu[i >> 1] : pv[i >> 1];
-      }
-    }
+    const int32_t k = valid ? ks[r] : 0, val = vs[r], oth = os[r];
     const int d = (k >> shift) & (DIGITS - 1);
     uint64_t m = __ballot(valid);
 #pragma unroll
@@ -277,13 +315,14 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
         const int c = cnt[w][d];
         if ((c >> 16) == r) before += c & 0xFFFF;
       }
-      const int64_t pos = dbase[d] + run[d] + before + rank;
-      kout[pos] = k;
-      vout[pos] = val;
-      oout[pos] = oth;
+      const int slot = toff[d] + run[d] + before + rank;
+      lk[slot] = k;
+      lv[slot] = val;
+      lo[slot] = oth;
     }
     __syncthreads();
-    for (int dd = threadIdx.x; dd < DIGITS; dd += 256) {
+    {
+      const int dd = threadIdx.x;
       int add = 0;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
@@ -293,6 +332,17 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
       run[dd] += add;
     }
     __syncthreads();
+  }
+  // slot j of the tile holds the (j - toff[d])-th item of digit d
+  const int64_t rest = total - base;
+  const int tile_n = rest < RS_TILE ? (int)rest : RS_TILE;
+  for (int j = threadIdx.x; j < tile_n; j += 256) {
+    const int32_t k = lk[j];
+    const int d = (k >> shift) & (DIGITS - 1);
+    const int64_t pos = dbase[d] + (j - toff[d]);
+    kout[pos] = k;
+    vout[pos] = lv[j];
+    oout[pos] = lo[j];
   }
 }
 
