@@ -236,16 +236,18 @@ hipError_t launch_typed(const GemmCall& c, const GemmParams& p, hipStream_t s) {
 
 // ------------------------------------------------------------ reductions ----
 
-// 64 output elements per workgroup; 4 lane groups each sum every 4th split
-// (in split order), then the 4 group sums are added in group order.
-// One reduction: 64 outputs per workgroup, 4 groups of splits each walking
-// its splits in order, then the 4 group sums added in group order.
-template <typename T>
-__device__ __forceinline__ void reduce_body(const RedJob& j, int64_t blk) {
-  __shared__ float red[4][64];
+// One reduction: OPW outputs per workgroup and NG = 256 / OPW groups of
+// splits; group g walks splits g, g + NG, ... in order, then the group sums
+// are added in group order.  Few outputs with many splits (the column sums
+// of a long matrix) take small OPW, so that no thread walks a long chain of
+// dependent loads.
+template <typename T, int OPW>
+__device__ __forceinline__ void reduce_body_t(const RedJob& j, int64_t blk) {
+  constexpr int NG = 256 / OPW;
+  __shared__ float red[NG][OPW];
   const int64_t total = j.M * j.width;
-  const int64_t idx = blk * 64 + (threadIdx.x & 63);
-  const int g = threadIdx.x >> 6;
+  const int t = threadIdx.x % OPW, g = threadIdx.x / OPW;
+  const int64_t idx = blk * OPW + t;
   const int64_t r = idx / j.width, c = idx % j.width;
   const bool live = idx < total && c < j.N;
   float a = 0.f;
@@ -253,20 +255,25 @@ __device__ __forceinline__ void reduce_body(const RedJob& j, int64_t blk) {
     const float* q = j.part + r * j.N + c;
     const int64_t stride = j.M * j.N;
 #pragma unroll 8
-    for (int sidx = g; sidx < j.splits; sidx += 4) a += q[(int64_t)sidx * stride];
+    for (int sidx = g; sidx < j.splits; sidx += NG) a += q[(int64_t)sidx * stride];
   }
-  red[g][threadIdx.x & 63] = a;
+  red[g][t] = a;
   __syncthreads();
   if (g != 0 || idx >= total) return;
   if (c >= j.N) {   // EPI_F32 padding columns
     reinterpret_cast<float*>(j.ep.out)[r * j.ep.ldo + c] = 0.f;
     return;
   }
-  const int t = threadIdx.x & 63;
-  float sum = red[0][t] + red[1][t];
-  sum += red[2][t];
-  sum += red[3][t];
+  float sum = red[0][t];
+  for (int k = 1; k < NG; ++k) sum += red[k][t];
   epi_store1<T>(j.ep, r, c, sum);
+}
+
+template <typename T>
+__device__ __forceinline__ void reduce_body(const RedJob& j, int64_t blk) {
+  if (j.opw == 4) reduce_body_t<T, 4>(j, blk);
+  else if (j.opw == 16) reduce_body_t<T, 16>(j, blk);
+  else reduce_body_t<T, 64>(j, blk);
 }
 
 // Up to two independent reductions in one launch: blocks [0, j0.blocks)
@@ -346,7 +353,9 @@ RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const E
   RedJob j;
   j.part = partials; j.splits = splits; j.M = M; j.N = N; j.ep = epi;
   j.width = epi.mode == EPI_F32 ? epi.ldo : N;
-  j.blocks = (M * j.width + 63) / 64;
+  // about 32 splits per thread at most where the outputs allow it
+  j.opw = splits > 512 ? 4 : splits > 128 ? 16 : 64;
+  j.blocks = (M * j.width + j.opw - 1) / j.opw;
   return j;
 }
 

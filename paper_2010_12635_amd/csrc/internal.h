@@ -37,6 +37,7 @@ struct RedJob {
   const float* part;
   int splits;
   int64_t M, N, width, blocks;
+  int opw;                      // outputs per workgroup: 64, 16 or 4 (256 / opw groups of splits)
   Epilogue ep;
 };
 RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const Epilogue& epi);

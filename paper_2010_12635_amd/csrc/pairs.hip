@@ -386,7 +386,7 @@ struct SegParams {
 // Sum of g_k Z[other endpoint] over sorted entries [e0, e1) into acc.
 template <typename T>
 __device__ __forceinline__ void seg_sum(const SegParams& p, int64_t e0, int64_t e1, int64_t col0, float* acc) {
-  constexpr int VE = Vec<T>::N, U = 4;
+  constexpr int VE = Vec<T>::N, U = 8;
   const T* __restrict__ Z = reinterpret_cast<const T*>(p.Z);
   for (int64_t e = e0; e < e1; e += U) {
     int32_t kk[U], other[U];
