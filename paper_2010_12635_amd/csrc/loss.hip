@@ -36,78 +36,94 @@ __device__ __forceinline__ float group_sum(float v) {
   return v;
 }
 
+// Rows handled per lane group and iteration: all their loads go out before
+// any is used (one memory latency per iteration instead of one per row).
+constexpr int LOSS_R = 4;
+
 template <typename T, int LPR>
 __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
-  __shared__ float s_loss[4 * G];
-  __shared__ int32_t s_corr[4 * G];
+  constexpr int RG = 4 * G;                          // rows per workgroup and sub-step
+  __shared__ float s_loss[RG];
+  __shared__ int32_t s_corr[RG];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane / LPR, li = lane % LPR;
   const int slot = wave * G + g;
   const int64_t col0 = (int64_t)li * VE;
-  // the workgroup walks row groups blockIdx.x, blockIdx.x + gridDim.x, ...
+  const bool col_ok = col0 < p.C;
+  const T* __restrict__ logits = reinterpret_cast<const T*>(p.logits);
+  // the workgroup walks blocks of LOSS_R * RG rows: blockIdx.x, blockIdx.x
+  // + gridDim.x, ...; a slot takes rows base + r * RG + slot, r = 0 .. LOSS_R - 1
   // (in that order for the per-slot sums)
   float acc_loss = 0.f;
   int32_t acc_corr = 0;
-  for (int64_t base = (int64_t)blockIdx.x * (4 * G); base < p.n; base += (int64_t)gridDim.x * (4 * G)) {
-  const int64_t row = base + slot;
-  const bool row_ok = row < p.n;
-  float z[VE];
+  for (int64_t base = (int64_t)blockIdx.x * (LOSS_R * RG); base < p.n; base += (int64_t)gridDim.x * (LOSS_R * RG)) {
+    uint4 raw[LOSS_R];
+    int32_t lab[LOSS_R];
+    uint8_t msk[LOSS_R];
 #pragma unroll
-  for (int i = 0; i < VE; ++i) z[i] = -INFINITY;
-  if (row_ok && col0 < p.C) {
-    float x[VE];
-    unpack<T>(ldg16(reinterpret_cast<const T*>(p.logits) + row * p.ld + col0), x);
-#pragma unroll
-    for (int i = 0; i < VE; ++i)
-      if (col0 + i < p.C) z[i] = x[i];
-  }
-  // row maximum and arg-max (lowest index on ties)
-  float mx = -INFINITY;
-  int am = 0x7fffffff;
-#pragma unroll
-  for (int i = 0; i < VE; ++i)
-    if (col0 + i < p.C && (z[i] > mx || am == 0x7fffffff)) { mx = z[i]; am = (int)(col0 + i); }
-#pragma unroll
-  for (int o = LPR / 2; o > 0; o >>= 1) {
-    const float om = __shfl_xor(mx, o);
-    const int oa = __shfl_xor(am, o);
-    if (om > mx || (om == mx && oa < am)) { mx = om; am = oa; }
-  }
-  const float rmax = mx;
-  float se = 0.f;
-#pragma unroll
-  for (int i = 0; i < VE; ++i)
-    if (col0 + i < p.C) se += expf(z[i] - rmax);
-  se = group_sum<LPR>(se);
-  const float lse = rmax + logf(se);
-  const int32_t y = row_ok ? p.labels[row] : 0;
-  float zy = 0.f;
-#pragma unroll
-  for (int i = 0; i < VE; ++i)
-    if (col0 + i == y) zy = z[i];
-  zy = group_sum<LPR>(zy);
-  const bool in_mask = row_ok && (p.mask == nullptr || p.mask[row] != 0);
-  if (row_ok && col0 < p.C) {
-    const float sc = (p.loss_scale ? *p.loss_scale : 1.f) * p.inv_count;
-    float d[VE];
-#pragma unroll
-    for (int i = 0; i < VE; ++i) {
-      const int64_t c = col0 + i;
-      if (c < p.C && in_mask) d[i] = (expf(z[i] - lse) - (c == y ? 1.f : 0.f)) * sc;
-      else d[i] = 0.f;
+    for (int r = 0; r < LOSS_R; ++r) {
+      int64_t row = base + r * RG + slot;
+      row = row < p.n ? row : p.n - 1;               // in bounds; not counted below
+      raw[r] = ldg16(logits + row * p.ld + (col_ok ? col0 : 0));
+      lab[r] = p.labels[row];
+      msk[r] = p.mask ? p.mask[row] : (uint8_t)1;
     }
-    uint4 raw = pack<T>(d);
-    stg16(reinterpret_cast<T*>(p.dlogits) + row * p.ld + col0, raw);
-    bool bad = false;
-    const T* e = reinterpret_cast<const T*>(&raw);
 #pragma unroll
-    for (int i = 0; i < VE; ++i) bad |= !finite_f32(to_f32<T>(e[i]));
-    if (bad) raise_flag(p.flag);
-  }
-  acc_loss += in_mask ? (lse - zy) : 0.f;
-  acc_corr += (in_mask && am == y) ? 1 : 0;
+    for (int r = 0; r < LOSS_R; ++r) {
+      const int64_t row = base + r * RG + slot;
+      const bool row_ok = row < p.n;
+      float x[VE], z[VE];
+      unpack<T>(raw[r], x);
+#pragma unroll
+      for (int i = 0; i < VE; ++i) z[i] = (row_ok && col0 + i < p.C) ? x[i] : -INFINITY;
+      // row maximum and arg-max (lowest index on ties)
+      float mx = -INFINITY;
+      int am = 0x7fffffff;
+#pragma unroll
+      for (int i = 0; i < VE; ++i)
+        if (col0 + i < p.C && (z[i] > mx || am == 0x7fffffff)) { mx = z[i]; am = (int)(col0 + i); }
+#pragma unroll
+      for (int o = LPR / 2; o > 0; o >>= 1) {
+        const float om = __shfl_xor(mx, o);
+        const int oa = __shfl_xor(am, o);
+        if (om > mx || (om == mx && oa < am)) { mx = om; am = oa; }
+      }
+      const float rmax = mx;
+      float se = 0.f;
+#pragma unroll
+      for (int i = 0; i < VE; ++i)
+        if (col0 + i < p.C) se += expf(z[i] - rmax);
+      se = group_sum<LPR>(se);
+      const float lse = rmax + logf(se);
+      const int32_t y = row_ok ? lab[r] : 0;
+      float zy = 0.f;
+#pragma unroll
+      for (int i = 0; i < VE; ++i)
+        if (col0 + i == y) zy = z[i];
+      zy = group_sum<LPR>(zy);
+      const bool in_mask = row_ok && msk[r] != 0;
+      if (row_ok && col_ok) {
+        const float sc = (p.loss_scale ? *p.loss_scale : 1.f) * p.inv_count;
+        float d[VE];
+#pragma unroll
+        for (int i = 0; i < VE; ++i) {
+          const int64_t c = col0 + i;
+          if (c < p.C && in_mask) d[i] = (expf(z[i] - lse) - (c == y ? 1.f : 0.f)) * sc;
+          else d[i] = 0.f;
+        }
+        uint4 o = pack<T>(d);
+        stg16(reinterpret_cast<T*>(p.dlogits) + row * p.ld + col0, o);
+        bool bad = false;
+        const T* e = reinterpret_cast<const T*>(&o);
+#pragma unroll
+        for (int i = 0; i < VE; ++i) bad |= !finite_f32(to_f32<T>(e[i]));
+        if (bad) raise_flag(p.flag);
+      }
+      acc_loss += in_mask ? (lse - zy) : 0.f;
+      acc_corr += (in_mask && am == y) ? 1 : 0;
+    }
   }
   if (li == 0) {
     s_loss[slot] = acc_loss;
@@ -117,7 +133,7 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   if (threadIdx.x == 0) {
     float a = 0.f;
     int32_t c = 0;
-    for (int i = 0; i < 4 * G; ++i) { a += s_loss[i]; c += s_corr[i]; }
+    for (int i = 0; i < RG; ++i) { a += s_loss[i]; c += s_corr[i]; }
     p.part_loss[blockIdx.x] = a;
     p.part_corr[blockIdx.x] = c;
   }
@@ -155,7 +171,8 @@ int64_t loss_blocks(int64_t n, int64_t rows_per_group) {
 
 template <typename T, int LPR>
 hipError_t launch_cfg(const LossParams& p, hipStream_t s) {
-  hipLaunchKernelGGL((softmax_ce_kernel<T, LPR>), dim3((unsigned)loss_blocks(p.n, 4 * (64 / LPR))), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((softmax_ce_kernel<T, LPR>), dim3((unsigned)loss_blocks(p.n, LOSS_R * 4 * (64 / LPR))), dim3(256), 0, s,
+                     p);
   return hipGetLastError();
 }
 
@@ -177,7 +194,7 @@ int64_t rows_per_block(int prec, int64_t C) {
   const int64_t nvec = (C + VE - 1) / VE;
   int l = 1;
   while (l < nvec && l < 64) l <<= 1;
-  return 4 * (64 / l);
+  return LOSS_R * 4 * (64 / l);
 }
 
 }  // namespace
