@@ -58,14 +58,29 @@ __device__ __forceinline__ bool finite_f32(float x) {
 // ---------------------------------------------------------------------------
 struct Philox8 { uint64_t w[4]; };
 
+// Full 128-bit product a * m from four 32 x 32 -> 64-bit multiply-adds
+// (schoolbook: no partial sum exceeds 64 bits, and the high word of the
+// exact product is below 2^64).  The compiler maps each step to one
+// v_mad_u64_u32; the 64-bit product and the 64-bit high product written
+// as such cost about a third more multiplies.
+__device__ __forceinline__ void mul_64x64_128(uint64_t a, uint64_t m, uint64_t& lo, uint64_t& hi) {
+  const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32), m0 = (uint32_t)m, m1 = (uint32_t)(m >> 32);
+  const uint64_t p00 = (uint64_t)a0 * m0;
+  const uint64_t p01 = (uint64_t)a0 * m1 + (p00 >> 32);
+  const uint64_t p10 = (uint64_t)a1 * m0 + (uint32_t)p01;
+  hi = (uint64_t)a1 * m1 + (p01 >> 32) + (p10 >> 32);
+  lo = (p10 << 32) | (uint32_t)p00;
+}
+
 __device__ __forceinline__ Philox8 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
                                                   uint64_t k0, uint64_t k1) {
   const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
   const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
-    uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+    uint64_t lo0, hi0, lo1, hi1;
+    mul_64x64_128(c0, M0, lo0, hi0);
+    mul_64x64_128(c2, M1, lo1, hi1);
     uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
     c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
     k0 += W0; k1 += W1;
@@ -177,17 +192,24 @@ __device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, i
 #pragma unroll
       for (int i = 0; i < VE; ++i) acc[i] = acc[i] > 0.f ? acc[i] : 0.f;
       if (ep.dropout) {
+        // the VE <= 8 elements span one Philox block, or two when the vector
+        // crosses a multiple of 8; the second block is drawn only then (one
+        // draw in the code per call site instead of one per element)
         const uint64_t e0 = (uint64_t)row * (uint64_t)cols + (uint64_t)col0;
-        uint64_t blk = e0 >> 3;
-        Philox8 o = philox4x64_10(blk, ep.epoch, 0, 0, ep.seed, ep.layer);
+        const uint64_t b0 = e0 >> 3, b1 = (e0 + VE - 1) >> 3;
+        {
+          const Philox8 o = philox4x64_10(b0, ep.epoch, 0, 0, ep.seed, ep.layer);
 #pragma unroll
-        for (int i = 0; i < VE; ++i) {
-          uint64_t e = e0 + i;
-          if ((e >> 3) != blk) {
-            blk = e >> 3;
-            o = philox4x64_10(blk, ep.epoch, 0, 0, ep.seed, ep.layer);
-          }
-          acc[i] = philox_word(o, (uint32_t)(e & 7)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
+          for (int i = 0; i < VE; ++i)
+            if (((e0 + i) >> 3) == b0)
+              acc[i] = philox_word(o, (uint32_t)((e0 + i) & 7)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
+        }
+        if (b1 != b0) {
+          const Philox8 o = philox4x64_10(b1, ep.epoch, 0, 0, ep.seed, ep.layer);
+#pragma unroll
+          for (int i = 0; i < VE; ++i)
+            if (((e0 + i) >> 3) != b0)
+              acc[i] = philox_word(o, (uint32_t)((e0 + i) & 7)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
         }
       }
     }

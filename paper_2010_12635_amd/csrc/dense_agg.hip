@@ -415,15 +415,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // The chunks that do not fill a whole trip of the unrolled loop are done
   // first, so that nothing follows the loop: with a compute after it the
   // register allocator rotates the accumulators on every trip.
+  // The launch guarantees n >= 256, i.e. nc >= 8 chunks, so each loop below
+  // runs at least once; written as do-while, it has no path that skips it
+  // (where such a path meets the loop exit the register allocator spills
+  // accumulators, and the reloads before the loop make the compiler wait
+  // for a whole chunk of loads more than the ring needs at the loop head).
   if (DEPTH == 2) {
     Fr f0, f1;
     int64_t c = 0;
     if (nc & 1) { load(f0, 0); compute(f0); c = 1; }
     load(f0, c);
-    for (; c + 2 <= nc; c += 2) {
+    do {
       load(f1, c + 1); MM_FENCE(); compute(f0); MM_FENCE();
       load(f0, c + 2); MM_FENCE(); compute(f1); MM_FENCE();
-    }
+      c += 2;
+    } while (c + 2 <= nc);
   } else {
     Fr f0, f1, f2;
     int64_t c = 0;
@@ -433,11 +439,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     c = r3;
     load(f0, c);
     load(f1, c + 1);
-    for (; c + 3 <= nc; c += 3) {
+    do {
       load(f2, c + 2); MM_FENCE(); compute(f0); MM_FENCE();
       load(f0, c + 3); MM_FENCE(); compute(f1); MM_FENCE();
       load(f1, c + 4); MM_FENCE(); compute(f2); MM_FENCE();
-    }
+      c += 3;
+    } while (c + 3 <= nc);
   }
 #undef MM_FENCE
 
