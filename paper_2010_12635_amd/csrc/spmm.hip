@@ -97,8 +97,10 @@ __device__ __forceinline__ void gather_tail(float* acc, const T* __restrict__ X,
   }
 }
 
+// Light rows for workgroup bx of nbx (bx: position among the light-row
+// workgroups of the launch).
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
-__global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
+__device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, int64_t bx, int64_t nbx) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -107,8 +109,8 @@ __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
   if (col0 >= p.F) return;
   const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
   // the grid is capped (at most 2^32 work-items per dispatch dimension):
-  // a workgroup takes row slots blockIdx.x, blockIdx.x + gridDim.x, ...
-  for (int64_t slot = ((int64_t)blockIdx.x * 4 + wave) * G + g; slot < p.n_rows; slot += (int64_t)gridDim.x * 4 * G) {
+  // a workgroup takes row slots bx, bx + nbx, ...
+  for (int64_t slot = (bx * 4 + wave) * G + g; slot < p.n_rows; slot += nbx * 4 * G) {
     const int64_t row = p.row_perm ? (int64_t)p.row_perm[slot] : slot;
     const int64_t beg = (int64_t)p.rowptr[row], end = (int64_t)p.rowptr[row + 1];
     if (!p.row_perm && p.heavy_threshold > 0 && end - beg > p.heavy_threshold) continue;
@@ -136,6 +138,11 @@ __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
   }
 }
 
+template <typename T, typename IdxT, int LPR, bool HAS_VAL>
+__global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
+  spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, blockIdx.x, gridDim.x);
+}
+
 template <typename IdxT>
 struct HeavyParams {
   const IdxT* rowptr;
@@ -156,13 +163,13 @@ struct HeavyParams {
   Epilogue epi;
 };
 
-// One workgroup per (chunk, column block).
+// One workgroup per (chunk, column block): launch position bx of the chunks.
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
-__global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT> p) {
+__device__ __forceinline__ void spmm_heavy_body(const HeavyParams<IdxT>& p, int64_t bx) {
   constexpr int VE = Vec<T>::N;
   constexpr int NG = 256 / LPR;
   __shared__ float red[4 * LPR * VE];
-  const int64_t chunk = p.chunk_order ? (int64_t)p.chunk_order[blockIdx.x] : (int64_t)blockIdx.x;
+  const int64_t chunk = p.chunk_order ? (int64_t)p.chunk_order[bx] : bx;
   const int g = threadIdx.x / LPR, li = threadIdx.x % LPR;
   const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
   const int32_t h = p.chunk_heavy[chunk];
@@ -209,6 +216,24 @@ __global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT>
   }
 }
 
+template <typename T, typename IdxT, int LPR, bool HAS_VAL>
+__global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT> p) {
+  spmm_heavy_body<T, IdxT, LPR, HAS_VAL>(p, blockIdx.x);
+}
+
+// Heavy chunks and light rows in one launch: workgroups [0, n_heavy) take
+// the chunks (longest work first), the rest walk the light rows, so that the
+// hubs are reduced while the light rows run instead of in a launch of their
+// own (on graphs with few hubs that launch leaves most of the chip idle).
+// A workgroup is wholly one or the other, so the chunk body's barriers are
+// reached by all its threads.
+template <typename T, typename IdxT, int LPR, bool HAS_VAL>
+__global__ __launch_bounds__(256) void spmm_fused_kernel(SpmmParams<IdxT> p, HeavyParams<IdxT> hp, int64_t n_heavy) {
+  const int64_t b = blockIdx.x;
+  if (b < n_heavy) spmm_heavy_body<T, IdxT, LPR, HAS_VAL>(hp, b);
+  else spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, b - n_heavy, (int64_t)gridDim.x - n_heavy);
+}
+
 // One thread per (heavy row, column): fixed-order sum of the chunk partials.
 template <typename T, typename IdxT>
 __global__ __launch_bounds__(256) void spmm_heavy_fixup_kernel(HeavyParams<IdxT> p) {
@@ -221,6 +246,10 @@ __global__ __launch_bounds__(256) void spmm_heavy_fixup_kernel(HeavyParams<IdxT>
   for (int64_t c = c0; c < c1; ++c) a += p.partials[c * p.ldp + col];
   epi_store1<T>(p.epi, row, col, a);
 }
+
+// Chunk workgroups below which the chunks share the light rows' launch
+// (8 per compute unit).
+constexpr int64_t SPMM_FUSE_CHUNKS = 8 * 256;
 
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
@@ -239,14 +268,16 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   p.heavy_threshold = A.n_heavy > 0 ? A.heavy_threshold : 0;
   p.X = X; p.ldx = ldx; p.F = F; p.epi = epi;
   const int64_t rows_per_block = 4 * G;
+  const int64_t lblocks = p.n_rows > 0 ? std::min<int64_t>((p.n_rows + rows_per_block - 1) / rows_per_block, 1 << 20) : 0;
   hipError_t e = hipSuccess;
-  if (p.n_rows > 0) {
-    const int64_t blocks = (p.n_rows + rows_per_block - 1) / rows_per_block;
-    dim3 grid((unsigned)(blocks < (1 << 20) ? blocks : (1 << 20)), (unsigned)colblocks);
-    hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), grid, dim3(256), 0, s, p);
-    e = hipGetLastError();
+  if (A.n_heavy <= 0) {
+    if (lblocks > 0) {
+      hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), dim3((unsigned)lblocks, (unsigned)colblocks),
+                         dim3(256), 0, s, p);
+      e = hipGetLastError();
+    }
+    return e;
   }
-  if (e != hipSuccess || A.n_heavy <= 0) return e;
 
   HeavyParams<IdxT> hp;
   hp.rowptr = p.rowptr; hp.colidx = A.colidx; hp.values = A.values; hp.dinv = A.dinv;
@@ -256,8 +287,23 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   hp.X = X; hp.ldx = ldx; hp.F = F;
   hp.ldp = colblocks * LPR * VE;
   hp.partials = partials; hp.epi = epi;
-  dim3 gridc((unsigned)A.n_chunks, (unsigned)colblocks);
-  hipLaunchKernelGGL((spmm_heavy_chunk_kernel<T, IdxT, LPR, HAS_VAL>), gridc, dim3(256), 0, s, hp);
+  if (lblocks > 0 && A.n_chunks * colblocks < SPMM_FUSE_CHUNKS) {
+    // few chunks (fewer than 8 workgroups per compute unit on their own):
+    // one launch with the light rows (grid below 2^32 work-items)
+    dim3 gridf2((unsigned)(A.n_chunks + lblocks), (unsigned)colblocks);
+    hipLaunchKernelGGL((spmm_fused_kernel<T, IdxT, LPR, HAS_VAL>), gridf2, dim3(256), 0, s, p, hp, (int64_t)A.n_chunks);
+  } else {
+    // many chunks fill the chip by themselves and keep their first-column
+    // order to themselves (mixed with light rows: +2 % on R-MAT scale 21)
+    if (lblocks > 0) {
+      hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), dim3((unsigned)lblocks, (unsigned)colblocks),
+                         dim3(256), 0, s, p);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((spmm_heavy_chunk_kernel<T, IdxT, LPR, HAS_VAL>), dim3((unsigned)A.n_chunks, (unsigned)colblocks),
+                       dim3(256), 0, s, hp);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 gridf((unsigned)A.n_heavy, (unsigned)((F + 255) / 256));
