@@ -36,11 +36,13 @@ __device__ __forceinline__ float group_sum(float v) {
   return v;
 }
 
-// Rows handled per lane group and iteration: all their loads go out before
-// any is used (one memory latency per iteration instead of one per row).
-constexpr int LOSS_R = 4;
+// Rows handled per lane group and iteration (R): all their loads go out
+// before any is used (one memory latency per iteration instead of one per
+// row).  R = 4 when one row per iteration would give more than
+// LOSS_R4_GROUPS workgroups, else R = 1 (fewer rows keep more workgroups).
+constexpr int64_t LOSS_R4_GROUPS = 16384;
 
-template <typename T, int LPR>
+template <typename T, int LPR, int LOSS_R>
 __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
@@ -169,10 +171,17 @@ int64_t loss_blocks(int64_t n, int64_t rows_per_group) {
   return nb < 65536 ? nb : 65536;
 }
 
+int loss_rows_per_iter(int64_t n, int64_t rows_per_group) {
+  return (n + rows_per_group - 1) / rows_per_group > LOSS_R4_GROUPS ? 4 : 1;
+}
+
 template <typename T, int LPR>
 hipError_t launch_cfg(const LossParams& p, hipStream_t s) {
-  hipLaunchKernelGGL((softmax_ce_kernel<T, LPR>), dim3((unsigned)loss_blocks(p.n, LOSS_R * 4 * (64 / LPR))), dim3(256), 0, s,
-                     p);
+  constexpr int64_t RG = 4 * (64 / LPR);
+  if (loss_rows_per_iter(p.n, RG) == 4)
+    hipLaunchKernelGGL((softmax_ce_kernel<T, LPR, 4>), dim3((unsigned)loss_blocks(p.n, 4 * RG)), dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL((softmax_ce_kernel<T, LPR, 1>), dim3((unsigned)loss_blocks(p.n, RG)), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
@@ -189,19 +198,21 @@ hipError_t launch_t(const LossParams& p, hipStream_t s) {
   return launch_cfg<T, 64>(p, s);
 }
 
-int64_t rows_per_block(int prec, int64_t C) {
+// Rows per workgroup iteration for n rows (as the launch chooses).
+int64_t rows_per_block(int prec, int64_t C, int64_t n) {
   const int VE = prec == 0 ? 4 : 8;
   const int64_t nvec = (C + VE - 1) / VE;
   int l = 1;
   while (l < nvec && l < 64) l <<= 1;
-  return LOSS_R * 4 * (64 / l);
+  const int64_t rg = 4 * (64 / l);
+  return loss_rows_per_iter(n, rg) * rg;
 }
 
 }  // namespace
 
 size_t loss_workspace_bytes(int64_t n, int64_t C) {
-  const int64_t nb = (n + rows_per_block(0, C) - 1) / rows_per_block(0, C) + 1;   // fp32 needs the most blocks
-  const int64_t nb16 = (n + rows_per_block(1, C) - 1) / rows_per_block(1, C) + 1;
+  const int64_t nb = (n + rows_per_block(0, C, n) - 1) / rows_per_block(0, C, n) + 1;   // fp32 needs the most blocks
+  const int64_t nb16 = (n + rows_per_block(1, C, n) - 1) / rows_per_block(1, C, n) + 1;
   const int64_t m = nb > nb16 ? nb : nb16;
   return (size_t)m * (sizeof(float) + sizeof(int32_t)) + 256;
 }
@@ -209,7 +220,7 @@ size_t loss_workspace_bytes(int64_t n, int64_t C) {
 hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* logits, const int32_t* labels,
                        const uint8_t* mask, int64_t n_mask, const float* loss_scale, float* loss, void* dlogits,
                        int32_t* n_correct, int32_t* flag, void* ws, hipStream_t s) {
-  const int64_t nb = loss_blocks(n, rows_per_block(prec, C));
+  const int64_t nb = loss_blocks(n, rows_per_block(prec, C, n));
   LossParams p;
   p.n = n; p.C = C; p.ld = ld; p.logits = logits; p.labels = labels; p.mask = mask;
   p.inv_count = 1.f / (float)n_mask;

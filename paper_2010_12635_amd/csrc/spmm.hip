@@ -209,10 +209,15 @@ __device__ __forceinline__ void spmm_heavy_body(const HeavyParams<IdxT>& p, int6
       s[i] += red[(2 * LPR + li) * VE + i];
       s[i] += red[(3 * LPR + li) * VE + i];
     }
-    float* out = p.partials + chunk * p.ldp + col0;
+    if (p.heavy_chunk_off[h + 1] - p.heavy_chunk_off[h] == 1) {
+      // the row's only chunk holds its whole sum: the epilogue stores it here
+      if (col0 < p.F) epi_store_vec<T>(p.epi, row, col0, s);
+    } else {
+      float* out = p.partials + chunk * p.ldp + col0;
 #pragma unroll
-    for (int i = 0; i < VE; ++i)
-      if (col0 + i < p.ldp) out[i] = s[i];
+      for (int i = 0; i < VE; ++i)
+        if (col0 + i < p.ldp) out[i] = s[i];
+    }
   }
 }
 
@@ -234,7 +239,8 @@ __global__ __launch_bounds__(256) void spmm_fused_kernel(SpmmParams<IdxT> p, Hea
   else spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, b - n_heavy, (int64_t)gridDim.x - n_heavy);
 }
 
-// One thread per (heavy row, column): fixed-order sum of the chunk partials.
+// One thread per (heavy row, column): fixed-order sum of the chunk partials
+// (rows of a single chunk were stored by their chunk).
 template <typename T, typename IdxT>
 __global__ __launch_bounds__(256) void spmm_heavy_fixup_kernel(HeavyParams<IdxT> p) {
   const int64_t h = blockIdx.x;
@@ -242,6 +248,7 @@ __global__ __launch_bounds__(256) void spmm_heavy_fixup_kernel(HeavyParams<IdxT>
   if (col >= p.F) return;
   const int64_t row = p.heavy_rows[h];
   const int64_t c0 = p.heavy_chunk_off[h], c1 = p.heavy_chunk_off[h + 1];
+  if (c1 - c0 == 1) return;
   float a = 0.f;
   for (int64_t c = c0; c < c1; ++c) a += p.partials[c * p.ldp + col];
   epi_store1<T>(p.epi, row, col, a);
@@ -306,6 +313,7 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (A.n_chunks == A.n_heavy) return hipSuccess;     // every heavy row is one chunk: all stored
   dim3 gridf((unsigned)A.n_heavy, (unsigned)((F + 255) / 256));
   hipLaunchKernelGGL((spmm_heavy_fixup_kernel<T, IdxT>), gridf, dim3(256), 0, s, hp);
   return hipGetLastError();
