@@ -32,8 +32,10 @@ def to_dev(a, prec, ld=None):
 
 
 def host(t, f=None):
-    x = t.float().cpu().numpy().astype(np.float64)
-    return x if f is None else x[:, :f]
+    # the logical columns only (padding may hold any bits)
+    if f is not None:
+        t = t[:, :f]
+    return t.float().cpu().numpy().astype(np.float64)
 
 
 def rounded(a, prec):
@@ -140,9 +142,16 @@ def test_schedule_lists_heavy_rows():
 
 # ------------------------------------------------------------ layer fwd ----
 
-def _layer_case(n, f_in, f_out, seed, hubs=True):
+# hub rows of 7, 2 and 1 chunk(s) at the tests' chunk size (96 entries)
+HUBS = [(1, 600), (2, 150), (3, 70)]
+# heavy rows of one chunk only: every heavy row is stored by its chunk and
+# no fix-up pass runs
+HUBS_ONE_CHUNK = [(3, 70), (5, 60)]
+
+
+def _layer_case(n, f_in, f_out, seed, hubs=HUBS):
     rng = np.random.default_rng(seed)
-    src, dst = hub_graph(n, 4 * n, [(1, 600), (2, 150)] if hubs else [], seed)
+    src, dst = hub_graph(n, 4 * n, hubs, seed)
     g = O.graph(n, src, dst)
     h = rng.standard_normal((n, f_in)).astype(np.float32)
     w = (rng.standard_normal((f_in, f_out)) / np.sqrt(f_in)).astype(np.float32)
@@ -155,6 +164,8 @@ FWD_CASES = [
     (3000, 500, 64, G.GCN_ACT_RELU, 0.5, "csr"),
     (3000, 128, 7, G.GCN_ACT_NONE, 0.0, "csr"),
     (2100, 40, 130, G.GCN_ACT_RELU, 0.3, "csr"),
+    (2100, 40, 130, G.GCN_ACT_RELU, 0.3, "csr_dinv"),
+    (1800, 72, 24, G.GCN_ACT_RELU, 0.5, "csr_onechunk"),
     (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1500, 64, 32, G.GCN_ACT_NONE, 0.0, "tiled"),
     (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "tiled"),
@@ -170,16 +181,20 @@ FWD_CASES = [
 
 
 def _graph_for(n, src, dst, prec, storage):
-    return DeviceGraph(n, src, dst, prec=prec, dense=storage != "csr", tiled=storage == "tiled",
-                       heavy_threshold=48, chunk_nnz=96)
+    # "csr_dinv": CSR without stored values, every edge weight formed from dinv;
+    # "csr_onechunk": CSR whose heavy rows are all one chunk
+    csr = storage in ("csr", "csr_dinv", "csr_onechunk")
+    return DeviceGraph(n, src, dst, prec=prec, dense=not csr, tiled=storage == "tiled",
+                       values=storage != "csr_dinv", heavy_threshold=48, chunk_nnz=96)
 
 
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
 @pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_act{c[3]}_p{c[4]}_{c[5]}")
 def test_layer_fwd(prec, case):
     n, f_in, f_out, act, p, storage = case
-    dense = storage != "csr"
-    g, src, dst, h, w, b = _layer_case(n, f_in, f_out, seed=n + f_in)
+    dense = storage not in ("csr", "csr_dinv", "csr_onechunk")
+    g, src, dst, h, w, b = _layer_case(n, f_in, f_out, seed=n + f_in,
+                                       hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS)
     dg = _graph_for(n, src, dst, prec, storage)
     L = G.GcnLayer(f_in, f_out, round8(f_in), round8(f_out), act, p, 3, 0)
     H, W = to_dev(h, prec), to_dev(w, prec, round8(f_out))
@@ -212,6 +227,8 @@ BWD_CASES = [
     (3000, 500, 64, G.GCN_ACT_NONE, 0.0, "csr"),
     (3000, 64, 7, G.GCN_ACT_RELU, 0.5, "csr"),
     (2100, 130, 40, G.GCN_ACT_RELU, 0.3, "csr"),
+    (3000, 64, 7, G.GCN_ACT_RELU, 0.5, "csr_dinv"),
+    (1800, 24, 72, G.GCN_ACT_RELU, 0.5, "csr_onechunk"),
     (1500, 64, 32, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "dense"),
@@ -225,8 +242,9 @@ BWD_CASES = [
 @pytest.mark.parametrize("case", BWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_below{c[3]}_p{c[4]}_{c[5]}")
 def test_layer_bwd(prec, case):
     n, f_in, f_out, act_below, p, storage = case
-    dense = storage != "csr"
-    g, src, dst, h, w, _ = _layer_case(n, f_in, f_out, seed=7 * n + f_out)
+    dense = storage not in ("csr", "csr_dinv", "csr_onechunk")
+    g, src, dst, h, w, _ = _layer_case(n, f_in, f_out, seed=7 * n + f_out,
+                                       hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS)
     rng = np.random.default_rng(n)
     if act_below == G.GCN_ACT_RELU:   # H as produced by ReLU + dropout: exact zeros
         h = np.where(rng.random(h.shape) < 0.5, 0.0, np.abs(h) * 2).astype(np.float32)
