@@ -172,18 +172,29 @@ __device__ __forceinline__ void epi_store1(const Epilogue& ep, int64_t row, int6
   if (!finite_f32(to_f32<T>(o))) raise_flag(ep.flag);
 }
 
+// Bias of the Vec<T>::N columns from col0 (any col0 >= 0; entries past cols
+// re-read column 0 and are never added), for a caller that stores the same
+// columns of many rows and loads them once.
+template <typename T>
+__device__ __forceinline__ void epi_load_bias(const Epilogue& ep, int64_t col0, float (&bv)[Vec<T>::N]) {
+  constexpr int VE = Vec<T>::N;
+#pragma unroll
+  for (int i = 0; i < VE; ++i) bv[i] = 0.f;
+  if (!ep.bias || ep.mode != EPI_AGG) return;
+#pragma unroll
+  for (int i = 0; i < VE; ++i) bv[i] = ep.bias[col0 + i < ep.cols ? col0 + i : 0];
+}
+
 // Vector epilogue: Vec<T>::N consecutive columns starting at col0 (col0 is a
 // multiple of the vector width, col0 < cols).  Columns >= cols are written 0.
+// bv holds the bias of these columns (epi_load_bias).
 template <typename T>
-__device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, int64_t col0, float* acc) {
+__device__ __forceinline__ void epi_store_vec_b(const Epilogue& ep, int64_t row, int64_t col0, float* acc,
+                                                const float (&bv)[Vec<T>::N]) {
   constexpr int VE = Vec<T>::N;
   const int64_t cols = ep.cols;
   if (ep.mode == EPI_AGG) {
     if (ep.bias) {
-      // all VE loads in flight at once (an index past cols re-reads col0)
-      float bv[VE];
-#pragma unroll
-      for (int i = 0; i < VE; ++i) bv[i] = ep.bias[col0 + i < cols ? col0 + i : col0];
 #pragma unroll
       for (int i = 0; i < VE; ++i)
         if (col0 + i < cols) acc[i] += bv[i];
@@ -225,6 +236,14 @@ __device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, i
   }
   stg16(reinterpret_cast<T*>(ep.out) + row * ep.ldo + col0, raw);
   if (bad) raise_flag(ep.flag);
+}
+
+// The same, loading the bias of these columns itself.
+template <typename T>
+__device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, int64_t col0, float* acc) {
+  float bv[Vec<T>::N];
+  epi_load_bias<T>(ep, col0, bv);
+  epi_store_vec_b<T>(ep, row, col0, acc, bv);
 }
 
 }  // namespace gcn
