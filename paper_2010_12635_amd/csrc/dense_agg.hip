@@ -10,7 +10,12 @@
 //    that lane order, and the four 16-row pieces of a 64-row block follow
 //    each other, so each operand load is one contiguous 1 KiB and a wave's
 //    k range is one contiguous stream (row-major rows give 16 short runs per
-//    load, which measured far below the stream rate on MI355X).
+//    load, which measured far below the stream rate on MI355X).  Tiled
+//    A_hat is read once per call, with non-temporal loads (measured 7-13 %
+//    faster at n = 16384, F = 64 and 32; Xt, which every workgroup re-reads,
+//    keeps ordinary loads).  Row-major A_hat does not: each of its 128-byte
+//    lines serves two consecutive chunks, and with non-temporal loads the
+//    line is gone before the second (O1 training 23 % slower).
 //    X is transposed into the same tiled layout (Xt) before the product.
 //  * A workgroup owns 64 rows and a 64-column block; its 8 waves split the
 //    k range in 8 contiguous parts, each keeping its partial 64 x 64 tile in
@@ -199,7 +204,8 @@ __global__ __launch_bounds__(64 * DA_WAVES) void dense_agg_kernel(DaParams p) {
 
   auto load = [&](Frag<TN>& f, int64_t c) {
 #pragma unroll
-    for (int tm = 0; tm < 4; ++tm) f.a[tm] = ldg16(abase[tm] + c * astep);
+    for (int tm = 0; tm < 4; ++tm)
+      f.a[tm] = TILED ? ldg16_nt(abase[tm] + c * astep) : ldg16(abase[tm] + c * astep);
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) f.b[tn] = ldg16(bbase + c * 4 * PIECE + tn * PIECE);
   };
