@@ -10,7 +10,8 @@ MFMA-bound dense aggregation it leads to.
   MFMA kernel: the benchmark's widest (n = 32768, F = 2048, the launch the
   model-size sweep times, 256 x 256 tiles), shapes whose tile count falls
   below the compute-unit count (256 x 128 and 128 x 128 tiles, ragged n and
-  F), and an fp32 shape: sampled output rows against the oracle's per-row
+  F), 256 x 256 tiles with ragged n and F in fp16 and fp32, and an fp32
+  256 x 128 shape: sampled output rows against the oracle's per-row
   formula."""
 import numpy as np
 import pytest
@@ -99,7 +100,10 @@ def test_identity_input_layer(prec, storage, f_out):
     (16384, 520, G.GCN_BF16),   # 256 x 128: 192 tiles of 256 x 256 would not fill the chip
     (32768, 256, G.GCN_F32),    # 256 x 128, fp32 MFMA
     (6000, 1000, G.GCN_F16),    # 128 x 128, ragged rows and columns
-], ids=["n32768_F2048_f16", "n16384_F520_bf16", "n32768_F256_f32", "n6000_F1000_f16"])
+    (33000, 600, G.GCN_F16),    # 256 x 256 with ragged rows and columns (bias of the lanes past F)
+    (33000, 600, G.GCN_F32),    # the same tiles in fp32 (four 16x16x4 steps per fragment pair)
+], ids=["n32768_F2048_f16", "n16384_F520_bf16", "n32768_F256_f32", "n6000_F1000_f16", "n33000_F600_f16",
+        "n33000_F600_f32"])
 def test_wide_dense_aggregation_at_full_size(n, F, prec):
     print(f"[wide] n={n} F={F} tiled {PNAME[prec]}", flush=True)
     rng = np.random.default_rng(21)
