@@ -261,7 +261,11 @@ gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* 
 
 /* ---------------------------------------------------------------------------
  * gcn_layer_bwd: gradients of gcn_layer_fwd given dZ = dLoss/dZ (n x f_out,
- * ld_out, prec, already multiplied by the loss scale):
+ * ld_out, prec, already multiplied by the loss scale).  The chain rule through
+ * one layer of Eq. (1) (Section "Graph Convolutions"), Z = A_hat (H W) + b,
+ * with A_hat symmetric because G is undirected (Section "Introduction");
+ * gradients stay multiplied by the dynamic loss scale of the O1/O2 levels
+ * (Section "Background and Motivation") until the optimiser step:
  *   G_S      = A_hat^T dZ = A_hat dZ           (GS: n x f_out, ld_out, prec)
  *   dW       = H^T G_S                          (f_in x ld_out fp32; cols >= f_out set to 0)
  *   dbias    = column sums of dZ                (ld_out fp32, may be NULL)
@@ -285,6 +289,12 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec,
  * gcn_loss: masked mean softmax cross-entropy over logits (n x C, ld, prec)
  * and labels (int32 in [0, C)); mask (uint8, NULL = every row) selects the
  * n_mask training rows (n_mask = number of nonzero mask entries, > 0).
+ * This is the training loss of the semi-supervised vertex classification
+ * that the paper scores by accuracy (Section "Experimental Setup", its
+ * experiments subsection; the GCN of Section "Graph Convolutions" with the
+ * original model's architecture), and the seed of
+ * the backward pass: dlogits carries the loss scale S of the O1/O2 levels
+ * (Section "Background and Motivation").
  *   *loss        = mean over masked rows of logsumexp(z_i) - z_i[y_i]   (fp32, unscaled)
  *   dlogits      = S * (softmax(z_i) - onehot(y_i)) / n_mask on masked rows, 0 elsewhere
  *   *n_correct   = masked rows whose arg-max (lowest index on ties) is y_i (may be NULL)

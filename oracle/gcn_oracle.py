@@ -197,12 +197,30 @@ def transpose_csr(g: Graph, values):
     return Graph(g.n, rowptr, t_cols.astype(np.int32)), t_vals
 
 
-def spmm(g: Graph, values, x):
-    """Y = A X for A in CSR (fp64): Y[i] = sum over stored (i, j) of a_ij X[j]."""
+def spmm(g: Graph, values, x, block_entries=1 << 22):
+    """Y = A X for A in CSR (fp64): Y[i] = sum over stored (i, j) of a_ij X[j].
+
+    Rows are taken in consecutive blocks of about ``block_entries`` stored
+    entries (at least one row per block), so that the products a_ij X[j]
+    held at once stay bounded on graphs with many millions of entries; each
+    row's terms are summed in entry order."""
     x = np.asarray(x, np.float64)
-    prod = values[:, None] * x[g.colidx.astype(np.int64)]
+    values = np.asarray(values, np.float64)
+    rp = np.asarray(g.rowptr, np.int64)
     y = np.zeros((g.n, x.shape[1]), np.float64)
-    np.add.at(y, g.rows(), prod)
+    r0 = 0
+    while r0 < g.n:
+        # last row r1 whose block still holds at most block_entries entries
+        r1 = int(np.searchsorted(rp, rp[r0] + block_entries, side="right")) - 1
+        r1 = min(max(r1, r0 + 1), g.n)
+        p0, p1 = int(rp[r0]), int(rp[r1])
+        if p1 > p0:
+            prod = values[p0:p1, None] * x[g.colidx[p0:p1].astype(np.int64)]
+            counts = np.diff(rp[r0:r1 + 1])
+            live = counts > 0
+            starts = rp[r0:r1][live] - p0
+            y[r0:r1][live] = np.add.reduceat(prod, starts, axis=0)
+        r0 = r1
     return y
 
 

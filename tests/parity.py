@@ -8,6 +8,12 @@ TOL_F16 = 2e-2
 TOL_BF16 = 1e-1
 
 
+def f32(x):
+    """x rounded to binary32, as the C ABI receives float arguments (e.g.
+    dropout_p): the oracle is given the value the library actually sees."""
+    return float(np.float32(x))
+
+
 def tol_for(prec):
     return {0: TOL_F32, 1: TOL_F16, 2: TOL_BF16}[prec]
 

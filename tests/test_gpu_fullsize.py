@@ -5,7 +5,10 @@ that the oracle computes one by one, plus a property that holds at any size:
 * layer-1 forward rows: H1[i] = dropout(ReLU(sum_j A_hat_ij (X W1)_j + b1))
   for the highest-degree rows (heavy-row path) and random rows;
 * backward on host-drawn H, W, dZ: sampled rows of G_S = A_hat dZ and of
-  dZ_below, and u^T dW v = (H u) . (A_hat (dZ v)) for random u, v."""
+  dZ_below (hub rows included), and the whole of dW = H^T (A_hat dZ) and
+  db = column sums of dZ, element by element against the oracle's product
+  (on R-MAT scale 21 dW sums over 2^21 vertices, the longest reduction of
+  the path), in fp16 and in fp32."""
 import numpy as np
 import pytest
 import torch
@@ -14,12 +17,12 @@ from oracle import gcn_oracle as O
 from paper_2010_12635_amd import gcn as G
 from paper_2010_12635_amd import inputs as I
 from paper_2010_12635_amd.model import DeviceGraph, GCN2, round8
-from tests.parity import assert_close, tol_for
+from tests.parity import assert_close
 
 pytestmark = pytest.mark.gpu
 
 WORKLOADS = [("sbm16k_dense", G.GCN_F16), ("sbm16k_dense", G.GCN_F32), ("ba200k", G.GCN_F16),
-             ("rmat21", G.GCN_F16)]
+             ("ba200k", G.GCN_F32), ("rmat21", G.GCN_F16), ("rmat21", G.GCN_F32)]
 
 
 def _rounded(a, prec):
@@ -102,13 +105,13 @@ def test_fullsize_sampled(name, prec):
     dzb_want = np.where(hr[rows] > 0, (gs_want @ wr.T) / 0.5, 0.0)
     dzb_got = dZb[rsel].float().cpu().numpy()[:, :fi].astype(np.float64)
     assert_close(dzb_got, dzb_want, prec, f"{name} dZ_below sampled rows")
-    # projection of dW: u^T dW v = (H u) . (A_hat (dZ v))
-    u = rng.standard_normal(fi)
-    v = rng.standard_normal(fo)
-    proj_want = float((hr @ u) @ O.norm_adj_matvec(n, wl["src"], wl["dst"], dzr @ v))
-    proj_got = float(u @ dW.cpu().numpy()[:, :fo].astype(np.float64) @ v)
-    scale_ref = float(np.abs(hr @ u) @ np.abs(O.norm_adj_matvec(n, wl["src"], wl["dst"], np.abs(dzr @ v))))
-    assert abs(proj_got - proj_want) <= tol_for(prec) * scale_ref, (proj_got, proj_want, scale_ref)
+    # the whole weight gradient: dW = H^T (A_hat dZ), every element
+    print(f"[fullsize] {name}: oracle A_hat dZ over all {n} rows", flush=True)
+    gs_all = O.norm_adj_matvec(n, wl["src"], wl["dst"], dzr)
+    assert_close(gs_all[rows], gs_want, 0, f"{name} oracle G_S rows agree")   # two oracle routes, fp64
+    dw_want = hr.T @ gs_all
+    assert_close(dW.cpu().numpy()[:, :fo].astype(np.float64), dw_want, prec, f"{name} dW (all {fi}x{fo})")
+    assert np.all(dW.cpu().numpy()[:, fo:] == 0)
     db_want = dzr.sum(axis=0)
     assert_close(db.cpu().numpy()[:fo], db_want, prec, f"{name} db")
     assert ov.item() == 0

@@ -248,7 +248,9 @@ def test_gae_step_matches_oracle(prec):
     scale = 256.0 if prec else 1.0
     l_o, _, g_o = O.pair_loss(zr, u, v, n_pos, loss_scale=scale)
     assert abs(m.loss.item() - l_o) <= 1e-5 * abs(l_o)
-    dz = O.pair_backward(n, zr, u, v, m.pair_g.cpu().numpy().astype(np.float64))
+    # the per-pair gradient (fp32 on the device in every mode)
+    assert_close(m.pair_g.cpu().numpy().astype(np.float64), g_o, G.GCN_F32, "pair gradient")
+    dz = O.pair_backward(n, zr, u, v, g_o)
     dzr = host(m.dZ, m.f_e)
     assert_close(dzr, dz, prec, "dZ")
     _, dw2, db2, dz1 = O.layer_bwd(g, vals, h1r, rnd(m.W2w().float().cpu().numpy()[:, :m.f_e]), dzr, "relu", 0.0)

@@ -10,7 +10,7 @@ from oracle import gcn_oracle as O
 from paper_2010_12635_amd import gcn as G
 from paper_2010_12635_amd import inputs as I
 from paper_2010_12635_amd.model import DeviceGraph, GCN2, round8
-from tests.parity import assert_close, hub_graph, tol_for
+from tests.parity import assert_close, f32, hub_graph, tol_for
 
 pytestmark = pytest.mark.gpu
 
@@ -208,17 +208,66 @@ def test_layer_fwd(prec, case):
     torch.cuda.synchronize()
     hr, wr = rounded(h, prec), rounded(w, prec)
     vals = O.norm_values(g)
-    s_o, z_o, out_o = O.layer_fwd(g, vals, hr, wr, b, "relu" if act else "none", p, True, seed, 3, epoch,
+    p32 = f32(p)     # the ABI takes dropout_p as binary32
+    s_o, z_o, out_o = O.layer_fwd(g, vals, hr, wr, b, "relu" if act else "none", p32, True, seed, 3, epoch,
                                   dense=O.dense_adj(g, vals) if dense else None)
     assert_close(host(S, f_out), s_o, prec, "S = H W")
     assert_close(host(Hout, f_out), out_o, prec, "H_out")
     assert int(ov.item()) == 0
     if p > 0:   # dropout decisions are bit-identical: zero pattern of kept positives matches
-        keep = O.dropout_keep(seed, 3, epoch, n, f_out, p)
+        keep = O.dropout_keep(seed, 3, epoch, n, f_out, p32)
         got = host(Hout, f_out)
         # positions whose sign no rounding of the device path can flip
         pos = z_o > (1e-3 if prec == 0 else 10 * tol_for(prec) * np.sqrt(np.mean(z_o * z_o)))
         assert np.array_equal(got[pos] != 0, keep[pos])
+
+
+def test_dropout_threshold_uses_binary32_p():
+    """The keep threshold is floor(p * 2^32) of the binary32 p the ABI takes.
+
+    p64 is chosen (from the oracle's Philox words) so that for one element e
+    the threshold of p64 itself lies at or below its word w while the
+    threshold of float32(p64) lies above it: the device must drop e, as the
+    oracle does when given the binary32 value, although the oracle given
+    p64 would keep it.  Every other decision must match too.  Graph without
+    edges (A_hat = I), H = 1, W = I: Z = 1 everywhere, so H_out is zero
+    exactly where an element is dropped."""
+    n, f, seed, layer, epoch = 64, 8, 987654321, 2, 11
+    e_all = np.arange(n * f, dtype=np.uint64)
+    ctr = np.zeros((n * f // 8, 4), np.uint64)
+    ctr[:, 0] = np.arange(n * f // 8, dtype=np.uint64)
+    ctr[:, 1] = epoch
+    key = np.zeros((n * f // 8, 2), np.uint64)
+    key[:, 0], key[:, 1] = seed, layer
+    out = O.philox4x64(ctr, key)
+    words = np.empty((n * f // 8, 8), np.uint64)
+    words[:, 0::2] = out & np.uint64(0xFFFFFFFF)
+    words[:, 1::2] = out >> np.uint64(32)
+    words = words.reshape(-1)
+    # binary32 spacing in [1/4, 1/2) is 2^-25, i.e. 128 threshold units
+    cand = [int(e) for e in e_all if 2**30 <= int(words[e]) < 2**31 and int(words[e]) % 128 >= 70]
+    assert cand, "no suitable element for this seed"
+    e = cand[0]
+    w = int(words[e])
+    p32 = (w // 128 + 1) / 2.0**25                      # smallest binary32 above w / 2^32
+    p64 = p32 - 0.45 / 2.0**25                          # rounds to p32 in binary32
+    assert f32(p64) == p32 and np.floor(p64 * 2.0**32) <= w < np.floor(p32 * 2.0**32)
+    keep64 = O.dropout_keep(seed, layer, epoch, n, f, p64)
+    keep32 = O.dropout_keep(seed, layer, epoch, n, f, f32(p64))
+    assert keep64.reshape(-1)[e] and not keep32.reshape(-1)[e]
+    empty = np.zeros(0, np.int32)
+    for prec in PRECS:
+        dg = DeviceGraph(n, empty, empty, prec=prec)
+        L = G.GcnLayer(f, f, 8, 8, G.GCN_ACT_RELU, p64, layer, 0)
+        H, W = to_dev(np.ones((n, f)), prec), to_dev(np.eye(f), prec)
+        S = torch.empty((n, 8), dtype=G.torch_dtype(prec), device=dev())
+        Hout = torch.empty_like(S)
+        ov = torch.zeros(1, dtype=torch.int32, device=dev())
+        ws = torch.empty(G.gcn_layer_workspace_size(dg.adj, L, prec), dtype=torch.uint8, device=dev())
+        G.gcn_layer_fwd(dg.adj, L, prec, True, H, W, None, seed, epoch, S, Hout, ov, ws)
+        torch.cuda.synchronize()
+        got = host(Hout, f) != 0
+        assert np.array_equal(got, keep32), PNAME[prec]
 
 
 # ------------------------------------------------------------ layer bwd ----
@@ -262,7 +311,7 @@ def test_layer_bwd(prec, case):
     torch.cuda.synchronize()
     hr, wr, dzr = rounded(h, prec), rounded(w, prec), rounded(dz, prec)
     vals = O.norm_values(g)
-    gs_o, dw_o, db_o, dzb_o = O.layer_bwd(g, vals, hr, wr, dzr, "relu" if act_below else "none", p,
+    gs_o, dw_o, db_o, dzb_o = O.layer_bwd(g, vals, hr, wr, dzr, "relu" if act_below else "none", f32(p),
                                           dense=O.dense_adj(g, vals) if dense else None)
     assert_close(host(GS, f_out), gs_o, prec, "G_S")
     assert_close(dW.cpu().numpy()[:, :f_out], dw_o, prec, "dW")

@@ -163,6 +163,30 @@ def test_spmm_matches_scipy_and_dense():
     ref = sp.csr_matrix((vals, g.colidx, g.rowptr), shape=(n, n)) @ x
     assert np.allclose(y, ref, rtol=1e-13, atol=1e-13)
     assert np.allclose(y, O.dense_adj(g) @ x, rtol=1e-13, atol=1e-13)
+    # row blocks of a few entries (rows split across no block, a block per
+    # row for rows longer than the budget) give the same sums
+    for be in (1, 7, 64):
+        assert np.array_equal(O.spmm(g, vals, x, block_entries=be), y)
+
+
+def test_spmm_general_csr_with_empty_rows():
+    # a CSR that is not of the form A + I: empty rows (first, inner, last),
+    # repeated columns, rectangular use of X's rows
+    rng = np.random.default_rng(11)
+    n = 40
+    counts = rng.integers(0, 6, n)
+    counts[[0, 17, 18, n - 1]] = 0
+    rowptr = np.zeros(n + 1, np.int64)
+    np.cumsum(counts, out=rowptr[1:])
+    colidx = rng.integers(0, n, rowptr[-1]).astype(np.int32)
+    vals = rng.standard_normal(rowptr[-1])
+    g = O.Graph(n, rowptr, colidx)
+    x = rng.standard_normal((n, 5))
+    ref = sp.csr_matrix((vals, colidx, rowptr), shape=(n, n)) @ x
+    for be in (1, 3, 1 << 22):
+        y = O.spmm(g, vals, x, block_entries=be)
+        assert np.allclose(y, ref, rtol=1e-13, atol=1e-13)
+        assert np.all(y[[0, 17, 18, n - 1]] == 0)
 
 
 # ---------------------------------------------------------------- dropout RNG
@@ -389,6 +413,26 @@ def test_adam_first_step_closed_form():
     assert np.allclose(w1, w0 - 0.01 * g / (np.abs(g) + 1e-8), rtol=1e-15)
 
 
+def test_adam_constant_gradient_closed_form_over_many_steps():
+    # a constant gradient g keeps m_t = (1 - b1^t) g and v_t = (1 - b2^t) g^2,
+    # so the bias-corrected moments are exactly g and g^2 at every step t and
+    # each step moves theta by lr * g / (|g| + eps) (Kingma & Ba); after T
+    # steps theta_T = theta_0 - T lr g / (|g| + eps).  A dropped bias
+    # correction, a swapped beta or a missing square root breaks this from
+    # the second step on.
+    g = np.array([3.0, -0.5, 1e-3, -7.0, 1e-8, -2e-8])
+    w0 = np.array([1.0, 2.0, 3.0, 4.0, 5.0, 6.0])
+    st_ = O.AdamState(g.size)
+    sc = O.LossScaler(scale=256.0, interval=10**9)
+    w = w0
+    T = 25
+    for t in range(T):
+        w, applied = O.adam_step(w, g * 256.0, st_, sc, lr=0.01)
+        assert applied
+    assert st_.t == T
+    assert np.allclose(w, w0 - T * 0.01 * g / (np.abs(g) + 1e-8), rtol=1e-13, atol=0)
+
+
 def test_adam_overflow_skips_and_backs_off():
     st_ = O.AdamState(3)
     sc = O.LossScaler(scale=2.0**16)
@@ -510,6 +554,42 @@ def test_adam_half_small_gradient_underflows_to_infinity():
     w3, _, v3 = O.adam_step_half(w0, g, np.zeros(2), np.zeros(2), 1, "bf16")
     assert np.all(v3 > 0)
     assert np.all(np.abs(w3 - (1.0 - 0.01 * np.sign(g))) <= 2 * 2.0**-8)
+
+
+def test_adam_half_first_moment_is_binary32_then_binary16():
+    """O3 reading: each elementwise line is evaluated in binary32, one
+    rounding per arithmetic operation, and the line's result is rounded to
+    binary16.  A case where that differs from rounding the line's exact
+    value once, derived with integers:
+
+    b1 = binary32(0.9) = 15099494 * 2^-24, so 1 - b1 = 1677722 * 2^-24
+    (exact: the operands are within a factor 2).  Take m = -1355 * 2^-11
+    = -0.66162109375 and g = 5 * 2^-4 = 0.3125 (both binary16).
+      b1 * m        = -20459814370 * 2^-35 exactly (35 bits); in binary32
+                      (24 bits: multiples of 2^11 units) -20459814912 * 2^-35.
+      (1 - b1) * g  = 8388610 * 2^-28 = 1073742080 * 2^-35 (exact in binary32).
+      binary32 sum  = -19386072832 * 2^-35, rounded to a multiple of 2^11:
+                      -19386073088 * 2^-35 = -1155.5 * 2^-11, which is the
+                      midpoint of the binary16 neighbours -1155 * 2^-11 and
+                      -1156 * 2^-11; ties to even give -1156 * 2^-11.
+      exact sum     = -19386072290 * 2^-35 = -1155.49995... * 2^-11, which
+                      rounds once to -1155 * 2^-11.
+    So m' = -0.564453125 under the binary32 reading and -0.56396484375
+    under round-once."""
+    bm = 15099494 * -1355                       # b1 * m in units of 2^-35
+    assert bm == -20459814370
+    q, r = divmod(-bm, 2048)                    # binary32 keeps 24 bits: 2^11-unit multiples
+    bm32 = -(q + (r > 1024 or (r == 1024 and q % 2 == 1))) * 2048
+    assert bm32 == -20459814912
+    og = (2**24 - 15099494) * 5 * 128           # (1 - b1) g in units of 2^-35
+    assert og == 1073742080
+    q, r = divmod(-(bm32 + og), 2048)
+    s32 = -(q + (r > 1024 or (r == 1024 and q % 2 == 1))) * 2048
+    assert s32 == -1155 * 2**24 - 2**23          # exactly the binary16 midpoint
+    assert (bm + og) > s32                      # the exact sum lies above it (towards -1155)
+    m1 = np.array([-1355 * 2.0**-11])
+    w1, m2, v2 = O.adam_step_half(np.array([0.5]), np.float32([0.3125]), m1, np.array([0.25]), 2, "f16")
+    assert m2[0] == -1156 * 2.0**-11 == -0.564453125
 
 
 def test_adam_half_tracks_fp64_adam_for_large_gradients():
