@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 6
+#define GCN_ABI_VERSION 7
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -284,6 +284,27 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec,
                          int32_t act_below, float p_below,
                          float* dW, float* dbias, void* dZ_below, void* GS,
                          int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * gcn_layer_bwd_noalloc: gcn_layer_bwd without a workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * or harnesses that forbid hipMalloc).  The call's scratch lives in a fixed
+ * device array of GCN_NOALLOC_SCRATCH_BYTES bytes inside this library, one
+ * per GPU, held until the process ends; the call itself allocates nothing.
+ * Arguments, results and errors are those of gcn_layer_bwd (same kernels,
+ * bit-identical outputs), plus GCN_ERR_CAPACITY when the call would need
+ * more scratch than the array holds (gcn_layer_workspace_size() tells how
+ * much it needs).  Every call on one GPU shares that GPU's array and leaves
+ * its contents behind: calls that overlap on one GPU (several streams or
+ * host threads) race, and the caller must serialise them.  The current HIP
+ * device must be the device of `stream`.
+ * ------------------------------------------------------------------------- */
+#define GCN_NOALLOC_SCRATCH_BYTES (64u << 20)
+gcn_status gcn_layer_bwd_noalloc(const gcn_adj* A, const gcn_layer* L, int32_t prec,
+                                 const void* H, const void* W, const void* dZ,
+                                 int32_t act_below, float p_below,
+                                 float* dW, float* dbias, void* dZ_below, void* GS,
+                                 int32_t* overflow, void* stream);
 
 /* ---------------------------------------------------------------------------
  * gcn_loss: masked mean softmax cross-entropy over logits (n x C, ld, prec)

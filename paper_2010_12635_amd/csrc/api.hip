@@ -3,6 +3,7 @@
 // device memory; scratch comes from the caller's workspace.
 #include <cmath>
 #include <cstdlib>
+#include <mutex>
 
 #include "../../include/gcn.h"
 #include "internal.h"
@@ -412,10 +413,12 @@ gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* 
   return finish(hipSuccess, s);
 }
 
-gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
-                         const void* dZ, int32_t act_below, float p_below, float* dW, float* dbias, void* dZ_below,
-                         void* GS, int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
-  hipStream_t s = static_cast<hipStream_t>(stream);
+namespace {
+
+// Argument checks of gcn_layer_bwd that do not concern the workspace.
+gcn_status layer_bwd_check(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
+                           const void* dZ, int32_t act_below, float p_below, const float* dW, const float* dbias,
+                           const void* dZ_below, const void* GS) {
   if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
   gcn_status st = check_adj(A, prec);
   if (st != GCN_OK) return st;
@@ -430,10 +433,20 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
   if ((H && !aligned16(H)) || !aligned16(W) || !aligned16(dZ) || !aligned16(dW) || !aligned16(GS) ||
       (dZ_below && !aligned16(dZ_below)) || (dbias && !aligned16(dbias)))
     return GCN_ERR_ALIGNMENT;
-  const LayerPlan plan = plan_layer(A, L, prec);
-  if (!workspace || workspace_bytes < plan_bytes(plan)) return GCN_ERR_WORKSPACE;
-  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
-  float* cs = static_cast<float*>(workspace);     // column-sum partials of dZ
+  return GCN_OK;
+}
+
+// The kernel sequence of gcn_layer_bwd on checked arguments; `workspace`
+// holds at least plan_bytes(plan) bytes, 16-byte aligned.  Every scratch
+// word is written before it is read (column-sum, wgrad and chunk partials
+// are stored whole by their producers), so the workspace need not be
+// cleared between calls.
+gcn_status layer_bwd_run(const gcn_adj* A, const gcn_layer* L, int32_t prec, const LayerPlan& plan,
+                         const void* H, const void* W, const void* dZ, int32_t act_below, float p_below, float* dW,
+                         float* dbias, void* dZ_below, void* GS, int32_t* overflow, float* workspace,
+                         hipStream_t s) {
+  const bool ident = L->identity_input != 0;
+  float* cs = workspace;                           // column-sum partials of dZ
   float* ws = cs + plan.cs_floats;                 // per-step scratch
   const int64_t n = A->n;
   const bool dense = A->format != GCN_CSR;
@@ -476,6 +489,68 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
     GCN_HIP(row_product(prec, GS, L->ld_out, W, L->ld_out, true, n, L->f_in, L->f_out, plan.dh_split, ws, ed, s));
   }
   return finish(hipSuccess, s);
+}
+
+
+}  // namespace
+
+gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
+                         const void* dZ, int32_t act_below, float p_below, float* dW, float* dbias, void* dZ_below,
+                         void* GS, int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  gcn_status st = layer_bwd_check(A, L, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS);
+  if (st != GCN_OK) return st;
+  const LayerPlan plan = plan_layer(A, L, prec);
+  if (!workspace || workspace_bytes < plan_bytes(plan)) return GCN_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
+  return layer_bwd_run(A, L, prec, plan, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS, overflow,
+                       static_cast<float*>(workspace), s);
+}
+
+// ---------------------------------------------------------------------------
+// gcn_layer_bwd_noalloc: gcn_layer_bwd with its scratch in a fixed device
+// array of this library instead of a caller workspace.  In host code the
+// array's name is only a stand-in: the kernels get the device address that
+// hipGetSymbolAddress returns for the current device, fetched once per
+// device and kept.
+
+__device__ __align__(256) unsigned char scratch[GCN_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void* scratch_addr[MAX_DEVICES];
+
+gcn_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return GCN_ERR_DEVICE;
+  if (dev < 0 || dev >= MAX_DEVICES) return GCN_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_addr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return GCN_ERR_DEVICE;
+    scratch_addr[dev] = ptr;
+  }
+  *out = scratch_addr[dev];
+  return GCN_OK;
+}
+
+}  // namespace
+
+gcn_status gcn_layer_bwd_noalloc(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
+                                 const void* dZ, int32_t act_below, float p_below, float* dW, float* dbias,
+                                 void* dZ_below, void* GS, int32_t* overflow, void* stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  gcn_status st = layer_bwd_check(A, L, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS);
+  if (st != GCN_OK) return st;
+  const LayerPlan plan = plan_layer(A, L, prec);
+  if (plan_bytes(plan) > (size_t)GCN_NOALLOC_SCRATCH_BYTES) return GCN_ERR_CAPACITY;
+  void* scr = nullptr;
+  st = scratch_of_current_device(&scr);
+  if (st != GCN_OK) return st;
+  return layer_bwd_run(A, L, prec, plan, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS, overflow,
+                       static_cast<float*>(scr), s);
 }
 
 gcn_status gcn_loss_workspace_size(int64_t n, int64_t C, size_t* bytes) {

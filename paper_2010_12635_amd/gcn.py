@@ -19,7 +19,7 @@ __all__ = [
     "GcnAdamConfig", "lib", "LIB_PATH", "EXPORTED", "torch_dtype",
     "gcn_status_string", "gcn_abi_version", "gcn_normalize_workspace_size", "gcn_normalize",
     "gcn_schedule_size", "gcn_schedule", "gcn_layer_workspace_size", "gcn_layer_fwd",
-    "gcn_layer_bwd", "gcn_loss_workspace_size", "gcn_loss", "gcn_optimizer_step",
+    "gcn_layer_bwd", "gcn_layer_bwd_noalloc", "gcn_loss_workspace_size", "gcn_loss", "gcn_optimizer_step",
     "gcn_transform_workspace_size", "gcn_transform", "gcn_aggregate_workspace_size", "gcn_aggregate",
     "gcn_sample_pairs", "gcn_pair_loss_workspace_size", "gcn_pair_loss", "gcn_pair_backward_workspace_size",
     "gcn_pair_backward", "gcn_pair_metrics_workspace_size", "gcn_pair_metrics",
@@ -36,7 +36,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgcn.so")
 EXPORTED = (
     "gcn_status_string", "gcn_abi_version", "gcn_normalize_workspace_size", "gcn_normalize",
     "gcn_schedule_size", "gcn_schedule", "gcn_layer_workspace_size", "gcn_layer_fwd",
-    "gcn_layer_bwd", "gcn_loss_workspace_size", "gcn_loss", "gcn_optimizer_step",
+    "gcn_layer_bwd", "gcn_layer_bwd_noalloc", "gcn_loss_workspace_size", "gcn_loss", "gcn_optimizer_step",
     "gcn_transform_workspace_size", "gcn_transform", "gcn_aggregate_workspace_size", "gcn_aggregate",
     "gcn_dense_tiled_elems", "gcn_densify",
     "gcn_sample_pairs", "gcn_pair_loss_workspace_size", "gcn_pair_loss", "gcn_pair_backward_workspace_size",
@@ -122,6 +122,7 @@ def lib():
                                 P, P, P, P, SZ, P]),
         "gcn_layer_bwd": (I32, [PADJ, PLAY, I32, P, P, P, I32, ctypes.c_float, P, P, P, P, P, P,
                                 SZ, P]),
+        "gcn_layer_bwd_noalloc": (I32, [PADJ, PLAY, I32, P, P, P, I32, ctypes.c_float, P, P, P, P, P, P]),
         "gcn_loss_workspace_size": (I32, [I64, I64, PSZ]),
         "gcn_loss": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, P, P, P, P, SZ, P]),
         "gcn_optimizer_step": (I32, [I64, P, P, P, P, P, I32, ctypes.POINTER(GcnAdamConfig), P, P, P]),
@@ -230,6 +231,17 @@ def gcn_layer_bwd(adj, layer, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_
                              _ptr(overflow), _ptr(workspace), workspace.numel() * workspace.element_size(),
                              _stream(stream))
     _check(st, "gcn_layer_bwd")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20    # GCN_NOALLOC_SCRATCH_BYTES
+
+
+def gcn_layer_bwd_noalloc(adj, layer, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS, overflow,
+                          stream=None):
+    st = lib().gcn_layer_bwd_noalloc(ctypes.byref(adj), ctypes.byref(layer), prec, _ptr(H), _ptr(W), _ptr(dZ),
+                                     act_below, p_below, _ptr(dW), _ptr(dbias), _ptr(dZ_below), _ptr(GS),
+                                     _ptr(overflow), _stream(stream))
+    _check(st, "gcn_layer_bwd_noalloc")
 
 
 def gcn_loss_workspace_size(n, C) -> int:

@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert G.gcn_abi_version() == 6
+    assert G.gcn_abi_version() == 7
     assert G.gcn_status_string(0) == "GCN_OK"
     for s in range(1, 9):
         assert G.gcn_status_string(s).startswith("GCN_ERR_")
@@ -154,3 +154,25 @@ def test_cast_and_half_optimizer_validation_codes():
     assert h(10, 0x1000, 0x2000, 0x3000, None, None, 1, ctypes.byref(cfg), 0x5000, 0x6000, None) == 1
     bad = G.GcnAdamConfig(0.0, 0.9, 0.999, 1e-8, 0.5, 2.0, 2000, 1.0, 2.0**24)
     assert h(10, 0x1000, 0x2000, 0x3000, 0x4000, None, 1, ctypes.byref(bad), 0x5000, 0x6000, None) == 1
+
+
+def test_layer_bwd_noalloc_validation_codes():
+    # the same argument checks as gcn_layer_bwd, then the size of the
+    # library's fixed scratch array: both before anything touches a device
+    lib = G.lib()
+    L = G.GcnLayer(16, 8, 16, 8, G.GCN_ACT_NONE, 0.0, 0, 0)
+
+    def call(adj, layer, prec=G.GCN_F16, H=0x10000):
+        return lib.gcn_layer_bwd_noalloc(ctypes.byref(adj), ctypes.byref(layer), prec, H, 0x20000, 0x30000,
+                                         G.GCN_ACT_RELU, 0.5, 0x40000, None, None, 0x50000, None, None)
+
+    assert call(_adj(), L, prec=7) == 1                                   # bad precision
+    assert call(_adj(), L, H=0x10004) == 3                                # misaligned
+    assert call(_adj(n=0), L) == 2
+    # dense A_hat of 2^20 vertices with 64 gradient columns: the transposed
+    # dZ alone needs 128 MiB of scratch, more than the array holds
+    a = _adj(n=1 << 20, fmt=G.GCN_DENSE_TILED)
+    a.dense = 0x8000
+    big = G.GcnLayer(64, 64, 64, 64, G.GCN_ACT_NONE, 0.0, 0, 0)
+    assert G.gcn_layer_workspace_size(a, big, G.GCN_F16) > G.NOALLOC_SCRATCH_BYTES
+    assert call(a, big) == 5                                              # GCN_ERR_CAPACITY
