@@ -508,6 +508,46 @@ def summarize_counters(fetch_dir, write_dir, out_path, command):
     return summary
 
 
+def summarize_mfma(pmc_dir, out_path, command):
+    """Matrix-core activity per kernel from one rocprofv3 --pmc run of
+    SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_F16/_F32 and
+    GRBM_GUI_ACTIVE: utilisation = busy cycles summed over the SIMDs /
+    (GPU-active cycles x 1024 SIMDs), as rocprofv3's MfmaUtil; executed
+    flops = MOPS x 512, over the dispatch's duration."""
+    import csv
+    from collections import defaultdict
+    rows = list(csv.DictReader(open(os.path.join(pmc_dir, "run_counter_collection.csv"))))
+    per = defaultdict(lambda: defaultdict(dict))
+    for r in rows:
+        per[r["Kernel_Name"]][int(r["Dispatch_Id"])][r["Counter_Name"]] = float(r["Counter_Value"])
+        per[r["Kernel_Name"]][int(r["Dispatch_Id"])]["_ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    lines = ["# Matrix-core (MFMA) counters", "", "Command (from the repository root, on one MI355X):", "", "```", command,
+             "```", "", "Per kernel, averaged over its dispatches: `util` = SQ_VALU_MFMA_BUSY_CYCLES / "
+             "(GRBM_GUI_ACTIVE x 1024 SIMDs) (rocprofv3's MfmaUtil); `TFLOP/s` = (SQ_INSTS_VALU_MFMA_MOPS_F16 + "
+             "_F32) x 512 / dispatch time (the profiler's own clock, slowed by counter collection); `peak frac` "
+             "against 2500 (f16) or 157.3 (fp32) TFLOP/s.", "",
+             "| kernel | dispatches | avg us | util % | MFMA TFLOP/s | peak frac |", "|---|---:|---:|---:|---:|---:|"]
+    out = {}
+    for k, disp in sorted(per.items(), key=lambda kv: -sum(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for d in kv[1].values())):
+        ds = [d for d in disp.values() if "SQ_VALU_MFMA_BUSY_CYCLES" in d and "GRBM_GUI_ACTIVE" in d]
+        if not ds or sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] for d in ds) == 0:
+            continue
+        util = sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] / (d["GRBM_GUI_ACTIVE"] * 1024) for d in ds) / len(ds)
+        f16 = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0) + d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) for d in ds)
+        f32 = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0) for d in ds)
+        ns = sum(d["_ns"] for d in ds)
+        tf = (f16 + f32) * 512 / (ns * 1e-9) / 1e12
+        peak = 2500.0 if f16 >= f32 else 157.3
+        name = k.replace("gcn::(anonymous namespace)::", "")
+        name = name if len(name) < 100 else name[:100] + "..."
+        lines.append(f"| `{name}` | {len(ds)} | {ns / len(ds) / 1e3:.1f} | {100 * util:.1f} | {tf:.1f} | {tf / peak:.3f} |")
+        out[name] = dict(util=round(util, 4), tflops=round(tf, 1), peak_frac=round(tf / peak, 4), avg_us=round(ns / len(ds) / 1e3, 1))
+    lines += ["", "```json", json.dumps(out, indent=1), "```", ""]
+    with open(out_path, "w") as fh:
+        fh.write("\n".join(lines))
+    return out
+
+
 def summarize_stats(stats_dir, out_path, command, title):
     """Kernel time table from a rocprofv3 --stats run (run_kernel_stats.csv)."""
     import csv
@@ -661,6 +701,9 @@ def main():
                     help="write a kernel time table from a rocprofv3 --stats folder and exit")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the traffic summary from two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--summarize-mfma", nargs=2, metavar=("PMC_DIR", "OUT_MD"),
+                    help="write the matrix-core counter table from a rocprofv3 --pmc output folder and exit "
+                         "(with --stats-command: the command that produced it)")
     args = ap.parse_args()
 
     if args.summarize_stats:
@@ -668,6 +711,12 @@ def main():
         if not args.stats_command:
             sys.exit("--summarize-stats needs --stats-command (the command that produced the statistics)")
         summarize_stats(d, out, args.stats_command, title)
+        return
+
+    if args.summarize_mfma:
+        if not args.stats_command:
+            sys.exit("--summarize-mfma needs --stats-command (the command that produced the counters)")
+        print(json.dumps(summarize_mfma(*args.summarize_mfma, args.stats_command)))
         return
 
     if args.summarize_counters:

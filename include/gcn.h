@@ -31,7 +31,7 @@
  *            ignored; columns [f, ld) of an output may be overwritten with 0.
  * Streams.   `stream` is a hipStream_t (NULL = default stream).  All calls are
  *            asynchronous on it, except gcn_normalize and gcn_schedule, which
- *            synchronise it once to return sizes to the host.
+ *            synchronise it (once and twice) to return sizes to the host.
  * Errors.    Every call validates its arguments on the host before it
  *            launches anything and returns a gcn_status; a call that returns
  *            an argument error has had no effect.  GCN_ERR_DEVICE reports a
@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 7
+#define GCN_ABI_VERSION 8
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -78,11 +78,17 @@ typedef enum gcn_act { GCN_ACT_NONE = 0, GCN_ACT_RELU = 1 } gcn_act;
  * DENSE_TILED: the dense matrix stored in matrix-core operand order (see
  * gcn_densify); ld_dense is ignored.
  * The heavy-row schedule (filled by gcn_schedule) lets the CSR product split
- * rows with more than heavy_threshold entries across workgroups; with
- * n_heavy == 0 every row is processed whole.  gcn_schedule also lists the
- * other ("light") rows in order of decreasing degree (row_perm), so that the
- * rows a wavefront processes together have similar lengths; with
- * row_perm == NULL rows are processed in index order. */
+ * rows with more than heavy_threshold entries into pieces that separate lane
+ * groups sum, each into an fp32 partial row, the partials of a row then
+ * added in piece order (run-to-run deterministic); with n_heavy == 0 every
+ * row is processed whole.  With col_parts = P > 1 the columns are cut into
+ * P ranges [p n / P, (p + 1) n / P) and a heavy row's pieces never cross a
+ * range boundary; the pieces of range p run on the chip's XCD p mod 8, so
+ * each XCD's L2 caches the rows of X of its own column ranges only.
+ * gcn_schedule also lists the other ("light") rows in order of decreasing
+ * degree (row_perm), so that the rows a wavefront processes together have
+ * similar lengths; with row_perm == NULL rows are processed in index
+ * order. */
 typedef struct gcn_adj {
   int64_t n;
   int64_t nnz;
@@ -97,16 +103,30 @@ typedef struct gcn_adj {
   const void* dense;     /* [n x ld_dense] (GCN_DENSE) */
   int64_t ld_dense;
   int64_t heavy_threshold;        /* rows with more entries are "heavy"      */
-  int64_t chunk_nnz;              /* entries per chunk of a heavy row        */
+  int64_t chunk_nnz;              /* most entries in one piece of a heavy row */
   int64_t n_heavy;                /* number of heavy rows                    */
-  int64_t n_chunks;               /* total chunks over all heavy rows        */
+  int64_t n_chunks;               /* total pieces over all heavy rows        */
   const int32_t* heavy_rows;      /* [n_heavy] ascending row ids             */
-  const int32_t* heavy_chunk_off; /* [n_heavy + 1] first chunk of each row   */
-  const int32_t* chunk_heavy;     /* [n_chunks] heavy-row slot of a chunk    */
+  const int32_t* heavy_chunk_off; /* [n_heavy + 1] first piece of each row   */
+  const int32_t* chunk_heavy;     /* [n_chunks] heavy-row slot of a piece    */
   int64_t n_light;                /* rows listed in row_perm                 */
   const int32_t* row_perm;        /* [n_light] light rows, degree descending */
-  const int32_t* chunk_order;     /* [n_chunks] launch order of the chunks by
-                                     their first column, or NULL            */
+  const int32_t* chunk_order;     /* [n_chunks] pieces by the column of their
+                                     first entry (grouped by column range)  */
+  const int64_t* chunk_beg;       /* [n_chunks + 1] first entry of each piece
+                                     (pieces of a row are consecutive)      */
+  const int64_t* part_off;        /* [col_parts + 1] pieces of column range p
+                                     are chunk_order[part_off[p] ..
+                                     part_off[p + 1])                       */
+  int64_t col_parts;              /* column ranges P: 1 or a multiple of 8   */
+  int64_t part_slots;             /* most pieces on one XCD (P > 1)          */
+  const void* piece_desc;         /* [n_chunks] 16-byte piece descriptors in
+                                     chunk_order positions                  */
+  const int32_t* piece_pos;       /* [n_chunks] chunk_order position of each
+                                     piece                                  */
+  const void* row_desc;           /* [n_light] 16-byte light-row descriptors
+                                     in row_perm order (required with
+                                     row_perm)                              */
 } gcn_adj;
 
 /* One layer: H (n x f_in, ld_in) -> H_out (n x f_out, ld_out); W is
@@ -198,21 +218,26 @@ gcn_status gcn_densify(const gcn_adj* A, int32_t format, int32_t value_prec, voi
 
 /* ---------------------------------------------------------------------------
  * gcn_schedule: fill the heavy-row fields of a CSR gcn_adj (n, nnz, index,
- * rowptr, colidx must be set) so that rows with more than heavy_threshold
- * entries are aggregated in chunks of chunk_nnz entries by separate
- * workgroups and summed in a fixed order (run-to-run deterministic), the
- * remaining rows listed by decreasing length (row_perm), and the chunks
- * launched in order of their first column (chunk_order; chunks of
- * different hubs that cover the same column range then run together and
- * share the cached rows of X).  The launch orders are permutations whose
- * ties may come out in any order; results do not depend on them.
- * heavy_threshold <= 0 and chunk_nnz <= 0 select the defaults (512 and
- * 2048).  sched: device buffer of at least gcn_schedule_size() bytes that
- * must outlive every use of *A.  Synchronises `stream` once.
+ * rowptr, colidx must be set).  Rows with more than heavy_threshold entries
+ * are cut into pieces: first at the boundaries of the col_parts column
+ * ranges, then every chunk_nnz entries; a lane group sums each piece into
+ * an fp32 partial row and a fix-up adds a row's partials in piece order
+ * (run-to-run deterministic).  The pieces are launched grouped by column
+ * range (range p on XCD p mod 8) and, inside a range, in order of the
+ * column of their first entry (chunk_order; pieces of different hubs that
+ * cover the same columns then run together and share the cached rows of
+ * X).  The remaining rows are listed by decreasing length (row_perm).  The
+ * launch orders are permutations whose ties may come out in any order;
+ * results do not depend on them.  heavy_threshold <= 0, chunk_nnz <= 0 and
+ * col_parts <= 0 select the defaults (heavy_threshold 128, chunk_nnz 256,
+ * col_parts 1); col_parts must
+ * otherwise be 1, 8, 16, 32 or 64 (GCN_ERR_INVALID_ARG).  sched: device
+ * buffer of at least gcn_schedule_size() bytes (same arguments) that must
+ * outlive every use of *A.  Synchronises `stream` twice.
  * ------------------------------------------------------------------------- */
 gcn_status gcn_schedule_size(int64_t n, int64_t nnz, int64_t heavy_threshold, int64_t chunk_nnz,
-                             size_t* bytes);
-gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz,
+                             int64_t col_parts, size_t* bytes);
+gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, int64_t col_parts,
                         void* sched, size_t sched_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------

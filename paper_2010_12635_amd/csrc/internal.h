@@ -9,6 +9,11 @@
 
 namespace gcn {
 
+// Accelerator complex dies of gfx950 (MI355X): consecutive workgroups of a
+// launch are dealt to them in turn, workgroup w to die w % XCDS, each die
+// with its own L2.
+constexpr int64_t XCDS = 8;
+
 // ----------------------------------------------------------------- GEMM ----
 // C[M x N] = sum_k A(m, k) * B(k, n) with fp32 accumulation on MFMA.
 // A(m, k) = a_kc ? A[m * lda + k] : A[k * lda + m]
@@ -55,6 +60,15 @@ hipError_t colsum_partial_launch(int prec, const void* X, int64_t rows, int64_t 
                                  int64_t ldp, int* splits, hipStream_t s);
 
 // ----------------------------------------------------------------- SpMM ----
+// Where a light row or a heavy-row piece lies: first entry, row, number of
+// entries (pieces: bit 31 set when the piece is its row's only one).
+struct RowDesc {
+  int64_t beg;
+  int32_t row;
+  int32_t len;
+};
+static_assert(sizeof(RowDesc) == 16, "one 16-byte load per descriptor");
+
 struct CsrView {
   int64_t n, nnz;
   bool idx64;
@@ -68,7 +82,13 @@ struct CsrView {
   const int32_t* chunk_heavy;
   int64_t n_light;
   const int32_t* row_perm;   // light rows, degree descending (NULL: index order)
-  const int32_t* chunk_order;  // launch order of the heavy chunks (NULL: chunk order)
+  const int32_t* chunk_order;  // pieces by first column, grouped by column range
+  const int64_t* chunk_beg;    // [n_chunks + 1] first entry of each piece
+  const int64_t* part_off;     // [parts + 1] ranges of chunk_order per column range
+  int64_t parts, part_slots;   // column ranges (1 or a multiple of XCDS); most pieces per XCD
+  const RowDesc* piece_desc;   // [n_chunks] in chunk_order positions
+  const int32_t* piece_pos;    // [n_chunks] chunk_order position of each piece
+  const RowDesc* row_desc;     // [n_light] in row_perm order
 };
 // Y = A_hat X (+ epilogue) for X: n x F (ld), Y described by epi.
 int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F);
@@ -110,12 +130,18 @@ hipError_t normalize_run(int64_t n, int64_t num_edges, const int32_t* src, const
                          int value_prec, void* values, void* dense, int64_t ld_dense,
                          int64_t* nnz_out, int32_t* bad_ids, void* ws, size_t ws_bytes,
                          hipStream_t s);
-size_t schedule_bytes(int64_t n, int64_t nnz, int64_t threshold, int64_t chunk_nnz);
+// Heavy-row pieces and light-row order (see gcn_schedule in gcn.h); the
+// pointers returned point into `sched`.
+struct SchedOut {
+  int32_t *heavy_rows, *heavy_chunk_off, *chunk_heavy, *row_perm, *chunk_order, *piece_pos;
+  int64_t *chunk_beg, *part_off;
+  RowDesc *piece_desc, *row_desc;
+  int64_t n_heavy, n_chunks, n_light, part_slots;
+};
+size_t schedule_bytes(int64_t n, int64_t nnz, int64_t threshold, int64_t chunk_nnz, int64_t parts);
 hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, const int32_t* colidx,
-                        int64_t threshold, int64_t chunk_nnz, void* sched, size_t sched_bytes,
-                        int32_t** heavy_rows, int32_t** heavy_chunk_off, int32_t** chunk_heavy,
-                        int32_t** row_perm, int32_t** chunk_order, int64_t* n_heavy, int64_t* n_chunks,
-                        int64_t* n_light, hipStream_t s);
+                        int64_t threshold, int64_t chunk_nnz, int64_t parts, void* sched, size_t sched_bytes,
+                        SchedOut* out, hipStream_t s);
 
 // ----------------------------------------------------------------- loss ----
 size_t loss_workspace_bytes(int64_t n, int64_t C);

@@ -14,6 +14,7 @@
 //   values   dinv[row] * dinv[col] in the value precision; optional dense
 #include "internal.h"
 
+#include <algorithm>
 #include <vector>
 
 namespace gcn {
@@ -313,31 +314,70 @@ __global__ __launch_bounds__(256) void values_kernel(int64_t n, const int64_t* _
 }
 
 // ---------------------------------------------------------------- schedule ----
+// Heavy rows are cut into pieces: at the boundaries of the P column ranges
+// (column c lies in range floor(c P / n)) and then every `seg` entries.
+// Range q ends at the first entry of the (sorted) row whose column c has
+// c P >= (q + 1) n, i.e. c >= ceil((q + 1) n / P).
+// First column of range q: ceil(q n / P).
+__device__ __forceinline__ int64_t range_first(int64_t q, int64_t n, int64_t parts) {
+  return (q * n + parts - 1) / parts;
+}
+
+__device__ __forceinline__ int64_t range_end(const int32_t* __restrict__ colidx, int64_t lo, int64_t hi, int64_t bound) {
+  while (lo < hi) {                       // first k in [lo, hi) with colidx[k] >= bound
+    const int64_t mid = lo + ((hi - lo) >> 1);
+    if ((int64_t)colidx[mid] < bound) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
 template <typename IdxT>
-__global__ void heavy_flag_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr, int64_t chunk,
-                                  int64_t* __restrict__ flag, int64_t* __restrict__ nch) {
+__global__ void piece_count_kernel(int64_t n, const IdxT* __restrict__ rowptr, const int32_t* __restrict__ colidx,
+                                   int64_t thr, int64_t seg, int64_t parts, int64_t* __restrict__ flag,
+                                   int64_t* __restrict__ npieces) {
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r <= n; r += (int64_t)gridDim.x * blockDim.x) {
-    if (r == n) { flag[n] = 0; nch[n] = 0; continue; }
-    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
-    const bool h = d > thr;
-    flag[r] = h ? 1 : 0;
-    nch[r] = h ? (d + chunk - 1) / chunk : 0;
+    if (r == n) { flag[n] = 0; npieces[n] = 0; continue; }
+    const int64_t beg = (int64_t)rowptr[r], end = (int64_t)rowptr[r + 1];
+    if (end - beg <= thr) { flag[r] = 0; npieces[r] = 0; continue; }
+    int64_t cnt = 0, a = beg;
+    for (int64_t q = 0; q < parts; ++q) {
+      const int64_t b = q + 1 == parts ? end : range_end(colidx, a, end, range_first(q + 1, n, parts));
+      cnt += (b - a + seg - 1) / seg;
+      a = b;
+    }
+    flag[r] = 1;
+    npieces[r] = cnt;
   }
 }
 
 template <typename IdxT>
-__global__ void heavy_fill_kernel(int64_t n, const IdxT* __restrict__ rowptr, int64_t thr,
-                                  const int64_t* __restrict__ hidx, const int64_t* __restrict__ choff,
+__global__ void piece_fill_kernel(int64_t n, int64_t nnz, const IdxT* __restrict__ rowptr,
+                                  const int32_t* __restrict__ colidx, int64_t thr, int64_t seg, int64_t parts,
+                                  const int64_t* __restrict__ hidx, const int64_t* __restrict__ poff,
                                   int32_t* __restrict__ heavy_rows, int32_t* __restrict__ heavy_chunk_off,
-                                  int32_t* __restrict__ chunk_heavy) {
+                                  int32_t* __restrict__ chunk_heavy, int64_t* __restrict__ chunk_beg) {
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r <= n; r += (int64_t)gridDim.x * blockDim.x) {
-    if (r == n) { heavy_chunk_off[hidx[n]] = (int32_t)choff[n]; continue; }
-    const int64_t d = (int64_t)rowptr[r + 1] - (int64_t)rowptr[r];
-    if (d <= thr) continue;
+    if (r == n) {
+      heavy_chunk_off[hidx[n]] = (int32_t)poff[n];
+      chunk_beg[poff[n]] = nnz;
+      continue;
+    }
+    const int64_t beg = (int64_t)rowptr[r], end = (int64_t)rowptr[r + 1];
+    if (end - beg <= thr) continue;
     const int64_t h = hidx[r];
     heavy_rows[h] = (int32_t)r;
-    heavy_chunk_off[h] = (int32_t)choff[r];
-    for (int64_t c = choff[r]; c < choff[r + 1]; ++c) chunk_heavy[c] = (int32_t)h;
+    heavy_chunk_off[h] = (int32_t)poff[r];
+    int64_t c = poff[r], a = beg;
+    for (int64_t q = 0; q < parts; ++q) {
+      const int64_t b = q + 1 == parts ? end : range_end(colidx, a, end, range_first(q + 1, n, parts));
+      for (int64_t k = a; k < b; k += seg) {
+        chunk_heavy[c] = (int32_t)h;
+        chunk_beg[c] = k;
+        ++c;
+      }
+      a = b;
+    }
   }
 }
 
@@ -419,19 +459,55 @@ __global__ __launch_bounds__(256) void light_scatter_kernel(int64_t n, const Idx
   }
 }
 
-// Chunk launch order: counting sort of the chunks by the column bucket of
-// their first entry (CHUNK_BUCKETS buckets over [0, n)).
+// Piece launch order: counting sort of the pieces by the column bucket of
+// their first entry (CHUNK_BUCKETS buckets over [0, n)).  The bucket of a
+// column, c * 4096 / n, nests in its column range c * P / n for every P
+// that divides 4096, so the sorted pieces of range p are one run, starting
+// at the offset of bucket p * 4096 / P.
 constexpr int64_t CHUNK_BUCKETS = 4096;
 
+__global__ void part_off_kernel(int64_t parts, const int64_t* __restrict__ boff, int64_t* __restrict__ part_off) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q <= parts) part_off[q] = boff[q * (CHUNK_BUCKETS / parts)];
+}
+
+// 16-byte descriptors in launch order, so that a lane group learns where a
+// row or piece lies with one load: light rows {first entry, row, length};
+// pieces {first entry, row, length | 2^31 if the row has no other piece},
+// plus the launch position of every piece (its partial row's slot).
 template <typename IdxT>
-__global__ void chunk_key_kernel(int64_t n, int64_t n_chunks, const IdxT* __restrict__ rowptr,
-                                 const int32_t* __restrict__ colidx, const int32_t* __restrict__ heavy_rows,
-                                 const int32_t* __restrict__ heavy_chunk_off, const int32_t* __restrict__ chunk_heavy,
-                                 int64_t chunk, int32_t* __restrict__ key, int32_t* __restrict__ hist) {
-  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * blockDim.x) {
+__global__ void light_desc_kernel(int64_t n_light, const IdxT* __restrict__ rowptr, const int32_t* __restrict__ perm,
+                                  RowDesc* __restrict__ desc) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_light; i += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t r = perm[i];
+    const int64_t b = (int64_t)rowptr[r];
+    desc[i] = RowDesc{b, r, (int32_t)((int64_t)rowptr[r + 1] - b)};
+  }
+}
+
+template <typename IdxT>
+__global__ void piece_desc_kernel(int64_t n_chunks, const IdxT* __restrict__ rowptr, const int32_t* __restrict__ order,
+                                  const int32_t* __restrict__ chunk_heavy, const int32_t* __restrict__ heavy_rows,
+                                  const int32_t* __restrict__ heavy_chunk_off, const int64_t* __restrict__ chunk_beg,
+                                  RowDesc* __restrict__ desc, int32_t* __restrict__ pos_of) {
+  for (int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; pos < n_chunks; pos += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t c = order[pos];
     const int32_t h = chunk_heavy[c];
-    const int64_t start = (int64_t)rowptr[heavy_rows[h]] + (c - heavy_chunk_off[h]) * chunk;
-    const int32_t b = (int32_t)((int64_t)colidx[start] * CHUNK_BUCKETS / n);
+    const int32_t r = heavy_rows[h];
+    const int64_t b = chunk_beg[c];
+    const int64_t rend = (int64_t)rowptr[r + 1];
+    const int64_t e = chunk_beg[c + 1] < rend ? chunk_beg[c + 1] : rend;
+    const bool single = heavy_chunk_off[h + 1] - heavy_chunk_off[h] == 1;
+    desc[pos] = RowDesc{b, r, (int32_t)((uint32_t)(e - b) | (single ? 0x80000000u : 0u))};
+    pos_of[c] = (int32_t)pos;
+  }
+}
+
+__global__ void chunk_key_kernel(int64_t n, int64_t n_chunks, const int32_t* __restrict__ colidx,
+                                 const int64_t* __restrict__ chunk_beg, int32_t* __restrict__ key,
+                                 int32_t* __restrict__ hist) {
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < n_chunks; c += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t b = (int32_t)((int64_t)colidx[chunk_beg[c]] * CHUNK_BUCKETS / n);
     key[c] = b;
     atomicAdd(&hist[b], 1);
   }
@@ -547,8 +623,16 @@ hipError_t normalize_run(int64_t n, int64_t E, const int32_t* src, const int32_t
   return hipSuccess;
 }
 
-size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
-  const int64_t max_chunks = nnz / chunk_nnz + n + 1;
+// Most pieces a schedule can hold: every heavy row (more than thr entries,
+// so at most nnz / (thr + 1) of them) has at most one piece per column range
+// plus one per chunk_nnz entries.
+int64_t max_pieces(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz, int64_t parts) {
+  const int64_t rows = std::min<int64_t>(n, nnz / (thr + 1));
+  return nnz / chunk_nnz + rows * parts + 1;
+}
+
+size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz, int64_t parts) {
+  const int64_t max_chunks = max_pieces(n, nnz, thr, chunk_nnz, parts);
   const int64_t nb = light_buckets(n, thr);
   int64_t scan_n = (n + 1 > nb + 1) ? n + 1 : nb + 1;
   if (scan_n < CHUNK_BUCKETS + 1) scan_n = CHUNK_BUCKETS + 1;
@@ -561,9 +645,14 @@ size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
   b += align256(sizeof(int32_t) * n);                           // heavy_rows
   b += align256(sizeof(int32_t) * (n + 1));                     // heavy_chunk_off
   b += align256(sizeof(int32_t) * max_chunks);                  // chunk_heavy
+  b += align256(sizeof(int64_t) * (max_chunks + 1));            // chunk_beg
+  b += align256(sizeof(int64_t) * (parts + 1));                 // part_off
+  b += align256(sizeof(RowDesc) * max_chunks);                  // piece descriptors
+  b += align256(sizeof(int32_t) * max_chunks);                  // launch position of each piece
+  b += align256(sizeof(RowDesc) * n);                           // light-row descriptors
   b += align256(sizeof(int32_t) * n);                           // row_perm
   b += align256(sizeof(int64_t) * (n + 1));                     // flags -> heavy index
-  b += align256(sizeof(int64_t) * (n + 1));                     // chunks per row -> chunk offsets
+  b += align256(sizeof(int64_t) * (n + 1));                     // pieces per row -> piece offsets
   b += align256(sizeof(int32_t) * nb);                          // (block, degree) histogram
   b += align256(sizeof(int32_t) * nb);                          // bucket cursors
   b += align256(sizeof(int64_t) * (nb + 1));                    // bucket offsets
@@ -572,12 +661,10 @@ size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz) {
 }
 
 hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, const int32_t* colidx, int64_t thr,
-                        int64_t chunk, void* sched, size_t sched_bytes, int32_t** heavy_rows,
-                        int32_t** heavy_chunk_off, int32_t** chunk_heavy, int32_t** row_perm, int32_t** chunk_order,
-                        int64_t* n_heavy, int64_t* n_chunks, int64_t* n_light, hipStream_t s) {
+                        int64_t chunk, int64_t parts, void* sched, size_t sched_bytes, SchedOut* out, hipStream_t s) {
   char* w = static_cast<char*>(sched);
   auto take = [&](size_t bytes) { char* p = w; w += align256(bytes); return p; };
-  const int64_t max_chunks = nnz / chunk + n + 1;
+  const int64_t max_chunks = max_pieces(n, nnz, thr, chunk, parts);
   const int64_t nb = light_buckets(n, thr);
   int64_t scan_n = (n + 1 > nb + 1) ? n + 1 : nb + 1;
   if (scan_n < CHUNK_BUCKETS + 1) scan_n = CHUNK_BUCKETS + 1;
@@ -589,6 +676,11 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   int32_t* hr = (int32_t*)take(sizeof(int32_t) * n);
   int32_t* hco = (int32_t*)take(sizeof(int32_t) * (n + 1));
   int32_t* ch = (int32_t*)take(sizeof(int32_t) * max_chunks);
+  int64_t* cbeg = (int64_t*)take(sizeof(int64_t) * (max_chunks + 1));
+  int64_t* poff = (int64_t*)take(sizeof(int64_t) * (parts + 1));
+  RowDesc* pdesc = (RowDesc*)take(sizeof(RowDesc) * max_chunks);
+  int32_t* ppos = (int32_t*)take(sizeof(int32_t) * max_chunks);
+  RowDesc* ldesc = (RowDesc*)take(sizeof(RowDesc) * n);
   int32_t* perm = (int32_t*)take(sizeof(int32_t) * n);
   int64_t* hidx = (int64_t*)take(sizeof(int64_t) * (n + 1));
   int64_t* choff = (int64_t*)take(sizeof(int64_t) * (n + 1));
@@ -600,16 +692,16 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   hipError_t e;
 #define GCN_TRY(x) do { e = (x); if (e != hipSuccess) return e; } while (0)
   if (idx64)
-    hipLaunchKernelGGL(heavy_flag_kernel<int64_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, chunk, hidx, choff);
+    hipLaunchKernelGGL(piece_count_kernel<int64_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int64_t*)rowptr, colidx, thr, chunk, parts, hidx, choff);
   else
-    hipLaunchKernelGGL(heavy_flag_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, chunk, hidx, choff);
+    hipLaunchKernelGGL(piece_count_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int32_t*)rowptr, colidx, thr, chunk, parts, hidx, choff);
   GCN_TRY(hipGetLastError());
   GCN_TRY(scan_exclusive(hidx, n + 1, scr, s));
   GCN_TRY(scan_exclusive(choff, n + 1, scr, s));
   if (idx64)
-    hipLaunchKernelGGL(heavy_fill_kernel<int64_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int64_t*)rowptr, thr, hidx, choff, hr, hco, ch);
+    hipLaunchKernelGGL(piece_fill_kernel<int64_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, nnz, (const int64_t*)rowptr, colidx, thr, chunk, parts, hidx, choff, hr, hco, ch, cbeg);
   else
-    hipLaunchKernelGGL(heavy_fill_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, (const int32_t*)rowptr, thr, hidx, choff, hr, hco, ch);
+    hipLaunchKernelGGL(piece_fill_kernel<int32_t>, dim3(grid_for(n + 1)), dim3(256), 0, s, n, nnz, (const int32_t*)rowptr, colidx, thr, chunk, parts, hidx, choff, hr, hco, ch, cbeg);
   GCN_TRY(hipGetLastError());
   // light rows, block by block, by decreasing degree inside a block
   GCN_TRY(fill_zero(hist, sizeof(int32_t) * nb, s));
@@ -632,27 +724,56 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   GCN_TRY(hipMemcpyAsync(&host[1], choff + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipMemcpyAsync(&host[2], boff + nb, sizeof(int64_t), hipMemcpyDeviceToHost, s));
   GCN_TRY(hipStreamSynchronize(s));
-  // chunks in order of the column bucket of their first entry
+  // light-row descriptors in row_perm order
+  if (host[2] > 0) {
+    if (idx64)
+      hipLaunchKernelGGL(light_desc_kernel<int64_t>, dim3(grid_for(host[2])), dim3(256), 0, s, host[2], (const int64_t*)rowptr, perm, ldesc);
+    else
+      hipLaunchKernelGGL(light_desc_kernel<int32_t>, dim3(grid_for(host[2])), dim3(256), 0, s, host[2], (const int32_t*)rowptr, perm, ldesc);
+    GCN_TRY(hipGetLastError());
+  }
+  // pieces in order of the column bucket of their first entry, which groups
+  // them by column range
   const int64_t nch = host[1];
-  *chunk_order = nullptr;
-  if (nch > 0 && colidx) {
+  if (nch > max_chunks) return hipErrorInvalidValue;
+  int64_t slots = 0;
+  if (nch > 0) {
     GCN_TRY(fill_zero(chist, sizeof(int32_t) * CHUNK_BUCKETS, s));
     GCN_TRY(fill_zero(ccur, sizeof(int32_t) * CHUNK_BUCKETS, s));
-    if (idx64)
-      hipLaunchKernelGGL(chunk_key_kernel<int64_t>, dim3(grid_for(nch)), dim3(256), 0, s, n, nch, (const int64_t*)rowptr, colidx, hr, hco, ch, chunk, ckey, chist);
-    else
-      hipLaunchKernelGGL(chunk_key_kernel<int32_t>, dim3(grid_for(nch)), dim3(256), 0, s, n, nch, (const int32_t*)rowptr, colidx, hr, hco, ch, chunk, ckey, chist);
+    hipLaunchKernelGGL(chunk_key_kernel, dim3(grid_for(nch)), dim3(256), 0, s, n, nch, colidx, cbeg, ckey, chist);
     GCN_TRY(hipGetLastError());
     hipLaunchKernelGGL(widen_kernel, dim3(grid_for(CHUNK_BUCKETS + 1)), dim3(256), 0, s, CHUNK_BUCKETS, chist, cboff);
     GCN_TRY(hipGetLastError());
     GCN_TRY(scan_exclusive(cboff, CHUNK_BUCKETS + 1, scr, s));
     hipLaunchKernelGGL(chunk_scatter_kernel, dim3(grid_for(nch)), dim3(256), 0, s, nch, ckey, cboff, ccur, corder);
     GCN_TRY(hipGetLastError());
-    *chunk_order = corder;
+    hipLaunchKernelGGL(part_off_kernel, dim3(grid_for(parts + 1)), dim3(256), 0, s, parts, cboff, poff);
+    GCN_TRY(hipGetLastError());
+    if (idx64)
+      hipLaunchKernelGGL(piece_desc_kernel<int64_t>, dim3(grid_for(nch)), dim3(256), 0, s, nch, (const int64_t*)rowptr, corder, ch, hr, hco, cbeg, pdesc, ppos);
+    else
+      hipLaunchKernelGGL(piece_desc_kernel<int32_t>, dim3(grid_for(nch)), dim3(256), 0, s, nch, (const int32_t*)rowptr, corder, ch, hr, hco, cbeg, pdesc, ppos);
+    GCN_TRY(hipGetLastError());
+    // the most pieces one XCD takes: ranges x, x + 8, ... run on XCD x
+    std::vector<int64_t> hp((size_t)parts + 1);
+    GCN_TRY(hipMemcpyAsync(hp.data(), poff, sizeof(int64_t) * (parts + 1), hipMemcpyDeviceToHost, s));
+    GCN_TRY(hipStreamSynchronize(s));
+    if (parts > 1) {
+      for (int64_t x = 0; x < XCDS; ++x) {
+        int64_t t = 0;
+        for (int64_t q = x; q < parts; q += XCDS) t += hp[q + 1] - hp[q];
+        slots = std::max(slots, t);
+      }
+    } else {
+      slots = nch;
+    }
   }
 #undef GCN_TRY
-  *heavy_rows = hr; *heavy_chunk_off = hco; *chunk_heavy = ch; *row_perm = perm;
-  *n_heavy = host[0]; *n_chunks = host[1]; *n_light = host[2];
+  out->heavy_rows = hr; out->heavy_chunk_off = hco; out->chunk_heavy = ch; out->row_perm = perm;
+  out->chunk_order = nch > 0 ? corder : nullptr;
+  out->chunk_beg = cbeg; out->part_off = poff; out->part_slots = slots;
+  out->piece_desc = pdesc; out->piece_pos = ppos; out->row_desc = ldesc;
+  out->n_heavy = host[0]; out->n_chunks = nch; out->n_light = host[2];
   return hipSuccess;
 }
 

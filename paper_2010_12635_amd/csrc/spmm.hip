@@ -10,14 +10,19 @@
 //    time to keep several gathers in flight.  Rows are taken in the order of
 //    the schedule's permutation (decreasing degree), so the groups of a
 //    wave walk rows of similar length.  fp32 accumulation.
-//  * Heavy rows (power-law hubs): split into chunks of chunk_nnz entries;
-//    one workgroup per chunk reduces its entries across 256/LPR lane groups
-//    through LDS in a fixed order into an fp32 partial row.  Chunks are
-//    launched in the schedule's order of their first column, so chunks of
-//    different hubs that cover the same columns run at the same time and
-//    find those rows of X in cache.  A fixup kernel
-//    sums the partials of each heavy row in chunk order and applies the
-//    epilogue.  No atomics: results are run-to-run identical.
+//  * Heavy rows (power-law hubs): cut by the schedule into pieces that never
+//    cross a column range [q n / P, (q + 1) n / P) and hold at most
+//    chunk_nnz entries; a lane group sums one piece, like a light row, into
+//    an fp32 partial row.  The pieces of range q run on XCD q mod 8 (the
+//    launch deals workgroup w to XCD w mod 8), so the L2 of each die only
+//    caches rows of X from its own 1/P-th of the columns: on R-MAT graphs,
+//    whose hubs' neighbours are spread over every column, this is what
+//    makes the gathered rows of the hubs hit in L2.  Inside a range the
+//    pieces run in order of their first column.  A fix-up sums each heavy
+//    row's partials in piece order (4 waves over quarters of the pieces,
+//    then the quarters in wave order) and applies the epilogue; a row of
+//    one piece is stored by its piece.  No atomics: results are run-to-run
+//    identical.
 #include "internal.h"
 
 namespace gcn {
@@ -27,13 +32,12 @@ namespace {
 template <typename IdxT>
 struct SpmmParams {
   int64_t n;
-  int64_t n_rows;               // rows to process: n_light with a permutation, else n
-  const int32_t* row_perm;      // may be NULL
+  int64_t n_rows;               // rows to process: n_light with descriptors, else n
+  const RowDesc* row_desc;      // light rows in schedule order (NULL: every row, index order)
   const IdxT* rowptr;
   const int32_t* colidx;
   const void* values;
   const float* dinv;
-  int64_t heavy_threshold;      // 0: no heavy split
   const void* X;
   int64_t ldx;
   int64_t F;
@@ -97,8 +101,35 @@ __device__ __forceinline__ void gather_tail(float* acc, const T* __restrict__ X,
   }
 }
 
+// Entries [e, end) of one row into acc: rounds of 8 gathers, then the tail.
+template <typename T, int LPR, bool HAS_VAL>
+__device__ __forceinline__ void row_sum(float* acc, const T* __restrict__ X, int64_t ldx,
+                                        const int32_t* __restrict__ colidx, const void* values, const float* dinv,
+                                        float drow, int64_t e, int64_t end) {
+  for (; e + 8 <= end; e += 8) gather_block<T, HAS_VAL, 8>(acc, X, ldx, colidx, values, dinv, drow, e, 1);
+  if constexpr (LPR * Vec<T>::N * (int)sizeof(T) <= 256) {
+    // neighbour rows of at most 256 bytes: the walk is bound by dependent
+    // load latency, so the last 1 .. 7 entries go in one round rather than
+    // a round of 4 and single steps (up to 5 dependent rounds)
+    if (e < end) gather_tail<T, HAS_VAL, 8>(acc, X, ldx, colidx, values, dinv, drow, e, end);
+  } else {
+    // wider rows are bound by the gathered bytes, which the in-bounds
+    // repeats of a one-round tail would add to
+    if (e + 4 <= end) {
+      gather_block<T, HAS_VAL, 4>(acc, X, ldx, colidx, values, dinv, drow, e, 1);
+      e += 4;
+    }
+    for (; e < end; ++e) gather_block<T, HAS_VAL, 1>(acc, X, ldx, colidx, values, dinv, drow, e, 1);
+  }
+}
+
+__device__ __forceinline__ int64_t desc_beg(uint4 d) { return (int64_t)((uint64_t)d.x | ((uint64_t)d.y << 32)); }
+
 // Light rows for workgroup bx of nbx (bx: position among the light-row
-// workgroups of the launch).
+// workgroups of the launch).  With the schedule's descriptors a lane group
+// walks rows slot, slot + stride, ... and loads the next row's descriptor
+// before it gathers the current row, so that one dependent load (instead
+// of the permutation and the row pointers) stands between two rows.
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 __device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, int64_t bx, int64_t nbx) {
   constexpr int VE = Vec<T>::N;
@@ -108,32 +139,35 @@ __device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, int64_
   const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
   if (col0 >= p.F) return;
   const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
-  // the grid is capped (at most 2^32 work-items per dispatch dimension):
-  // a workgroup takes row slots bx, bx + nbx, ...
-  for (int64_t slot = (bx * 4 + wave) * G + g; slot < p.n_rows; slot += nbx * 4 * G) {
-    const int64_t row = p.row_perm ? (int64_t)p.row_perm[slot] : slot;
+  const int64_t stride = nbx * 4 * G;
+  int64_t slot = (bx * 4 + wave) * G + g;
+  if (p.row_desc) {
+    uint4 d = slot < p.n_rows ? ldg16(p.row_desc + slot) : make_uint4(0, 0, 0, 0);
+    while (slot < p.n_rows) {
+      const int64_t beg = desc_beg(d);
+      const int64_t row = (int64_t)(int32_t)d.z;
+      const int64_t end = beg + (int64_t)(int32_t)d.w;
+      const int64_t nslot = slot + stride;
+      if (nslot < p.n_rows) d = ldg16(p.row_desc + nslot);
+      const float drow = HAS_VAL ? 0.f : p.dinv[row];
+      float acc[VE];
+#pragma unroll
+      for (int i = 0; i < VE; ++i) acc[i] = 0.f;
+      row_sum<T, LPR, HAS_VAL>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, beg, end);
+      epi_store_vec<T>(p.epi, row, col0, acc);
+      slot = nslot;
+    }
+    return;
+  }
+  // no schedule: every row, in index order
+  for (; slot < p.n_rows; slot += stride) {
+    const int64_t row = slot;
     const int64_t beg = (int64_t)p.rowptr[row], end = (int64_t)p.rowptr[row + 1];
-    if (!p.row_perm && p.heavy_threshold > 0 && end - beg > p.heavy_threshold) continue;
     const float drow = HAS_VAL ? 0.f : p.dinv[row];
     float acc[VE];
 #pragma unroll
     for (int i = 0; i < VE; ++i) acc[i] = 0.f;
-    int64_t e = beg;
-    for (; e + 8 <= end; e += 8) gather_block<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-    if constexpr (LPR * Vec<T>::N * (int)sizeof(T) <= 256) {
-      // neighbour rows of at most 256 bytes: the walk is bound by dependent
-      // load latency, so the last 1 .. 7 entries go in one round rather than
-      // a round of 4 and single steps (up to 5 dependent rounds)
-      if (e < end) gather_tail<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, end);
-    } else {
-      // wider rows are bound by the gathered bytes, which the in-bounds
-      // repeats of a one-round tail would add to
-      if (e + 4 <= end) {
-        gather_block<T, HAS_VAL, 4>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-        e += 4;
-      }
-      for (; e < end; ++e) gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, 1);
-    }
+    row_sum<T, LPR, HAS_VAL>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, beg, end);
     epi_store_vec<T>(p.epi, row, col0, acc);
   }
 }
@@ -143,120 +177,134 @@ __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
   spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, blockIdx.x, gridDim.x);
 }
 
-template <typename IdxT>
-struct HeavyParams {
-  const IdxT* rowptr;
+struct PieceParams {
+  const RowDesc* desc;          // [n_chunks] in launch (chunk_order) positions
+  const int32_t* pos_of;        // [n_chunks] launch position of each piece
+  const int32_t* heavy_rows;
+  const int32_t* heavy_chunk_off;
+  const int64_t* part_off;
+  int64_t n_chunks;
+  int64_t parts;
   const int32_t* colidx;
   const void* values;
   const float* dinv;
-  const int32_t* heavy_rows;
-  const int32_t* heavy_chunk_off;
-  const int32_t* chunk_heavy;
-  const int32_t* chunk_order;   // launch order (may be NULL)
-  int64_t chunk_nnz;
-  int64_t n_chunks;
   const void* X;
   int64_t ldx;
   int64_t F;
   int64_t ldp;                  // floats per partial row
-  float* partials;              // [n_chunks][ldp]
+  float* partials;              // [n_chunks][ldp], by launch position
   Epilogue epi;
 };
 
-// One workgroup per (chunk, column block): launch position bx of the chunks.
-template <typename T, typename IdxT, int LPR, bool HAS_VAL>
-__device__ __forceinline__ void spmm_heavy_body(const HeavyParams<IdxT>& p, int64_t bx) {
+// Launch position of the k-th piece of die x's list, or -1: with column
+// ranges die x takes the pieces of ranges x, x + XCDS, ... in turn; without,
+// there is one list.
+__device__ __forceinline__ int64_t piece_at(const PieceParams& p, int64_t x, int64_t k) {
+  if (p.parts <= 1) return k < p.n_chunks ? k : -1;
+  for (int64_t q = x; q < p.parts; q += XCDS) {
+    const int64_t len = p.part_off[q + 1] - p.part_off[q];
+    if (k < len) return p.part_off[q] + k;
+    k -= len;
+  }
+  return -1;
+}
+
+// Piece workgroup w of nw: its lane groups walk their die's list with the
+// next piece's descriptor loaded ahead (nw is a multiple of XCDS when there
+// are column ranges, so piece workgroup w runs on die w % XCDS).
+template <typename T, int LPR, bool HAS_VAL>
+__device__ __forceinline__ void spmm_piece_body(const PieceParams& p, int64_t w, int64_t nw) {
   constexpr int VE = Vec<T>::N;
-  constexpr int NG = 256 / LPR;
-  __shared__ float red[4 * LPR * VE];
-  const int64_t chunk = p.chunk_order ? (int64_t)p.chunk_order[bx] : bx;
-  const int g = threadIdx.x / LPR, li = threadIdx.x % LPR;
-  const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
-  const int32_t h = p.chunk_heavy[chunk];
-  const int64_t row = p.heavy_rows[h];
-  const int64_t rbeg = (int64_t)p.rowptr[row], rend = (int64_t)p.rowptr[row + 1];
-  const int64_t cbeg = rbeg + (chunk - p.heavy_chunk_off[h]) * p.chunk_nnz;
-  const int64_t cend = min(rend, cbeg + p.chunk_nnz);
-  float acc[VE];
-#pragma unroll
-  for (int i = 0; i < VE; ++i) acc[i] = 0.f;
-  if (col0 < p.F) {
-    const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
-    const float drow = HAS_VAL ? 0.f : p.dinv[row];
-    int64_t e = cbeg + g;
-    for (; e + 7 * NG < cend; e += 8 * NG)
-      gather_block<T, HAS_VAL, 8>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, NG);
-    for (; e < cend; e += NG)
-      gather_block<T, HAS_VAL, 1>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, e, NG);
-  }
-  // reduce over the lane groups of a wave (xor butterfly over the group
-  // bits of the lane id), then over the 4 waves through LDS in wave order
-#pragma unroll
-  for (int o = 32; o >= LPR; o >>= 1)
-#pragma unroll
-    for (int i = 0; i < VE; ++i) acc[i] += __shfl_xor(acc[i], o);
+  constexpr int G = 64 / LPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane < LPR) {
+  const int g = lane / LPR, li = lane % LPR;
+  const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
+  if (col0 >= p.F) return;
+  const bool ranges = p.parts > 1;
+  const int64_t x = ranges ? w % XCDS : 0;
+  const int64_t j = ranges ? w / XCDS : w;
+  const int64_t per = ranges ? nw / XCDS : nw;
+  int64_t k = j * (4 * G) + wave * G + g;
+  const int64_t stride = per * (4 * G);
+  int64_t pos = piece_at(p, x, k);
+  uint4 d = pos >= 0 ? ldg16(p.desc + pos) : make_uint4(0, 0, 0, 0);
+  const T* __restrict__ X = reinterpret_cast<const T*>(p.X) + col0;
+  while (pos >= 0) {
+    const int64_t beg = desc_beg(d);
+    const int64_t row = (int64_t)(int32_t)d.z;
+    const int64_t end = beg + (int64_t)(d.w & 0x7fffffffu);
+    const bool single = (d.w & 0x80000000u) != 0;
+    k += stride;
+    const int64_t npos = piece_at(p, x, k);
+    if (npos >= 0) d = ldg16(p.desc + npos);
+    const float drow = HAS_VAL ? 0.f : p.dinv[row];
+    float acc[VE];
 #pragma unroll
-    for (int i = 0; i < VE; ++i) red[(wave * LPR + lane) * VE + i] = acc[i];
-  }
-  __syncthreads();
-  if (threadIdx.x < LPR && col0 < p.ldp) {
-    float s[VE];
-#pragma unroll
-    for (int i = 0; i < VE; ++i) {
-      s[i] = red[(0 * LPR + li) * VE + i] + red[(1 * LPR + li) * VE + i];
-      s[i] += red[(2 * LPR + li) * VE + i];
-      s[i] += red[(3 * LPR + li) * VE + i];
-    }
-    if (p.heavy_chunk_off[h + 1] - p.heavy_chunk_off[h] == 1) {
-      // the row's only chunk holds its whole sum: the epilogue stores it here
-      if (col0 < p.F) epi_store_vec<T>(p.epi, row, col0, s);
+    for (int i = 0; i < VE; ++i) acc[i] = 0.f;
+    row_sum<T, LPR, HAS_VAL>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, beg, end);
+    if (single) {
+      // the row's only piece holds its whole sum: the epilogue stores it here
+      epi_store_vec<T>(p.epi, row, col0, acc);
     } else {
-      float* out = p.partials + chunk * p.ldp + col0;
+      float4* out = reinterpret_cast<float4*>(p.partials + pos * p.ldp + col0);
 #pragma unroll
-      for (int i = 0; i < VE; ++i)
-        if (col0 + i < p.ldp) out[i] = s[i];
+      for (int i = 0; i < VE / 4; ++i) out[i] = make_float4(acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]);
     }
+    pos = npos;
   }
 }
 
+// Pieces and light rows in one launch: workgroups [0, n_piece_wg) take the
+// pieces, the rest walk the light rows.
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
-__global__ __launch_bounds__(256) void spmm_heavy_chunk_kernel(HeavyParams<IdxT> p) {
-  spmm_heavy_body<T, IdxT, LPR, HAS_VAL>(p, blockIdx.x);
-}
-
-// Heavy chunks and light rows in one launch: workgroups [0, n_heavy) take
-// the chunks (longest work first), the rest walk the light rows, so that the
-// hubs are reduced while the light rows run instead of in a launch of their
-// own (on graphs with few hubs that launch leaves most of the chip idle).
-// A workgroup is wholly one or the other, so the chunk body's barriers are
-// reached by all its threads.
-template <typename T, typename IdxT, int LPR, bool HAS_VAL>
-__global__ __launch_bounds__(256) void spmm_fused_kernel(SpmmParams<IdxT> p, HeavyParams<IdxT> hp, int64_t n_heavy) {
+__global__ __launch_bounds__(256) void spmm_main_kernel(SpmmParams<IdxT> p, PieceParams pp, int64_t n_piece_wg) {
   const int64_t b = blockIdx.x;
-  if (b < n_heavy) spmm_heavy_body<T, IdxT, LPR, HAS_VAL>(hp, b);
-  else spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, b - n_heavy, (int64_t)gridDim.x - n_heavy);
+  if (b < n_piece_wg) spmm_piece_body<T, LPR, HAS_VAL>(pp, b, n_piece_wg);
+  else spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, b - n_piece_wg, (int64_t)gridDim.x - n_piece_wg);
 }
 
-// One thread per (heavy row, column): fixed-order sum of the chunk partials
-// (rows of a single chunk were stored by their chunk).
-template <typename T, typename IdxT>
-__global__ __launch_bounds__(256) void spmm_heavy_fixup_kernel(HeavyParams<IdxT> p) {
+// Workgroup (heavy row, 64 columns): wave v adds the partials of the v-th
+// quarter of the row's pieces in piece order (8 loads in flight), then the
+// quarters are added in wave order and the epilogue stores the row.  Rows
+// of one piece were stored by their piece.
+template <typename T>
+__global__ __launch_bounds__(256) void spmm_piece_fixup_kernel(PieceParams p) {
+  __shared__ float red[4][64];
   const int64_t h = blockIdx.x;
-  const int64_t col = (int64_t)blockIdx.y * 256 + threadIdx.x;
-  if (col >= p.F) return;
-  const int64_t row = p.heavy_rows[h];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t col = (int64_t)blockIdx.y * 64 + lane;
   const int64_t c0 = p.heavy_chunk_off[h], c1 = p.heavy_chunk_off[h + 1];
-  if (c1 - c0 == 1) return;
+  if (c1 - c0 == 1) return;                       // the same for the whole workgroup
+  const int64_t quarter = (c1 - c0 + 3) / 4;
+  const int64_t a0 = c0 + wave * quarter;
+  const int64_t a1 = a0 + quarter < c1 ? a0 + quarter : c1;
   float a = 0.f;
-  for (int64_t c = c0; c < c1; ++c) a += p.partials[c * p.ldp + col];
-  epi_store1<T>(p.epi, row, col, a);
+  if (col < p.F) {
+    const float* __restrict__ part = p.partials + col;
+    int64_t c = a0;
+    for (; c + 8 <= a1; c += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)p.pos_of[c + u] * p.ldp];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) a += v[u];
+    }
+    for (; c < a1; ++c) a += part[(int64_t)p.pos_of[c] * p.ldp];
+  }
+  red[wave][lane] = a;
+  __syncthreads();
+  if (wave == 0 && col < p.F) {
+    float t = red[0][lane] + red[1][lane];
+    t += red[2][lane];
+    t += red[3][lane];
+    epi_store1<T>(p.epi, p.heavy_rows[h], col, t);
+  }
 }
 
-// Chunk workgroups below which the chunks share the light rows' launch
-// (8 per compute unit).
-constexpr int64_t SPMM_FUSE_CHUNKS = 8 * 256;
+// Workgroups of each kind in one launch: enough for every lane group to
+// walk several rows (or pieces) with its descriptor loads ahead, and about
+// four rounds of workgroups over the chip's 256 compute units.
+constexpr int64_t SPMM_WG_CAP = 8192;
 
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
@@ -266,16 +314,15 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   const int64_t colblocks = (F + LPR * VE - 1) / (LPR * VE);
   SpmmParams<IdxT> p;
   p.n = A.n;
-  p.row_perm = A.row_perm;
+  p.row_desc = A.row_perm ? A.row_desc : nullptr;
   p.n_rows = A.row_perm ? A.n_light : A.n;
   p.rowptr = reinterpret_cast<const IdxT*>(A.rowptr);
   p.colidx = A.colidx;
   p.values = A.values;
   p.dinv = A.dinv;
-  p.heavy_threshold = A.n_heavy > 0 ? A.heavy_threshold : 0;
   p.X = X; p.ldx = ldx; p.F = F; p.epi = epi;
-  const int64_t rows_per_block = 4 * G;
-  const int64_t lblocks = p.n_rows > 0 ? std::min<int64_t>((p.n_rows + rows_per_block - 1) / rows_per_block, 1 << 20) : 0;
+  const int64_t per_wg = 4 * G;
+  int64_t lblocks = p.n_rows > 0 ? std::min<int64_t>((p.n_rows + per_wg - 1) / per_wg, SPMM_WG_CAP) : 0;
   hipError_t e = hipSuccess;
   if (A.n_heavy <= 0) {
     if (lblocks > 0) {
@@ -285,37 +332,30 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
     }
     return e;
   }
-
-  HeavyParams<IdxT> hp;
-  hp.rowptr = p.rowptr; hp.colidx = A.colidx; hp.values = A.values; hp.dinv = A.dinv;
-  hp.heavy_rows = A.heavy_rows; hp.heavy_chunk_off = A.heavy_chunk_off; hp.chunk_heavy = A.chunk_heavy;
-  hp.chunk_order = A.chunk_order;
-  hp.chunk_nnz = A.chunk_nnz; hp.n_chunks = A.n_chunks;
-  hp.X = X; hp.ldx = ldx; hp.F = F;
-  hp.ldp = colblocks * LPR * VE;
-  hp.partials = partials; hp.epi = epi;
-  if (lblocks > 0 && A.n_chunks * colblocks < SPMM_FUSE_CHUNKS) {
-    // few chunks (fewer than 8 workgroups per compute unit on their own):
-    // one launch with the light rows (grid below 2^32 work-items)
-    dim3 gridf2((unsigned)(A.n_chunks + lblocks), (unsigned)colblocks);
-    hipLaunchKernelGGL((spmm_fused_kernel<T, IdxT, LPR, HAS_VAL>), gridf2, dim3(256), 0, s, p, hp, (int64_t)A.n_chunks);
+  PieceParams pp;
+  pp.desc = A.piece_desc; pp.pos_of = A.piece_pos;
+  pp.heavy_rows = A.heavy_rows; pp.heavy_chunk_off = A.heavy_chunk_off; pp.part_off = A.part_off;
+  pp.n_chunks = A.n_chunks; pp.parts = A.parts;
+  pp.colidx = A.colidx; pp.values = A.values; pp.dinv = A.dinv;
+  pp.X = X; pp.ldx = ldx; pp.F = F;
+  pp.ldp = colblocks * LPR * VE;
+  pp.partials = partials; pp.epi = epi;
+  int64_t n_piece_wg;
+  if (A.parts > 1) {
+    n_piece_wg = XCDS * std::min<int64_t>((A.part_slots + per_wg - 1) / per_wg, SPMM_WG_CAP / XCDS);
+    // keep the grid's x extent a multiple of XCDS, so that every column
+    // block (grid y) deals its piece workgroups to the dies alike
+    lblocks = (lblocks + XCDS - 1) / XCDS * XCDS;
   } else {
-    // many chunks fill the chip by themselves and keep their first-column
-    // order to themselves (mixed with light rows: +2 % on R-MAT scale 21)
-    if (lblocks > 0) {
-      hipLaunchKernelGGL((spmm_rows_kernel<T, IdxT, LPR, HAS_VAL>), dim3((unsigned)lblocks, (unsigned)colblocks),
-                         dim3(256), 0, s, p);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL((spmm_heavy_chunk_kernel<T, IdxT, LPR, HAS_VAL>), dim3((unsigned)A.n_chunks, (unsigned)colblocks),
-                       dim3(256), 0, s, hp);
+    n_piece_wg = std::min<int64_t>((A.n_chunks + per_wg - 1) / per_wg, SPMM_WG_CAP);
   }
+  hipLaunchKernelGGL((spmm_main_kernel<T, IdxT, LPR, HAS_VAL>),
+                     dim3((unsigned)(n_piece_wg + lblocks), (unsigned)colblocks), dim3(256), 0, s, p, pp, n_piece_wg);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (A.n_chunks == A.n_heavy) return hipSuccess;     // every heavy row is one chunk: all stored
-  dim3 gridf((unsigned)A.n_heavy, (unsigned)((F + 255) / 256));
-  hipLaunchKernelGGL((spmm_heavy_fixup_kernel<T, IdxT>), gridf, dim3(256), 0, s, hp);
+  if (A.n_chunks == A.n_heavy) return hipSuccess;     // every heavy row is one piece: all stored
+  dim3 gridf((unsigned)A.n_heavy, (unsigned)((F + 63) / 64));
+  hipLaunchKernelGGL((spmm_piece_fixup_kernel<T>), gridf, dim3(256), 0, s, pp);
   return hipGetLastError();
 }
 

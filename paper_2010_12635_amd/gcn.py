@@ -68,7 +68,9 @@ class GcnAdj(ctypes.Structure):
         ("n_heavy", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
         ("heavy_rows", ctypes.c_void_p), ("heavy_chunk_off", ctypes.c_void_p),
         ("chunk_heavy", ctypes.c_void_p), ("n_light", ctypes.c_int64), ("row_perm", ctypes.c_void_p),
-        ("chunk_order", ctypes.c_void_p),
+        ("chunk_order", ctypes.c_void_p), ("chunk_beg", ctypes.c_void_p), ("part_off", ctypes.c_void_p),
+        ("col_parts", ctypes.c_int64), ("part_slots", ctypes.c_int64),
+        ("piece_desc", ctypes.c_void_p), ("piece_pos", ctypes.c_void_p), ("row_desc", ctypes.c_void_p),
     ]
 
 
@@ -115,8 +117,8 @@ def lib():
         "gcn_abi_version": (I32, []),
         "gcn_normalize_workspace_size": (I32, [I64, I64, PSZ]),
         "gcn_normalize": (I32, [I64, I64, P, P, I32, P, P, I64, P, P, I32, P, P, I64, PI64, P, SZ, P]),
-        "gcn_schedule_size": (I32, [I64, I64, I64, I64, PSZ]),
-        "gcn_schedule": (I32, [PADJ, I64, I64, P, SZ, P]),
+        "gcn_schedule_size": (I32, [I64, I64, I64, I64, I64, PSZ]),
+        "gcn_schedule": (I32, [PADJ, I64, I64, I64, P, SZ, P]),
         "gcn_layer_workspace_size": (I32, [PADJ, PLAY, I32, PSZ]),
         "gcn_layer_fwd": (I32, [PADJ, PLAY, I32, I32, P, P, P, ctypes.c_uint64, ctypes.c_uint64,
                                 P, P, P, P, SZ, P]),
@@ -197,14 +199,15 @@ def gcn_normalize(n, src, dst, index, rowptr, colidx, deg, dinv, value_prec, val
     return nnz.value
 
 
-def gcn_schedule_size(n, nnz, heavy_threshold=0, chunk_nnz=0) -> int:
+def gcn_schedule_size(n, nnz, heavy_threshold=0, chunk_nnz=0, col_parts=0) -> int:
     b = ctypes.c_size_t(0)
-    _check(lib().gcn_schedule_size(n, nnz, heavy_threshold, chunk_nnz, ctypes.byref(b)), "gcn_schedule_size")
+    _check(lib().gcn_schedule_size(n, nnz, heavy_threshold, chunk_nnz, col_parts, ctypes.byref(b)),
+           "gcn_schedule_size")
     return b.value
 
 
-def gcn_schedule(adj: GcnAdj, sched, heavy_threshold=0, chunk_nnz=0, stream=None):
-    st = lib().gcn_schedule(ctypes.byref(adj), heavy_threshold, chunk_nnz, _ptr(sched),
+def gcn_schedule(adj: GcnAdj, sched, heavy_threshold=0, chunk_nnz=0, col_parts=0, stream=None):
+    st = lib().gcn_schedule(ctypes.byref(adj), heavy_threshold, chunk_nnz, col_parts, _ptr(sched),
                             sched.numel() * sched.element_size(), _stream(stream))
     _check(st, "gcn_schedule")
 

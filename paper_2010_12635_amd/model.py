@@ -36,9 +36,12 @@ class DeviceGraph:
     """A_hat on the device, built by gcn_normalize (+ gcn_schedule for CSR)."""
 
     def __init__(self, n, src, dst, prec=G.GCN_F16, index=G.GCN_I32, dense=False, values=True,
-                 schedule=True, device="cuda", heavy_threshold=0, chunk_nnz=0, stream=None, tiled=None):
+                 schedule=True, device="cuda", heavy_threshold=0, chunk_nnz=0, stream=None, tiled=None,
+                 col_parts=0):
         """dense=True stores A_hat densely: in the tiled operand order by
-        default (tiled=None or True), row-major when tiled=False."""
+        default (tiled=None or True), row-major when tiled=False.
+        heavy_threshold, chunk_nnz, col_parts: gcn_schedule's arguments
+        (0 = the library's defaults)."""
         self.n = int(n)
         self.prec = prec
         dev = torch.device(device)
@@ -88,9 +91,9 @@ class DeviceGraph:
             a.ld_dense = self.ld_dense
         self.sched = None
         if schedule and not dense:
-            nbytes = G.gcn_schedule_size(self.n, self.nnz, heavy_threshold, chunk_nnz)
+            nbytes = G.gcn_schedule_size(self.n, self.nnz, heavy_threshold, chunk_nnz, col_parts)
             self.sched = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-            G.gcn_schedule(a, self.sched, heavy_threshold, chunk_nnz, stream)
+            G.gcn_schedule(a, self.sched, heavy_threshold, chunk_nnz, col_parts, stream)
 
     def csr_host(self):
         rp = self.rowptr.cpu().numpy().astype(np.int64)

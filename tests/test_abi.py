@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert G.gcn_abi_version() == 7
+    assert G.gcn_abi_version() == 8
     assert G.gcn_status_string(0) == "GCN_OK"
     for s in range(1, 9):
         assert G.gcn_status_string(s).startswith("GCN_ERR_")
@@ -41,7 +41,7 @@ def test_abi_version_and_status_strings():
 
 
 def test_struct_sizes_match_header_layout():
-    assert ctypes.sizeof(G.GcnAdj) == 8 * 2 + 4 * 4 + 8 * 5 + 8 * 5 + 8 * 3 + 8 * 3
+    assert ctypes.sizeof(G.GcnAdj) == 8 * 2 + 4 * 4 + 8 * 5 + 8 * 5 + 8 * 3 + 8 * 3 + 8 * 4 + 8 * 3
     assert ctypes.sizeof(G.GcnLayer) == 8 * 4 + 4 * 4
     assert ctypes.sizeof(G.GcnScaler) == 16
     assert ctypes.sizeof(G.GcnAdamConfig) == 36
@@ -51,6 +51,11 @@ def test_workspace_queries():
     assert G.gcn_normalize_workspace_size(1000, 5000) > 4 * (2 * 5000 + 1000)
     assert G.gcn_loss_workspace_size(1000, 7) > 0
     assert G.gcn_schedule_size(1000, 9000) > 0
+    assert G.gcn_schedule_size(1000, 9000, col_parts=16) >= G.gcn_schedule_size(1000, 9000, col_parts=1)
+    for bad in (2, 4, 12, 128):       # column ranges: 1 or a multiple of 8 up to 64
+        with pytest.raises(G.GcnError) as e:
+            G.gcn_schedule_size(1000, 9000, col_parts=bad)
+        assert e.value.status == 1
     with pytest.raises(G.GcnError):
         G.gcn_normalize_workspace_size(0, 10)
     with pytest.raises(G.GcnError):

@@ -106,38 +106,92 @@ def test_normalize_empty_and_bad_ids():
     assert e.value.status == 8
 
 
-def test_schedule_lists_heavy_rows():
+def _expected_pieces(g, heavy, chunk, parts):
+    """Pieces of the heavy rows as the schedule defines them: each row's
+    entries cut where the column range floor(c P / n) changes, then every
+    `chunk` entries; returns (first entry of each piece, pieces per row)."""
+    n = g.n
+    begs, counts = [], []
+    for r in heavy:
+        a0, a1 = int(g.rowptr[r]), int(g.rowptr[r + 1])
+        cols = g.colidx[a0:a1].astype(np.int64)
+        rng = cols * parts // n
+        cuts = [a0 + int(np.searchsorted(rng, q + 1, side="left")) for q in range(parts - 1)]
+        bounds = [a0] + cuts + [a1]
+        k0 = len(begs)
+        for a, b in zip(bounds[:-1], bounds[1:]):
+            begs.extend(range(a, b, chunk))
+        counts.append(len(begs) - k0)
+    return np.array(begs, np.int64), np.array(counts, np.int64)
+
+
+@pytest.mark.parametrize("parts", [1, 8, 16])
+def test_schedule_lists_heavy_rows(parts):
     n = 3000
     src, dst = hub_graph(n, 9000, [(5, 400), (17, 120), (2999, 1000)], seed=3)
     g = O.graph(n, src, dst)
-    dg = DeviceGraph(n, src, dst, prec=G.GCN_F16, heavy_threshold=32, chunk_nnz=64)
+    dg = DeviceGraph(n, src, dst, prec=G.GCN_F16, heavy_threshold=32, chunk_nnz=64, col_parts=parts)
     a = dg.adj
+    assert a.col_parts == parts
     heavy = np.flatnonzero(g.deg > 32)
     assert a.n_heavy == heavy.size
-    hr = torch.empty(0)  # noqa: F841
     # read the schedule arrays back through their device addresses
     base = dg.sched
     off = lambda p: (p - base.data_ptr())
-    rows = base[off(a.heavy_rows): off(a.heavy_rows) + 4 * a.n_heavy].view(torch.int32).cpu().numpy()
+    rd = lambda ptr, count, dt, sz: base[off(ptr): off(ptr) + sz * count].view(dt).cpu().numpy()
+    rows = rd(a.heavy_rows, a.n_heavy, torch.int32, 4)
     assert np.array_equal(rows, heavy)
-    cho = base[off(a.heavy_chunk_off): off(a.heavy_chunk_off) + 4 * (a.n_heavy + 1)].view(torch.int32).cpu().numpy()
-    want = np.concatenate([[0], np.cumsum((g.deg[heavy] + 63) // 64)])
-    assert np.array_equal(cho, want)
-    assert a.n_chunks == want[-1]
+    want_beg, want_cnt = _expected_pieces(g, heavy, 64, parts)
+    cho = rd(a.heavy_chunk_off, a.n_heavy + 1, torch.int32, 4)
+    assert np.array_equal(cho, np.concatenate([[0], np.cumsum(want_cnt)]))
+    assert a.n_chunks == want_beg.size
+    beg = rd(a.chunk_beg, a.n_chunks + 1, torch.int64, 8)
+    assert np.array_equal(beg[:-1], want_beg) and beg[-1] == g.nnz
+    owner = rd(a.chunk_heavy, a.n_chunks, torch.int32, 4)
+    assert np.array_equal(owner, np.repeat(np.arange(heavy.size), want_cnt))
     # light rows: every row with deg <= threshold exactly once, degree
     # non-increasing (below 2^20 rows the order is one global degree order)
-    perm = base[off(a.row_perm): off(a.row_perm) + 4 * a.n_light].view(torch.int32).cpu().numpy()
+    perm = rd(a.row_perm, a.n_light, torch.int32, 4)
     light = np.flatnonzero(g.deg <= 32)
     assert a.n_light == light.size
     assert np.array_equal(np.sort(perm), light)
     assert np.all(np.diff(g.deg[perm]) <= 0)
-    # chunk launch order: every chunk once, first columns in non-decreasing buckets
-    order = base[off(a.chunk_order): off(a.chunk_order) + 4 * a.n_chunks].view(torch.int32).cpu().numpy()
+    # launch order: every piece once, first columns in non-decreasing
+    # buckets, the pieces of column range q in chunk_order[part_off[q] ..
+    # part_off[q + 1]), and part_slots the most pieces of one XCD
+    order = rd(a.chunk_order, a.n_chunks, torch.int32, 4)
     assert np.array_equal(np.sort(order), np.arange(a.n_chunks))
-    owner = np.repeat(np.arange(heavy.size), np.diff(want))
-    first = np.array([g.rowptr[heavy[owner[c]]] + (c - want[owner[c]]) * 64 for c in range(a.n_chunks)])
-    bucket = g.colidx[first].astype(np.int64) * 4096 // n
-    assert np.all(np.diff(bucket[order]) >= 0)
+    first_col = g.colidx[want_beg].astype(np.int64)
+    assert np.all(np.diff(first_col[order] * 4096 // n) >= 0)
+    # 16-byte descriptors: light rows {first entry, row, length} in row_perm
+    # order; pieces {first entry, row, length | 2^31 for a row's only piece}
+    # in launch order, and the launch position of every piece
+    ld = rd(a.row_desc, a.n_light * 4, torch.int32, 4).reshape(-1, 4)
+    assert np.array_equal(ld[:, 0].astype(np.uint32).astype(np.int64) + (ld[:, 1].astype(np.int64) << 32),
+                          g.rowptr[perm])
+    assert np.array_equal(ld[:, 2], perm) and np.array_equal(ld[:, 3], g.deg[perm])
+    pd = rd(a.piece_desc, a.n_chunks * 4, torch.int32, 4).reshape(-1, 4)
+    ends = np.minimum(beg[1:], g.rowptr[heavy[owner] + 1])
+    single = np.repeat(want_cnt == 1, want_cnt)
+    assert np.array_equal(pd[:, 0].astype(np.uint32).astype(np.int64) + (pd[:, 1].astype(np.int64) << 32),
+                          want_beg[order])
+    assert np.array_equal(pd[:, 2], heavy[owner][order])
+    lenf = pd[:, 3].astype(np.uint32)
+    assert np.array_equal(lenf & 0x7FFFFFFF, (ends - want_beg)[order]) and np.array_equal(lenf >> 31, single[order])
+    pos = rd(a.piece_pos, a.n_chunks, torch.int32, 4)
+    assert np.array_equal(order[pos], np.arange(a.n_chunks))
+    if parts > 1:
+        po = rd(a.part_off, parts + 1, torch.int64, 8)
+        assert po[0] == 0 and po[-1] == a.n_chunks and np.all(np.diff(po) >= 0)
+        for q in range(parts):
+            assert np.all(first_col[order[po[q]:po[q + 1]]] * parts // n == q)
+            # a piece never crosses its range: its last entry is in range q too
+            last = np.minimum(beg[1:], g.rowptr[heavy[owner] + 1])[order[po[q]:po[q + 1]]] - 1
+            assert np.all(g.colidx[last].astype(np.int64) * parts // n == q)
+        per_xcd = [sum(po[q + 1] - po[q] for q in range(x, parts, 8)) for x in range(8)]
+        assert a.part_slots == max(per_xcd)
+    else:
+        assert a.part_slots == a.n_chunks
 
 
 # ------------------------------------------------------------ layer fwd ----
@@ -166,6 +220,9 @@ FWD_CASES = [
     (2100, 40, 130, G.GCN_ACT_RELU, 0.3, "csr"),
     (2100, 40, 130, G.GCN_ACT_RELU, 0.3, "csr_dinv"),
     (1800, 72, 24, G.GCN_ACT_RELU, 0.5, "csr_onechunk"),
+    (3000, 500, 64, G.GCN_ACT_RELU, 0.5, "csr_parts"),
+    (2100, 40, 130, G.GCN_ACT_RELU, 0.3, "csr_parts"),
+    (3000, 128, 7, G.GCN_ACT_NONE, 0.0, "csr_smallpieces"),
     (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1500, 64, 32, G.GCN_ACT_NONE, 0.0, "tiled"),
     (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "tiled"),
@@ -180,19 +237,28 @@ FWD_CASES = [
 ]
 
 
+CSR_STORAGES = ("csr", "csr_dinv", "csr_onechunk", "csr_parts", "csr_smallpieces")
+
+
 def _graph_for(n, src, dst, prec, storage):
+    # "csr": heavy rows cut every 96 entries, one column range;
     # "csr_dinv": CSR without stored values, every edge weight formed from dinv;
-    # "csr_onechunk": CSR whose heavy rows are all one chunk
-    csr = storage in ("csr", "csr_dinv", "csr_onechunk")
+    # "csr_onechunk": CSR whose heavy rows are all one piece;
+    # "csr_parts": 16 column ranges (the XCD-mapped launch);
+    # "csr_smallpieces": 8 column ranges and pieces of 8 entries, so that a
+    # hub has dozens of pieces for the fix-up to add
+    csr = storage in CSR_STORAGES
+    parts = {"csr_parts": 16, "csr_smallpieces": 8}.get(storage, 1)
+    chunk = 8 if storage == "csr_smallpieces" else 96
     return DeviceGraph(n, src, dst, prec=prec, dense=not csr, tiled=storage == "tiled",
-                       values=storage != "csr_dinv", heavy_threshold=48, chunk_nnz=96)
+                       values=storage != "csr_dinv", heavy_threshold=48, chunk_nnz=chunk, col_parts=parts)
 
 
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
 @pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_act{c[3]}_p{c[4]}_{c[5]}")
 def test_layer_fwd(prec, case):
     n, f_in, f_out, act, p, storage = case
-    dense = storage not in ("csr", "csr_dinv", "csr_onechunk")
+    dense = storage not in CSR_STORAGES
     g, src, dst, h, w, b = _layer_case(n, f_in, f_out, seed=n + f_in,
                                        hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS)
     dg = _graph_for(n, src, dst, prec, storage)
@@ -278,6 +344,8 @@ BWD_CASES = [
     (2100, 130, 40, G.GCN_ACT_RELU, 0.3, "csr"),
     (3000, 64, 7, G.GCN_ACT_RELU, 0.5, "csr_dinv"),
     (1800, 24, 72, G.GCN_ACT_RELU, 0.5, "csr_onechunk"),
+    (3000, 64, 7, G.GCN_ACT_RELU, 0.5, "csr_parts"),
+    (2100, 130, 40, G.GCN_ACT_RELU, 0.3, "csr_smallpieces"),
     (1500, 64, 32, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "dense"),
@@ -291,7 +359,7 @@ BWD_CASES = [
 @pytest.mark.parametrize("case", BWD_CASES, ids=lambda c: f"n{c[0]}_{c[1]}x{c[2]}_below{c[3]}_p{c[4]}_{c[5]}")
 def test_layer_bwd(prec, case):
     n, f_in, f_out, act_below, p, storage = case
-    dense = storage not in ("csr", "csr_dinv", "csr_onechunk")
+    dense = storage not in CSR_STORAGES
     g, src, dst, h, w, _ = _layer_case(n, f_in, f_out, seed=7 * n + f_out,
                                        hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS)
     rng = np.random.default_rng(n)
