@@ -100,7 +100,7 @@ def spmm_bytes(n, nnz, F, s, s_p):
     return (n + 1) * s_p + nnz * (4 + s) + 2 * s * n * F
 
 
-def run_gpu(wl, prec, steps, warmup, dense=True, level=None):
+def run_gpu(wl, prec, steps, warmup, dense=True, level=None, graph=False):
     import torch
     from paper_2010_12635_amd import gcn as G
     from paper_2010_12635_amd.model import DeviceGraph, GCN2
@@ -118,7 +118,28 @@ def run_gpu(wl, prec, steps, warmup, dense=True, level=None):
     scale0 = spec.loss_scale0 if prec != G.GCN_F32 else 1.0
     m = GCN2(dg, wl["X"], wl["labels"], wl["mask"], wl["W1"], wl["W2"], wl["b1"], wl["b2"], prec=prec,
              dropout=0.0 if spec.dropout is None else spec.dropout, seed=wl["dropout_seed"], loss_scale=scale0,
-             level=level)
+             level=level, device_epoch=graph)
+    if graph:
+        # one epoch captured into a HIP graph, replayed per epoch (the
+        # dropout counter comes from the device-resident optimiser state)
+        m.capture()
+        for _ in range(warmup):
+            m.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record()
+        for _ in range(steps):
+            m.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        res = dict(prec=prec, gpu_ms=e0.elapsed_time(e1), wall_s=time.perf_counter() - t0, loss=float(m.loss.item()),
+                   scaler=m.scaler_state(), peak_bytes=int(torch.cuda.max_memory_allocated() - base), n=dg.n,
+                   nnz=dg.nnz, n_correct=int(m.n_correct.item()), n_mask=m.n_mask)
+        del m, dg
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        return res
     timer = EventTimer()
     gtimer = EventTimer()
     for ep in range(warmup):
@@ -511,9 +532,12 @@ def summarize_counters(fetch_dir, write_dir, out_path, command):
 def summarize_mfma(pmc_dir, out_path, command):
     """Matrix-core activity per kernel from one rocprofv3 --pmc run of
     SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_F16/_F32 and
-    GRBM_GUI_ACTIVE: utilisation = busy cycles summed over the SIMDs /
-    (GPU-active cycles x 1024 SIMDs), as rocprofv3's MfmaUtil; executed
-    flops = MOPS x 512, over the dispatch's duration."""
+    GRBM_GUI_ACTIVE: utilisation = matrix-pipe busy cycles summed over the
+    SIMDs / (GPU-active cycles of one die x 1024 SIMDs); GRBM_GUI_ACTIVE
+    comes summed over the 8 dies (it reads 8 x the clock x the duration),
+    so one die's count is a eighth of it.  Executed flops = MOPS x 512
+    over the dispatch's duration; clock = one die's active cycles over the
+    duration."""
     import csv
     from collections import defaultdict
     rows = list(csv.DictReader(open(os.path.join(pmc_dir, "run_counter_collection.csv"))))
@@ -523,16 +547,19 @@ def summarize_mfma(pmc_dir, out_path, command):
         per[r["Kernel_Name"]][int(r["Dispatch_Id"])]["_ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
     lines = ["# Matrix-core (MFMA) counters", "", "Command (from the repository root, on one MI355X):", "", "```", command,
              "```", "", "Per kernel, averaged over its dispatches: `util` = SQ_VALU_MFMA_BUSY_CYCLES / "
-             "(GRBM_GUI_ACTIVE x 1024 SIMDs) (rocprofv3's MfmaUtil); `TFLOP/s` = (SQ_INSTS_VALU_MFMA_MOPS_F16 + "
-             "_F32) x 512 / dispatch time (the profiler's own clock, slowed by counter collection); `peak frac` "
-             "against 2500 (f16) or 157.3 (fp32) TFLOP/s.", "",
-             "| kernel | dispatches | avg us | util % | MFMA TFLOP/s | peak frac |", "|---|---:|---:|---:|---:|---:|"]
+             "((GRBM_GUI_ACTIVE / 8) x 1024 SIMDs), the share of SIMD cycles in which the matrix pipe was busy "
+             "(GRBM_GUI_ACTIVE reads as the sum over the 8 dies); `clock` = GRBM_GUI_ACTIVE / 8 / duration; "
+             "`TFLOP/s` = (SQ_INSTS_VALU_MFMA_MOPS_F16 + _F32) x 512 / duration, the matrix-core flops actually "
+             "executed; `peak frac` against 2500 (f16) or 157.3 (fp32) TFLOP/s at 2.4 GHz.", "",
+             "| kernel | dispatches | avg us | util % | clock GHz | MFMA TFLOP/s | peak frac |",
+             "|---|---:|---:|---:|---:|---:|---:|"]
     out = {}
     for k, disp in sorted(per.items(), key=lambda kv: -sum(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for d in kv[1].values())):
         ds = [d for d in disp.values() if "SQ_VALU_MFMA_BUSY_CYCLES" in d and "GRBM_GUI_ACTIVE" in d]
         if not ds or sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] for d in ds) == 0:
             continue
-        util = sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] / (d["GRBM_GUI_ACTIVE"] * 1024) for d in ds) / len(ds)
+        util = sum(d["SQ_VALU_MFMA_BUSY_CYCLES"] / (d["GRBM_GUI_ACTIVE"] / 8 * 1024) for d in ds) / len(ds)
+        clock = sum(d["GRBM_GUI_ACTIVE"] / 8 / d["_ns"] for d in ds) / len(ds)
         f16 = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_F16", 0) + d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) for d in ds)
         f32 = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0) for d in ds)
         ns = sum(d["_ns"] for d in ds)
@@ -540,8 +567,10 @@ def summarize_mfma(pmc_dir, out_path, command):
         peak = 2500.0 if f16 >= f32 else 157.3
         name = k.replace("gcn::(anonymous namespace)::", "")
         name = name if len(name) < 100 else name[:100] + "..."
-        lines.append(f"| `{name}` | {len(ds)} | {ns / len(ds) / 1e3:.1f} | {100 * util:.1f} | {tf:.1f} | {tf / peak:.3f} |")
-        out[name] = dict(util=round(util, 4), tflops=round(tf, 1), peak_frac=round(tf / peak, 4), avg_us=round(ns / len(ds) / 1e3, 1))
+        lines.append(f"| `{name}` | {len(ds)} | {ns / len(ds) / 1e3:.1f} | {100 * util:.1f} | {clock:.2f} | {tf:.1f} "
+                     f"| {tf / peak:.3f} |")
+        out[name] = dict(util=round(util, 4), clock_ghz=round(clock, 3), tflops=round(tf, 1), peak_frac=round(tf / peak, 4),
+                         avg_us=round(ns / len(ds) / 1e3, 1))
     lines += ["", "```json", json.dumps(out, indent=1), "```", ""]
     with open(out_path, "w") as fh:
         fh.write("\n".join(lines))
@@ -611,7 +640,7 @@ def aggregation_roofline(spec, r, prec):
     return roof
 
 
-def training_record(wl, prec, steps, warmup, pname, fp32=True, level=None):
+def training_record(wl, prec, steps, warmup, pname, fp32=True, level=None, graph=True):
     """Train a workload for `steps` timed epochs in `prec` (and in fp32
     beside it): epochs/s, peak device memory, the aggregation roofline and
     the feature-transform rate of each precision."""
@@ -628,6 +657,11 @@ def training_record(wl, prec, steps, warmup, pname, fp32=True, level=None):
                wall_s_timed=round(r["wall_s"], 4), host_submit_ms_per_step=round(r["host_submit_s"] * 1e3 / steps, 4),
                fp32=None)
     rec["_r"] = r
+    if graph:
+        rg = run_gpu(wl, prec, steps, warmup, dense=spec.dense_adj, graph=True)
+        rec["graph"] = dict(epochs_per_s=round(steps / (rg["gpu_ms"] * 1e-3), 2), ms_per_step=round(rg["gpu_ms"] / steps, 4),
+                            final_loss=rg["loss"], note="the same epochs replayed from one HIP graph capture")
+        log(f"[bench] {spec.name} {pname} graph replay: {rg['gpu_ms'] / steps:.3f} ms/epoch, loss {rg['loss']:.4f}")
     if fp32 and prec != 0:
         log(f"[bench] {spec.name} f32: {warmup} warmup + {steps} timed epochs")
         r32 = run_gpu(wl, 0, steps, warmup, dense=spec.dense_adj)

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 8
+#define GCN_ABI_VERSION 9
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -144,6 +144,13 @@ typedef struct gcn_layer {
   float dropout_p;       /* in [0, 1); only with GCN_ACT_RELU and training  */
   int32_t layer_id;      /* dropout stream id                               */
   int32_t identity_input;/* 1: H is the n x n identity (f_in == n)         */
+  const struct gcn_scaler* epoch_from;
+                         /* NULL, or the device loss-scale state whose
+                            step + skipped (optimiser calls so far) is added
+                            to the epoch argument of gcn_layer_fwd when its
+                            kernels run: a training epoch captured into a
+                            HIP graph then draws a new dropout mask at every
+                            replay                                          */
 } gcn_layer;
 
 /* Dynamic loss-scale state, device-resident (16 bytes). */

@@ -197,7 +197,8 @@ size_t aggregate_bytes(const gcn_adj* A, int32_t prec, int64_t F) {
 }
 
 Epilogue agg_epi(void* Y, int64_t ldy, int64_t n, int64_t F, const float* bias, int32_t act, float p,
-                 int32_t training, uint64_t seed, int32_t layer_id, uint64_t epoch, int32_t* overflow) {
+                 int32_t training, uint64_t seed, int32_t layer_id, uint64_t epoch, int32_t* overflow,
+                 const gcn_scaler* epoch_from = nullptr) {
   Epilogue ea = base_epi(Y, ldy, n, F, EPI_AGG, overflow);
   ea.bias = bias;
   ea.relu = act == GCN_ACT_RELU;
@@ -210,6 +211,7 @@ Epilogue agg_epi(void* Y, int64_t ldy, int64_t n, int64_t F, const float* bias, 
   ea.seed = seed;
   ea.layer = (uint64_t)(uint32_t)layer_id;
   ea.epoch = epoch;
+  ea.epoch_ctr = epoch_from ? &epoch_from->step : nullptr;   // step and skipped are adjacent int32
   return ea;
 }
 
@@ -381,7 +383,7 @@ gcn_status gcn_layer_fwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, int
   }
 
   Epilogue ea = agg_epi(H_out, L->ld_out, n, L->f_out, bias, L->act, L->dropout_p, training, seed, L->layer_id,
-                        epoch, overflow);
+                        epoch, overflow, L->epoch_from);
   GCN_HIP(aggregate(A, prec, Sx, L->ld_out, L->f_out, ea, ws, nullptr, s));
   return finish(hipSuccess, s);
 }

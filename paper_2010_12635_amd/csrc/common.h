@@ -130,6 +130,7 @@ struct Epilogue {
   uint64_t seed;
   uint64_t layer;
   uint64_t epoch;
+  const int32_t* epoch_ctr;  // if set, two int32 counters added to epoch when the kernel runs
   // EPI_DMASK
   const void* hmask;     // H (T), same shape as output
   int64_t ldh;
@@ -137,9 +138,18 @@ struct Epilogue {
   int32_t* flag;
 };
 
+// Dropout counter word: the epoch argument, plus, when the layer names a
+// device-resident loss-scale state, its applied and skipped optimiser steps
+// as the kernel finds them (so that a captured and replayed epoch draws a
+// new mask each time).
+__device__ __forceinline__ uint64_t dropout_epoch(const Epilogue& ep) {
+  if (!ep.epoch_ctr) return ep.epoch;
+  return ep.epoch + (uint64_t)(uint32_t)ep.epoch_ctr[0] + (uint64_t)(uint32_t)ep.epoch_ctr[1];
+}
+
 // Keep decision for element linear index e = row * cols + col.
 __device__ __forceinline__ bool dropout_keep(const Epilogue& ep, uint64_t e) {
-  Philox8 o = philox4x64_10(e >> 3, ep.epoch, 0, 0, ep.seed, ep.layer);
+  Philox8 o = philox4x64_10(e >> 3, dropout_epoch(ep), 0, 0, ep.seed, ep.layer);
   return philox_word(o, (uint32_t)(e & 7)) >= ep.thr;
 }
 
@@ -218,14 +228,14 @@ __device__ __forceinline__ void epi_store_vec_b(const Epilogue& ep, int64_t row,
         const uint64_t e0 = (uint64_t)row * (uint64_t)cols + (uint64_t)col0;
         const uint64_t b0 = e0 >> 3, b1 = (e0 + VE - 1) >> 3;
         {
-          const Philox8 o = philox4x64_10(b0, ep.epoch, 0, 0, ep.seed, ep.layer);
+          const Philox8 o = philox4x64_10(b0, dropout_epoch(ep), 0, 0, ep.seed, ep.layer);
 #pragma unroll
           for (int i = 0; i < VE; ++i)
             if (((e0 + i) >> 3) == b0)
               acc[i] = philox_word(o, (uint32_t)((e0 + i) & 7)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
         }
         if (b1 != b0) {
-          const Philox8 o = philox4x64_10(b1, ep.epoch, 0, 0, ep.seed, ep.layer);
+          const Philox8 o = philox4x64_10(b1, dropout_epoch(ep), 0, 0, ep.seed, ep.layer);
 #pragma unroll
           for (int i = 0; i < VE; ++i)
             if (((e0 + i) >> 3) != b0)

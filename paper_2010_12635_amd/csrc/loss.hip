@@ -1,5 +1,7 @@
 // Masked softmax cross-entropy for vertex classification, fused with the
-// scaled gradient: one read of the logits, one write of dlogits.  A group of
+// scaled gradient: one read of the logits, one write of dlogits, one
+// exponential per element (exp(z - max) serves the sum and, times the
+// reciprocal of the sum, the softmax).  A group of
 // LPR lanes owns one row (16 bytes of classes per lane); max, sum of
 // exponentials, label logit and arg-max are reduced with lane shuffles
 // inside the group.  Per-row losses are summed per workgroup in row order
@@ -60,6 +62,7 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   // (in that order for the per-slot sums)
   float acc_loss = 0.f;
   int32_t acc_corr = 0;
+  const float sc = (p.loss_scale ? *p.loss_scale : 1.f) * p.inv_count;
   for (int64_t base = (int64_t)blockIdx.x * (LOSS_R * RG); base < p.n; base += (int64_t)gridDim.x * (LOSS_R * RG)) {
     uint4 raw[LOSS_R];
     int32_t lab[LOSS_R];
@@ -93,12 +96,18 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
         if (om > mx || (om == mx && oa < am)) { mx = om; am = oa; }
       }
       const float rmax = mx;
+      // exp(z - max) once per element: the sum of exponentials and, scaled
+      // by its reciprocal, the softmax of the gradient
+      float ez[VE];
       float se = 0.f;
 #pragma unroll
-      for (int i = 0; i < VE; ++i)
-        if (col0 + i < p.C) se += expf(z[i] - rmax);
+      for (int i = 0; i < VE; ++i) {
+        ez[i] = (col0 + i < p.C) ? expf(z[i] - rmax) : 0.f;
+        se += ez[i];
+      }
       se = group_sum<LPR>(se);
       const float lse = rmax + logf(se);
+      const float inv_se = 1.f / se;
       const int32_t y = row_ok ? lab[r] : 0;
       float zy = 0.f;
 #pragma unroll
@@ -107,12 +116,11 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
       zy = group_sum<LPR>(zy);
       const bool in_mask = row_ok && msk[r] != 0;
       if (row_ok && col_ok) {
-        const float sc = (p.loss_scale ? *p.loss_scale : 1.f) * p.inv_count;
         float d[VE];
 #pragma unroll
         for (int i = 0; i < VE; ++i) {
           const int64_t c = col0 + i;
-          if (c < p.C && in_mask) d[i] = (expf(z[i] - lse) - (c == y ? 1.f : 0.f)) * sc;
+          if (c < p.C && in_mask) d[i] = (ez[i] * inv_se - (c == y ? 1.f : 0.f)) * sc;
           else d[i] = 0.f;
         }
         uint4 o = pack<T>(d);

@@ -80,6 +80,7 @@ class GcnLayer(ctypes.Structure):
         ("ld_in", ctypes.c_int64), ("ld_out", ctypes.c_int64),
         ("act", ctypes.c_int32), ("dropout_p", ctypes.c_float),
         ("layer_id", ctypes.c_int32), ("identity_input", ctypes.c_int32),
+        ("epoch_from", ctypes.c_void_p),
     ]
 
 

@@ -142,7 +142,12 @@ class GCN2:
 
     def __init__(self, graph: DeviceGraph, X, labels, mask, W1, W2, b1=None, b2=None, prec=G.GCN_F16,
                  dropout=0.5, seed=0, loss_scale=65536.0, adam: AdamConfig | None = None, device="cuda",
-                 level: str | None = None):
+                 level: str | None = None, device_epoch: bool = False):
+        """device_epoch: the dropout counter of an epoch is read on the device
+        from the loss-scale state (optimiser calls so far) instead of being
+        passed by the host, so that one captured epoch (capture()) can be
+        replayed; the epoch argument of step() is then ignored, and epochs
+        count from 0 at construction."""
         dev = torch.device(device)
         if level is None:
             level = "O0" if prec == G.GCN_F32 else "O2"
@@ -251,6 +256,11 @@ class GCN2:
         self.L1 = G.GcnLayer(self.f_in, self.f_h, self.ld_x, self.ld_h, G.GCN_ACT_RELU, self.p, 0,
                              1 if self.featureless else 0)
         self.L2 = G.GcnLayer(self.f_h, self.C, self.ld_h, self.ld_c, G.GCN_ACT_NONE, 0.0, 1, 0)
+        self.device_epoch = bool(device_epoch)
+        if self.device_epoch:
+            self.L1.epoch_from = self.scaler.data_ptr()
+            self.L2.epoch_from = self.scaler.data_ptr()
+        self.graph = None
         ws = max(G.gcn_layer_workspace_size(self.adj, self.L1, prec),
                  G.gcn_layer_workspace_size(self.adj, self.L2, prec),
                  G.gcn_loss_workspace_size(n, self.C),
@@ -284,6 +294,10 @@ class GCN2:
         ``gemm_timer`` if given); the arithmetic is the same as
         gcn_layer_fwd."""
         a = self.adj
+        if self.device_epoch:
+            if agg_timer is not None or gemm_timer is not None:
+                raise ValueError("timed split calls take the epoch from the host; use device_epoch=False")
+            epoch = 0         # the device counter supplies the epoch
         if self.level == "O1":
             self.cast_inputs(stream)
         if agg_timer is None:
@@ -346,6 +360,24 @@ class GCN2:
         self.forward(epoch, True, stream, agg_timer, gemm_timer)
         self.loss_and_backward(stream)
         self.optimizer_step(stream)
+
+    def capture(self):
+        """Record one training epoch (forward, loss, backward, optimiser)
+        into a HIP graph; replay() then runs it.  Needs device_epoch=True
+        (the graph reads its dropout epoch on the device).  Nothing runs
+        while capturing: the model's state is unchanged."""
+        if not self.device_epoch:
+            raise ValueError("capture() needs device_epoch=True")
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.step(0)
+        self.graph = g
+        return g
+
+    def replay(self):
+        """One training epoch from the captured graph; asynchronous."""
+        self.graph.replay()
 
     def scaler_state(self):
         s = self.scaler.cpu()
