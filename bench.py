@@ -419,9 +419,12 @@ def cpu_baseline(wl, budget_s, min_epochs=1):
         w1 = master[o[0]:o[1]].reshape(w1.shape); b1 = master[o[1]:o[2]]
         w2 = master[o[2]:o[3]].reshape(w2.shape); b2 = master[o[3]:o[4]]
         _, _, h1 = O.layer_fwd(g, vals, x, w1, b1, "relu", p, True, wl["dropout_seed"], 0, epochs, dense=dense)
+        log(f"[bench] cpu oracle: layer 1 forward, {time.perf_counter() - t0:.1f} s")
         _, z2, _ = O.layer_fwd(g, vals, h1, w2, b2, "none", dense=dense)
         _, dz2, _ = O.softmax_ce(z2, wl["labels"], wl["mask"], 1.0)
+        log(f"[bench] cpu oracle: layer 2 forward and loss, {time.perf_counter() - t0:.1f} s")
         _, dw2, db2, dz1 = O.layer_bwd(g, vals, h1, w2, dz2, "relu", p, dense=dense)
+        log(f"[bench] cpu oracle: layer 2 backward, {time.perf_counter() - t0:.1f} s")
         _, dw1, db1, _ = O.layer_bwd(g, vals, x, w1, dz1, "none", 0.0, dense=dense, need_dh=False)
         master, _ = O.adam_step(master, np.concatenate([dw1.ravel(), db1, dw2.ravel(), db2]), ad, sc,
                                 lr=spec.lr)
@@ -438,7 +441,7 @@ def cpu_baseline(wl, budget_s, min_epochs=1):
                        f"{len(os.sched_getaffinity(0))} (NumPy's elementwise work runs on one thread)")
 
 
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "dense_agg_sbm16k_traffic.md")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "aggregation_rmat21_sbm16k_traffic.md")
 # sources of the kernels whose counters are reported (with the shared
 # device helpers they include)
 DENSE_SOURCES = ("dense_agg.hip", "xpose.h", "common.h")
@@ -499,20 +502,30 @@ def summarize_counters(fetch_dir, write_dir, out_path, command):
     rows_out = []
     for k in kernels[:24]:
         rows_out.append((k, len(fetch[k]), avg(fetch, k) * f_scale, avg(write, k) * w_scale))
+
+    def per_call(pred, unit_pred):
+        """Bytes of the kernels matching pred per call of the kernels
+        matching unit_pred (one aggregation = one main-kernel launch plus
+        whatever else it launches)."""
+        tot = sum((sum(fetch[k]) * f_scale + sum(write.get(k, [])) * w_scale) for k in fetch if pred(k))
+        units = sum(len(fetch[k]) for k in fetch if unit_pred(k))
+        return tot / max(1, units)
+
+    f16 = lambda k: "DF16" in k
     # one dense aggregation = one transposition of X + one dense_agg_kernel
-    agg = [r for r in rows_out if "dense_agg_kernel" in r[0] and "DF16" in r[0]]
-    xp = [r for r in rows_out if "transpose_tiled_kernel" in r[0] and "DF16" in r[0]]
-    per_launch = sum(r[2] + r[3] for r in agg) / max(1, len(agg)) + sum(r[2] + r[3] for r in xp) / max(1, len(xp))
-    spmm = [r for r in rows_out if "spmm_" in r[0] and "DF16" in r[0]]
+    dense_per_launch = per_call(lambda k: f16(k) and ("dense_agg_kernel" in k or "transpose_tiled_kernel" in k),
+                                lambda k: f16(k) and "dense_agg_kernel" in k)
+    # one CSR aggregation = one spmm_main_kernel (pieces + light rows) + its fix-up
+    spmm_per_launch = per_call(lambda k: f16(k) and "spmm_" in k, lambda k: f16(k) and "spmm_main_kernel" in k)
     summary = {
         "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
-        "dense_agg_f16": int(per_launch),
+        "dense_agg_f16": int(dense_per_launch),
         "dense_agg_f16_source_hash": kernel_hash(*DENSE_SOURCES),
-        # light, heavy and fixup kernels of one F=hidden and one F=classes aggregation, halved: bytes per launch
-        "spmm_f16": int(sum(r[2] + r[3] for r in spmm) / 2),
+        # averaged over the F = hidden and F = classes calls of an epoch (forward and backward)
+        "spmm_f16": int(spmm_per_launch),
         "spmm_f16_source_hash": kernel_hash(*SPMM_SOURCES),
     }
-    lines = ["# HBM traffic counters: dense aggregation (SBM n=16384) and CSR aggregation (R-MAT scale 21), fp16", "",
+    lines = ["# HBM traffic counters: CSR aggregation (R-MAT scale 21) and dense aggregation (SBM n=16384), fp16", "",
              "Commands (from the repository root, on one MI355X; one counter per run):", "", "```", command, "```", "",
              f"Scaling: a plain 256 MiB device copy (`--copy-calibration 256`, `__amd_rocclr_copyBuffer`) reads "
              f"{sum(cf) / len(cf) / 2**20:.1f} MiB of FETCH_SIZE and {sum(cw) / len(cw) / 2**20:.1f} MiB of WRITE_SIZE, "
@@ -799,12 +812,6 @@ def main():
     head["roofline"]["achievable_copy_gbs"] = copy_gbs
     head["roofline"]["frac_of_achievable"] = round(head["roofline"]["achieved"] / copy_gbs, 4)
 
-    cpu = None
-    if args.cpu_epochs > 0:
-        log("[bench] cpu oracle baseline on the headline workload")
-        cpu = cpu_baseline(wl, args.cpu_seconds, args.cpu_epochs)
-        log(f"[bench] cpu oracle: {cpu}")
-    del wl
 
     tiny = None
     if args.tiny_epochs > 0:
@@ -932,6 +939,14 @@ def main():
                 fp32=None if top32 is None else dict(achieved=top32["agg_l1_tflops"], peak=MFMA_PEAK_TFLOPS[0],
                                                      frac=top32["agg_l1_mfma_frac"])),
             points=pts)
+
+    cpu = None
+    if args.cpu_epochs > 0:
+        # last, after every GPU measurement: the oracle on the host cores
+        log("[bench] cpu oracle baseline on the headline workload")
+        cpu = cpu_baseline(wl, args.cpu_seconds, args.cpu_epochs)
+        log(f"[bench] cpu oracle: {cpu}")
+    del wl
 
     out = {
         "metric": METRIC,

@@ -132,7 +132,7 @@ LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
   upd((int64_t)p.dw_split * L->f_in * L->f_out);
   int64_t cs = 0;
   if (A->format != GCN_CSR) {
-    upd((int64_t)(dense_agg_workspace_bytes(prec, n, L->f_out) / sizeof(float)) + 1);
+    upd((int64_t)(dense_agg_workspace_bytes(prec, n, L->f_out, A->format == GCN_DENSE_TILED) / sizeof(float)) + 1);
     cs = dense_agg_colsum_rows(prec, n) * L->f_out;
   } else {
     upd(spmm_partials_floats(view_of(A), prec, L->f_out));
@@ -189,7 +189,7 @@ hipError_t aggregate(const gcn_adj* A, int32_t prec, const void* X, int64_t ldx,
 size_t aggregate_bytes(const gcn_adj* A, int32_t prec, int64_t F) {
   int64_t f = 0;
   if (A->format != GCN_CSR) {
-    f = (int64_t)(dense_agg_workspace_bytes(prec, A->n, F) / sizeof(float)) + 1;
+    f = (int64_t)(dense_agg_workspace_bytes(prec, A->n, F, A->format == GCN_DENSE_TILED) / sizeof(float)) + 1;
   } else {
     f = spmm_partials_floats(view_of(A), prec, F);
   }

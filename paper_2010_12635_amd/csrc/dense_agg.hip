@@ -367,6 +367,9 @@ struct MmParams {
   int64_t rblocks;    // 64-row blocks of A_hat
   int64_t fblocks;    // 64-row blocks of X^T
   int64_t tiles, cb, per_xcd;
+  int64_t ksplit, kc; // k ranges of kc chunks (the last one shorter), one per workgroup of a tile
+  float* part;        // ksplit > 1: fp32 partial products [ksplit][n][ldp]
+  int64_t ldp;        // F rounded up to a whole output vector
   Epilogue epi;
 };
 
@@ -394,6 +397,51 @@ __device__ __forceinline__ void mm_store_strip(const MmParams& p, const float* s
 
 // A wave owns WR x WC 64 x 64 blocks of the output (WR, WC in {1, 2}); the
 // workgroup's 2 x 2 waves own (128 WR) x (128 WC).
+// The same strip as fp32 partial products of k range `split`, for the
+// fixed-order reduction that applies the epilogue.
+template <int W, int OV>
+__device__ __forceinline__ void mm_store_strip_part(const MmParams& p, const float* st, int lane, int64_t row0,
+                                                    int64_t col0, int64_t split) {
+  constexpr int VPR = W / OV;
+  float* part = p.part + split * p.n * p.ldp;
+#pragma unroll 1
+  for (int k = 0; k < 16 * VPR / 64; ++k) {
+    const int idx = k * 64 + lane;
+    const int r = idx / VPR, cv = idx % VPR;
+    const int64_t row = row0 + r, col = col0 + cv * OV;
+    if (row >= p.n || col >= p.F) continue;
+    float4* o = reinterpret_cast<float4*>(part + row * p.ldp + col);
+#pragma unroll
+    for (int e = 0; e < OV / 4; ++e)
+      o[e] = make_float4(st[r * MM_LDR + cv * OV + 4 * e], st[r * MM_LDR + cv * OV + 4 * e + 1],
+                         st[r * MM_LDR + cv * OV + 4 * e + 2], st[r * MM_LDR + cv * OV + 4 * e + 3]);
+  }
+}
+
+// Sum of the k ranges' partials in range order, one output vector per
+// thread, through the vector epilogue (one Philox block per 8 outputs).
+template <typename T>
+__global__ __launch_bounds__(256) void mm_reduce_kernel(const float* __restrict__ part, int64_t ksplit, int64_t n,
+                                                        int64_t F, int64_t ldp, Epilogue epi) {
+  constexpr int VE = Vec<T>::N;
+  const int64_t vpr = ldp / VE;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= n * vpr) return;
+  const int64_t row = idx / vpr, col0 = (idx - row * vpr) * VE;
+  float acc[VE];
+#pragma unroll
+  for (int i = 0; i < VE; ++i) acc[i] = 0.f;
+  for (int64_t k = 0; k < ksplit; ++k) {
+    const float4* q = reinterpret_cast<const float4*>(part + (k * n + row) * ldp + col0);
+#pragma unroll
+    for (int e = 0; e < VE / 4; ++e) {
+      const float4 v = q[e];
+      acc[4 * e] += v.x; acc[4 * e + 1] += v.y; acc[4 * e + 2] += v.z; acc[4 * e + 3] += v.w;
+    }
+  }
+  epi_store_vec<T>(epi, row, col0, acc);
+}
+
 template <typename T, int WR, int WC, int DEPTH>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void dense_mm_kernel(MmParams p) {
   constexpr int VE = Vec<T>::N, KC = 4 * VE, PIECE = 16 * KC;
@@ -402,22 +450,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t b = blockIdx.x;
-  const int64_t t = (b & 7) * p.per_xcd + (b >> 3);
-  if (t >= p.tiles) return;
+  // units are (k range, tile), k range outermost, so that the workgroups of
+  // one die (consecutive units) share rows of A_hat as before
+  const int64_t u = (b & 7) * p.per_xcd + (b >> 3);
+  if (u >= p.tiles * p.ksplit) return;
+  const int64_t split = u / p.tiles;
+  const int64_t t = u - split * p.tiles;
   const int64_t tr = t / p.cb, tc = t - (t / p.cb) * p.cb;
   const int64_t rb0 = (tr * 2 + (wave >> 1)) * WR;   // this wave's first 64-row block
   const int64_t fb0 = (tc * 2 + (wave & 1)) * WC;    // and first 64-column block
-  const int64_t nc = p.nc;
-  const int64_t blk = nc * 4 * PIECE;                 // elements of one 64-row block
+  const int64_t c_lo = split * p.kc;                  // this workgroup's k chunks: [c_lo, c_lo + nc)
+  const int64_t nc = min(p.nc, c_lo + p.kc) - c_lo;   // >= 8 (the launch sizes the ranges so)
+  const int64_t blk = p.nc * 4 * PIECE;               // elements of one 64-row block
   const T* __restrict__ A = reinterpret_cast<const T*>(p.A);
   const T* __restrict__ Xt = reinterpret_cast<const T*>(p.Xt);
   // blocks past the padded extent read the last one (never stored)
   const T* abase[WR];
   const T* bbase[WC];
 #pragma unroll
-  for (int i = 0; i < WR; ++i) abase[i] = A + min(rb0 + i, p.rblocks - 1) * blk + lane * VE;
+  for (int i = 0; i < WR; ++i) abase[i] = A + min(rb0 + i, p.rblocks - 1) * blk + c_lo * 4 * PIECE + lane * VE;
 #pragma unroll
-  for (int i = 0; i < WC; ++i) bbase[i] = Xt + min(fb0 + i, p.fblocks - 1) * blk + lane * VE;
+  for (int i = 0; i < WC; ++i) bbase[i] = Xt + min(fb0 + i, p.fblocks - 1) * blk + c_lo * 4 * PIECE + lane * VE;
 
   f32x4 acc[TM][TN];
 #pragma unroll
@@ -498,10 +551,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #undef MM_SCHED
 
   // epilogue: one 16-row strip of the wave's block at a time (the strip
-  // index is spelled out so that every accumulator index is static)
+  // index is spelled out so that every accumulator index is static); with
+  // k ranges the strips go out as fp32 partials instead
   float* st = stage[wave];
   float bv[VE];
   epi_load_bias<T>(p.epi, fb0 * 64 + (lane % (16 * TN / VE)) * VE, bv);
+  const bool partial = p.ksplit > 1;
 #define MM_STRIP(S)                                                                             \
   if ((S) < TM) {                                                                               \
     MM_SYNC();                                                                            \
@@ -509,7 +564,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       _Pragma("unroll") for (int v = 0; v < 4; ++v)                                             \
         st[((lane >> 4) * 4 + v) * MM_LDR + j * 16 + (lane & 15)] = acc[(S) < TM ? (S) : 0][j][v]; \
     MM_SYNC();                                                                            \
-    mm_store_strip<T, 16 * TN>(p, st, lane, (rb0 + (S) / 4) * 64 + ((S) % 4) * 16, fb0 * 64, bv); \
+    if (partial) mm_store_strip_part<16 * TN, VE>(p, st, lane, (rb0 + (S) / 4) * 64 + ((S) % 4) * 16, fb0 * 64, split); \
+    else mm_store_strip<T, 16 * TN>(p, st, lane, (rb0 + (S) / 4) * 64 + ((S) % 4) * 16, fb0 * 64, bv); \
   }
   MM_STRIP(0) MM_STRIP(1) MM_STRIP(2) MM_STRIP(3) MM_STRIP(4) MM_STRIP(5) MM_STRIP(6) MM_STRIP(7)
 #undef MM_STRIP
@@ -519,6 +575,11 @@ int64_t xt_elems(int prec, int64_t n, int64_t F) {
   const int64_t kc = prec == 0 ? 16 : 32;
   const int64_t nc = (n + kc - 1) / kc;
   return ((F + 63) / 64) * 64 * nc * kc;
+}
+
+// Bytes of the transposed X, rounded up to 256 (the partials follow it).
+size_t xt_bytes(int prec, int64_t n, int64_t F) {
+  return ((size_t)xt_elems(prec, n, F) * (prec == 0 ? 4 : 2) + 255) / 256 * 256;
 }
 
 #ifndef MM_MIN_F
@@ -536,6 +597,44 @@ int64_t xt_elems(int prec, int64_t n, int64_t F) {
 // 4.8 ms; the streaming kernel takes 0.77 ms at F = 128, 1.5 ms at 256).
 bool use_dense_mm(int64_t n, int64_t F) { return F >= MM_MIN_F && n >= 256; }
 
+// Tile shape and k ranges of the wide kernel.  Fewer tiles than compute
+// units: first cut the k loop of every tile into 2, 4 or 8 ranges of at
+// least MM_SPLIT_MIN chunks each (their fp32 partials are added in range
+// order by a reduction that applies the epilogue), keeping the 128 x 128
+// accumulator tile per wave.  Where the k loop is too short for that, step
+// down to 256 x 128 or 128 x 128 workgroup tiles if that alone fills the
+// compute units, else cut the k loop into ranges of at least 8 chunks.
+// Measured in 16-bit: n = 16384, F = 512 (128 tiles): two ranges 0.29 ms,
+// 256 x 128 tiles 0.36 ms; n = 4096, F = 2048 (k loop of 128 chunks): two
+// ranges 0.108 ms, 256 x 128 tiles 0.10 ms; n = 4096, F = 512 (32 tiles):
+// eight ranges 0.054 ms, 128 x 128 tiles 0.061 ms.
+#ifndef MM_SPLIT_MIN
+#define MM_SPLIT_MIN 128
+#endif
+struct MmPlan { int wr, wc; int64_t ksplit, kc; };
+
+MmPlan mm_plan(int prec, int64_t n, int64_t F) {
+  const int64_t kcw = prec == 0 ? 16 : 32;
+  const int64_t nc = (n + kcw - 1) / kcw;
+  MmPlan pl{2, F > 384 ? 2 : 1, 1, nc};
+  auto tiles_of = [&](int wr, int wc) { return (n + 128 * wr - 1) / (128 * wr) * ((F + 128 * wc - 1) / (128 * wc)); };
+  auto split = [&](int64_t min_chunks) {
+    while (tiles_of(pl.wr, pl.wc) * pl.ksplit < MM_SMALL_TILES && pl.ksplit < 8) {
+      const int64_t k2 = pl.ksplit * 2, kc = (nc + k2 - 1) / k2;
+      if (kc < min_chunks || nc - (k2 - 1) * kc < 8) break;
+      pl.ksplit = k2;
+    }
+  };
+  split(MM_SPLIT_MIN);
+  if (pl.ksplit == 1 && tiles_of(pl.wr, pl.wc) < MM_SMALL_TILES) {
+    if (pl.wc == 2 && tiles_of(2, 1) >= MM_SMALL_TILES) pl.wc = 1;
+    else if (tiles_of(1, 1) >= MM_SMALL_TILES) pl.wr = pl.wc = 1;
+    else split(8);
+  }
+  pl.kc = (nc + pl.ksplit - 1) / pl.ksplit;
+  return pl;
+}
+
 template <typename T>
 hipError_t launch_t(const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx, int64_t F,
                     const Epilogue& epi, void* ws, float* colsum, hipStream_t s) {
@@ -549,29 +648,32 @@ hipError_t launch_t(const void* A, int64_t lda, bool tiled, int64_t n, const voi
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (tiled && use_dense_mm(n, F)) {
+    const MmPlan pl = mm_plan(sizeof(T) == 4 ? 0 : 1, n, F);
+    const int WR = pl.wr, WC = pl.wc;
     MmParams q;
     q.A = A; q.Xt = Xt; q.n = n; q.F = F; q.nc = nc;
     q.rblocks = (n + 63) / 64;
     q.fblocks = fblocks;
-    int WR = 2, WC = F > 384 ? 2 : 1;
-#ifndef MM_NO_SMALL
-    // fewer tiles than compute units: step down to 256 x 128, then to
-    // 128 x 128 workgroup tiles, so that more of the chip is busy
-    auto tiles_of = [&](int wr, int wc) { return (n + 128 * wr - 1) / (128 * wr) * ((F + 128 * wc - 1) / (128 * wc)); };
-    if (tiles_of(WR, WC) < MM_SMALL_TILES) {
-      if (WC == 2 && tiles_of(2, 1) >= MM_SMALL_TILES) WC = 1;
-      else WR = WC = 1;
-    }
-#endif
     const int64_t rt = (n + 128 * WR - 1) / (128 * WR);
     q.cb = (F + 128 * WC - 1) / (128 * WC);
     q.tiles = rt * q.cb;
-    q.per_xcd = (q.tiles + 7) / 8;
+    q.ksplit = pl.ksplit;
+    q.kc = pl.kc;
+    q.part = pl.ksplit > 1 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + xt_bytes(sizeof(T) == 4 ? 0 : 1, n, F))
+                           : nullptr;
+    q.ldp = (F + Vec<T>::N - 1) / Vec<T>::N * Vec<T>::N;
+    q.per_xcd = (q.tiles * q.ksplit + 7) / 8;
     q.epi = epi;
     const dim3 g((unsigned)(8 * q.per_xcd));
     if (WR == 1) hipLaunchKernelGGL((dense_mm_kernel<T, 1, 1, MM_DEPTH>), g, dim3(256), 0, s, q);
     else if (WC == 2) hipLaunchKernelGGL((dense_mm_kernel<T, 2, 2, MM_DEPTH>), g, dim3(256), 0, s, q);
     else hipLaunchKernelGGL((dense_mm_kernel<T, 2, 1, 2>), g, dim3(256), 0, s, q);
+    e = hipGetLastError();
+    if (e != hipSuccess || pl.ksplit == 1) return e;
+    // the k ranges' partials, added in range order, through the epilogue
+    const int64_t vecs = n * (q.ldp / Vec<T>::N);
+    hipLaunchKernelGGL(mm_reduce_kernel<T>, dim3((unsigned)((vecs + 255) / 256)), dim3(256), 0, s, q.part, pl.ksplit,
+                       n, F, q.ldp, epi);
     return hipGetLastError();
   }
   DaParams p;
@@ -633,8 +735,14 @@ hipError_t densify_t(const CsrView& A, bool tiled, void* dense, int64_t ld, hipS
 
 }  // namespace
 
-size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F) {
-  return (size_t)xt_elems(prec, n, F) * (prec == 0 ? 4 : 2);
+size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F, bool tiled) {
+  size_t b = xt_bytes(prec, n, F);
+  if (tiled && use_dense_mm(n, F)) {
+    const MmPlan pl = mm_plan(prec, n, F);
+    const int64_t ve = prec == 0 ? 4 : 8;
+    if (pl.ksplit > 1) b += (size_t)pl.ksplit * (size_t)n * (size_t)((F + ve - 1) / ve * ve) * sizeof(float);
+  }
+  return b;
 }
 
 int64_t dense_tiled_elems(int prec, int64_t n) {

@@ -111,10 +111,11 @@ hipError_t wgrad_launch(int prec, const void* H, int64_t ldh, const void* G, int
 
 // ------------------------------------------------ dense-A_hat aggregation ----
 // Y = epilogue(A_hat X) for dense A_hat (n x lda); ws holds the padded
-// transpose of X (dense_agg_workspace_bytes).  With colsum != NULL the
+// transpose of X and, for the wide kernel with k ranges, their fp32
+// partials (dense_agg_workspace_bytes).  With colsum != NULL the
 // transposition also writes column-sum partials of X, [rows][F] floats with
 // rows = dense_agg_colsum_rows(); reduce with make_job(colsum, rows, 1, F, ..).
-size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F);
+size_t dense_agg_workspace_bytes(int prec, int64_t n, int64_t F, bool tiled);
 int64_t dense_agg_colsum_rows(int prec, int64_t n);
 hipError_t dense_agg_launch(int prec, const void* A, int64_t lda, bool tiled, int64_t n, const void* X, int64_t ldx,
                             int64_t F, const Epilogue& epi, void* ws, float* colsum, hipStream_t s);

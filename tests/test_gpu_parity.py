@@ -231,6 +231,9 @@ FWD_CASES = [
     (1300, 40, 200, G.GCN_ACT_RELU, 0.5, "tiled"),
     (777, 24, 520, G.GCN_ACT_RELU, 0.3, "tiled"),
     (2048, 16, 256, G.GCN_ACT_NONE, 0.0, "tiled"),
+    # few 256-wide tiles and a long k loop: the tiles' k loops cut into
+    # ranges whose fp32 partials a reduction adds (2 ranges in 16-bit, 4 in fp32)
+    (8200, 40, 200, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "dense"),
     (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "dense"),
     (777, 16, 130, G.GCN_ACT_RELU, 0.5, "dense"),
@@ -352,6 +355,7 @@ BWD_CASES = [
     (777, 40, 130, G.GCN_ACT_RELU, 0.5, "tiled"),   # three 64-feature groups, ragged tail
     (1300, 200, 300, G.GCN_ACT_RELU, 0.5, "tiled"),  # wide G_S = A_hat dZ
     (600, 64, 448, G.GCN_ACT_NONE, 0.0, "tiled"),
+    (8200, 24, 520, G.GCN_ACT_RELU, 0.5, "tiled"),   # G_S = A_hat dZ over k ranges
 ]
 
 
