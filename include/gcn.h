@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 9
+#define GCN_ABI_VERSION 10
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -80,7 +80,7 @@ typedef enum gcn_act { GCN_ACT_NONE = 0, GCN_ACT_RELU = 1 } gcn_act;
  * The heavy-row schedule (filled by gcn_schedule) lets the CSR product split
  * rows with more than heavy_threshold entries into pieces that separate lane
  * groups sum, each into an fp32 partial row, the partials of a row then
- * added in piece order (run-to-run deterministic); with n_heavy == 0 every
+ * added in a fixed order (run-to-run deterministic); with n_heavy == 0 every
  * row is processed whole.  With col_parts = P > 1 the columns are cut into
  * P ranges [p n / P, (p + 1) n / P) and a heavy row's pieces never cross a
  * range boundary; the pieces of range p run on the chip's XCD p mod 8, so
@@ -127,7 +127,20 @@ typedef struct gcn_adj {
   const void* row_desc;           /* [n_light] 16-byte light-row descriptors
                                      in row_perm order (required with
                                      row_perm)                              */
+  int64_t n_fix;                  /* heavy rows of more than one piece       */
+  int64_t n_fix_big;              /* how many of them have more than
+                                     GCN_FIX_BIG_PIECES pieces              */
+  const int32_t* fix_rows;        /* [n_fix] heavy-row slots (indices into
+                                     heavy_rows) of the rows of more than one
+                                     piece: the n_fix_big rows of more than
+                                     GCN_FIX_BIG_PIECES pieces first, each
+                                     group in ascending order               */
 } gcn_adj;
+
+/* A heavy row of more than this many pieces has its partials added by a
+ * whole workgroup (contiguous runs of pieces per lane group, then the runs
+ * in order); fewer, by one lane group in piece order. */
+#define GCN_FIX_BIG_PIECES 32
 
 /* One layer: H (n x f_in, ld_in) -> H_out (n x f_out, ld_out); W is
  * f_in x f_out with leading dimension ld_out; bias has f_out entries.
@@ -228,8 +241,9 @@ gcn_status gcn_densify(const gcn_adj* A, int32_t format, int32_t value_prec, voi
  * rowptr, colidx must be set).  Rows with more than heavy_threshold entries
  * are cut into pieces: first at the boundaries of the col_parts column
  * ranges, then every chunk_nnz entries; a lane group sums each piece into
- * an fp32 partial row and a fix-up adds a row's partials in piece order
- * (run-to-run deterministic).  The pieces are launched grouped by column
+ * an fp32 partial row and a fix-up adds a row's partials in a fixed order
+ * (run-to-run deterministic; fix_rows lists the rows it visits).  The
+ * pieces are launched grouped by column
  * range (range p on XCD p mod 8) and, inside a range, in order of the
  * column of their first entry (chunk_order; pieces of different hubs that
  * cover the same columns then run together and share the cached rows of

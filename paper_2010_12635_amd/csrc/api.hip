@@ -5,7 +5,7 @@
 #include <cstdlib>
 #include <mutex>
 
-#include "../../include/gcn.h"
+#include "gcn.h"
 #include "internal.h"
 
 using namespace gcn;
@@ -78,6 +78,9 @@ gcn_status check_adj(const gcn_adj* A, int32_t prec) {
     if (!valid_parts(A->col_parts)) return GCN_ERR_INVALID_ARG;
     if (A->col_parts > 1 && (!A->part_off || A->part_slots <= 0)) return GCN_ERR_INVALID_ARG;
     if (!A->chunk_order || !A->piece_desc || !A->piece_pos) return GCN_ERR_INVALID_ARG;
+    if (A->n_fix < 0 || A->n_fix > A->n_heavy || A->n_fix_big < 0 || A->n_fix_big > A->n_fix) return GCN_ERR_SHAPE;
+    if (A->n_chunks > A->n_heavy && A->n_fix == 0) return GCN_ERR_INVALID_ARG;  // rows of several pieces unlisted
+    if (A->n_fix > 0 && !A->fix_rows) return GCN_ERR_INVALID_ARG;
   }
   if (A->row_perm && !A->row_desc) return GCN_ERR_INVALID_ARG;
   if (A->n_heavy > 0 && !A->row_perm) return GCN_ERR_INVALID_ARG;   // the light rows must be listed
@@ -102,6 +105,9 @@ CsrView view_of(const gcn_adj* A) {
   v.piece_desc = A->n_heavy > 0 ? static_cast<const RowDesc*>(A->piece_desc) : nullptr;
   v.piece_pos = A->n_heavy > 0 ? A->piece_pos : nullptr;
   v.row_desc = A->row_perm ? static_cast<const RowDesc*>(A->row_desc) : nullptr;
+  v.n_fix = A->n_heavy > 0 ? A->n_fix : 0;
+  v.n_fix_big = A->n_heavy > 0 ? A->n_fix_big : 0;
+  v.fix_rows = A->n_heavy > 0 ? A->fix_rows : nullptr;
   return v;
 }
 
@@ -342,6 +348,9 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, 
   A->piece_desc = o.piece_desc;
   A->piece_pos = o.piece_pos;
   A->row_desc = o.row_desc;
+  A->n_fix = o.n_fix;
+  A->n_fix_big = o.n_fix_big;
+  A->fix_rows = o.fix_rows;
   return finish(hipSuccess, s);
 }
 

@@ -284,30 +284,57 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(RedJob j0, RedJob 
   else reduce_body<T>(j1, (int64_t)blockIdx.x - j0.blocks);
 }
 
-// Column sums: a workgroup sums `rows_per_block` consecutive rows, 4 row
-// groups x 64 columns, each walking its rows in order; the row groups are
-// then added in group order.
+// Column sums: a workgroup sums `rows_per_block` consecutive rows of the
+// lpr * VE columns from blockIdx.y * lpr * VE.  Lane li of a row slot owns
+// VE columns (one 16-byte load per row); the 256 / lpr slots walk rows
+// r0 + slot, r0 + slot + slots, ... in that order with eight rows in flight,
+// then the slots are added in slot order through LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ X, int64_t rows, int64_t cols,
                                                              int64_t ld, int64_t ldp, int64_t rows_per_block,
-                                                             float* __restrict__ part) {
-  __shared__ float red[256];
-  const int64_t c = (int64_t)blockIdx.y * 64 + (threadIdx.x & 63);
-  const int rg = threadIdx.x >> 6;
+                                                             int lpr_log2, float* __restrict__ part) {
+  constexpr int VE = Vec<T>::N;
+  __shared__ float red[256 * VE];
+  const int lpr = 1 << lpr_log2, slots = 256 >> lpr_log2, width = lpr * VE;
+  const int li = threadIdx.x & (lpr - 1), slot = threadIdx.x >> lpr_log2;
+  const int64_t c0 = ((int64_t)blockIdx.y * lpr + li) * VE;
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
   const int64_t r1 = min(rows, r0 + rows_per_block);
-  float a = 0.f;
-  if (c < cols) {
-#pragma unroll 8
-    for (int64_t r = r0 + rg; r < r1; r += 4) a += to_f32<T>(X[r * ld + c]);
+  float a[VE];
+#pragma unroll
+  for (int i = 0; i < VE; ++i) a[i] = 0.f;
+  if (c0 < ldp) {                 // c0 + VE <= ldp <= ld: ldp is a multiple of 8
+    const T* __restrict__ x = X + c0;
+    int64_t r = r0 + slot;
+    for (; r + 7 * slots < r1; r += 8 * slots) {
+      uint4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = ldg16(x + (r + u * slots) * ld);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        float f[VE];
+        unpack<T>(v[u], f);
+#pragma unroll
+        for (int i = 0; i < VE; ++i) a[i] += f[i];
+      }
+    }
+    for (; r < r1; r += slots) {
+      float f[VE];
+      unpack<T>(ldg16(x + r * ld), f);
+#pragma unroll
+      for (int i = 0; i < VE; ++i) a[i] += f[i];
+    }
   }
-  red[threadIdx.x] = a;
+#pragma unroll
+  for (int i = 0; i < VE; ++i) red[slot * width + li * VE + i] = a[i];
   __syncthreads();
-  if (rg == 0 && c < ldp) {
-    float s = red[threadIdx.x] + red[threadIdx.x + 64];
-    s += red[threadIdx.x + 128];
-    s += red[threadIdx.x + 192];
-    part[(int64_t)blockIdx.x * ldp + c] = c < cols ? s : 0.f;
+  for (int t = threadIdx.x; t < width; t += 256) {
+    const int64_t c = (int64_t)blockIdx.y * width + t;
+    if (c < ldp) {
+      float sum = red[t];
+      for (int k = 1; k < slots; ++k) sum += red[k * width + t];
+      part[(int64_t)blockIdx.x * ldp + c] = c < cols ? sum : 0.f;
+    }
   }
 }
 
@@ -385,13 +412,18 @@ int64_t colsum_partials_floats(int64_t rows, int64_t ld) {
 
 hipError_t colsum_partial_launch(int prec, const void* X, int64_t rows, int64_t cols, int64_t ld, float* partials,
                                  int64_t ldp, int* splits, hipStream_t s) {
+  if (ldp % 8 || ld < ldp || (reinterpret_cast<uintptr_t>(X) & 15u)) return hipErrorInvalidValue;
   const int64_t rpb = colsum_rows_per_block(rows);
   const int64_t nb = (rows + rpb - 1) / rpb;
-  dim3 grid((unsigned)nb, (unsigned)((ldp + 63) / 64));
+  const int ve = prec == 0 ? 4 : 8;
+  int lg = 0;
+  while ((int64_t)(1 << lg) * ve < ldp && lg < 6) ++lg;
+  const int64_t width = (int64_t)ve << lg;
+  dim3 grid((unsigned)nb, (unsigned)((ldp + width - 1) / width));
   switch (prec) {
-    case 0: hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, rows, cols, ld, ldp, rpb, partials); break;
-    case 1: hipLaunchKernelGGL(colsum_partial_kernel<f16>, grid, dim3(256), 0, s, (const f16*)X, rows, cols, ld, ldp, rpb, partials); break;
-    case 2: hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, rows, cols, ld, ldp, rpb, partials); break;
+    case 0: hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, dim3(256), 0, s, (const float*)X, rows, cols, ld, ldp, rpb, lg, partials); break;
+    case 1: hipLaunchKernelGGL(colsum_partial_kernel<f16>, grid, dim3(256), 0, s, (const f16*)X, rows, cols, ld, ldp, rpb, lg, partials); break;
+    case 2: hipLaunchKernelGGL(colsum_partial_kernel<bf16>, grid, dim3(256), 0, s, (const bf16*)X, rows, cols, ld, ldp, rpb, lg, partials); break;
     default: return hipErrorInvalidValue;
   }
   *splits = (int)nb;

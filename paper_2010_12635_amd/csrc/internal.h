@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "common.h"
+#include "gcn.h"
 
 namespace gcn {
 
@@ -89,6 +90,8 @@ struct CsrView {
   const RowDesc* piece_desc;   // [n_chunks] in chunk_order positions
   const int32_t* piece_pos;    // [n_chunks] chunk_order position of each piece
   const RowDesc* row_desc;     // [n_light] in row_perm order
+  int64_t n_fix, n_fix_big;    // heavy rows of > 1 piece; of them, rows of > GCN_FIX_BIG_PIECES
+  const int32_t* fix_rows;     // [n_fix] their heavy-row slots, the big ones first
 };
 // Y = A_hat X (+ epilogue) for X: n x F (ld), Y described by epi.
 int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F);
@@ -134,10 +137,10 @@ hipError_t normalize_run(int64_t n, int64_t num_edges, const int32_t* src, const
 // Heavy-row pieces and light-row order (see gcn_schedule in gcn.h); the
 // pointers returned point into `sched`.
 struct SchedOut {
-  int32_t *heavy_rows, *heavy_chunk_off, *chunk_heavy, *row_perm, *chunk_order, *piece_pos;
+  int32_t *heavy_rows, *heavy_chunk_off, *chunk_heavy, *row_perm, *chunk_order, *piece_pos, *fix_rows;
   int64_t *chunk_beg, *part_off;
   RowDesc *piece_desc, *row_desc;
-  int64_t n_heavy, n_chunks, n_light, part_slots;
+  int64_t n_heavy, n_chunks, n_light, part_slots, n_fix, n_fix_big;
 };
 size_t schedule_bytes(int64_t n, int64_t nnz, int64_t threshold, int64_t chunk_nnz, int64_t parts);
 hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, const int32_t* colidx,

@@ -25,17 +25,49 @@ struct LossParams {
   int32_t* flag;
 };
 
-template <int LPR>
-__device__ __forceinline__ float group_max(float v) {
-#pragma unroll
-  for (int o = LPR / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+// Reductions over a lane group of LPR lanes (aligned, a power of two),
+// every lane ending with the result: lanes exchange values through DPP
+// moves inside rows of 16 lanes (quad permutations, then the half-row and
+// row mirrors, each pairing a lane with one of the other half once the
+// halves agree), across rows through lane shuffles.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
 }
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true);
+}
+constexpr int DPP_XOR1 = 0xB1;         // quad_perm [1, 0, 3, 2]
+constexpr int DPP_XOR2 = 0x4E;         // quad_perm [2, 3, 0, 1]
+constexpr int DPP_HALF_MIRROR = 0x141; // lane i <-> 7 - i of each 8
+constexpr int DPP_MIRROR = 0x140;      // lane i <-> 15 - i of each 16
+
 template <int LPR>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int o = LPR / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if (LPR >= 2) v += dpp_f<DPP_XOR1>(v);
+  if (LPR >= 4) v += dpp_f<DPP_XOR2>(v);
+  if (LPR >= 8) v += dpp_f<DPP_HALF_MIRROR>(v);
+  if (LPR >= 16) v += dpp_f<DPP_MIRROR>(v);
+  if (LPR >= 32) v += __shfl_xor(v, 16);
+  if (LPR >= 64) v += __shfl_xor(v, 32);
   return v;
+}
+
+// (maximum, lowest index among the maxima) over the group
+__device__ __forceinline__ void argmax_step(float& mx, int& am, float om, int oa) {
+  const bool take = om > mx || (om == mx && oa < am);
+  mx = take ? om : mx;
+  am = take ? oa : am;
+}
+template <int LPR>
+__device__ __forceinline__ void group_argmax(float& mx, int& am) {
+  if (LPR >= 2) argmax_step(mx, am, dpp_f<DPP_XOR1>(mx), dpp_i<DPP_XOR1>(am));
+  if (LPR >= 4) argmax_step(mx, am, dpp_f<DPP_XOR2>(mx), dpp_i<DPP_XOR2>(am));
+  if (LPR >= 8) argmax_step(mx, am, dpp_f<DPP_HALF_MIRROR>(mx), dpp_i<DPP_HALF_MIRROR>(am));
+  if (LPR >= 16) argmax_step(mx, am, dpp_f<DPP_MIRROR>(mx), dpp_i<DPP_MIRROR>(am));
+  if (LPR >= 32) argmax_step(mx, am, __shfl_xor(mx, 16), __shfl_xor(am, 16));
+  if (LPR >= 64) argmax_step(mx, am, __shfl_xor(mx, 32), __shfl_xor(am, 32));
 }
 
 // Rows handled per lane group and iteration (R): all their loads go out
@@ -44,7 +76,35 @@ __device__ __forceinline__ float group_sum(float v) {
 // LOSS_R4_GROUPS workgroups, else R = 1 (fewer rows keep more workgroups).
 constexpr int64_t LOSS_R4_GROUPS = 16384;
 
-template <typename T, int LPR, int LOSS_R>
+template <typename T> __device__ __forceinline__ float max_finite();
+template <> __device__ __forceinline__ float max_finite<float>() { return 3.40282347e38f; }
+template <> __device__ __forceinline__ float max_finite<f16>() { return 65504.f; }
+template <> __device__ __forceinline__ float max_finite<bf16>() { return 3.38953139e38f; }
+
+// Any non-finite element among the VE packed values (exponent field all ones).
+template <typename T> __device__ __forceinline__ bool packed_nonfinite(uint4 o);
+template <> __device__ __forceinline__ bool packed_nonfinite<float>(uint4 o) {
+  const uint32_t e = 0x7f800000u;
+  return (o.x & e) == e || (o.y & e) == e || (o.z & e) == e || (o.w & e) == e;
+}
+template <uint32_t E>
+__device__ __forceinline__ bool half_pair_nonfinite(uint32_t w) {
+  return (w & E) == E || (w & (E << 16)) == (E << 16);
+}
+template <> __device__ __forceinline__ bool packed_nonfinite<f16>(uint4 o) {
+  return half_pair_nonfinite<0x7c00u>(o.x) || half_pair_nonfinite<0x7c00u>(o.y) ||
+         half_pair_nonfinite<0x7c00u>(o.z) || half_pair_nonfinite<0x7c00u>(o.w);
+}
+template <> __device__ __forceinline__ bool packed_nonfinite<bf16>(uint4 o) {
+  return half_pair_nonfinite<0x7f80u>(o.x) || half_pair_nonfinite<0x7f80u>(o.y) ||
+         half_pair_nonfinite<0x7f80u>(o.z) || half_pair_nonfinite<0x7f80u>(o.w);
+}
+
+// FULL: C = LPR * VE, so every lane holds VE classes and no element needs
+// a bounds test.  The exponentials use the hardware
+// base-2 exponential of (z - max) log2(e) (relative error a few 1e-7 for the
+// arguments <= 0 that occur here).
+template <typename T, int LPR, int LOSS_R, bool FULL>
 __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
@@ -54,8 +114,9 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane / LPR, li = lane % LPR;
   const int slot = wave * G + g;
-  const int64_t col0 = (int64_t)li * VE;
-  const bool col_ok = col0 < p.C;
+  const int col0 = li * VE;
+  const bool col_ok = FULL || col0 < p.C;
+  const int nv = FULL ? VE : (int)(p.C - col0 < VE ? (p.C - col0 > 0 ? p.C - col0 : 0) : VE);   // classes of this lane
   const T* __restrict__ logits = reinterpret_cast<const T*>(p.logits);
   // the workgroup walks blocks of LOSS_R * RG rows: blockIdx.x, blockIdx.x
   // + gridDim.x, ...; a slot takes rows base + r * RG + slot, r = 0 .. LOSS_R - 1
@@ -63,6 +124,7 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   float acc_loss = 0.f;
   int32_t acc_corr = 0;
   const float sc = (p.loss_scale ? *p.loss_scale : 1.f) * p.inv_count;
+  constexpr float LOG2E = 1.4426950408889634f;
   for (int64_t base = (int64_t)blockIdx.x * (LOSS_R * RG); base < p.n; base += (int64_t)gridDim.x * (LOSS_R * RG)) {
     uint4 raw[LOSS_R];
     int32_t lab[LOSS_R];
@@ -79,57 +141,59 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
     for (int r = 0; r < LOSS_R; ++r) {
       const int64_t row = base + r * RG + slot;
       const bool row_ok = row < p.n;
-      float x[VE], z[VE];
-      unpack<T>(raw[r], x);
+      float z[VE];
+      unpack<T>(raw[r], z);
+      if (!FULL) {
 #pragma unroll
-      for (int i = 0; i < VE; ++i) z[i] = (row_ok && col0 + i < p.C) ? x[i] : -INFINITY;
-      // row maximum and arg-max (lowest index on ties)
-      float mx = -INFINITY;
-      int am = 0x7fffffff;
-#pragma unroll
-      for (int i = 0; i < VE; ++i)
-        if (col0 + i < p.C && (z[i] > mx || am == 0x7fffffff)) { mx = z[i]; am = (int)(col0 + i); }
-#pragma unroll
-      for (int o = LPR / 2; o > 0; o >>= 1) {
-        const float om = __shfl_xor(mx, o);
-        const int oa = __shfl_xor(am, o);
-        if (om > mx || (om == mx && oa < am)) { mx = om; am = oa; }
+        for (int i = 0; i < VE; ++i) z[i] = i < nv ? z[i] : -INFINITY;
       }
-      const float rmax = mx;
+      // row maximum and arg-max (lowest index on ties; a lane without
+      // classes offers -inf at an index past every class)
+      float mx = z[0];
+      int am = col_ok ? col0 : 0x7fffffff;
+#pragma unroll
+      for (int i = 1; i < VE; ++i) {
+        const bool gt = z[i] > mx;
+        mx = gt ? z[i] : mx;
+        am = gt ? col0 + i : am;
+      }
+      group_argmax<LPR>(mx, am);
+      const float mlog = mx * LOG2E;
       // exp(z - max) once per element: the sum of exponentials and, scaled
       // by its reciprocal, the softmax of the gradient
       float ez[VE];
       float se = 0.f;
 #pragma unroll
       for (int i = 0; i < VE; ++i) {
-        ez[i] = (col0 + i < p.C) ? expf(z[i] - rmax) : 0.f;
+        ez[i] = __builtin_amdgcn_exp2f(fmaf(z[i], LOG2E, -mlog));
+        if (!FULL) ez[i] = i < nv ? ez[i] : 0.f;
         se += ez[i];
       }
       se = group_sum<LPR>(se);
-      const float lse = rmax + logf(se);
+      const float lse = mx + logf(se);
       const float inv_se = 1.f / se;
       const int32_t y = row_ok ? lab[r] : 0;
+      const int ky = y - col0;                       // the label's element in this lane, if in [0, VE)
       float zy = 0.f;
 #pragma unroll
-      for (int i = 0; i < VE; ++i)
-        if (col0 + i == y) zy = z[i];
+      for (int i = 0; i < VE; ++i) zy = i == ky ? z[i] : zy;
       zy = group_sum<LPR>(zy);
       const bool in_mask = row_ok && msk[r] != 0;
       if (row_ok && col_ok) {
         float d[VE];
+        const float s_in = in_mask ? sc : 0.f;
 #pragma unroll
-        for (int i = 0; i < VE; ++i) {
-          const int64_t c = col0 + i;
-          if (c < p.C && in_mask) d[i] = (ez[i] * inv_se - (c == y ? 1.f : 0.f)) * sc;
-          else d[i] = 0.f;
+        for (int i = 0; i < VE; ++i) d[i] = (ez[i] * inv_se - (i == ky ? 1.f : 0.f)) * s_in;
+        if (!FULL) {
+#pragma unroll
+          for (int i = 0; i < VE; ++i) d[i] = i < nv ? d[i] : 0.f;
         }
-        uint4 o = pack<T>(d);
+        const uint4 o = pack<T>(d);
         stg16(reinterpret_cast<T*>(p.dlogits) + row * p.ld + col0, o);
-        bool bad = false;
-        const T* e = reinterpret_cast<const T*>(&o);
-#pragma unroll
-        for (int i = 0; i < VE; ++i) bad |= !finite_f32(to_f32<T>(e[i]));
-        if (bad) raise_flag(p.flag);
+        // |d| <= |s_in| (softmax values lie in [0, 1]): with finite logits
+        // (lse finite) and |s_in| at most the largest finite value of T no
+        // element can overflow; otherwise every element is checked
+        if (!(finite_f32(lse) && fabsf(s_in) <= max_finite<T>()) && packed_nonfinite<T>(o)) raise_flag(p.flag);
       }
       acc_loss += in_mask ? (lse - zy) : 0.f;
       acc_corr += (in_mask && am == y) ? 1 : 0;
@@ -149,6 +213,8 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   }
 }
 
+// Thread t adds partials t, t + 256, ... in that order (eight loads in
+// flight), then the 256 sums are added by a fixed tree.
 __global__ __launch_bounds__(256) void loss_final_kernel(const float* __restrict__ part, const int32_t* __restrict__ corr,
                                                          int64_t nb, float inv_count, float* loss, int32_t* n_correct,
                                                          int32_t* flag) {
@@ -156,7 +222,16 @@ __global__ __launch_bounds__(256) void loss_final_kernel(const float* __restrict
   __shared__ int32_t sc[256];
   float a = 0.f;
   int32_t c = 0;
-  for (int64_t i = threadIdx.x; i < nb; i += 256) { a += part[i]; c += corr[i]; }
+  int64_t i = threadIdx.x;
+  for (; i + 7 * 256 < nb; i += 8 * 256) {
+    float v[8];
+    int32_t k[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) { v[u] = part[i + u * 256]; k[u] = corr[i + u * 256]; }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) { a += v[u]; c += k[u]; }
+  }
+  for (; i < nb; i += 256) { a += part[i]; c += corr[i]; }
   sl[threadIdx.x] = a;
   sc[threadIdx.x] = c;
   __syncthreads();
@@ -183,14 +258,20 @@ int loss_rows_per_iter(int64_t n, int64_t rows_per_group) {
   return (n + rows_per_group - 1) / rows_per_group > LOSS_R4_GROUPS ? 4 : 1;
 }
 
-template <typename T, int LPR>
-hipError_t launch_cfg(const LossParams& p, hipStream_t s) {
+template <typename T, int LPR, bool FULL>
+hipError_t launch_full(const LossParams& p, hipStream_t s) {
   constexpr int64_t RG = 4 * (64 / LPR);
   if (loss_rows_per_iter(p.n, RG) == 4)
-    hipLaunchKernelGGL((softmax_ce_kernel<T, LPR, 4>), dim3((unsigned)loss_blocks(p.n, 4 * RG)), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((softmax_ce_kernel<T, LPR, 4, FULL>), dim3((unsigned)loss_blocks(p.n, 4 * RG)), dim3(256), 0, s,
+                       p);
   else
-    hipLaunchKernelGGL((softmax_ce_kernel<T, LPR, 1>), dim3((unsigned)loss_blocks(p.n, RG)), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((softmax_ce_kernel<T, LPR, 1, FULL>), dim3((unsigned)loss_blocks(p.n, RG)), dim3(256), 0, s, p);
   return hipGetLastError();
+}
+
+template <typename T, int LPR>
+hipError_t launch_cfg(const LossParams& p, hipStream_t s) {
+  return p.C == LPR * Vec<T>::N ? launch_full<T, LPR, true>(p, s) : launch_full<T, LPR, false>(p, s);
 }
 
 template <typename T>

@@ -503,6 +503,31 @@ __global__ void piece_desc_kernel(int64_t n_chunks, const IdxT* __restrict__ row
   }
 }
 
+// Heavy rows whose partials the fix-up adds (more than one piece), flagged
+// for two stable compactions: big[h] for more than GCN_FIX_BIG_PIECES
+// pieces, small[h] for 2 .. GCN_FIX_BIG_PIECES; entry n_heavy is 0.
+__global__ void fix_flag_kernel(int64_t n_heavy, const int32_t* __restrict__ heavy_chunk_off, int64_t* __restrict__ big,
+                                int64_t* __restrict__ small) {
+  for (int64_t h = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; h <= n_heavy; h += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t m = h < n_heavy ? heavy_chunk_off[h + 1] - heavy_chunk_off[h] : 0;
+    big[h] = m > GCN_FIX_BIG_PIECES ? 1 : 0;
+    small[h] = m >= 2 && m <= GCN_FIX_BIG_PIECES ? 1 : 0;
+  }
+}
+
+// fix_rows = [big rows ascending, small rows ascending] from the exclusive
+// scans of the flags.
+__global__ void fix_scatter_kernel(int64_t n_heavy, const int32_t* __restrict__ heavy_chunk_off,
+                                   const int64_t* __restrict__ big_off, const int64_t* __restrict__ small_off,
+                                   int32_t* __restrict__ fix_rows) {
+  const int64_t n_big = big_off[n_heavy];
+  for (int64_t h = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; h < n_heavy; h += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t m = heavy_chunk_off[h + 1] - heavy_chunk_off[h];
+    if (m > GCN_FIX_BIG_PIECES) fix_rows[big_off[h]] = (int32_t)h;
+    else if (m >= 2) fix_rows[n_big + small_off[h]] = (int32_t)h;
+  }
+}
+
 __global__ void chunk_key_kernel(int64_t n, int64_t n_chunks, const int32_t* __restrict__ colidx,
                                  const int64_t* __restrict__ chunk_beg, int32_t* __restrict__ key,
                                  int32_t* __restrict__ hist) {
@@ -649,6 +674,7 @@ size_t schedule_bytes(int64_t n, int64_t nnz, int64_t thr, int64_t chunk_nnz, in
   b += align256(sizeof(int64_t) * (parts + 1));                 // part_off
   b += align256(sizeof(RowDesc) * max_chunks);                  // piece descriptors
   b += align256(sizeof(int32_t) * max_chunks);                  // launch position of each piece
+  b += align256(sizeof(int32_t) * n);                           // fix_rows
   b += align256(sizeof(RowDesc) * n);                           // light-row descriptors
   b += align256(sizeof(int32_t) * n);                           // row_perm
   b += align256(sizeof(int64_t) * (n + 1));                     // flags -> heavy index
@@ -680,6 +706,7 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   int64_t* poff = (int64_t*)take(sizeof(int64_t) * (parts + 1));
   RowDesc* pdesc = (RowDesc*)take(sizeof(RowDesc) * max_chunks);
   int32_t* ppos = (int32_t*)take(sizeof(int32_t) * max_chunks);
+  int32_t* fixr = (int32_t*)take(sizeof(int32_t) * n);
   RowDesc* ldesc = (RowDesc*)take(sizeof(RowDesc) * n);
   int32_t* perm = (int32_t*)take(sizeof(int32_t) * n);
   int64_t* hidx = (int64_t*)take(sizeof(int64_t) * (n + 1));
@@ -736,7 +763,7 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   // them by column range
   const int64_t nch = host[1];
   if (nch > max_chunks) return hipErrorInvalidValue;
-  int64_t slots = 0;
+  int64_t slots = 0, n_fix = 0, n_fix_big = 0;
   if (nch > 0) {
     GCN_TRY(fill_zero(chist, sizeof(int32_t) * CHUNK_BUCKETS, s));
     GCN_TRY(fill_zero(ccur, sizeof(int32_t) * CHUNK_BUCKETS, s));
@@ -754,10 +781,23 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
     else
       hipLaunchKernelGGL(piece_desc_kernel<int32_t>, dim3(grid_for(nch)), dim3(256), 0, s, nch, (const int32_t*)rowptr, corder, ch, hr, hco, cbeg, pdesc, ppos);
     GCN_TRY(hipGetLastError());
+    // rows for the fix-up; hidx and choff (free again) hold the flag scans
+    const int64_t nh = host[0];
+    hipLaunchKernelGGL(fix_flag_kernel, dim3(grid_for(nh + 1)), dim3(256), 0, s, nh, hco, hidx, choff);
+    GCN_TRY(hipGetLastError());
+    GCN_TRY(scan_exclusive(hidx, nh + 1, scr, s));
+    GCN_TRY(scan_exclusive(choff, nh + 1, scr, s));
+    hipLaunchKernelGGL(fix_scatter_kernel, dim3(grid_for(nh)), dim3(256), 0, s, nh, hco, hidx, choff, fixr);
+    GCN_TRY(hipGetLastError());
+    int64_t nfix[2] = {0, 0};
+    GCN_TRY(hipMemcpyAsync(&nfix[0], hidx + nh, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    GCN_TRY(hipMemcpyAsync(&nfix[1], choff + nh, sizeof(int64_t), hipMemcpyDeviceToHost, s));
     // the most pieces one XCD takes: ranges x, x + 8, ... run on XCD x
     std::vector<int64_t> hp((size_t)parts + 1);
     GCN_TRY(hipMemcpyAsync(hp.data(), poff, sizeof(int64_t) * (parts + 1), hipMemcpyDeviceToHost, s));
     GCN_TRY(hipStreamSynchronize(s));
+    n_fix_big = nfix[0];
+    n_fix = nfix[0] + nfix[1];
     if (parts > 1) {
       for (int64_t x = 0; x < XCDS; ++x) {
         int64_t t = 0;
@@ -773,6 +813,7 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
   out->chunk_order = nch > 0 ? corder : nullptr;
   out->chunk_beg = cbeg; out->part_off = poff; out->part_slots = slots;
   out->piece_desc = pdesc; out->piece_pos = ppos; out->row_desc = ldesc;
+  out->fix_rows = fixr; out->n_fix = n_fix; out->n_fix_big = n_fix_big;
   out->n_heavy = host[0]; out->n_chunks = nch; out->n_light = host[2];
   return hipSuccess;
 }

@@ -18,11 +18,12 @@
 //    caches rows of X from its own 1/P-th of the columns: on R-MAT graphs,
 //    whose hubs' neighbours are spread over every column, this is what
 //    makes the gathered rows of the hubs hit in L2.  Inside a range the
-//    pieces run in order of their first column.  A fix-up sums each heavy
-//    row's partials in piece order (4 waves over quarters of the pieces,
-//    then the quarters in wave order) and applies the epilogue; a row of
-//    one piece is stored by its piece.  No atomics: results are run-to-run
-//    identical.
+//    pieces run in order of their first column.  A fix-up adds the
+//    partials of each row of several pieces in a fixed order (a lane group
+//    per row in piece order; a workgroup per row of more than
+//    GCN_FIX_BIG_PIECES pieces, contiguous runs per lane group, then the
+//    runs in order) and applies the epilogue; a row of one piece is stored
+//    by its piece.  No atomics: results are run-to-run identical.
 #include "internal.h"
 
 namespace gcn {
@@ -191,6 +192,8 @@ struct PieceParams {
   const int32_t* heavy_rows;
   const int32_t* heavy_chunk_off;
   const int64_t* part_off;
+  const int32_t* fix_rows;      // [n_fix] heavy-row slots of the rows of > 1 piece, big ones first
+  int64_t n_fix, n_fix_big;
   int64_t n_chunks;
   int64_t parts;
   const int32_t* colidx;
@@ -271,42 +274,98 @@ __global__ __launch_bounds__(256) void spmm_main_kernel(SpmmParams<IdxT> p, Piec
   else spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, b - n_piece_wg, (int64_t)gridDim.x - n_piece_wg);
 }
 
-// Workgroup (heavy row, 64 columns): wave v adds the partials of the v-th
-// quarter of the row's pieces in piece order (8 loads in flight), then the
-// quarters are added in wave order and the epilogue stores the row.  Rows
-// of one piece were stored by their piece.
-template <typename T>
-__global__ __launch_bounds__(256) void spmm_piece_fixup_kernel(PieceParams p) {
-  __shared__ float red[4][64];
-  const int64_t h = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t col = (int64_t)blockIdx.y * 64 + lane;
-  const int64_t c0 = p.heavy_chunk_off[h], c1 = p.heavy_chunk_off[h + 1];
-  if (c1 - c0 == 1) return;                       // the same for the whole workgroup
-  const int64_t quarter = (c1 - c0 + 3) / 4;
-  const int64_t a0 = c0 + wave * quarter;
-  const int64_t a1 = a0 + quarter < c1 ? a0 + quarter : c1;
-  float a = 0.f;
-  if (col < p.F) {
-    const float* __restrict__ part = p.partials + col;
-    int64_t c = a0;
-    for (; c + 8 <= a1; c += 8) {
-      float v[8];
+// Partials of launch positions pos_of[a0 .. a1) (VE columns from col0) into
+// acc, in that order: rounds of 4 rows in flight, the last 1 .. 3 in one
+// round at clamped in-bounds positions whose surplus terms are dropped.
+template <int VE>
+__device__ __forceinline__ void add_partials(float* acc, const PieceParams& p, int64_t col0, int64_t a0, int64_t a1) {
+  const float* __restrict__ part = p.partials + col0;
+  int64_t c = a0;
+  for (; c + 4 <= a1; c += 4) {
+    int32_t q[4];
+    float4 v[4][VE / 4];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)p.pos_of[c + u] * p.ldp];
+    for (int u = 0; u < 4; ++u) q[u] = p.pos_of[c + u];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) a += v[u];
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int i = 0; i < VE / 4; ++i) v[u][i] = reinterpret_cast<const float4*>(part + (int64_t)q[u] * p.ldp)[i];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int i = 0; i < VE / 4; ++i) {
+        acc[4 * i] += v[u][i].x; acc[4 * i + 1] += v[u][i].y;
+        acc[4 * i + 2] += v[u][i].z; acc[4 * i + 3] += v[u][i].w;
+      }
+  }
+  if (c < a1) {
+    int32_t q[3];
+    float4 v[3][VE / 4];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) q[u] = p.pos_of[c + u < a1 ? c + u : a1 - 1];
+#pragma unroll
+    for (int u = 0; u < 3; ++u)
+#pragma unroll
+      for (int i = 0; i < VE / 4; ++i) v[u][i] = reinterpret_cast<const float4*>(part + (int64_t)q[u] * p.ldp)[i];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+      const bool live = c + u < a1;
+#pragma unroll
+      for (int i = 0; i < VE / 4; ++i) {
+        acc[4 * i] = live ? acc[4 * i] + v[u][i].x : acc[4 * i];
+        acc[4 * i + 1] = live ? acc[4 * i + 1] + v[u][i].y : acc[4 * i + 1];
+        acc[4 * i + 2] = live ? acc[4 * i + 2] + v[u][i].z : acc[4 * i + 2];
+        acc[4 * i + 3] = live ? acc[4 * i + 3] + v[u][i].w : acc[4 * i + 3];
+      }
     }
-    for (; c < a1; ++c) a += part[(int64_t)p.pos_of[c] * p.ldp];
   }
-  red[wave][lane] = a;
-  __syncthreads();
-  if (wave == 0 && col < p.F) {
-    float t = red[0][lane] + red[1][lane];
-    t += red[2][lane];
-    t += red[3][lane];
-    epi_store1<T>(p.epi, p.heavy_rows[h], col, t);
+}
+
+// Fix-up of the heavy rows of more than one piece (fix_rows), the lane
+// geometry that of the main kernel (lane li of a group owns VE columns):
+//  * workgroups [0, n_fix_big): one row of more than GCN_FIX_BIG_PIECES
+//    pieces each; lane group k of the workgroup adds the k-th contiguous run
+//    of the row's pieces in piece order, the runs are then added in group
+//    order through LDS and the epilogue stores the row;
+//  * the other workgroups: one row per lane group, its partials added in
+//    piece order.
+template <typename T, int LPR>
+__global__ __launch_bounds__(256) void spmm_fixup_kernel(PieceParams p) {
+  constexpr int VE = Vec<T>::N;
+  constexpr int NG = 4 * (64 / LPR);              // lane groups per workgroup
+  const int gi = threadIdx.x / LPR, li = threadIdx.x % LPR;
+  const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
+  const bool live = col0 < p.F;
+  const int64_t b = blockIdx.x;
+  float acc[VE];
+#pragma unroll
+  for (int i = 0; i < VE; ++i) acc[i] = 0.f;
+  if (b < p.n_fix_big) {
+    __shared__ float red[NG][LPR * VE];
+    const int64_t h = p.fix_rows[b];
+    const int64_t c0 = p.heavy_chunk_off[h], c1 = p.heavy_chunk_off[h + 1];
+    const int64_t per = (c1 - c0 + NG - 1) / NG;
+    const int64_t a0 = c0 + gi * per < c1 ? c0 + gi * per : c1;
+    const int64_t a1 = a0 + per < c1 ? a0 + per : c1;
+    if (live) add_partials<VE>(acc, p, col0, a0, a1);
+#pragma unroll
+    for (int i = 0; i < VE; ++i) red[gi][li * VE + i] = acc[i];
+    __syncthreads();
+    if (gi == 0 && live) {
+#pragma unroll
+      for (int i = 0; i < VE; ++i) acc[i] = red[0][li * VE + i];
+      for (int k = 1; k < NG; ++k)
+#pragma unroll
+        for (int i = 0; i < VE; ++i) acc[i] += red[k][li * VE + i];
+      epi_store_vec<T>(p.epi, p.heavy_rows[h], col0, acc);
+    }
+    return;
   }
+  const int64_t slot = p.n_fix_big + (b - p.n_fix_big) * NG + gi;
+  if (slot >= p.n_fix || !live) return;
+  const int64_t h = p.fix_rows[slot];
+  add_partials<VE>(acc, p, col0, p.heavy_chunk_off[h], p.heavy_chunk_off[h + 1]);
+  epi_store_vec<T>(p.epi, p.heavy_rows[h], col0, acc);
 }
 
 // Workgroups of each kind in one launch: enough for every lane group to
@@ -343,6 +402,7 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   PieceParams pp;
   pp.desc = A.piece_desc; pp.pos_of = A.piece_pos;
   pp.heavy_rows = A.heavy_rows; pp.heavy_chunk_off = A.heavy_chunk_off; pp.part_off = A.part_off;
+  pp.fix_rows = A.fix_rows; pp.n_fix = A.n_fix; pp.n_fix_big = A.n_fix_big;
   pp.n_chunks = A.n_chunks; pp.parts = A.parts;
   pp.colidx = A.colidx; pp.values = A.values; pp.dinv = A.dinv;
   pp.X = X; pp.ldx = ldx; pp.F = F;
@@ -361,9 +421,9 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
                      dim3((unsigned)(n_piece_wg + lblocks), (unsigned)colblocks), dim3(256), 0, s, p, pp, n_piece_wg);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (A.n_chunks == A.n_heavy) return hipSuccess;     // every heavy row is one piece: all stored
-  dim3 gridf((unsigned)A.n_heavy, (unsigned)((F + 63) / 64));
-  hipLaunchKernelGGL((spmm_piece_fixup_kernel<T>), gridf, dim3(256), 0, s, pp);
+  if (A.n_fix <= 0) return hipSuccess;               // every heavy row is one piece: all stored
+  const int64_t fix_wg = A.n_fix_big + (A.n_fix - A.n_fix_big + per_wg - 1) / per_wg;
+  hipLaunchKernelGGL((spmm_fixup_kernel<T, LPR>), dim3((unsigned)fix_wg, (unsigned)colblocks), dim3(256), 0, s, pp);
   return hipGetLastError();
 }
 

@@ -71,6 +71,7 @@ class GcnAdj(ctypes.Structure):
         ("chunk_order", ctypes.c_void_p), ("chunk_beg", ctypes.c_void_p), ("part_off", ctypes.c_void_p),
         ("col_parts", ctypes.c_int64), ("part_slots", ctypes.c_int64),
         ("piece_desc", ctypes.c_void_p), ("piece_pos", ctypes.c_void_p), ("row_desc", ctypes.c_void_p),
+        ("n_fix", ctypes.c_int64), ("n_fix_big", ctypes.c_int64), ("fix_rows", ctypes.c_void_p),
     ]
 
 
@@ -95,6 +96,9 @@ class GcnAdamConfig(ctypes.Structure):
                 ("interval", ctypes.c_int32), ("min_scale", ctypes.c_float),
                 ("max_scale", ctypes.c_float)]
 
+
+ABI_VERSION = 10          # GCN_ABI_VERSION of the structs above
+FIX_BIG_PIECES = 32       # GCN_FIX_BIG_PIECES
 
 _lib = None
 
@@ -150,6 +154,9 @@ def lib():
         f = getattr(L, name)
         f.restype = res
         f.argtypes = args
+    if L.gcn_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"{LIB_PATH} has ABI version {L.gcn_abi_version()}, this binding expects "
+                           f"{ABI_VERSION}: rebuild it")
     _lib = L
     return L
 

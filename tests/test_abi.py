@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert G.gcn_abi_version() == 9
+    assert G.gcn_abi_version() == 10
     assert G.gcn_status_string(0) == "GCN_OK"
     for s in range(1, 9):
         assert G.gcn_status_string(s).startswith("GCN_ERR_")
@@ -41,7 +41,7 @@ def test_abi_version_and_status_strings():
 
 
 def test_struct_sizes_match_header_layout():
-    assert ctypes.sizeof(G.GcnAdj) == 8 * 2 + 4 * 4 + 8 * 5 + 8 * 5 + 8 * 3 + 8 * 3 + 8 * 4 + 8 * 3
+    assert ctypes.sizeof(G.GcnAdj) == 8 * 2 + 4 * 4 + 8 * 5 + 8 * 5 + 8 * 3 + 8 * 3 + 8 * 4 + 8 * 3 + 8 * 3
     assert ctypes.sizeof(G.GcnLayer) == 8 * 4 + 4 * 4 + 8
     assert ctypes.sizeof(G.GcnScaler) == 16
     assert ctypes.sizeof(G.GcnAdamConfig) == 36

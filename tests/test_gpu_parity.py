@@ -128,7 +128,8 @@ def _expected_pieces(g, heavy, chunk, parts):
 @pytest.mark.parametrize("parts", [1, 8, 16])
 def test_schedule_lists_heavy_rows(parts):
     n = 3000
-    src, dst = hub_graph(n, 9000, [(5, 400), (17, 120), (2999, 1000)], seed=3)
+    # hub 1234 has more than GCN_FIX_BIG_PIECES pieces of 64 entries
+    src, dst = hub_graph(n, 9000, [(5, 400), (17, 120), (2999, 1000), (1234, 4000)], seed=3)
     g = O.graph(n, src, dst)
     dg = DeviceGraph(n, src, dst, prec=G.GCN_F16, heavy_threshold=32, chunk_nnz=64, col_parts=parts)
     a = dg.adj
@@ -192,6 +193,13 @@ def test_schedule_lists_heavy_rows(parts):
         assert a.part_slots == max(per_xcd)
     else:
         assert a.part_slots == a.n_chunks
+    # rows for the fix-up: every heavy row of several pieces once, those of
+    # more than GCN_FIX_BIG_PIECES pieces first, each group ascending
+    big = np.flatnonzero(want_cnt > G.FIX_BIG_PIECES)
+    small = np.flatnonzero((want_cnt >= 2) & (want_cnt <= G.FIX_BIG_PIECES))
+    assert a.n_fix_big == big.size and a.n_fix == big.size + small.size
+    fix = rd(a.fix_rows, a.n_fix, torch.int32, 4)
+    assert np.array_equal(fix, np.concatenate([big, small]))
 
 
 # ------------------------------------------------------------ layer fwd ----
@@ -223,6 +231,9 @@ FWD_CASES = [
     (3000, 500, 64, G.GCN_ACT_RELU, 0.5, "csr_parts"),
     (2100, 40, 130, G.GCN_ACT_RELU, 0.3, "csr_parts"),
     (3000, 128, 7, G.GCN_ACT_NONE, 0.0, "csr_smallpieces"),
+    # rows wider than one lane group (2 column blocks in 16-bit, 3 in fp32),
+    # a hub of more than GCN_FIX_BIG_PIECES pieces, dropout in the fix-up
+    (2000, 24, 600, G.GCN_ACT_RELU, 0.5, "csr_smallpieces"),
     (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1500, 64, 32, G.GCN_ACT_NONE, 0.0, "tiled"),
     (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "tiled"),
@@ -349,6 +360,7 @@ BWD_CASES = [
     (1800, 24, 72, G.GCN_ACT_RELU, 0.5, "csr_onechunk"),
     (3000, 64, 7, G.GCN_ACT_RELU, 0.5, "csr_parts"),
     (2100, 130, 40, G.GCN_ACT_RELU, 0.3, "csr_smallpieces"),
+    (2000, 40, 600, G.GCN_ACT_RELU, 0.5, "csr"),
     (1500, 64, 32, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "dense"),
@@ -420,9 +432,10 @@ def test_bwd_power_of_two_scale_invariance():
 # ----------------------------------------------------------------- loss ----
 
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
-@pytest.mark.parametrize("C", [7, 40, 64])
-def test_loss(prec, C):
-    n = 5000
+@pytest.mark.parametrize("C,n", [(7, 5000), (40, 5000), (64, 5000), (32, 5000),
+                                 # more than 16384 row groups: four rows per lane group and iteration
+                                 (64, 600_003), (40, 600_003)])
+def test_loss(prec, C, n):
     rng = np.random.default_rng(C)
     z = (rng.standard_normal((n, C)) * 3).astype(np.float32)
     y = rng.integers(0, C, n).astype(np.int32)
