@@ -87,8 +87,9 @@ typedef enum gcn_act { GCN_ACT_NONE = 0, GCN_ACT_RELU = 1 } gcn_act;
  * each XCD's L2 caches the rows of X of its own column ranges only.
  * gcn_schedule also lists the other ("light") rows in order of decreasing
  * degree (row_perm), so that the rows a wavefront processes together have
- * similar lengths; with row_perm == NULL rows are processed in index
- * order. */
+ * similar lengths, the rows of a single entry last (n_light_single of them,
+ * which a lane group takes four at a time); with row_perm == NULL rows
+ * are processed in index order. */
 typedef struct gcn_adj {
   int64_t n;
   int64_t nnz;
@@ -127,6 +128,8 @@ typedef struct gcn_adj {
   const void* row_desc;           /* [n_light] 16-byte light-row descriptors
                                      in row_perm order (required with
                                      row_perm)                              */
+  int64_t n_light_single;         /* the last n_light_single rows of row_perm
+                                     (and row_desc) have exactly one entry  */
   int64_t n_fix;                  /* heavy rows of more than one piece       */
   int64_t n_fix_big;              /* how many of them have more than
                                      GCN_FIX_BIG_PIECES pieces              */

@@ -85,6 +85,7 @@ gcn_status check_adj(const gcn_adj* A, int32_t prec) {
   if (A->row_perm && !A->row_desc) return GCN_ERR_INVALID_ARG;
   if (A->n_heavy > 0 && !A->row_perm) return GCN_ERR_INVALID_ARG;   // the light rows must be listed
   if (A->row_perm && (A->n_light < 0 || A->n_light > A->n)) return GCN_ERR_SHAPE;
+  if (A->row_perm && (A->n_light_single < 0 || A->n_light_single > A->n_light)) return GCN_ERR_SHAPE;
   return GCN_OK;
 }
 
@@ -105,6 +106,7 @@ CsrView view_of(const gcn_adj* A) {
   v.piece_desc = A->n_heavy > 0 ? static_cast<const RowDesc*>(A->piece_desc) : nullptr;
   v.piece_pos = A->n_heavy > 0 ? A->piece_pos : nullptr;
   v.row_desc = A->row_perm ? static_cast<const RowDesc*>(A->row_desc) : nullptr;
+  v.n_light_single = A->row_perm ? A->n_light_single : 0;
   v.n_fix = A->n_heavy > 0 ? A->n_fix : 0;
   v.n_fix_big = A->n_heavy > 0 ? A->n_fix_big : 0;
   v.fix_rows = A->n_heavy > 0 ? A->fix_rows : nullptr;
@@ -348,6 +350,7 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, 
   A->piece_desc = o.piece_desc;
   A->piece_pos = o.piece_pos;
   A->row_desc = o.row_desc;
+  A->n_light_single = o.n_light_single;
   A->n_fix = o.n_fix;
   A->n_fix_big = o.n_fix_big;
   A->fix_rows = o.fix_rows;

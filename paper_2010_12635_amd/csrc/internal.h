@@ -90,6 +90,7 @@ struct CsrView {
   const RowDesc* piece_desc;   // [n_chunks] in chunk_order positions
   const int32_t* piece_pos;    // [n_chunks] chunk_order position of each piece
   const RowDesc* row_desc;     // [n_light] in row_perm order
+  int64_t n_light_single;      // the last rows of row_perm / row_desc with exactly one entry
   int64_t n_fix, n_fix_big;    // heavy rows of > 1 piece; of them, rows of > GCN_FIX_BIG_PIECES
   const int32_t* fix_rows;     // [n_fix] their heavy-row slots, the big ones first
 };
@@ -140,7 +141,7 @@ struct SchedOut {
   int32_t *heavy_rows, *heavy_chunk_off, *chunk_heavy, *row_perm, *chunk_order, *piece_pos, *fix_rows;
   int64_t *chunk_beg, *part_off;
   RowDesc *piece_desc, *row_desc;
-  int64_t n_heavy, n_chunks, n_light, part_slots, n_fix, n_fix_big;
+  int64_t n_heavy, n_chunks, n_light, part_slots, n_fix, n_fix_big, n_light_single;
 };
 size_t schedule_bytes(int64_t n, int64_t nnz, int64_t threshold, int64_t chunk_nnz, int64_t parts);
 hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, const int32_t* colidx,

@@ -71,6 +71,7 @@ class GcnAdj(ctypes.Structure):
         ("chunk_order", ctypes.c_void_p), ("chunk_beg", ctypes.c_void_p), ("part_off", ctypes.c_void_p),
         ("col_parts", ctypes.c_int64), ("part_slots", ctypes.c_int64),
         ("piece_desc", ctypes.c_void_p), ("piece_pos", ctypes.c_void_p), ("row_desc", ctypes.c_void_p),
+        ("n_light_single", ctypes.c_int64),
         ("n_fix", ctypes.c_int64), ("n_fix_big", ctypes.c_int64), ("fix_rows", ctypes.c_void_p),
     ]
 

@@ -41,7 +41,7 @@ def test_abi_version_and_status_strings():
 
 
 def test_struct_sizes_match_header_layout():
-    assert ctypes.sizeof(G.GcnAdj) == 8 * 2 + 4 * 4 + 8 * 5 + 8 * 5 + 8 * 3 + 8 * 3 + 8 * 4 + 8 * 3 + 8 * 3
+    assert ctypes.sizeof(G.GcnAdj) == 8 * 2 + 4 * 4 + 8 * 5 + 8 * 5 + 8 * 3 + 8 * 3 + 8 * 4 + 8 * 3 + 8 * 4
     assert ctypes.sizeof(G.GcnLayer) == 8 * 4 + 4 * 4 + 8
     assert ctypes.sizeof(G.GcnScaler) == 16
     assert ctypes.sizeof(G.GcnAdamConfig) == 36

@@ -57,18 +57,22 @@ def test_csr_at_2pow26(big):
         assert np.array_equal(got, big["nbrs"][int(r)]), r
         assert dinv[r] == np.float32(1.0 / np.sqrt(np.float64(deg[r])))
     assert dg.adj.n_heavy == int((deg > 512).sum()) >= 1
-    # light-row schedule: every light row once, in blocks of 4096 consecutive
-    # ids, decreasing degree inside a block
+    # light-row schedule: every light row once; the rows of several entries
+    # in blocks of 4096 consecutive ids, decreasing degree inside a block,
+    # then the rows of one entry
     a = dg.adj
     base = dg.sched
     o = a.row_perm - base.data_ptr()
     perm = base[o: o + 4 * a.n_light].view(torch.int32).cpu().numpy()
     light = deg <= 512
     assert a.n_light == int(light.sum())
-    blk = perm.astype(np.int64) // 4096
+    assert a.n_light_single == int((deg == 1).sum()) > 0
+    multi = perm[: a.n_light - a.n_light_single]
+    assert np.all(deg[perm[a.n_light - a.n_light_single:]] == 1) and np.all(deg[multi] > 1)
+    blk = multi.astype(np.int64) // 4096
     assert np.all(np.diff(blk) >= 0)
     same = np.diff(blk) == 0
-    assert np.all(np.diff(deg[perm].astype(np.int64))[same] <= 0)
+    assert np.all(np.diff(deg[multi].astype(np.int64))[same] <= 0)
     assert np.all(light[perm]) and np.unique(perm).size == perm.size
 
 

@@ -128,8 +128,9 @@ def _expected_pieces(g, heavy, chunk, parts):
 @pytest.mark.parametrize("parts", [1, 8, 16])
 def test_schedule_lists_heavy_rows(parts):
     n = 3000
-    # hub 1234 has more than GCN_FIX_BIG_PIECES pieces of 64 entries
-    src, dst = hub_graph(n, 9000, [(5, 400), (17, 120), (2999, 1000), (1234, 4000)], seed=3)
+    # hub 1234 has more than GCN_FIX_BIG_PIECES pieces of 64 entries; about
+    # 2 % of the vertices are isolated
+    src, dst = hub_graph(n, 3000, [(5, 400), (17, 120), (2999, 1000), (1234, 4000)], seed=3)
     g = O.graph(n, src, dst)
     dg = DeviceGraph(n, src, dst, prec=G.GCN_F16, heavy_threshold=32, chunk_nnz=64, col_parts=parts)
     a = dg.adj
@@ -157,6 +158,9 @@ def test_schedule_lists_heavy_rows(parts):
     assert a.n_light == light.size
     assert np.array_equal(np.sort(perm), light)
     assert np.all(np.diff(g.deg[perm]) <= 0)
+    # the rows of one entry (isolated vertices) are the last n_light_single
+    assert a.n_light_single == np.count_nonzero(g.deg[light] == 1) > 0
+    assert np.all(g.deg[perm[a.n_light - a.n_light_single:]] == 1)
     # launch order: every piece once, first columns in non-decreasing
     # buckets, the pieces of column range q in chunk_order[part_off[q] ..
     # part_off[q + 1]), and part_slots the most pieces of one XCD
@@ -211,9 +215,9 @@ HUBS = [(1, 600), (2, 150), (3, 70)]
 HUBS_ONE_CHUNK = [(3, 70), (5, 60)]
 
 
-def _layer_case(n, f_in, f_out, seed, hubs=HUBS):
+def _layer_case(n, f_in, f_out, seed, hubs=HUBS, m_random=None):
     rng = np.random.default_rng(seed)
-    src, dst = hub_graph(n, 4 * n, hubs, seed)
+    src, dst = hub_graph(n, 4 * n if m_random is None else m_random, hubs, seed)
     g = O.graph(n, src, dst)
     h = rng.standard_normal((n, f_in)).astype(np.float32)
     w = (rng.standard_normal((f_in, f_out)) / np.sqrt(f_in)).astype(np.float32)
@@ -234,6 +238,8 @@ FWD_CASES = [
     # rows wider than one lane group (2 column blocks in 16-bit, 3 in fp32),
     # a hub of more than GCN_FIX_BIG_PIECES pieces, dropout in the fix-up
     (2000, 24, 600, G.GCN_ACT_RELU, 0.5, "csr_smallpieces"),
+    (3001, 64, 130, G.GCN_ACT_RELU, 0.5, "csr_isolated"),
+    (2003, 40, 7, G.GCN_ACT_NONE, 0.0, "csr_isolated_dinv"),
     (1500, 500, 64, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1500, 64, 32, G.GCN_ACT_NONE, 0.0, "tiled"),
     (1003, 40, 7, G.GCN_ACT_NONE, 0.0, "tiled"),
@@ -251,7 +257,11 @@ FWD_CASES = [
 ]
 
 
-CSR_STORAGES = ("csr", "csr_dinv", "csr_onechunk", "csr_parts", "csr_smallpieces")
+CSR_STORAGES = ("csr", "csr_dinv", "csr_onechunk", "csr_parts", "csr_smallpieces", "csr_isolated",
+                "csr_isolated_dinv")
+# storages whose graph has about half its vertices isolated (one-entry rows
+# for the bundled path, bundles with 1 .. 4 live rows)
+SPARSE_STORAGES = ("csr_isolated", "csr_isolated_dinv")
 
 
 def _graph_for(n, src, dst, prec, storage):
@@ -265,7 +275,8 @@ def _graph_for(n, src, dst, prec, storage):
     parts = {"csr_parts": 16, "csr_smallpieces": 8}.get(storage, 1)
     chunk = 8 if storage == "csr_smallpieces" else 96
     return DeviceGraph(n, src, dst, prec=prec, dense=not csr, tiled=storage == "tiled",
-                       values=storage != "csr_dinv", heavy_threshold=48, chunk_nnz=chunk, col_parts=parts)
+                       values=storage not in ("csr_dinv", "csr_isolated_dinv"), heavy_threshold=48, chunk_nnz=chunk,
+                       col_parts=parts)
 
 
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
@@ -274,7 +285,8 @@ def test_layer_fwd(prec, case):
     n, f_in, f_out, act, p, storage = case
     dense = storage not in CSR_STORAGES
     g, src, dst, h, w, b = _layer_case(n, f_in, f_out, seed=n + f_in,
-                                       hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS)
+                                       hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS,
+                                       m_random=n // 3 if storage in SPARSE_STORAGES else None)
     dg = _graph_for(n, src, dst, prec, storage)
     L = G.GcnLayer(f_in, f_out, round8(f_in), round8(f_out), act, p, 3, 0)
     H, W = to_dev(h, prec), to_dev(w, prec, round8(f_out))
@@ -361,6 +373,7 @@ BWD_CASES = [
     (3000, 64, 7, G.GCN_ACT_RELU, 0.5, "csr_parts"),
     (2100, 130, 40, G.GCN_ACT_RELU, 0.3, "csr_smallpieces"),
     (2000, 40, 600, G.GCN_ACT_RELU, 0.5, "csr"),
+    (3001, 130, 40, G.GCN_ACT_RELU, 0.3, "csr_isolated"),
     (1500, 64, 32, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "tiled"),
     (1003, 130, 7, G.GCN_ACT_RELU, 0.5, "dense"),
@@ -377,7 +390,8 @@ def test_layer_bwd(prec, case):
     n, f_in, f_out, act_below, p, storage = case
     dense = storage not in CSR_STORAGES
     g, src, dst, h, w, _ = _layer_case(n, f_in, f_out, seed=7 * n + f_out,
-                                       hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS)
+                                       hubs=HUBS_ONE_CHUNK if storage == "csr_onechunk" else HUBS,
+                                       m_random=n // 3 if storage in SPARSE_STORAGES else None)
     rng = np.random.default_rng(n)
     if act_below == G.GCN_ACT_RELU:   # H as produced by ReLU + dropout: exact zeros
         h = np.where(rng.random(h.shape) < 0.5, 0.0, np.abs(h) * 2).astype(np.float32)
