@@ -445,7 +445,7 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "aggregation_rmat21_sbm16k_traf
 # sources of the kernels whose counters are reported (with the shared
 # device helpers they include)
 DENSE_SOURCES = ("dense_agg.hip", "xpose.h", "common.h")
-SPMM_SOURCES = ("spmm.hip", "normalize.hip", "common.h")
+SPMM_SOURCES = ("spmm_impl.h", "spmm_f16.hip", "spmm.hip", "normalize.hip", "common.h")
 
 
 def kernel_hash(*files):
@@ -636,7 +636,8 @@ def aggregation_roofline(spec, r, prec):
     else:
         s_p = 8 if spec.index64 else 4
         per_epoch_bytes = spmm_bytes(n, r["nnz"], r["f_h"], s, s_p) + spmm_bytes(n, r["nnz"], r["C"], s, s_p)
-        kname = "CSR aggregation: spmm_rows_kernel + heavy-row chunk/fixup kernels"
+        kname = ("CSR aggregation: spmm_main_kernel (heavy-row pieces, light rows, one-entry rows in bundles) "
+                 "+ spmm_fixup_kernel")
         traffic = load_traffic("spmm_f16", *SPMM_SOURCES) if prec == 1 and spec.name == "rmat21" else None
     n_epochs_timed = r["agg_launches"] // 2
     achieved = per_epoch_bytes * n_epochs_timed / (r["agg_ms"] * 1e-3) / 1e9

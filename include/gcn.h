@@ -270,10 +270,10 @@ gcn_status gcn_schedule(gcn_adj* A, int64_t heavy_threshold, int64_t chunk_nnz, 
  *   Z     = A_hat S + bias                    (bias fp32 [f_out], may be NULL)
  *   H_out = dropout(ReLU(Z)) if act == RELU, else Z     (n x f_out, ld_out)
  * Inverted dropout (training != 0, dropout_p > 0): element (i, j) with
- * e = i * f_out + j is kept iff word (e % 8) of Philox-4x64-10 with key
- * (seed, layer_id) and counter (e / 8, epoch, 0, 0) -- word 2t is the low
- * and 2t + 1 the high half of output t -- is >= floor(p * 2^32); kept
- * values are multiplied by 1 / (1 - p) in fp32.
+ * e = i * f_out + j is kept iff output word (e % 4) of Philox-4x32-10 with
+ * counter (b mod 2^32, b / 2^32, epoch mod 2^32, layer_id), b = e / 4, and
+ * key (seed mod 2^32, seed / 2^32) is >= floor(p * 2^32); kept values are
+ * multiplied by 1 / (1 - p) in fp32.
  * S is caller scratch that the backward pass does not need.  workspace: at
  * least gcn_layer_workspace_size() bytes.  *overflow is set to 1 if any
  * stored element of H_out is not finite.

@@ -29,8 +29,10 @@ leaves open:
   (the casts of the O1 cast policy and of every 16-bit tensor).
 * adam_step_half(): the O3 level, Adam with parameters and moments held in
   16 bits and no loss scale, each elementwise operation rounded.
-* philox4x64(): the counter-based generator (Salmon et al., SC'11) that
-  draws the dropout keep decisions and the decoder's pairs.
+* philox4x32(), philox4x64(): the counter-based generators (Salmon et al.,
+  SC'11) that draw the dropout keep decisions (4x32, the generator behind
+  PyTorch's GPU dropout, the framework the paper trains with) and the
+  decoder's pairs (4x64).
 * Link prediction (Section "Graph Auto-Encoders", Eq. (2): the decoder
   sigma(Z Z^T) read on sampled vertex pairs): sample_pairs() draws an
   epoch's positive and negative pairs, pair_loss() scores them by inner
@@ -49,7 +51,7 @@ import numpy as np
 
 __all__ = [
     "Graph", "graph", "norm_values", "dinv_f32", "dense_adj", "transpose_csr",
-    "spmm", "philox4x64", "dropout_keep", "layer_fwd", "softmax_ce",
+    "spmm", "philox4x32", "philox4x64", "dropout_words", "dropout_keep", "layer_fwd", "softmax_ce",
     "graph_degrees", "graph_rows", "dropout_keep_rows", "norm_adj_matvec",
     "layer_bwd", "adam_step", "LossScaler", "AdamState",
     "PAIR_STREAM", "sample_pairs", "pair_loss", "pair_backward", "auc_ap",
@@ -225,8 +227,9 @@ def spmm(g: Graph, values, x, block_entries=1 << 22):
 
 
 # ---------------------------------------------------------------------------
-# Counter-based RNG for dropout: Philox-4x64-10 (Salmon, Moraes, Dror, Shaw,
-# "Parallel random numbers: as easy as 1, 2, 3", SC'11)
+# Counter-based RNGs: Philox-4x64-10 (the decoder's pairs) and Philox-4x32-10
+# (dropout) (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as
+# 1, 2, 3", SC'11)
 # ---------------------------------------------------------------------------
 
 _M64 = (1 << 64) - 1
@@ -278,28 +281,66 @@ def philox4x64(ctr, key, rounds=10):
         return np.stack([x0, x1, x2, x3], axis=-1)
 
 
+_P32_M0 = 0xD2511F53
+_P32_M1 = 0xCD9E8D57
+_P32_W0 = 0x9E3779B9
+_P32_W1 = 0xBB67AE85
+
+
+def philox4x32(ctr, key, rounds=10):
+    """Philox-4x32 with ``rounds`` rounds.  ctr: array [..., 4] of 32-bit
+    words, key: [..., 2] (any integer dtype; values taken mod 2^32).  Returns
+    uint64 [..., 4] holding the four 32-bit output words.
+
+    Each round forms the 64-bit products M0*x0 and M1*x2 (exact in uint64),
+    the new state (hi(M1*x2) ^ x1 ^ k0, lo(M1*x2), hi(M0*x0) ^ x3 ^ k1,
+    lo(M0*x0)), and bumps the key by the two Weyl constants mod 2^32 between
+    rounds."""
+    mask = np.uint64(0xFFFFFFFF)
+    s32 = np.uint64(32)
+    c = np.array(ctr, dtype=np.uint64, copy=True) & mask
+    k = np.array(key, dtype=np.uint64, copy=True) & mask
+    x0, x1, x2, x3 = c[..., 0], c[..., 1], c[..., 2], c[..., 3]
+    k0, k1 = k[..., 0], k[..., 1]
+    for r in range(rounds):
+        p0 = x0 * np.uint64(_P32_M0)
+        p1 = x2 * np.uint64(_P32_M1)
+        x0, x1, x2, x3 = (p1 >> s32) ^ x1 ^ k0, p1 & mask, (p0 >> s32) ^ x3 ^ k1, p0 & mask
+        if r + 1 < rounds:
+            k0 = (k0 + np.uint64(_P32_W0)) & mask
+            k1 = (k1 + np.uint64(_P32_W1)) & mask
+    return np.stack([x0, x1, x2, x3], axis=-1)
+
+
+def dropout_words(seed, layer_id, epoch, e):
+    """The 32-bit dropout word of each element linear index e (uint64 array):
+    word e % 4 of the Philox-4x32-10 block with counter (b mod 2^32,
+    b div 2^32, epoch mod 2^32, layer_id), b = e div 4, and key
+    (seed mod 2^32, seed div 2^32 mod 2^32)."""
+    e = np.asarray(e, np.uint64)
+    b = e >> np.uint64(2)
+    mask = np.uint64(0xFFFFFFFF)
+    ctr = np.empty(e.shape + (4,), np.uint64)
+    ctr[..., 0] = b & mask
+    ctr[..., 1] = b >> np.uint64(32)
+    ctr[..., 2] = np.uint64(int(epoch) & 0xFFFFFFFF)
+    ctr[..., 3] = np.uint64(int(layer_id) & 0xFFFFFFFF)
+    key = np.empty(e.shape + (2,), np.uint64)
+    key[..., 0] = np.uint64(int(seed) & 0xFFFFFFFF)
+    key[..., 1] = np.uint64((int(seed) >> 32) & 0xFFFFFFFF)
+    out = philox4x32(ctr, key)
+    w = (e & np.uint64(3)).astype(np.int64)
+    return np.take_along_axis(out, w[..., None], axis=-1)[..., 0]
+
+
 def dropout_keep(seed, layer_id, epoch, n, f, p):
     """Keep mask (bool n x f) of inverted dropout with drop probability p.
 
-    Element (i, j) has linear index e = i*f + j over the logical width f.
-    One Philox-4x64-10 block with key (seed, layer_id) and counter
-    (e // 8, epoch, 0, 0) yields 8 32-bit words (word 2t is the low half of
-    output t, word 2t+1 the high half); element e takes word e % 8 and is
-    kept iff word >= floor(p * 2^32)."""
-    blocks = np.arange((n * f + 7) // 8, dtype=np.uint64)
-    ctr = np.zeros((blocks.size, 4), np.uint64)
-    ctr[:, 0] = blocks
-    ctr[:, 1] = np.uint64(epoch)
-    key = np.zeros((blocks.size, 2), np.uint64)
-    key[:, 0] = np.uint64(seed & _M64)
-    key[:, 1] = np.uint64(layer_id)
-    out = philox4x64(ctr, key)                               # [blocks, 4]
-    words = np.empty((blocks.size, 8), np.uint64)
-    words[:, 0::2] = out & np.uint64(0xFFFFFFFF)
-    words[:, 1::2] = out >> np.uint64(32)
-    w = words.reshape(-1)[: n * f]
+    Element (i, j) has linear index e = i*f + j over the logical width f and
+    is kept iff its word (dropout_words) >= floor(p * 2^32)."""
+    e = np.arange(n * f, dtype=np.uint64)
     thr = np.uint64(int(np.floor(p * 4294967296.0)))
-    return (w >= thr).reshape(n, f)
+    return (dropout_words(seed, layer_id, epoch, e) >= thr).reshape(n, f)
 
 
 def dropout_keep_rows(seed, layer_id, epoch, rows, f, p):
@@ -307,19 +348,8 @@ def dropout_keep_rows(seed, layer_id, epoch, rows, f, p):
     e = i*f + j over the logical width f)."""
     rows = np.asarray(rows, np.int64)
     e = (rows[:, None] * f + np.arange(f, dtype=np.int64)[None, :]).astype(np.uint64)
-    blocks = e >> np.uint64(3)
-    ctr = np.zeros(blocks.shape + (4,), np.uint64)
-    ctr[..., 0] = blocks
-    ctr[..., 1] = np.uint64(epoch)
-    key = np.zeros(blocks.shape + (2,), np.uint64)
-    key[..., 0] = np.uint64(seed & _M64)
-    key[..., 1] = np.uint64(layer_id)
-    out = philox4x64(ctr, key)
-    w = (e & np.uint64(7)).astype(np.int64)
-    word64 = np.take_along_axis(out, (w // 2)[..., None], axis=-1)[..., 0]
-    word = np.where(w % 2 == 0, word64 & np.uint64(0xFFFFFFFF), word64 >> np.uint64(32))
     thr = np.uint64(int(np.floor(p * 4294967296.0)))
-    return word >= thr
+    return dropout_words(seed, layer_id, epoch, e) >= thr
 
 
 # ---------------------------------------------------------------------------

@@ -147,10 +147,45 @@ __device__ __forceinline__ uint64_t dropout_epoch(const Epilogue& ep) {
   return ep.epoch + (uint64_t)(uint32_t)ep.epoch_ctr[0] + (uint64_t)(uint32_t)ep.epoch_ctr[1];
 }
 
-// Keep decision for element linear index e = row * cols + col.
+// Philox-4x32-10 (same paper): ten rounds of two 32x32->64-bit multiplies
+// (one v_mad_u64_u32 each), the key bumped by two Weyl constants between
+// rounds.  The dropout stream: four words per block, about half the
+// arithmetic per word of the 4x64 variant.
+struct Philox4 { uint32_t w[4]; };
+
+__device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                                 uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)c0 * 0xD2511F53u, p1 = (uint64_t)c2 * 0xCD9E8D57u;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0, n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  Philox4 o;
+  o.w[0] = c0; o.w[1] = c1; o.w[2] = c2; o.w[3] = c3;
+  return o;
+}
+
+// Dropout block b (elements 4b .. 4b + 3): counter (b mod 2^32, b div 2^32,
+// epoch mod 2^32, layer), key (seed mod 2^32, seed div 2^32).
+__device__ __forceinline__ Philox4 dropout_block(const Epilogue& ep, uint64_t b) {
+  return philox4x32_10((uint32_t)b, (uint32_t)(b >> 32), (uint32_t)dropout_epoch(ep), (uint32_t)ep.layer,
+                       (uint32_t)ep.seed, (uint32_t)(ep.seed >> 32));
+}
+
+__device__ __forceinline__ uint32_t philox4_word(const Philox4& o, uint32_t w) {
+  return w == 0 ? o.w[0] : w == 1 ? o.w[1] : w == 2 ? o.w[2] : o.w[3];
+}
+
+// Keep decision for element linear index e = row * cols + col: word e mod 4
+// of block e div 4 at or above floor(p 2^32).
 __device__ __forceinline__ bool dropout_keep(const Epilogue& ep, uint64_t e) {
-  Philox8 o = philox4x64_10(e >> 3, dropout_epoch(ep), 0, 0, ep.seed, ep.layer);
-  return philox_word(o, (uint32_t)(e & 7)) >= ep.thr;
+  return philox4_word(dropout_block(ep, e >> 2), (uint32_t)(e & 3)) >= ep.thr;
 }
 
 // Called by the lanes that saw a non-finite value: the lowest of them
@@ -222,24 +257,30 @@ __device__ __forceinline__ void epi_store_vec_b(const Epilogue& ep, int64_t row,
 #pragma unroll
       for (int i = 0; i < VE; ++i) acc[i] = acc[i] > 0.f ? acc[i] : 0.f;
       if (ep.dropout) {
-        // the VE <= 8 elements span one Philox block, or two when the vector
-        // crosses a multiple of 8; the second block is drawn only then (one
-        // draw in the code per call site instead of one per element)
+        // the VE elements from e0 = row * cols + col0: VE / 4 whole blocks
+        // when e0 is a multiple of 4 (cols a multiple of 4), else up to
+        // VE / 4 + 1 blocks, each element taking its word
         const uint64_t e0 = (uint64_t)row * (uint64_t)cols + (uint64_t)col0;
-        const uint64_t b0 = e0 >> 3, b1 = (e0 + VE - 1) >> 3;
-        {
-          const Philox8 o = philox4x64_10(b0, dropout_epoch(ep), 0, 0, ep.seed, ep.layer);
+        if ((e0 & 3) == 0) {
 #pragma unroll
-          for (int i = 0; i < VE; ++i)
-            if (((e0 + i) >> 3) == b0)
-              acc[i] = philox_word(o, (uint32_t)((e0 + i) & 7)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
-        }
-        if (b1 != b0) {
-          const Philox8 o = philox4x64_10(b1, dropout_epoch(ep), 0, 0, ep.seed, ep.layer);
+          for (int j = 0; j < VE / 4; ++j) {
+            const Philox4 o = dropout_block(ep, (e0 >> 2) + j);
 #pragma unroll
-          for (int i = 0; i < VE; ++i)
-            if (((e0 + i) >> 3) != b0)
-              acc[i] = philox_word(o, (uint32_t)((e0 + i) & 7)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
+            for (int q = 0; q < 4; ++q)
+              acc[4 * j + q] = o.w[q] >= ep.thr ? acc[4 * j + q] * ep.keep_scale : 0.f;
+          }
+        } else {
+          const uint64_t b0 = e0 >> 2, bl = (e0 + VE - 1) >> 2;
+#pragma unroll
+          for (int j = 0; j <= VE / 4; ++j) {
+            if (b0 + j <= bl) {
+              const Philox4 o = dropout_block(ep, b0 + j);
+#pragma unroll
+              for (int i = 0; i < VE; ++i)
+                if (((e0 + i) >> 2) == b0 + j)
+                  acc[i] = philox4_word(o, (uint32_t)((e0 + i) & 3)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
+            }
+          }
         }
       }
     }

@@ -326,16 +326,7 @@ def test_dropout_threshold_uses_binary32_p():
     exactly where an element is dropped."""
     n, f, seed, layer, epoch = 64, 8, 987654321, 2, 11
     e_all = np.arange(n * f, dtype=np.uint64)
-    ctr = np.zeros((n * f // 8, 4), np.uint64)
-    ctr[:, 0] = np.arange(n * f // 8, dtype=np.uint64)
-    ctr[:, 1] = epoch
-    key = np.zeros((n * f // 8, 2), np.uint64)
-    key[:, 0], key[:, 1] = seed, layer
-    out = O.philox4x64(ctr, key)
-    words = np.empty((n * f // 8, 8), np.uint64)
-    words[:, 0::2] = out & np.uint64(0xFFFFFFFF)
-    words[:, 1::2] = out >> np.uint64(32)
-    words = words.reshape(-1)
+    words = O.dropout_words(seed, layer, epoch, e_all)
     # binary32 spacing in [1/4, 1/2) is 2^-25, i.e. 128 threshold units
     cand = [int(e) for e in e_all if 2**30 <= int(words[e]) < 2**31 and int(words[e]) % 128 >= 70]
     assert cand, "no suitable element for this seed"

@@ -218,16 +218,47 @@ def test_dropout_p0_keeps_all_and_fraction():
     assert (keep != O.dropout_keep(124, 1, 3, 500, 40, 0.5)).mean() > 0.4
 
 
+def test_philox4x32_known_answers():
+    # the generator's published known-answer vectors (tests/golden)
+    path = os.path.join(os.path.dirname(__file__), "golden", "philox4x32_10_kat.txt")
+    rows = [ln.split() for ln in open(path) if ln.strip() and not ln.startswith("#")]
+    assert len(rows) == 3
+    for r in rows:
+        v = [int(x, 16) for x in r]
+        got = O.philox4x32(np.array([v[0:4]], np.uint64), np.array([v[4:6]], np.uint64))[0]
+        assert [int(x) for x in got] == v[6:10]
+
+
+def test_philox4x32_rounds_and_key_schedule():
+    # brute force with Python integers of one round structure, independent of
+    # numpy's uint64 arithmetic: 7 rounds at a random counter and key
+    M0, M1, W0, W1 = 0xD2511F53, 0xCD9E8D57, 0x9E3779B9, 0xBB67AE85
+    c = [0x01234567, 0x89ABCDEF, 0xDEADBEEF, 0x0BADF00D]
+    k = [0xCAFEBABE, 0x12345678]
+    x, kk = list(c), list(k)
+    for r in range(7):
+        p0, p1 = M0 * x[0], M1 * x[2]
+        x = [(p1 >> 32) ^ x[1] ^ kk[0], p1 & 0xFFFFFFFF, (p0 >> 32) ^ x[3] ^ kk[1], p0 & 0xFFFFFFFF]
+        kk = [(kk[0] + W0) & 0xFFFFFFFF, (kk[1] + W1) & 0xFFFFFFFF]
+    got = O.philox4x32(np.array([c], np.uint64), np.array([k], np.uint64), rounds=7)[0]
+    assert [int(v) for v in got] == x
+
+
 def test_dropout_word_layout():
-    # element e uses word e % 8 of block e // 8: check one block by hand
-    seed, layer, epoch = 99, 2, 5
-    out = O.philox4x64(np.array([[3, epoch, 0, 0]], np.uint64), np.array([[seed, layer]], np.uint64))[0]
-    words = []
-    for x in out:
-        words += [int(x) & 0xFFFFFFFF, int(x) >> 32]
+    # element e uses word e % 4 of block e // 4, counter (b lo, b hi, epoch,
+    # layer), key (seed lo, seed hi): check two blocks by hand
+    seed, layer, epoch = (7 << 32) + 99, 2, 5
     thr = int(math.floor(0.5 * 2**32))
-    keep = O.dropout_keep(seed, layer, epoch, 4, 8, 0.5)  # 32 elements, block 3 = row 3
+    keep = O.dropout_keep(seed, layer, epoch, 4, 8, 0.5)  # 32 elements, blocks 6, 7 = row 3
+    words = []
+    for b in (6, 7):
+        out = O.philox4x32(np.array([[b, 0, epoch, layer]], np.uint64), np.array([[99, 7]], np.uint64))[0]
+        words += [int(x) for x in out]
     assert [bool(w >= thr) for w in words] == keep[3].tolist()
+    # a block index past 2^32 carries into counter word 1
+    e = np.array([(2**32 + 5) * 4 + 1], np.uint64)
+    out = O.philox4x32(np.array([[5, 1, epoch, layer]], np.uint64), np.array([[99, 7]], np.uint64))[0]
+    assert int(O.dropout_words(seed, layer, epoch, e)[0]) == int(out[1])
 
 
 def test_dropout_scales_kept_by_two():
