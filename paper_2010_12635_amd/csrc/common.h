@@ -239,12 +239,46 @@ __device__ __forceinline__ void epi_load_bias(const Epilogue& ep, int64_t col0, 
   for (int i = 0; i < VE; ++i) bv[i] = ep.bias[col0 + i < ep.cols ? col0 + i : 0];
 }
 
+// Keep bits of the VE elements from e0 = row * cols + col0 (bit i: element
+// e0 + i kept): VE / 4 whole blocks when e0 is a multiple of 4 (cols a
+// multiple of 4), else up to VE / 4 + 1 blocks, each element taking its word.
+template <int VE>
+__device__ __forceinline__ uint32_t dropout_bits(const Epilogue& ep, int64_t row, int64_t col0) {
+  const uint64_t e0 = (uint64_t)row * (uint64_t)ep.cols + (uint64_t)col0;
+  uint32_t bits = 0;
+  if ((e0 & 3) == 0) {
+#pragma unroll
+    for (int j = 0; j < VE / 4; ++j) {
+      const Philox4 o = dropout_block(ep, (e0 >> 2) + j);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) bits |= (o.w[q] >= ep.thr ? 1u : 0u) << (4 * j + q);
+    }
+  } else {
+    const uint64_t b0 = e0 >> 2, bl = (e0 + VE - 1) >> 2;
+#pragma unroll
+    for (int j = 0; j <= VE / 4; ++j) {
+      if (b0 + j <= bl) {
+        const Philox4 o = dropout_block(ep, b0 + j);
+#pragma unroll
+        for (int i = 0; i < VE; ++i)
+          if (((e0 + i) >> 2) == b0 + j) bits |= (philox4_word(o, (uint32_t)((e0 + i) & 3)) >= ep.thr ? 1u : 0u) << i;
+      }
+    }
+  }
+  return bits;
+}
+
+// Whether an epilogue draws dropout decisions (a caller may draw them with
+// dropout_bits ahead of time, while its loads are in flight).
+__device__ __forceinline__ bool epi_draws(const Epilogue& ep) { return ep.mode == EPI_AGG && ep.relu && ep.dropout; }
+
 // Vector epilogue: Vec<T>::N consecutive columns starting at col0 (col0 is a
 // multiple of the vector width, col0 < cols).  Columns >= cols are written 0.
-// bv holds the bias of these columns (epi_load_bias).
+// bv holds the bias of these columns (epi_load_bias); keep, when >= 0, the
+// dropout_bits of these columns drawn earlier.
 template <typename T>
 __device__ __forceinline__ void epi_store_vec_b(const Epilogue& ep, int64_t row, int64_t col0, float* acc,
-                                                const float (&bv)[Vec<T>::N]) {
+                                                const float (&bv)[Vec<T>::N], int32_t keep = -1) {
   constexpr int VE = Vec<T>::N;
   const int64_t cols = ep.cols;
   if (ep.mode == EPI_AGG) {
@@ -257,31 +291,9 @@ __device__ __forceinline__ void epi_store_vec_b(const Epilogue& ep, int64_t row,
 #pragma unroll
       for (int i = 0; i < VE; ++i) acc[i] = acc[i] > 0.f ? acc[i] : 0.f;
       if (ep.dropout) {
-        // the VE elements from e0 = row * cols + col0: VE / 4 whole blocks
-        // when e0 is a multiple of 4 (cols a multiple of 4), else up to
-        // VE / 4 + 1 blocks, each element taking its word
-        const uint64_t e0 = (uint64_t)row * (uint64_t)cols + (uint64_t)col0;
-        if ((e0 & 3) == 0) {
+        const uint32_t kb = keep >= 0 ? (uint32_t)keep : dropout_bits<VE>(ep, row, col0);
 #pragma unroll
-          for (int j = 0; j < VE / 4; ++j) {
-            const Philox4 o = dropout_block(ep, (e0 >> 2) + j);
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              acc[4 * j + q] = o.w[q] >= ep.thr ? acc[4 * j + q] * ep.keep_scale : 0.f;
-          }
-        } else {
-          const uint64_t b0 = e0 >> 2, bl = (e0 + VE - 1) >> 2;
-#pragma unroll
-          for (int j = 0; j <= VE / 4; ++j) {
-            if (b0 + j <= bl) {
-              const Philox4 o = dropout_block(ep, b0 + j);
-#pragma unroll
-              for (int i = 0; i < VE; ++i)
-                if (((e0 + i) >> 2) == b0 + j)
-                  acc[i] = philox4_word(o, (uint32_t)((e0 + i) & 3)) >= ep.thr ? acc[i] * ep.keep_scale : 0.f;
-            }
-          }
-        }
+        for (int i = 0; i < VE; ++i) acc[i] = (kb >> i) & 1u ? acc[i] * ep.keep_scale : 0.f;
       }
     }
   }
@@ -300,10 +312,11 @@ __device__ __forceinline__ void epi_store_vec_b(const Epilogue& ep, int64_t row,
 
 // The same, loading the bias of these columns itself.
 template <typename T>
-__device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, int64_t col0, float* acc) {
+__device__ __forceinline__ void epi_store_vec(const Epilogue& ep, int64_t row, int64_t col0, float* acc,
+                                              int32_t keep = -1) {
   float bv[Vec<T>::N];
   epi_load_bias<T>(ep, col0, bv);
-  epi_store_vec_b<T>(ep, row, col0, acc, bv);
+  epi_store_vec_b<T>(ep, row, col0, acc, bv, keep);
 }
 
 }  // namespace gcn

@@ -168,6 +168,11 @@ __device__ __forceinline__ void single_bundle(const SpmmParams<IdxT>& p, const T
     if (HAS_VAL) v[k] = to_f32<T>(reinterpret_cast<const T*>(p.values)[beg[k]]);
     else drow[k] = p.dinv[row[k]];
   }
+  // dropout decisions drawn while the index loads are out
+  int32_t keep[B];
+  const bool draws = epi_draws(p.epi);
+#pragma unroll
+  for (int k = 0; k < B; ++k) keep[k] = draws ? (int32_t)dropout_bits<VE>(p.epi, row[k], col0) : -1;
 #pragma unroll
   for (int k = 0; k < B; ++k) x[k] = ldg16(X + (int64_t)c[k] * p.ldx);
   if (!HAS_VAL) {
@@ -181,7 +186,7 @@ __device__ __forceinline__ void single_bundle(const SpmmParams<IdxT>& p, const T
 #pragma unroll
       for (int i = 0; i < VE; ++i) acc[i] = 0.f;
       fma_vec<T>(acc, v[k], x[k]);
-      epi_store_vec<T>(p.epi, row[k], col0, acc);
+      epi_store_vec<T>(p.epi, row[k], col0, acc, keep[k]);
     }
   }
 }
@@ -215,11 +220,13 @@ __device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, int64_
       const int64_t nslot = slot + stride;
       if (nslot < n_multi) d = ldg16(p.row_desc + nslot);
       const float drow = HAS_VAL ? 0.f : p.dinv[row];
+      // the row's dropout decisions are drawn while its first loads are out
+      const int32_t keep = epi_draws(p.epi) ? (int32_t)dropout_bits<VE>(p.epi, row, col0) : -1;
       float acc[VE];
 #pragma unroll
       for (int i = 0; i < VE; ++i) acc[i] = 0.f;
       row_sum<T, LPR, HAS_VAL>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, beg, end);
-      epi_store_vec<T>(p.epi, row, col0, acc);
+      epi_store_vec<T>(p.epi, row, col0, acc, keep);
       slot = nslot;
     }
     for (; slot < units; slot += stride) {
