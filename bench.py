@@ -768,11 +768,9 @@ def main():
         return
 
     if args.summarize_counters:
-        flags = ("--steps 3 --warmup 1 --no-fp32 --cpu-epochs 0 --dense-steps 5 --seeds 1 --no-levels --ba-epochs 0 "
-                 "--tiny-epochs 0 --gae-epochs 0 --table1 none --no-largest --copy-calibration 256")
-        cmd = (f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py {flags}\n"
-               f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py {flags}")
-        print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, cmd)))
+        if not args.stats_command:
+            sys.exit("--summarize-counters needs --stats-command (the two commands that produced the counters)")
+        print(json.dumps(summarize_counters(*args.summarize_counters, TRAFFIC_SUMMARY, args.stats_command)))
         return
 
     if args.gpus != 1:
