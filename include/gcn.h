@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define GCN_ABI_VERSION 10
+#define GCN_ABI_VERSION 11
 
 typedef enum gcn_status {
   GCN_OK = 0,
@@ -321,9 +321,15 @@ gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* 
  *   dZ_below = (G_S W^T) * [H > 0] / (1 - p_below)   if act_below == RELU
  *            =  G_S W^T                               if act_below == NONE
  *              (n x f_in, ld_in, prec; NULL skips it, e.g. for the first layer)
+ *   dbias_below = column sums of dZ_below as stored (ld_in fp32, cols >=
+ *              f_in set to 0; may be NULL, needs dZ_below): the bias
+ *              gradient of the layer below, which its own gcn_layer_bwd call
+ *              then need not compute (pass dbias = NULL there); summed by
+ *              the workgroups that write dZ_below, without a pass of its own
  * The ReLU derivative at 0 is 0.  *overflow is set to 1 if any stored
- * element of GS, dW, dbias or dZ_below is not finite.  dW and dbias are
- * summed in a fixed order (run-to-run deterministic).
+ * element of GS, dW, dbias, dZ_below or dbias_below is not finite.  dW,
+ * dbias and dbias_below are summed in a fixed order (run-to-run
+ * deterministic).
  * With L->identity_input, dW = I^T G_S = G_S widened to fp32 (exactly what
  * the product with I gives); dZ_below must be NULL (GCN_ERR_INVALID_ARG
  * otherwise: there is nothing below an input layer).
@@ -331,7 +337,7 @@ gcn_status gcn_aggregate(const gcn_adj* A, int64_t F, int32_t prec, const void* 
 gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec,
                          const void* H, const void* W, const void* dZ,
                          int32_t act_below, float p_below,
-                         float* dW, float* dbias, void* dZ_below, void* GS,
+                         float* dW, float* dbias, void* dZ_below, float* dbias_below, void* GS,
                          int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
@@ -352,7 +358,7 @@ gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec,
 gcn_status gcn_layer_bwd_noalloc(const gcn_adj* A, const gcn_layer* L, int32_t prec,
                                  const void* H, const void* W, const void* dZ,
                                  int32_t act_below, float p_below,
-                                 float* dW, float* dbias, void* dZ_below, void* GS,
+                                 float* dW, float* dbias, void* dZ_below, float* dbias_below, void* GS,
                                  int32_t* overflow, void* stream);
 
 /* ---------------------------------------------------------------------------

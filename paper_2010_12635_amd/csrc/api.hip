@@ -1,6 +1,7 @@
 // C ABI of libgcn: argument validation on the host, then the kernel
 // sequence of each call on the caller's stream.  Nothing here allocates
 // device memory; scratch comes from the caller's workspace.
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <mutex>
@@ -122,6 +123,7 @@ struct LayerPlan {
   int dw_split;      // dW = H^T G_S
   int dh_split;      // dZ_below = G_S W^T
   int64_t cs_floats; // column-sum partial region (multiple of 64 floats)
+  int64_t cb_floats; // column-sum partials of dZ_below (multiple of 64 floats)
   int64_t floats;    // total
 };
 
@@ -147,7 +149,11 @@ LayerPlan plan_layer(const gcn_adj* A, const gcn_layer* L, int32_t prec) {
     cs = colsum_partials_floats(n, L->ld_out);
   }
   p.cs_floats = (cs + 63) / 64 * 64;
-  p.floats = p.cs_floats + f;
+  // column sums of dZ_below: one row per product workgroup, or the
+  // column-sum pass over dZ_below where the generic GEMM computes it
+  const int64_t cb = std::max<int64_t>((int64_t)tsgemm_colsum_rows_max() * L->f_in, colsum_partials_floats(n, L->ld_in));
+  p.cb_floats = ident ? 0 : (cb + 63) / 64 * 64;
+  p.floats = p.cs_floats + p.cb_floats + f;
   return p;
 }
 
@@ -462,7 +468,7 @@ namespace {
 // Argument checks of gcn_layer_bwd that do not concern the workspace.
 gcn_status layer_bwd_check(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
                            const void* dZ, int32_t act_below, float p_below, const float* dW, const float* dbias,
-                           const void* dZ_below, const void* GS) {
+                           const void* dZ_below, const float* dbias_below, const void* GS) {
   if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
   gcn_status st = check_adj(A, prec);
   if (st != GCN_OK) return st;
@@ -471,11 +477,12 @@ gcn_status layer_bwd_check(const gcn_adj* A, const gcn_layer* L, int32_t prec, c
   const bool ident = L->identity_input != 0;
   if (ident && L->f_in != A->n) return GCN_ERR_SHAPE;
   if (ident && dZ_below) return GCN_ERR_INVALID_ARG;
+  if (dbias_below && !dZ_below) return GCN_ERR_INVALID_ARG;
   if ((!ident && !H) || !W || !dZ || !dW || !GS) return GCN_ERR_INVALID_ARG;
   if (act_below != GCN_ACT_NONE && act_below != GCN_ACT_RELU) return GCN_ERR_INVALID_ARG;
   if (!(p_below >= 0.f && p_below < 1.f)) return GCN_ERR_INVALID_ARG;
   if ((H && !aligned16(H)) || !aligned16(W) || !aligned16(dZ) || !aligned16(dW) || !aligned16(GS) ||
-      (dZ_below && !aligned16(dZ_below)) || (dbias && !aligned16(dbias)))
+      (dZ_below && !aligned16(dZ_below)) || (dbias && !aligned16(dbias)) || (dbias_below && !aligned16(dbias_below)))
     return GCN_ERR_ALIGNMENT;
   return GCN_OK;
 }
@@ -487,11 +494,12 @@ gcn_status layer_bwd_check(const gcn_adj* A, const gcn_layer* L, int32_t prec, c
 // cleared between calls.
 gcn_status layer_bwd_run(const gcn_adj* A, const gcn_layer* L, int32_t prec, const LayerPlan& plan,
                          const void* H, const void* W, const void* dZ, int32_t act_below, float p_below, float* dW,
-                         float* dbias, void* dZ_below, void* GS, int32_t* overflow, float* workspace,
-                         hipStream_t s) {
+                         float* dbias, void* dZ_below, float* dbias_below, void* GS, int32_t* overflow,
+                         float* workspace, hipStream_t s) {
   const bool ident = L->identity_input != 0;
   float* cs = workspace;                           // column-sum partials of dZ
-  float* ws = cs + plan.cs_floats;                 // per-step scratch
+  float* cb = cs + plan.cs_floats;                 // column-sum partials of dZ_below
+  float* ws = cb + plan.cb_floats;                 // per-step scratch
   const int64_t n = A->n;
   const bool dense = A->format != GCN_CSR;
 
@@ -530,7 +538,28 @@ gcn_status layer_bwd_run(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
     ed.keep_scale = 1.f / (1.f - p_below);
     ed.hmask = H;
     ed.ldh = L->ld_in;
-    GCN_HIP(row_product(prec, GS, L->ld_out, W, L->ld_out, true, n, L->f_in, L->f_out, plan.dh_split, ws, ed, s));
+    if (!dbias_below) {
+      GCN_HIP(row_product(prec, GS, L->ld_out, W, L->ld_out, true, n, L->f_in, L->f_out, plan.dh_split, ws, ed, s));
+    } else {
+      // the bias gradient of the layer below, the column sums of dZ_below:
+      // from the product's own workgroups where the row-streaming kernel
+      // runs, else from a column-sum pass over the stored dZ_below
+      Epilogue eb = base_epi(dbias_below, L->ld_in, 1, L->f_in, EPI_F32, overflow);
+      RedJob jc{};
+      if (use_tsgemm(prec, n, L->f_out)) {
+        int rows = 0;
+        GCN_HIP(tsgemm_launch(prec, GS, L->ld_out, W, L->ld_out, true, n, L->f_in, L->f_out, ed, s, cb, &rows));
+        jc = make_job(cb, rows, 1, L->f_in, eb);
+      } else {
+        GCN_HIP(run_gemm(prec, true, true, GS, L->ld_out, W, L->ld_out, n, L->f_in, L->f_out, plan.dh_split, false,
+                         ws, ed, s));
+        int nb = 0;
+        GCN_HIP(colsum_partial_launch(prec, dZ_below, n, L->f_in, L->ld_in, cb, L->ld_in, &nb, s));
+        eb.cols = L->ld_in;
+        jc = make_job(cb, nb, 1, L->ld_in, eb);
+      }
+      GCN_HIP(reduce_partials2(prec, jc, nullptr, s));
+    }
   }
   return finish(hipSuccess, s);
 }
@@ -540,14 +569,15 @@ gcn_status layer_bwd_run(const gcn_adj* A, const gcn_layer* L, int32_t prec, con
 
 gcn_status gcn_layer_bwd(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
                          const void* dZ, int32_t act_below, float p_below, float* dW, float* dbias, void* dZ_below,
-                         void* GS, int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
+                         float* dbias_below, void* GS, int32_t* overflow, void* workspace, size_t workspace_bytes,
+                         void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  gcn_status st = layer_bwd_check(A, L, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS);
+  gcn_status st = layer_bwd_check(A, L, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, dbias_below, GS);
   if (st != GCN_OK) return st;
   const LayerPlan plan = plan_layer(A, L, prec);
   if (!workspace || workspace_bytes < plan_bytes(plan)) return GCN_ERR_WORKSPACE;
   if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
-  return layer_bwd_run(A, L, prec, plan, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS, overflow,
+  return layer_bwd_run(A, L, prec, plan, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, dbias_below, GS, overflow,
                        static_cast<float*>(workspace), s);
 }
 
@@ -584,16 +614,16 @@ gcn_status scratch_of_current_device(void** out) {
 
 gcn_status gcn_layer_bwd_noalloc(const gcn_adj* A, const gcn_layer* L, int32_t prec, const void* H, const void* W,
                                  const void* dZ, int32_t act_below, float p_below, float* dW, float* dbias,
-                                 void* dZ_below, void* GS, int32_t* overflow, void* stream) {
+                                 void* dZ_below, float* dbias_below, void* GS, int32_t* overflow, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  gcn_status st = layer_bwd_check(A, L, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS);
+  gcn_status st = layer_bwd_check(A, L, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, dbias_below, GS);
   if (st != GCN_OK) return st;
   const LayerPlan plan = plan_layer(A, L, prec);
   if (plan_bytes(plan) > (size_t)GCN_NOALLOC_SCRATCH_BYTES) return GCN_ERR_CAPACITY;
   void* scr = nullptr;
   st = scratch_of_current_device(&scr);
   if (st != GCN_OK) return st;
-  return layer_bwd_run(A, L, prec, plan, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS, overflow,
+  return layer_bwd_run(A, L, prec, plan, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, dbias_below, GS, overflow,
                        static_cast<float*>(scr), s);
 }
 

@@ -102,9 +102,15 @@ hipError_t spmm_launch(const CsrView& A, int prec, const void* X, int64_t ldx, i
 // ------------------------------------------------- tall-skinny products ----
 // C (M x N) = A (M x K, row-major, lda) . B, B(k, n) = b_kc ? B[n * ldb + k]
 // : B[k * ldb + n]; epilogue EPI_STORE or EPI_DMASK (16-byte row stores).
+// With colsum (B k-contiguous only), each workgroup also writes the column
+// sums of what it stored, as stored, to row w of colsum ([rows][N] floats,
+// *colsum_rows = the workgroups per column block, at most
+// tsgemm_colsum_rows_max()).
 bool tsgemm_supported(int prec, int64_t K);
+int tsgemm_colsum_rows_max();
 hipError_t tsgemm_launch(int prec, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_kc, int64_t M,
-                         int64_t N, int64_t K, const Epilogue& epi, hipStream_t s);
+                         int64_t N, int64_t K, const Epilogue& epi, hipStream_t s, float* colsum = nullptr,
+                         int* colsum_rows = nullptr);
 
 // ----------------------------------------------------- weight gradient ----
 // partials[s][m][n] = sum over the s-th vertex span of H[k][m] * G[k][n];

@@ -53,14 +53,22 @@ struct TsParams {
   int64_t kpad;            // K rounded up to the k chunk
   int nblk;                // columns per workgroup (multiple of 16)
   Epilogue epi;
+  float* colsum;           // CS: [gridDim.x][N] column sums of the stored C, one row per workgroup
 };
 
 // Dynamic LDS: B block [nblk][kpad + VE] (T), then 4 per-wave staging
 // buffers [16][nblk + 4] (fp32).
 // DM: epilogue multiplies by the ReLU/dropout derivative read from H
 // (EPI_DMASK with relu); otherwise a plain store.
-template <typename T, bool BKC, bool DM, int TM, int TNW>
+// CS: the workgroup also sums the stored values (as stored, i.e. rounded to
+// T) of each of its columns: the store pass writes them back to its staging
+// buffer, a lane adds the tile's 16 rows of its columns (tiles in order),
+// and at the end the four waves' sums are added in wave order into the
+// workgroup's row of p.colsum (bias gradient of the layer below, without a
+// pass of its own over C).
+template <typename T, bool BKC, bool DM, int CSM, int TM, int TNW>
 __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
+  constexpr bool CS = CSM != 0;
   constexpr int VE = Vec<T>::N;
   constexpr int KC = 4 * VE;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -134,6 +142,14 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
   const int tnw = min(TNW, nblk / 16);              // live column tiles of this block
   constexpr int OV = Vec<T>::N;
   const int vpr = nblk / OV;
+  // CSM == 1 (vpr divides 64): a lane always stores the same column vector
+  // and sums it in registers (creg); CSM == 2: the tile's stored values go
+  // back to LDS and a lane sums columns lane and lane + 64 (csum)
+  constexpr bool cs_reg = CSM == 1;
+  float csum[2] = {0.f, 0.f};
+  float creg[OV];
+#pragma unroll
+  for (int j = 0; j < OV; ++j) creg[j] = 0.f;
 
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int64_t r0 = tile * tile_rows + (int64_t)wave * (TM * 16);
@@ -265,7 +281,13 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
         if (idx >= 16 * vpr) break;
         const int rr = idx / vpr, cv = idx % vpr;
         const int64_t row = r0 + tm * 16 + rr, col = n0 + cv * OV;
-        if (row >= p.M || col >= p.N) continue;
+        if (row >= p.M || col >= p.N) {
+          if constexpr (CS && !cs_reg) {
+#pragma unroll
+            for (int j = 0; j < OV; ++j) myC[rr * ldc + cv * OV + j] = 0.f;
+          }
+          continue;
+        }
         float v[OV];
 #pragma unroll
         for (int j = 0; j < OV; ++j) v[j] = myC[rr * ldc + cv * OV + j];
@@ -276,6 +298,16 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
 #pragma unroll
           for (int j = 0; j < OV; ++j) v[j] = h[j] > 0.f ? v[j] * p.epi.keep_scale : 0.f;
         }
+        if constexpr (CS) {
+          if constexpr (cs_reg) {
+#pragma unroll
+            for (int j = 0; j < OV; ++j) creg[j] += col + j < p.N ? to_f32<T>(from_f32<T>(v[j])) : 0.f;
+          } else {
+#pragma unroll
+            for (int j = 0; j < OV; ++j)
+              myC[rr * ldc + cv * OV + j] = col + j < p.N ? to_f32<T>(from_f32<T>(v[j])) : 0.f;
+          }
+        }
         Epilogue plain = p.epi;
         plain.mode = EPI_STORE;
         epi_store_vec<T>(plain, row, col, v);
@@ -283,6 +315,52 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      if constexpr (CS && !cs_reg) {
+        // the tile's stored values are in myC: rows in order per column
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int c = lane + 64 * h;
+          if (c < nblk) {
+            float a = myC[c];
+#pragma unroll
+            for (int r = 1; r < 16; ++r) a += myC[r * ldc + c];
+            csum[h] += a;
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      }
+    }
+  }
+  if constexpr (CS) {
+    if constexpr (cs_reg) {
+      // lanes l, l + vpr, l + 2 vpr, ... hold the same columns: butterfly
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1)
+        if (off >= vpr)
+#pragma unroll
+          for (int j = 0; j < OV; ++j) creg[j] += __shfl_xor(creg[j], off);
+    }
+    __syncthreads();
+    if constexpr (cs_reg) {
+      if (lane < vpr)
+#pragma unroll
+        for (int j = 0; j < OV; ++j) myC[lane * OV + j] = creg[j];
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (lane + 64 * h < nblk) myC[lane + 64 * h] = csum[h];
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < nblk; c += 256) {
+      if (n0 + c < p.N) {
+        float a = sC[c];
+        a += sC[1 * 16 * ldc + c];
+        a += sC[2 * 16 * ldc + c];
+        a += sC[3 * 16 * ldc + c];
+        p.colsum[(int64_t)blockIdx.x * p.N + n0 + c] = a;
+      }
     }
   }
 }
@@ -295,8 +373,8 @@ int ts_nblk(int64_t N, int64_t kpad) {
   return (int)nb;
 }
 
-template <typename T, bool BKC, bool DM, int TM>
-hipError_t launch_tm(const TsParams& p, hipStream_t s) {
+template <typename T, bool BKC, bool DM, int CSM, int TM>
+hipError_t launch_tm(const TsParams& p, int* grid_rows, hipStream_t s) {
   const int tnw = p.nblk / 16;
   const size_t lds = ((size_t)p.nblk * (p.kpad + Vec<T>::N) * sizeof(T) + 15) / 16 * 16 +
                      (size_t)4 * 16 * (p.nblk + 4) * sizeof(float);
@@ -305,14 +383,15 @@ hipError_t launch_tm(const TsParams& p, hipStream_t s) {
   const int64_t ntiles = (p.M + 64 * TM - 1) / (64 * TM);
   const int64_t per_col = std::max<int64_t>(1, 512 / nb);
   dim3 grid((unsigned)std::min<int64_t>(ntiles, per_col), (unsigned)nb);
+  if (grid_rows) *grid_rows = (int)grid.x;
 #define TS_L(TNW_)                                                                                          \
   do {                                                                                                      \
     if (lds > 65536) {                                                                                      \
-      hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&tsgemm_kernel<T, BKC, DM, TM, TNW_>),  \
+      hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&tsgemm_kernel<T, BKC, DM, CSM, TM, TNW_>),\
                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);           \
       if (ea != hipSuccess) return ea;                                                                      \
     }                                                                                                       \
-    hipLaunchKernelGGL((tsgemm_kernel<T, BKC, DM, TM, TNW_>), grid, dim3(256), lds, s, p);                     \
+    hipLaunchKernelGGL((tsgemm_kernel<T, BKC, DM, CSM, TM, TNW_>), grid, dim3(256), lds, s, p);                \
   } while (0)
   if (tnw <= 1) TS_L(1);
   else if (tnw <= 2) TS_L(2);
@@ -322,8 +401,9 @@ hipError_t launch_tm(const TsParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <typename T, bool BKC, bool DM>
-hipError_t launch_b(TsParams p, hipStream_t s) {
+template <typename T, bool BKC, bool DM, bool CS>
+hipError_t launch_b(TsParams p, int* grid_rows, hipStream_t s) {
+  constexpr int OV = Vec<T>::N;
   constexpr int KC = 4 * Vec<T>::N;
   p.kpad = (p.K + KC - 1) / KC * KC;
   p.nblk = ts_nblk<T>(p.N, p.kpad);
@@ -333,16 +413,27 @@ hipError_t launch_b(TsParams p, hipStream_t s) {
   // fragment sets, i.e. one wave per SIMD; TM = 2 keeps two)
   // (the H-mask epilogue with 128-column blocks holds another 32 registers:
   // one row tile per wave keeps two waves per SIMD there)
-  if (tiles64 >= 256 && !(DM && p.nblk > 64)) return launch_tm<T, BKC, DM, 2>(p, s);
-  return launch_tm<T, BKC, DM, 1>(p, s);
+  const bool two = tiles64 >= 256 && !(DM && p.nblk > 64);
+  if constexpr (CS) {
+    if (64 % (p.nblk / OV) == 0)
+      return two ? launch_tm<T, BKC, DM, 1, 2>(p, grid_rows, s) : launch_tm<T, BKC, DM, 1, 1>(p, grid_rows, s);
+    return two ? launch_tm<T, BKC, DM, 2, 2>(p, grid_rows, s) : launch_tm<T, BKC, DM, 2, 1>(p, grid_rows, s);
+  }
+  return two ? launch_tm<T, BKC, DM, 0, 2>(p, grid_rows, s) : launch_tm<T, BKC, DM, 0, 1>(p, grid_rows, s);
 }
 
+// Column sums (CS) are only asked of dZ_below = (G_S W^T) * mask, whose B
+// is k-contiguous.
 template <typename T>
-hipError_t launch_t(const TsParams& p, bool bkc, hipStream_t s) {
+hipError_t launch_t(const TsParams& p, bool bkc, int* grid_rows, hipStream_t s) {
   const bool dm = p.epi.mode == EPI_DMASK && p.epi.relu;
-  if (!bkc && !dm) return launch_b<T, false, false>(p, s);
-  if (!dm) return launch_b<T, true, false>(p, s);
-  return bkc ? launch_b<T, true, true>(p, s) : launch_b<T, false, true>(p, s);
+  if (p.colsum) {
+    if (!bkc) return hipErrorInvalidValue;
+    return dm ? launch_b<T, true, true, true>(p, grid_rows, s) : launch_b<T, true, false, true>(p, grid_rows, s);
+  }
+  if (!bkc && !dm) return launch_b<T, false, false, false>(p, grid_rows, s);
+  if (!dm) return launch_b<T, true, false, false>(p, grid_rows, s);
+  return bkc ? launch_b<T, true, true, false>(p, grid_rows, s) : launch_b<T, false, true, false>(p, grid_rows, s);
 }
 
 }  // namespace
@@ -354,14 +445,17 @@ bool tsgemm_supported(int prec, int64_t K) {
   return (kpad + 16 / s) * s * 16 <= TS_LDS_B_BYTES;   // at least one 16-column block fits
 }
 
+int tsgemm_colsum_rows_max() { return 512; }
+
 hipError_t tsgemm_launch(int prec, const void* A, int64_t lda, const void* B, int64_t ldb, bool b_kc, int64_t M,
-                         int64_t N, int64_t K, const Epilogue& epi, hipStream_t s) {
+                         int64_t N, int64_t K, const Epilogue& epi, hipStream_t s, float* colsum, int* colsum_rows) {
   TsParams p;
   p.A = A; p.lda = lda; p.B = B; p.ldb = ldb; p.M = M; p.N = N; p.K = K; p.kpad = 0; p.nblk = 0; p.epi = epi;
+  p.colsum = colsum;
   switch (prec) {
-    case 0: return launch_t<float>(p, b_kc, s);
-    case 1: return launch_t<f16>(p, b_kc, s);
-    case 2: return launch_t<bf16>(p, b_kc, s);
+    case 0: return launch_t<float>(p, b_kc, colsum_rows, s);
+    case 1: return launch_t<f16>(p, b_kc, colsum_rows, s);
+    case 2: return launch_t<bf16>(p, b_kc, colsum_rows, s);
   }
   return hipErrorInvalidValue;
 }

@@ -98,7 +98,7 @@ class GcnAdamConfig(ctypes.Structure):
                 ("max_scale", ctypes.c_float)]
 
 
-ABI_VERSION = 10          # GCN_ABI_VERSION of the structs above
+ABI_VERSION = 11          # GCN_ABI_VERSION of the structs and signatures here
 FIX_BIG_PIECES = 32       # GCN_FIX_BIG_PIECES
 
 _lib = None
@@ -128,9 +128,9 @@ def lib():
         "gcn_layer_workspace_size": (I32, [PADJ, PLAY, I32, PSZ]),
         "gcn_layer_fwd": (I32, [PADJ, PLAY, I32, I32, P, P, P, ctypes.c_uint64, ctypes.c_uint64,
                                 P, P, P, P, SZ, P]),
-        "gcn_layer_bwd": (I32, [PADJ, PLAY, I32, P, P, P, I32, ctypes.c_float, P, P, P, P, P, P,
+        "gcn_layer_bwd": (I32, [PADJ, PLAY, I32, P, P, P, I32, ctypes.c_float, P, P, P, P, P, P, P,
                                 SZ, P]),
-        "gcn_layer_bwd_noalloc": (I32, [PADJ, PLAY, I32, P, P, P, I32, ctypes.c_float, P, P, P, P, P, P]),
+        "gcn_layer_bwd_noalloc": (I32, [PADJ, PLAY, I32, P, P, P, I32, ctypes.c_float, P, P, P, P, P, P, P]),
         "gcn_loss_workspace_size": (I32, [I64, I64, PSZ]),
         "gcn_loss": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, P, P, P, P, SZ, P]),
         "gcn_optimizer_step": (I32, [I64, P, P, P, P, P, I32, ctypes.POINTER(GcnAdamConfig), P, P, P]),
@@ -237,10 +237,10 @@ def gcn_layer_fwd(adj, layer, prec, training, H, W, bias, seed, epoch, S, H_out,
 
 
 def gcn_layer_bwd(adj, layer, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS, overflow,
-                  workspace, stream=None):
+                  workspace, stream=None, dbias_below=None):
     st = lib().gcn_layer_bwd(ctypes.byref(adj), ctypes.byref(layer), prec, _ptr(H), _ptr(W), _ptr(dZ),
-                             act_below, p_below, _ptr(dW), _ptr(dbias), _ptr(dZ_below), _ptr(GS),
-                             _ptr(overflow), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                             act_below, p_below, _ptr(dW), _ptr(dbias), _ptr(dZ_below), _ptr(dbias_below),
+                             _ptr(GS), _ptr(overflow), _ptr(workspace), workspace.numel() * workspace.element_size(),
                              _stream(stream))
     _check(st, "gcn_layer_bwd")
 
@@ -249,10 +249,10 @@ NOALLOC_SCRATCH_BYTES = 64 << 20    # GCN_NOALLOC_SCRATCH_BYTES
 
 
 def gcn_layer_bwd_noalloc(adj, layer, prec, H, W, dZ, act_below, p_below, dW, dbias, dZ_below, GS, overflow,
-                          stream=None):
+                          stream=None, dbias_below=None):
     st = lib().gcn_layer_bwd_noalloc(ctypes.byref(adj), ctypes.byref(layer), prec, _ptr(H), _ptr(W), _ptr(dZ),
-                                     act_below, p_below, _ptr(dW), _ptr(dbias), _ptr(dZ_below), _ptr(GS),
-                                     _ptr(overflow), _stream(stream))
+                                     act_below, p_below, _ptr(dW), _ptr(dbias), _ptr(dZ_below),
+                                     _ptr(dbias_below), _ptr(GS), _ptr(overflow), _stream(stream))
     _check(st, "gcn_layer_bwd_noalloc")
 
 

@@ -342,10 +342,12 @@ class GCN2:
         else:
             G.gcn_loss(self.n, self.C, self.ld_c, self.prec, self.Z2, self.labels, self.mask, self.n_mask,
                        self.scale_ptr(), self.loss, self.dZ2, self.n_correct, self.overflow, self.ws, stream)
+        # db1 (the column sums of dZ1) comes from the call that writes dZ1
         G.gcn_layer_bwd(a, self.L2, self.prec, self.H1, self.W2w(), self.dZ2, G.GCN_ACT_RELU, self.p,
-                        self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream)
+                        self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream,
+                        dbias_below=self.db1())
         G.gcn_layer_bwd(a, self.L1, self.prec, self.X, self.W1w(), self.dZ1, G.GCN_ACT_NONE, 0.0,
-                        self.dW1(), self.db1(), None, self.SG1, self.overflow, self.ws, stream)
+                        self.dW1(), None, None, self.SG1, self.overflow, self.ws, stream)
 
     def optimizer_step(self, stream=None):
         if self.level == "O3":
@@ -487,9 +489,10 @@ class GAE2:
         G.gcn_pair_backward(self.n, self.f_e, self.ld_e, self.prec, self.Z, self.pair_u, self.pair_v, self.K,
                             self.pair_g, self.dZ, self.ld_e, self.overflow, self.ws, stream)
         G.gcn_layer_bwd(a, self.L2, self.prec, self.H1, self.W2w(), self.dZ, G.GCN_ACT_RELU, 0.0,
-                        self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream)
+                        self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream,
+                        dbias_below=self.db1())
         G.gcn_layer_bwd(a, self.L1, self.prec, self.X, self.W1w(), self.dZ1, G.GCN_ACT_NONE, 0.0,
-                        self.dW1(), self.db1(), None, self.SG1, self.overflow, self.ws, stream)
+                        self.dW1(), None, None, self.SG1, self.overflow, self.ws, stream)
 
     def optimizer_step(self, stream=None):
         G.gcn_optimizer_step(self.P, self.master, self.grad, self.m, self.v, self.working, self.prec,

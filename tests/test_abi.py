@@ -33,7 +33,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert G.gcn_abi_version() == 10
+    assert G.gcn_abi_version() == 11
     assert G.gcn_status_string(0) == "GCN_OK"
     for s in range(1, 9):
         assert G.gcn_status_string(s).startswith("GCN_ERR_")
@@ -167,12 +167,14 @@ def test_layer_bwd_noalloc_validation_codes():
     lib = G.lib()
     L = G.GcnLayer(16, 8, 16, 8, G.GCN_ACT_NONE, 0.0, 0, 0)
 
-    def call(adj, layer, prec=G.GCN_F16, H=0x10000):
+    def call(adj, layer, prec=G.GCN_F16, H=0x10000, dZb=None, dbb=None):
         return lib.gcn_layer_bwd_noalloc(ctypes.byref(adj), ctypes.byref(layer), prec, H, 0x20000, 0x30000,
-                                         G.GCN_ACT_RELU, 0.5, 0x40000, None, None, 0x50000, None, None)
+                                         G.GCN_ACT_RELU, 0.5, 0x40000, None, dZb, dbb, 0x50000, None, None)
 
     assert call(_adj(), L, prec=7) == 1                                   # bad precision
     assert call(_adj(), L, H=0x10004) == 3                                # misaligned
+    assert call(_adj(), L, dbb=0x60000) == 1                              # dbias_below needs dZ_below
+    assert call(_adj(), L, dZb=0x70000, dbb=0x60004) == 3                 # misaligned dbias_below
     assert call(_adj(n=0), L) == 2
     # dense A_hat of 2^20 vertices with 64 gradient columns: the transposed
     # dZ alone needs 128 MiB of scratch, more than the array holds

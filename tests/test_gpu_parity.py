@@ -393,10 +393,11 @@ def test_layer_bwd(prec, case):
     dW = torch.full((f_in, round8(f_out)), 7.0, dtype=torch.float32, device=dev())
     db = torch.full((round8(f_out),), 7.0, dtype=torch.float32, device=dev())
     dZb = torch.empty((n, round8(f_in)), dtype=G.torch_dtype(prec), device=dev())
+    dbb = torch.full((round8(f_in),), 7.0, dtype=torch.float32, device=dev())
     GS = torch.empty((n, round8(f_out)), dtype=G.torch_dtype(prec), device=dev())
     ov = torch.zeros(1, dtype=torch.int32, device=dev())
     ws = torch.empty(G.gcn_layer_workspace_size(dg.adj, L, prec), dtype=torch.uint8, device=dev())
-    G.gcn_layer_bwd(dg.adj, L, prec, H, W, dZ, act_below, p, dW, db, dZb, GS, ov, ws)
+    G.gcn_layer_bwd(dg.adj, L, prec, H, W, dZ, act_below, p, dW, db, dZb, GS, ov, ws, dbias_below=dbb)
     torch.cuda.synchronize()
     hr, wr, dzr = rounded(h, prec), rounded(w, prec), rounded(dz, prec)
     vals = O.norm_values(g)
@@ -408,6 +409,14 @@ def test_layer_bwd(prec, case):
     assert_close(db.cpu().numpy()[:f_out], db_o, prec, "db")
     assert np.all(db.cpu().numpy()[f_out:] == 0)
     assert_close(host(dZb, f_in), dzb_o, prec, "dZ_below")
+    # the bias gradient of the layer below: the column sums of dZ_below as
+    # stored (checked against the stored values summed in fp64, to fp32
+    # summation error, and against the oracle's exact dZ_below)
+    stored = host(dZb, f_in).astype(np.float64)
+    got_bb = dbb.cpu().numpy()
+    assert np.all(np.abs(got_bb[:f_in] - stored.sum(0)) <= 2e-5 * np.abs(stored).sum(0) + 1e-30)
+    assert np.all(got_bb[f_in:] == 0)
+    assert_close(got_bb[:f_in], dzb_o.sum(0), prec, "db_below")
     assert int(ov.item()) == 0
 
 

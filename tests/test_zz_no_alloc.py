@@ -39,6 +39,7 @@ def _outputs(n, L, prec):
     return dict(dW=torch.full((L.f_in, L.ld_out), 7.0, dtype=torch.float32, device="cuda"),
                 db=torch.full((L.ld_out,), 7.0, dtype=torch.float32, device="cuda"),
                 dZb=torch.zeros((n, L.ld_in), dtype=dt, device="cuda"),
+                dbb=torch.full((L.ld_in,), 7.0, dtype=torch.float32, device="cuda"),
                 GS=torch.zeros((n, L.ld_out), dtype=dt, device="cuda"),
                 ov=torch.zeros(1, dtype=torch.int32, device="cuda"))
 
@@ -54,10 +55,10 @@ def test_noalloc_matches_workspace_call_twice(prec, storage):
         ref = _outputs(n, L, prec)
         ws = torch.empty(need, dtype=torch.uint8, device="cuda")
         G.gcn_layer_bwd(dg.adj, L, prec, H, W, dZ, G.GCN_ACT_RELU, 0.5, ref["dW"], ref["db"], ref["dZb"], ref["GS"],
-                        ref["ov"], ws)
+                        ref["ov"], ws, dbias_below=ref["dbb"])
         got = _outputs(n, L, prec)
         G.gcn_layer_bwd_noalloc(dg.adj, L, prec, H, W, dZ, G.GCN_ACT_RELU, 0.5, got["dW"], got["db"], got["dZb"],
-                                got["GS"], got["ov"])
+                                got["GS"], got["ov"], dbias_below=got["dbb"])
         torch.cuda.synchronize()
         for key in ref:
             assert torch.equal(ref[key], got[key]), (storage, prec, k, key)
