@@ -374,14 +374,21 @@ gcn_status gcn_layer_bwd_noalloc(const gcn_adj* A, const gcn_layer* L, int32_t p
  *   *loss        = mean over masked rows of logsumexp(z_i) - z_i[y_i]   (fp32, unscaled)
  *   dlogits      = S * (softmax(z_i) - onehot(y_i)) / n_mask on masked rows, 0 elsewhere
  *   *n_correct   = masked rows whose arg-max (lowest index on ties) is y_i (may be NULL)
+ *   dlogits_colsum = column sums of dlogits as stored (fp32 [ld], entries
+ *                  [C, ld) set to 0; may be NULL): the output layer's bias
+ *                  gradient, which its gcn_layer_bwd call then need not
+ *                  compute (dbias = NULL there); summed by the loss kernel's
+ *                  own workgroups, without a pass of its own over dlogits
  * S is *loss_scale (device float; NULL means 1).  Class padding [C, ld) is
- * excluded from the softmax.  The loss is reduced in a fixed order.
+ * excluded from the softmax.  The loss and the column sums are reduced in a
+ * fixed order.
  * ------------------------------------------------------------------------- */
 gcn_status gcn_loss_workspace_size(int64_t n, int64_t C, size_t* bytes);
 gcn_status gcn_loss(int64_t n, int64_t C, int64_t ld, int32_t prec, const void* logits,
                     const int32_t* labels, const uint8_t* mask, int64_t n_mask,
-                    const float* loss_scale, float* loss, void* dlogits, int32_t* n_correct,
-                    int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream);
+                    const float* loss_scale, float* loss, void* dlogits, float* dlogits_colsum,
+                    int32_t* n_correct, int32_t* overflow, void* workspace, size_t workspace_bytes,
+                    void* stream);
 
 /* ---------------------------------------------------------------------------
  * gcn_optimizer_step: one step of Adam on fp32 master weights with dynamic

@@ -636,18 +636,20 @@ gcn_status gcn_loss_workspace_size(int64_t n, int64_t C, size_t* bytes) {
 
 gcn_status gcn_loss(int64_t n, int64_t C, int64_t ld, int32_t prec, const void* logits, const int32_t* labels,
                     const uint8_t* mask, int64_t n_mask, const float* loss_scale, float* loss, void* dlogits,
-                    int32_t* n_correct, int32_t* overflow, void* workspace, size_t workspace_bytes, void* stream) {
+                    float* dlogits_colsum, int32_t* n_correct, int32_t* overflow, void* workspace,
+                    size_t workspace_bytes, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (!valid_prec(prec)) return GCN_ERR_INVALID_ARG;
   if (n <= 0 || C <= 0 || ld < C || n_mask <= 0 || n_mask > n) return GCN_ERR_SHAPE;
   if (ld % 8) return GCN_ERR_ALIGNMENT;
   if (C > 64 * (prec == GCN_F32 ? 4 : 8)) return GCN_ERR_UNSUPPORTED;
   if (!logits || !labels || !loss || !dlogits) return GCN_ERR_INVALID_ARG;
-  if (!aligned16(logits) || !aligned16(dlogits)) return GCN_ERR_ALIGNMENT;
+  if (!aligned16(logits) || !aligned16(dlogits) || (dlogits_colsum && !aligned16(dlogits_colsum)))
+    return GCN_ERR_ALIGNMENT;
   if (!workspace || workspace_bytes < loss_workspace_bytes(n, C)) return GCN_ERR_WORKSPACE;
   if (!aligned16(workspace)) return GCN_ERR_ALIGNMENT;
-  GCN_HIP(loss_launch(prec, n, C, ld, logits, labels, mask, n_mask, loss_scale, loss, dlogits, n_correct, overflow,
-                      workspace, s));
+  GCN_HIP(loss_launch(prec, n, C, ld, logits, labels, mask, n_mask, loss_scale, loss, dlogits, dlogits_colsum,
+                      n_correct, overflow, workspace, s));
   return finish(hipSuccess, s);
 }
 

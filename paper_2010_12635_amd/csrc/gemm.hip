@@ -271,7 +271,8 @@ __device__ __forceinline__ void reduce_body_t(const RedJob& j, int64_t blk) {
 
 template <typename T>
 __device__ __forceinline__ void reduce_body(const RedJob& j, int64_t blk) {
-  if (j.opw == 4) reduce_body_t<T, 4>(j, blk);
+  if (j.opw == 1) reduce_body_t<T, 1>(j, blk);
+  else if (j.opw == 4) reduce_body_t<T, 4>(j, blk);
   else if (j.opw == 16) reduce_body_t<T, 16>(j, blk);
   else reduce_body_t<T, 64>(j, blk);
 }
@@ -380,8 +381,9 @@ RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const E
   RedJob j;
   j.part = partials; j.splits = splits; j.M = M; j.N = N; j.ep = epi;
   j.width = epi.mode == EPI_F32 ? epi.ldo : N;
-  // about 32 splits per thread at most where the outputs allow it
-  j.opw = splits > 512 ? 4 : splits > 128 ? 16 : 64;
+  // about 32 splits per thread at most where the outputs allow it (one
+  // output per workgroup, 64 splits per thread, beyond 4096 splits)
+  j.opw = splits > 4096 ? 1 : splits > 512 ? 4 : splits > 128 ? 16 : 64;
   j.blocks = (M * j.width + j.opw - 1) / j.opw;
   return j;
 }

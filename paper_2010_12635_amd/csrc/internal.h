@@ -43,7 +43,7 @@ struct RedJob {
   const float* part;
   int splits;
   int64_t M, N, width, blocks;
-  int opw;                      // outputs per workgroup: 64, 16 or 4 (256 / opw groups of splits)
+  int opw;                      // outputs per workgroup: 64, 16, 4 or 1 (256 / opw groups of splits)
   Epilogue ep;
 };
 RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const Epilogue& epi);
@@ -158,8 +158,8 @@ hipError_t schedule_run(int64_t n, int64_t nnz, bool idx64, const void* rowptr, 
 size_t loss_workspace_bytes(int64_t n, int64_t C);
 hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* logits,
                        const int32_t* labels, const uint8_t* mask, int64_t n_mask,
-                       const float* loss_scale, float* loss, void* dlogits, int32_t* n_correct,
-                       int32_t* flag, void* ws, hipStream_t s);
+                       const float* loss_scale, float* loss, void* dlogits, float* dlogits_colsum,
+                       int32_t* n_correct, int32_t* flag, void* ws, hipStream_t s);
 
 // ------------------------------------------------------------ optimiser ----
 struct AdamHyper {

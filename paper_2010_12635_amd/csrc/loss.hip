@@ -22,6 +22,7 @@ struct LossParams {
   void* dlogits;
   float* part_loss;     // [blocks]
   int32_t* part_corr;   // [blocks]
+  float* part_cs;       // [blocks][C] column sums of the stored dlogits, or NULL
   int32_t* flag;
 };
 
@@ -123,6 +124,10 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
   // (in that order for the per-slot sums)
   float acc_loss = 0.f;
   int32_t acc_corr = 0;
+  float acc_cs[VE];                                 // this lane's classes over its rows (as stored)
+#pragma unroll
+  for (int i = 0; i < VE; ++i) acc_cs[i] = 0.f;
+  const bool want_cs = p.part_cs != nullptr;
   const float sc = (p.loss_scale ? *p.loss_scale : 1.f) * p.inv_count;
   constexpr float LOG2E = 1.4426950408889634f;
   for (int64_t base = (int64_t)blockIdx.x * (LOSS_R * RG); base < p.n; base += (int64_t)gridDim.x * (LOSS_R * RG)) {
@@ -190,6 +195,12 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
         }
         const uint4 o = pack<T>(d);
         stg16(reinterpret_cast<T*>(p.dlogits) + row * p.ld + col0, o);
+        if (want_cs) {
+          float st[VE];
+          unpack<T>(o, st);
+#pragma unroll
+          for (int i = 0; i < VE; ++i) acc_cs[i] += st[i];
+        }
         // |d| <= |s_in| (softmax values lie in [0, 1]): with finite logits
         // (lse finite) and |s_in| at most the largest finite value of T no
         // element can overflow; otherwise every element is checked
@@ -203,6 +214,11 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
     s_loss[slot] = acc_loss;
     s_corr[slot] = acc_corr;
   }
+  __shared__ float s_cs[RG][LPR * VE];
+  if (want_cs) {
+#pragma unroll
+    for (int i = 0; i < VE; ++i) s_cs[slot][li * VE + i] = acc_cs[i];
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     float a = 0.f;
@@ -210,6 +226,14 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
     for (int i = 0; i < RG; ++i) { a += s_loss[i]; c += s_corr[i]; }
     p.part_loss[blockIdx.x] = a;
     p.part_corr[blockIdx.x] = c;
+  }
+  if (want_cs) {
+    // the workgroup's column sums: its row slots added in slot order
+    for (int cidx = threadIdx.x; cidx < p.C; cidx += 256) {
+      float a = s_cs[0][cidx];
+      for (int k = 1; k < RG; ++k) a += s_cs[k][cidx];
+      p.part_cs[(int64_t)blockIdx.x * p.C + cidx] = a;
+    }
   }
 }
 
@@ -248,10 +272,13 @@ __global__ __launch_bounds__(256) void loss_final_kernel(const float* __restrict
 }
 
 // Workgroups of the loss kernel: one per row group up to 65536 (each then
-// walks several groups).
+// walks several groups).  Capping them at 2048 to bound the column-sum
+// partials made the kernel slower on R-MAT scale 21 (105 -> 118 us) than
+// the wider reduction of 16384 partials costs.
+constexpr int64_t LOSS_MAX_BLOCKS = 65536;
 int64_t loss_blocks(int64_t n, int64_t rows_per_group) {
   const int64_t nb = (n + rows_per_group - 1) / rows_per_group;
-  return nb < 65536 ? nb : 65536;
+  return nb < LOSS_MAX_BLOCKS ? nb : LOSS_MAX_BLOCKS;
 }
 
 int loss_rows_per_iter(int64_t n, int64_t rows_per_group) {
@@ -299,23 +326,36 @@ int64_t rows_per_block(int prec, int64_t C, int64_t n) {
 
 }  // namespace
 
+// Workgroups of the softmax launch at most (fp32 needs the most).
+int64_t loss_max_blocks(int64_t n, int64_t C) {
+  const int64_t nb = loss_blocks(n, rows_per_block(0, C, n));
+  const int64_t nb16 = loss_blocks(n, rows_per_block(1, C, n));
+  return nb > nb16 ? nb : nb16;
+}
+
+// [loss partials][correct-count partials][column-sum partials (blocks x C)]
 size_t loss_workspace_bytes(int64_t n, int64_t C) {
-  const int64_t nb = (n + rows_per_block(0, C, n) - 1) / rows_per_block(0, C, n) + 1;   // fp32 needs the most blocks
-  const int64_t nb16 = (n + rows_per_block(1, C, n) - 1) / rows_per_block(1, C, n) + 1;
-  const int64_t m = nb > nb16 ? nb : nb16;
-  return (size_t)m * (sizeof(float) + sizeof(int32_t)) + 256;
+  const int64_t m = loss_max_blocks(n, C) + 1;
+  const size_t a = ((size_t)m * sizeof(float) + 255) & ~size_t(255);
+  const size_t b = ((size_t)m * sizeof(int32_t) + 255) & ~size_t(255);
+  return a + b + (size_t)m * (size_t)C * sizeof(float) + 256;
 }
 
 hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* logits, const int32_t* labels,
                        const uint8_t* mask, int64_t n_mask, const float* loss_scale, float* loss, void* dlogits,
-                       int32_t* n_correct, int32_t* flag, void* ws, hipStream_t s) {
+                       float* dlogits_colsum, int32_t* n_correct, int32_t* flag, void* ws, hipStream_t s) {
   const int64_t nb = loss_blocks(n, rows_per_block(prec, C, n));
+  const int64_t m = loss_max_blocks(n, C) + 1;
   LossParams p;
   p.n = n; p.C = C; p.ld = ld; p.logits = logits; p.labels = labels; p.mask = mask;
   p.inv_count = 1.f / (float)n_mask;
   p.loss_scale = loss_scale; p.dlogits = dlogits;
-  p.part_loss = reinterpret_cast<float*>(ws);
-  p.part_corr = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(ws) + ((nb * sizeof(float) + 255) & ~size_t(255)));
+  char* w = reinterpret_cast<char*>(ws);
+  p.part_loss = reinterpret_cast<float*>(w);
+  w += ((size_t)m * sizeof(float) + 255) & ~size_t(255);
+  p.part_corr = reinterpret_cast<int32_t*>(w);
+  w += ((size_t)m * sizeof(int32_t) + 255) & ~size_t(255);
+  p.part_cs = dlogits_colsum ? reinterpret_cast<float*>(w) : nullptr;
   p.flag = flag;
   hipError_t e;
   switch (prec) {
@@ -327,7 +367,13 @@ hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* l
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(loss_final_kernel, dim3(1), dim3(256), 0, s, p.part_loss, p.part_corr, nb, p.inv_count, loss,
                      n_correct, flag);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess || !dlogits_colsum) return e;
+  // the workgroups' column sums added in workgroup order; classes [C, ld) get 0
+  Epilogue eb{};
+  eb.out = dlogits_colsum; eb.ldo = ld; eb.rows = 1; eb.cols = C; eb.mode = EPI_F32; eb.flag = flag;
+  eb.keep_scale = 1.f;
+  return reduce_partials2(prec, make_job(p.part_cs, (int)nb, 1, C, eb), nullptr, s);
 }
 
 }  // namespace gcn

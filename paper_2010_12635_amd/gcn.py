@@ -132,7 +132,7 @@ def lib():
                                 SZ, P]),
         "gcn_layer_bwd_noalloc": (I32, [PADJ, PLAY, I32, P, P, P, I32, ctypes.c_float, P, P, P, P, P, P, P]),
         "gcn_loss_workspace_size": (I32, [I64, I64, PSZ]),
-        "gcn_loss": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, P, P, P, P, SZ, P]),
+        "gcn_loss": (I32, [I64, I64, I64, I32, P, P, P, I64, P, P, P, P, P, P, P, SZ, P]),
         "gcn_optimizer_step": (I32, [I64, P, P, P, P, P, I32, ctypes.POINTER(GcnAdamConfig), P, P, P]),
         "gcn_transform_workspace_size": (I32, [I64, I64, I64, I32, PSZ]),
         "gcn_transform": (I32, [I64, I64, I64, I32, P, I64, P, I64, P, I64, P, P, SZ, P]),
@@ -263,10 +263,10 @@ def gcn_loss_workspace_size(n, C) -> int:
 
 
 def gcn_loss(n, C, ld, prec, logits, labels, mask, n_mask, loss_scale, loss, dlogits, n_correct, overflow,
-             workspace, stream=None):
+             workspace, stream=None, dlogits_colsum=None):
     st = lib().gcn_loss(n, C, ld, prec, _ptr(logits), _ptr(labels), _ptr(mask), n_mask, _ptr(loss_scale),
-                        _ptr(loss), _ptr(dlogits), _ptr(n_correct), _ptr(overflow), _ptr(workspace),
-                        workspace.numel() * workspace.element_size(), _stream(stream))
+                        _ptr(loss), _ptr(dlogits), _ptr(dlogits_colsum), _ptr(n_correct), _ptr(overflow),
+                        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "gcn_loss")
 
 

@@ -339,12 +339,16 @@ class GCN2:
                        self.scale_ptr(), self.loss, self.dZ2f, self.n_correct, self.overflow, self.ws, stream)
             G.gcn_cast(self.n, self.C, G.GCN_F32, self.dZ2f, self.ld_c, self.prec, self.dZ2, self.ld_c,
                        self.overflow, stream)
+            db2 = self.db2()
         else:
+            # db2 (the column sums of dZ2) comes from the loss kernel
             G.gcn_loss(self.n, self.C, self.ld_c, self.prec, self.Z2, self.labels, self.mask, self.n_mask,
-                       self.scale_ptr(), self.loss, self.dZ2, self.n_correct, self.overflow, self.ws, stream)
+                       self.scale_ptr(), self.loss, self.dZ2, self.n_correct, self.overflow, self.ws, stream,
+                       dlogits_colsum=self.db2())
+            db2 = None
         # db1 (the column sums of dZ1) comes from the call that writes dZ1
         G.gcn_layer_bwd(a, self.L2, self.prec, self.H1, self.W2w(), self.dZ2, G.GCN_ACT_RELU, self.p,
-                        self.dW2(), self.db2(), self.dZ1, self.SG2, self.overflow, self.ws, stream,
+                        self.dW2(), db2, self.dZ1, self.SG2, self.overflow, self.ws, stream,
                         dbias_below=self.db1())
         G.gcn_layer_bwd(a, self.L1, self.prec, self.X, self.W1w(), self.dZ1, G.GCN_ACT_NONE, 0.0,
                         self.dW1(), None, None, self.SG1, self.overflow, self.ws, stream)

@@ -131,10 +131,12 @@ def test_normalize_validation_codes():
 
 def test_loss_and_optimizer_validation_codes():
     lib = G.lib()
-    assert lib.gcn_loss(10, 7, 7, 1, 0x1000, 0x2000, None, 5, None, 0x3000, 0x4000, None, None,
+    assert lib.gcn_loss(10, 7, 7, 1, 0x1000, 0x2000, None, 5, None, 0x3000, 0x4000, None, None, None,
                         0x5000, 1 << 20, None) == 3                          # ld % 8
-    assert lib.gcn_loss(10, 7, 8, 1, 0x1000, 0x2000, None, 0, None, 0x3000, 0x4000, None, None,
+    assert lib.gcn_loss(10, 7, 8, 1, 0x1000, 0x2000, None, 0, None, 0x3000, 0x4000, None, None, None,
                         0x5000, 1 << 20, None) == 2                          # empty mask
+    assert lib.gcn_loss(10, 7, 8, 1, 0x1000, 0x2000, None, 5, None, 0x3000, 0x4000, 0x4004, None, None,
+                        0x5000, 1 << 20, None) == 3                          # misaligned column sums
     cfg = G.GcnAdamConfig(0.01, 0.9, 0.999, 1e-8, 0.5, 2.0, 2000, 1.0, 2.0**24)
     assert lib.gcn_optimizer_step(0, 0x1000, 0x2000, 0x3000, 0x4000, None, 1, ctypes.byref(cfg),
                                   0x5000, 0x6000, None) == 2

@@ -461,8 +461,9 @@ def test_loss(prec, C, n):
     loss = torch.zeros(1, device=dev())
     nc = torch.zeros(1, dtype=torch.int32, device=dev())
     ws = torch.empty(G.gcn_loss_workspace_size(n, C), dtype=torch.uint8, device=dev())
+    dcs = torch.full((ld,), 7.0, dtype=torch.float32, device=dev())
     G.gcn_loss(n, C, ld, prec, Z, torch.as_tensor(y).to(dev()), torch.as_tensor(mask).to(dev()), int(mask.sum()),
-               scale, loss, dZ, nc, None, ws)
+               scale, loss, dZ, nc, None, ws, dlogits_colsum=dcs)
     torch.cuda.synchronize()
     zr = rounded(z, prec)
     l_o, d_o, nc_o = O.softmax_ce(zr, y, mask, 1024.0)
@@ -470,6 +471,13 @@ def test_loss(prec, C, n):
     assert_close(host(dZ, C), d_o, prec, "dlogits")
     assert np.all(host(dZ)[:, C:] == 0)
     assert nc.item() == nc_o
+    # column sums of dlogits (the output layer's bias gradient): against the
+    # stored values summed in fp64, to fp32 summation error, and the oracle
+    stored = host(dZ, C).astype(np.float64)
+    got = dcs.cpu().numpy()
+    assert np.all(np.abs(got[:C] - stored.sum(0)) <= 2e-5 * np.abs(stored).sum(0) + 1e-30)
+    assert np.all(got[C:] == 0)
+    assert_close(got[:C], d_o.sum(0), prec, "dlogits column sums")
 
 
 # ------------------------------------------------------------ optimiser ----
