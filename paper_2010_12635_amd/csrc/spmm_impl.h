@@ -138,6 +138,37 @@ __device__ __forceinline__ void row_sum(float* acc, const T* __restrict__ X, int
 
 __device__ __forceinline__ int64_t desc_beg(uint4 d) { return (int64_t)((uint64_t)d.x | ((uint64_t)d.y << 32)); }
 
+// The bias of the workgroup's column block (LPR * VE columns from
+// blockIdx.y * LPR * VE), staged in LDS once per workgroup, zeros where
+// there is no bias: a lane then reads its columns from LDS at each row's
+// store instead of waiting on eight global loads there (R-MAT scale 21,
+// F = 128: bias + ReLU had cost 0.19 ms of a 1.65 ms call).  Every thread
+// of the workgroup must call it.
+template <typename T, int LPR>
+__device__ __forceinline__ void stage_bias(const Epilogue& ep, float* sb) {
+  constexpr int W = LPR * Vec<T>::N;
+  const bool has = ep.mode == EPI_AGG && ep.bias;
+  for (int i = threadIdx.x; i < W; i += 256) {
+    const int64_t c = (int64_t)blockIdx.y * W + i;
+    sb[i] = has && c < ep.cols ? ep.bias[c] : 0.f;
+  }
+  __syncthreads();
+}
+
+// Lane li's bias columns from the staged block (two 16-byte LDS reads for
+// fp16/bf16, one for fp32; no branch, so the row loop keeps no extra
+// scalar state).
+template <typename T>
+__device__ __forceinline__ void staged_bias(const float* sb, int li, float (&bv)[Vec<T>::N]) {
+  constexpr int VE = Vec<T>::N;
+  const float4* q = reinterpret_cast<const float4*>(sb) + li * (VE / 4);
+#pragma unroll
+  for (int j = 0; j < VE / 4; ++j) {
+    const float4 t = q[j];
+    bv[4 * j] = t.x; bv[4 * j + 1] = t.y; bv[4 * j + 2] = t.z; bv[4 * j + 3] = t.w;
+  }
+}
+
 // Rows of one entry, SINGLE_BUNDLE of them (descriptors k0 .. k0 + cnt - 1)
 // at once: descriptors, then column indices and values, then the gathers
 // go out together, so the bundle costs the dependent loads of one row.
@@ -148,7 +179,7 @@ constexpr int SINGLE_BUNDLE = 4;
 
 template <typename T, typename IdxT, bool HAS_VAL>
 __device__ __forceinline__ void single_bundle(const SpmmParams<IdxT>& p, const T* __restrict__ X, int64_t col0,
-                                              int64_t k0, int64_t cnt) {
+                                              const float* sb, int li, int64_t k0, int64_t cnt) {
   constexpr int VE = Vec<T>::N;
   constexpr int B = SINGLE_BUNDLE;
   int64_t beg[B];
@@ -186,7 +217,9 @@ __device__ __forceinline__ void single_bundle(const SpmmParams<IdxT>& p, const T
 #pragma unroll
       for (int i = 0; i < VE; ++i) acc[i] = 0.f;
       fma_vec<T>(acc, v[k], x[k]);
-      epi_store_vec<T>(p.epi, row[k], col0, acc, keep[k]);
+      float bv[VE];
+      staged_bias<T>(sb, li, bv);
+      epi_store_vec_b<T>(p.epi, row[k], col0, acc, bv, keep[k]);
     }
   }
 }
@@ -199,7 +232,7 @@ __device__ __forceinline__ void single_bundle(const SpmmParams<IdxT>& p, const T
 // pointers) stands between two rows; then bundles of SINGLE_BUNDLE rows of
 // one entry.
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
-__device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, int64_t bx, int64_t nbx) {
+__device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, const float* sb, int64_t bx, int64_t nbx) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -226,13 +259,15 @@ __device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, int64_
 #pragma unroll
       for (int i = 0; i < VE; ++i) acc[i] = 0.f;
       row_sum<T, LPR, HAS_VAL>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, beg, end);
-      epi_store_vec<T>(p.epi, row, col0, acc, keep);
+      float bv[VE];
+      staged_bias<T>(sb, li, bv);
+      epi_store_vec_b<T>(p.epi, row, col0, acc, bv, keep);
       slot = nslot;
     }
     for (; slot < units; slot += stride) {
       const int64_t k0 = n_multi + (slot - n_multi) * SINGLE_BUNDLE;
       const int64_t cnt = p.n_rows - k0 < SINGLE_BUNDLE ? p.n_rows - k0 : SINGLE_BUNDLE;
-      single_bundle<T, IdxT, HAS_VAL>(p, X, col0, k0, cnt);
+      single_bundle<T, IdxT, HAS_VAL>(p, X, col0, sb, li, k0, cnt);
     }
     return;
   }
@@ -245,13 +280,17 @@ __device__ __forceinline__ void spmm_rows_body(const SpmmParams<IdxT>& p, int64_
 #pragma unroll
     for (int i = 0; i < VE; ++i) acc[i] = 0.f;
     row_sum<T, LPR, HAS_VAL>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, beg, end);
-    epi_store_vec<T>(p.epi, row, col0, acc);
+    float bv[VE];
+    staged_bias<T>(sb, li, bv);
+    epi_store_vec_b<T>(p.epi, row, col0, acc, bv);
   }
 }
 
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 __global__ __launch_bounds__(256) void spmm_rows_kernel(SpmmParams<IdxT> p) {
-  spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, blockIdx.x, gridDim.x);
+  __shared__ __align__(16) float sb[LPR * Vec<T>::N];
+  stage_bias<T, LPR>(p.epi, sb);
+  spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, sb, blockIdx.x, gridDim.x);
 }
 
 struct PieceParams {
@@ -292,7 +331,7 @@ __device__ __forceinline__ int64_t piece_at(const PieceParams& p, int64_t x, int
 // next piece's descriptor loaded ahead (nw is a multiple of XCDS when there
 // are column ranges, so piece workgroup w runs on die w % XCDS).
 template <typename T, int LPR, bool HAS_VAL>
-__device__ __forceinline__ void spmm_piece_body(const PieceParams& p, int64_t w, int64_t nw) {
+__device__ __forceinline__ void spmm_piece_body(const PieceParams& p, const float* sb, int64_t w, int64_t nw) {
   constexpr int VE = Vec<T>::N;
   constexpr int G = 64 / LPR;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -323,7 +362,9 @@ __device__ __forceinline__ void spmm_piece_body(const PieceParams& p, int64_t w,
     row_sum<T, LPR, HAS_VAL>(acc, X, p.ldx, p.colidx, p.values, p.dinv, drow, beg, end);
     if (single) {
       // the row's only piece holds its whole sum: the epilogue stores it here
-      epi_store_vec<T>(p.epi, row, col0, acc);
+      float bv[VE];
+      staged_bias<T>(sb, li, bv);
+      epi_store_vec_b<T>(p.epi, row, col0, acc, bv);
     } else {
       float4* out = reinterpret_cast<float4*>(p.partials + pos * p.ldp + col0);
 #pragma unroll
@@ -337,9 +378,11 @@ __device__ __forceinline__ void spmm_piece_body(const PieceParams& p, int64_t w,
 // pieces, the rest walk the light rows.
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 __global__ __launch_bounds__(256) void spmm_main_kernel(SpmmParams<IdxT> p, PieceParams pp, int64_t n_piece_wg) {
+  __shared__ __align__(16) float sb[LPR * Vec<T>::N];
+  stage_bias<T, LPR>(p.epi, sb);
   const int64_t b = blockIdx.x;
-  if (b < n_piece_wg) spmm_piece_body<T, LPR, HAS_VAL>(pp, b, n_piece_wg);
-  else spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, b - n_piece_wg, (int64_t)gridDim.x - n_piece_wg);
+  if (b < n_piece_wg) spmm_piece_body<T, LPR, HAS_VAL>(pp, sb, b, n_piece_wg);
+  else spmm_rows_body<T, IdxT, LPR, HAS_VAL>(p, sb, b - n_piece_wg, (int64_t)gridDim.x - n_piece_wg);
 }
 
 // Partials of launch positions pos_of[a0 .. a1) (VE columns from col0) into
@@ -405,6 +448,10 @@ __global__ __launch_bounds__(256) void spmm_fixup_kernel(PieceParams p) {
   const int64_t col0 = ((int64_t)blockIdx.y * LPR + li) * VE;
   const bool live = col0 < p.F;
   const int64_t b = blockIdx.x;
+  __shared__ __align__(16) float sb[LPR * VE];
+  stage_bias<T, LPR>(p.epi, sb);
+  float bv[VE];
+  staged_bias<T>(sb, li, bv);
   float acc[VE];
 #pragma unroll
   for (int i = 0; i < VE; ++i) acc[i] = 0.f;
@@ -425,7 +472,7 @@ __global__ __launch_bounds__(256) void spmm_fixup_kernel(PieceParams p) {
       for (int k = 1; k < NG; ++k)
 #pragma unroll
         for (int i = 0; i < VE; ++i) acc[i] += red[k][li * VE + i];
-      epi_store_vec<T>(p.epi, p.heavy_rows[h], col0, acc);
+      epi_store_vec_b<T>(p.epi, p.heavy_rows[h], col0, acc, bv);
     }
     return;
   }
@@ -433,13 +480,24 @@ __global__ __launch_bounds__(256) void spmm_fixup_kernel(PieceParams p) {
   if (slot >= p.n_fix || !live) return;
   const int64_t h = p.fix_rows[slot];
   add_partials<VE>(acc, p, col0, p.heavy_chunk_off[h], p.heavy_chunk_off[h + 1]);
-  epi_store_vec<T>(p.epi, p.heavy_rows[h], col0, acc);
+  epi_store_vec_b<T>(p.epi, p.heavy_rows[h], col0, acc, bv);
 }
 
 // Workgroups of each kind in one launch: enough for every lane group to
 // walk several rows (or pieces) with its descriptor loads ahead, and about
 // four rounds of workgroups over the chip's 256 compute units.
 constexpr int64_t SPMM_WG_CAP = 8192;
+
+// Resident workgroups of the main kernel per compute unit.  Its 82-86
+// VGPRs would allow five waves per SIMD; more gathers in flight then evict
+// the reused rows from L2 (R-MAT scale 21: 1.707 against 1.674 ms at
+// F = 128, 0.887 against 0.853 ms at F = 64, no epilogue), so the launch
+// asks for dynamic LDS that leaves room for four 256-thread workgroups in
+// the 160 KB of LDS of a gfx950 compute unit (the static LDS of the kernel
+// is at most 2 KB).
+constexpr int SPMM_WG_PER_CU = 4;
+constexpr unsigned SPMM_LDS_PER_CU = 160u * 1024u;
+constexpr unsigned SPMM_OCCUPANCY_LDS = SPMM_LDS_PER_CU / SPMM_WG_PER_CU - 2048u;
 
 template <typename T, typename IdxT, int LPR, bool HAS_VAL>
 hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
@@ -488,7 +546,8 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
     n_piece_wg = std::min<int64_t>((A.n_chunks + per_wg - 1) / per_wg, SPMM_WG_CAP);
   }
   hipLaunchKernelGGL((spmm_main_kernel<T, IdxT, LPR, HAS_VAL>),
-                     dim3((unsigned)(n_piece_wg + lblocks), (unsigned)colblocks), dim3(256), 0, s, p, pp, n_piece_wg);
+                     dim3((unsigned)(n_piece_wg + lblocks), (unsigned)colblocks), dim3(256), SPMM_OCCUPANCY_LDS, s,
+                     p, pp, n_piece_wg);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (A.n_fix <= 0) return hipSuccess;               // every heavy row is one piece: all stored
