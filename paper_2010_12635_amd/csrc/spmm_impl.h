@@ -172,10 +172,11 @@ __device__ __forceinline__ void staged_bias(const float* sb, int li, float (&bv)
 // Rows of one entry, SINGLE_BUNDLE of them (descriptors k0 .. k0 + cnt - 1)
 // at once: descriptors, then column indices and values, then the gathers
 // go out together, so the bundle costs the dependent loads of one row.
-// Each sum is its single term (bit-identical to the row walk).  Four rows:
-// eight would take the kernel from 95-99 to 128 VGPRs (four waves per SIMD
-// instead of five).
-constexpr int SINGLE_BUNDLE = 4;
+// Each sum is its single term (bit-identical to the row walk).  Eight rows
+// (R-MAT scale 21 against four: F = 128 1.670 -> 1.642 ms, F = 64 0.852 ->
+// 0.835 ms, no epilogue); their registers cost no occupancy, which the
+// launch holds at four workgroups per compute unit anyway.
+constexpr int SINGLE_BUNDLE = 8;
 
 template <typename T, typename IdxT, bool HAS_VAL>
 __device__ __forceinline__ void single_bundle(const SpmmParams<IdxT>& p, const T* __restrict__ X, int64_t col0,
@@ -488,13 +489,14 @@ __global__ __launch_bounds__(256) void spmm_fixup_kernel(PieceParams p) {
 // four rounds of workgroups over the chip's 256 compute units.
 constexpr int64_t SPMM_WG_CAP = 8192;
 
-// Resident workgroups of the main kernel per compute unit.  Its 82-86
-// VGPRs would allow five waves per SIMD; more gathers in flight then evict
-// the reused rows from L2 (R-MAT scale 21: 1.707 against 1.674 ms at
-// F = 128, 0.887 against 0.853 ms at F = 64, no epilogue), so the launch
-// asks for dynamic LDS that leaves room for four 256-thread workgroups in
-// the 160 KB of LDS of a gfx950 compute unit (the static LDS of the kernel
-// is at most 2 KB).
+// Resident workgroups of the main kernel per compute unit.  Five waves per
+// SIMD put more gathers in flight, which evict the reused rows from L2
+// (R-MAT scale 21 with bundles of four rows at 82-86 VGPRs: 1.707 against
+// 1.674 ms at F = 128, 0.887 against 0.853 ms at F = 64, no epilogue), so
+// the launch asks for dynamic LDS that leaves room for four 256-thread
+// workgroups in the 160 KB of LDS of a gfx950 compute unit (the static LDS
+// of the kernel is at most 2 KB).  With bundles of eight the fp16 variants
+// need 108-122 VGPRs and hold four waves per SIMD by their registers too.
 constexpr int SPMM_WG_PER_CU = 4;
 constexpr unsigned SPMM_LDS_PER_CU = 160u * 1024u;
 constexpr unsigned SPMM_OCCUPANCY_LDS = SPMM_LDS_PER_CU / SPMM_WG_PER_CU - 2048u;
