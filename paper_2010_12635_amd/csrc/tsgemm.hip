@@ -365,19 +365,35 @@ __global__ __launch_bounds__(256) void tsgemm_kernel(TsParams p) {
   }
 }
 
+// Dynamic LDS of one workgroup: the B block, then the four staging buffers.
+template <typename T>
+size_t ts_lds_bytes(int64_t nblk, int64_t kpad) {
+  return ((size_t)nblk * (kpad + Vec<T>::N) * sizeof(T) + 15) / 16 * 16 + (size_t)4 * 16 * (nblk + 4) * sizeof(float);
+}
+
+// Half of a gfx950 compute unit's 160 KB of LDS.
+constexpr size_t TS_LDS_TWO_WG = 80 * 1024;
+
 template <typename T>
 int ts_nblk(int64_t N, int64_t kpad) {
   int64_t nb = std::min<int64_t>(128, (N + 15) / 16 * 16);
   const int64_t cap = (TS_LDS_B_BYTES / ((kpad + Vec<T>::N) * (int64_t)sizeof(T))) / 16 * 16;
   nb = std::min<int64_t>(nb, std::max<int64_t>(cap, 16));
+  // fp32: equal narrower column blocks rather than one workgroup (one wave
+  // per SIMD) per compute unit: a 128 x 128 fp32 block of W with its
+  // staging needs 101 KB, and the 16x16x4 fp32 matrix instructions then
+  // wait on each B read from LDS with no other wave to issue
+  if (sizeof(T) == 4) {
+    for (int64_t parts = 2; nb > 16 && ts_lds_bytes<T>(nb, kpad) > TS_LDS_TWO_WG; ++parts)
+      nb = std::min<int64_t>(nb, ((N + parts - 1) / parts + 15) / 16 * 16);
+  }
   return (int)nb;
 }
 
 template <typename T, bool BKC, bool DM, int CSM, int TM>
 hipError_t launch_tm(const TsParams& p, int* grid_rows, hipStream_t s) {
   const int tnw = p.nblk / 16;
-  const size_t lds = ((size_t)p.nblk * (p.kpad + Vec<T>::N) * sizeof(T) + 15) / 16 * 16 +
-                     (size_t)4 * 16 * (p.nblk + 4) * sizeof(float);
+  const size_t lds = ts_lds_bytes<T>(p.nblk, p.kpad);
   // persistent workgroups: enough to fill every CU twice, each looping over row tiles
   const int64_t nb = (p.N + p.nblk - 1) / p.nblk;
   const int64_t ntiles = (p.M + 64 * TM - 1) / (64 * TM);
