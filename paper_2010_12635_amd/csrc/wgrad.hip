@@ -131,18 +131,23 @@ struct Tile {
   }
 };
 
-template <typename T>
+// NARROW (N <= 64, one column block): the four waves take 32 rows x 64
+// columns each instead of 2 x 2 tiles of 64 x 64, so that no wave
+// multiplies the zero columns 64 .. 127 (fp32 dW of a 64-column layer had
+// half of its matrix instructions on zeros).
+template <typename T, bool NARROW>
 __global__ __launch_bounds__(256) void wgrad_kernel(WgParams p) {
   constexpr int VE = Vec<T>::N;
   constexpr int KT = Tile<T>::KT;
   constexpr int LDK = KT + VE;
-  constexpr int TM = 4, TN = 4;                    // wave tile 64 x 64, waves 2 x 2
+  constexpr int TM = NARROW ? 2 : 4, TN = 4;       // wave tile 32 x 64 (4 x 1 waves) or 64 x 64 (2 x 2)
   __shared__ __align__(16) T sA[2][WG_B * LDK];
   __shared__ __align__(16) T sB[2][WG_B * LDK];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wr = NARROW ? wave * 32 : (wave >> 1) * 64;   // first row and column of the wave's tile
+  const int wc = NARROW ? 0 : (wave & 1) * 64;
   const int64_t split = blockIdx.x;
   const int64_t m0 = (int64_t)blockIdx.y * WG_B, n0 = (int64_t)blockIdx.z * WG_B;
   const int64_t kb = split * p.span, ke = std::min(p.n, kb + p.span);
@@ -159,8 +164,8 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgParams p) {
   Tile<T> t0, t1;
   auto load = [&](Tile<T>& x, int64_t t) { x.load(p, Hg, Gg, m0, n0, kb + t * KT, ke, kb, tid); };
   auto compute = [&](int st) {
-    const T* as = sA[st] + (wm * 64 + (lane & 15)) * LDK + (lane >> 4) * VE;
-    const T* bs = sB[st] + (wn * 64 + (lane & 15)) * LDK + (lane >> 4) * VE;
+    const T* as = sA[st] + (wr + (lane & 15)) * LDK + (lane >> 4) * VE;
+    const T* bs = sB[st] + (wc + (lane & 15)) * LDK + (lane >> 4) * VE;
 #pragma unroll
     for (int ks = 0; ks < KT / (4 * VE); ++ks) {
       uint4 af[TM], bf[TN];
@@ -200,8 +205,8 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgParams p) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + v;
-        const int64_t nn = n0 + wn * 64 + j * 16 + (lane & 15);
+        const int64_t m = m0 + wr + i * 16 + (lane >> 4) * 4 + v;
+        const int64_t nn = n0 + wc + j * 16 + (lane & 15);
         if (m < p.M && nn < p.N) out[m * p.N + nn] = acc[i][j][v];
       }
 }
@@ -209,7 +214,8 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgParams p) {
 template <typename T>
 hipError_t launch_t(const WgParams& p, int splits, hipStream_t s) {
   dim3 grid((unsigned)splits, (unsigned)((p.M + WG_B - 1) / WG_B), (unsigned)((p.N + WG_B - 1) / WG_B));
-  hipLaunchKernelGGL(wgrad_kernel<T>, grid, dim3(256), 0, s, p);
+  if (p.N <= 64) hipLaunchKernelGGL((wgrad_kernel<T, true>), grid, dim3(256), 0, s, p);
+  else hipLaunchKernelGGL((wgrad_kernel<T, false>), grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
