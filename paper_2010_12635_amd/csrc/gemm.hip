@@ -252,8 +252,8 @@ __device__ __forceinline__ void reduce_body_t(const RedJob& j, int64_t blk) {
   const bool live = idx < total && c < j.N;
   float a = 0.f;
   if (live) {
-    const float* q = j.part + r * j.N + c;
-    const int64_t stride = j.M * j.N;
+    const float* q = j.part + r * j.ld + c;
+    const int64_t stride = j.M * j.ld;
 #pragma unroll 8
     for (int sidx = g; sidx < j.splits; sidx += NG) a += q[(int64_t)sidx * stride];
   }
@@ -378,8 +378,12 @@ hipError_t gemm_launch(const GemmCall& c, hipStream_t s) {
 }
 
 RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const Epilogue& epi) {
+  return make_job_ld(partials, splits, M, N, N, epi);
+}
+
+RedJob make_job_ld(const float* partials, int splits, int64_t M, int64_t N, int64_t ld, const Epilogue& epi) {
   RedJob j;
-  j.part = partials; j.splits = splits; j.M = M; j.N = N; j.ep = epi;
+  j.part = partials; j.splits = splits; j.M = M; j.N = N; j.ld = ld; j.ep = epi;
   j.width = epi.mode == EPI_F32 ? epi.ldo : N;
   // about 32 splits per thread at most where the outputs allow it (one
   // output per workgroup, 64 splits per thread, beyond 4096 splits)

@@ -43,10 +43,13 @@ struct RedJob {
   const float* part;
   int splits;
   int64_t M, N, width, blocks;
+  int64_t ld;                   // floats between partial rows of one split (N unless given)
   int opw;                      // outputs per workgroup: 64, 16, 4 or 1 (256 / opw groups of splits)
   Epilogue ep;
 };
 RedJob make_job(const float* partials, int splits, int64_t M, int64_t N, const Epilogue& epi);
+// The same for partial rows ld >= N floats apart (split stride M * ld).
+RedJob make_job_ld(const float* partials, int splits, int64_t M, int64_t N, int64_t ld, const Epilogue& epi);
 // One launch for job a and, if b != NULL, job b.
 hipError_t reduce_partials2(int prec, const RedJob& a, const RedJob* b, hipStream_t s);
 hipError_t reduce_partials(int prec, const float* partials, int splits, int64_t M, int64_t N,

@@ -22,7 +22,8 @@ struct LossParams {
   void* dlogits;
   float* part_loss;     // [blocks]
   int32_t* part_corr;   // [blocks]
-  float* part_cs;       // [blocks][C] column sums of the stored dlogits, or NULL
+  float* part_cs;       // [blocks][ldcs] column sums of the stored dlogits, or NULL
+  int64_t ldcs;         // row stride of part_cs: C rounded up to 8
   int32_t* flag;
 };
 
@@ -232,7 +233,7 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(LossParams p) {
     for (int cidx = threadIdx.x; cidx < p.C; cidx += 256) {
       float a = s_cs[0][cidx];
       for (int k = 1; k < RG; ++k) a += s_cs[k][cidx];
-      p.part_cs[(int64_t)blockIdx.x * p.C + cidx] = a;
+      p.part_cs[(int64_t)blockIdx.x * p.ldcs + cidx] = a;
     }
   }
 }
@@ -333,12 +334,21 @@ int64_t loss_max_blocks(int64_t n, int64_t C) {
   return nb > nb16 ? nb : nb16;
 }
 
-// [loss partials][correct-count partials][column-sum partials (blocks x C)]
+// More column-sum partial rows than this are first summed in blocks of
+// consecutive rows (one launch), then the blocks' rows (a second).
+constexpr int64_t LOSS_CS_ONE_STAGE = 4096;
+
+int64_t loss_cs_ld(int64_t C) { return (C + 7) / 8 * 8; }
+
+// [loss partials][correct-count partials][column-sum partials (blocks x
+// ldcs)][their block sums]
 size_t loss_workspace_bytes(int64_t n, int64_t C) {
   const int64_t m = loss_max_blocks(n, C) + 1;
+  const int64_t ldcs = loss_cs_ld(C);
   const size_t a = ((size_t)m * sizeof(float) + 255) & ~size_t(255);
   const size_t b = ((size_t)m * sizeof(int32_t) + 255) & ~size_t(255);
-  return a + b + (size_t)m * (size_t)C * sizeof(float) + 256;
+  const size_t c = ((size_t)m * (size_t)ldcs * sizeof(float) + 255) & ~size_t(255);
+  return a + b + c + (size_t)colsum_partials_floats(m, ldcs) * sizeof(float) + 256;
 }
 
 hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* logits, const int32_t* labels,
@@ -356,6 +366,9 @@ hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* l
   p.part_corr = reinterpret_cast<int32_t*>(w);
   w += ((size_t)m * sizeof(int32_t) + 255) & ~size_t(255);
   p.part_cs = dlogits_colsum ? reinterpret_cast<float*>(w) : nullptr;
+  p.ldcs = loss_cs_ld(C);
+  w += ((size_t)m * (size_t)p.ldcs * sizeof(float) + 255) & ~size_t(255);
+  float* cs_blocks = reinterpret_cast<float*>(w);
   p.flag = flag;
   hipError_t e;
   switch (prec) {
@@ -369,11 +382,20 @@ hipError_t loss_launch(int prec, int64_t n, int64_t C, int64_t ld, const void* l
                      n_correct, flag);
   e = hipGetLastError();
   if (e != hipSuccess || !dlogits_colsum) return e;
-  // the workgroups' column sums added in workgroup order; classes [C, ld) get 0
+  // the workgroups' column sums added in a fixed order; classes [C, ld) get 0
   Epilogue eb{};
   eb.out = dlogits_colsum; eb.ldo = ld; eb.rows = 1; eb.cols = C; eb.mode = EPI_F32; eb.flag = flag;
   eb.keep_scale = 1.f;
-  return reduce_partials2(prec, make_job(p.part_cs, (int)nb, 1, C, eb), nullptr, s);
+  if (nb <= LOSS_CS_ONE_STAGE)
+    return reduce_partials2(prec, make_job_ld(p.part_cs, (int)nb, 1, C, p.ldcs, eb), nullptr, s);
+  // many workgroups (R-MAT scale 21: 16384): blocks of consecutive partial
+  // rows first, with coalesced row reads over the whole chip, then the
+  // blocks' sums (one launch of one output per workgroup reading a column
+  // each took 24 us in fp16 and 41 us in fp32)
+  int blocks = 0;
+  e = colsum_partial_launch(0, p.part_cs, nb, C, p.ldcs, cs_blocks, p.ldcs, &blocks, s);
+  if (e != hipSuccess) return e;
+  return reduce_partials2(prec, make_job_ld(cs_blocks, blocks, 1, C, p.ldcs, eb), nullptr, s);
 }
 
 }  // namespace gcn
