@@ -448,7 +448,10 @@ def test_bwd_power_of_two_scale_invariance():
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
 @pytest.mark.parametrize("C,n", [(7, 5000), (40, 5000), (64, 5000), (32, 5000),
                                  # more than 16384 row groups: four rows per lane group and iteration
-                                 (64, 600_003), (40, 600_003)])
+                                 (64, 600_003), (40, 600_003),
+                                 # more than 4096 workgroups with C not a multiple of 8: the
+                                 # column-sum partials (rows padded to 8) summed in two stages
+                                 (7, 1_200_003)])
 def test_loss(prec, C, n):
     rng = np.random.default_rng(C)
     z = (rng.standard_normal((n, C)) * 3).astype(np.float32)
