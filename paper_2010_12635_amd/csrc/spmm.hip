@@ -24,6 +24,8 @@ int lpr_for(int prec, int64_t F) {
 
 }  // namespace
 
+// Floats of the heavy-row partials: enough for the widest lane groups, and
+// so also when the launch gathers in narrower column blocks.
 int64_t spmm_partials_floats(const CsrView& A, int prec, int64_t F) {
   if (A.n_heavy <= 0) return 0;
   const int VE = prec == 0 ? 4 : 8;

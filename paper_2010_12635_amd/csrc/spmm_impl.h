@@ -558,11 +558,22 @@ hipError_t launch_cfg(const CsrView& A, const void* X, int64_t ldx, int64_t F, c
   return hipGetLastError();
 }
 
+// Neighbour rows wider than 256 bytes are gathered in 256-byte column
+// blocks (grid y; the blocks of the first columns run first) once the
+// gathered table exceeds 128 MiB: each pass then keeps twice as many reused
+// rows in L2.  R-MAT scale 21, fp32, F = 128 (1 GiB table): 3.63 -> 3.30
+// ms; Barabasi-Albert n = 200000, fp32, F = 256 (205 MB): 0.483 -> 0.471
+// ms; a 67 MB table (R-MAT scale 17, fp16, F = 256) was 6 % slower split.
+constexpr int64_t SPMM_ROW_BLOCK_BYTES = 256;
+constexpr int64_t SPMM_SPLIT_TABLE_BYTES = (int64_t)128 << 20;
+
 template <typename T, typename IdxT, bool HAS_VAL>
 hipError_t launch_lpr(const CsrView& A, const void* X, int64_t ldx, int64_t F, const Epilogue& epi,
                       float* partials, hipStream_t s) {
   constexpr int VE = Vec<T>::N;
-  const int64_t nvec = (F + VE - 1) / VE;
+  constexpr int64_t LPR_BLOCK = SPMM_ROW_BLOCK_BYTES / (VE * (int64_t)sizeof(T));   // 16 lanes
+  int64_t nvec = (F + VE - 1) / VE;
+  if (nvec > LPR_BLOCK && A.n * F * (int64_t)sizeof(T) > SPMM_SPLIT_TABLE_BYTES) nvec = LPR_BLOCK;
   if (nvec <= 1) return launch_cfg<T, IdxT, 1, HAS_VAL>(A, X, ldx, F, epi, partials, s);
   if (nvec <= 2) return launch_cfg<T, IdxT, 2, HAS_VAL>(A, X, ldx, F, epi, partials, s);
   if (nvec <= 4) return launch_cfg<T, IdxT, 4, HAS_VAL>(A, X, ldx, F, epi, partials, s);
