@@ -314,6 +314,32 @@ def test_layer_fwd(prec, case):
         assert np.array_equal(got[pos] != 0, keep[pos])
 
 
+# neighbour rows wider than 256 bytes from a table of more than 128 MiB:
+# the aggregation gathers them in 256-byte column blocks (grid y), heavy-row
+# pieces and their fix-up included; bias and ReLU in the epilogue
+@pytest.mark.parametrize("prec,n", [(G.GCN_F32, 70_000), (G.GCN_F16, 140_000)], ids=["f32", "f16"])
+def test_aggregate_wide_rows_of_a_large_table(prec, n):
+    F = 520
+    assert n * F * (4 if prec == G.GCN_F32 else 2) > 128 << 20
+    rng = np.random.default_rng(n)
+    src, dst = hub_graph(n, 4 * n, HUBS, n)
+    g = O.graph(n, src, dst)
+    x = rng.standard_normal((n, F)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(F)).astype(np.float32)
+    dg = DeviceGraph(n, src, dst, prec=prec, heavy_threshold=48, chunk_nnz=96)
+    assert dg.adj.n_fix > 0
+    X = to_dev(x, prec)
+    Y = torch.empty_like(X)
+    ov = torch.zeros(1, dtype=torch.int32, device=dev())
+    ws = torch.empty(G.gcn_aggregate_workspace_size(dg.adj, F, prec), dtype=torch.uint8, device=dev())
+    G.gcn_aggregate(dg.adj, F, prec, X, F, torch.as_tensor(b).to(dev()), G.GCN_ACT_RELU, 0.0, 0, 0, 0, 0,
+                    Y, F, ov, ws)
+    torch.cuda.synchronize()
+    z = O.spmm(g, O.norm_values(g), rounded(x, prec)) + b.astype(np.float64)[None, :]
+    assert_close(host(Y, F), np.maximum(z, 0.0), prec, "relu(A_hat X + b)")
+    assert int(ov.item()) == 0
+
+
 def test_dropout_threshold_uses_binary32_p():
     """The keep threshold is floor(p * 2^32) of the binary32 p the ABI takes.
 
