@@ -590,6 +590,34 @@ def summarize_mfma(pmc_dir, out_path, command):
     return out
 
 
+def aggregation_calls(stats_dir):
+    """Per-call CSR aggregation times from the kernel trace of a --stats run:
+    one call = spmm_main_kernel plus the spmm_fixup_kernel that follows it
+    (the unit the benchmark's roofline divides by), per storage type."""
+    import csv
+    path = os.path.join(stats_dir, "run_kernel_trace.csv")
+    if not os.path.exists(path):
+        return []
+    ks = sorted(((r["Kernel_Name"], int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+                 for r in csv.DictReader(open(path))), key=lambda k: k[1])
+    calls = {}
+    for i, (name, t0, t1) in enumerate(ks):
+        if "spmm_main_kernel" not in name:
+            continue
+        us = (t1 - t0) / 1e3
+        if i + 1 < len(ks) and "spmm_fixup_kernel" in ks[i + 1][0]:
+            us += (ks[i + 1][2] - ks[i + 1][1]) / 1e3
+        key = "fp16" if ("DF16_" in name and "DF16b" not in name) else "bf16" if "DF16b" in name else "fp32"
+        calls.setdefault(key, []).append(us)
+    if not calls:
+        return []
+    out = ["", "CSR aggregation calls (`spmm_main_kernel` + the `spmm_fixup_kernel` after it), from "
+           "`run_kernel_trace.csv` of the same run:", "", "| storage | calls | avg us per call |", "|---|---:|---:|"]
+    for key, v in sorted(calls.items()):
+        out.append(f"| {key} | {len(v)} | {sum(v) / len(v):.1f} |")
+    return out
+
+
 def summarize_stats(stats_dir, out_path, command, title):
     """Kernel time table from a rocprofv3 --stats run (run_kernel_stats.csv)."""
     import csv
@@ -602,6 +630,7 @@ def summarize_stats(stats_dir, out_path, command, title):
         name = name if len(name) < 110 else name[:110] + "..."
         lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} "
                      f"| {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    lines += aggregation_calls(stats_dir)
     with open(out_path, "w") as fh:
         fh.write("\n".join(lines) + "\n")
 
