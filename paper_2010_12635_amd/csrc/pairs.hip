@@ -230,12 +230,14 @@ __global__ __launch_bounds__(256) void rs_hist_kernel(int64_t n, const int32_t* 
 // out digit run by digit run, so that neighbouring lanes store to
 // neighbouring addresses (placed straight at their global positions, every
 // lane of a store would hit another cache line).
-// Each item carries its pair index k and the other endpoint of the pair.
+// Each item carries the gradient g_k of its pair (as bits) and the other
+// endpoint: the segment sums then read g_k with the entry instead of
+// gathering it by pair index.
 template <int BITS>
 __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_t* __restrict__ pu,
                                                          const int32_t* __restrict__ pv,
                                                          const int32_t* __restrict__ kin, const int32_t* __restrict__ vin,
-                                                         const int32_t* __restrict__ oin,
+                                                         const int32_t* __restrict__ oin, const float* __restrict__ g,
                                                          int64_t total, int shift, int64_t nblk,
                                                          const int64_t* __restrict__ off, int32_t* __restrict__ kout,
                                                          int32_t* __restrict__ vout, int32_t* __restrict__ oout) {
@@ -263,7 +265,7 @@ __global__ __launch_bounds__(256) void rs_scatter_kernel(int64_t n, const int32_
       os[r] = oin[i];
     } else {                                        // first pass: items in pair order
       ks[r] = entry_key(n, pu, pv, i);
-      vs[r] = (int32_t)(i >> 1);
+      vs[r] = __float_as_int(g[i >> 1]);
       os[r] = (i & 1) ? pu[i >> 1] : pv[i >> 1];
     }
   }
@@ -371,9 +373,8 @@ struct SegParams {
   const void* Z;
   const int32_t* pu;
   const int32_t* pv;
-  const float* g;
   const int64_t* off;                               // [n + 1]
-  const int32_t* pk;                                // sorted entries: pair index
+  const int32_t* pg;                                // sorted entries: the pair's gradient g_k (bits)
   const int32_t* po;                                // sorted entries: other endpoint
   int64_t nseg;
   float* head;                                      // [nseg][ldp]
@@ -389,16 +390,14 @@ __device__ __forceinline__ void seg_sum(const SegParams& p, int64_t e0, int64_t 
   constexpr int VE = Vec<T>::N, U = 8;
   const T* __restrict__ Z = reinterpret_cast<const T*>(p.Z);
   for (int64_t e = e0; e < e1; e += U) {
-    int32_t kk[U], other[U];
+    int32_t other[U];
+    float w[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t ee = e + u < e1 ? e + u : e1 - 1;
-      kk[u] = p.pk[ee];
+      w[u] = __int_as_float(p.pg[ee]);
       other[u] = p.po[ee];
     }
-    float w[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) w[u] = p.g[kk[u]];
 #pragma unroll
     for (int u = 0; u < U; ++u) w[u] = e + u < e1 ? w[u] : 0.f;
     uint4 x[U];
@@ -741,7 +740,7 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
   GCN_TRY(hipGetLastError());                                                                               \
   GCN_TRY(segment_scan_exclusive(hist, nhw, scr, s));                                                       \
   hipLaunchKernelGGL(rs_scatter_kernel<B>, dim3((unsigned)nblk), dim3(256), 0, s, n, pair_u, pair_v, kin, vin, \
-                     oin, total, shift, nblk, hist, kout, vout, oout);                                      \
+                     oin, g, total, shift, nblk, hist, kout, vout, oout);                                      \
   GCN_TRY(hipGetLastError());
       RS_PASS(8)
 #undef RS_PASS
@@ -757,8 +756,8 @@ hipError_t pair_backward_launch(int prec, int64_t n, int64_t F, int64_t ld, cons
   hipLaunchKernelGGL(rs_bounds_kernel, dim3(bb), dim3(256), 0, s, n, kin ? kin : kA, total, off);
   GCN_TRY(hipGetLastError());
   SegParams p;
-  p.n = n; p.F = F; p.ld = ld; p.Z = Z; p.pu = pair_u; p.pv = pair_v; p.g = g; p.off = off;
-  p.pk = vin ? vin : vA;
+  p.n = n; p.F = F; p.ld = ld; p.Z = Z; p.pu = pair_u; p.pv = pair_v; p.off = off;
+  p.pg = vin ? vin : vA;
   p.po = oin ? oin : oA;
   p.nseg = nseg; p.head = head; p.tail = tail; p.tail_row = trow; p.ldp = ldp;
   Epilogue ep{};
@@ -829,7 +828,7 @@ hipError_t pair_metrics_launch(const float* scores, int64_t n_pos, int64_t n_neg
     GCN_TRY(hipGetLastError());
     GCN_TRY(segment_scan_exclusive(L.hist, ((int64_t)1 << RS_MAX_BITS) * nblk, L.scr, s));
     hipLaunchKernelGGL(rs_scatter_kernel<RS_MAX_BITS>, dim3((unsigned)nblk), dim3(256), 0, s, (int64_t)0, nullptr,
-                       nullptr, kin, pin, iin, total, shift, nblk, L.hist, kout, pout, iout);
+                       nullptr, kin, pin, iin, nullptr, total, shift, nblk, L.hist, kout, pout, iout);
     GCN_TRY(hipGetLastError());
     int32_t* t;
     t = kin; kin = kout; kout = t;
