@@ -42,8 +42,64 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+class HipTimingEvent:
+    """A HIP event for timing only, created with hipEventDisableSystemFence:
+    recording it orders the stream like any event but skips the system-scope
+    release (a cache write-back and invalidation) that a default event
+    performs, which would otherwise slow the kernel after every bracket.
+    Calls go to the HIP runtime that torch has loaded (same process, same
+    runtime as the library)."""
+    DISABLE_SYSTEM_FENCE = 0x20000000
+    _hip = None
+
+    @classmethod
+    def runtime(cls):
+        if cls._hip is None:
+            import ctypes
+            hip = ctypes.CDLL("libamdhip64.so.7")
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = hip
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+        self.h = ctypes.c_void_p()
+        st = self.runtime().hipEventCreateWithFlags(ctypes.byref(self.h), self.DISABLE_SYSTEM_FENCE)
+        if st != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({st})")
+
+    def record(self):
+        import torch
+        st = self.runtime().hipEventRecord(self.h, ctypes_stream(torch.cuda.current_stream().cuda_stream))
+        if st != 0:
+            raise RuntimeError(f"hipEventRecord failed ({st})")
+
+    def elapsed_time(self, end):
+        import ctypes
+        ms = ctypes.c_float()
+        st = self.runtime().hipEventElapsedTime(ctypes.byref(ms), self.h, end.h)
+        if st != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({st})")
+        return ms.value
+
+    def __del__(self):
+        try:
+            if self._hip is not None and self.h:
+                self._hip.hipEventDestroy(self.h)
+        except Exception:      # interpreter shutdown
+            pass
+
+
+def ctypes_stream(handle):
+    import ctypes
+    return ctypes.c_void_p(handle)
+
+
 class EventTimer:
-    """Brackets library calls with HIP events on the current stream."""
+    """Brackets library calls with HIP timing events on the current stream."""
 
     def __init__(self):
         import torch
@@ -55,14 +111,11 @@ class EventTimer:
     def reserve(self, brackets):
         """Create the events of ``brackets`` brackets up front, so that the
         timed loop only records them."""
-        self.pool = [self.torch.cuda.Event(enable_timing=True) for _ in range(2 * brackets)]
-        for e in self.pool:      # torch creates the HIP event at its first record
-            e.record()
-        self.torch.cuda.synchronize()
+        self.pool = [HipTimingEvent() for _ in range(2 * brackets)]
         self.pool.reverse()
 
     def _event(self):
-        return self.pool.pop() if self.pool else self.torch.cuda.Event(enable_timing=True)
+        return self.pool.pop() if self.pool else HipTimingEvent()
 
     def __call__(self):
         timer = self
